@@ -1,0 +1,310 @@
+"""Plain CPU oracle of the sparse permutohedral-lattice hot path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import or call this
+module: only the tests, the smoke check and the CPU-baseline leg of the
+benchmark use it.  It shares no code with the HIP library.
+
+It follows the paper (Rosu et al., "LatticeNet", arXiv 2108.03917):
+
+* Sec. "Permutohedral Lattice": the lattice is (d+1)Z^{d+1} projected along
+  the all-ones vector onto the hyperplane H_d; vertex coordinates sum to zero;
+  the enclosing simplex of a point comes from a simple rounding algorithm
+  (cited there to Baek & Adams); each vertex has 2(d+1) neighbours at
+  +-[-1,..,-1,d,-1,..,-1]; vertices are stored sparsely in a hash map.
+* Sec. "Method": positions are scaled as G / sigma.
+* Sec. "Common Operations on Permutohedral Lattice": splat (barycentric
+  weighting onto the d+1 simplex vertices, summed), convolve over the 1-hop
+  ring of 2(d+1)+1 vertices (an unallocated neighbour counts as zero, caption
+  of the convolution figure), slice (the inverse of splat with the same
+  weights).
+* Eq. (splat): x_v = sum_{p in J_v} b_pv f_p.   Eq. (slice): f_p = sum_{v in I_p} b_pv x_v.
+
+Precision.  Where floating point decides an integer (which simplex encloses a
+point, hence every lattice key), this oracle takes that decision in float32
+with one fixed sequence of individually rounded operations, no fused
+multiply-add, exactly as the HIP kernel does: the paper fixes no precision,
+and bit-exact keys need both sides to round the same way.  Everything that is
+an output value (barycentric weights, splat, conv, slice) is computed in
+float64 from those float32 elevated coordinates.
+
+Readings of the paper taken here (the paper is silent on them):
+
+* Elevation: x = alpha * E * (g / sigma), with E the orthonormal basis of H_d
+  whose j-th column is (1,..,1,-j,0,..,0)/sqrt(j(j+1)) (j ones).  Default
+  alpha = (d+1) sqrt(2/3), the scale of the lattice-filtering work the paper
+  builds on.  alpha is a parameter.
+* Rounding to the remainder-0 point uses round-half-to-even on x * fl(1/(d+1)).
+* Rank ties: the lower coordinate index ranks first (rank 0 = largest).
+* All d+1 vertices of every point's simplex are allocated, zero weight or not.
+* Splat output is the raw sum of Eq. (splat) plus the weight channel
+  w_v = sum b_pv; the optional normalised form divides by w_v (0 where w_v=0).
+* Tap order of the 1-ring: tap 0 is the vertex itself, tap 1+j is c + n_j and
+  tap d+2+j is c - n_j (j = 0..d), with n_j = (d+1) e_j - 1.
+* Conv weight layout [C_out][T][C_in]: y_v[o] = sum_t sum_i x_{nbr(v,t)}[i] W[o,t,i].
+* Batched clouds are independent lattices; canonical vertex order is
+  ascending (batch, c_0, .., c_{d-1}).
+
+Parity unpinned: alpha, the rounding-tie rule and the rank-tie rule are
+conventions that the paper does not fix; both sides adopt the ones above.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+import scipy.sparse as sp
+
+F32 = np.float32
+
+
+def default_alpha(d: int) -> float:
+    """Default elevation scale (d+1) sqrt(2/3) (reading of Sec. "Permutohedral Lattice")."""
+    return (d + 1) * np.sqrt(2.0 / 3.0)
+
+
+def scale_factors(d: int, sigma, alpha: Optional[float] = None) -> np.ndarray:
+    """Per-axis float32 factors f_j = alpha / (sigma_{j-1} sqrt(j(j+1))), j = 1..d.
+
+    Folds the position scaling G / sigma (Sec. "Method") into the orthonormal
+    elevation basis.  Computed in float64, rounded once to float32."""
+    if alpha is None or alpha <= 0:
+        alpha = default_alpha(d)
+    sig = np.broadcast_to(np.asarray(sigma, dtype=F32), (d,))
+    out = np.empty(d, dtype=F32)
+    for j in range(1, d + 1):
+        out[j - 1] = F32(float(alpha) / (np.float64(sig[j - 1]) * np.sqrt(np.float64(j * (j + 1)))))
+    return out
+
+
+def elevate(pos: np.ndarray, factors: np.ndarray) -> np.ndarray:
+    """Elevate d-dim points onto H_d in float32 (Sec. "Permutohedral Lattice").
+
+    x_d = -d s_d ;  x_i = (s_{i+1} + .. + s_d) - i s_i ;  x_0 = s_1 + .. + s_d,
+    with s_j = g_{j-1} f_j.  The running sum goes from j = d down to 1 and
+    every product and sum is rounded to float32 on its own."""
+    pos = np.asarray(pos, dtype=F32)
+    m, d = pos.shape
+    x = np.empty((m, d + 1), dtype=F32)
+    S = np.zeros(m, dtype=F32)
+    for j in range(d, 0, -1):
+        s = pos[:, j - 1] * F32(factors[j - 1])          # float32 product
+        t = F32(j) * s                                   # float32 product
+        x[:, j] = S - t                                  # float32 difference
+        S = S + s                                        # float32 sum
+    x[:, 0] = S
+    return x
+
+
+def enclosing_simplex(x: np.ndarray):
+    """Remainder-0 point and ranks of the enclosing simplex (Sec. "Permutohedral Lattice").
+
+    Steps of the rounding algorithm the paper cites:
+      1. r_i = (d+1) * round(x_i / (d+1))                       (remainder-0 point)
+      2. rank_i = position of Delta_i = x_i - r_i in descending order (ties: lower i first)
+      3. s = sum r_i / (d+1); rank += s, and coordinates whose rank leaves
+         [0, d] wrap around by -+(d+1) with r_i moved by -+(d+1).
+    Returns (r int64 [m, d+1], rank int64 [m, d+1]); sum(r) == 0 afterwards."""
+    x = np.asarray(x, dtype=F32)
+    m, dp1 = x.shape
+    inv = F32(1.0 / dp1)
+    q = np.rint(x * inv)                                 # float32 product, round-half-even
+    r = q.astype(np.int64) * dp1
+    delta = x - r.astype(F32)                            # float32 difference
+    gt = delta[:, None, :] > delta[:, :, None]           # [p, i, j]: Delta_j > Delta_i
+    eq = delta[:, None, :] == delta[:, :, None]
+    lower = np.arange(dp1)[None, :] < np.arange(dp1)[:, None]   # [i, j]: j < i
+    rank = gt.sum(axis=2) + (eq & lower[None]).sum(axis=2)
+    rank = rank.astype(np.int64)
+    s = r.sum(axis=1) // dp1
+    rank = rank + s[:, None]
+    neg = rank < 0
+    big = rank > dp1 - 1
+    rank[neg] += dp1
+    r[neg] += dp1
+    rank[big] -= dp1
+    r[big] -= dp1
+    return r, rank
+
+
+def barycentric(x: np.ndarray, r: np.ndarray, rank: np.ndarray) -> np.ndarray:
+    """Barycentric weights b_k of the d+1 simplex vertices, in float64.
+
+    With delta_i = (x_i - r_i) / (d+1) and z_q the delta whose rank is q
+    (z_0 >= .. >= z_d):  b_k = z_{d-k} - z_{d+1-k} for k = 1..d and
+    b_0 = 1 - (z_0 - z_d).  Vertex k is the one with remainder k (see
+    ``simplex_keys``).  The weights are >= 0 and sum to 1."""
+    x = np.asarray(x, dtype=np.float64)
+    m, dp1 = x.shape
+    d = dp1 - 1
+    delta = (x - r) / dp1
+    z = np.empty_like(delta)
+    np.put_along_axis(z, rank, delta, axis=1)            # z[p, rank_i] = delta_i
+    b = np.empty((m, dp1))
+    for k in range(1, d + 1):
+        b[:, k] = z[:, d - k] - z[:, d + 1 - k]
+    b[:, 0] = 1.0 - (z[:, 0] - z[:, d])
+    return b
+
+
+def simplex_keys(r: np.ndarray, rank: np.ndarray) -> np.ndarray:
+    """Integer keys of the d+1 simplex vertices: [m, k, i] (Sec. "Permutohedral Lattice").
+
+    Vertex k has c_i = r_i + k when rank_i <= d - k, else r_i + k - (d+1);
+    every coordinate of vertex k is congruent to k mod (d+1) and each key
+    sums to zero."""
+    m, dp1 = r.shape
+    d = dp1 - 1
+    keys = np.empty((m, dp1, dp1), dtype=np.int64)
+    for k in range(dp1):
+        keys[:, k, :] = r + k - dp1 * (rank > d - k)
+    return keys
+
+
+@dataclass
+class Lattice:
+    d: int
+    keys: np.ndarray            # int64 [V, d+1], canonical order
+    vbatch: Optional[np.ndarray]  # int64 [V] batch id of each vertex, or None
+    idx: np.ndarray             # int64 [m, d+1]: vertex of remainder k for point p
+    bary: np.ndarray            # float64 [m, d+1]
+    x: np.ndarray               # float32 [m, d+1] elevated positions
+    B: sp.csr_matrix            # [m, V] barycentric weight matrix
+
+    @property
+    def V(self) -> int:
+        return int(self.keys.shape[0])
+
+    @property
+    def m(self) -> int:
+        return int(self.idx.shape[0])
+
+
+def _single(pos, factors):
+    x = elevate(pos, factors)
+    r, rank = enclosing_simplex(x)
+    b = barycentric(x, r, rank)
+    keys = simplex_keys(r, rank)
+    return x, b, keys
+
+
+def build(pos: np.ndarray, sigma, alpha: Optional[float] = None,
+          batch: Optional[np.ndarray] = None) -> Lattice:
+    """Allocate the sparse lattice of a cloud: vertex set V, I_p and b_pv (Sec. "Notation").
+
+    The vertex set is the set of distinct keys over all points' simplices;
+    with ``batch`` each batch id is its own lattice and the vertex lists are
+    concatenated in batch order."""
+    pos = np.asarray(pos, dtype=F32)
+    m, d = pos.shape
+    fac = scale_factors(d, sigma, alpha)
+    x, b, keys = _single(pos, fac)
+    flat = keys.reshape(m * (d + 1), d + 1)[:, :d]      # c_d is implied by the zero sum
+    if batch is not None:
+        bcol = np.repeat(np.asarray(batch, dtype=np.int64), d + 1)[:, None]
+        flat = np.concatenate([bcol, flat], axis=1)
+    uniq, inv = np.unique(flat, axis=0, return_inverse=True)
+    inv = inv.reshape(m, d + 1)
+    if batch is not None:
+        vbatch = uniq[:, 0].copy()
+        coords = uniq[:, 1:]
+    else:
+        vbatch = None
+        coords = uniq
+    full = np.concatenate([coords, -coords.sum(axis=1, keepdims=True)], axis=1)
+    V = full.shape[0]
+    B = sp.csr_matrix((b.ravel(), (np.repeat(np.arange(m), d + 1), inv.ravel())), shape=(m, V))
+    return Lattice(d, full, vbatch, inv, b, x, B)
+
+
+def splat(lat: Lattice, feat: np.ndarray, normalize: bool = False):
+    """Eq. (splat): x_v = sum_{p in J_v} b_pv f_p, in float64.
+
+    Returns (values [V, C], weight [V], scale [V, C]) where weight is
+    w_v = sum_p b_pv and scale = sum_p |b_pv f_p| (the magnitude against which
+    rounding error of any summation order is measured).  With ``normalize``
+    the values are x_v / w_v (0 where w_v = 0)."""
+    f = np.asarray(feat, dtype=np.float64)
+    Bt = lat.B.T.tocsr()
+    values = Bt @ f
+    weight = np.asarray(Bt.sum(axis=1)).ravel()
+    scale = abs(Bt) @ np.abs(f)
+    if normalize:
+        with np.errstate(divide="ignore", invalid="ignore"):
+            nz = weight != 0
+            values = np.where(nz[:, None], values / np.where(nz, weight, 1.0)[:, None], 0.0)
+            scale = np.where(nz[:, None], scale / np.where(nz, weight, 1.0)[:, None], 0.0)
+    return values, weight, scale
+
+
+def neighbor_offsets(d: int) -> np.ndarray:
+    """Tap offsets [T, d+1]: 0, then +n_j, then -n_j, n_j = (d+1) e_j - 1 (Sec. "Permutohedral Lattice")."""
+    n = (d + 1) * np.eye(d + 1, dtype=np.int64) - 1
+    return np.concatenate([np.zeros((1, d + 1), dtype=np.int64), n, -n], axis=0)
+
+
+def neighbors(lat: Lattice) -> np.ndarray:
+    """1-ring table [V, T]: vertex index of key + offset_t, -1 when not allocated."""
+    d = lat.d
+    cols = ([("b", np.int64)] if lat.vbatch is not None else []) + [(f"c{i}", np.int64) for i in range(d)]
+    dt = np.dtype(cols)
+
+    def pack(coords, vb):
+        rec = np.empty(coords.shape[0], dtype=dt)
+        if vb is not None:
+            rec["b"] = vb
+        for i in range(d):
+            rec[f"c{i}"] = coords[:, i]
+        return rec
+
+    table = pack(lat.keys, lat.vbatch)                  # canonical order is sorted
+    offs = neighbor_offsets(d)
+    nbr = np.full((lat.V, offs.shape[0]), -1, dtype=np.int64)
+    for t, o in enumerate(offs):
+        q = pack(lat.keys + o, lat.vbatch)
+        pos = np.searchsorted(table, q)
+        hit = pos < lat.V
+        hit[hit] = table[pos[hit]] == q[hit]
+        nbr[hit, t] = pos[hit]
+    return nbr
+
+
+def conv(values: np.ndarray, nbr: np.ndarray, weight: np.ndarray, bias: Optional[np.ndarray] = None):
+    """1-ring lattice convolution in float64 (Sec. "Common Operations": Convolving).
+
+    y_v = sum_t x_{nbr(v,t)} W_t^T (+ bias), with an absent neighbour
+    contributing zero.  ``weight`` is [C_out][T][C_in].  Returns (y, scale)
+    with scale = sum_t |x_{nbr(v,t)}| |W_t|^T."""
+    x = np.asarray(values, dtype=np.float64)
+    W = np.asarray(weight, dtype=np.float64)
+    V = x.shape[0]
+    c_out, T, c_in = W.shape
+    y = np.zeros((V, c_out))
+    scale = np.zeros((V, c_out))
+    for t in range(T):
+        present = nbr[:, t] >= 0
+        g = np.zeros((V, c_in))
+        g[present] = x[nbr[present, t]]
+        y += g @ W[:, t, :].T
+        scale += np.abs(g) @ np.abs(W[:, t, :]).T
+    if bias is not None:
+        y += np.asarray(bias, dtype=np.float64)[None, :]
+        scale += np.abs(np.asarray(bias, dtype=np.float64))[None, :]
+    return y, scale
+
+
+def slice_(lat: Lattice, values: np.ndarray):
+    """Eq. (slice): f_p = sum_{v in I_p} b_pv x_v, in float64.  Returns (out, scale)."""
+    y = np.asarray(values, dtype=np.float64)
+    return lat.B @ y, abs(lat.B) @ np.abs(y)
+
+
+def round_bf16(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (round to nearest, ties to even), returned as float32.
+
+    Standard bit method: add 0x7FFF plus the lowest kept bit, then clear the
+    low 16 bits.  Inputs here are finite."""
+    u = np.ascontiguousarray(a, dtype=F32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    u = ((u + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
+    return u.view(F32)

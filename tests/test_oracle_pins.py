@@ -1,0 +1,420 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Every check here is independent of the oracle's own formulas: worked examples
+derived by hand, invariants the paper states (Sec. "Permutohedral Lattice",
+Eq. splat / Eq. slice), brute-force Delaunay search on tiny inputs, closed
+forms (affine reproduction, isometry), and library routines.
+"""
+import itertools
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from datagen.clouds import conv_weight, random_cloud
+from oracle import lattice_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _random_hyperplane_points(d, n, seed, spread=12.0):
+    rng = np.random.default_rng(seed)
+    x = rng.uniform(-spread, spread, size=(n, d + 1))
+    x -= x.mean(axis=1, keepdims=True)
+    return x.astype(np.float32)
+
+
+# --------------------------------------------------------------------------
+# elevation (Sec. "Permutohedral Lattice", Sec. "Method": G / sigma)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d", [1, 2, 3, 4])
+def test_elevation_is_scaled_isometry_onto_hyperplane(d):
+    """alpha E is alpha times an isometry from R^d onto H_d: columns orthogonal,
+    norm alpha, each summing to zero (so every elevated point lies on H_d)."""
+    sigma = np.ones(d, dtype=np.float32)
+    alpha = 1.0
+    fac = O.scale_factors(d, sigma, alpha)
+    cols = O.elevate(np.eye(d, dtype=np.float32), fac).astype(np.float64)  # row j = column j of E
+    G = cols @ cols.T
+    assert np.allclose(G, np.eye(d), atol=1e-6)
+    assert np.allclose(cols.sum(axis=1), 0.0, atol=1e-6)
+
+
+@pytest.mark.parametrize("d", [2, 3, 4])
+def test_elevation_norm_and_sum(d):
+    rng = np.random.default_rng(7)
+    g = rng.uniform(-3, 3, size=(500, d)).astype(np.float32)
+    sigma = rng.uniform(0.2, 2.0, size=d).astype(np.float32)
+    alpha = O.default_alpha(d)
+    x = O.elevate(g, O.scale_factors(d, sigma, alpha)).astype(np.float64)
+    s = g.astype(np.float64) / sigma.astype(np.float64)
+    assert np.allclose(np.linalg.norm(x, axis=1), alpha * np.linalg.norm(s, axis=1), rtol=2e-6)
+    assert np.all(np.abs(x.sum(axis=1)) <= 1e-5 * np.abs(x).max(axis=1) + 1e-6)
+
+
+def test_scale_factor_values():
+    f = O.scale_factors(3, [0.5, 0.25, 2.0], alpha=1.0)
+    expect = [1 / (0.5 * np.sqrt(2)), 1 / (0.25 * np.sqrt(6)), 1 / (2.0 * np.sqrt(12))]
+    assert np.allclose(f, expect, rtol=1e-7)
+    assert f.dtype == np.float32
+    # sigma given as a scalar broadcasts over the d axes
+    assert np.array_equal(O.scale_factors(3, 0.3), O.scale_factors(3, [0.3] * 3))
+
+
+# --------------------------------------------------------------------------
+# enclosing simplex, keys, barycentric weights
+# --------------------------------------------------------------------------
+
+def test_worked_examples():
+    cases = json.load(open(os.path.join(GOLDEN, "simplex_worked_examples.json")))["cases"]
+    for c in cases:
+        x = np.array([c["x"]], dtype=np.float32)
+        r, rank = O.enclosing_simplex(x)
+        b = O.barycentric(x, r, rank)[0]
+        keys = O.simplex_keys(r, rank)[0]
+        got = {tuple(int(v) for v in k): float(w) for k, w in zip(keys, b)}
+        listed = 0.0
+        for v, (num, den) in zip(c["vertices"], c["weights"]):
+            assert tuple(v) in got, c["name"]
+            assert abs(got[tuple(v)] - float(Fraction(num, den))) < 2e-7, c["name"]
+            listed += float(Fraction(num, den))
+        assert abs(listed - 1.0) < 1e-12
+        for k, w in got.items():
+            if list(k) not in c["vertices"]:
+                assert abs(w) < 1e-7, c["name"]
+
+
+@pytest.mark.parametrize("d", [1, 2, 3, 4])
+def test_key_invariants(d):
+    """Keys sum to 0; vertex k is congruent to k mod (d+1); consecutive simplex
+    vertices differ by -n_j with j running over a permutation of 0..d."""
+    x = _random_hyperplane_points(d, 2000, seed=d)
+    r, rank = O.enclosing_simplex(x)
+    keys = O.simplex_keys(r, rank)
+    assert np.all(keys.sum(axis=2) == 0)
+    for k in range(d + 1):
+        assert np.all(np.mod(keys[:, k, :] - k, d + 1) == 0)
+    n = (d + 1) * np.eye(d + 1, dtype=np.int64) - 1
+    cyc = np.concatenate([keys, keys[:, :1, :]], axis=1)
+    for p in range(0, 2000, 7):
+        js = []
+        for k in range(d + 1):
+            diff = cyc[p, k + 1] - cyc[p, k]   # k = d closes the cycle back to remainder 0
+            # -n_j: all ones except -d at coordinate j
+            j = int(np.argmin(diff))
+            assert np.array_equal(diff, -n[j]), (p, k, diff)
+            js.append(j)
+        assert sorted(js) == list(range(d + 1))
+
+
+@pytest.mark.parametrize("d", [1, 2, 3, 4])
+def test_barycentric_reconstruction(d):
+    """b >= 0, sum b = 1 and sum_k b_k c_k = x: x lies in the simplex spanned by the keys."""
+    x = _random_hyperplane_points(d, 5000, seed=10 + d)
+    r, rank = O.enclosing_simplex(x)
+    b = O.barycentric(x, r, rank)
+    keys = O.simplex_keys(r, rank).astype(np.float64)
+    assert b.min() >= -1e-6
+    assert np.allclose(b.sum(axis=1), 1.0, atol=1e-12)
+    rec = np.einsum("pk,pki->pi", b, keys)
+    x64 = x.astype(np.float64)
+    # x in fp32 is off H_d by rounding; compare on H_d
+    x64 = x64 - x64.mean(axis=1, keepdims=True)
+    assert np.allclose(rec, x64, atol=1e-5)
+
+
+def _delaunay_simplex(x, d, n_near=3):
+    """Brute force: the (d+1)-set of A*_d points, one per remainder class,
+    that contains x and whose circumsphere holds no lattice point."""
+    x = x.astype(np.float64)
+    x = x - x.mean()
+    dp1 = d + 1
+    cands, cls = [], []
+    for k in range(dp1):
+        u = (x - k) / dp1
+        base = np.floor(u[:d]).astype(np.int64)
+        for off in itertools.product(range(-2, 3), repeat=d):
+            z = base + np.array(off)
+            zd = -k - z.sum()
+            c = k + dp1 * np.append(z, zd)
+            cands.append(c)
+            cls.append(k)
+    cands = np.array(cands, dtype=np.float64)
+    cls = np.array(cls)
+    dist = np.linalg.norm(cands - x, axis=1)
+    near = [np.argsort(np.where(cls == k, dist, np.inf))[:n_near] for k in range(dp1)]
+    found = []
+    for combo in itertools.product(*near):
+        P = cands[list(combo)]                          # [d+1, d+1]
+        A = np.vstack([P.T, np.ones(dp1)])              # (d+2) x (d+1)
+        if np.linalg.matrix_rank(A) < dp1:              # affinely dependent: not a d-simplex
+            continue
+        lam, *_ = np.linalg.lstsq(A, np.append(x, 1.0), rcond=None)
+        if lam.min() < -1e-9 or np.abs(A @ lam - np.append(x, 1.0)).max() > 1e-9:
+            continue
+        M = np.vstack([2 * (P[1:] - P[0]), np.ones(dp1)])
+        rhs = np.append((P[1:] ** 2).sum(1) - (P[0] ** 2).sum(), 0.0)
+        o = np.linalg.solve(M, rhs)
+        R2 = ((P[0] - o) ** 2).sum()
+        inside = ((cands - o) ** 2).sum(1) < R2 * (1 - 1e-9)
+        if inside.any():
+            continue
+        found.append((P, lam))
+    return found
+
+
+@pytest.mark.parametrize("d", [1, 2, 3, 4])
+def test_enclosing_simplex_matches_brute_force_delaunay(d):
+    x = _random_hyperplane_points(d, 60 if d == 4 else 120, seed=100 + d, spread=9.0)
+    r, rank = O.enclosing_simplex(x)
+    keys = O.simplex_keys(r, rank)
+    b = O.barycentric(x, r, rank)
+    checked = 0
+    for p in range(x.shape[0]):
+        if b[p].min() < 1e-4:      # within rounding of a face: several simplices are correct
+            continue
+        found = _delaunay_simplex(x[p], d)
+        assert len(found) == 1, (p, len(found))
+        P, lam = found[0]
+        assert {tuple(v) for v in P.astype(np.int64)} == {tuple(v) for v in keys[p]}
+        order = {tuple(v): w for v, w in zip(P.astype(np.int64), lam)}
+        for k in range(d + 1):
+            assert abs(order[tuple(keys[p, k])] - b[p, k]) < 1e-5
+        checked += 1
+    assert checked > x.shape[0] // 2
+
+
+def test_rank_ties_lower_index_first():
+    """All Delta equal: ranks follow the coordinate index; the simplex is still valid."""
+    x = np.zeros((1, 4), dtype=np.float32)
+    r, rank = O.enclosing_simplex(x)
+    assert rank.tolist() == [[0, 1, 2, 3]]
+    assert r.tolist() == [[0, 0, 0, 0]]
+    b = O.barycentric(x, r, rank)
+    assert b.tolist() == [[1.0, 0.0, 0.0, 0.0]]
+
+
+# --------------------------------------------------------------------------
+# splat / slice (Eq. splat, Eq. slice)
+# --------------------------------------------------------------------------
+
+def _small_lattice(d=3, m=3000, seed=3, C=5, n_batch=0):
+    w = random_cloud(m, d, seed, extent=1.0, C=C, n_batch=n_batch)
+    lat = O.build(w.pos, 0.15, batch=w.batch)
+    return w, lat
+
+
+def test_splat_mass_conservation():
+    w, lat = _small_lattice()
+    vals, wt, _ = O.splat(lat, w.feat)
+    assert np.allclose(vals.sum(0), w.feat.astype(np.float64).sum(0), rtol=1e-10, atol=1e-9)
+    assert abs(wt.sum() - w.m) < 1e-8
+
+
+def test_splat_normalised_constant_field():
+    w, lat = _small_lattice()
+    const = np.full((w.m, 3), 2.5, dtype=np.float32)
+    vals, wt, _ = O.splat(lat, const, normalize=True)
+    nz = wt > 0
+    assert np.allclose(vals[nz], 2.5, rtol=1e-12)
+    assert np.all(vals[~nz] == 0)
+
+
+def test_splat_then_slice_of_constant_is_constant():
+    w, lat = _small_lattice()
+    const = np.full((w.m, 2), -1.25, dtype=np.float32)
+    vals, _, _ = O.splat(lat, const, normalize=True)
+    out, _ = O.slice_(lat, vals)
+    # zero-weight vertices of a simplex carry 0 but also get weight 0 in the slice
+    assert np.allclose(out, -1.25, rtol=1e-12)
+
+
+def test_single_point_splat_equals_weights():
+    pos = np.array([[0.123, -0.456, 0.789]], dtype=np.float32)
+    lat = O.build(pos, 0.1)
+    vals, wt, _ = O.splat(lat, np.array([[3.0]], dtype=np.float32))
+    assert lat.V == 4
+    for k in range(4):
+        v = lat.idx[0, k]
+        assert np.isclose(vals[v, 0], 3.0 * lat.bary[0, k])
+        assert np.isclose(wt[v], lat.bary[0, k])
+
+
+def test_slice_reproduces_affine_field():
+    """Barycentric interpolation is exact for affine functions: y_v = a . c_v + b0
+    slices to a . x_p + b0 (splat/slice are piecewise linear, Sec. "Permutohedral Lattice")."""
+    w, lat = _small_lattice(d=4, m=2000, seed=5)
+    rng = np.random.default_rng(0)
+    a = rng.standard_normal((lat.d + 1, 3))
+    b0 = rng.standard_normal(3)
+    y = lat.keys.astype(np.float64) @ a + b0
+    out, _ = O.slice_(lat, y)
+    expect = lat.x.astype(np.float64) @ a + b0
+    # fp32 x is off H_d by rounding; project before comparing
+    xh = lat.x.astype(np.float64)
+    xh = xh - xh.mean(axis=1, keepdims=True)
+    expect = xh @ a + b0
+    assert np.allclose(out, expect, atol=1e-4 * np.abs(expect).max())
+
+
+def test_splat_slice_adjoint():
+    """<S f, y> = <f, Y y>: splat and slice use the same weights (Sec. "Common Operations")."""
+    w, lat = _small_lattice(C=4)
+    rng = np.random.default_rng(1)
+    y = rng.standard_normal((lat.V, 4))
+    Sf, _, _ = O.splat(lat, w.feat)
+    Yy, _ = O.slice_(lat, y)
+    lhs = (Sf * y).sum()
+    rhs = (w.feat.astype(np.float64) * Yy).sum()
+    assert np.isclose(lhs, rhs, rtol=1e-10)
+
+
+def test_point_on_vertex_slices_vertex_value():
+    """A point on a remainder-0 lattice vertex has weight 1 there."""
+    d = 3
+    c = np.array([4, -4, 8, -8], dtype=np.float64)
+    # invert the elevation: g = sigma * E^T c / alpha, E from elevating unit vectors
+    fac = O.scale_factors(d, 1.0, 1.0)
+    E = O.elevate(np.eye(d, dtype=np.float32), fac).astype(np.float64).T   # [d+1, d]
+    g = (E.T @ c)[None, :].astype(np.float32)
+    lat = O.build(g, 1.0, alpha=1.0)
+    k0 = [k for k in range(4) if np.array_equal(lat.keys[lat.idx[0, k]], c.astype(np.int64))]
+    assert len(k0) == 1
+    assert lat.bary[0, k0[0]] > 1 - 1e-5
+
+
+def test_batched_lattice_is_concatenation_of_independent_lattices():
+    w = random_cloud(3000, 3, 11, extent=1.0, C=3, n_batch=4)
+    lat = O.build(w.pos, 0.2, batch=w.batch)
+    start = 0
+    for bb in range(4):
+        sel = w.batch == bb
+        sub = O.build(w.pos[sel], 0.2)
+        assert np.array_equal(lat.keys[start:start + sub.V], sub.keys)
+        assert np.all(lat.vbatch[start:start + sub.V] == bb)
+        vals, _, _ = O.splat(lat, w.feat)
+        svals, _, _ = O.splat(sub, w.feat[sel])
+        assert np.allclose(vals[start:start + sub.V], svals, rtol=1e-12, atol=1e-12)
+        start += sub.V
+    assert start == lat.V
+    nbr = O.neighbors(lat)
+    present = nbr >= 0
+    rows = np.repeat(np.arange(lat.V)[:, None], nbr.shape[1], axis=1)
+    assert np.all(lat.vbatch[nbr[present]] == lat.vbatch[rows[present]])
+
+
+# --------------------------------------------------------------------------
+# neighbours (Sec. "Permutohedral Lattice": 2(d+1) neighbours at +-n_j)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d", [2, 3, 4])
+def test_neighbour_offsets_symmetry_and_presence(d):
+    w = random_cloud(1500, d, 20 + d, extent=1.0, C=1)
+    lat = O.build(w.pos, 0.2)
+    nbr = O.neighbors(lat)
+    T = 2 * (d + 1) + 1
+    assert nbr.shape == (lat.V, T)
+    assert np.array_equal(nbr[:, 0], np.arange(lat.V))
+    keyset = {tuple(k) for k in lat.keys}
+    n = (d + 1) * np.eye(d + 1, dtype=np.int64) - 1
+    for v in range(0, lat.V, 3):
+        for j in range(d + 1):
+            for t, sgn in ((1 + j, 1), (d + 2 + j, -1)):
+                q = tuple(lat.keys[v] + sgn * n[j])
+                u = nbr[v, t]
+                if q in keyset:
+                    assert u >= 0 and tuple(lat.keys[u]) == q
+                    back = d + 2 + j if sgn == 1 else 1 + j
+                    assert nbr[u, back] == v
+                else:
+                    assert u == -1
+
+
+@pytest.mark.parametrize("d", [2, 3, 4])
+def test_simplex_edges_are_one_ring_taps(d):
+    """Cyclically consecutive simplex vertices k, k+1 differ by -n_j (the edge
+    vectors of the lattice): vertex k+1 must be tap d+2+j of vertex k."""
+    w = random_cloud(800, d, 30 + d, extent=1.0, C=1)
+    lat = O.build(w.pos, 0.2)
+    nbr = O.neighbors(lat)
+    for p in range(w.m):
+        for k in range(d + 1):
+            a = lat.idx[p, k]
+            b = lat.idx[p, (k + 1) % (d + 1)]
+            taps = np.nonzero(nbr[a] == b)[0]
+            assert len(taps) == 1
+            t = int(taps[0])
+            assert t >= 1
+            diff = lat.keys[b] - lat.keys[a]
+            off = O.neighbor_offsets(d)[t]
+            assert np.array_equal(diff, off)
+
+
+# --------------------------------------------------------------------------
+# convolution (Sec. "Common Operations": Convolving)
+# --------------------------------------------------------------------------
+
+def test_conv_identity_centre_tap():
+    w, lat = _small_lattice(C=6)
+    nbr = O.neighbors(lat)
+    x = np.random.default_rng(2).standard_normal((lat.V, 6))
+    W = np.zeros((6, nbr.shape[1], 6))
+    W[:, 0, :] = np.eye(6)
+    y, _ = O.conv(x, nbr, W)
+    assert np.allclose(y, x, rtol=0, atol=0)
+
+
+def test_conv_impulse_pins_tap_order_and_sign():
+    """One non-zero vertex u (value e_i): a vertex v whose tap t reaches u
+    receives W[:, t, i]; every other vertex receives 0."""
+    d = 3
+    w, lat = _small_lattice(d=d, C=2)
+    nbr = O.neighbors(lat)
+    T = nbr.shape[1]
+    W = conv_weight(3, 4, d, seed=9).astype(np.float64)
+    u = lat.V // 2
+    x = np.zeros((lat.V, 3))
+    x[u, 1] = 1.0
+    y, _ = O.conv(x, nbr, W)
+    offs = O.neighbor_offsets(d)
+    keyidx = {tuple(k): i for i, k in enumerate(lat.keys)}
+    expect = np.zeros_like(y)
+    for t in range(T):
+        v = keyidx.get(tuple(lat.keys[u] - offs[t]))   # key_v + off_t = key_u
+        if v is not None:
+            expect[v] += W[:, t, 1]
+    assert np.allclose(y, expect, atol=0)
+    assert np.abs(expect).sum() > 0
+
+
+def test_conv_equals_dense_im2col_matmul():
+    """The per-tap sum equals one dense [V, T C_in] x [T C_in, C_out] product."""
+    w, lat = _small_lattice(C=3)
+    nbr = O.neighbors(lat)
+    T = nbr.shape[1]
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((lat.V, 5))
+    W = rng.standard_normal((7, T, 5))
+    Z = np.zeros((lat.V, T, 5))
+    for t in range(T):
+        ok = nbr[:, t] >= 0
+        Z[ok, t] = x[nbr[ok, t]]
+    dense = Z.reshape(lat.V, T * 5) @ W.reshape(7, T * 5).T
+    y, _ = O.conv(x, nbr, W)
+    assert np.allclose(y, dense, rtol=1e-12, atol=1e-12)
+
+
+def test_bf16_rounding_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(5)
+    a = np.concatenate([
+        rng.standard_normal(100000).astype(np.float32) * 10.0 ** rng.integers(-6, 6, 100000),
+        # exact ties between two bf16 neighbours, both parities
+        np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 0.0, -0.0, 65504.0], dtype=np.float32),
+    ]).astype(np.float32)
+    ref = torch.from_numpy(a).to(torch.bfloat16).to(torch.float32).numpy()
+    got = O.round_bf16(a)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
