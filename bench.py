@@ -1,0 +1,262 @@
+"""Benchmark of the lattice hot path on one MI355X.
+
+One step = one pass of the whole path over one synthetic cloud: splat (build
+the lattice and splat the point features), build the 1-ring neighbour table,
+every lattice convolution the workload lists (chained: each one's output
+feeds the next), and slice the last output back onto the points.  The inputs
+(positions, features, batch ids, weights already rounded to bf16 where the
+conv is bf16) are resident in HBM before the timed region; every step
+rebuilds the lattice from scratch.
+
+Prints one JSON line.  `value` is points per second of whole steps; the
+`roofline` object reports the step's dominant kernel against its own
+roofline, timed with HIP events recorded on the stream the kernels run on;
+`cpu_baseline` is the CPU oracle timed on this host on a bounded sample.
+
+Usage: python bench.py [--steps K] [--warmup W] [--config N] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+DEFAULT_CONFIG = 2          # part-segmentation-shaped batch: 16 objects x 2500 points
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+WORKLOAD_NAMES = {
+    1: "tiny-spheres-4096pts-d3",
+    2: "partseg-16x2500pts-d3-sigma0.04-C64-conv64x64-f32+bf16",
+    3: "indoor-room-200kpts-d3-sigma0.04-C64-conv64x64+64x128-bf16",
+    4: "lidar-scan-64beam-d3-sigma0.3-C128-conv128x128-bf16",
+    5: "spatiotemporal-4scans-d4-sigma0.3-C64-conv64x64-bf16",
+}
+
+
+class Pipeline:
+    """Device-resident inputs and buffers of one workload, and one step over them."""
+
+    def __init__(self, w, stream=None):
+        import torch
+
+        from paper_2108_03917_amd import Lattice
+
+        self.w = w
+        dev = torch.device("cuda:0")
+        torch.cuda.set_device(dev)
+        self.L = Lattice(w.d, w.sigma, max_points=w.m, stream=stream)
+        self.pos = torch.from_numpy(w.pos).to(dev)
+        self.feat = torch.from_numpy(w.feat).to(dev)
+        self.batch = None if w.batch is None else torch.from_numpy(w.batch).to(dev)
+        mv = self.L.max_vertices(w.m)
+        self.values = torch.empty((mv, w.C), dtype=torch.float32, device=dev)
+        self.convs = list(w.convs)
+        self.weights, self.outs = [], []
+        for cv in self.convs:
+            wd = torch.from_numpy(cv.weight).to(dev)
+            if cv.dtype == "bf16":
+                wd = self.L.weights_to_bf16(wd)   # parameters: rounded once, outside the step
+            self.weights.append(wd)
+            self.outs.append(torch.empty((mv, cv.c_out), dtype=torch.float32, device=dev))
+        c_last = self.convs[-1].c_out if self.convs else w.C
+        self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+
+    @property
+    def conv_spec(self):
+        return self.convs[-1]
+
+    def run(self, ev=None):
+        """One step.  With `ev` (a list of torch events) an event is recorded
+        before every stage and one after the last, on the current stream."""
+        L = self.L
+        k = 0
+
+        def mark():
+            nonlocal k
+            if ev is not None:
+                ev[k].record()
+                k += 1
+
+        mark()
+        L.splat(self.pos, self.feat, self.batch, values=self.values, want_weight=False)
+        mark()
+        L.build_neighbors()
+        x = self.values
+        for cv, wd, out in zip(self.convs, self.weights, self.outs):
+            mark()
+            L.conv(x, wd, dtype=cv.dtype, out=out)
+            x = out
+        mark()
+        L.slice(x, out=self.sliced)
+        mark()
+        return self.sliced
+
+    def stage_names(self):
+        return ["splat", "neighbors"] + [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}" for i, c in enumerate(self.convs)] \
+            + ["slice"]
+
+
+def algorithmic_work(w, V):
+    """Compulsory HBM bytes (and MFMA flops) of each stage of one step.
+
+    splat:     read positions (4d B), batch id (4 B), features (4C B) and write
+               the simplex record (vertex index + weight, 8(d+1) B) per point;
+               write the value row (4C B) and packed key (8 B) per vertex.
+    neighbors: read the key (8 B), write T indices (4T B) per vertex.
+    conv:      read the input row (4 C_in), neighbour row (4T), write the output
+               row (4 C_out) per vertex, plus the weights once; 2 T C_in C_out
+               flops per vertex.
+    slice:     read the record (8(d+1)) and write the output row (4C) per point,
+               read each vertex row once (4C per vertex)."""
+    d, m, C = w.d, w.m, w.C
+    T = 2 * (d + 1) + 1
+    work = {}
+    work["splat"] = {"bytes": m * (4 * d + 4 * C + 8 * (d + 1) + (4 if w.batch is not None else 0))
+                     + V * (4 * C + 8)}
+    work["neighbors"] = {"bytes": V * (8 + 4 * T)}
+    for i, cv in enumerate(w.convs):
+        s = 2 if cv.dtype == "bf16" else 4
+        work[f"conv{i}_{cv.c_in}x{cv.c_out}_{cv.dtype}"] = {
+            "bytes": V * (4 * cv.c_in + 4 * T + 4 * cv.c_out) + T * cv.c_in * cv.c_out * s,
+            "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": cv.dtype}
+    c_last = w.convs[-1].c_out if w.convs else C
+    work["slice"] = {"bytes": m * (8 * (d + 1) + 4 * c_last) + V * 4 * c_last}
+    return work
+
+
+def roofline_entry(name, ms, wk):
+    """achieved vs peak for one stage: MFMA-bound convs where their arithmetic
+    intensity exceeds the ridge, HBM otherwise."""
+    if "flops" in wk:
+        peak_t = MFMA_PEAK_TFLOPS[wk["dtype"]]
+        ridge = peak_t * 1e12 / (HBM_PEAK_GBS * 1e9)
+        if wk["flops"] / wk["bytes"] >= ridge:
+            a = wk["flops"] / (ms * 1e-3) / 1e12
+            return {"bound": "mfma", "achieved": a, "peak": peak_t, "unit": "TFLOP/s", "frac": a / peak_t}
+    a = wk["bytes"] / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a / HBM_PEAK_GBS}
+
+
+def cpu_baseline(w, budget_s=20.0):
+    """The CPU oracle, as it stands, over the same workload: whole steps
+    (lattice build, splat, neighbours, every conv, slice) repeated until
+    about `budget_s` seconds, reported as points/s."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import lattice_oracle as O
+
+    def one():
+        lat = O.build(w.pos, w.sigma, batch=w.batch)
+        x, _, _ = O.splat(lat, w.feat)
+        nbr = O.neighbors(lat)
+        for cv in w.convs:
+            xi = x
+            Wt = cv.weight
+            if cv.dtype == "bf16":
+                xi = O.round_bf16(x.astype(np.float32))
+                Wt = O.round_bf16(Wt)
+            x, _ = O.conv(xi, nbr, Wt)
+        O.slice_(lat, x)
+
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        one()
+        n += 1
+        if time.perf_counter() - t0 >= budget_s or n >= 50:
+            break
+    dt = time.perf_counter() - t0
+    threads = 1
+    for info in threadpool_info():
+        threads = max(threads, int(info.get("num_threads", 1)))
+    return {"value": n * w.m / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} whole step(s) of the {w.name} workload ({w.m} points), {dt:.1f} s"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=DEFAULT_CONFIG)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested): the lattice path has no "
+              "multi-GPU mode", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from datagen.clouds import make_workload
+
+    w = make_workload(args.config)
+    pipe = Pipeline(w)
+    for _ in range(args.warmup):
+        pipe.run()
+    torch.cuda.synchronize()
+    V = pipe.L.num_vertices()
+
+    names = pipe.stage_names()
+    nev = len(names) + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        pipe.run(evs[s])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sec = t1 - t0
+    stage_ms = {n: 0.0 for n in names}
+    for s in range(args.steps):
+        for i, n in enumerate(names):
+            stage_ms[n] += evs[s][i].elapsed_time(evs[s][i + 1])
+    stage_ms = {n: v / args.steps for n, v in stage_ms.items()}
+
+    work = algorithmic_work(w, V)
+    stages = {n: dict(ms=stage_ms[n], **roofline_entry(n, stage_ms[n], work[n])) for n in names}
+    dominant = max(names, key=lambda n: stage_ms[n])
+    rf = dict(stages[dominant])
+    rf.pop("ms")
+    rf["kernel"] = dominant
+    rf["traffic"] = None
+
+    out = {
+        "metric": "points/s for splat+conv+slice",
+        "value": w.m * args.steps / sec,
+        "unit": "points/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": sec * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 splat/slice, " + "+".join(f"{c.dtype} conv" for c in w.convs),
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_NAMES.get(args.config, w.name), "points": w.m, "d": w.d,
+                   "sigma": float(w.sigma[0]), "channels": w.C, "vertices": V,
+                   "convs": [f"{c.c_in}->{c.c_out} {c.dtype}" for c in w.convs]},
+        "roofline": rf,
+        "stages": stages,
+        "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -353,3 +353,9 @@ def random_cloud(m: int, d: int, seed: int, extent: float = 1.0, C: int = 4,
 def conv_weight(c_in: int, c_out: int, d: int, seed: int, std: float = 0.1) -> np.ndarray:
     """Seeded N(0, std^2) weights in ``[C_out][2(d+1)+1][C_in]`` layout."""
     return _conv_weight(np.random.default_rng(seed), c_in, c_out, 2 * (d + 1) + 1, std)
+
+
+def random_rows(n: int, C: int, seed: int, std: float = 1.0) -> np.ndarray:
+    """Seeded N(0, std^2) float32 rows [n, C]: stand-alone inputs for one stage
+    (vertex values fed to a convolution or a slice)."""
+    return (np.random.default_rng(seed).standard_normal((n, C)) * std).astype(np.float32)

@@ -1,0 +1,248 @@
+/*
+ * lattice.h -- C ABI of the sparse permutohedral-lattice hot path for MI355X (gfx950).
+ *
+ * The library implements the three lattice operations of LatticeNet
+ * (Rosu et al., arXiv 2108.03917) in the order the paper states them:
+ * splat a point cloud onto the occupied vertices of a d-dimensional
+ * permutohedral lattice, convolve the vertex values over the 1-hop ring,
+ * and slice the result back onto the points.
+ *
+ *   Sec. "Notation": a cloud is P = (G, F) with positions G in R^{m x d} and
+ *     features F in R^{m x f_d}; a lattice vertex is (c_v, x_v) with integer
+ *     coordinates c_v in Z^{d+1} and values x_v in R^{v_d}; I_p is the set of
+ *     d+1 vertices of the simplex containing point p.
+ *   Sec. "Permutohedral Lattice": the lattice is (d+1)Z^{d+1} projected along
+ *     the all-ones vector onto the hyperplane H_d, so every key sums to zero;
+ *     the enclosing simplex comes from a rounding algorithm; the 2(d+1)
+ *     neighbours of a vertex sit at +-[-1,..,-1,d,-1,..,-1]; vertices are kept
+ *     sparsely in a hash map keyed by c_v.
+ *   Sec. "Method": positions are scaled as G / sigma, sigma in R^d.
+ *   Sec. "Common Operations on Permutohedral Lattice": splatting (barycentric
+ *     weights onto the d+1 simplex vertices, summed per vertex), convolving
+ *     over the 2(d+1)+1 vertices of the 1-hop ring (an unallocated neighbour
+ *     contributes zero), slicing (the reverse of splatting with the same
+ *     barycentric weights); Eq. (splat) and Eq. (slice).
+ *
+ * Conventions fixed by this library where the paper leaves them open
+ * (the CPU test oracle adopts the same ones):
+ *   - elevation x = alpha * E * (g / sigma), E the orthonormal basis of H_d
+ *     whose j-th column is (1,..,1,-j,0,..,0)/sqrt(j(j+1)) (j ones);
+ *     alpha <= 0 selects (d+1) * sqrt(2/3);
+ *   - round half to even when rounding to the remainder-0 point; rank ties go
+ *     to the lower coordinate index;
+ *   - all d+1 vertices of every point's simplex are allocated;
+ *   - 1-ring tap order: tap 0 = the vertex, tap 1+j = c + n_j,
+ *     tap d+2+j = c - n_j (j = 0..d), n_j = (d+1) e_j - 1;
+ *   - convolution weights are laid out [C_out][T][C_in], T = 2(d+1)+1.
+ *
+ * Memory.  Every pointer marked "dev" is device memory on the device that was
+ * current at lattice_create; "host" pointers are host memory.  The caller owns
+ * every buffer it passes in; the lattice owns its internal buffers (hash
+ * table, packed vertex keys, per-point simplex records, neighbour table,
+ * counters).  All work is enqueued on the stream given at creation; no call
+ * except lattice_num_vertices, lattice_get_status and lattice_destroy
+ * synchronises with the host.  The number of occupied vertices V stays on the
+ * device between splat, conv and slice: kernels read it there.
+ *
+ * Errors.  Functions return a lattice_status.  Argument and call-order errors
+ * are detected synchronously and nothing is enqueued.  Failures that only the
+ * device can see (hash table full, key coordinate out of range, batch id out
+ * of range) set a device status word; lattice_num_vertices and
+ * lattice_get_status report it.  It is cleared by the next lattice_splat.
+ * lattice_last_error returns a message for the last failure on a lattice.
+ *
+ * Threading.  A lattice is not thread safe; calls on one lattice must be
+ * serialised by the caller.  Distinct lattices are independent.
+ */
+#ifndef LATTICE_H
+#define LATTICE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lattice lattice;
+
+typedef enum {
+    LATTICE_OK = 0,
+    LATTICE_E_ARG = 1,      /* bad argument (null pointer, d, C, m out of range, ...) */
+    LATTICE_E_STATE = 2,    /* call out of order, e.g. conv or slice before splat      */
+    LATTICE_E_RANGE = 3,    /* device: a key coordinate or batch id does not fit 16 bits */
+    LATTICE_E_CAPACITY = 4, /* device: the hash table is full                          */
+    LATTICE_E_NOMEM = 5,    /* device or host allocation failed                        */
+    LATTICE_E_HIP = 6       /* a HIP runtime call failed (no device, launch failure)   */
+} lattice_status;
+
+typedef enum {
+    LATTICE_F32 = 0,  /* fp32 inputs and weights, fp32 accumulation (fp32 MFMA or FMA) */
+    LATTICE_BF16 = 1  /* inputs rounded to bf16 (nearest even), bf16 weights, fp32 accumulation on MFMA */
+} lattice_dtype;
+
+/* Largest lattice dimension, and the tap count of the 1-ring for dimension d. */
+#define LATTICE_MAX_D 4
+#define LATTICE_TAPS(d) (2 * ((d) + 1) + 1)
+
+/*
+ * lattice_create -- allocate a lattice for clouds of up to max_points points.
+ *
+ * Sec. "Permutohedral Lattice" and Sec. "Method" (G / sigma).
+ *   d              lattice dimension, 1..4 (the paper's clouds use d = 3; the
+ *                  space-time lattice uses d = 4).
+ *   sigma          host [d] fp32, per-axis lattice scale, each > 0.
+ *   alpha          elevation scale; <= 0 selects (d+1) * sqrt(2/3).
+ *   max_points     upper bound on m for every later splat, >= 1.
+ *   hash_capacity  number of hash slots; 0 selects the next power of two
+ *                  >= (d+1) * max_points, which can never fill up.  A non-zero
+ *                  value is rounded up to a power of two; a table that fills
+ *                  makes splat report LATTICE_E_CAPACITY.
+ *   stream         hipStream_t every call of this lattice is enqueued on
+ *                  (NULL = the null stream).
+ *   out            host: receives the new lattice.
+ * Returns LATTICE_E_ARG, LATTICE_E_NOMEM or LATTICE_E_HIP on failure, in
+ * which case *out is NULL.
+ */
+lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t max_points,
+                              int64_t hash_capacity, void *stream, lattice **out);
+
+/* Release every buffer of L (after synchronising its stream).  NULL is a no-op. */
+void lattice_destroy(lattice *L);
+
+/*
+ * lattice_max_vertices -- the row count callers allocate for per-vertex
+ * buffers (values, conv output): min((d+1) * m, hash capacity).  The actual V
+ * of a splat is never larger.  Returns -1 for a NULL lattice or m < 0.
+ */
+int64_t lattice_max_vertices(const lattice *L, int64_t m);
+
+/*
+ * lattice_splat -- build the sparse lattice of a cloud and splat its features.
+ *
+ * Sec. "Permutohedral Lattice" (enclosing simplex, hash map of keys) and
+ * Eq. (splat):  x_v = sum_{p in J_v} b_pv f_p.  Also w_v = sum_{p in J_v} b_pv.
+ *   pos        dev [m][d] fp32, row-major point positions (unscaled).
+ *   batch      dev [m] int32 batch id per point in [0, 65535], or NULL.  Each
+ *              id is an independent lattice sharing one table; neighbours
+ *              never cross ids.  Must be NULL when d = 4.
+ *   m          number of points, 0 <= m <= max_points (m = 0 gives V = 0).
+ *   feat       dev [m][C] fp32 row-major features, or NULL when C = 0 (then
+ *              only the lattice is built).
+ *   C          feature channels, 0..4096.
+ *   normalize  0: values hold the raw sum x_v;  1: values hold x_v / w_v
+ *              (0 where w_v = 0).
+ *   values     dev [>= lattice_max_vertices(L, m)][C] fp32 output; rows 0..V-1
+ *              are written (may be NULL when C = 0 or m = 0).
+ *   weight     dev [>= lattice_max_vertices(L, m)] fp32 output w_v, or NULL.
+ * Resets the lattice: the previous vertex set, records and neighbour table
+ * are discarded.  Device-side failures are reported by lattice_num_vertices.
+ */
+lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch, int64_t m,
+                             const float *feat, int C, int normalize, float *values, float *weight);
+
+/*
+ * lattice_build_neighbors -- build the 1-hop-ring neighbour table of the
+ * last splat's vertices now (otherwise the first lattice_conv builds it).
+ *
+ * Sec. "Permutohedral Lattice": the 2(d+1) neighbours of vertex c are
+ * c +- n_j, n_j = (d+1) e_j - 1; Sec. "Common Operations": the convolution
+ * spans the vertex and these neighbours (T = 2(d+1)+1 taps).  One hash
+ * lookup per tap; a neighbour that is not allocated gets index -1.
+ * Returns LATTICE_E_STATE before the first splat; a no-op when the table of
+ * the current lattice exists.
+ */
+lattice_status lattice_build_neighbors(lattice *L);
+
+/*
+ * lattice_conv -- 1-hop-ring lattice convolution over the occupied vertices.
+ *
+ * Sec. "Common Operations on Permutohedral Lattice" (Convolving) and the
+ * caption of its figure (an unallocated neighbour contributes zero):
+ *   y_v[o] = bias[o] + sum_{t < T} sum_{i < C_in} x_{nbr(v,t)}[i] * W[o][t][i].
+ *   in      dev [V][C_in] fp32 vertex values (rows of the last splat's vertices).
+ *   C_in    input channels, 1..1024.
+ *   w       dev weights [C_out][T][C_in]: fp32 for LATTICE_F32, bf16 (raw
+ *           16-bit patterns) for LATTICE_BF16 (see lattice_weights_to_bf16).
+ *   C_out   output channels, 1..1024.
+ *   dt      LATTICE_F32 or LATTICE_BF16.  With LATTICE_BF16 the inputs are
+ *           rounded to bf16 (nearest even) as they are gathered, products are
+ *           exact and sums are fp32.
+ *   bias    dev [C_out] fp32 or NULL.
+ *   out     dev [>= V][C_out] fp32; must not overlap `in`.
+ * The first conv after a splat also builds the neighbour table (2(d+1) hash
+ * lookups per vertex).  Returns LATTICE_E_STATE before the first splat.
+ */
+lattice_status lattice_conv(lattice *L, const float *in, int C_in, const void *w, int C_out,
+                            lattice_dtype dt, const float *bias, float *out);
+
+/*
+ * lattice_slice -- interpolate vertex values back onto the points.
+ *
+ * Eq. (slice):  f_p = sum_{v in I_p} b_pv x_v, with the barycentric weights
+ * of the last splat.
+ *   values  dev [V][C] fp32.
+ *   C       channels, 1..4096.
+ *   out     dev [m][C] fp32 (m of the last splat).
+ * Returns LATTICE_E_STATE before the first splat.
+ */
+lattice_status lattice_slice(lattice *L, const float *values, int C, float *out);
+
+/*
+ * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to
+ * even) on the lattice's stream: the weight format LATTICE_BF16 convs take.
+ *   src  dev [n] fp32;  dst  dev [n] uint16 (bf16 bit patterns).
+ */
+lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst);
+
+/*
+ * lattice_num_vertices -- synchronise the stream and return V of the last
+ * splat in *V.  Returns the device status (LATTICE_E_CAPACITY,
+ * LATTICE_E_RANGE) if the splat failed on the device, LATTICE_E_STATE before
+ * the first splat.
+ */
+lattice_status lattice_num_vertices(lattice *L, int64_t *V);
+
+/* lattice_get_status -- synchronise and return the device status of the last splat. */
+lattice_status lattice_get_status(lattice *L);
+
+/*
+ * Introspection of the sparse lattice (for tests and downstream operators).
+ * Outputs are dev buffers with at least V rows; vertex order is the order in
+ * which the hash table created the vertices and is not deterministic.
+ *   lattice_get_keys      keys dev [V][d+1] int32 (sum to zero per row);
+ *                         batch dev [V] int32 or NULL.
+ *   lattice_get_neighbors nbr dev [V][T] int32, -1 where a neighbour is not
+ *                         allocated (builds the table if needed).
+ *   lattice_get_point_simplex  idx dev [m][d+1] int32 vertex index of the
+ *                         simplex vertex with remainder k (column k); bary dev
+ *                         [m][d+1] fp32 its barycentric weight.  Either may be NULL.
+ */
+lattice_status lattice_get_keys(lattice *L, int32_t *keys, int32_t *batch);
+lattice_status lattice_get_neighbors(lattice *L, int32_t *nbr);
+lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary);
+
+/*
+ * Stage timing.  With lattice_set_timing(L, 1) the library records a pair of
+ * hipEvents on its stream around every stage it launches (splat, neighbours,
+ * conv, slice) and accumulates their elapsed times; lattice_get_timing
+ * synchronises and returns, per stage, the summed milliseconds and the number
+ * of launches since the last reset (arrays of LATTICE_NUM_STAGES).
+ * lattice_set_timing(L, 0) stops recording; (L, 2) resets the sums.
+ */
+#define LATTICE_NUM_STAGES 4
+enum { LATTICE_STAGE_SPLAT = 0, LATTICE_STAGE_NEIGHBORS = 1, LATTICE_STAGE_CONV = 2, LATTICE_STAGE_SLICE = 3 };
+lattice_status lattice_set_timing(lattice *L, int mode);
+lattice_status lattice_get_timing(lattice *L, double *ms, int64_t *count);
+
+/* Query the hash capacity and dimension of L. */
+int64_t lattice_hash_capacity(const lattice *L);
+int lattice_dim(const lattice *L);
+
+const char *lattice_status_string(lattice_status s);
+const char *lattice_last_error(const lattice *L);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LATTICE_H */

@@ -1,0 +1,289 @@
+// 1-hop-ring lattice convolution (Sec. "Common Operations on Permutohedral
+// Lattice", Convolving; an unallocated neighbour contributes zero):
+//   y_v[o] = bias[o] + sum_t sum_i x_{nbr(v,t)}[i] W[o][t][i].
+//
+// After the gather this is one dense product Y[V x C_out] = Z[V x K] W^T with
+// K = T C_in, where row v of Z is the concatenation of the T neighbour rows.
+// Both Z (gathered rows) and W ([C_out][T][C_in]) are K-contiguous, which is
+// the operand layout the MFMA instructions consume.
+//
+// k_conv_mfma: a workgroup owns a BM x BN output tile and walks K in chunks
+// of 128 bytes per row (64 bf16 or 32 fp32 channels of one tap).  Per chunk
+// it gathers the BM neighbour rows from global memory (fp32, rounded to bf16
+// on the way for the bf16 path), stages them and the BN weight rows in LDS
+// (double buffered: the next chunk's global loads are in flight while the
+// current chunk feeds the matrix cores), and each wavefront computes a 64 x 64
+// sub-tile as 2 x 2 MFMA 32x32 blocks.  The tile loop is persistent: V lives
+// on the device, so the grid is sized for the largest lattice and every
+// workgroup reads V and strides over the tiles.
+//
+// k_conv_generic: one thread per output element, for channel counts the MFMA
+// tiling does not cover (e.g. 8 -> 16).
+#include "internal.h"
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16 bits, round to nearest with ties to even (inputs are finite;
+// NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+constexpr int kRowBytes = 144;  // one LDS row: 128 bytes of K plus 16 bytes of padding
+
+// Largest tap count (d = 4): the tile's neighbour rows are staged in LDS.
+constexpr int kMaxTaps = LATTICE_TAPS(LATTICE_MAX_D);
+
+// BM x BN output tile per workgroup; each wavefront owns a WR x WC sub-tile
+// made of (WR/32) x (WC/32) MFMA 32x32 blocks.
+template <bool BF16, int BM, int BN, int WR, int WC>
+__global__ __launch_bounds__((BM / WR) * (BN / WC) * 64) void k_conv_mfma(
+    const float *__restrict__ in, int C_in, const void *__restrict__ wv, int C_out, int T,
+    const float *__restrict__ bias, float *__restrict__ out, const int32_t *__restrict__ nbr,
+    const int32_t *__restrict__ counters) {
+    constexpr int WN = BN / WC;             // wavefronts along N
+    constexpr int NT = (BM / WR) * WN * 64;
+    constexpr int TI = WR / 32;             // MFMA blocks per wave along M
+    constexpr int TJ = WC / 32;             // MFMA blocks per wave along N
+    constexpr int KC = BF16 ? 64 : 32;      // K elements per chunk (128 bytes of LDS row)
+    constexpr int A_SEGS = KC * 4 / 16;     // 16-byte fp32 source segments per gathered row
+    constexpr int A_RPP = NT / A_SEGS;      // gathered rows per pass
+    constexpr int A_PASSES = BM / A_RPP;
+    constexpr int B_RPP = NT / 8;           // weight rows per pass (8 x 16 B per row)
+    constexpr int B_PASSES = BN / B_RPP;
+    constexpr int ESZ = BF16 ? 2 : 4;
+    static_assert(A_PASSES * A_RPP == BM, "A tiling");
+    static_assert(B_PASSES * B_RPP == BN, "B tiling");
+
+    __shared__ __attribute__((aligned(16))) char lds[2 * (BM + BN) * kRowBytes];
+    __shared__ int32_t nbr_s[BM * kMaxTaps];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WN;
+    const int wn = wave % WN;
+    const int64_t V = counters[CNT_V];
+    const int64_t n_mt = (V + BM - 1) / BM;
+    const int n_nt = C_out / BN;
+    const int64_t ntiles = n_mt * n_nt;
+    const int64_t K = (int64_t)T * C_in;
+    const int CPT = C_in / KC;
+    const int NQ = T * CPT;
+
+    const int a_seg = tid % A_SEGS;
+    const int a_row0 = tid / A_SEGS;
+    const int b_seg = tid & 7;
+    const int b_row0 = tid >> 3;
+    const int lrow = lane & 31;
+    const int khalf = lane >> 5;
+
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t row_base = (tile / n_nt) * BM;
+        const int col_base = (int)(tile % n_nt) * BN;
+
+        // The tile's neighbour rows are one contiguous run of BM * T indices.
+        for (int i = tid; i < BM * T; i += NT) {
+            const int64_t e = row_base * T + i;
+            nbr_s[i] = (e < V * T) ? nbr[e] : -1;
+        }
+        __syncthreads();
+
+        f32x16_t acc[TI][TJ];
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+        f32x4_t areg[A_PASSES];
+        u32x4_t breg[B_PASSES];
+        bool present[A_PASSES];
+
+        // Branch-free gather: an absent neighbour reads row 0 (V >= 1 whenever
+        // a tile exists) and is zeroed when it is written to LDS, so all loads
+        // of a chunk are in flight together and stay in flight during compute.
+        auto load_chunk = [&](int q) {
+            const int t = q / CPT;
+            const int c0 = (q - t * CPT) * KC;
+#pragma unroll
+            for (int i = 0; i < A_PASSES; ++i) {
+                const int u = nbr_s[(a_row0 + i * A_RPP) * T + t];
+                present[i] = u >= 0;
+                const int64_t row = u >= 0 ? u : 0;
+                areg[i] = *reinterpret_cast<const f32x4_t *>(in + row * C_in + c0 + a_seg * 4);
+            }
+#pragma unroll
+            for (int i = 0; i < B_PASSES; ++i) {
+                const int64_t n = col_base + b_row0 + i * B_RPP;
+                const char *src = reinterpret_cast<const char *>(wv) + (n * K + (int64_t)t * C_in + c0) * ESZ + b_seg * 16;
+                breg[i] = *reinterpret_cast<const u32x4_t *>(src);
+            }
+        };
+        auto store_chunk = [&](int buf) {
+            char *A = lds + buf * (BM + BN) * kRowBytes;
+            char *B = A + BM * kRowBytes;
+#pragma unroll
+            for (int i = 0; i < A_PASSES; ++i) {
+                const int row = a_row0 + i * A_RPP;
+                const f32x4_t x = present[i] ? areg[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+                if (BF16) {
+                    u32x2_t pk;
+                    pk[0] = bf16_bits(x[0]) | (bf16_bits(x[1]) << 16);
+                    pk[1] = bf16_bits(x[2]) | (bf16_bits(x[3]) << 16);
+                    *reinterpret_cast<u32x2_t *>(A + row * kRowBytes + a_seg * 8) = pk;
+                } else {
+                    *reinterpret_cast<f32x4_t *>(A + row * kRowBytes + a_seg * 16) = x;
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < B_PASSES; ++i) {
+                const int n = b_row0 + i * B_RPP;
+                *reinterpret_cast<u32x4_t *>(B + n * kRowBytes + b_seg * 16) = breg[i];
+            }
+        };
+        auto compute = [&](int buf) {
+            const char *A = lds + buf * (BM + BN) * kRowBytes;
+            const char *B = A + BM * kRowBytes;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int boff = g * 32 + khalf * 16;
+                u32x4_t a[TI], b[TJ];
+#pragma unroll
+                for (int i = 0; i < TI; ++i)
+                    a[i] = *reinterpret_cast<const u32x4_t *>(A + (wm * WR + i * 32 + lrow) * kRowBytes + boff);
+#pragma unroll
+                for (int j = 0; j < TJ; ++j)
+                    b[j] = *reinterpret_cast<const u32x4_t *>(B + (wn * WC + j * 32 + lrow) * kRowBytes + boff);
+                if (BF16) {
+#pragma unroll
+                    for (int i = 0; i < TI; ++i)
+#pragma unroll
+                        for (int j = 0; j < TJ; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                __builtin_bit_cast(bf16x8_t, a[i]), __builtin_bit_cast(bf16x8_t, b[j]), acc[i][j], 0,
+                                0, 0);
+                } else {
+                    // Lane half h holds k = g*8 + 4h + c in component c; step c
+                    // pairs the same components of A and B, so every k meets its
+                    // own weight exactly once.
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+#pragma unroll
+                        for (int i = 0; i < TI; ++i)
+#pragma unroll
+                            for (int j = 0; j < TJ; ++j)
+                                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                                    __uint_as_float(a[i][c]), __uint_as_float(b[j][c]), acc[i][j], 0, 0, 0);
+                }
+            }
+        };
+
+        load_chunk(0);
+        store_chunk(0);
+        __syncthreads();
+        for (int q = 0; q < NQ; ++q) {
+            if (q + 1 < NQ) load_chunk(q + 1);
+            compute(q & 1);
+            if (q + 1 < NQ) store_chunk((q + 1) & 1);
+            __syncthreads();
+        }
+
+        // 32x32 accumulator layout: register r of lane l holds
+        // row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) {
+                const int col = col_base + wn * WC + j * 32 + lrow;
+                const float bc = bias ? bias[col] : 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = row_base + wm * WR + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
+                    if (row < V) out[row * C_out + col] = acc[i][j][r] + bc;
+                }
+            }
+    }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_conv_generic(const float *__restrict__ in, int C_in,
+                                                      const void *__restrict__ wv, int C_out, int T,
+                                                      const float *__restrict__ bias, float *__restrict__ out,
+                                                      const int32_t *__restrict__ nbr,
+                                                      const int32_t *__restrict__ counters) {
+    const int64_t V = counters[CNT_V];
+    const int64_t n = V * C_out;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
+        const int64_t v = e / C_out;
+        const int o = (int)(e - v * C_out);
+        float acc = bias ? bias[o] : 0.f;
+        for (int t = 0; t < T; ++t) {
+            const int u = nbr[v * T + t];
+            if (u < 0) continue;
+            const float *x = in + (int64_t)u * C_in;
+            const int64_t wbase = ((int64_t)o * T + t) * C_in;
+            for (int i = 0; i < C_in; ++i) {
+                float xv, wvv;
+                if (BF16) {
+                    xv = __uint_as_float(bf16_bits(x[i]) << 16);
+                    wvv = bf16_to_f32(reinterpret_cast<const uint16_t *>(wv)[wbase + i]);
+                } else {
+                    xv = x[i];
+                    wvv = reinterpret_cast<const float *>(wv)[wbase + i];
+                }
+                acc = fmaf(xv, wvv, acc);
+            }
+        }
+        out[e] = acc;
+    }
+}
+
+template <bool BF16, int BM, int BN, int WR, int WC>
+hipError_t launch_mfma(lattice *L, const float *in, int C_in, const void *w, int C_out, const float *bias,
+                       float *out) {
+    constexpr int NT = (BM / WR) * (BN / WC) * 64;
+    const int64_t tiles = ((L->max_vertices + BM - 1) / BM) * (C_out / BN);
+    int64_t grid = (int64_t)L->cu_count * 2;
+    if (grid > tiles) grid = tiles;
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL((k_conv_mfma<BF16, BM, BN, WR, WC>), dim3((unsigned)grid), dim3(NT), 0, L->stream, in, C_in,
+                       w, C_out, L->T, bias, out, L->nbr, L->counters);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_conv(lattice *L, const float *in, int C_in, const void *w, int C_out, lattice_dtype dt,
+                       const float *bias, float *out) {
+    const bool bf16 = dt == LATTICE_BF16;
+    const int KC = bf16 ? 64 : 32;
+    const bool aligned = ((reinterpret_cast<uintptr_t>(in) & 15) == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    if (aligned && C_in % KC == 0 && C_out % 64 == 0) {
+        if (C_out % 128 == 0)
+            return bf16 ? launch_mfma<true, 128, 128, 64, 64>(L, in, C_in, w, C_out, bias, out)
+                        : launch_mfma<false, 128, 128, 64, 64>(L, in, C_in, w, C_out, bias, out);
+        return bf16 ? launch_mfma<true, 128, 64, 32, 64>(L, in, C_in, w, C_out, bias, out)
+                    : launch_mfma<false, 128, 64, 32, 64>(L, in, C_in, w, C_out, bias, out);
+    }
+    const unsigned grid = grid_for(L->max_vertices * (int64_t)C_out, 256, L->cu_count, 8);
+    if (bf16)
+        hipLaunchKernelGGL(k_conv_generic<true>, dim3(grid), dim3(256), 0, L->stream, in, C_in, w, C_out, L->T, bias,
+                           out, L->nbr, L->counters);
+    else
+        hipLaunchKernelGGL(k_conv_generic<false>, dim3(grid), dim3(256), 0, L->stream, in, C_in, w, C_out, L->T, bias,
+                           out, L->nbr, L->counters);
+    return hipGetLastError();
+}

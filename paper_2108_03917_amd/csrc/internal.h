@@ -1,0 +1,93 @@
+// Internal declarations shared by the host API (lattice.hip) and the kernel
+// translation units (splat.hip, neighbors.hip, conv.hip, slice.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lattice.h"
+
+// Device status bits, OR-ed into counters[CNT_STATUS] by kernels.
+enum : int { ST_CAPACITY = 1, ST_RANGE = 2 };
+// Slots of the device counter array.
+enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_WORDS = 4 };
+
+// Packed 64-bit vertex key: 16 bits per coordinate c_0..c_{d-1}, each stored
+// as c + KEY_BIAS (so a field is never 0 for |c| <= KEY_MAX), and for d <= 3
+// the batch id in bits 48..63.  c_d is implied by the zero sum.  0 marks an
+// empty hash slot.
+constexpr int KEY_BIAS = 32768;
+constexpr int KEY_MAX = 32767;
+
+struct lattice_timer {
+    double ms = 0.0;    // summed elapsed time of read event pairs
+    int64_t count = 0;  // number of read event pairs
+};
+
+struct lattice {
+    int d = 0;
+    int T = 0;
+    double alpha = 0.0;
+    float sigma[LATTICE_MAX_D] = {0};
+    float factors[LATTICE_MAX_D] = {0};  // alpha / (sigma_{j-1} sqrt(j(j+1))), fp32
+    float inv_dp1 = 0.f;                 // fp32(1/(d+1))
+    int64_t max_points = 0;
+    int64_t cap = 0;          // hash slots, power of two
+    int64_t max_vertices = 0; // min((d+1) max_points, cap)
+    int device = 0;
+    hipStream_t stream = nullptr;
+
+    uint64_t *tkeys = nullptr;  // [cap]
+    int32_t *tvals = nullptr;   // [cap] vertex index of an occupied slot
+    uint64_t *vkeys = nullptr;  // [max_vertices] packed key of each vertex
+    int32_t *idx = nullptr;     // [max_points][d+1]
+    float *bary = nullptr;      // [max_points][d+1]
+    int32_t *nbr = nullptr;     // [max_vertices][T]
+    float *wsum = nullptr;      // [max_vertices] weight scratch for normalised splats
+    int32_t *counters = nullptr;  // [CNT_WORDS] device
+    int32_t *host_counters = nullptr;  // pinned [CNT_WORDS]
+
+    int64_t m = 0;
+    bool splatted = false;
+    bool nbr_valid = false;
+    bool batched = false;
+    int cu_count = 256;
+
+    int timing = 0;
+    lattice_timer timers[LATTICE_NUM_STAGES];
+    void *events = nullptr;  // per-stage event pools and pending pairs (lattice.hip)
+
+    char err[512] = {0};
+};
+
+// ---- kernel launchers (each returns the launch status) ----
+
+// splat.hip
+hipError_t launch_clear_table(lattice *L);
+hipError_t launch_insert(lattice *L, const float *pos, const int32_t *batch, int64_t m);
+hipError_t launch_clear_rows(lattice *L, float *values, int C, float *weight);
+hipError_t launch_accumulate(lattice *L, int64_t m, const float *feat, int C, float *values,
+                             float *weight);
+hipError_t launch_normalize(lattice *L, float *values, int C, const float *weight);
+hipError_t launch_export_keys(lattice *L, int32_t *keys, int32_t *batch);
+hipError_t launch_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst);
+
+// neighbors.hip
+hipError_t launch_neighbors(lattice *L);
+
+// conv.hip
+hipError_t launch_conv(lattice *L, const float *in, int C_in, const void *w, int C_out,
+                       lattice_dtype dt, const float *bias, float *out);
+
+// slice.hip
+hipError_t launch_slice(lattice *L, const float *values, int C, float *out);
+
+// Grid size for a grid-stride kernel over `work` items with `per_block`
+// items per block, capped so that the launch stays a few waves deep.
+static inline unsigned grid_for(int64_t work, int64_t per_block, int cu_count, int blocks_per_cu = 8) {
+    int64_t g = (work + per_block - 1) / per_block;
+    int64_t cap = (int64_t)cu_count * blocks_per_cu;
+    if (g > cap) g = cap;
+    if (g < 1) g = 1;
+    return (unsigned)g;
+}

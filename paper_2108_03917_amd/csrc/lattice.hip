@@ -1,0 +1,426 @@
+// Host side of the C ABI declared in include/lattice.h: argument checking,
+// ownership of the lattice's device buffers, call ordering, device status,
+// and per-stage event timing.  Every kernel is enqueued on the lattice's
+// stream; nothing here computes any part of the method on the host except
+// the fp32 elevation factors (computed once per lattice in fp64).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+void set_err(lattice *L, const char *fmt, ...) {
+    if (!L) return;
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(L->err, sizeof(L->err), fmt, ap);
+    va_end(ap);
+}
+
+lattice_status hip_fail(lattice *L, hipError_t e, const char *what) {
+    set_err(L, "%s: %s", what, hipGetErrorString(e));
+    return LATTICE_E_HIP;
+}
+
+#define HIP_TRY(L, expr)                                  \
+    do {                                                  \
+        hipError_t e_ = (expr);                           \
+        if (e_ != hipSuccess) return hip_fail(L, e_, #expr); \
+    } while (0)
+
+int64_t next_pow2(int64_t x) {
+    int64_t p = 64;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+void free_all(lattice *L) {
+    (void)hipFree(L->tkeys);
+    (void)hipFree(L->tvals);
+    (void)hipFree(L->vkeys);
+    (void)hipFree(L->idx);
+    (void)hipFree(L->bary);
+    (void)hipFree(L->nbr);
+    (void)hipFree(L->wsum);
+    (void)hipFree(L->counters);
+    if (L->host_counters) (void)hipHostFree(L->host_counters);
+}
+
+// Event pairs of one stage that have been recorded but not yet read.
+struct stage_events {
+    std::vector<hipEvent_t> pool;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
+};
+
+stage_events *events_of(lattice *L) { return reinterpret_cast<stage_events *>(L->events); }
+
+lattice_status timer_begin(lattice *L, int stage, hipEvent_t *out) {
+    *out = nullptr;
+    if (!L->timing) return LATTICE_OK;
+    stage_events *se = events_of(L) + stage;
+    hipEvent_t e;
+    if (!se->pool.empty()) {
+        e = se->pool.back();
+        se->pool.pop_back();
+    } else {
+        HIP_TRY(L, hipEventCreate(&e));
+    }
+    HIP_TRY(L, hipEventRecord(e, L->stream));
+    *out = e;
+    return LATTICE_OK;
+}
+
+lattice_status timer_end(lattice *L, int stage, hipEvent_t start) {
+    if (!L->timing || !start) return LATTICE_OK;
+    stage_events *se = events_of(L) + stage;
+    hipEvent_t e;
+    if (!se->pool.empty()) {
+        e = se->pool.back();
+        se->pool.pop_back();
+    } else {
+        HIP_TRY(L, hipEventCreate(&e));
+    }
+    HIP_TRY(L, hipEventRecord(e, L->stream));
+    se->pending.emplace_back(start, e);
+    return LATTICE_OK;
+}
+
+lattice_status check_launch(lattice *L, hipError_t e, const char *what) {
+    if (e != hipSuccess) return hip_fail(L, e, what);
+    return LATTICE_OK;
+}
+
+// Copy the first V rows (V on the device) of an int32 or fp32 table.
+__global__ void k_copy_rows(const uint32_t *__restrict__ src, uint32_t *__restrict__ dst, int64_t row_words,
+                            const int32_t *counters, int64_t fixed_rows) {
+    const int64_t rows = fixed_rows >= 0 ? fixed_rows : (int64_t)counters[CNT_V];
+    const int64_t n = rows * row_words;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+}
+
+lattice_status copy_rows(lattice *L, const void *src, void *dst, int64_t row_words, int64_t fixed_rows,
+                         int64_t bound_rows) {
+    const unsigned grid = grid_for(bound_rows * row_words, 256, L->cu_count, 4);
+    hipLaunchKernelGGL(k_copy_rows, dim3(grid), dim3(256), 0, L->stream, reinterpret_cast<const uint32_t *>(src),
+                       reinterpret_cast<uint32_t *>(dst), row_words, L->counters, fixed_rows);
+    return check_launch(L, hipGetLastError(), "copy_rows");
+}
+
+lattice_status ensure_neighbors(lattice *L) {
+    if (L->nbr_valid) return LATTICE_OK;
+    hipEvent_t t0;
+    lattice_status s = timer_begin(L, LATTICE_STAGE_NEIGHBORS, &t0);
+    if (s) return s;
+    s = check_launch(L, launch_neighbors(L), "neighbors");
+    if (s) return s;
+    s = timer_end(L, LATTICE_STAGE_NEIGHBORS, t0);
+    if (s) return s;
+    L->nbr_valid = true;
+    return LATTICE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *lattice_status_string(lattice_status s) {
+    switch (s) {
+        case LATTICE_OK: return "ok";
+        case LATTICE_E_ARG: return "invalid argument";
+        case LATTICE_E_STATE: return "call out of order";
+        case LATTICE_E_RANGE: return "key coordinate or batch id out of range";
+        case LATTICE_E_CAPACITY: return "hash table full";
+        case LATTICE_E_NOMEM: return "out of memory";
+        case LATTICE_E_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char *lattice_last_error(const lattice *L) { return L ? L->err : "null lattice"; }
+
+lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t max_points, int64_t hash_capacity,
+                              void *stream, lattice **out) {
+    if (!out) return LATTICE_E_ARG;
+    *out = nullptr;
+    if (d < 1 || d > LATTICE_MAX_D || !sigma || max_points < 1 || max_points > (int64_t)1 << 28 ||
+        hash_capacity < 0 || hash_capacity > (int64_t)1 << 30)
+        return LATTICE_E_ARG;
+    for (int j = 0; j < d; ++j)
+        if (!(sigma[j] > 0.f) || !isfinite(sigma[j])) return LATTICE_E_ARG;
+    if (!isfinite(alpha)) return LATTICE_E_ARG;
+
+    lattice *L = new (std::nothrow) lattice();
+    if (!L) return LATTICE_E_NOMEM;
+    L->d = d;
+    L->T = LATTICE_TAPS(d);
+    L->alpha = alpha > 0 ? alpha : (d + 1) * sqrt(2.0 / 3.0);
+    for (int j = 1; j <= d; ++j) {
+        L->sigma[j - 1] = sigma[j - 1];
+        L->factors[j - 1] = (float)(L->alpha / ((double)sigma[j - 1] * sqrt((double)(j * (j + 1)))));
+    }
+    L->inv_dp1 = (float)(1.0 / (d + 1));
+    L->max_points = max_points;
+    const int64_t keys_max = (int64_t)(d + 1) * max_points;
+    L->cap = next_pow2(hash_capacity > 0 ? hash_capacity : keys_max);
+    if (L->cap > (int64_t)1 << 30) {
+        delete L;
+        return LATTICE_E_ARG;
+    }
+    L->max_vertices = keys_max < L->cap ? keys_max : L->cap;
+    L->stream = reinterpret_cast<hipStream_t>(stream);
+
+    hipError_t e = hipGetDevice(&L->device);
+    if (e != hipSuccess) {
+        delete L;
+        return LATTICE_E_HIP;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, L->device) == hipSuccess && cus > 0)
+        L->cu_count = cus;
+
+    const int dp1 = d + 1;
+    bool ok = hipMalloc(&L->tkeys, L->cap * sizeof(uint64_t)) == hipSuccess &&
+              hipMalloc(&L->tvals, L->cap * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->vkeys, L->max_vertices * sizeof(uint64_t)) == hipSuccess &&
+              hipMalloc(&L->idx, max_points * dp1 * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->bary, max_points * dp1 * sizeof(float)) == hipSuccess &&
+              hipMalloc(&L->nbr, L->max_vertices * L->T * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->wsum, L->max_vertices * sizeof(float)) == hipSuccess &&
+              hipMalloc(&L->counters, CNT_WORDS * sizeof(int32_t)) == hipSuccess &&
+              hipHostMalloc(&L->host_counters, CNT_WORDS * sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
+    if (!ok) {
+        (void)hipGetLastError();
+        free_all(L);
+        delete L;
+        return LATTICE_E_NOMEM;
+    }
+    L->events = new (std::nothrow) stage_events[LATTICE_NUM_STAGES];
+    if (!L->events) {
+        free_all(L);
+        delete L;
+        return LATTICE_E_NOMEM;
+    }
+    *out = L;
+    return LATTICE_OK;
+}
+
+void lattice_destroy(lattice *L) {
+    if (!L) return;
+    (void)hipStreamSynchronize(L->stream);
+    stage_events *se = events_of(L);
+    if (se) {
+        for (int s = 0; s < LATTICE_NUM_STAGES; ++s) {
+            for (auto &pr : se[s].pending) {
+                (void)hipEventDestroy(pr.first);
+                (void)hipEventDestroy(pr.second);
+            }
+            for (auto e : se[s].pool) (void)hipEventDestroy(e);
+        }
+        delete[] se;
+    }
+    free_all(L);
+    delete L;
+}
+
+int64_t lattice_max_vertices(const lattice *L, int64_t m) {
+    if (!L || m < 0) return -1;
+    const int64_t k = (int64_t)(L->d + 1) * m;
+    return k < L->cap ? k : L->cap;
+}
+
+int64_t lattice_hash_capacity(const lattice *L) { return L ? L->cap : -1; }
+int lattice_dim(const lattice *L) { return L ? L->d : -1; }
+
+lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch, int64_t m, const float *feat, int C,
+                             int normalize, float *values, float *weight) {
+    if (!L) return LATTICE_E_ARG;
+    if (m < 0 || m > L->max_points) {
+        set_err(L, "splat: m = %lld outside [0, %lld]", (long long)m, (long long)L->max_points);
+        return LATTICE_E_ARG;
+    }
+    if (C < 0 || C > 4096 || (m > 0 && !pos) || (m > 0 && C > 0 && !feat) || (m > 0 && C > 0 && !values)) {
+        set_err(L, "splat: bad pointer or channel count (C = %d)", C);
+        return LATTICE_E_ARG;
+    }
+    if (batch && L->d == 4) {
+        set_err(L, "splat: batch ids need d <= 3 (a d = 4 key uses all 64 bits)");
+        return LATTICE_E_ARG;
+    }
+    hipEvent_t t0;
+    lattice_status s = timer_begin(L, LATTICE_STAGE_SPLAT, &t0);
+    if (s) return s;
+    float *wbuf = weight ? weight : (normalize && C > 0 ? L->wsum : nullptr);
+    if ((s = check_launch(L, launch_clear_table(L), "clear_table"))) return s;
+    if ((s = check_launch(L, launch_insert(L, pos, batch, m), "insert"))) return s;
+    if (C > 0 || wbuf)
+        if ((s = check_launch(L, launch_clear_rows(L, C > 0 ? values : nullptr, C, wbuf), "clear_rows"))) return s;
+    if ((s = check_launch(L, launch_accumulate(L, m, feat, C, values, wbuf), "accumulate"))) return s;
+    if (normalize && C > 0)
+        if ((s = check_launch(L, launch_normalize(L, values, C, wbuf), "normalize"))) return s;
+    if ((s = timer_end(L, LATTICE_STAGE_SPLAT, t0))) return s;
+    L->m = m;
+    L->splatted = true;
+    L->nbr_valid = false;
+    L->batched = batch != nullptr;
+    return LATTICE_OK;
+}
+
+lattice_status lattice_build_neighbors(lattice *L) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "build_neighbors: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    return ensure_neighbors(L);
+}
+
+lattice_status lattice_conv(lattice *L, const float *in, int C_in, const void *w, int C_out, lattice_dtype dt,
+                            const float *bias, float *out) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "conv: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    if (!in || !w || !out || C_in < 1 || C_in > 1024 || C_out < 1 || C_out > 1024 ||
+        (dt != LATTICE_F32 && dt != LATTICE_BF16) || (const void *)in == (const void *)out) {
+        set_err(L, "conv: bad argument (C_in = %d, C_out = %d, dtype = %d)", C_in, C_out, (int)dt);
+        return LATTICE_E_ARG;
+    }
+    lattice_status s = ensure_neighbors(L);
+    if (s) return s;
+    hipEvent_t t0;
+    if ((s = timer_begin(L, LATTICE_STAGE_CONV, &t0))) return s;
+    if ((s = check_launch(L, launch_conv(L, in, C_in, w, C_out, dt, bias, out), "conv"))) return s;
+    return timer_end(L, LATTICE_STAGE_CONV, t0);
+}
+
+lattice_status lattice_slice(lattice *L, const float *values, int C, float *out) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "slice: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    if (C < 1 || C > 4096 || (L->m > 0 && (!values || !out))) {
+        set_err(L, "slice: bad argument (C = %d)", C);
+        return LATTICE_E_ARG;
+    }
+    hipEvent_t t0;
+    lattice_status s = timer_begin(L, LATTICE_STAGE_SLICE, &t0);
+    if (s) return s;
+    if ((s = check_launch(L, launch_slice(L, values, C, out), "slice"))) return s;
+    return timer_end(L, LATTICE_STAGE_SLICE, t0);
+}
+
+lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst) {
+    if (!L || n < 0 || (n > 0 && (!src || !dst))) return LATTICE_E_ARG;
+    return check_launch(L, launch_to_bf16(L, src, n, dst), "to_bf16");
+}
+
+static lattice_status read_counters(lattice *L) {
+    HIP_TRY(L, hipMemcpyAsync(L->host_counters, L->counters, CNT_WORDS * sizeof(int32_t), hipMemcpyDeviceToHost,
+                              L->stream));
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    return LATTICE_OK;
+}
+
+static lattice_status device_status(lattice *L) {
+    const int st = L->host_counters[CNT_STATUS];
+    if (st & ST_CAPACITY) {
+        set_err(L, "splat: hash table of %lld slots is full", (long long)L->cap);
+        return LATTICE_E_CAPACITY;
+    }
+    if (st & ST_RANGE) {
+        set_err(L, "splat: a key coordinate exceeds +-%d or a batch id is outside [0, 65535]", KEY_MAX);
+        return LATTICE_E_RANGE;
+    }
+    return LATTICE_OK;
+}
+
+lattice_status lattice_num_vertices(lattice *L, int64_t *V) {
+    if (!L || !V) return LATTICE_E_ARG;
+    *V = 0;
+    if (!L->splatted) return LATTICE_E_STATE;
+    lattice_status s = read_counters(L);
+    if (s) return s;
+    *V = L->host_counters[CNT_V];
+    return device_status(L);
+}
+
+lattice_status lattice_get_status(lattice *L) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) return LATTICE_E_STATE;
+    lattice_status s = read_counters(L);
+    if (s) return s;
+    return device_status(L);
+}
+
+lattice_status lattice_get_keys(lattice *L, int32_t *keys, int32_t *batch) {
+    if (!L || !keys) return LATTICE_E_ARG;
+    if (!L->splatted) return LATTICE_E_STATE;
+    return check_launch(L, launch_export_keys(L, keys, batch), "export_keys");
+}
+
+lattice_status lattice_get_neighbors(lattice *L, int32_t *nbr) {
+    if (!L || !nbr) return LATTICE_E_ARG;
+    if (!L->splatted) return LATTICE_E_STATE;
+    lattice_status s = ensure_neighbors(L);
+    if (s) return s;
+    return copy_rows(L, L->nbr, nbr, L->T, -1, L->max_vertices);
+}
+
+lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) return LATTICE_E_STATE;
+    lattice_status s = LATTICE_OK;
+    if (idx && L->m > 0) s = copy_rows(L, L->idx, idx, L->d + 1, L->m, L->m);
+    if (!s && bary && L->m > 0) s = copy_rows(L, L->bary, bary, L->d + 1, L->m, L->m);
+    return s;
+}
+
+lattice_status lattice_set_timing(lattice *L, int mode) {
+    if (!L || mode < 0 || mode > 2) return LATTICE_E_ARG;
+    if (mode == 2) {
+        HIP_TRY(L, hipStreamSynchronize(L->stream));
+        stage_events *se = events_of(L);
+        for (int s = 0; s < LATTICE_NUM_STAGES; ++s) {
+            for (auto &pr : se[s].pending) {
+                se[s].pool.push_back(pr.first);
+                se[s].pool.push_back(pr.second);
+            }
+            se[s].pending.clear();
+            L->timers[s].ms = 0.0;
+            L->timers[s].count = 0;
+        }
+        return LATTICE_OK;
+    }
+    L->timing = mode;
+    return LATTICE_OK;
+}
+
+lattice_status lattice_get_timing(lattice *L, double *ms, int64_t *count) {
+    if (!L || !ms || !count) return LATTICE_E_ARG;
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    stage_events *se = events_of(L);
+    for (int s = 0; s < LATTICE_NUM_STAGES; ++s) {
+        for (auto &pr : se[s].pending) {
+            float t = 0.f;
+            HIP_TRY(L, hipEventElapsedTime(&t, pr.first, pr.second));
+            L->timers[s].ms += t;
+            L->timers[s].count += 1;
+            se[s].pool.push_back(pr.first);
+            se[s].pool.push_back(pr.second);
+        }
+        se[s].pending.clear();
+        ms[s] = L->timers[s].ms;
+        count[s] = L->timers[s].count;
+    }
+    return LATTICE_OK;
+}
+
+}  // extern "C"

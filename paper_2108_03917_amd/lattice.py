@@ -1,0 +1,288 @@
+"""Thin ctypes binding of liblattice.so (include/lattice.h).
+
+Argument marshalling only: tensors are passed to the library as raw device
+pointers together with the current HIP stream, and output tensors are
+allocated with torch.  Every step of splat, neighbours, conv and slice runs in
+the library's HIP kernels.  When the library has not been built, importing
+works but every call raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "_lib", "liblattice.so")
+
+OK, E_ARG, E_STATE, E_RANGE, E_CAPACITY, E_NOMEM, E_HIP = range(7)
+F32, BF16 = 0, 1
+STAGES = ("splat", "neighbors", "conv", "slice")
+
+EXPORTS = (
+    "lattice_create", "lattice_destroy", "lattice_max_vertices", "lattice_splat", "lattice_build_neighbors",
+    "lattice_conv",
+    "lattice_slice", "lattice_weights_to_bf16", "lattice_num_vertices", "lattice_get_status",
+    "lattice_get_keys", "lattice_get_neighbors", "lattice_get_point_simplex", "lattice_set_timing",
+    "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
+    "lattice_last_error",
+)
+
+_lib = None
+
+
+class LatticeError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[{status}] {message}")
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load liblattice.so and declare its signatures; raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
+                           "(python -m paper_2108_03917_amd._build)")
+    lib = ctypes.CDLL(path)
+    P, I64, I, D, St = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_int
+    sig = {
+        "lattice_create": (St, [I, P, D, I64, I64, P, ctypes.POINTER(P)]),
+        "lattice_destroy": (None, [P]),
+        "lattice_max_vertices": (I64, [P, I64]),
+        "lattice_splat": (St, [P, P, P, I64, P, I, I, P, P]),
+        "lattice_build_neighbors": (St, [P]),
+        "lattice_conv": (St, [P, P, I, P, I, I, P, P]),
+        "lattice_slice": (St, [P, P, I, P]),
+        "lattice_weights_to_bf16": (St, [P, P, I64, P]),
+        "lattice_num_vertices": (St, [P, ctypes.POINTER(I64)]),
+        "lattice_get_status": (St, [P]),
+        "lattice_get_keys": (St, [P, P, P]),
+        "lattice_get_neighbors": (St, [P, P]),
+        "lattice_get_point_simplex": (St, [P, P, P]),
+        "lattice_set_timing": (St, [P, I]),
+        "lattice_get_timing": (St, [P, ctypes.POINTER(D), ctypes.POINTER(I64)]),
+        "lattice_hash_capacity": (I64, [P]),
+        "lattice_dim": (I, [P]),
+        "lattice_status_string": (ctypes.c_char_p, [I]),
+        "lattice_last_error": (ctypes.c_char_p, [P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype, name: str) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+class Lattice:
+    """A sparse permutohedral lattice on the current device and stream."""
+
+    def __init__(self, d: int, sigma, alpha: float = 0.0, max_points: int = 1, hash_capacity: int = 0,
+                 stream: Optional[torch.cuda.Stream] = None):
+        self._lib = load_library()
+        sig = torch.as_tensor(sigma, dtype=torch.float32).broadcast_to((d,)).contiguous()
+        self.d = d
+        self.taps = 2 * (d + 1) + 1
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        self.device = self.stream.device
+        self._sigma = (ctypes.c_float * d)(*[float(s) for s in sig])
+        h = ctypes.c_void_p()
+        st = self._lib.lattice_create(d, self._sigma, float(alpha), int(max_points), int(hash_capacity),
+                                      ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h))
+        if st != OK:
+            raise LatticeError(st, f"lattice_create: {self._lib.lattice_status_string(st).decode()}")
+        self._h = h
+        self.max_points = int(max_points)
+        self.m = 0
+        self._V = None   # V of the current lattice once read back, else None
+
+    # -- lifetime ---------------------------------------------------------
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self._lib.lattice_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, st: int, what: str):
+        if st != OK:
+            msg = self._lib.lattice_last_error(self._h)
+            raise LatticeError(st, f"{what}: {self._lib.lattice_status_string(st).decode()}: "
+                                   f"{msg.decode() if msg else ''}")
+
+    # -- queries ----------------------------------------------------------
+    def max_vertices(self, m: Optional[int] = None) -> int:
+        return int(self._lib.lattice_max_vertices(self._h, self.m if m is None else int(m)))
+
+    @property
+    def hash_capacity(self) -> int:
+        return int(self._lib.lattice_hash_capacity(self._h))
+
+    def num_vertices(self) -> int:
+        V = ctypes.c_int64()
+        self._check(self._lib.lattice_num_vertices(self._h, ctypes.byref(V)), "num_vertices")
+        self._V = int(V.value)
+        return self._V
+
+    def _rows_needed(self) -> int:
+        """Rows a per-vertex buffer must have: V when it is known on the host,
+        else the bound max_vertices(m)."""
+        return self._V if self._V is not None else self.max_vertices(self.m)
+
+    def status(self) -> int:
+        return int(self._lib.lattice_get_status(self._h))
+
+    # -- the hot path -----------------------------------------------------
+    def splat(self, pos: torch.Tensor, feat: Optional[torch.Tensor] = None, batch: Optional[torch.Tensor] = None,
+              normalize: bool = False, values: Optional[torch.Tensor] = None,
+              weight: Optional[torch.Tensor] = None, want_weight: bool = True):
+        """Build the lattice of ``pos`` [m, d] and splat ``feat`` [m, C].
+
+        Returns (values, weight): [max_vertices, C] and [max_vertices]
+        tensors whose first V rows hold the result (V stays on the device)."""
+        _dev(pos, torch.float32, "pos")
+        m = pos.shape[0]
+        if pos.dim() != 2 or pos.shape[1] != self.d:
+            raise ValueError(f"pos must be [m, {self.d}]")
+        C = 0
+        if feat is not None:
+            _dev(feat, torch.float32, "feat")
+            if feat.dim() != 2 or feat.shape[0] != m:
+                raise ValueError("feat must be [m, C]")
+            C = feat.shape[1]
+        if batch is not None:
+            _dev(batch, torch.int32, "batch")
+            if batch.shape != (m,):
+                raise ValueError("batch must be [m]")
+        mv = int(self._lib.lattice_max_vertices(self._h, m))
+        if C > 0 and values is None:
+            values = torch.empty((mv, C), dtype=torch.float32, device=pos.device)
+        if want_weight and weight is None:
+            weight = torch.empty((max(mv, 1),), dtype=torch.float32, device=pos.device)
+        if values is not None:
+            _dev(values, torch.float32, "values")
+            if values.numel() < mv * C:
+                raise ValueError("values has fewer than max_vertices rows")
+        if weight is not None:
+            _dev(weight, torch.float32, "weight")
+            if weight.numel() < mv:
+                raise ValueError("weight has fewer than max_vertices rows")
+        st = self._lib.lattice_splat(self._h, _ptr(pos), _ptr(batch), m, _ptr(feat), C, int(bool(normalize)),
+                                     _ptr(values), _ptr(weight))
+        self.m = m
+        self._V = None
+        self._check(st, "splat")
+        return values, weight
+
+    def build_neighbors(self):
+        """Build the 1-ring neighbour table of the current lattice now."""
+        self._check(self._lib.lattice_build_neighbors(self._h), "build_neighbors")
+
+    def conv(self, x: torch.Tensor, w: torch.Tensor, dtype: str = "f32", bias: Optional[torch.Tensor] = None,
+             out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """1-ring convolution of vertex values ``x`` [>= V, C_in] with weights
+        [C_out, T, C_in] (fp32 for "f32", bf16 for "bf16")."""
+        _dev(x, torch.float32, "x")
+        if dtype == "f32":
+            _dev(w, torch.float32, "w")
+            dt = F32
+        elif dtype == "bf16":
+            _dev(w, torch.bfloat16, "w")
+            dt = BF16
+        else:
+            raise ValueError("dtype must be 'f32' or 'bf16'")
+        C_out, T, C_in = w.shape
+        if T != self.taps or x.dim() != 2 or x.shape[1] != C_in:
+            raise ValueError(f"w must be [C_out, {self.taps}, C_in] with C_in = x.shape[1]")
+        if bias is not None:
+            _dev(bias, torch.float32, "bias")
+            if bias.numel() != C_out:
+                raise ValueError("bias must have C_out elements")
+        if out is None:
+            out = torch.empty((max(x.shape[0], 1), C_out), dtype=torch.float32, device=x.device)
+        _dev(out, torch.float32, "out")
+        need = self._rows_needed()
+        if x.shape[0] < need or out.dim() != 2 or out.shape[1] != C_out or out.shape[0] < need:
+            raise ValueError(f"x and out need >= {need} rows (out [rows, {C_out}])")
+        self._check(self._lib.lattice_conv(self._h, _ptr(x), C_in, _ptr(w), C_out, dt, _ptr(bias), _ptr(out)),
+                    "conv")
+        return out
+
+    def slice(self, values: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Eq. (slice) onto the points of the last splat: [m, C]."""
+        _dev(values, torch.float32, "values")
+        C = values.shape[1]
+        if values.dim() != 2 or values.shape[0] < self._rows_needed():
+            raise ValueError(f"values needs >= {self._rows_needed()} rows")
+        if out is None:
+            out = torch.empty((self.m, C), dtype=torch.float32, device=values.device)
+        _dev(out, torch.float32, "out")
+        if out.numel() < self.m * C:
+            raise ValueError("out needs [m, C]")
+        self._check(self._lib.lattice_slice(self._h, _ptr(values), C, _ptr(out)), "slice")
+        return out
+
+    def weights_to_bf16(self, w: torch.Tensor) -> torch.Tensor:
+        """Round fp32 weights to bf16 (nearest even) with the library's kernel."""
+        _dev(w, torch.float32, "w")
+        out = torch.empty(w.shape, dtype=torch.bfloat16, device=w.device)
+        self._check(self._lib.lattice_weights_to_bf16(self._h, _ptr(w), w.numel(), _ptr(out)), "weights_to_bf16")
+        return out
+
+    # -- introspection ----------------------------------------------------
+    def keys(self, with_batch: bool = False):
+        V = self.num_vertices()
+        keys = torch.empty((max(V, 1), self.d + 1), dtype=torch.int32, device=self.device)
+        b = torch.empty((max(V, 1),), dtype=torch.int32, device=self.device) if with_batch else None
+        self._check(self._lib.lattice_get_keys(self._h, _ptr(keys), _ptr(b)), "get_keys")
+        return (keys[:V], b[:V]) if with_batch else keys[:V]
+
+    def neighbors(self) -> torch.Tensor:
+        V = self.num_vertices()
+        nbr = torch.empty((max(V, 1), self.taps), dtype=torch.int32, device=self.device)
+        self._check(self._lib.lattice_get_neighbors(self._h, _ptr(nbr)), "get_neighbors")
+        return nbr[:V]
+
+    def point_simplex(self):
+        idx = torch.empty((max(self.m, 1), self.d + 1), dtype=torch.int32, device=self.device)
+        bary = torch.empty((max(self.m, 1), self.d + 1), dtype=torch.float32, device=self.device)
+        self._check(self._lib.lattice_get_point_simplex(self._h, _ptr(idx), _ptr(bary)), "get_point_simplex")
+        return idx[:self.m], bary[:self.m]
+
+    # -- stage timing -----------------------------------------------------
+    def set_timing(self, mode: int):
+        self._check(self._lib.lattice_set_timing(self._h, int(mode)), "set_timing")
+
+    def timing(self):
+        ms = (ctypes.c_double * 4)()
+        cnt = (ctypes.c_int64 * 4)()
+        self._check(self._lib.lattice_get_timing(self._h, ms, cnt), "get_timing")
+        return {s: (float(ms[i]), int(cnt[i])) for i, s in enumerate(STAGES)}
+
+
+def exported_symbols(path: str = LIB_PATH) -> Sequence[str]:
+    """Names from EXPORTS that the built library resolves."""
+    lib = ctypes.CDLL(path)
+    return [n for n in EXPORTS if hasattr(lib, n)]

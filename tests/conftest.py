@@ -8,3 +8,10 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    # Tests load the in-tree library; build it only when nothing is built yet.
+    from paper_2108_03917_amd.lattice import LIB_PATH
+
+    if not os.path.exists(LIB_PATH):
+        from paper_2108_03917_amd import _build
+
+        _build.build()

@@ -1,0 +1,87 @@
+"""CPU-side checks of the C ABI: the library loads, exports every function
+that include/lattice.h declares, and rejects bad arguments before touching a
+device (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2108_03917_amd import lattice as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lattice.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lattice_[a-z0-9_]+)\s*\(", text)) - {"lattice_status", "lattice_dtype"})
+
+
+def test_header_declares_the_hot_path():
+    names = _declared()
+    for n in ("lattice_create", "lattice_splat", "lattice_conv", "lattice_slice", "lattice_destroy"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(B.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(B.EXPORTS) == _declared()
+
+
+def test_binding_loads():
+    lib = B.load_library()
+    assert lib.lattice_status_string(0).decode() == "ok"
+    assert lib.lattice_status_string(B.E_CAPACITY).decode() == "hash table full"
+
+
+def test_create_rejects_bad_arguments_without_device():
+    lib = B.load_library()
+    out = ctypes.c_void_p()
+    sig = (ctypes.c_float * 4)(0.1, 0.1, 0.1, 0.1)
+    bad_sig = (ctypes.c_float * 3)(0.1, -1.0, 0.1)
+    nan_sig = (ctypes.c_float * 3)(0.1, float("nan"), 0.1)
+    cases = [
+        (0, sig, 0.0, 10, 0),        # d below 1
+        (5, sig, 0.0, 10, 0),        # d above 4
+        (3, None, 0.0, 10, 0),       # no sigma
+        (3, bad_sig, 0.0, 10, 0),    # sigma <= 0
+        (3, nan_sig, 0.0, 10, 0),    # sigma NaN
+        (3, sig, 0.0, 0, 0),         # no points
+        (3, sig, 0.0, 10, -1),       # negative capacity
+        (3, sig, float("inf"), 10, 0),
+    ]
+    for d, s, a, mp, cap in cases:
+        st = lib.lattice_create(d, s, a, mp, cap, None, ctypes.byref(out))
+        assert st == B.E_ARG, (d, a, mp, cap, st)
+        assert not out.value
+    assert lib.lattice_create(3, sig, 0.0, 10, 0, None, None) == B.E_ARG
+
+
+def test_null_lattice_is_rejected():
+    lib = B.load_library()
+    assert lib.lattice_max_vertices(None, 10) == -1
+    assert lib.lattice_hash_capacity(None) == -1
+    assert lib.lattice_dim(None) == -1
+    assert lib.lattice_splat(None, None, None, 0, None, 0, 0, None, None) == B.E_ARG
+    assert lib.lattice_conv(None, None, 1, None, 1, 0, None, None) == B.E_ARG
+    assert lib.lattice_slice(None, None, 1, None) == B.E_ARG
+    assert lib.lattice_get_status(None) == B.E_ARG
+    V = ctypes.c_int64()
+    assert lib.lattice_num_vertices(None, ctypes.byref(V)) == B.E_ARG
+    lib.lattice_destroy(None)
+
+
+def test_no_device_fails_loudly():
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("a device is present")
+    lib = B.load_library()
+    out = ctypes.c_void_p()
+    sig = (ctypes.c_float * 3)(0.1, 0.1, 0.1)
+    st = lib.lattice_create(3, sig, 0.0, 10, 0, None, ctypes.byref(out))
+    assert st in (B.E_HIP, B.E_NOMEM)
+    assert not out.value

@@ -1,0 +1,95 @@
+"""GPU parity on the five full-size synthetic workloads, and the end-to-end
+chain of the benchmark's workload in the benchmark's launch configuration.
+
+Per workload: the lattice (keys, per-point vertices, weights, neighbours) is
+compared bit-exactly; splat values within 1e-5 of the sum of |terms|; each of
+the workload's convolutions is fed the oracle's splat values and compared on
+every vertex; slice is fed the oracle's conv output and compared on every
+point.
+"""
+import numpy as np
+import pytest
+import torch
+
+from datagen.clouds import make_workload
+from oracle import lattice_oracle as O
+from tests.gpu_util import REL_BF16, REL_F32, GpuLattice, assert_close_scaled, check_lattice, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("config", [1, 2, 3, 4, 5])
+def test_full_config_parity(config):
+    from paper_2108_03917_amd import Lattice
+
+    w = make_workload(config)
+    print(f"\nconfig {config}: {w.name} m={w.m} d={w.d} C={w.C}", flush=True)
+    L = Lattice(w.d, w.sigma, max_points=w.m)
+    g = GpuLattice(L, w.pos, w.feat, batch=w.batch)
+    lat = O.build(w.pos, w.sigma, batch=w.batch)
+    check_lattice(g, lat)
+    vals, wref, scale = O.splat(lat, w.feat)
+    r = assert_close_scaled(g.values(), vals, scale, REL_F32, "splat")
+    print(f"  V={lat.V} splat max rel {r:.2e}", flush=True)
+    nbr = O.neighbors(lat)
+    assert np.array_equal(g.neighbors(), nbr)
+    x32 = vals.astype(np.float32)
+    xin = g.to_gpu_order(x32)
+    for cv in w.convs:
+        wd = to_dev(cv.weight)
+        if cv.dtype == "bf16":
+            wd = L.weights_to_bf16(wd)
+        out = L.conv(xin, wd, dtype=cv.dtype)
+        got = g.from_gpu_order(out)
+        if cv.dtype == "f32":
+            ref, cscale = O.conv(x32, nbr, cv.weight)
+            r = assert_close_scaled(got, ref, cscale, REL_F32, f"conv {cv.c_in}->{cv.c_out} f32")
+        else:
+            ref, cscale = O.conv(x32, nbr, cv.weight)
+            r = assert_close_scaled(got, ref, cscale, REL_BF16, f"conv {cv.c_in}->{cv.c_out} bf16")
+            refb, cscaleb = O.conv(O.round_bf16(x32), nbr, O.round_bf16(cv.weight))
+            assert_close_scaled(got, refb, cscaleb, REL_F32, f"conv {cv.c_in}->{cv.c_out} bf16-input")
+        print(f"  conv {cv.c_in}->{cv.c_out} {cv.dtype} max rel {r:.2e}", flush=True)
+        y32 = ref.astype(np.float32)
+        sl = L.slice(g.to_gpu_order(y32)).cpu().numpy()
+        sref, sscale = O.slice_(lat, y32)
+        r = assert_close_scaled(sl, sref, sscale, REL_F32, "slice")
+        print(f"  slice C={cv.c_out} max rel {r:.2e}", flush=True)
+    L.close()
+
+
+def test_bench_workload_end_to_end():
+    """splat -> every conv of the workload -> slice exactly as bench.py
+    launches it, against the oracle chain; the tolerance is 2e-2 (bf16) or
+    3e-5 (fp32 only) of the magnitude chain |B| |W|..|W| |B^T| |f|."""
+    import bench
+
+    w = make_workload(bench.DEFAULT_CONFIG)
+    step = bench.Pipeline(w)
+    out = step.run().cpu().numpy().astype(np.float64)
+    lat = O.build(w.pos, w.sigma, batch=w.batch)
+    x, _, scale = O.splat(lat, w.feat)
+    nbr = O.neighbors(lat)
+    any_bf16 = False
+    for cv in step.convs:
+        if cv.dtype == "bf16":
+            any_bf16 = True
+            x, _ = O.conv(O.round_bf16(x.astype(np.float32)), nbr, O.round_bf16(cv.weight))
+            _, scale = O.conv(scale, nbr, np.abs(O.round_bf16(cv.weight).astype(np.float64)))
+        else:
+            x, _ = O.conv(x, nbr, cv.weight)
+            _, scale = O.conv(scale, nbr, np.abs(cv.weight.astype(np.float64)))
+    ref, _ = O.slice_(lat, x)
+    _, rscale = O.slice_(lat, scale)
+    rel = REL_BF16 if any_bf16 else 3 * REL_F32
+    r = assert_close_scaled(out, ref, rscale, rel, "end-to-end")
+    print(f"\nend-to-end {w.name}: max rel {r:.2e}", flush=True)

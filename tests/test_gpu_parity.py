@@ -1,0 +1,317 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Bar (per stage): bit-exact key set, per-point simplex vertices and
+neighbour table after canonical ordering; barycentric weights within 1e-5
+absolute; fp32 splat / conv / slice within 1e-5 of the sum of |terms| of each
+output element; the bf16 MFMA conv within 2e-2 of that sum against the
+fp32-input oracle and within 1e-5 against the oracle fed the same
+bf16-rounded inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+from datagen.clouds import conv_weight, make_workload, random_cloud, random_rows
+from oracle import lattice_oracle as O
+from tests.gpu_util import (BARY_ABS, REL_BF16, REL_F32, GpuLattice, assert_close_scaled, check_lattice, dev,
+                            to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2108_03917_amd import load_library
+
+    load_library()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _lattice(d, sigma, m, **kw):
+    from paper_2108_03917_amd import Lattice
+
+    return Lattice(d, sigma, max_points=max(m, 1), **kw)
+
+
+# ---------------------------------------------------------------------------
+# splat: keys, simplex records, values (Sec. "Permutohedral Lattice", Eq. splat)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d,m,sigma,C", [(1, 3000, 0.05, 3), (2, 5000, 0.08, 5), (3, 6000, 0.15, 64),
+                                         (3, 7001, 0.1, 1), (4, 5000, 0.3, 16)])
+def test_splat_parity(d, m, sigma, C):
+    w = random_cloud(m, d, seed=100 + d, extent=1.0, C=C)
+    L = _lattice(d, sigma, m)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, sigma)
+    check_lattice(g, lat)
+    ref, wref, scale = O.splat(lat, w.feat)
+    assert_close_scaled(g.values(), ref, scale, REL_F32, "splat values")
+    assert_close_scaled(g.weight(), wref, wref, REL_F32, "splat weight")
+
+
+def test_splat_normalized_parity():
+    w = random_cloud(4000, 3, seed=7, extent=1.0, C=6)
+    L = _lattice(3, 0.12, w.m)
+    g = GpuLattice(L, w.pos, w.feat, normalize=True)
+    lat = O.build(w.pos, 0.12)
+    ref, wref, scale = O.splat(lat, w.feat, normalize=True)
+    # one more rounding (the division) on top of the sum
+    assert_close_scaled(g.values(), ref, scale, 2 * REL_F32, "normalised splat")
+    assert_close_scaled(g.weight(), wref, wref, REL_F32, "weight")
+
+
+def test_splat_batched_parity():
+    w = random_cloud(6000, 3, seed=8, extent=1.0, C=8, n_batch=5)
+    L = _lattice(3, 0.15, w.m)
+    g = GpuLattice(L, w.pos, w.feat, batch=w.batch)
+    lat = O.build(w.pos, 0.15, batch=w.batch)
+    check_lattice(g, lat)
+    ref, _, scale = O.splat(lat, w.feat)
+    assert_close_scaled(g.values(), ref, scale, REL_F32, "batched splat")
+    nbr = g.neighbors()
+    assert np.array_equal(nbr, O.neighbors(lat))
+
+
+def test_splat_alpha_one():
+    w = random_cloud(3000, 3, seed=9, extent=1.0, C=4)
+    L = _lattice(3, 0.1, w.m, alpha=1.0)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, 0.1, alpha=1.0)
+    check_lattice(g, lat)
+
+
+def test_splat_anisotropic_sigma():
+    w = random_cloud(3000, 3, seed=10, extent=1.0, C=2)
+    sig = [0.05, 0.2, 0.11]
+    L = _lattice(3, sig, w.m)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, np.array(sig, dtype=np.float32))
+    check_lattice(g, lat)
+
+
+def test_splat_order_independent():
+    """Hash insertion order changes with point order; the canonical lattice does not."""
+    w = random_cloud(5000, 3, seed=11, extent=1.0, C=4)
+    perm = np.random.default_rng(0).permutation(w.m)
+    L = _lattice(3, 0.1, w.m)
+    a = GpuLattice(L, w.pos, w.feat)
+    va, ia = a.values(), a.idx.copy()
+    b = GpuLattice(L, w.pos[perm], w.feat[perm])
+    assert np.array_equal(a.keys, b.keys)
+    assert np.array_equal(ia[perm], b.idx)
+    lat = O.build(w.pos, 0.1)
+    _, _, scale = O.splat(lat, w.feat)
+    assert_close_scaled(b.values(), va, scale, 2 * REL_F32, "reordered splat")
+
+
+# ---------------------------------------------------------------------------
+# neighbours (Sec. "Permutohedral Lattice": +-[-1,..,d,..,-1])
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d", [1, 2, 3, 4])
+def test_neighbors_parity(d):
+    w = random_cloud(4000, d, seed=200 + d, extent=1.0, C=1)
+    L = _lattice(d, 0.2, w.m)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, 0.2)
+    assert np.array_equal(g.neighbors(), O.neighbors(lat))
+
+
+# ---------------------------------------------------------------------------
+# conv (Sec. "Common Operations": Convolving over the 1-hop ring)
+# ---------------------------------------------------------------------------
+
+CONV_CASES = [
+    # d, sigma, m, C_in, C_out, dtype, bias
+    (3, 0.05, 4096, 8, 16, "f32", False),     # generic kernel (tiny config shape)
+    (3, 0.1, 6000, 64, 64, "f32", False),     # fp32 MFMA, BN = 64
+    (3, 0.1, 6000, 32, 128, "f32", True),     # fp32 MFMA, one chunk per tap, BN = 128
+    (3, 0.1, 6000, 64, 64, "bf16", False),    # bf16 MFMA, BN = 64
+    (3, 0.1, 6000, 64, 128, "bf16", True),    # bf16 MFMA, BN = 128
+    (3, 0.1, 5000, 128, 128, "bf16", False),  # two chunks per tap
+    (3, 0.1, 5000, 64, 192, "bf16", False),   # three N tiles of 64
+    (4, 0.3, 5000, 64, 64, "bf16", False),    # T = 11
+    (3, 0.1, 3000, 96, 64, "bf16", False),    # C_in not a multiple of 64: generic
+    (2, 0.05, 3000, 5, 7, "f32", True),       # odd channels, d = 2
+    (3, 0.5, 300, 64, 64, "bf16", False),     # V below one tile
+]
+
+
+def _conv_case(d, sigma, m, C_in, C_out, dtype, bias, seed=0):
+    w = random_cloud(m, d, seed=300 + seed, extent=1.0, C=1)
+    L = _lattice(d, sigma, m)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, sigma)
+    nbr = O.neighbors(lat)
+    x = random_rows(lat.V, C_in, seed=400 + seed)
+    W = conv_weight(C_in, C_out, d, seed=500 + seed)
+    b = random_rows(1, C_out, seed=600 + seed)[0] if bias else None
+    wd = to_dev(W)
+    if dtype == "bf16":
+        wd = L.weights_to_bf16(wd)
+    out = L.conv(g.to_gpu_order(x), wd, dtype=dtype, bias=None if b is None else to_dev(b))
+    got = g.from_gpu_order(out)
+    return L, g, lat, nbr, x, W, b, got
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=[f"d{c[0]}-{c[3]}x{c[4]}-{c[5]}{'-bias' if c[6] else ''}"
+                                                  for c in CONV_CASES])
+def test_conv_parity(case):
+    d, sigma, m, C_in, C_out, dtype, bias = case
+    L, g, lat, nbr, x, W, b, got = _conv_case(*case)
+    ref, scale = O.conv(x, nbr, W, b)
+    if dtype == "f32":
+        assert_close_scaled(got, ref, scale, REL_F32, "f32 conv")
+    else:
+        assert_close_scaled(got, ref, scale, REL_BF16, "bf16 conv vs fp32 oracle")
+        xr = O.round_bf16(x).astype(np.float64)
+        Wr = O.round_bf16(W).astype(np.float64)
+        ref_b, scale_b = O.conv(xr, nbr, Wr, b)
+        assert_close_scaled(got, ref_b, scale_b, REL_F32, "bf16 conv vs bf16-input oracle")
+
+
+def test_conv_weights_to_bf16_matches_oracle_rounding():
+    L = _lattice(3, 0.1, 10)
+    W = conv_weight(64, 128, 3, seed=1)
+    got = L.weights_to_bf16(to_dev(W)).float().cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), O.round_bf16(W).view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# slice (Eq. slice)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d,C", [(3, 1), (3, 3), (3, 16), (3, 64), (3, 128), (4, 64), (2, 12)])
+def test_slice_parity(d, C):
+    w = random_cloud(5000, d, seed=700 + d, extent=1.0, C=1)
+    L = _lattice(d, 0.15, w.m)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, 0.15)
+    y = random_rows(lat.V, C, seed=800 + C)
+    got = L.slice(g.to_gpu_order(y)).cpu().numpy()
+    ref, scale = O.slice_(lat, y)
+    assert_close_scaled(got, ref, scale, REL_F32, "slice")
+
+
+def test_splat_then_slice_constant_is_constant():
+    """Normalised splat then slice of a constant field returns the constant."""
+    w = random_cloud(5000, 3, seed=12, extent=1.0, C=1)
+    L = _lattice(3, 0.1, w.m)
+    const = np.full((w.m, 4), 2.5, dtype=np.float32)
+    vals, _ = L.splat(to_dev(w.pos), to_dev(const), normalize=True)
+    out = L.slice(vals).cpu().numpy()
+    assert np.allclose(out, 2.5, rtol=4e-6, atol=0)
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+def test_empty_cloud():
+    L = _lattice(3, 0.1, 16)
+    pos = torch.zeros((0, 3), device=dev())
+    feat = torch.zeros((0, 8), device=dev())
+    vals, _ = L.splat(pos, feat)
+    assert L.num_vertices() == 0
+    W = L.weights_to_bf16(to_dev(conv_weight(64, 64, 3, seed=0)))
+    x = torch.zeros((1, 64), device=dev())
+    L.conv(x, W, dtype="bf16")
+    out = L.slice(torch.zeros((1, 8), device=dev()))
+    assert out.shape == (0, 8)
+    assert L.neighbors().shape[0] == 0
+
+
+def test_single_point_and_duplicates():
+    pos = np.array([[0.123, -0.456, 0.789]] * 37, dtype=np.float32)
+    feat = random_rows(37, 3, seed=5)
+    L = _lattice(3, 0.1, 37)
+    g = GpuLattice(L, pos, feat)
+    lat = O.build(pos, 0.1)
+    assert g.V == 4
+    check_lattice(g, lat)
+    ref, wref, scale = O.splat(lat, feat)
+    assert_close_scaled(g.values(), ref, scale, REL_F32, "duplicate splat")
+    assert_close_scaled(g.weight(), wref, wref, REL_F32, "duplicate weight")
+
+
+def test_capacity_error_is_reported():
+    from paper_2108_03917_amd import LatticeError
+    from paper_2108_03917_amd.lattice import E_CAPACITY
+
+    w = random_cloud(4000, 3, seed=13, extent=1.0, C=2)
+    L = _lattice(3, 0.05, w.m, hash_capacity=64)
+    L.splat(to_dev(w.pos), to_dev(w.feat))
+    with pytest.raises(LatticeError) as ei:
+        L.num_vertices()
+    assert ei.value.status == E_CAPACITY
+    # the lattice recovers on the next splat that fits
+    small = np.array([[0.0, 0.0, 0.0], [0.01, 0.0, 0.0]], dtype=np.float32)
+    L.splat(to_dev(small), to_dev(np.ones((2, 2), dtype=np.float32)))
+    assert L.num_vertices() >= 4
+
+
+def test_range_error_is_reported():
+    from paper_2108_03917_amd import LatticeError
+    from paper_2108_03917_amd.lattice import E_RANGE
+
+    pos = np.array([[0.0, 0.0, 0.0], [5000.0, 0.0, 0.0]], dtype=np.float32)
+    L = _lattice(3, 0.01, 2)
+    L.splat(to_dev(pos), to_dev(np.ones((2, 1), dtype=np.float32)))
+    with pytest.raises(LatticeError) as ei:
+        L.num_vertices()
+    assert ei.value.status == E_RANGE
+    pos2 = np.array([[0.0, 0.0, 0.0], [np.nan, 0.0, 0.0]], dtype=np.float32)
+    L.splat(to_dev(pos2), to_dev(np.ones((2, 1), dtype=np.float32)))
+    assert L.status() == E_RANGE
+
+
+def test_batch_id_range_error():
+    from paper_2108_03917_amd.lattice import E_RANGE
+
+    pos = np.zeros((2, 3), dtype=np.float32)
+    L = _lattice(3, 0.1, 2)
+    L.splat(to_dev(pos), to_dev(np.ones((2, 1), dtype=np.float32)),
+            batch=to_dev(np.array([0, 70000], dtype=np.int32)))
+    assert L.status() == E_RANGE
+
+
+def test_state_and_argument_errors():
+    from paper_2108_03917_amd import LatticeError
+    from paper_2108_03917_amd.lattice import E_ARG, E_STATE
+
+    L = _lattice(3, 0.1, 10)
+    x = torch.zeros((4, 64), device=dev())
+    W = torch.zeros((64, 9, 64), device=dev())
+    with pytest.raises(LatticeError) as ei:
+        L.conv(x, W)
+    assert ei.value.status == E_STATE
+    with pytest.raises(LatticeError) as ei:
+        L.slice(x)
+    assert ei.value.status == E_STATE
+    with pytest.raises(LatticeError) as ei:
+        L.splat(torch.zeros((11, 3), device=dev()), torch.zeros((11, 2), device=dev()))
+    assert ei.value.status == E_ARG
+    L4 = _lattice(4, 0.1, 10)
+    with pytest.raises(LatticeError) as ei:
+        L4.splat(torch.zeros((2, 4), device=dev()), torch.zeros((2, 1), device=dev()),
+                 batch=torch.zeros(2, dtype=torch.int32, device=dev()))
+    assert ei.value.status == E_ARG
+
+
+def test_stage_timing_records_every_stage():
+    w = random_cloud(3000, 3, seed=14, extent=1.0, C=64)
+    L = _lattice(3, 0.1, w.m)
+    L.set_timing(1)
+    vals, _ = L.splat(to_dev(w.pos), to_dev(w.feat))
+    Wb = L.weights_to_bf16(to_dev(conv_weight(64, 64, 3, seed=2)))
+    y = L.conv(vals, Wb, dtype="bf16")
+    L.slice(y)
+    t = L.timing()
+    assert all(t[s][1] == 1 and t[s][0] > 0 for s in ("splat", "neighbors", "conv", "slice")), t
+    L.set_timing(2)
+    assert all(v == (0.0, 0) for v in L.timing().values())
