@@ -58,15 +58,20 @@ class Pipeline:
         self.feat = torch.from_numpy(w.feat).to(dev)
         self.batch = None if w.batch is None else torch.from_numpy(w.batch).to(dev)
         mv = self.L.max_vertices(w.m)
-        self.values = torch.empty((mv, w.C), dtype=torch.float32, device=dev)
         self.convs = list(w.convs)
+        # A stage stores its vertex rows as bf16 exactly when the next stage is
+        # a bf16 conv (which would round them to bf16 on load anyway); the
+        # rows the slice reads stay fp32.
+        def storage(i):
+            return torch.bfloat16 if i < len(self.convs) and self.convs[i].dtype == "bf16" else torch.float32
+        self.values = torch.empty((mv, w.C), dtype=storage(0), device=dev)
         self.weights, self.outs = [], []
-        for cv in self.convs:
+        for i, cv in enumerate(self.convs):
             wd = torch.from_numpy(cv.weight).to(dev)
             if cv.dtype == "bf16":
                 wd = self.L.weights_to_bf16(wd)   # parameters: rounded once, outside the step
             self.weights.append(wd)
-            self.outs.append(torch.empty((mv, cv.c_out), dtype=torch.float32, device=dev))
+            self.outs.append(torch.empty((mv, cv.c_out), dtype=storage(i + 1), device=dev))
         c_last = self.convs[-1].c_out if self.convs else w.C
         self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
         torch.cuda.synchronize()
@@ -111,23 +116,25 @@ def algorithmic_work(w, V):
 
     splat:     read positions (4d B), batch id (4 B), features (4C B) and write
                the simplex record (vertex index + weight, 8(d+1) B) per point;
-               write the value row (4C B) and packed key (8 B) per vertex.
+               write the value row (2C or 4C B) and packed key (8 B) per vertex.
     neighbors: read the key (8 B), write T indices (4T B) per vertex.
-    conv:      read the input row (4 C_in), neighbour row (4T), write the output
-               row (4 C_out) per vertex, plus the weights once; 2 T C_in C_out
-               flops per vertex.
+    conv:      read the input row (s C_in), neighbour row (4T), write the output
+               row (s' C_out) per vertex, plus the weights once; 2 T C_in C_out
+               flops per vertex (s, s' = 2 for bf16-stored rows, else 4).
     slice:     read the record (8(d+1)) and write the output row (4C) per point,
                read each vertex row once (4C per vertex)."""
     d, m, C = w.d, w.m, w.C
     T = 2 * (d + 1) + 1
     work = {}
+    s0 = 2 if w.convs and w.convs[0].dtype == "bf16" else 4
     work["splat"] = {"bytes": m * (4 * d + 4 * C + 8 * (d + 1) + (4 if w.batch is not None else 0))
-                     + V * (4 * C + 8)}
+                     + V * (s0 * C + 8)}
     work["neighbors"] = {"bytes": V * (8 + 4 * T)}
     for i, cv in enumerate(w.convs):
         s = 2 if cv.dtype == "bf16" else 4
+        s_out = 2 if i + 1 < len(w.convs) and w.convs[i + 1].dtype == "bf16" else 4
         work[f"conv{i}_{cv.c_in}x{cv.c_out}_{cv.dtype}"] = {
-            "bytes": V * (4 * cv.c_in + 4 * T + 4 * cv.c_out) + T * cv.c_in * cv.c_out * s,
+            "bytes": V * (s * cv.c_in + 4 * T + s_out * cv.c_out) + T * cv.c_in * cv.c_out * s,
             "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": cv.dtype}
     c_last = w.convs[-1].c_out if w.convs else C
     work["slice"] = {"bytes": m * (8 * (d + 1) + 4 * c_last) + V * 4 * c_last}

@@ -121,24 +121,29 @@ int64_t lattice_max_vertices(const lattice *L, int64_t m);
  *
  * Sec. "Permutohedral Lattice" (enclosing simplex, hash map of keys) and
  * Eq. (splat):  x_v = sum_{p in J_v} b_pv f_p.  Also w_v = sum_{p in J_v} b_pv.
- *   pos        dev [m][d] fp32, row-major point positions (unscaled).
- *   batch      dev [m] int32 batch id per point in [0, 65535], or NULL.  Each
- *              id is an independent lattice sharing one table; neighbours
- *              never cross ids.  Must be NULL when d = 4.
- *   m          number of points, 0 <= m <= max_points (m = 0 gives V = 0).
- *   feat       dev [m][C] fp32 row-major features, or NULL when C = 0 (then
- *              only the lattice is built).
- *   C          feature channels, 0..4096.
- *   normalize  0: values hold the raw sum x_v;  1: values hold x_v / w_v
- *              (0 where w_v = 0).
- *   values     dev [>= lattice_max_vertices(L, m)][C] fp32 output; rows 0..V-1
- *              are written (may be NULL when C = 0 or m = 0).
- *   weight     dev [>= lattice_max_vertices(L, m)] fp32 output w_v, or NULL.
+ *   pos          dev [m][d] fp32, row-major point positions (unscaled).
+ *   batch        dev [m] int32 batch id per point in [0, 65535], or NULL.
+ *                Each id is an independent lattice sharing one table;
+ *                neighbours never cross ids.  Must be NULL when d = 4.
+ *   m            number of points, 0 <= m <= max_points (m = 0 gives V = 0).
+ *   feat         dev [m][C] fp32 row-major features, or NULL when C = 0 (then
+ *                only the lattice is built).
+ *   C            feature channels, 0..4096.
+ *   normalize    0: values hold the raw sum x_v;  1: values hold x_v / w_v
+ *                (0 where w_v = 0).
+ *   values       dev [>= lattice_max_vertices(L, m)][C] output, rows 0..V-1
+ *                written (may be NULL when C = 0 or m = 0); sums are fp32.
+ *   values_dtype storage of `values`: LATTICE_F32, or LATTICE_BF16 (each sum
+ *                rounded to nearest even; for a following bf16 conv this is
+ *                the same rounding the conv would apply to fp32 rows).
+ *   weight       dev [>= lattice_max_vertices(L, m)] fp32 output w_v, or NULL.
  * Resets the lattice: the previous vertex set, records and neighbour table
- * are discarded.  Device-side failures are reported by lattice_num_vertices.
+ * are discarded.  Vertex order is hash-slot order.  Device-side failures are
+ * reported by lattice_num_vertices.
  */
 lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch, int64_t m,
-                             const float *feat, int C, int normalize, float *values, float *weight);
+                             const float *feat, int C, int normalize, void *values,
+                             lattice_dtype values_dtype, float *weight);
 
 /*
  * lattice_build_neighbors -- build the 1-hop-ring neighbour table of the
@@ -159,33 +164,39 @@ lattice_status lattice_build_neighbors(lattice *L);
  * Sec. "Common Operations on Permutohedral Lattice" (Convolving) and the
  * caption of its figure (an unallocated neighbour contributes zero):
  *   y_v[o] = bias[o] + sum_{t < T} sum_{i < C_in} x_{nbr(v,t)}[i] * W[o][t][i].
- *   in      dev [V][C_in] fp32 vertex values (rows of the last splat's vertices).
- *   C_in    input channels, 1..1024.
- *   w       dev weights [C_out][T][C_in]: fp32 for LATTICE_F32, bf16 (raw
- *           16-bit patterns) for LATTICE_BF16 (see lattice_weights_to_bf16).
- *   C_out   output channels, 1..1024.
- *   dt      LATTICE_F32 or LATTICE_BF16.  With LATTICE_BF16 the inputs are
- *           rounded to bf16 (nearest even) as they are gathered, products are
- *           exact and sums are fp32.
- *   bias    dev [C_out] fp32 or NULL.
- *   out     dev [>= V][C_out] fp32; must not overlap `in`.
+ *   in         dev [V][C_in] vertex values (rows of the last splat's vertices).
+ *   in_dtype   storage of `in`: LATTICE_F32 or LATTICE_BF16.
+ *   C_in       input channels, 1..1024.
+ *   w          dev weights [C_out][T][C_in]: fp32 for compute LATTICE_F32,
+ *              bf16 (raw 16-bit patterns) for LATTICE_BF16 (see
+ *              lattice_weights_to_bf16).
+ *   C_out      output channels, 1..1024.
+ *   dt         compute type.  LATTICE_F32: fp32 products and sums.
+ *              LATTICE_BF16: inputs rounded to bf16 (nearest even; a no-op
+ *              for bf16-stored input), exact products, fp32 sums.
+ *   bias       dev [C_out] fp32 or NULL.
+ *   out        dev [>= V][C_out] output; must not overlap `in`.
+ *   out_dtype  storage of `out`: LATTICE_F32, or LATTICE_BF16 (fp32 result
+ *              rounded to nearest even).
  * The first conv after a splat also builds the neighbour table (2(d+1) hash
  * lookups per vertex).  Returns LATTICE_E_STATE before the first splat.
  */
-lattice_status lattice_conv(lattice *L, const float *in, int C_in, const void *w, int C_out,
-                            lattice_dtype dt, const float *bias, float *out);
+lattice_status lattice_conv(lattice *L, const void *in, lattice_dtype in_dtype, int C_in, const void *w,
+                            int C_out, lattice_dtype dt, const float *bias, void *out,
+                            lattice_dtype out_dtype);
 
 /*
  * lattice_slice -- interpolate vertex values back onto the points.
  *
  * Eq. (slice):  f_p = sum_{v in I_p} b_pv x_v, with the barycentric weights
- * of the last splat.
- *   values  dev [V][C] fp32.
- *   C       channels, 1..4096.
- *   out     dev [m][C] fp32 (m of the last splat).
+ * of the last splat; fp32 products and sums.
+ *   values        dev [V][C] vertex values.
+ *   values_dtype  storage of `values`: LATTICE_F32 or LATTICE_BF16.
+ *   C             channels, 1..4096.
+ *   out           dev [m][C] fp32 (m of the last splat).
  * Returns LATTICE_E_STATE before the first splat.
  */
-lattice_status lattice_slice(lattice *L, const float *values, int C, float *out);
+lattice_status lattice_slice(lattice *L, const void *values, lattice_dtype values_dtype, int C, float *out);
 
 /*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to

@@ -8,14 +8,19 @@
 // the operand layout the MFMA instructions consume.
 //
 // k_conv_mfma: a workgroup owns a BM x BN output tile and walks K in chunks
-// of 128 bytes per row (64 bf16 or 32 fp32 channels of one tap).  Per chunk
-// it gathers the BM neighbour rows from global memory (fp32, rounded to bf16
-// on the way for the bf16 path), stages them and the BN weight rows in LDS
-// (double buffered: the next chunk's global loads are in flight while the
-// current chunk feeds the matrix cores), and each wavefront computes a 64 x 64
-// sub-tile as 2 x 2 MFMA 32x32 blocks.  The tile loop is persistent: V lives
-// on the device, so the grid is sized for the largest lattice and every
-// workgroup reads V and strides over the tiles.
+// of 128 LDS bytes per row (64 bf16 or 32 fp32 channels of one tap).  Per
+// chunk it gathers the BM neighbour rows and the BN weight rows from global
+// memory into registers, stages them in LDS (two buffers), and each wavefront
+// computes a WR x WC sub-tile as MFMA 32x32 blocks.  The register stage is a
+// ring of P chunks: the loads of chunk q+P are issued before chunk q is
+// multiplied, so P chunks of gathers are in flight while the matrix cores
+// work.  Three input modes:
+//   CM 0  fp32 rows, fp32 MFMA (32x32x2)
+//   CM 1  fp32 rows rounded to bf16 while staging, bf16 MFMA (32x32x16)
+//   CM 2  bf16 rows (already rounded by their producer), bf16 MFMA
+// The output is fp32 or, rounded to nearest even, bf16.  The tile loop is
+// persistent: V lives on the device, so the grid is sized for the largest
+// lattice and every workgroup reads V and strides over the tiles.
 //
 // k_conv_generic: one thread per output element, for channel counts the MFMA
 // tiling does not cover (e.g. 8 -> 16).
@@ -25,12 +30,10 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
-// fp32 -> bf16 bits, round to nearest with ties to even (inputs are finite;
-// NaN stays a quiet NaN).
+// fp32 -> bf16 bits, round to nearest with ties to even (NaN stays a quiet NaN).
 __device__ __forceinline__ uint32_t bf16_bits(float f) {
     const uint32_t u = __float_as_uint(f);
     if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
@@ -44,24 +47,24 @@ constexpr int kRowBytes = 144;  // one LDS row: 128 bytes of K plus 16 bytes of 
 // Largest tap count (d = 4): the tile's neighbour rows are staged in LDS.
 constexpr int kMaxTaps = LATTICE_TAPS(LATTICE_MAX_D);
 
-// BM x BN output tile per workgroup; each wavefront owns a WR x WC sub-tile
-// made of (WR/32) x (WC/32) MFMA 32x32 blocks.
-template <bool BF16, int BM, int BN, int WR, int WC>
+template <int CM, bool OUT_BF16, int BM, int BN, int WR, int WC, int P>
 __global__ __launch_bounds__((BM / WR) * (BN / WC) * 64) void k_conv_mfma(
-    const float *__restrict__ in, int C_in, const void *__restrict__ wv, int C_out, int T,
-    const float *__restrict__ bias, float *__restrict__ out, const int32_t *__restrict__ nbr,
+    const void *__restrict__ in, int C_in, const void *__restrict__ wv, int C_out, int T,
+    const float *__restrict__ bias, void *__restrict__ out, const int32_t *__restrict__ nbr,
     const int32_t *__restrict__ counters) {
-    constexpr int WN = BN / WC;             // wavefronts along N
+    constexpr bool BF16 = CM != 0;
+    constexpr int WN = BN / WC;                   // wavefronts along N
     constexpr int NT = (BM / WR) * WN * 64;
-    constexpr int TI = WR / 32;             // MFMA blocks per wave along M
-    constexpr int TJ = WC / 32;             // MFMA blocks per wave along N
-    constexpr int KC = BF16 ? 64 : 32;      // K elements per chunk (128 bytes of LDS row)
-    constexpr int A_SEGS = KC * 4 / 16;     // 16-byte fp32 source segments per gathered row
-    constexpr int A_RPP = NT / A_SEGS;      // gathered rows per pass
+    constexpr int TI = WR / 32;                   // MFMA blocks per wave along M
+    constexpr int TJ = WC / 32;                   // MFMA blocks per wave along N
+    constexpr int KC = BF16 ? 64 : 32;            // K elements per chunk (128 bytes of LDS row)
+    constexpr int IN_ESZ = CM == 2 ? 2 : 4;       // bytes per stored input element
+    constexpr int A_SEGS = KC * IN_ESZ / 16;      // 16-byte source segments per gathered row
+    constexpr int A_RPP = NT / A_SEGS;            // gathered rows per pass
     constexpr int A_PASSES = BM / A_RPP;
-    constexpr int B_RPP = NT / 8;           // weight rows per pass (8 x 16 B per row)
+    constexpr int B_RPP = NT / 8;                 // weight rows per pass (8 x 16 B per row)
     constexpr int B_PASSES = BN / B_RPP;
-    constexpr int ESZ = BF16 ? 2 : 4;
+    constexpr int W_ESZ = BF16 ? 2 : 4;
     static_assert(A_PASSES * A_RPP == BM, "A tiling");
     static_assert(B_PASSES * B_RPP == BN, "B tiling");
 
@@ -107,50 +110,51 @@ __global__ __launch_bounds__((BM / WR) * (BN / WC) * 64) void k_conv_mfma(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-        f32x4_t areg[A_PASSES];
-        u32x4_t breg[B_PASSES];
-        bool present[A_PASSES];
+        u32x4_t areg[P][A_PASSES];
+        u32x4_t breg[P][B_PASSES];
+        bool present[P][A_PASSES];
 
-        // Branch-free gather: an absent neighbour reads row 0 (V >= 1 whenever
-        // a tile exists) and is zeroed when it is written to LDS, so all loads
-        // of a chunk are in flight together and stay in flight during compute.
-        auto load_chunk = [&](int q) {
+        // Branch-free gather into ring slot s: an absent neighbour reads row 0
+        // (V >= 1 whenever a tile exists) and is zeroed when it is written to
+        // LDS, so the loads stay in flight until then.
+        auto load_chunk = [&](int q, int s) {
             const int t = q / CPT;
             const int c0 = (q - t * CPT) * KC;
 #pragma unroll
             for (int i = 0; i < A_PASSES; ++i) {
                 const int u = nbr_s[(a_row0 + i * A_RPP) * T + t];
-                present[i] = u >= 0;
+                present[s][i] = u >= 0;
                 const int64_t row = u >= 0 ? u : 0;
-                areg[i] = *reinterpret_cast<const f32x4_t *>(in + row * C_in + c0 + a_seg * 4);
+                areg[s][i] = *reinterpret_cast<const u32x4_t *>(reinterpret_cast<const char *>(in) +
+                                                                (row * C_in + c0) * IN_ESZ + a_seg * 16);
             }
 #pragma unroll
             for (int i = 0; i < B_PASSES; ++i) {
                 const int64_t n = col_base + b_row0 + i * B_RPP;
-                const char *src = reinterpret_cast<const char *>(wv) + (n * K + (int64_t)t * C_in + c0) * ESZ + b_seg * 16;
-                breg[i] = *reinterpret_cast<const u32x4_t *>(src);
+                breg[s][i] = *reinterpret_cast<const u32x4_t *>(reinterpret_cast<const char *>(wv) +
+                                                                (n * K + (int64_t)t * C_in + c0) * W_ESZ + b_seg * 16);
             }
         };
-        auto store_chunk = [&](int buf) {
+        auto store_chunk = [&](int s, int buf) {
             char *A = lds + buf * (BM + BN) * kRowBytes;
             char *B = A + BM * kRowBytes;
 #pragma unroll
             for (int i = 0; i < A_PASSES; ++i) {
                 const int row = a_row0 + i * A_RPP;
-                const f32x4_t x = present[i] ? areg[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
-                if (BF16) {
+                const u32x4_t x = present[s][i] ? areg[s][i] : u32x4_t{0u, 0u, 0u, 0u};
+                if (CM == 1) {
                     u32x2_t pk;
-                    pk[0] = bf16_bits(x[0]) | (bf16_bits(x[1]) << 16);
-                    pk[1] = bf16_bits(x[2]) | (bf16_bits(x[3]) << 16);
+                    pk[0] = bf16_bits(__uint_as_float(x[0])) | (bf16_bits(__uint_as_float(x[1])) << 16);
+                    pk[1] = bf16_bits(__uint_as_float(x[2])) | (bf16_bits(__uint_as_float(x[3])) << 16);
                     *reinterpret_cast<u32x2_t *>(A + row * kRowBytes + a_seg * 8) = pk;
                 } else {
-                    *reinterpret_cast<f32x4_t *>(A + row * kRowBytes + a_seg * 16) = x;
+                    *reinterpret_cast<u32x4_t *>(A + row * kRowBytes + a_seg * 16) = x;
                 }
             }
 #pragma unroll
             for (int i = 0; i < B_PASSES; ++i) {
                 const int n = b_row0 + i * B_RPP;
-                *reinterpret_cast<u32x4_t *>(B + n * kRowBytes + b_seg * 16) = breg[i];
+                *reinterpret_cast<u32x4_t *>(B + n * kRowBytes + b_seg * 16) = breg[s][i];
             }
         };
         auto compute = [&](int buf) {
@@ -190,14 +194,24 @@ __global__ __launch_bounds__((BM / WR) * (BN / WC) * 64) void k_conv_mfma(
             }
         };
 
-        load_chunk(0);
-        store_chunk(0);
+        // Prologue: chunks 0..P-1 into the ring, chunk 0 into LDS buffer 0.
+#pragma unroll
+        for (int s = 0; s < P; ++s)
+            if (s < NQ) load_chunk(s, s);
+        store_chunk(0, 0);
         __syncthreads();
-        for (int q = 0; q < NQ; ++q) {
-            if (q + 1 < NQ) load_chunk(q + 1);
-            compute(q & 1);
-            if (q + 1 < NQ) store_chunk((q + 1) & 1);
-            __syncthreads();
+        for (int q0 = 0; q0 < NQ; q0 += P) {
+#pragma unroll
+            for (int s = 0; s < P; ++s) {
+                const int q = q0 + s;
+                if (q < NQ) {
+                    // ring slot s held chunk q, already in LDS: refill it with chunk q+P
+                    if (q + P < NQ) load_chunk(q + P, s);
+                    compute(q & 1);
+                    if (q + 1 < NQ) store_chunk((s + 1) % P, (q + 1) & 1);
+                    __syncthreads();
+                }
+            }
         }
 
         // 32x32 accumulator layout: register r of lane l holds
@@ -211,16 +225,23 @@ __global__ __launch_bounds__((BM / WR) * (BN / WC) * 64) void k_conv_mfma(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int64_t row = row_base + wm * WR + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
-                    if (row < V) out[row * C_out + col] = acc[i][j][r] + bc;
+                    if (row < V) {
+                        const float y = acc[i][j][r] + bc;
+                        if (OUT_BF16)
+                            reinterpret_cast<uint16_t *>(out)[row * C_out + col] = (uint16_t)bf16_bits(y);
+                        else
+                            reinterpret_cast<float *>(out)[row * C_out + col] = y;
+                    }
                 }
             }
     }
 }
 
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_conv_generic(const float *__restrict__ in, int C_in,
+// Any storage/compute combination, one thread per output element.
+template <bool IN_BF16, bool BF16, bool OUT_BF16>
+__global__ __launch_bounds__(256) void k_conv_generic(const void *__restrict__ in, int C_in,
                                                       const void *__restrict__ wv, int C_out, int T,
-                                                      const float *__restrict__ bias, float *__restrict__ out,
+                                                      const float *__restrict__ bias, void *__restrict__ out,
                                                       const int32_t *__restrict__ nbr,
                                                       const int32_t *__restrict__ counters) {
     const int64_t V = counters[CNT_V];
@@ -233,57 +254,82 @@ __global__ __launch_bounds__(256) void k_conv_generic(const float *__restrict__ 
         for (int t = 0; t < T; ++t) {
             const int u = nbr[v * T + t];
             if (u < 0) continue;
-            const float *x = in + (int64_t)u * C_in;
-            const int64_t wbase = ((int64_t)o * T + t) * C_in;
+            const int64_t xb = (int64_t)u * C_in;
+            const int64_t wb = ((int64_t)o * T + t) * C_in;
             for (int i = 0; i < C_in; ++i) {
-                float xv, wvv;
+                float xv = IN_BF16 ? bf16_to_f32(reinterpret_cast<const uint16_t *>(in)[xb + i])
+                                   : reinterpret_cast<const float *>(in)[xb + i];
+                float wvv;
                 if (BF16) {
-                    xv = __uint_as_float(bf16_bits(x[i]) << 16);
-                    wvv = bf16_to_f32(reinterpret_cast<const uint16_t *>(wv)[wbase + i]);
+                    xv = __uint_as_float(bf16_bits(xv) << 16);
+                    wvv = bf16_to_f32(reinterpret_cast<const uint16_t *>(wv)[wb + i]);
                 } else {
-                    xv = x[i];
-                    wvv = reinterpret_cast<const float *>(wv)[wbase + i];
+                    wvv = reinterpret_cast<const float *>(wv)[wb + i];
                 }
                 acc = fmaf(xv, wvv, acc);
             }
         }
-        out[e] = acc;
+        if (OUT_BF16)
+            reinterpret_cast<uint16_t *>(out)[e] = (uint16_t)bf16_bits(acc);
+        else
+            reinterpret_cast<float *>(out)[e] = acc;
     }
 }
 
-template <bool BF16, int BM, int BN, int WR, int WC>
-hipError_t launch_mfma(lattice *L, const float *in, int C_in, const void *w, int C_out, const float *bias,
-                       float *out) {
+template <int CM, bool OUT_BF16, int BM, int BN, int WR, int WC, int P>
+hipError_t launch_mfma(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias, void *out) {
     constexpr int NT = (BM / WR) * (BN / WC) * 64;
     const int64_t tiles = ((L->max_vertices + BM - 1) / BM) * (C_out / BN);
     int64_t grid = (int64_t)L->cu_count * 2;
     if (grid > tiles) grid = tiles;
     if (grid < 1) grid = 1;
-    hipLaunchKernelGGL((k_conv_mfma<BF16, BM, BN, WR, WC>), dim3((unsigned)grid), dim3(NT), 0, L->stream, in, C_in,
-                       w, C_out, L->T, bias, out, L->nbr, L->counters);
+    hipLaunchKernelGGL((k_conv_mfma<CM, OUT_BF16, BM, BN, WR, WC, P>), dim3((unsigned)grid), dim3(NT), 0, L->stream,
+                       in, C_in, w, C_out, L->T, bias, out, L->nbr, L->counters);
     return hipGetLastError();
+}
+
+template <int CM, bool OUT_BF16>
+hipError_t launch_mfma_n(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias,
+                         void *out) {
+    constexpr int P = CM == 1 ? 2 : 3;
+    if (C_out % 128 == 0) return launch_mfma<CM, OUT_BF16, 128, 128, 64, 64, P>(L, in, C_in, w, C_out, bias, out);
+    return launch_mfma<CM, OUT_BF16, 128, 64, 32, 64, P>(L, in, C_in, w, C_out, bias, out);
+}
+
+template <bool IN_BF16, bool BF16, bool OUT_BF16>
+hipError_t launch_generic(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias,
+                          void *out) {
+    const unsigned grid = grid_for(L->max_vertices * (int64_t)C_out, 256, L->cu_count, 8);
+    hipLaunchKernelGGL((k_conv_generic<IN_BF16, BF16, OUT_BF16>), dim3(grid), dim3(256), 0, L->stream, in, C_in, w,
+                       C_out, L->T, bias, out, L->nbr, L->counters);
+    return hipGetLastError();
+}
+
+template <bool OUT_BF16>
+hipError_t dispatch_out(lattice *L, const void *in, lattice_dtype in_dt, int C_in, const void *w, int C_out,
+                        lattice_dtype dt, const float *bias, void *out) {
+    const bool in_bf16 = in_dt == LATTICE_BF16;
+    const bool bf16 = dt == LATTICE_BF16;
+    const bool aligned = ((reinterpret_cast<uintptr_t>(in) & 15) == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    if (aligned && C_out % 64 == 0) {
+        if (!bf16 && !in_bf16 && C_in % 32 == 0)
+            return launch_mfma_n<0, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
+        if (bf16 && !in_bf16 && C_in % 64 == 0)
+            return launch_mfma_n<1, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
+        if (bf16 && in_bf16 && C_in % 64 == 0)
+            return launch_mfma_n<2, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
+    }
+    if (in_bf16)
+        return bf16 ? launch_generic<true, true, OUT_BF16>(L, in, C_in, w, C_out, bias, out)
+                    : launch_generic<true, false, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
+    return bf16 ? launch_generic<false, true, OUT_BF16>(L, in, C_in, w, C_out, bias, out)
+                : launch_generic<false, false, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
 }
 
 }  // namespace
 
-hipError_t launch_conv(lattice *L, const float *in, int C_in, const void *w, int C_out, lattice_dtype dt,
-                       const float *bias, float *out) {
-    const bool bf16 = dt == LATTICE_BF16;
-    const int KC = bf16 ? 64 : 32;
-    const bool aligned = ((reinterpret_cast<uintptr_t>(in) & 15) == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
-    if (aligned && C_in % KC == 0 && C_out % 64 == 0) {
-        if (C_out % 128 == 0)
-            return bf16 ? launch_mfma<true, 128, 128, 64, 64>(L, in, C_in, w, C_out, bias, out)
-                        : launch_mfma<false, 128, 128, 64, 64>(L, in, C_in, w, C_out, bias, out);
-        return bf16 ? launch_mfma<true, 128, 64, 32, 64>(L, in, C_in, w, C_out, bias, out)
-                    : launch_mfma<false, 128, 64, 32, 64>(L, in, C_in, w, C_out, bias, out);
-    }
-    const unsigned grid = grid_for(L->max_vertices * (int64_t)C_out, 256, L->cu_count, 8);
-    if (bf16)
-        hipLaunchKernelGGL(k_conv_generic<true>, dim3(grid), dim3(256), 0, L->stream, in, C_in, w, C_out, L->T, bias,
-                           out, L->nbr, L->counters);
-    else
-        hipLaunchKernelGGL(k_conv_generic<false>, dim3(grid), dim3(256), 0, L->stream, in, C_in, w, C_out, L->T, bias,
-                           out, L->nbr, L->counters);
-    return hipGetLastError();
+hipError_t launch_conv(lattice *L, const void *in, lattice_dtype in_dt, int C_in, const void *w, int C_out,
+                       lattice_dtype dt, const float *bias, void *out, lattice_dtype out_dt) {
+    return out_dt == LATTICE_BF16 ? dispatch_out<true>(L, in, in_dt, C_in, w, C_out, dt, bias, out)
+                                  : dispatch_out<false>(L, in, in_dt, C_in, w, C_out, dt, bias, out);
 }

@@ -10,7 +10,7 @@
 // Device status bits, OR-ed into counters[CNT_STATUS] by kernels.
 enum : int { ST_CAPACITY = 1, ST_RANGE = 2 };
 // Slots of the device counter array.
-enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_WORDS = 4 };
+enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_H = 3, CNT_WORDS = 4 };
 
 // Packed 64-bit vertex key: 16 bits per coordinate c_0..c_{d-1}, each stored
 // as c + KEY_BIAS (so a field is never 0 for |c| <= KEY_MAX), and for d <= 3
@@ -18,6 +18,8 @@ enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_WORDS = 4 };
 // empty hash slot.
 constexpr int KEY_BIAS = 32768;
 constexpr int KEY_MAX = 32767;
+
+struct HEntry;  // hash table entry (keys.h)
 
 struct lattice_timer {
     double ms = 0.0;    // summed elapsed time of read event pairs
@@ -37,13 +39,16 @@ struct lattice {
     int device = 0;
     hipStream_t stream = nullptr;
 
-    uint64_t *tkeys = nullptr;  // [cap]
-    int32_t *tvals = nullptr;   // [cap] vertex index of an occupied slot
+    HEntry *tab = nullptr;      // [cap] hash table {key, pair count, vertex index}
     uint64_t *vkeys = nullptr;  // [max_vertices] packed key of each vertex
-    int32_t *idx = nullptr;     // [max_points][d+1]
+    int32_t *heavy = nullptr;   // [max_vertices] vertices whose pair list is long
+    int32_t *blk = nullptr;     // [cap / 2048][2] per-block sums of the numbering scan
+    int32_t *vinfo = nullptr;   // [max_vertices][2] (offset, count) of the vertex's pair list
+    int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
+    int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
+    int32_t *list = nullptr;    // [(d+1) max_points][2] (point, weight bits) grouped by vertex
     int32_t *nbr = nullptr;     // [max_vertices][T]
-    float *wsum = nullptr;      // [max_vertices] weight scratch for normalised splats
     int32_t *counters = nullptr;  // [CNT_WORDS] device
     int32_t *host_counters = nullptr;  // pinned [CNT_WORDS]
 
@@ -65,10 +70,10 @@ struct lattice {
 // splat.hip
 hipError_t launch_clear_table(lattice *L);
 hipError_t launch_insert(lattice *L, const float *pos, const int32_t *batch, int64_t m);
-hipError_t launch_clear_rows(lattice *L, float *values, int C, float *weight);
-hipError_t launch_accumulate(lattice *L, int64_t m, const float *feat, int C, float *values,
-                             float *weight);
-hipError_t launch_normalize(lattice *L, float *values, int C, const float *weight);
+hipError_t launch_number(lattice *L);
+hipError_t launch_fill(lattice *L, int64_t m);
+hipError_t launch_gather(lattice *L, const float *feat, int C, int normalize, void *values, lattice_dtype values_dt,
+                         float *weight);
 hipError_t launch_export_keys(lattice *L, int32_t *keys, int32_t *batch);
 hipError_t launch_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst);
 
@@ -76,11 +81,11 @@ hipError_t launch_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst
 hipError_t launch_neighbors(lattice *L);
 
 // conv.hip
-hipError_t launch_conv(lattice *L, const float *in, int C_in, const void *w, int C_out,
-                       lattice_dtype dt, const float *bias, float *out);
+hipError_t launch_conv(lattice *L, const void *in, lattice_dtype in_dt, int C_in, const void *w, int C_out,
+                       lattice_dtype dt, const float *bias, void *out, lattice_dtype out_dt);
 
 // slice.hip
-hipError_t launch_slice(lattice *L, const float *values, int C, float *out);
+hipError_t launch_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, float *out);
 
 // Grid size for a grid-stride kernel over `work` items with `per_block`
 // items per block, capped so that the launch stays a few waves deep.

@@ -1,15 +1,24 @@
 // Device helpers for packed lattice keys and the open-addressing hash table.
 //
 // The hash map of Sec. "Permutohedral Lattice" (key = vertex coordinates c_v)
-// is a linear-probing table of 64-bit packed keys with a parallel array of
-// vertex indices.  A slot is claimed with a 64-bit compare-and-swap from 0
-// (empty) to the key; the claiming thread later writes the vertex index.
+// is a linear-probing table of 16-byte entries {packed key, number of
+// (point, simplex vertex) pairs that hit the key, vertex index}: one 16-byte
+// load answers a lookup, and the splat's per-vertex point lists are sized
+// from the counts.  A slot is claimed with a 64-bit compare-and-swap of the
+// key from 0 (empty) to the key.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "internal.h"
+
+struct __attribute__((aligned(16))) HEntry {
+    unsigned long long key;  // 0 = empty
+    int32_t count;           // pairs (p, k) whose vertex k has this key
+    int32_t vid;             // vertex index (written by the thread that claimed the slot)
+};
+static_assert(sizeof(HEntry) == 16, "hash entry is 16 bytes");
 
 // 64-bit finaliser of MurmurHash3 (Appleby): a bijective mixer, so distinct
 // keys never collide before the mask is applied.
@@ -46,38 +55,39 @@ __device__ __forceinline__ void unpack_key(uint64_t key, int *c, uint32_t &batch
     batch = (D <= 3) ? (uint32_t)(key >> 48) : 0u;
 }
 
-// Insert `key`; returns its slot, or -1 when every slot was probed.
-// `is_new` is true for the one thread whose CAS claimed the slot.
-__device__ __forceinline__ int hash_insert(uint64_t *tkeys, uint32_t mask, uint64_t key, bool &is_new) {
-    uint32_t h = (uint32_t)key_mix(key) & mask;
-    is_new = false;
+// Look up N keys of a table that no thread is writing, all probes of one
+// round in flight together.  `want[k]` false skips key k.  Returns the vertex
+// index per key, -1 when absent.
+template <int N>
+__device__ __forceinline__ void hash_find_all(const HEntry *__restrict__ tab, uint32_t mask, const uint64_t *key,
+                                              const bool *want, int *out) {
+    uint32_t h[N];
+    bool pending[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        h[k] = (uint32_t)key_mix(key[k]) & mask;
+        pending[k] = want[k];
+        out[k] = -1;
+    }
     for (uint32_t probe = 0; probe <= mask; ++probe) {
-        uint64_t cur = __hip_atomic_load(tkeys + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (cur == key) return (int)h;
-        if (cur == 0) {
-            unsigned long long old = atomicCAS((unsigned long long *)(tkeys + h), 0ull,
-                                               (unsigned long long)key);
-            if (old == 0ull) {
-                is_new = true;
-                return (int)h;
+        HEntry e[N];
+#pragma unroll
+        for (int k = 0; k < N; ++k)
+            if (pending[k]) e[k] = tab[h[k]];
+        bool any = false;
+#pragma unroll
+        for (int k = 0; k < N; ++k) {
+            if (!pending[k]) continue;
+            if (e[k].key == key[k]) {
+                out[k] = e[k].vid;
+                pending[k] = false;
+            } else if (e[k].key == 0ull) {
+                pending[k] = false;
+            } else {
+                h[k] = (h[k] + 1) & mask;
+                any = true;
             }
-            if (old == (unsigned long long)key) return (int)h;
         }
-        h = (h + 1) & mask;
+        if (!any) return;
     }
-    return -1;
-}
-
-// Look up `key` in a table that no thread is writing; returns the vertex
-// index or -1 when the key is absent.
-__device__ __forceinline__ int hash_find(const uint64_t *__restrict__ tkeys, const int32_t *__restrict__ tvals,
-                                         uint32_t mask, uint64_t key) {
-    uint32_t h = (uint32_t)key_mix(key) & mask;
-    for (uint32_t probe = 0; probe <= mask; ++probe) {
-        uint64_t cur = tkeys[h];
-        if (cur == key) return tvals[h];
-        if (cur == 0) return -1;
-        h = (h + 1) & mask;
-    }
-    return -1;
 }

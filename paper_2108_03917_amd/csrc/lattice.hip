@@ -40,13 +40,16 @@ int64_t next_pow2(int64_t x) {
 }
 
 void free_all(lattice *L) {
-    (void)hipFree(L->tkeys);
-    (void)hipFree(L->tvals);
+    (void)hipFree(L->tab);
     (void)hipFree(L->vkeys);
+    (void)hipFree(L->heavy);
+    (void)hipFree(L->blk);
+    (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
+    (void)hipFree(L->rank);
     (void)hipFree(L->bary);
+    (void)hipFree(L->list);
     (void)hipFree(L->nbr);
-    (void)hipFree(L->wsum);
     (void)hipFree(L->counters);
     if (L->host_counters) (void)hipHostFree(L->host_counters);
 }
@@ -185,13 +188,16 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
         L->cu_count = cus;
 
     const int dp1 = d + 1;
-    bool ok = hipMalloc(&L->tkeys, L->cap * sizeof(uint64_t)) == hipSuccess &&
-              hipMalloc(&L->tvals, L->cap * sizeof(int32_t)) == hipSuccess &&
+    bool ok = hipMalloc(&L->tab, L->cap * 16) == hipSuccess &&
               hipMalloc(&L->vkeys, L->max_vertices * sizeof(uint64_t)) == hipSuccess &&
+              hipMalloc(&L->heavy, L->max_vertices * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->blk, ((L->cap + 2047) / 2048) * 2 * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->vinfo, L->max_vertices * 2 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->idx, max_points * dp1 * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->rank, max_points * dp1 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->bary, max_points * dp1 * sizeof(float)) == hipSuccess &&
+              hipMalloc(&L->list, max_points * dp1 * 2 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->nbr, L->max_vertices * L->T * sizeof(int32_t)) == hipSuccess &&
-              hipMalloc(&L->wsum, L->max_vertices * sizeof(float)) == hipSuccess &&
               hipMalloc(&L->counters, CNT_WORDS * sizeof(int32_t)) == hipSuccess &&
               hipHostMalloc(&L->host_counters, CNT_WORDS * sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
     if (!ok) {
@@ -238,13 +244,14 @@ int64_t lattice_hash_capacity(const lattice *L) { return L ? L->cap : -1; }
 int lattice_dim(const lattice *L) { return L ? L->d : -1; }
 
 lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch, int64_t m, const float *feat, int C,
-                             int normalize, float *values, float *weight) {
+                             int normalize, void *values, lattice_dtype values_dtype, float *weight) {
     if (!L) return LATTICE_E_ARG;
     if (m < 0 || m > L->max_points) {
         set_err(L, "splat: m = %lld outside [0, %lld]", (long long)m, (long long)L->max_points);
         return LATTICE_E_ARG;
     }
-    if (C < 0 || C > 4096 || (m > 0 && !pos) || (m > 0 && C > 0 && !feat) || (m > 0 && C > 0 && !values)) {
+    if (C < 0 || C > 4096 || (m > 0 && !pos) || (m > 0 && C > 0 && !feat) || (m > 0 && C > 0 && !values) ||
+        (values_dtype != LATTICE_F32 && values_dtype != LATTICE_BF16)) {
         set_err(L, "splat: bad pointer or channel count (C = %d)", C);
         return LATTICE_E_ARG;
     }
@@ -255,14 +262,13 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
     hipEvent_t t0;
     lattice_status s = timer_begin(L, LATTICE_STAGE_SPLAT, &t0);
     if (s) return s;
-    float *wbuf = weight ? weight : (normalize && C > 0 ? L->wsum : nullptr);
     if ((s = check_launch(L, launch_clear_table(L), "clear_table"))) return s;
     if ((s = check_launch(L, launch_insert(L, pos, batch, m), "insert"))) return s;
-    if (C > 0 || wbuf)
-        if ((s = check_launch(L, launch_clear_rows(L, C > 0 ? values : nullptr, C, wbuf), "clear_rows"))) return s;
-    if ((s = check_launch(L, launch_accumulate(L, m, feat, C, values, wbuf), "accumulate"))) return s;
-    if (normalize && C > 0)
-        if ((s = check_launch(L, launch_normalize(L, values, C, wbuf), "normalize"))) return s;
+    if ((s = check_launch(L, launch_number(L), "number"))) return s;
+    if ((s = check_launch(L, launch_fill(L, m), "fill"))) return s;
+    if (C > 0 || weight)
+        if ((s = check_launch(L, launch_gather(L, feat, C, normalize, values, values_dtype, weight), "gather")))
+            return s;
     if ((s = timer_end(L, LATTICE_STAGE_SPLAT, t0))) return s;
     L->m = m;
     L->splatted = true;
@@ -280,15 +286,16 @@ lattice_status lattice_build_neighbors(lattice *L) {
     return ensure_neighbors(L);
 }
 
-lattice_status lattice_conv(lattice *L, const float *in, int C_in, const void *w, int C_out, lattice_dtype dt,
-                            const float *bias, float *out) {
+lattice_status lattice_conv(lattice *L, const void *in, lattice_dtype in_dtype, int C_in, const void *w, int C_out,
+                            lattice_dtype dt, const float *bias, void *out, lattice_dtype out_dtype) {
     if (!L) return LATTICE_E_ARG;
     if (!L->splatted) {
         set_err(L, "conv: no lattice yet (call lattice_splat first)");
         return LATTICE_E_STATE;
     }
     if (!in || !w || !out || C_in < 1 || C_in > 1024 || C_out < 1 || C_out > 1024 ||
-        (dt != LATTICE_F32 && dt != LATTICE_BF16) || (const void *)in == (const void *)out) {
+        (dt != LATTICE_F32 && dt != LATTICE_BF16) || (in_dtype != LATTICE_F32 && in_dtype != LATTICE_BF16) ||
+        (out_dtype != LATTICE_F32 && out_dtype != LATTICE_BF16) || in == out) {
         set_err(L, "conv: bad argument (C_in = %d, C_out = %d, dtype = %d)", C_in, C_out, (int)dt);
         return LATTICE_E_ARG;
     }
@@ -296,24 +303,26 @@ lattice_status lattice_conv(lattice *L, const float *in, int C_in, const void *w
     if (s) return s;
     hipEvent_t t0;
     if ((s = timer_begin(L, LATTICE_STAGE_CONV, &t0))) return s;
-    if ((s = check_launch(L, launch_conv(L, in, C_in, w, C_out, dt, bias, out), "conv"))) return s;
+    if ((s = check_launch(L, launch_conv(L, in, in_dtype, C_in, w, C_out, dt, bias, out, out_dtype), "conv")))
+        return s;
     return timer_end(L, LATTICE_STAGE_CONV, t0);
 }
 
-lattice_status lattice_slice(lattice *L, const float *values, int C, float *out) {
+lattice_status lattice_slice(lattice *L, const void *values, lattice_dtype values_dtype, int C, float *out) {
     if (!L) return LATTICE_E_ARG;
     if (!L->splatted) {
         set_err(L, "slice: no lattice yet (call lattice_splat first)");
         return LATTICE_E_STATE;
     }
-    if (C < 1 || C > 4096 || (L->m > 0 && (!values || !out))) {
+    if (C < 1 || C > 4096 || (L->m > 0 && (!values || !out)) ||
+        (values_dtype != LATTICE_F32 && values_dtype != LATTICE_BF16)) {
         set_err(L, "slice: bad argument (C = %d)", C);
         return LATTICE_E_ARG;
     }
     hipEvent_t t0;
     lattice_status s = timer_begin(L, LATTICE_STAGE_SLICE, &t0);
     if (s) return s;
-    if ((s = check_launch(L, launch_slice(L, values, C, out), "slice"))) return s;
+    if ((s = check_launch(L, launch_slice(L, values, values_dtype, C, out), "slice"))) return s;
     return timer_end(L, LATTICE_STAGE_SLICE, t0);
 }
 

@@ -14,8 +14,7 @@ constexpr int kBlock = 256;
 
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_neighbors(const uint64_t *__restrict__ vkeys,
-                                                      const uint64_t *__restrict__ tkeys,
-                                                      const int32_t *__restrict__ tvals, uint32_t mask,
+                                                      const HEntry *__restrict__ tab, uint32_t mask,
                                                       const int32_t *counters, int32_t *__restrict__ nbr) {
     constexpr int DP1 = D + 1;
     constexpr int T = 2 * DP1 + 1;
@@ -25,8 +24,9 @@ __global__ __launch_bounds__(kBlock) void k_neighbors(const uint64_t *__restrict
         int c[D];
         uint32_t b;
         unpack_key<D>(vkeys[v], c, b);
-        int32_t *row = nbr + v * T;
-        row[0] = (int32_t)v;
+        // Keys of the 2(d+1) ring vertices: index j for +n_j, DP1 + j for -n_j.
+        uint64_t key[2 * DP1];
+        bool want[2 * DP1];
 #pragma unroll
         for (int j = 0; j < DP1; ++j) {
 #pragma unroll
@@ -38,12 +38,15 @@ __global__ __launch_bounds__(kBlock) void k_neighbors(const uint64_t *__restrict
                     const int n = (i == j ? DP1 : 0) - 1;
                     q[i] = sgn == 0 ? c[i] + n : c[i] - n;
                 }
-                uint64_t key;
-                int found = -1;
-                if (pack_key<D>(q, b, key)) found = hash_find(tkeys, tvals, mask, key);
-                row[sgn == 0 ? 1 + j : DP1 + 1 + j] = found;
+                want[sgn * DP1 + j] = pack_key<D>(q, b, key[sgn * DP1 + j]);
             }
         }
+        int found[2 * DP1];
+        hash_find_all<2 * DP1>(tab, mask, key, want, found);
+        int32_t *row = nbr + v * T;
+        row[0] = (int32_t)v;
+#pragma unroll
+        for (int t = 0; t < 2 * DP1; ++t) row[1 + t] = found[t];
     }
 }
 
@@ -55,8 +58,8 @@ hipError_t launch_neighbors(lattice *L) {
     switch (L->d) {
 #define NB_CASE(DD)                                                                                              \
     case DD:                                                                                                     \
-        hipLaunchKernelGGL(k_neighbors<DD>, dim3(grid), dim3(kBlock), 0, L->stream, L->vkeys, L->tkeys, L->tvals, \
-                           mask, L->counters, L->nbr);                                                           \
+        hipLaunchKernelGGL(k_neighbors<DD>, dim3(grid), dim3(kBlock), 0, L->stream, L->vkeys, L->tab, mask,       \
+                           L->counters, L->nbr);                                                                 \
         return hipGetLastError();
         NB_CASE(1)
         NB_CASE(2)

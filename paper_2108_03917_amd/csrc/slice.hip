@@ -10,9 +10,27 @@ namespace {
 
 constexpr int kBlock = 256;
 
-template <int D, bool VEC>
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+// Load 4 consecutive channels of a vertex row stored as fp32 or bf16.
+template <bool IN_BF16>
+__device__ __forceinline__ float4 load4(const void *values, int64_t at4) {
+    if (IN_BF16) {
+        const uint2 u = reinterpret_cast<const uint2 *>(values)[at4];
+        return make_float4(bf16_lo(u.x), bf16_hi(u.x), bf16_lo(u.y), bf16_hi(u.y));
+    }
+    return reinterpret_cast<const float4 *>(values)[at4];
+}
+template <bool IN_BF16>
+__device__ __forceinline__ float load1(const void *values, int64_t at) {
+    if (IN_BF16) return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(values)[at] << 16);
+    return reinterpret_cast<const float *>(values)[at];
+}
+
+template <int D, bool VEC, bool IN_BF16>
 __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, const int32_t *__restrict__ idx,
-                                                  const float *__restrict__ bary, const float *__restrict__ values,
+                                                  const float *__restrict__ bary, const void *__restrict__ values,
                                                   float *__restrict__ out) {
     constexpr int DP1 = D + 1;
     const int G = 1 << log2G;
@@ -34,14 +52,13 @@ __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, c
         }
         if (VEC) {
             const int C4 = C >> 2;
-            const float4 *val4 = reinterpret_cast<const float4 *>(values);
             float4 *out4 = reinterpret_cast<float4 *>(out) + p * C4;
             for (int c = j; c < C4; c += G) {
                 float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
                 for (int k = 0; k < DP1; ++k) {
                     if (v[k] < 0) continue;
-                    const float4 y = val4[(int64_t)v[k] * C4 + c];
+                    const float4 y = load4<IN_BF16>(values, (int64_t)v[k] * C4 + c);
                     acc.x = fmaf(b[k], y.x, acc.x);
                     acc.y = fmaf(b[k], y.y, acc.y);
                     acc.z = fmaf(b[k], y.z, acc.z);
@@ -54,7 +71,7 @@ __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, c
                 float acc = 0.f;
 #pragma unroll
                 for (int k = 0; k < DP1; ++k)
-                    if (v[k] >= 0) acc = fmaf(b[k], values[(int64_t)v[k] * C + c], acc);
+                    if (v[k] >= 0) acc = fmaf(b[k], load1<IN_BF16>(values, (int64_t)v[k] * C + c), acc);
                 out[p * C + c] = acc;
             }
         }
@@ -63,10 +80,11 @@ __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, c
 
 }  // namespace
 
-hipError_t launch_slice(lattice *L, const float *values, int C, float *out) {
+template <bool IN_BF16>
+static hipError_t slice_typed(lattice *L, const void *values, int C, float *out) {
     const int64_t m = L->m;
     if (m == 0) return hipSuccess;
-    const bool vec = (C % 4 == 0) && ((reinterpret_cast<uintptr_t>(values) & 15) == 0) &&
+    const bool vec = (C % 4 == 0) && ((reinterpret_cast<uintptr_t>(values) & (IN_BF16 ? 7 : 15)) == 0) &&
                      ((reinterpret_cast<uintptr_t>(out) & 15) == 0);
     const int lanes_needed = vec ? C / 4 : C;
     int log2G = 0;
@@ -74,14 +92,14 @@ hipError_t launch_slice(lattice *L, const float *values, int C, float *out) {
     const int64_t ppw = 64 >> log2G;
     const int64_t waves = (m + ppw - 1) / ppw;
     const unsigned grid = grid_for(waves * 64, kBlock, L->cu_count, 16);
-#define SL_CASE(DD)                                                                                          \
-    case DD:                                                                                                 \
-        if (vec)                                                                                             \
-            hipLaunchKernelGGL((k_slice<DD, true>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, log2G, L->idx, \
-                               L->bary, values, out);                                                        \
-        else                                                                                                 \
-            hipLaunchKernelGGL((k_slice<DD, false>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, log2G,      \
-                               L->idx, L->bary, values, out);                                                \
+#define SL_CASE(DD)                                                                                              \
+    case DD:                                                                                                     \
+        if (vec)                                                                                                 \
+            hipLaunchKernelGGL((k_slice<DD, true, IN_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, log2G, \
+                               L->idx, L->bary, values, out);                                                    \
+        else                                                                                                     \
+            hipLaunchKernelGGL((k_slice<DD, false, IN_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, log2G, \
+                               L->idx, L->bary, values, out);                                                    \
         return hipGetLastError();
     switch (L->d) {
         SL_CASE(1)
@@ -92,4 +110,8 @@ hipError_t launch_slice(lattice *L, const float *values, int C, float *out) {
             return hipErrorInvalidValue;
     }
 #undef SL_CASE
+}
+
+hipError_t launch_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, float *out) {
+    return values_dt == LATTICE_BF16 ? slice_typed<true>(L, values, C, out) : slice_typed<false>(L, values, C, out);
 }

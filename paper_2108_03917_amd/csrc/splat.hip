@@ -3,20 +3,32 @@
 // barycentric accumulation of Eq. (splat).
 //
 // Kernel sequence of one lattice_splat (all on the lattice's stream):
-//   k_clear_table   empty the hash table, zero V and the status word
+//   k_clear_table   empty the hash table, zero V, the pair count and the status
 //   k_insert        one thread per point: elevate, round, rank, wrap, weights,
-//                   keys, CAS-insert; new vertices get indices from one atomic
-//                   per wavefront (prefix sum of new-key counts over the wave)
-//   k_clear_rows    zero rows 0..V-1 of values / weight (V read on device)
-//   k_accumulate    G lanes per point: map slots to vertex indices, then
-//                   fp32 atomic adds of b_k * f_p into the d+1 vertex rows
-//   k_normalize     optional x_v / w_v
+//                   keys; CAS-insert of the d+1 keys (runs of equal keys in
+//                   neighbouring lanes are inserted once), a rank for every
+//                   (point, vertex) pair from the slot's counter
+//   k_scan_*        vertex indices and pair-list ranges in hash-slot order
+//   k_fill          per pair: slot -> vertex index, (p, b_pk) into the list
+//   k_gather        per vertex: x_v = sum b_pv f_p and w_v = sum b_pv
+//                   (optionally x_v / w_v), each row written once; vertices
+//                   with many pairs by k_gather_heavy, a workgroup each
 #include "internal.h"
 #include "keys.h"
 
 namespace {
 
 constexpr int kBlock = 256;
+
+// fp32 -> bf16 bits, round to nearest with ties to even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Vertices with more pairs than this are reduced by a whole workgroup.
+constexpr int kHeavy = 64;
 
 struct ElevParams {
     float f[LATTICE_MAX_D];
@@ -44,27 +56,22 @@ __device__ __forceinline__ void elevate(const float *g, const ElevParams &ep, fl
 
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_insert(const float *__restrict__ pos, const int32_t *__restrict__ batch,
-                                                   int64_t m, ElevParams ep, uint64_t *tkeys, int32_t *tvals,
-                                                   uint32_t mask, int32_t *__restrict__ idx, float *__restrict__ bary,
-                                                   uint64_t *__restrict__ vkeys, int32_t *counters) {
+                                                   int64_t m, ElevParams ep, HEntry *tab, uint32_t mask,
+                                                   int32_t *__restrict__ idx, int32_t *__restrict__ rank_out,
+                                                   float *__restrict__ bary, int32_t *counters) {
 #pragma clang fp contract(off)
     constexpr int DP1 = D + 1;
     const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const bool active = p < m;
     const int lane = threadIdx.x & 63;
 
-    int slot[DP1];
     uint64_t key[DP1];
-    bool isnew[DP1];
     float b[DP1];
 #pragma unroll
     for (int k = 0; k < DP1; ++k) {
-        slot[k] = -1;
         key[k] = 0;
-        isnew[k] = false;
+        b[k] = 0.f;
     }
-#pragma unroll
-    for (int k = 0; k < DP1; ++k) b[k] = 0.f;
     int status = 0;
 
     if (active) {
@@ -150,39 +157,74 @@ __global__ __launch_bounds__(kBlock) void k_insert(const float *__restrict__ pos
             for (int i = 0; i < D; ++i) c[i] = r[i] + k - ((rank[i] > D - k) ? DP1 : 0);
             if (!pack_key<D>(c, bid, key[k])) status |= ST_RANGE;
         }
-        if (status == 0) {
-#pragma unroll
-            for (int k = 0; k < DP1; ++k) {
-                bool nw;
-                const int sl = hash_insert(tkeys, mask, key[k], nw);
-                slot[k] = sl;
-                isnew[k] = nw;
-                if (sl < 0) status |= ST_CAPACITY;
-            }
-        }
     }
+    const bool ok = active && status == 0;
 
-    // One atomic per wavefront hands out indices to the keys this wave created.
-    int nnew = 0;
-#pragma unroll
-    for (int k = 0; k < DP1; ++k) nnew += isnew[k] ? 1 : 0;
-    int incl = nnew;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += y;
-    }
-    const int total = __shfl(incl, 63, 64);
-    int base = 0;
-    if (lane == 63 && total > 0) base = atomicAdd(counters + CNT_V, total);
-    base = __shfl(base, 63, 64);
-    int v = base + incl - nnew;
+    // Wave-level dedup: neighbouring lanes often carry the same key (points
+    // of one simplex share its vertex of remainder k).  A run of equal keys in
+    // consecutive lanes is inserted and counted once, by its first lane.
+    const uint64_t below_mask = (2ull << lane) - 1ull;  // lanes 0..lane (wraps to all ones at lane 63)
+    uint64_t hkey[DP1];
+    int head[DP1], runlen[DP1];
 #pragma unroll
     for (int k = 0; k < DP1; ++k) {
-        if (isnew[k]) {
-            tvals[slot[k]] = v;
-            vkeys[v] = key[k];
-            ++v;
+        const uint64_t kk = ok ? key[k] : 0ull;
+        const uint64_t prev = __shfl_up(kk, 1, 64);
+        const bool is_head = (lane == 0) || (kk != prev);
+        const uint64_t heads = __ballot(is_head);
+        head[k] = 63 - __clzll((long long)(heads & below_mask));
+        const uint64_t above = lane == 63 ? 0ull : (heads >> (lane + 1));
+        runlen[k] = above ? __ffsll((long long)above) : 64 - lane;
+        hkey[k] = (is_head && kk != 0ull) ? kk : 0ull;
+    }
+
+    // Head lanes claim or find their slots; the d+1 probes of one round are in
+    // flight together.
+    int slot[DP1];
+    bool pend[DP1];
+    uint32_t h[DP1];
+#pragma unroll
+    for (int k = 0; k < DP1; ++k) {
+        slot[k] = -1;
+        pend[k] = hkey[k] != 0ull;
+        h[k] = (uint32_t)key_mix(hkey[k]) & mask;
+    }
+    for (uint32_t probe = 0; probe <= mask; ++probe) {
+        unsigned long long old[DP1];
+#pragma unroll
+        for (int k = 0; k < DP1; ++k)
+            if (pend[k]) old[k] = atomicCAS(&tab[h[k]].key, 0ull, (unsigned long long)hkey[k]);
+        bool any = false;
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            if (!pend[k]) continue;
+            if (old[k] == 0ull || old[k] == hkey[k]) {
+                slot[k] = (int)h[k];
+                pend[k] = false;
+            } else {
+                h[k] = (h[k] + 1) & mask;
+                any = true;
+            }
+        }
+        if (!any) break;
+    }
+    // Each head reserves runlen places in its vertex's point list.
+    int base[DP1];
+#pragma unroll
+    for (int k = 0; k < DP1; ++k)
+        base[k] = (hkey[k] != 0ull && slot[k] >= 0) ? atomicAdd(&tab[slot[k]].count, runlen[k]) : 0;
+    int rk[DP1];
+#pragma unroll
+    for (int k = 0; k < DP1; ++k) {
+        const int sl = __shfl(slot[k], head[k], 64);
+        const int bs = __shfl(base[k], head[k], 64);
+        if (ok) {
+            slot[k] = sl;
+            rk[k] = bs + lane - head[k];
+            if (sl < 0) status |= ST_CAPACITY;
+        } else {
+            slot[k] = -1;
+            rk[k] = -1;
         }
     }
 
@@ -190,94 +232,375 @@ __global__ __launch_bounds__(kBlock) void k_insert(const float *__restrict__ pos
 #pragma unroll
         for (int k = 0; k < DP1; ++k) {
             idx[p * DP1 + k] = slot[k];
+            rank_out[p * DP1 + k] = rk[k];
             bary[p * DP1 + k] = status ? 0.f : b[k];
         }
     }
     if (status) atomicOr(counters + CNT_STATUS, status);
 }
 
-__global__ __launch_bounds__(kBlock) void k_clear_table(uint64_t *tkeys, int64_t cap, int32_t *counters) {
+__global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap, int32_t *counters) {
     const int64_t stride = (int64_t)gridDim.x * kBlock;
-    // cap is a power of two >= 64, so the table is a whole number of 16-byte vectors.
-    uint4 *t4 = reinterpret_cast<uint4 *>(tkeys);
-    const int64_t n4 = cap / 2;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n4; i += stride) t4[i] = make_uint4(0, 0, 0, 0);
+    uint4 *t4 = reinterpret_cast<uint4 *>(tab);
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < cap; i += stride) t4[i] = make_uint4(0, 0, 0, 0);
     if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS) counters[threadIdx.x] = 0;
 }
 
-__global__ __launch_bounds__(kBlock) void k_clear_rows(float *values, int C, float *weight,
-                                                       const int32_t *counters) {
-    const int64_t V = counters[CNT_V];
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    const int64_t t0 = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (values) {
-        const int64_t n = V * C;
-        if ((reinterpret_cast<uintptr_t>(values) & 15) == 0) {
-            float4 *v4 = reinterpret_cast<float4 *>(values);
-            const int64_t n4 = n / 4;
-            for (int64_t i = t0; i < n4; i += stride) v4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-            for (int64_t i = n4 * 4 + t0; i < n; i += stride) values[i] = 0.f;
-        } else {
-            for (int64_t i = t0; i < n; i += stride) values[i] = 0.f;
-        }
+// Vertex numbering and pair-list layout, in hash-slot order, by a three-phase
+// scan over the table (no same-address atomics):
+//   k_scan_count   per block of kScanSlots slots: occupied slots and pairs
+//   k_scan_blocks  one workgroup: exclusive prefix of the block sums; V and
+//                  the pair total
+//   k_scan_assign  per block, in slot order: vertex index, list offset and
+//                  count of every occupied slot; vertices with more than
+//                  kHeavy pairs are also listed for the workgroup-per-vertex
+//                  gather.
+constexpr int kScanSlots = 2048;
+
+__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
     }
-    if (weight)
-        for (int64_t i = t0; i < V; i += stride) weight[i] = 0.f;
+    return x;
 }
 
-// G lanes per point (G a power of two, 1..64); lane j of a group handles
-// channels j, j+G, ...  The group first maps the point's d+1 hash slots to
-// vertex indices (rewriting the per-point record in place), then adds
-// b_k * f_p[c] into row v_k with fp32 atomics.
+__global__ __launch_bounds__(kBlock) void k_scan_count(const HEntry *__restrict__ tab, int64_t cap,
+                                                       int32_t *__restrict__ blk) {
+    __shared__ int red[2][kBlock / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t s0 = (int64_t)blockIdx.x * kScanSlots;
+    const int64_t s1 = s0 + kScanSlots < cap ? s0 + kScanSlots : cap;
+    int occ = 0, cnt = 0;
+    for (int64_t s = s0 + threadIdx.x; s < s1; s += kBlock) {
+        const HEntry e = tab[s];
+        occ += e.key != 0ull;
+        cnt += e.count;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        occ += __shfl_xor(occ, off, 64);
+        cnt += __shfl_xor(cnt, off, 64);
+    }
+    if (lane == 0) {
+        red[0][wave] = occ;
+        red[1][wave] = cnt;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int o = 0, c = 0;
+        for (int w = 0; w < kBlock / 64; ++w) {
+            o += red[0][w];
+            c += red[1][w];
+        }
+        blk[2 * blockIdx.x] = o;
+        blk[2 * blockIdx.x + 1] = c;
+    }
+}
+
+__global__ __launch_bounds__(1024) void k_scan_blocks(int32_t *__restrict__ blk, int nb, int32_t *counters) {
+    __shared__ int wsum[2][16];
+    __shared__ int carry[2];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (threadIdx.x == 0) carry[0] = carry[1] = 0;
+    __syncthreads();
+    for (int b0 = 0; b0 < nb; b0 += 1024) {
+        const int b = b0 + threadIdx.x;
+        const int o = b < nb ? blk[2 * b] : 0;
+        const int c = b < nb ? blk[2 * b + 1] : 0;
+        const int io = wave_incl_scan(o, lane);
+        const int ic = wave_incl_scan(c, lane);
+        if (lane == 63) {
+            wsum[0][wave] = io;
+            wsum[1][wave] = ic;
+        }
+        __syncthreads();
+        int bo = carry[0], bc = carry[1];
+        for (int w = 0; w < wave; ++w) {
+            bo += wsum[0][w];
+            bc += wsum[1][w];
+        }
+        if (b < nb) {
+            blk[2 * b] = bo + io - o;
+            blk[2 * b + 1] = bc + ic - c;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            for (int w = 0; w < 16; ++w) {
+                carry[0] += wsum[0][w];
+                carry[1] += wsum[1][w];
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        counters[CNT_V] = carry[0];
+        counters[CNT_E] = carry[1];
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_scan_assign(HEntry *__restrict__ tab, int64_t cap,
+                                                        const int32_t *__restrict__ blk,
+                                                        uint64_t *__restrict__ vkeys, int32_t *__restrict__ vinfo,
+                                                        int32_t *__restrict__ heavy, int32_t *counters) {
+    __shared__ int wsum[2][kBlock / 64];
+    __shared__ int carry[2];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t s0 = (int64_t)blockIdx.x * kScanSlots;
+    const int64_t s1 = s0 + kScanSlots < cap ? s0 + kScanSlots : cap;
+    if (threadIdx.x == 0) {
+        carry[0] = blk[2 * blockIdx.x];
+        carry[1] = blk[2 * blockIdx.x + 1];
+    }
+    __syncthreads();
+    for (int64_t r = s0; r < s1; r += kBlock) {
+        const int64_t s = r + threadIdx.x;
+        HEntry e;
+        e.key = 0ull;
+        e.count = 0;
+        if (s < s1) e = tab[s];
+        const int o = e.key != 0ull;
+        const int c = e.count;
+        const int io = wave_incl_scan(o, lane);
+        const int ic = wave_incl_scan(c, lane);
+        if (lane == 63) {
+            wsum[0][wave] = io;
+            wsum[1][wave] = ic;
+        }
+        __syncthreads();
+        int bo = carry[0], bc = carry[1];
+        for (int w = 0; w < wave; ++w) {
+            bo += wsum[0][w];
+            bc += wsum[1][w];
+        }
+        if (o) {
+            const int v = bo + io - 1;
+            tab[s].vid = v;
+            vkeys[v] = e.key;
+            vinfo[2 * v] = bc + ic - c;
+            vinfo[2 * v + 1] = c;
+            if (c > kHeavy) heavy[atomicAdd(counters + CNT_H, 1)] = v;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            for (int w = 0; w < kBlock / 64; ++w) {
+                carry[0] += wsum[0][w];
+                carry[1] += wsum[1][w];
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// Per pair (p, k): map the hash slot to the vertex index (rewriting the
+// per-point record in place) and place (p, b_pk) at its rank in the vertex's
+// pair list.
 template <int D>
-__global__ __launch_bounds__(kBlock) void k_accumulate(int64_t m, int C, int log2G, const float *__restrict__ feat,
-                                                       int32_t *idx, const float *__restrict__ bary,
-                                                       const int32_t *__restrict__ tvals, float *values,
-                                                       float *weight) {
+__global__ __launch_bounds__(kBlock) void k_fill(int64_t n, int32_t *__restrict__ idx, const int32_t *__restrict__ rank,
+                                                 const float *__restrict__ bary, const HEntry *__restrict__ tab,
+                                                 const int32_t *__restrict__ vinfo, int32_t *__restrict__ list) {
     constexpr int DP1 = D + 1;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += stride) {
+        const int s = idx[e];
+        if (s < 0) continue;
+        const int v = tab[s].vid;
+        idx[e] = v;
+        const int64_t at = (int64_t)vinfo[2 * v] + rank[e];
+        list[2 * at] = (int32_t)(e / DP1);
+        list[2 * at + 1] = __float_as_int(bary[e]);
+    }
+}
+
+// Eq. (splat), pulled per vertex: x_v = sum over the vertex's pair list of
+// b_pv f_p, and w_v = sum b_pv.  G lanes per vertex own float4 column chunks;
+// every row of `values` is written exactly once (no zero fill, no float
+// atomics).  Four list entries are fetched before their feature rows are
+// used, to keep several row gathers in flight per lane.
+// Store 4 (VEC) or 1 value of a vertex row as fp32 or bf16 (nearest even).
+template <bool OUT_BF16>
+__device__ __forceinline__ void store4(void *values, int64_t at4, float4 a) {
+    if (OUT_BF16) {
+        uint2 pk;
+        pk.x = bf16_bits(a.x) | (bf16_bits(a.y) << 16);
+        pk.y = bf16_bits(a.z) | (bf16_bits(a.w) << 16);
+        reinterpret_cast<uint2 *>(values)[at4] = pk;
+    } else {
+        reinterpret_cast<float4 *>(values)[at4] = a;
+    }
+}
+template <bool OUT_BF16>
+__device__ __forceinline__ void store1(void *values, int64_t at, float a) {
+    if (OUT_BF16)
+        reinterpret_cast<uint16_t *>(values)[at] = (uint16_t)bf16_bits(a);
+    else
+        reinterpret_cast<float *>(values)[at] = a;
+}
+
+template <bool VEC, bool OUT_BF16>
+__global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ vinfo, const int32_t *__restrict__ list,
+                                                   const float *__restrict__ feat, int C, int log2G, int normalize,
+                                                   void *__restrict__ values, float *__restrict__ weight,
+                                                   const int32_t *counters) {
+    const int64_t V = counters[CNT_V];
     const int G = 1 << log2G;
     const int lane = threadIdx.x & 63;
     const int grp = lane >> log2G;
     const int j = lane & (G - 1);
-    const int ppw = 64 >> log2G;
+    const int vpw = 64 >> log2G;
     const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
     const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
-    for (int64_t p0 = wave * ppw; p0 < m; p0 += nwaves * ppw) {
-        const int64_t p = p0 + grp;
-        if (p >= m) continue;
-        int v[DP1];
-        float b[DP1];
-#pragma unroll
-        for (int k = 0; k < DP1; ++k) {
-            const int s = idx[p * DP1 + k];
-            v[k] = s >= 0 ? tvals[s] : -1;
-            b[k] = bary[p * DP1 + k];
-        }
-        if (j == 0) {
-#pragma unroll
-            for (int k = 0; k < DP1; ++k) {
-                idx[p * DP1 + k] = v[k];
-                if (weight && v[k] >= 0) unsafeAtomicAdd(weight + v[k], b[k]);
+    const int CV = VEC ? (C >> 2) : C;  // columns in units of float4 (VEC) or float
+    for (int64_t v0 = wave * vpw; v0 < V; v0 += nwaves * vpw) {
+        const int64_t v = v0 + grp;
+        if (v >= V) continue;
+        const int off = vinfo[2 * v];
+        const int cnt = vinfo[2 * v + 1];
+        if (cnt > kHeavy) continue;  // reduced by k_gather_heavy
+        const int2 *L2 = reinterpret_cast<const int2 *>(list) + off;
+        float w = 0.f;
+        for (int e = 0; e < cnt; ++e) w += __int_as_float(L2[e].y);
+        for (int c = j; c < CV; c += G) {
+            if (VEC) {
+                const float4 *f4 = reinterpret_cast<const float4 *>(feat);
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                int e = 0;
+                for (; e + 4 <= cnt; e += 4) {
+                    const int2 q0 = L2[e], q1 = L2[e + 1], q2 = L2[e + 2], q3 = L2[e + 3];
+                    const float4 y0 = f4[(int64_t)q0.x * CV + c], y1 = f4[(int64_t)q1.x * CV + c];
+                    const float4 y2 = f4[(int64_t)q2.x * CV + c], y3 = f4[(int64_t)q3.x * CV + c];
+                    const float b0 = __int_as_float(q0.y), b1 = __int_as_float(q1.y);
+                    const float b2 = __int_as_float(q2.y), b3 = __int_as_float(q3.y);
+                    acc.x = fmaf(b0, y0.x, acc.x); acc.y = fmaf(b0, y0.y, acc.y);
+                    acc.z = fmaf(b0, y0.z, acc.z); acc.w = fmaf(b0, y0.w, acc.w);
+                    acc.x = fmaf(b1, y1.x, acc.x); acc.y = fmaf(b1, y1.y, acc.y);
+                    acc.z = fmaf(b1, y1.z, acc.z); acc.w = fmaf(b1, y1.w, acc.w);
+                    acc.x = fmaf(b2, y2.x, acc.x); acc.y = fmaf(b2, y2.y, acc.y);
+                    acc.z = fmaf(b2, y2.z, acc.z); acc.w = fmaf(b2, y2.w, acc.w);
+                    acc.x = fmaf(b3, y3.x, acc.x); acc.y = fmaf(b3, y3.y, acc.y);
+                    acc.z = fmaf(b3, y3.z, acc.z); acc.w = fmaf(b3, y3.w, acc.w);
+                }
+                for (; e < cnt; ++e) {
+                    const int2 q = L2[e];
+                    const float4 y = f4[(int64_t)q.x * CV + c];
+                    const float bq = __int_as_float(q.y);
+                    acc.x = fmaf(bq, y.x, acc.x); acc.y = fmaf(bq, y.y, acc.y);
+                    acc.z = fmaf(bq, y.z, acc.z); acc.w = fmaf(bq, y.w, acc.w);
+                }
+                if (normalize) {
+                    acc.x = w != 0.f ? acc.x / w : 0.f;
+                    acc.y = w != 0.f ? acc.y / w : 0.f;
+                    acc.z = w != 0.f ? acc.z / w : 0.f;
+                    acc.w = w != 0.f ? acc.w / w : 0.f;
+                }
+                store4<OUT_BF16>(values, v * CV + c, acc);
+            } else {
+                float acc = 0.f;
+                for (int e = 0; e < cnt; ++e) {
+                    const int2 q = L2[e];
+                    acc = fmaf(__int_as_float(q.y), feat[(int64_t)q.x * C + c], acc);
+                }
+                if (normalize) acc = w != 0.f ? acc / w : 0.f;
+                store1<OUT_BF16>(values, v * C + c, acc);
             }
         }
-        const float *fp = feat + p * C;
-        for (int c = j; c < C; c += G) {
-            const float f = fp[c];
-#pragma unroll
-            for (int k = 0; k < DP1; ++k)
-                if (v[k] >= 0) unsafeAtomicAdd(values + (int64_t)v[k] * C + c, b[k] * f);
-        }
+        if (weight && j == 0) weight[v] = w;
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_normalize(float *values, int C, const float *__restrict__ weight,
-                                                      const int32_t *counters) {
-    const int64_t V = counters[CNT_V];
-    const int64_t n = V * C;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
-        const float w = weight[i / C];
-        values[i] = (w != 0.f) ? values[i] / w : 0.f;
+// Vertices with more than kHeavy pairs (dense regions, e.g. near a LiDAR
+// sensor): one workgroup of kHeavyBlock threads per vertex.  Groups of G
+// lanes (one float4 or float column each) take the pairs in a strided order,
+// partial sums meet in LDS, and the first group writes the row.
+// Deterministic for a given list order.
+constexpr int kHeavyBlock = 1024;
+
+template <bool VEC, bool OUT_BF16>
+__global__ __launch_bounds__(kHeavyBlock) void k_gather_heavy(const int32_t *__restrict__ heavy,
+                                                              const int32_t *__restrict__ vinfo,
+                                                              const int32_t *__restrict__ list,
+                                                              const float *__restrict__ feat, int C, int log2G,
+                                                              int normalize, void *__restrict__ values,
+                                                              float *__restrict__ weight, const int32_t *counters) {
+    __shared__ float4 red[kHeavyBlock];
+    __shared__ float wred[kHeavyBlock];
+    const int nheavy = counters[CNT_H];
+    const int G = 1 << log2G;
+    const int ngroups = kHeavyBlock >> log2G;
+    const int grp = threadIdx.x >> log2G;
+    const int j = threadIdx.x & (G - 1);
+    const int CV = VEC ? (C >> 2) : C;
+    for (int h = blockIdx.x; h < nheavy; h += gridDim.x) {
+        const int v = heavy[h];
+        const int off = vinfo[2 * v];
+        const int cnt = vinfo[2 * v + 1];
+        const int2 *L2 = reinterpret_cast<const int2 *>(list) + off;
+        float w = 0.f;
+        for (int e = grp; e < cnt; e += ngroups) w += __int_as_float(L2[e].y);
+        wred[threadIdx.x] = w;
+        __syncthreads();
+        float wt = 0.f;
+        for (int g = 0; g < ngroups; ++g) wt += wred[g * G];
+        for (int c0 = 0; c0 < CV; c0 += G) {
+            const int c = c0 + j;
+            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (c < CV) {
+                if (VEC) {
+                    const float4 *f4 = reinterpret_cast<const float4 *>(feat);
+                    int e = grp;
+                    for (; e + 3 * ngroups < cnt; e += 4 * ngroups) {
+                        const int2 q0 = L2[e], q1 = L2[e + ngroups], q2 = L2[e + 2 * ngroups], q3 = L2[e + 3 * ngroups];
+                        const float4 y0 = f4[(int64_t)q0.x * CV + c], y1 = f4[(int64_t)q1.x * CV + c];
+                        const float4 y2 = f4[(int64_t)q2.x * CV + c], y3 = f4[(int64_t)q3.x * CV + c];
+                        const float b0 = __int_as_float(q0.y), b1 = __int_as_float(q1.y);
+                        const float b2 = __int_as_float(q2.y), b3 = __int_as_float(q3.y);
+                        acc.x = fmaf(b0, y0.x, acc.x); acc.y = fmaf(b0, y0.y, acc.y);
+                        acc.z = fmaf(b0, y0.z, acc.z); acc.w = fmaf(b0, y0.w, acc.w);
+                        acc.x = fmaf(b1, y1.x, acc.x); acc.y = fmaf(b1, y1.y, acc.y);
+                        acc.z = fmaf(b1, y1.z, acc.z); acc.w = fmaf(b1, y1.w, acc.w);
+                        acc.x = fmaf(b2, y2.x, acc.x); acc.y = fmaf(b2, y2.y, acc.y);
+                        acc.z = fmaf(b2, y2.z, acc.z); acc.w = fmaf(b2, y2.w, acc.w);
+                        acc.x = fmaf(b3, y3.x, acc.x); acc.y = fmaf(b3, y3.y, acc.y);
+                        acc.z = fmaf(b3, y3.z, acc.z); acc.w = fmaf(b3, y3.w, acc.w);
+                    }
+                    for (; e < cnt; e += ngroups) {
+                        const int2 q = L2[e];
+                        const float4 y = f4[(int64_t)q.x * CV + c];
+                        const float bq = __int_as_float(q.y);
+                        acc.x = fmaf(bq, y.x, acc.x); acc.y = fmaf(bq, y.y, acc.y);
+                        acc.z = fmaf(bq, y.z, acc.z); acc.w = fmaf(bq, y.w, acc.w);
+                    }
+                } else {
+                    for (int e = grp; e < cnt; e += ngroups) {
+                        const int2 q = L2[e];
+                        acc.x = fmaf(__int_as_float(q.y), feat[(int64_t)q.x * C + c], acc.x);
+                    }
+                }
+            }
+            red[threadIdx.x] = acc;
+            __syncthreads();
+            if (grp == 0 && c < CV) {
+                float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int g = 0; g < ngroups; ++g) {
+                    const float4 r = red[g * G + j];
+                    t.x += r.x; t.y += r.y; t.z += r.z; t.w += r.w;
+                }
+                if (normalize) {
+                    t.x = wt != 0.f ? t.x / wt : 0.f;
+                    t.y = wt != 0.f ? t.y / wt : 0.f;
+                    t.z = wt != 0.f ? t.z / wt : 0.f;
+                    t.w = wt != 0.f ? t.w / wt : 0.f;
+                }
+                if (VEC)
+                    store4<OUT_BF16>(values, (int64_t)v * CV + c, t);
+                else
+                    store1<OUT_BF16>(values, (int64_t)v * C + c, t.x);
+            }
+            __syncthreads();
+        }
+        if (weight && threadIdx.x == 0) weight[v] = wt;
+        __syncthreads();
     }
 }
 
@@ -305,13 +628,7 @@ __global__ __launch_bounds__(kBlock) void k_export_keys(const uint64_t *__restri
 __global__ __launch_bounds__(kBlock) void k_to_bf16(const float *__restrict__ src, int64_t n, uint16_t *__restrict__ dst) {
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
-        const uint32_t u = __float_as_uint(src[i]);
-        uint16_t h;
-        if ((u & 0x7fffffffu) > 0x7f800000u)
-            h = (uint16_t)((u >> 16) | 0x40u);
-        else
-            h = (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-        dst[i] = h;
+        dst[i] = (uint16_t)bf16_bits(src[i]);
     }
 }
 
@@ -329,8 +646,8 @@ hipError_t dispatch_d(int d, F &&f) {
 }  // namespace
 
 hipError_t launch_clear_table(lattice *L) {
-    const unsigned grid = grid_for(L->cap / 2, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tkeys, L->cap, L->counters);
+    const unsigned grid = grid_for(L->cap, kBlock, L->cu_count, 4);
+    hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->counters);
     return hipGetLastError();
 }
 
@@ -343,38 +660,73 @@ hipError_t launch_insert(lattice *L, const float *pos, const int32_t *batch, int
     const uint32_t mask = (uint32_t)(L->cap - 1);
     return dispatch_d(L->d, [&](auto dc) {
         constexpr int D = decltype(dc)::value;
-        hipLaunchKernelGGL(k_insert<D>, dim3(grid), dim3(kBlock), 0, L->stream, pos, batch, m, ep, L->tkeys,
-                           L->tvals, mask, L->idx, L->bary, L->vkeys, L->counters);
+        hipLaunchKernelGGL(k_insert<D>, dim3(grid), dim3(kBlock), 0, L->stream, pos, batch, m, ep, L->tab, mask,
+                           L->idx, L->rank, L->bary, L->counters);
         return hipGetLastError();
     });
 }
 
-hipError_t launch_clear_rows(lattice *L, float *values, int C, float *weight) {
-    const int64_t work = L->max_vertices * (int64_t)(C > 0 ? C : 1);
-    const unsigned grid = grid_for(work / 4 + 1, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(k_clear_rows, dim3(grid), dim3(kBlock), 0, L->stream, values, C, weight, L->counters);
+int64_t scan_blocks(const lattice *L) { return (L->cap + kScanSlots - 1) / kScanSlots; }
+
+hipError_t launch_number(lattice *L) {
+    const int64_t nb = scan_blocks(L);
+    hipLaunchKernelGGL(k_scan_count, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->blk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, L->stream, L->blk, (int)nb, L->counters);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_scan_assign, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->blk,
+                       L->vkeys, L->vinfo, L->heavy, L->counters);
     return hipGetLastError();
 }
 
-hipError_t launch_accumulate(lattice *L, int64_t m, const float *feat, int C, float *values, float *weight) {
+hipError_t launch_fill(lattice *L, int64_t m) {
     if (m == 0) return hipSuccess;
-    int log2G = 0;
-    while ((1 << log2G) < C && log2G < 6) ++log2G;
-    const int64_t ppw = 64 >> log2G;
-    const int64_t waves = (m + ppw - 1) / ppw;
-    const unsigned grid = grid_for(waves * 64, kBlock, L->cu_count, 16);
+    const int64_t n = m * (L->d + 1);
+    const unsigned grid = grid_for(n, kBlock, L->cu_count, 16);
     return dispatch_d(L->d, [&](auto dc) {
         constexpr int D = decltype(dc)::value;
-        hipLaunchKernelGGL(k_accumulate<D>, dim3(grid), dim3(kBlock), 0, L->stream, m, C, log2G, feat, L->idx,
-                           L->bary, L->tvals, values, weight);
+        hipLaunchKernelGGL(k_fill<D>, dim3(grid), dim3(kBlock), 0, L->stream, n, L->idx, L->rank, L->bary, L->tab,
+                           L->vinfo, L->list);
         return hipGetLastError();
     });
 }
 
-hipError_t launch_normalize(lattice *L, float *values, int C, const float *weight) {
-    const unsigned grid = grid_for(L->max_vertices * (int64_t)C, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(k_normalize, dim3(grid), dim3(kBlock), 0, L->stream, values, C, weight, L->counters);
+template <bool OUT_BF16>
+static hipError_t gather_typed(lattice *L, const float *feat, int C, int normalize, void *values, float *weight) {
+    const bool vec = C > 0 && (C % 4 == 0) && ((reinterpret_cast<uintptr_t>(feat) & 15) == 0) &&
+                     ((reinterpret_cast<uintptr_t>(values) & (OUT_BF16 ? 7 : 15)) == 0);
+    const int lanes = vec ? C / 4 : (C > 0 ? C : 1);
+    int log2G = 0;
+    while ((1 << log2G) < lanes && log2G < 6) ++log2G;
+    const int64_t vpw = 64 >> log2G;
+    const int64_t waves = (L->max_vertices + vpw - 1) / vpw;
+    const unsigned grid = grid_for(waves * 64, kBlock, L->cu_count, 16);
+    if (vec)
+        hipLaunchKernelGGL((k_gather<true, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list, feat,
+                           C, log2G, normalize, values, weight, L->counters);
+    else
+        hipLaunchKernelGGL((k_gather<false, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list, feat,
+                           C, log2G, normalize, values, weight, L->counters);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // heavy vertices: G = lanes per column group, at most 64, so that a
+    // workgroup has at least 16 groups splitting each long pair list
+    const unsigned hgrid = (unsigned)(L->cu_count * 2);
+    if (vec)
+        hipLaunchKernelGGL((k_gather_heavy<true, OUT_BF16>), dim3(hgrid), dim3(kHeavyBlock), 0, L->stream, L->heavy,
+                           L->vinfo, L->list, feat, C, log2G, normalize, values, weight, L->counters);
+    else
+        hipLaunchKernelGGL((k_gather_heavy<false, OUT_BF16>), dim3(hgrid), dim3(kHeavyBlock), 0, L->stream, L->heavy,
+                           L->vinfo, L->list, feat, C, log2G, normalize, values, weight, L->counters);
     return hipGetLastError();
+}
+
+hipError_t launch_gather(lattice *L, const float *feat, int C, int normalize, void *values, lattice_dtype values_dt,
+                         float *weight) {
+    return values_dt == LATTICE_BF16 ? gather_typed<true>(L, feat, C, normalize, values, weight)
+                                     : gather_typed<false>(L, feat, C, normalize, values, weight);
 }
 
 hipError_t launch_export_keys(lattice *L, int32_t *keys, int32_t *batch) {

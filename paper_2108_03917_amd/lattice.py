@@ -53,10 +53,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_create": (St, [I, P, D, I64, I64, P, ctypes.POINTER(P)]),
         "lattice_destroy": (None, [P]),
         "lattice_max_vertices": (I64, [P, I64]),
-        "lattice_splat": (St, [P, P, P, I64, P, I, I, P, P]),
+        "lattice_splat": (St, [P, P, P, I64, P, I, I, P, I, P]),
         "lattice_build_neighbors": (St, [P]),
-        "lattice_conv": (St, [P, P, I, P, I, I, P, P]),
-        "lattice_slice": (St, [P, P, I, P]),
+        "lattice_conv": (St, [P, P, I, I, P, I, I, P, P, I]),
+        "lattice_slice": (St, [P, P, I, I, P]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
         "lattice_num_vertices": (St, [P, ctypes.POINTER(I64)]),
         "lattice_get_status": (St, [P]),
@@ -82,11 +82,16 @@ def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
 
-def _dev(t: torch.Tensor, dtype: torch.dtype, name: str) -> torch.Tensor:
+_STORAGE = {torch.float32: F32, torch.bfloat16: BF16}
+_TORCH = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def _dev(t: torch.Tensor, dtype, name: str) -> torch.Tensor:
     if not t.is_cuda:
         raise ValueError(f"{name} must be a device tensor")
-    if t.dtype != dtype:
-        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    allowed = dtype if isinstance(dtype, tuple) else (dtype,)
+    if t.dtype not in allowed:
+        raise ValueError(f"{name} must be {' or '.join(map(str, allowed))}, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return t
@@ -157,11 +162,12 @@ class Lattice:
     # -- the hot path -----------------------------------------------------
     def splat(self, pos: torch.Tensor, feat: Optional[torch.Tensor] = None, batch: Optional[torch.Tensor] = None,
               normalize: bool = False, values: Optional[torch.Tensor] = None,
-              weight: Optional[torch.Tensor] = None, want_weight: bool = True):
+              weight: Optional[torch.Tensor] = None, want_weight: bool = True, values_dtype: str = "f32"):
         """Build the lattice of ``pos`` [m, d] and splat ``feat`` [m, C].
 
         Returns (values, weight): [max_vertices, C] and [max_vertices]
-        tensors whose first V rows hold the result (V stays on the device)."""
+        tensors whose first V rows hold the result (V stays on the device).
+        ``values_dtype`` "bf16" stores the fp32 sums rounded to bf16."""
         _dev(pos, torch.float32, "pos")
         m = pos.shape[0]
         if pos.dim() != 2 or pos.shape[1] != self.d:
@@ -178,11 +184,13 @@ class Lattice:
                 raise ValueError("batch must be [m]")
         mv = int(self._lib.lattice_max_vertices(self._h, m))
         if C > 0 and values is None:
-            values = torch.empty((mv, C), dtype=torch.float32, device=pos.device)
+            values = torch.empty((mv, C), dtype=_TORCH[values_dtype], device=pos.device)
         if want_weight and weight is None:
             weight = torch.empty((max(mv, 1),), dtype=torch.float32, device=pos.device)
+        vdt = F32
         if values is not None:
-            _dev(values, torch.float32, "values")
+            _dev(values, (torch.float32, torch.bfloat16), "values")
+            vdt = _STORAGE[values.dtype]
             if values.numel() < mv * C:
                 raise ValueError("values has fewer than max_vertices rows")
         if weight is not None:
@@ -190,7 +198,7 @@ class Lattice:
             if weight.numel() < mv:
                 raise ValueError("weight has fewer than max_vertices rows")
         st = self._lib.lattice_splat(self._h, _ptr(pos), _ptr(batch), m, _ptr(feat), C, int(bool(normalize)),
-                                     _ptr(values), _ptr(weight))
+                                     _ptr(values), vdt, _ptr(weight))
         self.m = m
         self._V = None
         self._check(st, "splat")
@@ -201,10 +209,11 @@ class Lattice:
         self._check(self._lib.lattice_build_neighbors(self._h), "build_neighbors")
 
     def conv(self, x: torch.Tensor, w: torch.Tensor, dtype: str = "f32", bias: Optional[torch.Tensor] = None,
-             out: Optional[torch.Tensor] = None) -> torch.Tensor:
-        """1-ring convolution of vertex values ``x`` [>= V, C_in] with weights
-        [C_out, T, C_in] (fp32 for "f32", bf16 for "bf16")."""
-        _dev(x, torch.float32, "x")
+             out: Optional[torch.Tensor] = None, out_dtype: str = "f32") -> torch.Tensor:
+        """1-ring convolution of vertex values ``x`` [>= V, C_in] (fp32 or bf16
+        storage) with weights [C_out, T, C_in] (fp32 for dtype "f32", bf16 for
+        "bf16"); the output is stored as ``out_dtype``."""
+        _dev(x, (torch.float32, torch.bfloat16), "x")
         if dtype == "f32":
             _dev(w, torch.float32, "w")
             dt = F32
@@ -221,18 +230,19 @@ class Lattice:
             if bias.numel() != C_out:
                 raise ValueError("bias must have C_out elements")
         if out is None:
-            out = torch.empty((max(x.shape[0], 1), C_out), dtype=torch.float32, device=x.device)
-        _dev(out, torch.float32, "out")
+            out = torch.empty((max(x.shape[0], 1), C_out), dtype=_TORCH[out_dtype], device=x.device)
+        _dev(out, (torch.float32, torch.bfloat16), "out")
         need = self._rows_needed()
         if x.shape[0] < need or out.dim() != 2 or out.shape[1] != C_out or out.shape[0] < need:
             raise ValueError(f"x and out need >= {need} rows (out [rows, {C_out}])")
-        self._check(self._lib.lattice_conv(self._h, _ptr(x), C_in, _ptr(w), C_out, dt, _ptr(bias), _ptr(out)),
-                    "conv")
+        self._check(self._lib.lattice_conv(self._h, _ptr(x), _STORAGE[x.dtype], C_in, _ptr(w), C_out, dt,
+                                           _ptr(bias), _ptr(out), _STORAGE[out.dtype]), "conv")
         return out
 
     def slice(self, values: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-        """Eq. (slice) onto the points of the last splat: [m, C]."""
-        _dev(values, torch.float32, "values")
+        """Eq. (slice) onto the points of the last splat: [m, C] fp32
+        (``values`` stored as fp32 or bf16)."""
+        _dev(values, (torch.float32, torch.bfloat16), "values")
         C = values.shape[1]
         if values.dim() != 2 or values.shape[0] < self._rows_needed():
             raise ValueError(f"values needs >= {self._rows_needed()} rows")
@@ -241,7 +251,7 @@ class Lattice:
         _dev(out, torch.float32, "out")
         if out.numel() < self.m * C:
             raise ValueError("out needs [m, C]")
-        self._check(self._lib.lattice_slice(self._h, _ptr(values), C, _ptr(out)), "slice")
+        self._check(self._lib.lattice_slice(self._h, _ptr(values), _STORAGE[values.dtype], C, _ptr(out)), "slice")
         return out
 
     def weights_to_bf16(self, w: torch.Tensor) -> torch.Tensor:

@@ -66,9 +66,9 @@ def test_null_lattice_is_rejected():
     assert lib.lattice_max_vertices(None, 10) == -1
     assert lib.lattice_hash_capacity(None) == -1
     assert lib.lattice_dim(None) == -1
-    assert lib.lattice_splat(None, None, None, 0, None, 0, 0, None, None) == B.E_ARG
-    assert lib.lattice_conv(None, None, 1, None, 1, 0, None, None) == B.E_ARG
-    assert lib.lattice_slice(None, None, 1, None) == B.E_ARG
+    assert lib.lattice_splat(None, None, None, 0, None, 0, 0, None, 0, None) == B.E_ARG
+    assert lib.lattice_conv(None, None, 0, 1, None, 1, 0, None, None, 0) == B.E_ARG
+    assert lib.lattice_slice(None, None, 0, 1, None) == B.E_ARG
     assert lib.lattice_get_status(None) == B.E_ARG
     V = ctypes.c_int64()
     assert lib.lattice_num_vertices(None, ctypes.byref(V)) == B.E_ARG

@@ -175,6 +175,60 @@ def test_conv_parity(case):
         assert_close_scaled(got, ref_b, scale_b, REL_F32, "bf16 conv vs bf16-input oracle")
 
 
+BF16_ULP = 2.0 ** -8   # bound on the relative error of one round-to-nearest to bf16
+
+
+@pytest.mark.parametrize("case", [(3, 0.1, 6000, 64, 64), (3, 0.1, 5000, 128, 128), (4, 0.3, 5000, 64, 64),
+                                  (3, 0.1, 3000, 96, 32)])
+def test_conv_bf16_storage(case):
+    """bf16-stored input and output: the input is the bf16 value itself, the
+    output is the fp32 result rounded once to bf16."""
+    d, sigma, m, C_in, C_out = case
+    w = random_cloud(m, d, seed=900, extent=1.0, C=1)
+    L = _lattice(d, sigma, m)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, sigma)
+    nbr = O.neighbors(lat)
+    x = O.round_bf16(random_rows(lat.V, C_in, seed=901))
+    W = conv_weight(C_in, C_out, d, seed=902)
+    xin = g.to_gpu_order(x).to(torch.bfloat16)
+    wd = L.weights_to_bf16(to_dev(W))
+    ref, scale = O.conv(x, nbr, O.round_bf16(W))
+    out32 = L.conv(xin, wd, dtype="bf16")
+    assert_close_scaled(g.from_gpu_order(out32), ref, scale, REL_F32, "bf16-in conv")
+    out16 = L.conv(xin, wd, dtype="bf16", out_dtype="bf16")
+    assert out16.dtype == torch.bfloat16
+    got = g.from_gpu_order(out16.float())
+    assert_close_scaled(got, ref, REL_F32 * scale + BF16_ULP * np.abs(ref), 1.0, "bf16-out conv")
+    # fp32 compute with bf16 output
+    xf = g.to_gpu_order(x)
+    out16f = L.conv(xf, to_dev(W), dtype="f32", out_dtype="bf16")
+    reff, scalef = O.conv(x, nbr, W)
+    assert_close_scaled(g.from_gpu_order(out16f.float()), reff, REL_F32 * scalef + BF16_ULP * np.abs(reff), 1.0,
+                        "f32 conv, bf16 out")
+
+
+def test_splat_bf16_storage_and_slice_of_bf16():
+    w = random_cloud(6000, 3, seed=910, extent=1.0, C=64)
+    L = _lattice(3, 0.1, w.m)
+    vals, _ = L.splat(to_dev(w.pos), to_dev(w.feat), values_dtype="bf16")
+    assert vals.dtype == torch.bfloat16
+    V = L.num_vertices()
+    keys = L.keys().cpu().numpy().astype(np.int64)
+    from tests.gpu_util import canonical_perm
+    perm, rank = canonical_perm(keys, None, 3)
+    lat = O.build(w.pos, 0.1)
+    ref, _, scale = O.splat(lat, w.feat)
+    got = vals[:V].float().cpu().numpy().astype(np.float64)[perm]
+    assert_close_scaled(got, ref, REL_F32 * scale + BF16_ULP * np.abs(ref), 1.0, "bf16 splat")
+    # slice of bf16-stored vertex values
+    y = O.round_bf16(random_rows(lat.V, 64, seed=911))
+    yin = to_dev(np.ascontiguousarray(y[rank])).to(torch.bfloat16)
+    out = L.slice(yin).cpu().numpy()
+    sref, sscale = O.slice_(lat, y)
+    assert_close_scaled(out, sref, sscale, REL_F32, "slice of bf16 values")
+
+
 def test_conv_weights_to_bf16_matches_oracle_rounding():
     L = _lattice(3, 0.1, 10)
     W = conv_weight(64, 128, 3, seed=1)
