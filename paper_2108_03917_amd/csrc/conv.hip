@@ -200,17 +200,29 @@ __global__ __launch_bounds__((BM / WR) * (BN / WC) * 64) void k_conv_mfma(
             if (s < NQ) load_chunk(s, s);
         store_chunk(0, 0);
         __syncthreads();
-        for (int q0 = 0; q0 < NQ; q0 += P) {
+        // Steady state, free of branches so that the compiler keeps the ring's
+        // loads in flight across iterations: past the last chunk the refill
+        // re-reads chunk NQ-1 and the store writes an LDS buffer nobody reads.
+        const int NQP = (NQ / P) * P;
+        for (int q0 = 0; q0 < NQP; q0 += P) {
 #pragma unroll
             for (int s = 0; s < P; ++s) {
                 const int q = q0 + s;
-                if (q < NQ) {
-                    // ring slot s held chunk q, already in LDS: refill it with chunk q+P
-                    if (q + P < NQ) load_chunk(q + P, s);
-                    compute(q & 1);
-                    if (q + 1 < NQ) store_chunk((s + 1) % P, (q + 1) & 1);
-                    __syncthreads();
-                }
+                // ring slot s held chunk q, already in LDS: refill it with chunk q+P
+                load_chunk(q + P < NQ ? q + P : NQ - 1, s);
+                compute(q & 1);
+                store_chunk((s + 1) % P, (q + 1) & 1);
+                __syncthreads();
+            }
+        }
+        // Remainder (fewer than P chunks, all already loaded).
+#pragma unroll
+        for (int s = 0; s < P; ++s) {
+            const int q = NQP + s;
+            if (q < NQ) {
+                compute(q & 1);
+                if (q + 1 < NQ) store_chunk((s + 1) % P, (q + 1) & 1);
+                __syncthreads();
             }
         }
 
@@ -234,6 +246,151 @@ __global__ __launch_bounds__((BM / WR) * (BN / WC) * 64) void k_conv_mfma(
                     }
                 }
             }
+    }
+}
+
+// Weight-stationary variant: the workgroup's slice of W (BN output channels,
+// all K = T C_in) stays in LDS for the whole persistent loop, and every
+// wavefront independently computes 32-row x BN tiles, gathering its A rows
+// straight into MFMA operand registers (16 bytes per lane per k-group) PT taps
+// ahead of their use.  No barrier in the main loop.  The tap loop is unrolled
+// (T is a template parameter).  CM as for k_conv_mfma.  For the fp32 MFMA
+// (32x32x2), lane half h holds k = 8 g + 4 h + c in component c of its A and
+// B registers; step c pairs the same components, so every k meets its own
+// weight exactly once.
+template <int CM, bool OUT_BF16, int T, int C_IN, int CB, int PT>
+__global__ __launch_bounds__(512) void k_conv_ws(const void *__restrict__ in, const void *__restrict__ wv, int C_out,
+                                                 const float *__restrict__ bias, void *__restrict__ out,
+                                                 const int32_t *__restrict__ nbr, const int32_t *__restrict__ counters) {
+    constexpr bool BF16 = CM != 0;
+    constexpr int NW = 8;                        // wavefronts per workgroup
+    constexpr int BN = 32 * CB;
+    constexpr int K = T * C_IN;
+    constexpr int WESZ = BF16 ? 2 : 4;
+    constexpr int KSTRIDE = K * WESZ + 16;       // LDS bytes per weight row (16 B pad: no bank conflicts)
+    constexpr int KGE = BF16 ? 16 : 8;           // K elements per k-group
+    constexpr int KG = C_IN / KGE;               // k-groups per tap
+    constexpr int IN_ESZ = CM == 2 ? 2 : 4;
+    constexpr int AW = CM == 1 ? 2 : 1;          // 16-byte loads per lane per k-group (fp32 rows -> bf16)
+    static_assert(C_IN % KGE == 0, "channels");
+    extern __shared__ __attribute__((aligned(16))) char wlds[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int lrow = lane & 31;
+    const int khalf = lane >> 5;
+    const int n_nt = C_out / BN;
+    const int nt = blockIdx.x % n_nt;
+    const int col_base = nt * BN;
+    const int64_t V = counters[CNT_V];
+    const int64_t n_mt = (V + 31) / 32;
+
+    // W slice -> LDS, once.
+    {
+        constexpr int SEGS = K * WESZ / 16;
+        const char *src = reinterpret_cast<const char *>(wv) + (int64_t)col_base * K * WESZ;
+        for (int i = tid; i < BN * SEGS; i += NW * 64) {
+            const int n = i / SEGS, sg = i - n * SEGS;
+            *reinterpret_cast<u32x4_t *>(wlds + n * KSTRIDE + sg * 16) =
+                *reinterpret_cast<const u32x4_t *>(src + (int64_t)n * K * WESZ + sg * 16);
+        }
+    }
+    __syncthreads();
+
+    const int64_t wave0 = (int64_t)(blockIdx.x / n_nt) * NW + wave;
+    const int64_t nwaves = (int64_t)(gridDim.x / n_nt) * NW;
+    for (int64_t mt = wave0; mt < n_mt; mt += nwaves) {
+        const int64_t row = mt * 32 + lrow;
+        const bool live = row < V;
+        const int64_t rowc = live ? row : 0;
+        int nb[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) nb[t] = live ? nbr[rowc * T + t] : -1;
+
+        f32x16_t acc[CB];
+#pragma unroll
+        for (int j = 0; j < CB; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+
+        u32x4_t ar[PT][KG][AW];
+        auto load_tap = [&](int t, int slot) {
+            const int u = nb[t];
+            const int64_t rr = u >= 0 ? u : 0;
+            const char *base = reinterpret_cast<const char *>(in) + rr * C_IN * IN_ESZ;
+#pragma unroll
+            for (int g = 0; g < KG; ++g)
+#pragma unroll
+                for (int w = 0; w < AW; ++w)
+                    ar[slot][g][w] = *reinterpret_cast<const u32x4_t *>(
+                        base + (g * KGE + khalf * (KGE / 2)) * IN_ESZ + w * 16);
+        };
+        auto compute_tap = [&](int t, int slot) {
+            const bool pres = nb[t] >= 0;
+#pragma unroll
+            for (int g = 0; g < KG; ++g) {
+                u32x4_t a;
+                if (CM == 1) {
+                    const u32x4_t x0 = ar[slot][g][0], x1 = ar[slot][g][1];
+                    a[0] = bf16_bits(__uint_as_float(x0[0])) | (bf16_bits(__uint_as_float(x0[1])) << 16);
+                    a[1] = bf16_bits(__uint_as_float(x0[2])) | (bf16_bits(__uint_as_float(x0[3])) << 16);
+                    a[2] = bf16_bits(__uint_as_float(x1[0])) | (bf16_bits(__uint_as_float(x1[1])) << 16);
+                    a[3] = bf16_bits(__uint_as_float(x1[2])) | (bf16_bits(__uint_as_float(x1[3])) << 16);
+                } else {
+                    a = ar[slot][g][0];
+                }
+                if (!pres) a = u32x4_t{0u, 0u, 0u, 0u};
+                const int kb = (t * C_IN + g * KGE) * WESZ + khalf * 16;
+                u32x4_t b[CB];
+#pragma unroll
+                for (int j = 0; j < CB; ++j)
+                    b[j] = *reinterpret_cast<const u32x4_t *>(wlds + (j * 32 + lrow) * KSTRIDE + kb);
+                if (BF16) {
+#pragma unroll
+                    for (int j = 0; j < CB; ++j)
+                        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                                         __builtin_bit_cast(bf16x8_t, b[j]), acc[j],
+                                                                         0, 0, 0);
+                } else {
+                    // independent accumulators innermost, so consecutive MFMAs do not wait on each other
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+#pragma unroll
+                        for (int j = 0; j < CB; ++j)
+                            acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[c]),
+                                                                          __uint_as_float(b[j][c]), acc[j], 0, 0, 0);
+                }
+            }
+        };
+#pragma unroll
+        for (int t = 0; t < PT && t < T; ++t) load_tap(t, t);
+        // The fences keep the scheduler from hoisting later taps' loads above
+        // earlier taps' MFMAs, which would hold all T taps in registers.
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            __builtin_amdgcn_sched_barrier(0);
+            compute_tap(t, t % PT);
+            if (t + PT < T) load_tap(t + PT, t % PT);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+
+#pragma unroll
+        for (int j = 0; j < CB; ++j) {
+            const int col = col_base + j * 32 + lrow;
+            const float bc = bias ? bias[col] : 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t orow = mt * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
+                if (orow < V) {
+                    const float y = acc[j][r] + bc;
+                    if (OUT_BF16)
+                        reinterpret_cast<uint16_t *>(out)[orow * C_out + col] = (uint16_t)bf16_bits(y);
+                    else
+                        reinterpret_cast<float *>(out)[orow * C_out + col] = y;
+                }
+            }
+        }
     }
 }
 
@@ -279,8 +436,10 @@ __global__ __launch_bounds__(256) void k_conv_generic(const void *__restrict__ i
 template <int CM, bool OUT_BF16, int BM, int BN, int WR, int WC, int P>
 hipError_t launch_mfma(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias, void *out) {
     constexpr int NT = (BM / WR) * (BN / WC) * 64;
+    constexpr int LDS = 2 * (BM + BN) * kRowBytes + BM * kMaxTaps * 4;
+    constexpr int PER_CU = (160 * 1024) / LDS < 4 ? (160 * 1024) / LDS : 4;  // resident workgroups per CU
     const int64_t tiles = ((L->max_vertices + BM - 1) / BM) * (C_out / BN);
-    int64_t grid = (int64_t)L->cu_count * 2;
+    int64_t grid = (int64_t)L->cu_count * PER_CU;
     if (grid > tiles) grid = tiles;
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL((k_conv_mfma<CM, OUT_BF16, BM, BN, WR, WC, P>), dim3((unsigned)grid), dim3(NT), 0, L->stream,
@@ -292,6 +451,9 @@ template <int CM, bool OUT_BF16>
 hipError_t launch_mfma_n(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias,
                          void *out) {
     constexpr int P = CM == 1 ? 2 : 3;
+    // fp32: 64 x 64 tiles, four workgroups per CU (the fp32 MFMA is slow enough
+    // that four waves per SIMD keep it busy; small tiles shorten the tail)
+    if (CM == 0) return launch_mfma<CM, OUT_BF16, 64, 64, 32, 32, 2>(L, in, C_in, w, C_out, bias, out);
     if (C_out % 128 == 0) return launch_mfma<CM, OUT_BF16, 128, 128, 64, 64, P>(L, in, C_in, w, C_out, bias, out);
     return launch_mfma<CM, OUT_BF16, 128, 64, 32, 64, P>(L, in, C_in, w, C_out, bias, out);
 }
@@ -305,12 +467,81 @@ hipError_t launch_generic(lattice *L, const void *in, int C_in, const void *w, i
     return hipGetLastError();
 }
 
+constexpr int kWsMaxLds = 152 * 1024;  // weight slice budget of one workgroup
+
+template <int CM, bool OUT_BF16, int T, int C_IN, int CB, int PT>
+hipError_t launch_ws(lattice *L, const void *in, const void *w, int C_out, const float *bias, void *out) {
+    constexpr int BN = 32 * CB;
+    constexpr int WESZ = CM != 0 ? 2 : 4;
+    constexpr int LDS = BN * (T * C_IN * WESZ + 16);
+    static_assert(LDS <= kWsMaxLds, "weight slice exceeds LDS");
+    auto kern = k_conv_ws<CM, OUT_BF16, T, C_IN, CB, PT>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const int n_nt = C_out / BN;
+    const int64_t tiles = ((L->max_vertices + 31) / 32) * n_nt;
+    int64_t grid = (int64_t)L->cu_count;
+    grid = ((grid + n_nt - 1) / n_nt) * n_nt;  // whole groups of N slices
+    const int64_t need = ((tiles + 7) / 8 + n_nt - 1) / n_nt * n_nt;  // no more workgroups than 8-wave groups of tiles
+    if (grid > need) grid = need < n_nt ? n_nt : need;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(512), LDS, L->stream, in, w, C_out, bias, out, L->nbr,
+                       L->counters);
+    return hipGetLastError();
+}
+
+// Weight-stationary dispatch for the shapes it covers; returns false when
+// the shape is not covered (the caller falls back to k_conv_mfma).
+template <bool OUT_BF16>
+bool try_ws(lattice *L, const void *in, bool in_bf16, int C_in, const void *w, int C_out, bool bf16,
+            const float *bias, void *out, hipError_t *err) {
+#define WS(CM, TT, CI, CBV, PTV)                                                                   \
+    do {                                                                                           \
+        *err = launch_ws<CM, OUT_BF16, TT, CI, CBV, PTV>(L, in, w, C_out, bias, out);             \
+        return true;                                                                               \
+    } while (0)
+    const int T = L->T;
+    if (T != 9 && T != 11) return false;
+    if (!bf16) return false;  // fp32 runs on the LDS-tiled kernel
+    if (bf16 && in_bf16) {
+        if (C_in == 64) {
+            if (C_out % 128 == 0) {
+                if (T == 9) WS(2, 9, 64, 4, 2);
+                WS(2, 11, 64, 2, 3);
+            }
+            if (C_out % 64 == 0) {
+                if (T == 9) WS(2, 9, 64, 2, 3);
+                WS(2, 11, 64, 2, 3);
+            }
+        }
+        if (C_in == 128 && C_out % 64 == 0) {
+            if (T == 9) WS(2, 9, 128, 2, 2);
+            WS(2, 11, 128, 1, 2);
+        }
+        return false;
+    }
+    if (bf16 && !in_bf16 && C_in == 64 && C_out % 64 == 0) {
+        if (T == 9) WS(1, 9, 64, 2, 2);
+        WS(1, 11, 64, 2, 2);
+    }
+    return false;
+#undef WS
+}
+
 template <bool OUT_BF16>
 hipError_t dispatch_out(lattice *L, const void *in, lattice_dtype in_dt, int C_in, const void *w, int C_out,
                         lattice_dtype dt, const float *bias, void *out) {
     const bool in_bf16 = in_dt == LATTICE_BF16;
     const bool bf16 = dt == LATTICE_BF16;
     const bool aligned = ((reinterpret_cast<uintptr_t>(in) & 15) == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    if (aligned && L->conv_kernel != 1) {
+        hipError_t err = hipSuccess;
+        if (try_ws<OUT_BF16>(L, in, in_bf16, C_in, w, C_out, bf16, bias, out, &err)) return err;
+    }
     if (aligned && C_out % 64 == 0) {
         if (!bf16 && !in_bf16 && C_in % 32 == 0)
             return launch_mfma_n<0, OUT_BF16>(L, in, C_in, w, C_out, bias, out);

@@ -58,6 +58,8 @@ struct lattice {
     bool batched = false;
     int cu_count = 256;
 
+    int conv_kernel = 0;  // 0: weight-stationary where it applies, 1: always the LDS-tiled kernel
+
     int timing = 0;
     lattice_timer timers[LATTICE_NUM_STAGES];
     void *events = nullptr;  // per-stage event pools and pending pairs (lattice.hip)

@@ -55,6 +55,9 @@ __device__ __forceinline__ void unpack_key(uint64_t key, int *c, uint32_t &batch
     batch = (D <= 3) ? (uint32_t)(key >> 48) : 0u;
 }
 
+// Home slot of a key: the low bits of its mixed value.
+__device__ __forceinline__ uint32_t home_slot(uint64_t key, uint32_t mask) { return (uint32_t)key_mix(key) & mask; }
+
 // Look up N keys of a table that no thread is writing, all probes of one
 // round in flight together.  `want[k]` false skips key k.  Returns the vertex
 // index per key, -1 when absent.
@@ -65,7 +68,7 @@ __device__ __forceinline__ void hash_find_all(const HEntry *__restrict__ tab, ui
     bool pending[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) {
-        h[k] = (uint32_t)key_mix(key[k]) & mask;
+        h[k] = want[k] ? home_slot(key[k], mask) : 0u;
         pending[k] = want[k];
         out[k] = -1;
     }

@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kBlock) void k_insert(const float *__restrict__ pos
     for (int k = 0; k < DP1; ++k) {
         slot[k] = -1;
         pend[k] = hkey[k] != 0ull;
-        h[k] = (uint32_t)key_mix(hkey[k]) & mask;
+        h[k] = pend[k] ? home_slot(hkey[k], mask) : 0u;
     }
     for (uint32_t probe = 0; probe <= mask; ++probe) {
         unsigned long long old[DP1];
