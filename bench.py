@@ -43,7 +43,13 @@ WORKLOAD_NAMES = {
 
 
 class Pipeline:
-    """Device-resident inputs and buffers of one workload, and one step over them."""
+    """Device-resident inputs and buffers of one workload, and one step over them.
+
+    Everything runs on one side stream (default priority): a caller that reads
+    the outputs on another stream synchronises with `stream` first.  Every
+    buffer is allocated up front and the step never synchronises with the host
+    (V stays on the device), so the step can be captured once as a HIP graph
+    and replayed."""
 
     def __init__(self, w, stream=None):
         import torch
@@ -53,7 +59,9 @@ class Pipeline:
         self.w = w
         dev = torch.device("cuda:0")
         torch.cuda.set_device(dev)
-        self.L = Lattice(w.d, w.sigma, max_points=w.m, stream=stream)
+        self.stream = stream if stream is not None else torch.cuda.Stream(device=dev)
+        self.graph = None
+        self.L = Lattice(w.d, w.sigma, max_points=w.m, stream=self.stream)
         self.pos = torch.from_numpy(w.pos).to(dev)
         self.feat = torch.from_numpy(w.feat).to(dev)
         self.batch = None if w.batch is None else torch.from_numpy(w.batch).to(dev)
@@ -81,15 +89,42 @@ class Pipeline:
         return self.convs[-1]
 
     def run(self, ev=None):
-        """One step.  With `ev` (a list of torch events) an event is recorded
-        before every stage and one after the last, on the current stream."""
+        """One step, enqueued on the pipeline's stream.  With `ev` (a list of
+        torch events) an event is recorded on that stream before every stage
+        and one after the last."""
+        import torch
+
+        with torch.cuda.stream(self.stream):
+            return self._run(ev)
+
+    def capture(self):
+        """Capture one step as a graph (after at least one eager step, which
+        sets up every kernel's launch attributes)."""
+        import torch
+
+        self.stream.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=self.stream):
+            self._run(None)
+        self.stream.synchronize()
+        self.graph = g
+        return g
+
+    def replay(self):
+        import torch
+
+        with torch.cuda.stream(self.stream):
+            self.graph.replay()
+        return self.sliced
+
+    def _run(self, ev):
         L = self.L
         k = 0
 
         def mark():
             nonlocal k
             if ev is not None:
-                ev[k].record()
+                ev[k].record(self.stream)
                 k += 1
 
         mark()
@@ -190,6 +225,56 @@ def cpu_baseline(w, budget_s=20.0):
             "sample": f"{n} whole step(s) of the {w.name} workload ({w.m} points), {dt:.1f} s"}
 
 
+# Source files that define each stage's kernels; a stored traffic measurement
+# is used only while their contents are unchanged.
+STAGE_SOURCES = {
+    "splat": ["splat.hip", "keys.h", "internal.h"],
+    "neighbors": ["neighbors.hip", "keys.h", "internal.h"],
+    "conv": ["conv.hip", "internal.h"],
+    "slice": ["slice.hip", "internal.h"],
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def source_hash(stage: str) -> str:
+    import hashlib
+
+    h = hashlib.sha1()
+    kind = "conv" if stage.startswith("conv") else stage
+    for f in STAGE_SOURCES[kind]:
+        with open(os.path.join(ROOT, "paper_2108_03917_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, stage: str):
+    """HBM bytes per launch of a stage from committed rocprofv3 counter runs
+    (FETCH_SIZE and WRITE_SIZE, each scaled by its copy-kernel calibration), or
+    None when there is no measurement or the kernel source has changed."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as fh:
+        table = json.load(fh)
+    e = table.get("entries", {}).get(f"{workload}/{stage}")
+    if not e or e.get("source_sha1") != source_hash(stage):
+        return None
+    cal = table["calibration"]
+    return (e["fetch_kib"] * cal["fetch_scale"] + e["write_kib"] * cal["write_scale"]) * 1024.0
+
+
+def calibrate_copy(mib: int):
+    """A plain device copy of `mib` MiB (three times), the reference kernel for
+    scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+
+    x = torch.ones(mib * 1024 * 1024 // 4, dtype=torch.float32, device="cuda:0")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_mib": mib}))
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -198,7 +283,12 @@ def main(argv=None):
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    ap.add_argument("--graph", action="store_true", help="time graph replays of the step instead of eager steps")
     args = ap.parse_args(argv)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested): the lattice path has no "
               "multi-GPU mode", file=sys.stderr)
@@ -212,23 +302,38 @@ def main(argv=None):
     pipe = Pipeline(w)
     for _ in range(args.warmup):
         pipe.run()
-    torch.cuda.synchronize()
+    pipe.stream.synchronize()
     V = pipe.L.num_vertices()
 
+    # Timed region 1: whole steps (eager, or graph replays with --graph).
+    step = pipe.run
+    if args.graph:
+        pipe.capture()
+        for _ in range(3):
+            pipe.replay()
+        step = pipe.replay
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sec = t1 - t0
+
+    # Timed region 2: the same steps run eagerly with HIP events recorded on
+    # the pipeline's stream around every stage (each conv and the slice are
+    # one kernel launch), for the per-stage times and the roofline.
     names = pipe.stage_names()
     nev = len(names) + 1
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        pipe.run(evs[s])
+    for s_ in range(args.steps):
+        pipe.run(evs[s_])
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    sec = t1 - t0
     stage_ms = {n: 0.0 for n in names}
-    for s in range(args.steps):
+    for s_ in range(args.steps):
         for i, n in enumerate(names):
-            stage_ms[n] += evs[s][i].elapsed_time(evs[s][i + 1])
+            stage_ms[n] += evs[s_][i].elapsed_time(evs[s_][i + 1])
     stage_ms = {n: v / args.steps for n, v in stage_ms.items()}
 
     work = algorithmic_work(w, V)
@@ -237,7 +342,10 @@ def main(argv=None):
     rf = dict(stages[dominant])
     rf.pop("ms")
     rf["kernel"] = dominant
-    rf["traffic"] = None
+    rf["traffic"] = measured_traffic(WORKLOAD_NAMES.get(args.config, w.name), dominant)
+    rf["algorithmic_bytes"] = work[dominant]["bytes"]
+    if "flops" in work[dominant]:
+        rf["algorithmic_flops"] = work[dominant]["flops"]
 
     out = {
         "metric": "points/s for splat+conv+slice",
@@ -258,6 +366,9 @@ def main(argv=None):
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
+        "timing": ("value: " + ("graph replays" if args.graph else "eager steps") + " of the whole step, no "
+                   "events inside; stages and roofline: HIP events around each stage of eager steps on the "
+                   "same stream"),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

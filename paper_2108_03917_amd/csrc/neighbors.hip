@@ -12,48 +12,45 @@ namespace {
 
 constexpr int kBlock = 256;
 
+// One thread per (vertex, ring tap): tap 1+j looks up c + n_j, tap d+2+j
+// looks up c - n_j; the thread of tap 1 also writes tap 0 (the vertex).
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_neighbors(const uint64_t *__restrict__ vkeys,
                                                       const HEntry *__restrict__ tab, uint32_t mask,
                                                       const int32_t *counters, int32_t *__restrict__ nbr) {
     constexpr int DP1 = D + 1;
-    constexpr int T = 2 * DP1 + 1;
-    const int64_t V = counters[CNT_V];
+    constexpr int R = 2 * DP1;  // ring taps
+    constexpr int T = R + 1;
+    const int64_t n = (int64_t)counters[CNT_V] * R;
     const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < V; v += stride) {
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += stride) {
+        const int64_t v = e / R;
+        const int tap = (int)(e - v * R);         // 0..R-1 -> row entry 1+tap
+        const int j = tap < DP1 ? tap : tap - DP1;
+        const bool plus = tap < DP1;
         int c[D];
         uint32_t b;
         unpack_key<D>(vkeys[v], c, b);
-        // Keys of the 2(d+1) ring vertices: index j for +n_j, DP1 + j for -n_j.
-        uint64_t key[2 * DP1];
-        bool want[2 * DP1];
+        // Only c_0..c_{d-1} are packed; c_d follows from the zero sum.
 #pragma unroll
-        for (int j = 0; j < DP1; ++j) {
-#pragma unroll
-            for (int sgn = 0; sgn < 2; ++sgn) {
-                // Only c_0..c_{d-1} are packed; c_d follows from the zero sum.
-                int q[D];
-#pragma unroll
-                for (int i = 0; i < D; ++i) {
-                    const int n = (i == j ? DP1 : 0) - 1;
-                    q[i] = sgn == 0 ? c[i] + n : c[i] - n;
-                }
-                want[sgn * DP1 + j] = pack_key<D>(q, b, key[sgn * DP1 + j]);
-            }
+        for (int i = 0; i < D; ++i) {
+            const int nj = (i == j ? DP1 : 0) - 1;
+            c[i] = plus ? c[i] + nj : c[i] - nj;
         }
-        int found[2 * DP1];
-        hash_find_all<2 * DP1>(tab, mask, key, want, found);
+        uint64_t key;
+        const bool want = pack_key<D>(c, b, key);
+        int found = -1;
+        hash_find_all<1>(tab, mask, &key, &want, &found);
         int32_t *row = nbr + v * T;
-        row[0] = (int32_t)v;
-#pragma unroll
-        for (int t = 0; t < 2 * DP1; ++t) row[1 + t] = found[t];
+        row[1 + tap] = found;
+        if (tap == 0) row[0] = (int32_t)v;
     }
 }
 
 }  // namespace
 
 hipError_t launch_neighbors(lattice *L) {
-    const unsigned grid = grid_for(L->max_vertices, kBlock, L->cu_count, 8);
+    const unsigned grid = grid_for(L->max_vertices * 2 * (L->d + 1), kBlock, L->cu_count, 16);
     const uint32_t mask = (uint32_t)(L->cap - 1);
     switch (L->d) {
 #define NB_CASE(DD)                                                                                              \

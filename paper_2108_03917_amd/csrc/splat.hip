@@ -54,14 +54,16 @@ __device__ __forceinline__ void elevate(const float *g, const ElevParams &ep, fl
     x[0] = S;
 }
 
+constexpr int kInsertBlock = 64;  // one wavefront per workgroup: small clouds still spread over every CU
+
 template <int D>
-__global__ __launch_bounds__(kBlock) void k_insert(const float *__restrict__ pos, const int32_t *__restrict__ batch,
+__global__ __launch_bounds__(kInsertBlock) void k_insert(const float *__restrict__ pos, const int32_t *__restrict__ batch,
                                                    int64_t m, ElevParams ep, HEntry *tab, uint32_t mask,
                                                    int32_t *__restrict__ idx, int32_t *__restrict__ rank_out,
                                                    float *__restrict__ bary, int32_t *counters) {
 #pragma clang fp contract(off)
     constexpr int DP1 = D + 1;
-    const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t p = (int64_t)blockIdx.x * kInsertBlock + threadIdx.x;
     const bool active = p < m;
     const int lane = threadIdx.x & 63;
 
@@ -656,11 +658,11 @@ hipError_t launch_insert(lattice *L, const float *pos, const int32_t *batch, int
     ElevParams ep;
     for (int i = 0; i < LATTICE_MAX_D; ++i) ep.f[i] = L->factors[i];
     ep.inv = L->inv_dp1;
-    const unsigned grid = (unsigned)((m + kBlock - 1) / kBlock);
+    const unsigned grid = (unsigned)((m + kInsertBlock - 1) / kInsertBlock);
     const uint32_t mask = (uint32_t)(L->cap - 1);
     return dispatch_d(L->d, [&](auto dc) {
         constexpr int D = decltype(dc)::value;
-        hipLaunchKernelGGL(k_insert<D>, dim3(grid), dim3(kBlock), 0, L->stream, pos, batch, m, ep, L->tab, mask,
+        hipLaunchKernelGGL(k_insert<D>, dim3(grid), dim3(kInsertBlock), 0, L->stream, pos, batch, m, ep, L->tab, mask,
                            L->idx, L->rank, L->bary, L->counters);
         return hipGetLastError();
     });

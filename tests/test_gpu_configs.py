@@ -75,7 +75,9 @@ def test_bench_workload_end_to_end():
 
     w = make_workload(bench.DEFAULT_CONFIG)
     step = bench.Pipeline(w)
-    out = step.run().cpu().numpy().astype(np.float64)
+    res = step.run()
+    step.stream.synchronize()   # the pipeline runs on its own stream
+    out = res.cpu().numpy().astype(np.float64)
     lat = O.build(w.pos, w.sigma, batch=w.batch)
     x, _, scale = O.splat(lat, w.feat)
     nbr = O.neighbors(lat)
