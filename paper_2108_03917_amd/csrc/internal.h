@@ -10,7 +10,9 @@
 // Device status bits, OR-ed into counters[CNT_STATUS] by kernels.
 enum : int { ST_CAPACITY = 1, ST_RANGE = 2 };
 // Slots of the device counter array.
-enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_H = 3, CNT_WORDS = 4 };
+// CNT_SPLIT and CNT_ROWS count the vertices whose pair list the splat gather
+// cuts into parts, and those parts.
+enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_SPLIT = 3, CNT_ROWS = 4, CNT_WORDS = 8 };
 
 // Packed 64-bit vertex key: 16 bits per coordinate c_0..c_{d-1}, each stored
 // as c + KEY_BIAS (so a field is never 0 for |c| <= KEY_MAX), and for d <= 3
@@ -41,9 +43,15 @@ struct lattice {
 
     HEntry *tab = nullptr;      // [cap] hash table {key, pair count, vertex index}
     uint64_t *vkeys = nullptr;  // [max_vertices] packed key of each vertex
-    int32_t *heavy = nullptr;   // [max_vertices] vertices whose pair list is long
-    int32_t *blk = nullptr;     // [cap / 2048][2] per-block sums of the numbering scan
+    int32_t *blk = nullptr;     // [scan_blocks_max()][4] per-block sums of the numbering scan
     int32_t *vinfo = nullptr;   // [max_vertices][2] (offset, count) of the vertex's pair list
+    // Long pair lists are gathered in parts (splat.hip); at most
+    // split_rows_max() parts and split vertices per splat.
+    int32_t *split = nullptr;   // [rows_max][3] (vertex, first part row, parts) per split vertex
+    int32_t *rowmap = nullptr;  // [rows_max] split index of each part row
+    float *pweight = nullptr;   // [rows_max] partial weight sums
+    float *partial = nullptr;   // [rows_max][partial_cols] partial feature sums, grown on demand
+    int64_t partial_cols = 0;
     int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
     int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
@@ -76,6 +84,8 @@ hipError_t launch_number(lattice *L);
 hipError_t launch_fill(lattice *L, int64_t m);
 hipError_t launch_gather(lattice *L, const float *feat, int C, int normalize, void *values, lattice_dtype values_dt,
                          float *weight);
+int64_t split_rows_max(const lattice *L);
+int64_t scan_blocks_max();
 hipError_t launch_export_keys(lattice *L, int32_t *keys, int32_t *batch);
 hipError_t launch_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst);
 

@@ -42,8 +42,11 @@ int64_t next_pow2(int64_t x) {
 void free_all(lattice *L) {
     (void)hipFree(L->tab);
     (void)hipFree(L->vkeys);
-    (void)hipFree(L->heavy);
     (void)hipFree(L->blk);
+    (void)hipFree(L->split);
+    (void)hipFree(L->rowmap);
+    (void)hipFree(L->pweight);
+    (void)hipFree(L->partial);
     (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
     (void)hipFree(L->rank);
@@ -190,8 +193,10 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
     const int dp1 = d + 1;
     bool ok = hipMalloc(&L->tab, L->cap * 16) == hipSuccess &&
               hipMalloc(&L->vkeys, L->max_vertices * sizeof(uint64_t)) == hipSuccess &&
-              hipMalloc(&L->heavy, L->max_vertices * sizeof(int32_t)) == hipSuccess &&
-              hipMalloc(&L->blk, ((L->cap + 2047) / 2048) * 2 * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->blk, scan_blocks_max() * 4 * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->split, split_rows_max(L) * 3 * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->rowmap, split_rows_max(L) * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->pweight, split_rows_max(L) * sizeof(float)) == hipSuccess &&
               hipMalloc(&L->vinfo, L->max_vertices * 2 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->idx, max_points * dp1 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->rank, max_points * dp1 * sizeof(int32_t)) == hipSuccess &&
@@ -258,6 +263,23 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
     if (batch && L->d == 4) {
         set_err(L, "splat: batch ids need d <= 3 (a d = 4 key uses all 64 bits)");
         return LATTICE_E_ARG;
+    }
+    // Scratch for the partial rows of long pair lists, sized for C columns
+    // (grown here, outside any timed or captured region of a caller that
+    // splats once before it times or captures).
+    const int64_t cols = (C + 3) & ~3;
+    if (cols > L->partial_cols) {
+        if (L->partial) HIP_TRY(L, hipFree(L->partial));
+        L->partial = nullptr;
+        L->partial_cols = 0;
+        if (hipMalloc(&L->partial, split_rows_max(L) * cols * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            L->partial = nullptr;
+            set_err(L, "splat: cannot allocate %lld bytes of gather scratch",
+                    (long long)(split_rows_max(L) * cols * sizeof(float)));
+            return LATTICE_E_NOMEM;
+        }
+        L->partial_cols = cols;
     }
     hipEvent_t t0;
     lattice_status s = timer_begin(L, LATTICE_STAGE_SPLAT, &t0);

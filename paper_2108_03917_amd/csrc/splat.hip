@@ -8,11 +8,12 @@
 //                   keys; CAS-insert of the d+1 keys (runs of equal keys in
 //                   neighbouring lanes are inserted once), a rank for every
 //                   (point, vertex) pair from the slot's counter
-//   k_scan_*        vertex indices and pair-list ranges in hash-slot order
+//   k_scan_count/assign  vertex indices and pair-list ranges in hash-slot order
 //   k_fill          per pair: slot -> vertex index, (p, b_pk) into the list
 //   k_gather        per vertex: x_v = sum b_pv f_p and w_v = sum b_pv
-//                   (optionally x_v / w_v), each row written once; vertices
-//                   with many pairs by k_gather_heavy, a workgroup each
+//                   (optionally x_v / w_v), each row written once; long pair
+//                   lists are summed in parts of kPart pairs
+//   k_gather_combine  per long list: the sum of its part rows
 #include "internal.h"
 #include "keys.h"
 
@@ -27,8 +28,6 @@ __device__ __forceinline__ uint32_t bf16_bits(float f) {
     return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Vertices with more pairs than this are reduced by a whole workgroup.
-constexpr int kHeavy = 64;
 
 struct ElevParams {
     float f[LATTICE_MAX_D];
@@ -248,16 +247,26 @@ __global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap
     if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS) counters[threadIdx.x] = 0;
 }
 
-// Vertex numbering and pair-list layout, in hash-slot order, by a three-phase
+// Vertex numbering and pair-list layout, in hash-slot order, by a two-pass
 // scan over the table (no same-address atomics):
-//   k_scan_count   per block of kScanSlots slots: occupied slots and pairs
-//   k_scan_blocks  one workgroup: exclusive prefix of the block sums; V and
-//                  the pair total
-//   k_scan_assign  per block, in slot order: vertex index, list offset and
-//                  count of every occupied slot; vertices with more than
-//                  kHeavy pairs are also listed for the workgroup-per-vertex
-//                  gather.
-constexpr int kScanSlots = 2048;
+//   k_scan_count   per block of `span` slots, four sums: occupied slots,
+//                  pairs, vertices whose pair list is longer than kPart
+//                  ("split" vertices) and the part rows of those vertices
+//   k_scan_assign  per block: its exclusive prefix (it sums the block sums
+//                  before it), then, in slot order, every occupied slot's
+//                  vertex index, pair-list offset and count; a split vertex
+//                  also gets a split index and ceil(count / kPart) part rows
+//                  (see k_gather).  The last block publishes the totals.
+// A scan block covers `span` slots, in chunks of kChunk (kSlotsPerThread
+// consecutive slots per thread): span is kChunk, or a multiple of it on
+// tables so large that kChunk would make more than kMaxScanBlocks blocks
+// (each block sums the block totals before it, so their number must stay
+// small).
+constexpr int kSlotsPerThread = 4;
+constexpr int64_t kChunk = (int64_t)kBlock * kSlotsPerThread;
+constexpr int64_t kMaxScanBlocks = 4096;
+constexpr int kPart = 32;  // pairs per gather work unit
+enum { Q_OCC = 0, Q_PAIRS = 1, Q_SPLIT = 2, Q_ROWS = 3, NQ = 4 };
 
 __device__ __forceinline__ int wave_incl_scan(int x, int lane) {
 #pragma unroll
@@ -268,130 +277,131 @@ __device__ __forceinline__ int wave_incl_scan(int x, int lane) {
     return x;
 }
 
-__global__ __launch_bounds__(kBlock) void k_scan_count(const HEntry *__restrict__ tab, int64_t cap,
-                                                       int32_t *__restrict__ blk) {
-    __shared__ int red[2][kBlock / 64];
+// The four scanned quantities of one slot.
+__device__ __forceinline__ int4 slot_q(const HEntry &e) {
+    const int occ = e.key != 0ull;
+    const int cnt = occ ? e.count : 0;
+    const int parts = (cnt + kPart - 1) / kPart;
+    return make_int4(occ, cnt, parts > 1, parts > 1 ? parts : 0);
+}
+
+__device__ __forceinline__ int4 add4(int4 a, int4 b) { return make_int4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+
+// Sum over the block (every thread gets the result).
+__device__ __forceinline__ int4 block_sum4(int4 q, int4 *red) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t s0 = (int64_t)blockIdx.x * kScanSlots;
-    const int64_t s1 = s0 + kScanSlots < cap ? s0 + kScanSlots : cap;
-    int occ = 0, cnt = 0;
-    for (int64_t s = s0 + threadIdx.x; s < s1; s += kBlock) {
-        const HEntry e = tab[s];
-        occ += e.key != 0ull;
-        cnt += e.count;
-    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
-        occ += __shfl_xor(occ, off, 64);
-        cnt += __shfl_xor(cnt, off, 64);
+        q.x += __shfl_xor(q.x, off, 64);
+        q.y += __shfl_xor(q.y, off, 64);
+        q.z += __shfl_xor(q.z, off, 64);
+        q.w += __shfl_xor(q.w, off, 64);
     }
-    if (lane == 0) {
-        red[0][wave] = occ;
-        red[1][wave] = cnt;
-    }
+    if (lane == 0) red[wave] = q;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int o = 0, c = 0;
-        for (int w = 0; w < kBlock / 64; ++w) {
-            o += red[0][w];
-            c += red[1][w];
-        }
-        blk[2 * blockIdx.x] = o;
-        blk[2 * blockIdx.x + 1] = c;
+    int4 t = red[0];
+#pragma unroll
+    for (int w = 1; w < kBlock / 64; ++w) t = add4(t, red[w]);
+    __syncthreads();
+    return t;
+}
+
+// Load the kSlotsPerThread slots of thread t in a chunk starting at c0.
+__device__ __forceinline__ void load_slots(const HEntry *tab, int64_t c0, int64_t s1, HEntry *e) {
+#pragma unroll
+    for (int i = 0; i < kSlotsPerThread; ++i) {
+        const int64_t s = c0 + (int64_t)threadIdx.x * kSlotsPerThread + i;
+        e[i].key = 0ull;
+        e[i].count = 0;
+        e[i].vid = 0;
+        if (s < s1) e[i] = tab[s];
     }
 }
 
-__global__ __launch_bounds__(1024) void k_scan_blocks(int32_t *__restrict__ blk, int nb, int32_t *counters) {
-    __shared__ int wsum[2][16];
-    __shared__ int carry[2];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (threadIdx.x == 0) carry[0] = carry[1] = 0;
-    __syncthreads();
-    for (int b0 = 0; b0 < nb; b0 += 1024) {
-        const int b = b0 + threadIdx.x;
-        const int o = b < nb ? blk[2 * b] : 0;
-        const int c = b < nb ? blk[2 * b + 1] : 0;
-        const int io = wave_incl_scan(o, lane);
-        const int ic = wave_incl_scan(c, lane);
-        if (lane == 63) {
-            wsum[0][wave] = io;
-            wsum[1][wave] = ic;
-        }
-        __syncthreads();
-        int bo = carry[0], bc = carry[1];
-        for (int w = 0; w < wave; ++w) {
-            bo += wsum[0][w];
-            bc += wsum[1][w];
-        }
-        if (b < nb) {
-            blk[2 * b] = bo + io - o;
-            blk[2 * b + 1] = bc + ic - c;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            for (int w = 0; w < 16; ++w) {
-                carry[0] += wsum[0][w];
-                carry[1] += wsum[1][w];
-            }
-        }
-        __syncthreads();
+__global__ __launch_bounds__(kBlock) void k_scan_count(const HEntry *__restrict__ tab, int64_t cap, int64_t span,
+                                                       int4 *__restrict__ blk) {
+    __shared__ int4 red[kBlock / 64];
+    const int64_t s0 = (int64_t)blockIdx.x * span;
+    const int64_t s1 = s0 + span < cap ? s0 + span : cap;
+    int4 q = make_int4(0, 0, 0, 0);
+    for (int64_t c0 = s0; c0 < s1; c0 += kChunk) {
+        HEntry e[kSlotsPerThread];
+        load_slots(tab, c0, s1, e);
+#pragma unroll
+        for (int i = 0; i < kSlotsPerThread; ++i) q = add4(q, slot_q(e[i]));
     }
-    if (threadIdx.x == 0) {
-        counters[CNT_V] = carry[0];
-        counters[CNT_E] = carry[1];
-    }
+    q = block_sum4(q, red);
+    if (threadIdx.x == 0) blk[blockIdx.x] = q;
 }
 
-__global__ __launch_bounds__(kBlock) void k_scan_assign(HEntry *__restrict__ tab, int64_t cap,
-                                                        const int32_t *__restrict__ blk,
+__global__ __launch_bounds__(kBlock) void k_scan_assign(HEntry *__restrict__ tab, int64_t cap, int64_t span, int nb,
+                                                        const int4 *__restrict__ blk,
                                                         uint64_t *__restrict__ vkeys, int32_t *__restrict__ vinfo,
-                                                        int32_t *__restrict__ heavy, int32_t *counters) {
-    __shared__ int wsum[2][kBlock / 64];
-    __shared__ int carry[2];
+                                                        int32_t *__restrict__ split, int32_t *__restrict__ rowmap,
+                                                        int32_t *counters) {
+    __shared__ int4 red[kBlock / 64];
+    __shared__ int4 wsum[kBlock / 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t s0 = (int64_t)blockIdx.x * kScanSlots;
-    const int64_t s1 = s0 + kScanSlots < cap ? s0 + kScanSlots : cap;
-    if (threadIdx.x == 0) {
-        carry[0] = blk[2 * blockIdx.x];
-        carry[1] = blk[2 * blockIdx.x + 1];
+    const int64_t s0 = (int64_t)blockIdx.x * span;
+    const int64_t s1 = s0 + span < cap ? s0 + span : cap;
+    // exclusive prefix of the blocks before this one
+    int4 carry = make_int4(0, 0, 0, 0);
+    for (int b = threadIdx.x; b < (int)blockIdx.x; b += kBlock) carry = add4(carry, blk[b]);
+    carry = block_sum4(carry, red);
+    if ((int)blockIdx.x == nb - 1 && threadIdx.x == 0) {
+        const int4 tot = add4(carry, blk[blockIdx.x]);
+        counters[CNT_V] = tot.x;
+        counters[CNT_E] = tot.y;
+        counters[CNT_SPLIT] = tot.z;
+        counters[CNT_ROWS] = tot.w;
     }
-    __syncthreads();
-    for (int64_t r = s0; r < s1; r += kBlock) {
-        const int64_t s = r + threadIdx.x;
-        HEntry e;
-        e.key = 0ull;
-        e.count = 0;
-        if (s < s1) e = tab[s];
-        const int o = e.key != 0ull;
-        const int c = e.count;
-        const int io = wave_incl_scan(o, lane);
-        const int ic = wave_incl_scan(c, lane);
-        if (lane == 63) {
-            wsum[0][wave] = io;
-            wsum[1][wave] = ic;
+    for (int64_t c0 = s0; c0 < s1; c0 += kChunk) {
+        HEntry e[kSlotsPerThread];
+        load_slots(tab, c0, s1, e);
+        int4 q[kSlotsPerThread];
+        int4 mine = make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < kSlotsPerThread; ++i) {
+            q[i] = slot_q(e[i]);
+            mine = add4(mine, q[i]);
         }
+        int4 inc;
+        inc.x = wave_incl_scan(mine.x, lane);
+        inc.y = wave_incl_scan(mine.y, lane);
+        inc.z = wave_incl_scan(mine.z, lane);
+        inc.w = wave_incl_scan(mine.w, lane);
+        if (lane == 63) wsum[wave] = inc;
         __syncthreads();
-        int bo = carry[0], bc = carry[1];
-        for (int w = 0; w < wave; ++w) {
-            bo += wsum[0][w];
-            bc += wsum[1][w];
+        // exclusive prefix of this thread's first slot
+        int4 at = carry;
+        int4 chunk = make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int w = 0; w < kBlock / 64; ++w) {
+            if (w < wave) at = add4(at, wsum[w]);
+            chunk = add4(chunk, wsum[w]);
         }
-        if (o) {
-            const int v = bo + io - 1;
-            tab[s].vid = v;
-            vkeys[v] = e.key;
-            vinfo[2 * v] = bc + ic - c;
-            vinfo[2 * v + 1] = c;
-            if (c > kHeavy) heavy[atomicAdd(counters + CNT_H, 1)] = v;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            for (int w = 0; w < kBlock / 64; ++w) {
-                carry[0] += wsum[0][w];
-                carry[1] += wsum[1][w];
+        at = make_int4(at.x + inc.x - mine.x, at.y + inc.y - mine.y, at.z + inc.z - mine.z, at.w + inc.w - mine.w);
+#pragma unroll
+        for (int i = 0; i < kSlotsPerThread; ++i) {
+            if (q[i].x) {
+                const int64_t s = c0 + (int64_t)threadIdx.x * kSlotsPerThread + i;
+                const int v = at.x;
+                tab[s].vid = v;
+                vkeys[v] = e[i].key;
+                vinfo[2 * v] = at.y;
+                vinfo[2 * v + 1] = q[i].y;
+                if (q[i].z) {
+                    const int sp = at.z, row0 = at.w;
+                    split[3 * sp] = v;
+                    split[3 * sp + 1] = row0;
+                    split[3 * sp + 2] = q[i].w;
+                    for (int j = 0; j < q[i].w; ++j) rowmap[row0 + j] = sp;
+                }
             }
+            at = add4(at, q[i]);
         }
-        __syncthreads();
+        carry = add4(carry, chunk);
+        __syncthreads();  // wsum is rewritten by the next chunk
     }
 }
 
@@ -415,11 +425,6 @@ __global__ __launch_bounds__(kBlock) void k_fill(int64_t n, int32_t *__restrict_
     }
 }
 
-// Eq. (splat), pulled per vertex: x_v = sum over the vertex's pair list of
-// b_pv f_p, and w_v = sum b_pv.  G lanes per vertex own float4 column chunks;
-// every row of `values` is written exactly once (no zero fill, no float
-// atomics).  Four list entries are fetched before their feature rows are
-// used, to keep several row gathers in flight per lane.
 // Store 4 (VEC) or 1 value of a vertex row as fp32 or bf16 (nearest even).
 template <bool OUT_BF16>
 __device__ __forceinline__ void store4(void *values, int64_t at4, float4 a) {
@@ -440,169 +445,177 @@ __device__ __forceinline__ void store1(void *values, int64_t at, float a) {
         reinterpret_cast<float *>(values)[at] = a;
 }
 
+__device__ __forceinline__ float4 fma4(float b, float4 y, float4 acc) {
+    acc.x = fmaf(b, y.x, acc.x);
+    acc.y = fmaf(b, y.y, acc.y);
+    acc.z = fmaf(b, y.z, acc.z);
+    acc.w = fmaf(b, y.w, acc.w);
+    return acc;
+}
+
+// Sum b f over list entries [e0, e1) for float4 column c (VEC) or column c.
+template <bool VEC>
+__device__ __forceinline__ float4 sum_pairs(const int2 *__restrict__ L2, int e0, int e1, const float *__restrict__ feat,
+                                            int CV, int c) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (VEC) {
+        const float4 *f4 = reinterpret_cast<const float4 *>(feat);
+        int e = e0;
+        for (; e + 4 <= e1; e += 4) {
+            const int2 q0 = L2[e], q1 = L2[e + 1], q2 = L2[e + 2], q3 = L2[e + 3];
+            const float4 y0 = f4[(int64_t)q0.x * CV + c], y1 = f4[(int64_t)q1.x * CV + c];
+            const float4 y2 = f4[(int64_t)q2.x * CV + c], y3 = f4[(int64_t)q3.x * CV + c];
+            acc = fma4(__int_as_float(q0.y), y0, acc);
+            acc = fma4(__int_as_float(q1.y), y1, acc);
+            acc = fma4(__int_as_float(q2.y), y2, acc);
+            acc = fma4(__int_as_float(q3.y), y3, acc);
+        }
+        for (; e < e1; ++e) {
+            const int2 q = L2[e];
+            acc = fma4(__int_as_float(q.y), f4[(int64_t)q.x * CV + c], acc);
+        }
+    } else {
+        for (int e = e0; e < e1; ++e) {
+            const int2 q = L2[e];
+            acc.x = fmaf(__int_as_float(q.y), feat[(int64_t)q.x * CV + c], acc.x);
+        }
+    }
+    return acc;
+}
+
+template <bool VEC>
+__device__ __forceinline__ float4 scale4(float4 a, float w, int normalize) {
+    if (!normalize) return a;
+    a.x = w != 0.f ? a.x / w : 0.f;
+    if (VEC) {
+        a.y = w != 0.f ? a.y / w : 0.f;
+        a.z = w != 0.f ? a.z / w : 0.f;
+        a.w = w != 0.f ? a.w / w : 0.f;
+    }
+    return a;
+}
+
+// Eq. (splat), pulled per vertex: x_v = sum over the vertex's pair list of
+// b_pv f_p, and w_v = sum b_pv.  Work units are groups of G lanes, each lane
+// owning float4 (VEC) or single column chunks.
+//   Phase 1: a vertex with at most kPart pairs is one unit: its row is summed
+//            and written once (no zero fill, no float atomics).
+//   Phase 2: a longer list is cut into parts of kPart pairs, one unit each,
+//            so that dense regions (thousands of points on one vertex near a
+//            LiDAR sensor) do not serialise on one group.  A part writes its
+//            partial row (and partial weight) to scratch; k_gather_combine
+//            adds them in part order.  (Combining in the last part to finish
+//            would need a device-scope release per part, which costs more
+//            than the extra launch: every XCD has its own L2.)
 template <bool VEC, bool OUT_BF16>
 __global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ vinfo, const int32_t *__restrict__ list,
-                                                   const float *__restrict__ feat, int C, int log2G, int normalize,
-                                                   void *__restrict__ values, float *__restrict__ weight,
-                                                   const int32_t *counters) {
+                                                   const int32_t *__restrict__ split,
+                                                   const int32_t *__restrict__ rowmap, float *__restrict__ partial,
+                                                   float *__restrict__ pweight, const float *__restrict__ feat,
+                                                   int C, int log2G, int normalize, void *__restrict__ values,
+                                                   float *__restrict__ weight, const int32_t *counters) {
     const int64_t V = counters[CNT_V];
+    const int64_t nrows = counters[CNT_ROWS];
     const int G = 1 << log2G;
     const int lane = threadIdx.x & 63;
     const int grp = lane >> log2G;
     const int j = lane & (G - 1);
-    const int vpw = 64 >> log2G;
+    const int gpw = 64 >> log2G;  // groups per wave
     const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
     const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
-    const int CV = VEC ? (C >> 2) : C;  // columns in units of float4 (VEC) or float
-    for (int64_t v0 = wave * vpw; v0 < V; v0 += nwaves * vpw) {
+    const int CV = VEC ? (C >> 2) : C;
+    const int2 *L2 = reinterpret_cast<const int2 *>(list);
+
+    // Phase 1: short lists.
+    for (int64_t v0 = wave * gpw; v0 < V; v0 += nwaves * gpw) {
         const int64_t v = v0 + grp;
         if (v >= V) continue;
         const int off = vinfo[2 * v];
         const int cnt = vinfo[2 * v + 1];
-        if (cnt > kHeavy) continue;  // reduced by k_gather_heavy
-        const int2 *L2 = reinterpret_cast<const int2 *>(list) + off;
+        if (cnt > kPart) continue;  // phase 2
         float w = 0.f;
-        for (int e = 0; e < cnt; ++e) w += __int_as_float(L2[e].y);
+        for (int e = off; e < off + cnt; ++e) w += __int_as_float(L2[e].y);
         for (int c = j; c < CV; c += G) {
-            if (VEC) {
-                const float4 *f4 = reinterpret_cast<const float4 *>(feat);
-                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                int e = 0;
-                for (; e + 4 <= cnt; e += 4) {
-                    const int2 q0 = L2[e], q1 = L2[e + 1], q2 = L2[e + 2], q3 = L2[e + 3];
-                    const float4 y0 = f4[(int64_t)q0.x * CV + c], y1 = f4[(int64_t)q1.x * CV + c];
-                    const float4 y2 = f4[(int64_t)q2.x * CV + c], y3 = f4[(int64_t)q3.x * CV + c];
-                    const float b0 = __int_as_float(q0.y), b1 = __int_as_float(q1.y);
-                    const float b2 = __int_as_float(q2.y), b3 = __int_as_float(q3.y);
-                    acc.x = fmaf(b0, y0.x, acc.x); acc.y = fmaf(b0, y0.y, acc.y);
-                    acc.z = fmaf(b0, y0.z, acc.z); acc.w = fmaf(b0, y0.w, acc.w);
-                    acc.x = fmaf(b1, y1.x, acc.x); acc.y = fmaf(b1, y1.y, acc.y);
-                    acc.z = fmaf(b1, y1.z, acc.z); acc.w = fmaf(b1, y1.w, acc.w);
-                    acc.x = fmaf(b2, y2.x, acc.x); acc.y = fmaf(b2, y2.y, acc.y);
-                    acc.z = fmaf(b2, y2.z, acc.z); acc.w = fmaf(b2, y2.w, acc.w);
-                    acc.x = fmaf(b3, y3.x, acc.x); acc.y = fmaf(b3, y3.y, acc.y);
-                    acc.z = fmaf(b3, y3.z, acc.z); acc.w = fmaf(b3, y3.w, acc.w);
-                }
-                for (; e < cnt; ++e) {
-                    const int2 q = L2[e];
-                    const float4 y = f4[(int64_t)q.x * CV + c];
-                    const float bq = __int_as_float(q.y);
-                    acc.x = fmaf(bq, y.x, acc.x); acc.y = fmaf(bq, y.y, acc.y);
-                    acc.z = fmaf(bq, y.z, acc.z); acc.w = fmaf(bq, y.w, acc.w);
-                }
-                if (normalize) {
-                    acc.x = w != 0.f ? acc.x / w : 0.f;
-                    acc.y = w != 0.f ? acc.y / w : 0.f;
-                    acc.z = w != 0.f ? acc.z / w : 0.f;
-                    acc.w = w != 0.f ? acc.w / w : 0.f;
-                }
+            const float4 acc = scale4<VEC>(sum_pairs<VEC>(L2, off, off + cnt, feat, CV, c), w, normalize);
+            if (VEC)
                 store4<OUT_BF16>(values, v * CV + c, acc);
-            } else {
-                float acc = 0.f;
-                for (int e = 0; e < cnt; ++e) {
-                    const int2 q = L2[e];
-                    acc = fmaf(__int_as_float(q.y), feat[(int64_t)q.x * C + c], acc);
-                }
-                if (normalize) acc = w != 0.f ? acc / w : 0.f;
-                store1<OUT_BF16>(values, v * C + c, acc);
-            }
+            else
+                store1<OUT_BF16>(values, v * C + c, acc.x);
         }
         if (weight && j == 0) weight[v] = w;
     }
+
+    // Phase 2: parts of long lists.
+    for (int64_t u0 = wave * gpw; u0 < nrows; u0 += nwaves * gpw) {
+        const int64_t u = u0 + grp;
+        const bool live = u < nrows;
+        int sp = 0, v = 0, row0 = 0, parts = 1, off = 0, cnt = 0, e0 = 0, e1 = 0;
+        if (live) {
+            sp = rowmap[u];
+            v = split[3 * sp];
+            row0 = split[3 * sp + 1];
+            parts = split[3 * sp + 2];
+            off = vinfo[2 * v];
+            cnt = vinfo[2 * v + 1];
+            const int part = (int)(u - row0);
+            e0 = off + part * kPart;
+            e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
+            float w = 0.f;
+            for (int e = e0; e < e1; ++e) w += __int_as_float(L2[e].y);
+            for (int c = j; c < CV; c += G) {
+                const float4 acc = sum_pairs<VEC>(L2, e0, e1, feat, CV, c);
+                if (VEC)
+                    reinterpret_cast<float4 *>(partial)[u * CV + c] = acc;
+                else
+                    partial[u * C + c] = acc.x;
+            }
+            if (j == 0) pweight[u] = w;
+        }
+    }
 }
 
-// Vertices with more than kHeavy pairs (dense regions, e.g. near a LiDAR
-// sensor): one workgroup of kHeavyBlock threads per vertex.  Groups of G
-// lanes (one float4 or float column each) take the pairs in a strided order,
-// partial sums meet in LDS, and the first group writes the row.
-// Deterministic for a given list order.
-constexpr int kHeavyBlock = 1024;
-
+// Rows of the vertices whose lists k_gather summed in parts: the parts are
+// added in part order, then scaled and stored like a phase-1 row.
 template <bool VEC, bool OUT_BF16>
-__global__ __launch_bounds__(kHeavyBlock) void k_gather_heavy(const int32_t *__restrict__ heavy,
-                                                              const int32_t *__restrict__ vinfo,
-                                                              const int32_t *__restrict__ list,
-                                                              const float *__restrict__ feat, int C, int log2G,
-                                                              int normalize, void *__restrict__ values,
-                                                              float *__restrict__ weight, const int32_t *counters) {
-    __shared__ float4 red[kHeavyBlock];
-    __shared__ float wred[kHeavyBlock];
-    const int nheavy = counters[CNT_H];
+__global__ __launch_bounds__(kBlock) void k_gather_combine(const int32_t *__restrict__ split, const float *partial,
+                                                           const float *pweight, int C, int log2G, int normalize,
+                                                           void *__restrict__ values, float *__restrict__ weight,
+                                                           const int32_t *counters) {
+    const int64_t ns = counters[CNT_SPLIT];
     const int G = 1 << log2G;
-    const int ngroups = kHeavyBlock >> log2G;
-    const int grp = threadIdx.x >> log2G;
-    const int j = threadIdx.x & (G - 1);
+    const int lane = threadIdx.x & 63;
+    const int grp = lane >> log2G;
+    const int j = lane & (G - 1);
+    const int gpw = 64 >> log2G;
+    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
     const int CV = VEC ? (C >> 2) : C;
-    for (int h = blockIdx.x; h < nheavy; h += gridDim.x) {
-        const int v = heavy[h];
-        const int off = vinfo[2 * v];
-        const int cnt = vinfo[2 * v + 1];
-        const int2 *L2 = reinterpret_cast<const int2 *>(list) + off;
+    for (int64_t s0 = wave * gpw; s0 < ns; s0 += nwaves * gpw) {
+        const int64_t sp = s0 + grp;
+        if (sp >= ns) continue;
+        const int v = split[3 * sp], row0 = split[3 * sp + 1], parts = split[3 * sp + 2];
         float w = 0.f;
-        for (int e = grp; e < cnt; e += ngroups) w += __int_as_float(L2[e].y);
-        wred[threadIdx.x] = w;
-        __syncthreads();
-        float wt = 0.f;
-        for (int g = 0; g < ngroups; ++g) wt += wred[g * G];
-        for (int c0 = 0; c0 < CV; c0 += G) {
-            const int c = c0 + j;
-            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (c < CV) {
+        for (int r = 0; r < parts; ++r) w += pweight[row0 + r];
+        for (int c = j; c < CV; c += G) {
+            float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int r = 0; r < parts; ++r) {
                 if (VEC) {
-                    const float4 *f4 = reinterpret_cast<const float4 *>(feat);
-                    int e = grp;
-                    for (; e + 3 * ngroups < cnt; e += 4 * ngroups) {
-                        const int2 q0 = L2[e], q1 = L2[e + ngroups], q2 = L2[e + 2 * ngroups], q3 = L2[e + 3 * ngroups];
-                        const float4 y0 = f4[(int64_t)q0.x * CV + c], y1 = f4[(int64_t)q1.x * CV + c];
-                        const float4 y2 = f4[(int64_t)q2.x * CV + c], y3 = f4[(int64_t)q3.x * CV + c];
-                        const float b0 = __int_as_float(q0.y), b1 = __int_as_float(q1.y);
-                        const float b2 = __int_as_float(q2.y), b3 = __int_as_float(q3.y);
-                        acc.x = fmaf(b0, y0.x, acc.x); acc.y = fmaf(b0, y0.y, acc.y);
-                        acc.z = fmaf(b0, y0.z, acc.z); acc.w = fmaf(b0, y0.w, acc.w);
-                        acc.x = fmaf(b1, y1.x, acc.x); acc.y = fmaf(b1, y1.y, acc.y);
-                        acc.z = fmaf(b1, y1.z, acc.z); acc.w = fmaf(b1, y1.w, acc.w);
-                        acc.x = fmaf(b2, y2.x, acc.x); acc.y = fmaf(b2, y2.y, acc.y);
-                        acc.z = fmaf(b2, y2.z, acc.z); acc.w = fmaf(b2, y2.w, acc.w);
-                        acc.x = fmaf(b3, y3.x, acc.x); acc.y = fmaf(b3, y3.y, acc.y);
-                        acc.z = fmaf(b3, y3.z, acc.z); acc.w = fmaf(b3, y3.w, acc.w);
-                    }
-                    for (; e < cnt; e += ngroups) {
-                        const int2 q = L2[e];
-                        const float4 y = f4[(int64_t)q.x * CV + c];
-                        const float bq = __int_as_float(q.y);
-                        acc.x = fmaf(bq, y.x, acc.x); acc.y = fmaf(bq, y.y, acc.y);
-                        acc.z = fmaf(bq, y.z, acc.z); acc.w = fmaf(bq, y.w, acc.w);
-                    }
+                    const float4 a = reinterpret_cast<const float4 *>(partial)[(int64_t)(row0 + r) * CV + c];
+                    t.x += a.x;
+                    t.y += a.y;
+                    t.z += a.z;
+                    t.w += a.w;
                 } else {
-                    for (int e = grp; e < cnt; e += ngroups) {
-                        const int2 q = L2[e];
-                        acc.x = fmaf(__int_as_float(q.y), feat[(int64_t)q.x * C + c], acc.x);
-                    }
+                    t.x += partial[(int64_t)(row0 + r) * C + c];
                 }
             }
-            red[threadIdx.x] = acc;
-            __syncthreads();
-            if (grp == 0 && c < CV) {
-                float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
-                for (int g = 0; g < ngroups; ++g) {
-                    const float4 r = red[g * G + j];
-                    t.x += r.x; t.y += r.y; t.z += r.z; t.w += r.w;
-                }
-                if (normalize) {
-                    t.x = wt != 0.f ? t.x / wt : 0.f;
-                    t.y = wt != 0.f ? t.y / wt : 0.f;
-                    t.z = wt != 0.f ? t.z / wt : 0.f;
-                    t.w = wt != 0.f ? t.w / wt : 0.f;
-                }
-                if (VEC)
-                    store4<OUT_BF16>(values, (int64_t)v * CV + c, t);
-                else
-                    store1<OUT_BF16>(values, (int64_t)v * C + c, t.x);
-            }
-            __syncthreads();
+            t = scale4<VEC>(t, w, normalize);
+            if (VEC)
+                store4<OUT_BF16>(values, (int64_t)v * CV + c, t);
+            else
+                store1<OUT_BF16>(values, (int64_t)v * C + c, t.x);
         }
-        if (weight && threadIdx.x == 0) weight[v] = wt;
-        __syncthreads();
+        if (weight && j == 0) weight[v] = w;
     }
 }
 
@@ -668,20 +681,29 @@ hipError_t launch_insert(lattice *L, const float *pos, const int32_t *batch, int
     });
 }
 
-int64_t scan_blocks(const lattice *L) { return (L->cap + kScanSlots - 1) / kScanSlots; }
+static int64_t scan_span(const lattice *L) {
+    const int64_t per = (L->cap + kMaxScanBlocks - 1) / kMaxScanBlocks;
+    return per > kChunk ? (per + kChunk - 1) / kChunk * kChunk : kChunk;
+}
+
+int64_t scan_blocks_max() { return kMaxScanBlocks; }
 
 hipError_t launch_number(lattice *L) {
-    const int64_t nb = scan_blocks(L);
-    hipLaunchKernelGGL(k_scan_count, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->blk);
+    const int64_t span = scan_span(L);
+    const int64_t nb = (L->cap + span - 1) / span;
+    int4 *blk = reinterpret_cast<int4 *>(L->blk);
+    hipLaunchKernelGGL(k_scan_count, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->tab, L->cap, span, blk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, L->stream, L->blk, (int)nb, L->counters);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_scan_assign, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->blk,
-                       L->vkeys, L->vinfo, L->heavy, L->counters);
+    hipLaunchKernelGGL(k_scan_assign, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->tab, L->cap, span, (int)nb,
+                       blk, L->vkeys, L->vinfo, L->split, L->rowmap, L->counters);
     return hipGetLastError();
 }
+
+// Bound on the part rows of one splat: a split list has cnt > kPart pairs and
+// ceil(cnt / kPart) < 2 cnt / kPart parts, and the lists hold at most
+// (d+1) m pairs.  The number of split vertices is below that too.
+int64_t split_rows_max(const lattice *L) { return 2 * (L->d + 1) * L->max_points / kPart + 1; }
 
 hipError_t launch_fill(lattice *L, int64_t m) {
     if (m == 0) return hipSuccess;
@@ -702,26 +724,26 @@ static hipError_t gather_typed(lattice *L, const float *feat, int C, int normali
     const int lanes = vec ? C / 4 : (C > 0 ? C : 1);
     int log2G = 0;
     while ((1 << log2G) < lanes && log2G < 6) ++log2G;
-    const int64_t vpw = 64 >> log2G;
-    const int64_t waves = (L->max_vertices + vpw - 1) / vpw;
+    const int64_t gpw = 64 >> log2G;
+    const int64_t waves = (L->max_vertices + gpw - 1) / gpw;
     const unsigned grid = grid_for(waves * 64, kBlock, L->cu_count, 16);
     if (vec)
-        hipLaunchKernelGGL((k_gather<true, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list, feat,
-                           C, log2G, normalize, values, weight, L->counters);
+        hipLaunchKernelGGL((k_gather<true, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
+                           L->split, L->rowmap, L->partial, L->pweight, feat, C, log2G, normalize, values,
+                           weight, L->counters);
     else
-        hipLaunchKernelGGL((k_gather<false, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list, feat,
-                           C, log2G, normalize, values, weight, L->counters);
+        hipLaunchKernelGGL((k_gather<false, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
+                           L->split, L->rowmap, L->partial, L->pweight, feat, C, log2G, normalize, values,
+                           weight, L->counters);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // heavy vertices: G = lanes per column group, at most 64, so that a
-    // workgroup has at least 16 groups splitting each long pair list
-    const unsigned hgrid = (unsigned)(L->cu_count * 2);
+    const unsigned g2 = grid_for(split_rows_max(L) * 64, kBlock, L->cu_count, 2);
     if (vec)
-        hipLaunchKernelGGL((k_gather_heavy<true, OUT_BF16>), dim3(hgrid), dim3(kHeavyBlock), 0, L->stream, L->heavy,
-                           L->vinfo, L->list, feat, C, log2G, normalize, values, weight, L->counters);
+        hipLaunchKernelGGL((k_gather_combine<true, OUT_BF16>), dim3(g2), dim3(kBlock), 0, L->stream, L->split,
+                           L->partial, L->pweight, C, log2G, normalize, values, weight, L->counters);
     else
-        hipLaunchKernelGGL((k_gather_heavy<false, OUT_BF16>), dim3(hgrid), dim3(kHeavyBlock), 0, L->stream, L->heavy,
-                           L->vinfo, L->list, feat, C, log2G, normalize, values, weight, L->counters);
+        hipLaunchKernelGGL((k_gather_combine<false, OUT_BF16>), dim3(g2), dim3(kBlock), 0, L->stream, L->split,
+                           L->partial, L->pweight, C, log2G, normalize, values, weight, L->counters);
     return hipGetLastError();
 }
 

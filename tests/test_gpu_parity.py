@@ -54,6 +54,53 @@ def test_splat_parity(d, m, sigma, C):
     assert_close_scaled(g.weight(), wref, wref, REL_F32, "splat weight")
 
 
+def _clustered_cloud(seed, C, m_dense=6000, m_sparse=3000):
+    """A few tight clusters (vertices hit by thousands of points) plus a
+    sparse background (short pair lists), so that one splat exercises both
+    the per-vertex and the split-list gather."""
+    rng = np.random.default_rng(seed)
+    centres = rng.uniform(-0.8, 0.8, size=(3, 3))
+    dense = centres[rng.integers(0, 3, m_dense)] + rng.normal(0, 0.01, size=(m_dense, 3))
+    sparse = rng.uniform(-1, 1, size=(m_sparse, 3))
+    pos = np.concatenate([dense, sparse]).astype(np.float32)[rng.permutation(m_dense + m_sparse)]
+    feat = rng.standard_normal((pos.shape[0], C)).astype(np.float32)
+    return pos, feat
+
+
+@pytest.mark.parametrize("C,values_dtype,normalize", [(3, "f32", False), (64, "f32", False), (64, "bf16", False),
+                                                      (128, "f32", True), (520, "f32", False), (0, "f32", False)])
+def test_splat_long_pair_lists(C, values_dtype, normalize):
+    """Vertices with up to thousands of (point, vertex) pairs: their lists are
+    summed in parts and combined by the last part; the result must not depend
+    on that split.  Two splats in a row on one lattice (the second smaller)
+    check that no per-split state leaks from the first."""
+    sigma = 0.1
+    L = _lattice(3, sigma, 9000)
+    for rep, (md, ms) in enumerate([(6000, 3000), (2500, 700)]):
+        pos, feat = _clustered_cloud(40 + rep, max(C, 1), md, ms)
+        feat_in = to_dev(feat) if C > 0 else None
+        vals, wt = L.splat(to_dev(pos), feat_in, normalize=normalize, values_dtype=values_dtype,
+                           want_weight=True)
+        V = L.num_vertices()
+        keys = L.keys().cpu().numpy().astype(np.int64)
+        from tests.gpu_util import canonical_perm
+        perm, rank = canonical_perm(keys, None, 3)
+        lat = O.build(pos, sigma)
+        assert V == lat.V
+        counts = np.bincount(lat.idx.reshape(-1), minlength=lat.V)
+        assert counts.max() > 500 and (counts > 32).sum() >= 3 and (counts <= 32).sum() > 100
+        ref, wref, scale = O.splat(lat, feat, normalize=normalize)
+        gw = wt[:V].cpu().numpy().astype(np.float64)[perm]
+        assert_close_scaled(gw, wref, wref, REL_F32, "split-list weight")
+        if C == 0:
+            continue
+        got = vals[:V].float().cpu().numpy().astype(np.float64)[perm]
+        tol = (2 if normalize else 1) * REL_F32 * scale
+        if values_dtype == "bf16":
+            tol = tol + BF16_ULP * np.abs(ref)
+        assert_close_scaled(got, ref, tol, 1.0, f"split-list splat C={C} rep={rep}")
+
+
 def test_splat_normalized_parity():
     w = random_cloud(4000, 3, seed=7, extent=1.0, C=6)
     L = _lattice(3, 0.12, w.m)
