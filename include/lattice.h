@@ -186,6 +186,23 @@ lattice_status lattice_conv(lattice *L, const void *in, lattice_dtype in_dtype, 
                             lattice_dtype out_dtype);
 
 /*
+ * lattice_set_conv_path -- choose the kernel family of later lattice_conv
+ * calls (the result is the same to the stated tolerances; this is for
+ * testing and benchmarking each kernel).
+ *   LATTICE_CONV_AUTO    the fastest kernel built for the shape (default)
+ *   LATTICE_CONV_TILED   the LDS-tiled kernel (weights and gathered rows
+ *                        staged per K chunk), else the generic one
+ *   LATTICE_CONV_WS      weight slice resident in LDS, rows gathered straight
+ *                        into registers, where built for the shape; else TILED
+ *   LATTICE_CONV_RS      weights resident in registers, rows gathered into
+ *                        LDS by direct loads (bf16 rows and weights, shapes
+ *                        it is built for); else as AUTO without it
+ * Returns LATTICE_E_ARG for another value.
+ */
+enum { LATTICE_CONV_AUTO = 0, LATTICE_CONV_TILED = 1, LATTICE_CONV_WS = 2, LATTICE_CONV_RS = 3 };
+lattice_status lattice_set_conv_path(lattice *L, int path);
+
+/*
  * lattice_slice -- interpolate vertex values back onto the points.
  *
  * Eq. (slice):  f_p = sum_{v in I_p} b_pv x_v, with the barycentric weights

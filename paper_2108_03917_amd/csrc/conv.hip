@@ -286,27 +286,62 @@ __global__ __launch_bounds__(512) void k_conv_ws(const void *__restrict__ in, co
     const int64_t V = counters[CNT_V];
     const int64_t n_mt = (V + 31) / 32;
 
-    // W slice -> LDS, once.
+    // W slice -> LDS, once: every load of the slice is issued before the
+    // first store so that their latencies overlap (a load-store loop would
+    // wait out one latency per 8 KB).  The first tile's neighbour indices
+    // are fetched in the same window.
+    const int64_t wave0 = (int64_t)(blockIdx.x / n_nt) * NW + wave;
+    const int64_t nwaves = (int64_t)(gridDim.x / n_nt) * NW;
+    int nbn[T];
+    {
+        const int64_t row = wave0 * 32 + lrow;
+        const bool live = row < V;
+#pragma unroll
+        for (int t = 0; t < T; ++t) nbn[t] = live ? nbr[row * T + t] : -1;
+    }
     {
         constexpr int SEGS = K * WESZ / 16;
+        constexpr int TOTAL = BN * SEGS;
+        constexpr int PER = (TOTAL + NW * 64 - 1) / (NW * 64);
         const char *src = reinterpret_cast<const char *>(wv) + (int64_t)col_base * K * WESZ;
-        for (int i = tid; i < BN * SEGS; i += NW * 64) {
-            const int n = i / SEGS, sg = i - n * SEGS;
-            *reinterpret_cast<u32x4_t *>(wlds + n * KSTRIDE + sg * 16) =
-                *reinterpret_cast<const u32x4_t *>(src + (int64_t)n * K * WESZ + sg * 16);
+        u32x4_t wr[PER];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int i = tid + q * NW * 64;
+            if (i < TOTAL) {
+                const int n = i / SEGS, sg = i - n * SEGS;
+                wr[q] = *reinterpret_cast<const u32x4_t *>(src + (int64_t)n * K * WESZ + sg * 16);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int i = tid + q * NW * 64;
+            if (i < TOTAL) {
+                const int n = i / SEGS, sg = i - n * SEGS;
+                *reinterpret_cast<u32x4_t *>(wlds + n * KSTRIDE + sg * 16) = wr[q];
+            }
         }
     }
     __syncthreads();
 
-    const int64_t wave0 = (int64_t)(blockIdx.x / n_nt) * NW + wave;
-    const int64_t nwaves = (int64_t)(gridDim.x / n_nt) * NW;
     for (int64_t mt = wave0; mt < n_mt; mt += nwaves) {
-        const int64_t row = mt * 32 + lrow;
-        const bool live = row < V;
-        const int64_t rowc = live ? row : 0;
+        // With up to two accumulator blocks, this tile's neighbour indices
+        // were fetched before it and the next tile's are fetched now; four
+        // blocks leave too few registers for that.
         int nb[T];
+        if constexpr (CB < 4) {
 #pragma unroll
-        for (int t = 0; t < T; ++t) nb[t] = live ? nbr[rowc * T + t] : -1;
+            for (int t = 0; t < T; ++t) nb[t] = nbn[t];
+            const int64_t row = (mt + nwaves) * 32 + lrow;
+            const bool live = row < V;
+#pragma unroll
+            for (int t = 0; t < T; ++t) nbn[t] = live ? nbr[row * T + t] : -1;
+        } else {
+            const int64_t row = mt * 32 + lrow;
+            const bool live = row < V;
+#pragma unroll
+            for (int t = 0; t < T; ++t) nb[t] = live ? nbr[row * T + t] : -1;
+        }
 
         f32x16_t acc[CB];
 #pragma unroll
@@ -389,6 +424,245 @@ __global__ __launch_bounds__(512) void k_conv_ws(const void *__restrict__ in, co
                     else
                         reinterpret_cast<float *>(out)[orow * C_out + col] = y;
                 }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_conv_rs: bf16 rows and weights, weights resident in registers.
+//
+// A gather in MFMA operand layout puts 32 different rows in one 64-lane load
+// (each lane 16 bytes), which the address unit serves one lane per cycle.
+// Here the gathered rows travel instead by direct-to-LDS loads in row order
+// (consecutive lanes read consecutive 16-byte chunks of a row, so a load is
+// a few full cache lines), into a two-tile LDS ring; the MFMA operand is
+// then read from LDS.  Each of the four wavefronts owns 32 output columns
+// and keeps their whole K x 32 weight slice in registers for the life of
+// the workgroup, so the weights cost neither LDS bandwidth nor address-unit
+// cycles after the prologue; with C_out = 64 two wavefronts share a column
+// group and split the rows.
+//
+// Per tile of MT rows (MT = 32 * 4 / (C_out / 32)):
+//   top:   wait for this tile's loads, barrier
+//          issue the next tile's row loads (addresses from its neighbour
+//          block, already in LDS) and the neighbour block of the tile after
+//          that
+//   body:  T taps x C_in/16 k-groups of ds_read + MFMA 32x32x16
+//   store: bias, fp32 or bf16
+// A missing neighbour (index -1) and the rows past V of the last tile read
+// a zero row.  16-byte chunk c of tile row r sits at chunk c ^ (r % 8) of
+// the row's LDS slot (and weight row n likewise with n % 8), so that the
+// 32-row operand reads spread over the LDS banks.
+namespace rs {
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void dma16(const void *src, char *lds_wave_base) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void *)lds_wave_base, 16, 0, 0);
+}
+
+// Wait for every outstanding memory operation of this wavefront (the
+// direct-to-LDS loads included), then the workgroup barrier.  The memory
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void drain_and_barrier() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+}  // namespace rs
+
+template <int C_IN, int C_OUT, int T>
+struct RsShape {
+    static constexpr int NW = 4;
+    static constexpr int NCG = C_OUT / 32;                 // column groups
+    static constexpr int NRG = NW / NCG;                   // row groups
+    static constexpr int MT = 32 * NRG;                    // rows per tile
+    static constexpr int K = T * C_IN;
+    static constexpr int KG = K / 16;                      // k-groups (one MFMA each)
+    static constexpr int GPT = C_IN / 16;                  // k-groups per tap
+    static constexpr int CPR = C_IN / 8;                   // 16-byte chunks per row
+    static constexpr int SLICE = MT * CPR;                 // chunks of one tap
+    static constexpr int TILE = T * SLICE;                 // chunks of one tile
+    static constexpr int TILE_BYTES = TILE * 16;
+    static constexpr int ADMA = TILE / (64 * NW);          // row loads per wavefront per tile
+    static constexpr int NB_INTS = MT * T;                 // neighbour block of a tile
+    static constexpr int NB_DMA = (NB_INTS * 4 + 1023) / 1024;
+    static constexpr int NB_BYTES = NB_DMA * 1024;
+    static constexpr int WCPR = K / 8;                     // chunks per weight row
+    static constexpr int W_ROWS_ROUND = (2 * TILE_BYTES) / (WCPR * 16) < C_OUT ? (2 * TILE_BYTES) / (WCPR * 16) : C_OUT;
+    static constexpr int W_ROUNDS = C_OUT / W_ROWS_ROUND;
+    static constexpr int W_DMA = W_ROWS_ROUND * WCPR / (64 * NW);  // weight loads per wavefront per round
+    static constexpr int LDS = 2 * TILE_BYTES + 2 * NB_BYTES;
+    static constexpr int PD = GPT >= 8 ? 1 : 2;            // operand read-ahead, in taps
+    static constexpr int DPT = ADMA / T;                   // row loads issued per tap
+    static_assert(DPT * T == ADMA, "row loads per tap");
+    static_assert(NCG * NRG == NW, "column groups");
+    static_assert(TILE % (64 * NW) == 0, "tile loads");
+    static_assert(CPR >= 8 && WCPR % 8 == 0, "swizzle");
+    static_assert(NB_DMA <= NW && NB_INTS % 4 == 0, "neighbour block");
+    static_assert(W_ROWS_ROUND % 32 == 0 && C_OUT % W_ROWS_ROUND == 0, "weight rounds");
+    static_assert((W_ROWS_ROUND * WCPR) % (64 * NW) == 0, "weight loads");
+    static_assert(LDS <= 160 * 1024, "LDS");
+};
+
+template <bool OUT_BF16, int T, int C_IN, int C_OUT>
+__global__ __launch_bounds__(256) void k_conv_rs(const uint16_t *__restrict__ in, const uint16_t *__restrict__ w,
+                                                 const float *__restrict__ bias, void *__restrict__ out,
+                                                 const int32_t *__restrict__ nbr, int64_t nbr_ints,
+                                                 const int32_t *__restrict__ counters,
+                                                 const uint16_t *__restrict__ zero_row) {
+    using S = RsShape<C_IN, C_OUT, T>;
+    extern __shared__ __attribute__((aligned(16))) char lds[];
+    auto abuf = [&](int b) { return lds + b * S::TILE_BYTES; };                      // row tiles
+    auto nbuf = [&](int b) { return lds + 2 * S::TILE_BYTES + b * S::NB_BYTES; };    // neighbour blocks
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l32 = lane & 31;
+    const int h = lane >> 5;
+    const int cg = wave % S::NCG;
+    const int rg = wave / S::NCG;
+    const int64_t V = counters[CNT_V];
+    const int64_t n_tiles = (V + S::MT - 1) / S::MT;
+    const int64_t tile0 = blockIdx.x;
+    const int64_t tstride = gridDim.x;
+    if (tile0 >= n_tiles) return;  // uniform over the workgroup
+
+    // Neighbour block of tile k -> nbuf(b): NB_INTS contiguous ints, one
+    // 1 KB load per wavefront for the first NB_DMA wavefronts; chunks past
+    // the block or past the buffer re-read an in-bounds chunk.
+    auto load_nbr = [&](int64_t k, int b) {
+        if (wave < S::NB_DMA) {
+            const int64_t j = (int64_t)wave * 64 + lane;
+            const int64_t last = (nbr_ints / 4 - 1) * 4;  // last whole 16-byte chunk of the table
+            int64_t at = k * S::NB_INTS + 4 * j;
+            if (4 * j >= S::NB_INTS) at = k * S::NB_INTS;
+            if (at > last) at = last;
+            rs::dma16(nbr + at, nbuf(b) + wave * 1024);
+        }
+    };
+    // Rows of tile k -> abuf(b).  A wavefront's ADMA loads are issued DPT
+    // per tap between the MFMAs of the current tile, so that the address
+    // unit drains them while the matrix cores work; the neighbour indices of
+    // tap t's loads are read from nbuf(b) one tap earlier (a direct-to-LDS
+    // load is not reordered with LDS reads, so reading an index right before
+    // its load would wait out the LDS latency).
+    auto read_nb = [&](int b, int t, int *u) {
+        const int32_t *nb = reinterpret_cast<const int32_t *>(nbuf(b));
+#pragma unroll
+        for (int i = 0; i < S::DPT; ++i) {
+            const int q = (wave * S::ADMA + t * S::DPT + i) * 64 + lane;
+            const int tt = q / S::SLICE;
+            const int r = (q - tt * S::SLICE) / S::CPR;
+            u[i] = nb[r * T + tt];
+        }
+    };
+    auto issue_rows = [&](int64_t k, int b, int t, const int *u) {
+        const int rows_left = (int)(V - k * S::MT < S::MT ? V - k * S::MT : S::MT);
+#pragma unroll
+        for (int i = 0; i < S::DPT; ++i) {
+            const int a = t * S::DPT + i;
+            const int q = (wave * S::ADMA + a) * 64 + lane;
+            const int tt = q / S::SLICE;
+            const int pr = q - tt * S::SLICE;
+            const int r = pr / S::CPR;
+            const int cs = pr - r * S::CPR;
+            const bool ok = r < rows_left && u[i] >= 0;
+            const uint16_t *src = ok ? in + (int64_t)u[i] * C_IN + ((cs ^ (r & 7)) * 8) : zero_row;
+            rs::dma16(src, abuf(b) + (wave * S::ADMA + a) * 1024);
+        }
+    };
+
+    // Prologue: weights -> registers, in rounds of W_ROWS_ROUND rows staged
+    // in the (still unused) tile buffers; the first tile's neighbour block
+    // travels with the first round.
+    u32x4_t bw[S::KG];
+#pragma unroll
+    for (int rd = 0; rd < S::W_ROUNDS; ++rd) {
+        const int n0 = rd * S::W_ROWS_ROUND;
+#pragma unroll
+        for (int a = 0; a < S::W_DMA; ++a) {
+            const int q = (wave * S::W_DMA + a) * 64 + lane;
+            const int r = q / S::WCPR;
+            const int cs = q - r * S::WCPR;
+            const int n = n0 + r;
+            rs::dma16(w + (int64_t)n * S::K + ((cs ^ (n & 7)) * 8), lds + (wave * S::W_DMA + a) * 1024);
+        }
+        if (rd == 0) load_nbr(tile0, 0);
+        rs::drain_and_barrier();
+        if (cg * 32 >= n0 && cg * 32 < n0 + S::W_ROWS_ROUND) {
+            const int n = cg * 32 + l32;
+            const char *row = lds + (n - n0) * S::WCPR * 16;
+#pragma unroll
+            for (int kg = 0; kg < S::KG; ++kg)
+                bw[kg] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ (n & 7)) * 16));
+        }
+        rs::drain_and_barrier();
+    }
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        int u[S::DPT];
+        read_nb(0, t, u);
+        issue_rows(tile0, 0, t, u);
+    }
+    if (tile0 + tstride < n_tiles) load_nbr(tile0 + tstride, 1);
+
+    const float bcol = bias ? bias[cg * 32 + l32] : 0.f;
+    int b = 0;
+    for (int64_t k = tile0; k < n_tiles; k += tstride, b ^= 1) {
+        rs::drain_and_barrier();
+        const bool next = k + tstride < n_tiles;
+        int ucur[S::DPT], unext[S::DPT];
+        if (next) read_nb(b ^ 1, 0, ucur);
+        if (k + 2 * tstride < n_tiles) load_nbr(k + 2 * tstride, b);
+
+        f32x16_t acc0, acc1;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            acc0[i] = 0.f;
+            acc1[i] = 0.f;
+        }
+        const int r = rg * 32 + l32;
+        const char *arow = abuf(b) + r * S::CPR * 16;
+        // Operand fragments are read PD taps ahead of their MFMAs (one
+        // wavefront per SIMD: nothing else hides the LDS latency).
+        constexpr int PD = S::PD;
+        u32x4_t af[PD + 1][S::GPT];
+        auto read_tap = [&](int t, int slot) {
+#pragma unroll
+            for (int g = 0; g < S::GPT; ++g)
+                af[slot][g] = *reinterpret_cast<const u32x4_t *>(arow + t * S::SLICE * 16 + (((2 * g + h) ^ (r & 7)) * 16));
+        };
+#pragma unroll
+        for (int t = 0; t < PD && t < T; ++t) read_tap(t, t);
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            if (next) {
+                issue_rows(k + tstride, b ^ 1, t, ucur);
+                if (t + 1 < T) read_nb(b ^ 1, t + 1, unext);
+#pragma unroll
+                for (int i = 0; i < S::DPT; ++i) ucur[i] = unext[i];
+            }
+            if (t + PD < T) read_tap(t + PD, (t + PD) % (PD + 1));
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int g = 0; g < S::GPT; ++g) {
+                const bf16x8_t a = __builtin_bit_cast(bf16x8_t, af[t % (PD + 1)][g]);
+                const bf16x8_t bb = __builtin_bit_cast(bf16x8_t, bw[t * S::GPT + g]);
+                if (t & 1)
+                    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc1, 0, 0, 0);
+                else
+                    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc0, 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const int col = cg * 32 + l32;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int64_t orow = k * S::MT + rg * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+            if (orow < V) {
+                const float y = acc0[i] + acc1[i] + bcol;
+                if (OUT_BF16)
+                    reinterpret_cast<uint16_t *>(out)[orow * C_OUT + col] = (uint16_t)bf16_bits(y);
+                else
+                    reinterpret_cast<float *>(out)[orow * C_OUT + col] = y;
             }
         }
     }
@@ -494,6 +768,42 @@ hipError_t launch_ws(lattice *L, const void *in, const void *w, int C_out, const
     return hipGetLastError();
 }
 
+template <bool OUT_BF16, int T, int C_IN, int C_OUT>
+hipError_t launch_rs(lattice *L, const void *in, const void *w, const float *bias, void *out) {
+    using S = RsShape<C_IN, C_OUT, T>;
+    auto kern = k_conv_rs<OUT_BF16, T, C_IN, C_OUT>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const int per_cu = (160 * 1024) / S::LDS < 2 ? 1 : 2;
+    const int64_t tiles = (L->max_vertices + S::MT - 1) / S::MT;
+    int64_t grid = (int64_t)L->cu_count * per_cu;
+    if (grid > tiles) grid = tiles;
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), S::LDS, L->stream,
+                       reinterpret_cast<const uint16_t *>(in), reinterpret_cast<const uint16_t *>(w), bias, out,
+                       L->nbr, L->max_vertices * (int64_t)L->T, L->counters, L->zero_row);
+    return hipGetLastError();
+}
+
+// Register-stationary dispatch (bf16 rows and weights); false when the shape
+// is not one it is built for.
+template <bool OUT_BF16>
+bool try_rs(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias, void *out,
+            hipError_t *err) {
+    const int T = L->T;
+    if (T == 9 && C_in == 64 && C_out == 64) *err = launch_rs<OUT_BF16, 9, 64, 64>(L, in, w, bias, out);
+    else if (T == 9 && C_in == 64 && C_out == 128) *err = launch_rs<OUT_BF16, 9, 64, 128>(L, in, w, bias, out);
+    else if (T == 9 && C_in == 128 && C_out == 128) *err = launch_rs<OUT_BF16, 9, 128, 128>(L, in, w, bias, out);
+    else if (T == 11 && C_in == 64 && C_out == 128) *err = launch_rs<OUT_BF16, 11, 64, 128>(L, in, w, bias, out);
+    else return false;
+    return true;
+}
+
 // Weight-stationary dispatch for the shapes it covers; returns false when
 // the shape is not covered (the caller falls back to k_conv_mfma).
 template <bool OUT_BF16>
@@ -538,7 +848,12 @@ hipError_t dispatch_out(lattice *L, const void *in, lattice_dtype in_dt, int C_i
     const bool in_bf16 = in_dt == LATTICE_BF16;
     const bool bf16 = dt == LATTICE_BF16;
     const bool aligned = ((reinterpret_cast<uintptr_t>(in) & 15) == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
-    if (aligned && L->conv_kernel != 1) {
+    const int path = L->conv_path;
+    if (aligned && (path == LATTICE_CONV_AUTO || path == LATTICE_CONV_RS) && bf16 && in_bf16) {
+        hipError_t err = hipSuccess;
+        if (try_rs<OUT_BF16>(L, in, C_in, w, C_out, bias, out, &err)) return err;
+    }
+    if (aligned && path != LATTICE_CONV_TILED) {
         hipError_t err = hipSuccess;
         if (try_ws<OUT_BF16>(L, in, in_bf16, C_in, w, C_out, bf16, bias, out, &err)) return err;
     }

@@ -58,6 +58,7 @@ struct lattice {
     int32_t *list = nullptr;    // [(d+1) max_points][2] (point, weight bits) grouped by vertex
     int32_t *nbr = nullptr;     // [max_vertices][T]
     int32_t *counters = nullptr;  // [CNT_WORDS] device
+    uint16_t *zero_row = nullptr; // [512] zeros: the row a missing neighbour reads
     int32_t *host_counters = nullptr;  // pinned [CNT_WORDS]
 
     int64_t m = 0;
@@ -66,7 +67,7 @@ struct lattice {
     bool batched = false;
     int cu_count = 256;
 
-    int conv_kernel = 0;  // 0: weight-stationary where it applies, 1: always the LDS-tiled kernel
+    int conv_path = LATTICE_CONV_AUTO;  // lattice_set_conv_path
 
     int timing = 0;
     lattice_timer timers[LATTICE_NUM_STAGES];

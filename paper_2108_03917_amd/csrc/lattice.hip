@@ -54,6 +54,7 @@ void free_all(lattice *L) {
     (void)hipFree(L->list);
     (void)hipFree(L->nbr);
     (void)hipFree(L->counters);
+    (void)hipFree(L->zero_row);
     if (L->host_counters) (void)hipHostFree(L->host_counters);
 }
 
@@ -204,6 +205,8 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
               hipMalloc(&L->list, max_points * dp1 * 2 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->nbr, L->max_vertices * L->T * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->counters, CNT_WORDS * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->zero_row, 512 * sizeof(uint16_t)) == hipSuccess &&
+              hipMemset(L->zero_row, 0, 512 * sizeof(uint16_t)) == hipSuccess &&
               hipHostMalloc(&L->host_counters, CNT_WORDS * sizeof(int32_t), hipHostMallocDefault) == hipSuccess;
     if (!ok) {
         (void)hipGetLastError();
@@ -296,6 +299,16 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
     L->splatted = true;
     L->nbr_valid = false;
     L->batched = batch != nullptr;
+    return LATTICE_OK;
+}
+
+lattice_status lattice_set_conv_path(lattice *L, int path) {
+    if (!L) return LATTICE_E_ARG;
+    if (path < LATTICE_CONV_AUTO || path > LATTICE_CONV_RS) {
+        set_err(L, "set_conv_path: unknown path %d", path);
+        return LATTICE_E_ARG;
+    }
+    L->conv_path = path;
     return LATTICE_OK;
 }
 

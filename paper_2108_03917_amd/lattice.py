@@ -27,7 +27,7 @@ EXPORTS = (
     "lattice_slice", "lattice_weights_to_bf16", "lattice_num_vertices", "lattice_get_status",
     "lattice_get_keys", "lattice_get_neighbors", "lattice_get_point_simplex", "lattice_set_timing",
     "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
-    "lattice_last_error",
+    "lattice_last_error", "lattice_set_conv_path",
 )
 
 _lib = None
@@ -64,6 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_get_neighbors": (St, [P, P]),
         "lattice_get_point_simplex": (St, [P, P, P]),
         "lattice_set_timing": (St, [P, I]),
+        "lattice_set_conv_path": (St, [P, I]),
         "lattice_get_timing": (St, [P, ctypes.POINTER(D), ctypes.POINTER(I64)]),
         "lattice_hash_capacity": (I64, [P]),
         "lattice_dim": (I, [P]),
@@ -282,6 +283,12 @@ class Lattice:
         return idx[:self.m], bary[:self.m]
 
     # -- stage timing -----------------------------------------------------
+    CONV_PATHS = {"auto": 0, "tiled": 1, "ws": 2, "rs": 3}
+
+    def set_conv_path(self, path: str):
+        """Kernel family of later convs: "auto", "tiled", "ws" or "rs"."""
+        self._check(self._lib.lattice_set_conv_path(self._h, self.CONV_PATHS[path]), "set_conv_path")
+
     def set_timing(self, mode: int):
         self._check(self._lib.lattice_set_timing(self._h, int(mode)), "set_timing")
 

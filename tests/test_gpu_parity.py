@@ -416,3 +416,43 @@ def test_stage_timing_records_every_stage():
     assert all(t[s][1] == 1 and t[s][0] > 0 for s in ("splat", "neighbors", "conv", "slice")), t
     L.set_timing(2)
     assert all(v == (0.0, 0) for v in L.timing().values())
+
+
+# ---------------------------------------------------------------------------
+# every conv kernel family on a lattice large enough for several tiles per
+# workgroup (the pipelined kernels prefetch across tiles) and a ragged tail
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def big_lattices():
+    out = {}
+    for d, sigma in [(3, 0.05), (4, 0.12)]:
+        w = random_cloud(40000, d, seed=970 + d, extent=1.0, C=1)
+        L = _lattice(d, sigma, w.m)
+        g = GpuLattice(L, w.pos, w.feat)
+        lat = O.build(w.pos, sigma)
+        out[d] = (L, g, lat, O.neighbors(lat))
+    return out
+
+
+@pytest.mark.parametrize("d,C_in,C_out", [(3, 64, 64), (3, 64, 128), (3, 128, 128), (4, 64, 128), (4, 64, 64),
+                                          (3, 128, 64)])
+def test_conv_every_path_bf16(big_lattices, d, C_in, C_out):
+    L, g, lat, nbr = big_lattices[d]
+    assert lat.V > 256 * 64 * 2  # more tiles than two per workgroup for every tiling
+    x = O.round_bf16(random_rows(lat.V, C_in, seed=971))
+    W = conv_weight(C_in, C_out, d, seed=972)
+    b = random_rows(1, C_out, seed=973)[0]
+    ref, scale = O.conv(x.astype(np.float64), nbr, O.round_bf16(W).astype(np.float64), b)
+    xin = g.to_gpu_order(x).to(torch.bfloat16)
+    wd = L.weights_to_bf16(to_dev(W))
+    try:
+        for path in ("tiled", "ws", "rs"):
+            L.set_conv_path(path)
+            for out_dtype in ("f32", "bf16"):
+                out = L.conv(xin, wd, dtype="bf16", bias=to_dev(b), out_dtype=out_dtype)
+                got = g.from_gpu_order(out.float())
+                tol = REL_F32 * scale + (BF16_ULP * np.abs(ref) if out_dtype == "bf16" else 0.0)
+                assert_close_scaled(got, ref, tol, 1.0, f"{path} conv {C_in}x{C_out} d={d} out {out_dtype}")
+    finally:
+        L.set_conv_path("auto")
