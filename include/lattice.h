@@ -195,8 +195,10 @@ lattice_status lattice_conv(lattice *L, const void *in, lattice_dtype in_dtype, 
  *   LATTICE_CONV_WS      weight slice resident in LDS, rows gathered straight
  *                        into registers, where built for the shape; else TILED
  *   LATTICE_CONV_RS      weights resident in registers, rows gathered into
- *                        LDS by direct loads (bf16 rows and weights, shapes
- *                        it is built for); else as AUTO without it
+ *                        LDS by direct loads, where built for the shape
+ *                        (bf16 rows and weights: 64 -> 64, 64 -> 128,
+ *                        128 -> 128 with 9 taps, 64 -> 64 and 64 -> 128 with
+ *                        11; fp32: 64 -> 64 with 9 taps); else as AUTO
  * Returns LATTICE_E_ARG for another value.
  */
 enum { LATTICE_CONV_AUTO = 0, LATTICE_CONV_TILED = 1, LATTICE_CONV_WS = 2, LATTICE_CONV_RS = 3 };

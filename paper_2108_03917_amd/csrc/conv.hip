@@ -430,26 +430,30 @@ __global__ __launch_bounds__(512) void k_conv_ws(const void *__restrict__ in, co
 }
 
 // ---------------------------------------------------------------------------
-// k_conv_rs: bf16 rows and weights, weights resident in registers.
+// k_conv_rs: weights resident in registers, rows gathered into LDS.
 //
 // A gather in MFMA operand layout puts 32 different rows in one 64-lane load
-// (each lane 16 bytes), which the address unit serves one lane per cycle.
-// Here the gathered rows travel instead by direct-to-LDS loads in row order
-// (consecutive lanes read consecutive 16-byte chunks of a row, so a load is
-// a few full cache lines), into a two-tile LDS ring; the MFMA operand is
-// then read from LDS.  Each of the four wavefronts owns 32 output columns
-// and keeps their whole K x 32 weight slice in registers for the life of
-// the workgroup, so the weights cost neither LDS bandwidth nor address-unit
-// cycles after the prologue; with C_out = 64 two wavefronts share a column
-// group and split the rows.
+// (each lane 16 bytes); measured on this chip such loads move about a third
+// of what row-order loads of the same rows do.  Here the gathered rows
+// travel by direct-to-LDS loads in row order (consecutive lanes read
+// consecutive 16-byte chunks of a row) into a two-tile LDS ring, and the
+// MFMA operands are read from LDS.  A wavefront owns 32 output columns and
+// 1/KS of the K = T C_in reduction, and keeps that K/KS x 32 weight slice in
+// registers for the life of the workgroup: after the prologue the weights
+// cost neither LDS bandwidth nor address-unit cycles.  With KS = 2 the two
+// halves are added through LDS at the end of each tile.
 //
-// Per tile of MT rows (MT = 32 * 4 / (C_out / 32)):
-//   top:   wait for this tile's loads, barrier
-//          issue the next tile's row loads (addresses from its neighbour
-//          block, already in LDS) and the neighbour block of the tile after
-//          that
-//   body:  T taps x C_in/16 k-groups of ds_read + MFMA 32x32x16
-//   store: bias, fp32 or bf16
+// Operand groups: a lane's 16-byte chunk (2g + h) of a row (h = lane / 32)
+// is the k-slice h of group g: bf16, 8 channels of one MFMA 32x32x16; fp32,
+// channels 8g + 4h + i, the k = h operand of MFMA 32x32x2 number i of the
+// group.  The weights are held in the same order.
+//
+// Per tile of MT rows:
+//   top:   wait for this tile's loads, barrier; issue the neighbour block
+//          of the tile after next and the next tile's row loads (addresses
+//          from its neighbour block, already in LDS)
+//   body:  T steps of KG/T operand groups (ds_read + MFMA)
+//   store: (KS = 2: partial sums through LDS) bias, fp32 or bf16
 // A missing neighbour (index -1) and the rows past V of the last tile read
 // a zero row.  16-byte chunk c of tile row r sits at chunk c ^ (r % 8) of
 // the row's LDS slot (and weight row n likewise with n % 8), so that the
@@ -465,18 +469,91 @@ __device__ __forceinline__ void dma16(const void *src, char *lds_wave_base) {
 // direct-to-LDS loads included), then the workgroup barrier.  The memory
 // clobber keeps the compiler from moving LDS accesses across it.
 __device__ __forceinline__ void drain_and_barrier() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Barrier after this wavefront's LDS operations (no wait on global memory).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// 4 x 4 transpose within each quad of lanes: on entry lane j of a quad
+// holds element (i, j) in v[i]; on return it holds element (j, i) in v[i].
+// Two exchange rounds (quad_perm 2,3,0,1 then 1,0,3,2).
+__device__ __forceinline__ void quad_transpose(float *v) {
+    const int j = threadIdx.x & 3;
+    int x[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __builtin_amdgcn_mov_dpp(__float_as_int(v[i]), 0x4E, 0xF, 0xF, false);
+    if (j < 2) {
+        v[2] = __int_as_float(x[0]);
+        v[3] = __int_as_float(x[1]);
+    } else {
+        v[0] = __int_as_float(x[2]);
+        v[1] = __int_as_float(x[3]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __builtin_amdgcn_mov_dpp(__float_as_int(v[i]), 0xB1, 0xF, 0xF, false);
+    if ((j & 1) == 0) {
+        v[1] = __int_as_float(x[0]);
+        v[3] = __int_as_float(x[2]);
+    } else {
+        v[0] = __int_as_float(x[1]);
+        v[2] = __int_as_float(x[3]);
+    }
+}
+
+// Store a 32 x 32 MFMA accumulator block (lane l: column l % 32, register i:
+// row 8 (i / 4) + 4 (l / 32) + i % 4) plus bias: after a quad transpose a
+// lane holds four consecutive columns of one row, stored as one 16-byte
+// (fp32) or 8-byte (bf16) write.  Rows at or past V are not written.
+template <bool OUT_BF16>
+__device__ __forceinline__ void store_block(f32x16_t acc, float bias_col, void *out, int64_t row0, int col0,
+                                            int C_out, int64_t V) {
+    const int lane = threadIdx.x & 63;
+    const int j = lane & 3;
+    const int h = lane >> 5;
+    const int c = col0 + (lane & 31) - j;  // first of the lane's four columns
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = acc[4 * q + i] + bias_col;  // bias of column (lane & 31)
+        quad_transpose(v);
+        // v[i] now: row 8q + 4h + j, column c + i (the bias moved with it)
+        const int64_t row = row0 + 8 * q + 4 * h + j;
+        if (row < V) {
+            if (OUT_BF16) {
+                uint2 pk;
+                pk.x = bf16_bits(v[0]) | (bf16_bits(v[1]) << 16);
+                pk.y = bf16_bits(v[2]) | (bf16_bits(v[3]) << 16);
+                *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(out) + row * C_out + c) = pk;
+            } else {
+                *reinterpret_cast<float4 *>(reinterpret_cast<float *>(out) + row * C_out + c) =
+                    make_float4(v[0], v[1], v[2], v[3]);
+            }
+        }
+    }
+}
+
+// Wait until at most N vector memory operations of this wavefront are
+// outstanding (and its LDS operations are done), then the barrier.
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
 }  // namespace rs
 
-template <int C_IN, int C_OUT, int T>
+template <bool BF16, int C_IN, int C_OUT, int T, int KS>
 struct RsShape {
     static constexpr int NW = 4;
+    static constexpr int ESZ = BF16 ? 2 : 4;
     static constexpr int NCG = C_OUT / 32;                 // column groups
-    static constexpr int NRG = NW / NCG;                   // row groups
+    static constexpr int NRG = NW / (NCG * KS);            // row groups
     static constexpr int MT = 32 * NRG;                    // rows per tile
     static constexpr int K = T * C_IN;
-    static constexpr int KG = K / 16;                      // k-groups (one MFMA each)
-    static constexpr int GPT = C_IN / 16;                  // k-groups per tap
-    static constexpr int CPR = C_IN / 8;                   // 16-byte chunks per row
+    static constexpr int CPR = C_IN * ESZ / 16;            // 16-byte chunks per row
+    static constexpr int GPT = CPR / 2;                    // operand groups per tap
+    static constexpr int KG = T * GPT;                     // operand groups
+    static constexpr int KGW = KG / KS;                    // operand groups per wavefront
+    static constexpr int GPS = KGW / T;                    // groups per step
     static constexpr int SLICE = MT * CPR;                 // chunks of one tap
     static constexpr int TILE = T * SLICE;                 // chunks of one tile
     static constexpr int TILE_BYTES = TILE * 16;
@@ -484,15 +561,15 @@ struct RsShape {
     static constexpr int NB_INTS = MT * T;                 // neighbour block of a tile
     static constexpr int NB_DMA = (NB_INTS * 4 + 1023) / 1024;
     static constexpr int NB_BYTES = NB_DMA * 1024;
-    static constexpr int WCPR = K / 8;                     // chunks per weight row
+    static constexpr int RED_BYTES = KS > 1 ? NCG * NRG * 16 * 64 * 4 : 0;  // partial sums
+    static constexpr int WCPR = K * ESZ / 16;              // chunks per weight row
     static constexpr int W_ROWS_ROUND = (2 * TILE_BYTES) / (WCPR * 16) < C_OUT ? (2 * TILE_BYTES) / (WCPR * 16) : C_OUT;
     static constexpr int W_ROUNDS = C_OUT / W_ROWS_ROUND;
     static constexpr int W_DMA = W_ROWS_ROUND * WCPR / (64 * NW);  // weight loads per wavefront per round
-    static constexpr int LDS = 2 * TILE_BYTES + 2 * NB_BYTES;
-    static constexpr int PD = GPT >= 8 ? 1 : 2;            // operand read-ahead, in taps
-    static constexpr int DPT = ADMA / T;                   // row loads issued per tap
-    static_assert(DPT * T == ADMA, "row loads per tap");
-    static_assert(NCG * NRG == NW, "column groups");
+    static constexpr int PD = GPS >= 8 ? 1 : 2;            // operand read-ahead, in steps
+    static constexpr int LDS = 2 * TILE_BYTES + 2 * NB_BYTES + RED_BYTES;
+    static_assert(NCG * NRG * KS == NW && NRG >= 1, "wavefront roles");
+    static_assert(KG % KS == 0 && KGW % T == 0, "groups per step");
     static_assert(TILE % (64 * NW) == 0, "tile loads");
     static_assert(CPR >= 8 && WCPR % 8 == 0, "swizzle");
     static_assert(NB_DMA <= NW && NB_INTS % 4 == 0, "neighbour block");
@@ -501,16 +578,19 @@ struct RsShape {
     static_assert(LDS <= 160 * 1024, "LDS");
 };
 
-template <bool OUT_BF16, int T, int C_IN, int C_OUT>
-__global__ __launch_bounds__(256) void k_conv_rs(const uint16_t *__restrict__ in, const uint16_t *__restrict__ w,
+template <bool BF16, bool OUT_BF16, int T, int C_IN, int C_OUT, int KS>
+__global__ __launch_bounds__(256) void k_conv_rs(const void *__restrict__ in_, const void *__restrict__ w_,
                                                  const float *__restrict__ bias, void *__restrict__ out,
                                                  const int32_t *__restrict__ nbr, int64_t nbr_ints,
                                                  const int32_t *__restrict__ counters,
                                                  const uint16_t *__restrict__ zero_row) {
-    using S = RsShape<C_IN, C_OUT, T>;
+    using S = RsShape<BF16, C_IN, C_OUT, T, KS>;
+    const char *in = reinterpret_cast<const char *>(in_);
+    const char *w = reinterpret_cast<const char *>(w_);
     extern __shared__ __attribute__((aligned(16))) char lds[];
     auto abuf = [&](int b) { return lds + b * S::TILE_BYTES; };                      // row tiles
     auto nbuf = [&](int b) { return lds + 2 * S::TILE_BYTES + b * S::NB_BYTES; };    // neighbour blocks
+    float *red = reinterpret_cast<float *>(lds + 2 * S::TILE_BYTES + 2 * S::NB_BYTES);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -518,12 +598,19 @@ __global__ __launch_bounds__(256) void k_conv_rs(const uint16_t *__restrict__ in
     const int l32 = lane & 31;
     const int h = lane >> 5;
     const int cg = wave % S::NCG;
-    const int rg = wave / S::NCG;
+    const int rg = (wave / S::NCG) % S::NRG;
+    const int ks = KS == 1 ? 0 : wave / (S::NCG * S::NRG);
     const int64_t V = counters[CNT_V];
     const int64_t n_tiles = (V + S::MT - 1) / S::MT;
     const int64_t tile0 = blockIdx.x;
     const int64_t tstride = gridDim.x;
     if (tile0 >= n_tiles) return;  // uniform over the workgroup
+
+    // The bias is in a register before the first direct-to-LDS load: its
+    // first use would otherwise make the compiler wait for every load issued
+    // before it.
+    float bcol = bias ? bias[cg * 32 + l32] : 0.f;
+    asm volatile("s_waitcnt vmcnt(0)" : "+v"(bcol));
 
     // Neighbour block of tile k -> nbuf(b): NB_INTS contiguous ints, one
     // 1 KB load per wavefront for the first NB_DMA wavefronts; chunks past
@@ -538,42 +625,30 @@ __global__ __launch_bounds__(256) void k_conv_rs(const uint16_t *__restrict__ in
             rs::dma16(nbr + at, nbuf(b) + wave * 1024);
         }
     };
-    // Rows of tile k -> abuf(b).  A wavefront's ADMA loads are issued DPT
-    // per tap between the MFMAs of the current tile, so that the address
-    // unit drains them while the matrix cores work; the neighbour indices of
-    // tap t's loads are read from nbuf(b) one tap earlier (a direct-to-LDS
-    // load is not reordered with LDS reads, so reading an index right before
-    // its load would wait out the LDS latency).
-    auto read_nb = [&](int b, int t, int *u) {
-        const int32_t *nb = reinterpret_cast<const int32_t *>(nbuf(b));
-#pragma unroll
-        for (int i = 0; i < S::DPT; ++i) {
-            const int q = (wave * S::ADMA + t * S::DPT + i) * 64 + lane;
-            const int tt = q / S::SLICE;
-            const int r = (q - tt * S::SLICE) / S::CPR;
-            u[i] = nb[r * T + tt];
-        }
+    // Row load a (0 .. ADMA-1) of this wavefront for tile k into abuf(b):
+    // the neighbour index first (from nbuf(b)), then the load.
+    auto row_nb = [&](int b, int a) {
+        const int q = (wave * S::ADMA + a) * 64 + lane;
+        const int t = q / S::SLICE;
+        const int r = (q - t * S::SLICE) / S::CPR;
+        return reinterpret_cast<const int32_t *>(nbuf(b))[r * T + t];
     };
-    auto issue_rows = [&](int64_t k, int b, int t, const int *u) {
-        const int rows_left = (int)(V - k * S::MT < S::MT ? V - k * S::MT : S::MT);
-#pragma unroll
-        for (int i = 0; i < S::DPT; ++i) {
-            const int a = t * S::DPT + i;
-            const int q = (wave * S::ADMA + a) * 64 + lane;
-            const int tt = q / S::SLICE;
-            const int pr = q - tt * S::SLICE;
-            const int r = pr / S::CPR;
-            const int cs = pr - r * S::CPR;
-            const bool ok = r < rows_left && u[i] >= 0;
-            const uint16_t *src = ok ? in + (int64_t)u[i] * C_IN + ((cs ^ (r & 7)) * 8) : zero_row;
-            rs::dma16(src, abuf(b) + (wave * S::ADMA + a) * 1024);
-        }
+    auto row_load = [&](int64_t k, int b, int a, int u) {
+        const int q = (wave * S::ADMA + a) * 64 + lane;
+        const int t = q / S::SLICE;
+        const int pr = q - t * S::SLICE;
+        const int r = pr / S::CPR;
+        const int cs = pr - r * S::CPR;
+        const bool ok = r < V - k * S::MT && u >= 0;
+        const void *src = ok ? (const void *)(in + ((int64_t)u * C_IN * S::ESZ + ((cs ^ (r & 7)) * 16)))
+                             : (const void *)zero_row;
+        rs::dma16(src, abuf(b) + (wave * S::ADMA + a) * 1024);
     };
 
     // Prologue: weights -> registers, in rounds of W_ROWS_ROUND rows staged
     // in the (still unused) tile buffers; the first tile's neighbour block
     // travels with the first round.
-    u32x4_t bw[S::KG];
+    u32x4_t bw[S::KGW];
 #pragma unroll
     for (int rd = 0; rd < S::W_ROUNDS; ++rd) {
         const int n0 = rd * S::W_ROWS_ROUND;
@@ -583,7 +658,7 @@ __global__ __launch_bounds__(256) void k_conv_rs(const uint16_t *__restrict__ in
             const int r = q / S::WCPR;
             const int cs = q - r * S::WCPR;
             const int n = n0 + r;
-            rs::dma16(w + (int64_t)n * S::K + ((cs ^ (n & 7)) * 8), lds + (wave * S::W_DMA + a) * 1024);
+            rs::dma16(w + ((int64_t)n * S::WCPR + (cs ^ (n & 7))) * 16, lds + (wave * S::W_DMA + a) * 1024);
         }
         if (rd == 0) load_nbr(tile0, 0);
         rs::drain_and_barrier();
@@ -591,27 +666,33 @@ __global__ __launch_bounds__(256) void k_conv_rs(const uint16_t *__restrict__ in
             const int n = cg * 32 + l32;
             const char *row = lds + (n - n0) * S::WCPR * 16;
 #pragma unroll
-            for (int kg = 0; kg < S::KG; ++kg)
-                bw[kg] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ (n & 7)) * 16));
+            for (int kk = 0; kk < S::KGW; ++kk) {
+                const int kg = ks * S::KGW + kk;
+                bw[kk] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ (n & 7)) * 16));
+            }
         }
         rs::drain_and_barrier();
     }
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-        int u[S::DPT];
-        read_nb(0, t, u);
-        issue_rows(tile0, 0, t, u);
-    }
+    for (int a = 0; a < S::ADMA; ++a) row_load(tile0, 0, a, row_nb(0, a));
     if (tile0 + tstride < n_tiles) load_nbr(tile0 + tstride, 1);
 
-    const float bcol = bias ? bias[cg * 32 + l32] : 0.f;
+    const int r = rg * 32 + l32;
     int b = 0;
     for (int64_t k = tile0; k < n_tiles; k += tstride, b ^= 1) {
         rs::drain_and_barrier();
         const bool next = k + tstride < n_tiles;
-        int ucur[S::DPT], unext[S::DPT];
-        if (next) read_nb(b ^ 1, 0, ucur);
         if (k + 2 * tstride < n_tiles) load_nbr(k + 2 * tstride, b);
+        // the next tile's row loads: all neighbour indices first (a
+        // direct-to-LDS load is not reordered with LDS reads, so alternating
+        // them would serialise both), then the loads
+        if (next) {
+            int u[S::ADMA];
+#pragma unroll
+            for (int i = 0; i < S::ADMA; ++i) u[i] = row_nb(b ^ 1, i);
+#pragma unroll
+            for (int i = 0; i < S::ADMA; ++i) row_load(k + tstride, b ^ 1, i, u[i]);
+        }
 
         f32x16_t acc0, acc1;
 #pragma unroll
@@ -619,53 +700,333 @@ __global__ __launch_bounds__(256) void k_conv_rs(const uint16_t *__restrict__ in
             acc0[i] = 0.f;
             acc1[i] = 0.f;
         }
-        const int r = rg * 32 + l32;
         const char *arow = abuf(b) + r * S::CPR * 16;
-        // Operand fragments are read PD taps ahead of their MFMAs (one
-        // wavefront per SIMD: nothing else hides the LDS latency).
-        constexpr int PD = S::PD;
-        u32x4_t af[PD + 1][S::GPT];
-        auto read_tap = [&](int t, int slot) {
-#pragma unroll
-            for (int g = 0; g < S::GPT; ++g)
-                af[slot][g] = *reinterpret_cast<const u32x4_t *>(arow + t * S::SLICE * 16 + (((2 * g + h) ^ (r & 7)) * 16));
+        // operand group kk of this wavefront: tap kg / GPT, group kg % GPT
+        auto read_group = [&](int kk) {
+            const int kg = ks * S::KGW + kk;
+            const int t = kg / S::GPT;
+            const int g = kg - t * S::GPT;
+            return *reinterpret_cast<const u32x4_t *>(arow + t * S::SLICE * 16 + (((2 * g + h) ^ (r & 7)) * 16));
         };
+        // Operand groups are read PD steps ahead of their MFMAs (one
+        // wavefront per SIMD: nothing else hides the LDS latency).  With
+        // PD = 1 a single set of registers: group g of step st+1 is read as
+        // soon as the MFMAs of group g of step st are issued.
+        constexpr int PD = S::PD;
+        constexpr int NSETS = PD == 1 ? 1 : PD + 1;
+        u32x4_t af[NSETS][S::GPS];
 #pragma unroll
-        for (int t = 0; t < PD && t < T; ++t) read_tap(t, t);
+        for (int st = 0; st < PD && st < T; ++st)
 #pragma unroll
-        for (int t = 0; t < T; ++t) {
-            if (next) {
-                issue_rows(k + tstride, b ^ 1, t, ucur);
-                if (t + 1 < T) read_nb(b ^ 1, t + 1, unext);
+            for (int g = 0; g < S::GPS; ++g) af[st][g] = read_group(st * S::GPS + g);
 #pragma unroll
-                for (int i = 0; i < S::DPT; ++i) ucur[i] = unext[i];
+        for (int st = 0; st < T; ++st) {
+            if (PD != 1 && st + PD < T) {
+#pragma unroll
+                for (int g = 0; g < S::GPS; ++g) af[(st + PD) % (PD + 1)][g] = read_group((st + PD) * S::GPS + g);
             }
-            if (t + PD < T) read_tap(t + PD, (t + PD) % (PD + 1));
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int g = 0; g < S::GPT; ++g) {
-                const bf16x8_t a = __builtin_bit_cast(bf16x8_t, af[t % (PD + 1)][g]);
-                const bf16x8_t bb = __builtin_bit_cast(bf16x8_t, bw[t * S::GPT + g]);
-                if (t & 1)
-                    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc1, 0, 0, 0);
-                else
-                    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bb, acc0, 0, 0, 0);
+            for (int g = 0; g < S::GPS; ++g) {
+                const u32x4_t a = af[PD == 1 ? 0 : st % (PD + 1)][g];
+                const u32x4_t bb = bw[st * S::GPS + g];
+                if (BF16) {
+                    if (g & 1)
+                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                                       __builtin_bit_cast(bf16x8_t, bb), acc1, 0, 0, 0);
+                    else
+                        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                                       __builtin_bit_cast(bf16x8_t, bb), acc0, 0, 0, 0);
+                } else {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if (c & 1)
+                            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[c]), __uint_as_float(bb[c]),
+                                                                        acc1, 0, 0, 0);
+                        else
+                            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[c]), __uint_as_float(bb[c]),
+                                                                        acc0, 0, 0, 0);
+                    }
+                }
+                if (PD == 1 && st + 1 < T) af[0][g] = read_group((st + 1) * S::GPS + g);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        const int col = cg * 32 + l32;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc0[i] += acc1[i];
+        if (KS > 1) {
+            // the second K half adds its partial sums through LDS
+            float *slot = red + ((cg * S::NRG + rg) * 16) * 64;
+            if (ks == 1) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) slot[i * 64 + lane] = acc0[i];
+            }
+            rs::lds_barrier();
+            if (ks == 0) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) acc0[i] += slot[i * 64 + lane];
+            }
+        }
+        if (KS == 1 || ks == 0) rs::store_block<OUT_BF16>(acc0, bcol, out, k * S::MT + rg * 32, cg * 32, C_OUT, V);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_conv_ring: register-resident weights like k_conv_rs, with the gathered
+// rows streamed through a ring of T tap slices (slot t holds tap t of some
+// tile) instead of two whole tiles, so that fp32 rows (and T = 11) fit in
+// LDS.  A slice is MT rows x C_in channels; each wavefront issues DPS
+// direct-to-LDS loads per slice.  At the top of slice j (tile i, tap t):
+//   wait until slices j .. j+PD are in LDS, barrier (slot of j-1 is free)
+//   t = 0: store tile i-1, clear the accumulators, and load the neighbour
+//   block of tile i+2
+//   read the operands of slice j+PD; MFMAs of slice j, with the loads of
+//   slice j+T-1 (tap t-1 of tile i+1; for t = 0 the last tap of tile i)
+//   into the freed slot issued between them.
+// The wait is a vmcnt bound: loads complete in issue order, so "at most N
+// loads newer than slice j+PD outstanding" means j+PD has landed; N counts
+// the DMA groups issued after it (and the neighbour-block load where that
+// is newer: for 1 <= t < T-1-PD).  Stores are not counted: a store still in flight only makes the
+// wait longer.  Loads past the last tile read the zero row so that every
+// wavefront issues the same number of loads per slice.
+//
+// fp32: a lane's 16-byte chunk (2g + h) of a row holds channels 8g + 4h + i,
+// i = 0..3, the k = h operand of MFMA 32x32x2 number i of the group; the
+// weights are held in the same permutation.
+template <bool BF16, int C_IN, int C_OUT, int T>
+struct RingShape {
+    static constexpr int NW = 4;
+    static constexpr int ESZ = BF16 ? 2 : 4;
+    static constexpr int NCG = C_OUT / 32;
+    static constexpr int NRG = NW / NCG;
+    static constexpr int MT = 32 * NRG;
+    static constexpr int K = T * C_IN;
+    static constexpr int CPR = C_IN * ESZ / 16;            // 16-byte chunks per row
+    static constexpr int GPT = CPR / 2;                    // 32-byte operand groups per tap
+    static constexpr int SLICE_BYTES = MT * CPR * 16;
+    static constexpr int DPS = SLICE_BYTES / (1024 * NW);  // loads per wavefront per slice
+    static constexpr int RING_BYTES = T * SLICE_BYTES;
+    static constexpr int NB_INTS = MT * T;
+    static constexpr int NB_BYTES = NW * 1024;             // one 1 KB load per wavefront
+    static constexpr int PD = BF16 ? 2 : 1;                // operand read-ahead, in slices
+    static constexpr int WCPR = K * ESZ / 16;              // chunks per weight row
+    static constexpr int W_ROWS_ROUND = (RING_BYTES / (WCPR * 16)) / 32 * 32 < C_OUT
+                                            ? (RING_BYTES / (WCPR * 16)) / 32 * 32 : C_OUT;
+    static constexpr int W_ROUNDS = C_OUT / W_ROWS_ROUND;
+    static constexpr int W_DMA = W_ROWS_ROUND * WCPR / (64 * NW);
+    static constexpr int LDS = RING_BYTES + 2 * NB_BYTES;
+    static_assert(NCG * NRG == NW && MT >= 32, "column groups");
+    static_assert(SLICE_BYTES % (1024 * NW) == 0, "slice loads");
+    static_assert(CPR >= 8 && WCPR % 8 == 0, "swizzle");
+    static_assert(NB_INTS * 4 <= NB_BYTES && NB_INTS % 4 == 0, "neighbour block");
+    static_assert(W_ROWS_ROUND >= 32 && C_OUT % W_ROWS_ROUND == 0, "weight rounds");
+    static_assert((W_ROWS_ROUND * WCPR) % (64 * NW) == 0, "weight loads");
+    static_assert(T - 2 - PD >= 1, "ring depth");
+    static_assert(GPT % DPS == 0, "loads spread over the operand groups");
+    static_assert(LDS <= 160 * 1024, "LDS");
+};
+
+template <bool BF16, bool OUT_BF16, int T, int C_IN, int C_OUT>
+__global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_, const void *__restrict__ w_,
+                                                   const float *__restrict__ bias, void *__restrict__ out,
+                                                   const int32_t *__restrict__ nbr, int64_t nbr_ints,
+                                                   const int32_t *__restrict__ counters,
+                                                   const uint16_t *__restrict__ zero_row) {
+    using S = RingShape<BF16, C_IN, C_OUT, T>;
+    const char *in = reinterpret_cast<const char *>(in_);
+    const char *w = reinterpret_cast<const char *>(w_);
+    extern __shared__ __attribute__((aligned(16))) char lds[];
+    auto slot = [&](int t) { return lds + t * S::SLICE_BYTES; };
+    auto nbuf = [&](int b) { return lds + S::RING_BYTES + b * S::NB_BYTES; };
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l32 = lane & 31;
+    const int h = lane >> 5;
+    const int cg = wave % S::NCG;
+    const int rg = wave / S::NCG;
+    const int64_t V = counters[CNT_V];
+    const int64_t n_tiles = (V + S::MT - 1) / S::MT;
+    const int64_t tile0 = blockIdx.x;
+    const int64_t tstride = gridDim.x;
+    if (tile0 >= n_tiles) return;  // uniform over the workgroup
+
+    // neighbour block of tile k (may be past the last tile) -> nbuf(b)
+    auto load_nbr = [&](int64_t k, int b) {
+        const int64_t last = (nbr_ints / 4 - 1) * 4;
+        const int64_t j = (int64_t)wave * 64 + lane;
+        int64_t at = k * S::NB_INTS + 4 * j;
+        if (4 * j >= S::NB_INTS) at = k * S::NB_INTS;
+        if (at > last) at = last;
+        rs::dma16(nbr + at, nbuf(b) + wave * 1024);
+    };
+    // tap t of tile k -> slot(t): the DPS neighbour indices of this
+    // wavefront's loads (from nbuf(b)), then one load at a time
+    auto slice_nb = [&](int b, int t, int *u) {
+        const int32_t *nb = reinterpret_cast<const int32_t *>(nbuf(b));
+#pragma unroll
+        for (int i = 0; i < S::DPS; ++i) {
+            const int q = (wave * S::DPS + i) * 64 + lane;
+            u[i] = nb[(q / S::CPR) * T + t];
+        }
+    };
+    auto slice_load = [&](int64_t k, int t, int i, int u) {
+        const int q = (wave * S::DPS + i) * 64 + lane;
+        const int r = q / S::CPR;
+        const int cs = q - r * S::CPR;
+        const bool ok = r < V - k * S::MT && u >= 0;
+        const void *src = ok ? (const void *)(in + ((int64_t)u * C_IN * S::ESZ + ((cs ^ (r & 7)) * 16)))
+                             : (const void *)zero_row;
+        rs::dma16(src, slot(t) + (wave * S::DPS + i) * 1024);
+    };
+    auto load_slice = [&](int64_t k, int b, int t) {
+        int u[S::DPS];
+        slice_nb(b, t, u);
+#pragma unroll
+        for (int i = 0; i < S::DPS; ++i) slice_load(k, t, i, u[i]);
+    };
+
+    // The bias is in a register before the first direct-to-LDS load: its
+    // first use would otherwise make the compiler wait for every load issued
+    // before it.
+    float bcol = bias ? bias[cg * 32 + l32] : 0.f;
+    asm volatile("s_waitcnt vmcnt(0)" : "+v"(bcol));
+
+    // Prologue: weights -> registers (rounds staged in the ring), the first
+    // two neighbour blocks, then taps 0..T-2 of the first tile.
+    u32x4_t bw[T * S::GPT];
+#pragma unroll
+    for (int rd = 0; rd < S::W_ROUNDS; ++rd) {
+        const int n0 = rd * S::W_ROWS_ROUND;
+#pragma unroll
+        for (int a = 0; a < S::W_DMA; ++a) {
+            const int q = (wave * S::W_DMA + a) * 64 + lane;
+            const int r = q / S::WCPR;
+            const int cs = q - r * S::WCPR;
+            const int n = n0 + r;
+            rs::dma16(w + ((int64_t)n * S::WCPR + (cs ^ (n & 7))) * 16, lds + (wave * S::W_DMA + a) * 1024);
+        }
+        if (rd == 0) {
+            load_nbr(tile0, 0);
+            load_nbr(tile0 + tstride, 1);
+        }
+        rs::drain_and_barrier();
+        if (cg * 32 >= n0 && cg * 32 < n0 + S::W_ROWS_ROUND) {
+            const int n = cg * 32 + l32;
+            const char *row = lds + (n - n0) * S::WCPR * 16;
+#pragma unroll
+            for (int kg = 0; kg < T * S::GPT; ++kg)
+                bw[kg] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ (n & 7)) * 16));
+        }
+        rs::drain_and_barrier();
+    }
+#pragma unroll
+    for (int t = 0; t < T - 1; ++t) load_slice(tile0, 0, t);
+
+    const int r = rg * 32 + l32;
+    // Operands: with PD = 1 one set of registers, group g of slice j+1
+    // read as soon as the MFMAs of group g of slice j are issued; with PD = 2
+    // a ring of PD + 1 sets.
+    constexpr int NSETS = S::PD == 1 ? 1 : S::PD + 1;
+    u32x4_t af[NSETS][S::GPT];
+    auto read_group = [&](int t, int sl, int g) {
+        const char *arow = slot(t) + r * S::CPR * 16;
+        af[sl][g] = *reinterpret_cast<const u32x4_t *>(arow + (((2 * g + h) ^ (r & 7)) * 16));
+    };
+    auto read_slice = [&](int t, int sl) {
+#pragma unroll
+        for (int g = 0; g < S::GPT; ++g) read_group(t, sl, g);
+    };
+    f32x16_t acc0, acc1;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        acc0[i] = 0.f;
+        acc1[i] = 0.f;
+    }
+    auto store_tile = [&](int64_t k) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc0[i] += acc1[i];
+        rs::store_block<OUT_BF16>(acc0, bcol, out, k * S::MT + rg * 32, cg * 32, C_OUT, V);
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const int64_t orow = k * S::MT + rg * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-            if (orow < V) {
-                const float y = acc0[i] + acc1[i] + bcol;
-                if (OUT_BF16)
-                    reinterpret_cast<uint16_t *>(out)[orow * C_OUT + col] = (uint16_t)bf16_bits(y);
-                else
-                    reinterpret_cast<float *>(out)[orow * C_OUT + col] = y;
+            acc0[i] = 0.f;
+            acc1[i] = 0.f;
+        }
+    };
+
+    int b = 0;  // parity of tile i's neighbour buffer
+    bool first = true;
+    for (int64_t k = tile0; k < n_tiles; k += tstride, b ^= 1) {
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            // wait for slices j .. j+PD (see above), then the barrier
+            if (t >= 1 && t < T - 1 - S::PD)
+                rs::wait_vm_barrier<(T - 2 - S::PD) * S::DPS + 1>();
+            else
+                rs::wait_vm_barrier<(T - 2 - S::PD) * S::DPS>();
+            // slice j+T-1: tap T-1 of this tile (t = 0) or tap t-1 of the next
+            const int64_t lk = t == 0 ? k : k + tstride;
+            const int lt = t == 0 ? T - 1 : t - 1;
+            int u[S::DPS];
+            slice_nb(t == 0 ? b : b ^ 1, lt, u);
+            if (t == 0) {
+                if (!first) store_tile(k - tstride);
+                first = false;
+                load_nbr(k + 2 * tstride, b);
+            }
+            if (k == tile0 && t == 0) {
+#pragma unroll
+                for (int p = 0; p < S::PD; ++p) read_slice(p, p);
+            }
+            // operands of slice j + PD (tap (t + PD) mod T), PD = 2
+            if (S::PD != 1) read_slice((t + S::PD) % T, (t + S::PD) % (S::PD + 1));
+            __builtin_amdgcn_sched_barrier(0);
+            // MFMAs of slice j, with the DPS loads of slice j+T-1 spread
+            // between them so that the address unit works while they run
+            constexpr int GPL = S::GPT / S::DPS;  // groups per load
+#pragma unroll
+            for (int g = 0; g < S::GPT; ++g) {
+                const u32x4_t a = af[S::PD == 1 ? 0 : t % (S::PD + 1)][g];
+                const u32x4_t bb = bw[t * S::GPT + g];
+                if (BF16) {
+                    if (g & 1)
+                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                                       __builtin_bit_cast(bf16x8_t, bb), acc1, 0, 0, 0);
+                    else
+                        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                                       __builtin_bit_cast(bf16x8_t, bb), acc0, 0, 0, 0);
+                } else {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if (c & 1)
+                            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[c]), __uint_as_float(bb[c]),
+                                                                        acc1, 0, 0, 0);
+                        else
+                            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[c]), __uint_as_float(bb[c]),
+                                                                        acc0, 0, 0, 0);
+                    }
+                }
+                if (S::PD == 1) read_group((t + 1) % T, 0, g);  // operands of slice j+1
+                if (g % GPL == GPL - 1) slice_load(lk, lt, g / GPL, u[g / GPL]);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
+        // The operands of the next tile's first PD slices were read into
+        // af[(t' + T) % (PD + 1)]; the tile body expects them at af[t'].
+        if (S::PD != 1 && T % (S::PD + 1) != 0) {
+            u32x4_t tmp[S::PD + 1][S::GPT];
+#pragma unroll
+            for (int p = 0; p < S::PD; ++p)
+#pragma unroll
+                for (int g = 0; g < S::GPT; ++g) tmp[p][g] = af[(p + T) % (S::PD + 1)][g];
+#pragma unroll
+            for (int p = 0; p < S::PD; ++p)
+#pragma unroll
+                for (int g = 0; g < S::GPT; ++g) af[p][g] = tmp[p][g];
+        }
     }
+    store_tile(n_tiles - 1 - (n_tiles - 1 - tile0) % tstride);
 }
 
 // Any storage/compute combination, one thread per output element.
@@ -768,10 +1129,10 @@ hipError_t launch_ws(lattice *L, const void *in, const void *w, int C_out, const
     return hipGetLastError();
 }
 
-template <bool OUT_BF16, int T, int C_IN, int C_OUT>
+template <bool BF16, bool OUT_BF16, int T, int C_IN, int C_OUT, int KS>
 hipError_t launch_rs(lattice *L, const void *in, const void *w, const float *bias, void *out) {
-    using S = RsShape<C_IN, C_OUT, T>;
-    auto kern = k_conv_rs<OUT_BF16, T, C_IN, C_OUT>;
+    using S = RsShape<BF16, C_IN, C_OUT, T, KS>;
+    auto kern = k_conv_rs<BF16, OUT_BF16, T, C_IN, C_OUT, KS>;
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
@@ -784,9 +1145,28 @@ hipError_t launch_rs(lattice *L, const void *in, const void *w, const float *bia
     int64_t grid = (int64_t)L->cu_count * per_cu;
     if (grid > tiles) grid = tiles;
     if (grid < 1) grid = 1;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), S::LDS, L->stream,
-                       reinterpret_cast<const uint16_t *>(in), reinterpret_cast<const uint16_t *>(w), bias, out,
-                       L->nbr, L->max_vertices * (int64_t)L->T, L->counters, L->zero_row);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), S::LDS, L->stream, in, w, bias, out, L->nbr,
+                       L->max_vertices * (int64_t)L->T, L->counters, L->zero_row);
+    return hipGetLastError();
+}
+
+template <bool BF16, bool OUT_BF16, int T, int C_IN, int C_OUT>
+hipError_t launch_ring(lattice *L, const void *in, const void *w, const float *bias, void *out) {
+    using S = RingShape<BF16, C_IN, C_OUT, T>;
+    auto kern = k_conv_ring<BF16, OUT_BF16, T, C_IN, C_OUT>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const int64_t tiles = (L->max_vertices + S::MT - 1) / S::MT;
+    int64_t grid = (int64_t)L->cu_count;
+    if (grid > tiles) grid = tiles;
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), S::LDS, L->stream, in, w, bias, out, L->nbr,
+                       L->max_vertices * (int64_t)L->T, L->counters, L->zero_row);
     return hipGetLastError();
 }
 
@@ -796,10 +1176,11 @@ template <bool OUT_BF16>
 bool try_rs(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias, void *out,
             hipError_t *err) {
     const int T = L->T;
-    if (T == 9 && C_in == 64 && C_out == 64) *err = launch_rs<OUT_BF16, 9, 64, 64>(L, in, w, bias, out);
-    else if (T == 9 && C_in == 64 && C_out == 128) *err = launch_rs<OUT_BF16, 9, 64, 128>(L, in, w, bias, out);
-    else if (T == 9 && C_in == 128 && C_out == 128) *err = launch_rs<OUT_BF16, 9, 128, 128>(L, in, w, bias, out);
-    else if (T == 11 && C_in == 64 && C_out == 128) *err = launch_rs<OUT_BF16, 11, 64, 128>(L, in, w, bias, out);
+    if (T == 11 && C_in == 64 && C_out == 64) *err = launch_ring<true, OUT_BF16, 11, 64, 64>(L, in, w, bias, out);
+    else if (T == 9 && C_in == 64 && C_out == 64) *err = launch_rs<true, OUT_BF16, 9, 64, 64, 1>(L, in, w, bias, out);
+    else if (T == 9 && C_in == 64 && C_out == 128) *err = launch_rs<true, OUT_BF16, 9, 64, 128, 1>(L, in, w, bias, out);
+    else if (T == 9 && C_in == 128 && C_out == 128) *err = launch_rs<true, OUT_BF16, 9, 128, 128, 1>(L, in, w, bias, out);
+    else if (T == 11 && C_in == 64 && C_out == 128) *err = launch_rs<true, OUT_BF16, 11, 64, 128, 1>(L, in, w, bias, out);
     else return false;
     return true;
 }
@@ -853,6 +1234,10 @@ hipError_t dispatch_out(lattice *L, const void *in, lattice_dtype in_dt, int C_i
         hipError_t err = hipSuccess;
         if (try_rs<OUT_BF16>(L, in, C_in, w, C_out, bias, out, &err)) return err;
     }
+    // fp32 64 -> 64: the register-resident kernel (K split over two
+    // wavefronts) only on request; the LDS-tiled kernel is faster there
+    if (aligned && path == LATTICE_CONV_RS && !bf16 && !in_bf16 && L->T == 9 && C_in == 64 && C_out == 64)
+        return launch_rs<false, OUT_BF16, 9, 64, 64, 2>(L, in, w, bias, out);
     if (aligned && path != LATTICE_CONV_TILED) {
         hipError_t err = hipSuccess;
         if (try_ws<OUT_BF16>(L, in, in_bf16, C_in, w, C_out, bf16, bias, out, &err)) return err;

@@ -456,3 +456,25 @@ def test_conv_every_path_bf16(big_lattices, d, C_in, C_out):
                 assert_close_scaled(got, ref, tol, 1.0, f"{path} conv {C_in}x{C_out} d={d} out {out_dtype}")
     finally:
         L.set_conv_path("auto")
+
+
+@pytest.mark.parametrize("d,C_in,C_out", [(3, 64, 64), (4, 64, 64), (3, 32, 128)])
+def test_conv_every_path_f32(big_lattices, d, C_in, C_out):
+    """fp32 rows and weights on every kernel family (the register-resident
+    ring kernel covers 64 -> 64 with 9 taps, the others fall back)."""
+    L, g, lat, nbr = big_lattices[d]
+    x = random_rows(lat.V, C_in, seed=981)
+    W = conv_weight(C_in, C_out, d, seed=982)
+    b = random_rows(1, C_out, seed=983)[0]
+    ref, scale = O.conv(x.astype(np.float64), nbr, W.astype(np.float64), b)
+    xin = g.to_gpu_order(x)
+    try:
+        for path in ("tiled", "ws", "rs"):
+            L.set_conv_path(path)
+            for out_dtype in ("f32", "bf16"):
+                out = L.conv(xin, to_dev(W), dtype="f32", bias=to_dev(b), out_dtype=out_dtype)
+                got = g.from_gpu_order(out.float())
+                tol = REL_F32 * scale + (BF16_ULP * np.abs(ref) if out_dtype == "bf16" else 0.0)
+                assert_close_scaled(got, ref, tol, 1.0, f"{path} f32 conv {C_in}x{C_out} d={d} out {out_dtype}")
+    finally:
+        L.set_conv_path("auto")
