@@ -81,7 +81,7 @@ struct lattice {
 // splat.hip
 hipError_t launch_clear_table(lattice *L);
 hipError_t launch_insert(lattice *L, const float *pos, const int32_t *batch, int64_t m);
-hipError_t launch_number(lattice *L);
+hipError_t launch_number(lattice *L, int64_t m);
 hipError_t launch_fill(lattice *L, int64_t m);
 hipError_t launch_gather(lattice *L, const float *feat, int C, int normalize, void *values, lattice_dtype values_dt,
                          float *weight);
@@ -99,6 +99,28 @@ hipError_t launch_conv(lattice *L, const void *in, lattice_dtype in_dt, int C_in
 
 // slice.hip
 hipError_t launch_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, float *out);
+
+// Workgroups are handed to the eight XCDs round robin (workgroup b runs on
+// XCD b % 8, checked on the device), and each XCD has its own L2.  Kernels
+// that give each workgroup one contiguous chunk of the work take chunk
+// xcd_order(b): the workgroups of one XCD then cover consecutive chunks, so
+// that neighbouring items (and the rows they share) meet in the same L2.
+// (Measured: this helps the pair-list fill; the vertex-row gathers of the
+// splat and the slice run faster with the plain interleaved order.)
+__device__ __forceinline__ int64_t xcd_order(int64_t b, int64_t nb) {
+    if (nb % 8 != 0) return b;
+    return (b % 8) * (nb / 8) + b / 8;
+}
+
+// This workgroup's chunk [lo, hi) of n items, chunks a multiple of `align`.
+__device__ __forceinline__ void block_chunk(int64_t n, int64_t align, int64_t &lo, int64_t &hi) {
+    const int64_t nb = gridDim.x;
+    int64_t per = (n + nb - 1) / nb;
+    per = (per + align - 1) / align * align;
+    lo = xcd_order(blockIdx.x, nb) * per;
+    if (lo > n) lo = n;
+    hi = lo + per < n ? lo + per : n;
+}
 
 // Grid size for a grid-stride kernel over `work` items with `per_block`
 // items per block, capped so that the launch stays a few waves deep.

@@ -289,7 +289,7 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
     if (s) return s;
     if ((s = check_launch(L, launch_clear_table(L), "clear_table"))) return s;
     if ((s = check_launch(L, launch_insert(L, pos, batch, m), "insert"))) return s;
-    if ((s = check_launch(L, launch_number(L), "number"))) return s;
+    if ((s = check_launch(L, launch_number(L, m), "number"))) return s;
     if ((s = check_launch(L, launch_fill(L, m), "fill"))) return s;
     if (C > 0 || weight)
         if ((s = check_launch(L, launch_gather(L, feat, C, normalize, values, values_dtype, weight), "gather")))

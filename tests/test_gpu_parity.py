@@ -478,3 +478,29 @@ def test_conv_every_path_f32(big_lattices, d, C_in, C_out):
                 assert_close_scaled(got, ref, tol, 1.0, f"{path} f32 conv {C_in}x{C_out} d={d} out {out_dtype}")
     finally:
         L.set_conv_path("auto")
+
+
+@pytest.mark.parametrize("d,ordered,batched", [(3, True, False), (4, True, False), (3, False, False),
+                                               (3, True, True)])
+def test_splat_large_cloud_insert_paths(d, ordered, batched):
+    """Clouds of at least 256 points per CU take the insert kernel that
+    merges each workgroup's keys in LDS first; spatially ordered points (a
+    sweep) share most vertices within a workgroup, shuffled ones almost none.
+    The point count leaves a ragged last workgroup."""
+    m = 70001
+    rng = np.random.default_rng(990 + d)
+    pos = rng.uniform(-1, 1, size=(m, d)).astype(np.float32)
+    if ordered:
+        pos = pos[np.lexsort(pos.T[::-1])]  # sorted along the first axis: neighbours in index order
+    batch = rng.integers(0, 7, size=m).astype(np.int32) if batched else None
+    if batched and ordered:
+        batch = np.sort(batch)
+    feat = rng.standard_normal((m, 8)).astype(np.float32)
+    sigma = 0.08 if d == 3 else 0.25
+    L = _lattice(d, sigma, m)
+    g = GpuLattice(L, pos, feat, batch=batch)
+    lat = O.build(pos, sigma, batch=batch)
+    check_lattice(g, lat)
+    ref, wref, scale = O.splat(lat, feat)
+    assert_close_scaled(g.values(), ref, scale, REL_F32, "large-cloud splat")
+    assert_close_scaled(g.weight(), wref, wref, REL_F32, "large-cloud weight")
