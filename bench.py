@@ -9,9 +9,11 @@ conv is bf16) are resident in HBM before the timed region; every step
 rebuilds the lattice from scratch.
 
 Prints one JSON line.  `value` is points per second of whole steps; the
-`roofline` object reports the step's dominant kernel against its own
-roofline, timed with HIP events recorded on the stream the kernels run on;
-`cpu_baseline` is the CPU oracle timed on this host on a bounded sample.
+`roofline` object reports the step's slowest single-kernel stage (the
+neighbour search, a conv or the slice) against its own roofline, timed with
+HIP events recorded on the stream the kernels run on; `stages` gives every
+stage, the multi-kernel splat included; `cpu_baseline` is the CPU oracle
+timed on this host on a bounded sample.
 
 Usage: python bench.py [--steps K] [--warmup W] [--config N] [--no-cpu-baseline]
 """
@@ -338,7 +340,11 @@ def main(argv=None):
 
     work = algorithmic_work(w, V)
     stages = {n: dict(ms=stage_ms[n], **roofline_entry(n, stage_ms[n], work[n])) for n in names}
-    dominant = max(names, key=lambda n: stage_ms[n])
+    # the roofline object covers one kernel: the slowest stage that is a
+    # single launch (neighbours, each conv, slice); the splat stage (seven
+    # kernels) is reported in `stages` with its own HBM roofline
+    single = [n for n in names if n != "splat"]
+    dominant = max(single, key=lambda n: stage_ms[n])
     rf = dict(stages[dominant])
     rf.pop("ms")
     rf["kernel"] = dominant
