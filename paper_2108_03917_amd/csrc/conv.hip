@@ -455,9 +455,9 @@ __global__ __launch_bounds__(512) void k_conv_ws(const void *__restrict__ in, co
 //   body:  T steps of KG/T operand groups (ds_read + MFMA)
 //   store: (KS = 2: partial sums through LDS) bias, fp32 or bf16
 // A missing neighbour (index -1) and the rows past V of the last tile read
-// a zero row.  16-byte chunk c of tile row r sits at chunk c ^ (r % 8) of
-// the row's LDS slot (and weight row n likewise with n % 8), so that the
-// 32-row operand reads spread over the LDS banks.
+// a zero row.  16-byte chunks of tile rows (and of staged weight rows) are
+// XOR-swizzled by row (rs::swz), so that the 32-row operand reads spread
+// over the LDS banks.
 namespace rs {
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -469,6 +469,18 @@ __device__ __forceinline__ void dma16(const void *src, char *lds_wave_base) {
 // direct-to-LDS loads included), then the workgroup barrier.  The memory
 // clobber keeps the compiler from moving LDS accesses across it.
 __device__ __forceinline__ void drain_and_barrier() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// XOR key of row r for rows of P 16-byte chunks in LDS: chunk c of row r is
+// stored at chunk c ^ swz<P>(r).  Sixteen consecutive rows of a 16-lane
+// read pass then hit sixteen different 16-byte bank groups (256 bytes of
+// banks): with P a multiple of 16 the key is r mod 16; with P an odd
+// multiple of 8, rows alternate between the two bank halves and the key is
+// (r / 2) mod 8.
+template <int P>
+__device__ __forceinline__ int swz(int r) {
+    static_assert(P % 16 == 0 || (P % 8 == 0 && (P / 8) % 2 == 1), "row pitch");
+    return P % 16 == 0 ? (r & 15) : ((r >> 1) & 7);
+}
 
 // Barrier after this wavefront's LDS operations (no wait on global memory).
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -640,7 +652,7 @@ __global__ __launch_bounds__(256) void k_conv_rs(const void *__restrict__ in_, c
         const int r = pr / S::CPR;
         const int cs = pr - r * S::CPR;
         const bool ok = r < V - k * S::MT && u >= 0;
-        const void *src = ok ? (const void *)(in + ((int64_t)u * C_IN * S::ESZ + ((cs ^ (r & 7)) * 16)))
+        const void *src = ok ? (const void *)(in + ((int64_t)u * C_IN * S::ESZ + ((cs ^ rs::swz<S::CPR>(r)) * 16)))
                              : (const void *)zero_row;
         rs::dma16(src, abuf(b) + (wave * S::ADMA + a) * 1024);
     };
@@ -658,7 +670,7 @@ __global__ __launch_bounds__(256) void k_conv_rs(const void *__restrict__ in_, c
             const int r = q / S::WCPR;
             const int cs = q - r * S::WCPR;
             const int n = n0 + r;
-            rs::dma16(w + ((int64_t)n * S::WCPR + (cs ^ (n & 7))) * 16, lds + (wave * S::W_DMA + a) * 1024);
+            rs::dma16(w + ((int64_t)n * S::WCPR + (cs ^ rs::swz<S::WCPR>(n))) * 16, lds + (wave * S::W_DMA + a) * 1024);
         }
         if (rd == 0) load_nbr(tile0, 0);
         rs::drain_and_barrier();
@@ -668,7 +680,7 @@ __global__ __launch_bounds__(256) void k_conv_rs(const void *__restrict__ in_, c
 #pragma unroll
             for (int kk = 0; kk < S::KGW; ++kk) {
                 const int kg = ks * S::KGW + kk;
-                bw[kk] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ (n & 7)) * 16));
+                bw[kk] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ rs::swz<S::WCPR>(n)) * 16));
             }
         }
         rs::drain_and_barrier();
@@ -706,7 +718,7 @@ __global__ __launch_bounds__(256) void k_conv_rs(const void *__restrict__ in_, c
             const int kg = ks * S::KGW + kk;
             const int t = kg / S::GPT;
             const int g = kg - t * S::GPT;
-            return *reinterpret_cast<const u32x4_t *>(arow + t * S::SLICE * 16 + (((2 * g + h) ^ (r & 7)) * 16));
+            return *reinterpret_cast<const u32x4_t *>(arow + t * S::SLICE * 16 + (((2 * g + h) ^ rs::swz<S::CPR>(r)) * 16));
         };
         // Operand groups are read PD steps ahead of their MFMAs (one
         // wavefront per SIMD: nothing else hides the LDS latency).  With
@@ -876,7 +888,7 @@ __global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_,
         const int r = q / S::CPR;
         const int cs = q - r * S::CPR;
         const bool ok = r < V - k * S::MT && u >= 0;
-        const void *src = ok ? (const void *)(in + ((int64_t)u * C_IN * S::ESZ + ((cs ^ (r & 7)) * 16)))
+        const void *src = ok ? (const void *)(in + ((int64_t)u * C_IN * S::ESZ + ((cs ^ rs::swz<S::CPR>(r)) * 16)))
                              : (const void *)zero_row;
         rs::dma16(src, slot(t) + (wave * S::DPS + i) * 1024);
     };
@@ -905,7 +917,7 @@ __global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_,
             const int r = q / S::WCPR;
             const int cs = q - r * S::WCPR;
             const int n = n0 + r;
-            rs::dma16(w + ((int64_t)n * S::WCPR + (cs ^ (n & 7))) * 16, lds + (wave * S::W_DMA + a) * 1024);
+            rs::dma16(w + ((int64_t)n * S::WCPR + (cs ^ rs::swz<S::WCPR>(n))) * 16, lds + (wave * S::W_DMA + a) * 1024);
         }
         if (rd == 0) {
             load_nbr(tile0, 0);
@@ -917,7 +929,7 @@ __global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_,
             const char *row = lds + (n - n0) * S::WCPR * 16;
 #pragma unroll
             for (int kg = 0; kg < T * S::GPT; ++kg)
-                bw[kg] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ (n & 7)) * 16));
+                bw[kg] = *reinterpret_cast<const u32x4_t *>(row + (((2 * kg + h) ^ rs::swz<S::WCPR>(n)) * 16));
         }
         rs::drain_and_barrier();
     }
@@ -932,7 +944,7 @@ __global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_,
     u32x4_t af[NSETS][S::GPT];
     auto read_group = [&](int t, int sl, int g) {
         const char *arow = slot(t) + r * S::CPR * 16;
-        af[sl][g] = *reinterpret_cast<const u32x4_t *>(arow + (((2 * g + h) ^ (r & 7)) * 16));
+        af[sl][g] = *reinterpret_cast<const u32x4_t *>(arow + (((2 * g + h) ^ rs::swz<S::CPR>(r)) * 16));
     };
     auto read_slice = [&](int t, int sl) {
 #pragma unroll
