@@ -308,3 +308,57 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
     lsb = (u >> 16) & 1
     u = ((u + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
     return u.view(F32)
+
+
+def deform_slice(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta: np.ndarray, b_delta: float,
+                 w_cls: Optional[np.ndarray] = None, b_cls: Optional[np.ndarray] = None):
+    """DeformSlice (Sec. "Proposed Operations", DeformSlicing; Eq. deformSlice),
+    optionally followed by the final linear classifier (Sec. "Implementation":
+    the two are one fused operation).  float64 throughout.
+
+    For point p with simplex vertices v = idx[p, k] and weights b_pk, in the
+    paper's order:
+      Gather       q_pk = b_pk x_v                                  [m, d+1, C]
+      MaxPool      mx_p = max over the d+1 vertices of q_pk, per channel
+      SubtractMax  q_pk - mx_p
+      Linear+Tanh  db_pk = tanh(b_delta + (q_pk - mx_p) . w_delta)  [m, d+1]
+      slice        f_p = sum_k (b_pk + db_pk) x_v                   [m, C]
+      classifier   logits_p = f_p W_cls^T + b_cls                   [m, n_cls]
+    The max runs over all d+1 vertices, v included (the formula; the prose
+    says "the other vertices").  The nonlinearity is tanh (the network
+    figure's Linear+Tanh).
+
+    Returns (out, delta, scale): out is f or the logits, delta the offsets,
+    and scale the magnitude against which a float32 evaluation's rounding is
+    measured: for f, sum_k (|b| + |db|)|x| plus sum_k |x| times the tanh
+    argument's sum of |terms| (tanh has slope at most 1); for the logits,
+    that scale and |f| carried through |W_cls| plus |b_cls|."""
+    idx = np.asarray(idx, dtype=np.int64)
+    b = np.asarray(bary, dtype=np.float64)
+    X = np.asarray(values, dtype=np.float64)
+    w = np.asarray(w_delta, dtype=np.float64)
+    m, dp1 = idx.shape
+    C = X.shape[1]
+    rows = np.zeros((m, dp1, C))
+    valid = idx >= 0
+    rows[valid] = X[idx[valid]]
+    q = b[:, :, None] * rows                                  # Gather
+    mx = q.max(axis=1)                                        # MaxPool
+    diff = q - mx[:, None, :]                                 # SubtractMax
+    arg = b_delta + diff @ w                                  # Linear
+    delta = np.tanh(arg)                                      #   + Tanh
+    f = ((b + delta)[:, :, None] * rows).sum(axis=1)          # slice with b + db
+    arg_scale = abs(b_delta) + (np.abs(q) + np.abs(mx)[:, None, :]) @ np.abs(w)
+    absrows = np.abs(rows)
+    f_scale = ((np.abs(b) + np.abs(delta))[:, :, None] * absrows).sum(axis=1) \
+        + (arg_scale[:, :, None] * absrows).sum(axis=1)
+    if w_cls is None:
+        return f, delta, f_scale
+    Wc = np.asarray(w_cls, dtype=np.float64)                  # [n_cls, C]
+    logits = f @ Wc.T
+    scale = (f_scale + np.abs(f)) @ np.abs(Wc).T
+    if b_cls is not None:
+        bc = np.asarray(b_cls, dtype=np.float64)
+        logits = logits + bc
+        scale = scale + np.abs(bc)
+    return logits, delta, scale

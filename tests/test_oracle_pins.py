@@ -418,3 +418,80 @@ def test_bf16_rounding_matches_torch():
     ref = torch.from_numpy(a).to(torch.bfloat16).to(torch.float32).numpy()
     got = O.round_bf16(a)
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+# --------------------------------------------------------------------------
+# DeformSlice + classifier (Sec. "Proposed Operations": DeformSlicing;
+# Sec. "Implementation": fused with the last linear layer)
+# --------------------------------------------------------------------------
+
+def test_deform_slice_worked_examples():
+    """Hand-derived tanh arguments (golden file) pin the Gather / MaxPool /
+    SubtractMax / Linear order; f and the logits follow by direct sums."""
+    import math
+    with open(os.path.join(GOLDEN, "deform_slice_worked_examples.json")) as fh:
+        ex = json.load(fh)["examples"]
+    for e in ex:
+        b = e["bary"]
+        rows = e["rows"]
+        dp1, C = len(rows), len(rows[0])
+        delta = [math.tanh(a) for a in e["args"]]
+        f = [sum((b[k] + delta[k]) * rows[k][c] for k in range(dp1)) for c in range(C)]
+        X = np.array(rows)
+        idx = np.arange(dp1)[None, :]
+        out, dl, _ = O.deform_slice(idx, np.array([b]), X, np.array(e["w_delta"]), e["b_delta"])
+        np.testing.assert_allclose(dl[0], delta, rtol=0, atol=1e-15)
+        np.testing.assert_allclose(out[0], f, rtol=0, atol=1e-13)
+        if "w_cls" in e:
+            logits, _, _ = O.deform_slice(idx, np.array([b]), X, np.array(e["w_delta"]), e["b_delta"],
+                                          np.array(e["w_cls"]), np.array(e["b_cls"]))
+            np.testing.assert_allclose(logits[0], [f[0], f[1] + 1.0, f[0] + f[1] - 1.0], rtol=0, atol=1e-13)
+
+
+def test_deform_slice_reduces_to_slice_and_saturates():
+    """Zero offset weights and bias give Eq. (slice); a large bias drives
+    every offset to +-1, adding +- the plain sum of the simplex's rows."""
+    w = random_cloud(300, 3, seed=61, extent=1.0, C=1)
+    lat = O.build(w.pos, 0.2)
+    X = np.random.default_rng(62).standard_normal((lat.V, 5))
+    f0, d0, _ = O.deform_slice(lat.idx, lat.bary, X, np.zeros(5), 0.0)
+    ref, _ = O.slice_(lat, X)
+    assert np.all(d0 == 0.0)
+    np.testing.assert_allclose(f0, ref, rtol=0, atol=1e-12)
+    rowsum = np.zeros((lat.m, 5))
+    for p in range(lat.m):
+        for k in range(4):
+            rowsum[p] += X[lat.idx[p, k]]
+    for sgn in (1.0, -1.0):
+        f, dl, _ = O.deform_slice(lat.idx, lat.bary, X, np.ones(5), sgn * 40.0)
+        assert np.all(dl == sgn)
+        np.testing.assert_allclose(f, ref + sgn * rowsum, rtol=0, atol=1e-12)
+
+
+def test_deform_slice_is_permutation_equivariant():
+    """Enumerating a simplex's vertices in another order permutes the
+    offsets the same way and leaves f unchanged (the max is symmetric)."""
+    w = random_cloud(200, 2, seed=63, extent=1.0, C=1)
+    lat = O.build(w.pos, 0.3)
+    rng = np.random.default_rng(64)
+    X = rng.standard_normal((lat.V, 6))
+    wd = rng.standard_normal(6)
+    f, dl, _ = O.deform_slice(lat.idx, lat.bary, X, wd, 0.3)
+    perm = np.argsort(rng.random(lat.idx.shape), axis=1)
+    idx_p = np.take_along_axis(lat.idx, perm, axis=1)
+    bary_p = np.take_along_axis(lat.bary, perm, axis=1)
+    f2, dl2, _ = O.deform_slice(idx_p, bary_p, X, wd, 0.3)
+    np.testing.assert_allclose(f2, f, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dl2, np.take_along_axis(dl, perm, axis=1), rtol=0, atol=0)
+
+
+def test_deform_slice_identity_classifier():
+    """An identity classifier with zero bias returns f itself."""
+    w = random_cloud(100, 3, seed=65, extent=1.0, C=1)
+    lat = O.build(w.pos, 0.2)
+    rng = np.random.default_rng(66)
+    X = rng.standard_normal((lat.V, 4))
+    wd = rng.standard_normal(4)
+    f, _, _ = O.deform_slice(lat.idx, lat.bary, X, wd, -0.2)
+    lg, _, _ = O.deform_slice(lat.idx, lat.bary, X, wd, -0.2, np.eye(4), np.zeros(4))
+    np.testing.assert_allclose(lg, f, rtol=0, atol=0)
