@@ -15,7 +15,11 @@ HIP events recorded on the stream the kernels run on; `stages` gives every
 stage, the multi-kernel splat included; `cpu_baseline` is the CPU oracle
 timed on this host on a bounded sample.
 
-Usage: python bench.py [--steps K] [--warmup W] [--config N] [--no-cpu-baseline]
+With --op deform the step ends in DeformSlice fused with the linear
+classifier (per-point logits, the network's output layer) instead of the
+plain slice, and the `roofline` object covers that kernel.
+
+Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -53,12 +57,13 @@ class Pipeline:
     (V stays on the device), so the step can be captured once as a HIP graph
     and replayed."""
 
-    def __init__(self, w, stream=None):
+    def __init__(self, w, stream=None, tail="slice"):
         import torch
 
         from paper_2108_03917_amd import Lattice
 
         self.w = w
+        self.tail = tail
         dev = torch.device("cuda:0")
         torch.cuda.set_device(dev)
         self.stream = stream if stream is not None else torch.cuda.Stream(device=dev)
@@ -83,7 +88,16 @@ class Pipeline:
             self.weights.append(wd)
             self.outs.append(torch.empty((mv, cv.c_out), dtype=storage(i + 1), device=dev))
         c_last = self.convs[-1].c_out if self.convs else w.C
-        self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
+        if tail == "deform":
+            from datagen.clouds import N_CLASSES, deform_weights
+
+            self.dw = deform_weights(c_last, N_CLASSES.get(w.config, 20), seed=100 + w.config)
+            self.w_delta = torch.from_numpy(self.dw.w_delta).to(dev)
+            self.w_cls = torch.from_numpy(self.dw.w_cls).to(dev)
+            self.b_cls = torch.from_numpy(self.dw.b_cls).to(dev)
+            self.sliced = torch.empty((w.m, self.w_cls.shape[0]), dtype=torch.float32, device=dev)
+        else:
+            self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
         torch.cuda.synchronize()
 
     @property
@@ -139,16 +153,19 @@ class Pipeline:
             L.conv(x, wd, dtype=cv.dtype, out=out)
             x = out
         mark()
-        L.slice(x, out=self.sliced)
+        if self.tail == "deform":
+            L.deform_slice(x, self.w_delta, self.dw.b_delta, self.w_cls, self.b_cls, out=self.sliced)
+        else:
+            L.slice(x, out=self.sliced)
         mark()
         return self.sliced
 
     def stage_names(self):
         return ["splat", "neighbors"] + [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}" for i, c in enumerate(self.convs)] \
-            + ["slice"]
+            + [self.tail]
 
 
-def algorithmic_work(w, V):
+def algorithmic_work(w, V, n_cls=0):
     """Compulsory HBM bytes (and MFMA flops) of each stage of one step.
 
     splat:     read positions (4d B), batch id (4 B), features (4C B) and write
@@ -159,7 +176,10 @@ def algorithmic_work(w, V):
                row (s' C_out) per vertex, plus the weights once; 2 T C_in C_out
                flops per vertex (s, s' = 2 for bf16-stored rows, else 4).
     slice:     read the record (8(d+1)) and write the output row (4C) per point,
-               read each vertex row once (4C per vertex)."""
+               read each vertex row once (4C per vertex).
+    deform:    DeformSlice + classifier: read the record (8(d+1)) and write
+               the logits (4 n_cls) per point, read each vertex row once (4C
+               per vertex), plus the weights (4(C + n_cls C + n_cls)) once."""
     d, m, C = w.d, w.m, w.C
     T = 2 * (d + 1) + 1
     work = {}
@@ -175,6 +195,7 @@ def algorithmic_work(w, V):
             "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": cv.dtype}
     c_last = w.convs[-1].c_out if w.convs else C
     work["slice"] = {"bytes": m * (8 * (d + 1) + 4 * c_last) + V * 4 * c_last}
+    work["deform"] = {"bytes": m * (8 * (d + 1) + 4 * n_cls) + V * 4 * c_last + 4 * (c_last + n_cls * c_last + n_cls)}
     return work
 
 
@@ -191,10 +212,11 @@ def roofline_entry(name, ms, wk):
     return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a / HBM_PEAK_GBS}
 
 
-def cpu_baseline(w, budget_s=20.0):
+def cpu_baseline(w, budget_s=20.0, dw=None):
     """The CPU oracle, as it stands, over the same workload: whole steps
-    (lattice build, splat, neighbours, every conv, slice) repeated until
-    about `budget_s` seconds, reported as points/s."""
+    (lattice build, splat, neighbours, every conv, slice -- or DeformSlice
+    with the classifier when `dw` holds its weights) repeated until about
+    `budget_s` seconds, reported as points/s."""
     from threadpoolctl import threadpool_info
 
     from oracle import lattice_oracle as O
@@ -210,7 +232,10 @@ def cpu_baseline(w, budget_s=20.0):
                 xi = O.round_bf16(x.astype(np.float32))
                 Wt = O.round_bf16(Wt)
             x, _ = O.conv(xi, nbr, Wt)
-        O.slice_(lat, x)
+        if dw is None:
+            O.slice_(lat, x)
+        else:
+            O.deform_slice(lat.idx, lat.bary, x, dw.w_delta, dw.b_delta, dw.w_cls, dw.b_cls)
 
     t0 = time.perf_counter()
     n = 0
@@ -234,6 +259,7 @@ STAGE_SOURCES = {
     "neighbors": ["neighbors.hip", "keys.h", "internal.h"],
     "conv": ["conv.hip", "internal.h"],
     "slice": ["slice.hip", "internal.h"],
+    "deform": ["deform.hip", "internal.h"],
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -283,6 +309,8 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG)
+    ap.add_argument("--op", choices=("slice", "deform"), default="slice",
+                    help="end the step with the plain slice or with DeformSlice + classifier")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
@@ -301,7 +329,7 @@ def main(argv=None):
     from datagen.clouds import make_workload
 
     w = make_workload(args.config)
-    pipe = Pipeline(w)
+    pipe = Pipeline(w, tail=args.op)
     for _ in range(args.warmup):
         pipe.run()
     pipe.stream.synchronize()
@@ -338,13 +366,15 @@ def main(argv=None):
             stage_ms[n] += evs[s_][i].elapsed_time(evs[s_][i + 1])
     stage_ms = {n: v / args.steps for n, v in stage_ms.items()}
 
-    work = algorithmic_work(w, V)
+    n_cls = pipe.w_cls.shape[0] if args.op == "deform" else 0
+    work = algorithmic_work(w, V, n_cls)
     stages = {n: dict(ms=stage_ms[n], **roofline_entry(n, stage_ms[n], work[n])) for n in names}
     # the roofline object covers one kernel: the slowest stage that is a
     # single launch (neighbours, each conv, slice); the splat stage (seven
     # kernels) is reported in `stages` with its own HBM roofline
+    # (with --op deform: the DeformSlice + classifier kernel itself)
     single = [n for n in names if n != "splat"]
-    dominant = max(single, key=lambda n: stage_ms[n])
+    dominant = "deform" if args.op == "deform" else max(single, key=lambda n: stage_ms[n])
     rf = dict(stages[dominant])
     rf.pop("ms")
     rf["kernel"] = dominant
@@ -354,7 +384,8 @@ def main(argv=None):
         rf["algorithmic_flops"] = work[dominant]["flops"]
 
     out = {
-        "metric": "points/s for splat+conv+slice",
+        "metric": "points/s for splat+conv+slice" if args.op == "slice" else
+                  "points/s for splat+conv+deformslice+classifier",
         "value": w.m * args.steps / sec,
         "unit": "points/s",
         "n_gpus": 1,
@@ -368,7 +399,8 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES.get(args.config, w.name), "points": w.m, "d": w.d,
                    "sigma": float(w.sigma[0]), "channels": w.C, "vertices": V,
-                   "convs": [f"{c.c_in}->{c.c_out} {c.dtype}" for c in w.convs]},
+                   "convs": [f"{c.c_in}->{c.c_out} {c.dtype}" for c in w.convs]}
+                  | ({"classes": n_cls, "tail": "deformslice+classifier"} if args.op == "deform" else {}),
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
@@ -377,7 +409,7 @@ def main(argv=None):
                    "same stream"),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, pipe.dw if args.op == "deform" else None)
     print(json.dumps(out))
     return 0
 

@@ -359,3 +359,31 @@ def random_rows(n: int, C: int, seed: int, std: float = 1.0) -> np.ndarray:
     """Seeded N(0, std^2) float32 rows [n, C]: stand-alone inputs for one stage
     (vertex values fed to a convolution or a slice)."""
     return (np.random.default_rng(seed).standard_normal((n, C)) * std).astype(np.float32)
+
+
+# Output classes of the label sets each workload stands in for (50 part
+# labels for part segmentation, 20 semantic classes for the indoor and the
+# single-scan LiDAR benchmarks, 26 for the multi-scan one with moving
+# classes); the tiny cloud takes 8.  Used only as the classifier's width.
+N_CLASSES = {1: 8, 2: 50, 3: 20, 4: 20, 5: 26}
+
+
+@dataclass
+class DeformWeights:
+    w_delta: np.ndarray  # float32 [C]: the offsets' linear layer
+    b_delta: float       # its bias
+    w_cls: np.ndarray    # float32 [n_cls][C]: the classifier
+    b_cls: np.ndarray    # float32 [n_cls]
+
+
+def deform_weights(C: int, n_cls: int, seed: int, gain: float = 3.0) -> DeformWeights:
+    """Seeded weights for a DeformSlice + classifier layer on C-channel vertex
+    values: w_delta ~ N(0, gain^2 / C) (so that the offsets' pre-activations
+    of N(0,1) rows spread over tanh's curved range rather than saturating),
+    b_delta ~ N(0, 0.25), w_cls ~ N(0, 1/C), b_cls ~ N(0, 0.01)."""
+    rng = np.random.default_rng(seed)
+    w_delta = (rng.standard_normal(C) * (gain / np.sqrt(C))).astype(np.float32)
+    b_delta = float(np.float32(rng.standard_normal() * 0.5))
+    w_cls = (rng.standard_normal((n_cls, C)) / np.sqrt(C)).astype(np.float32)
+    b_cls = (rng.standard_normal(n_cls) * 0.1).astype(np.float32)
+    return DeformWeights(w_delta, b_delta, w_cls, b_cls)

@@ -218,6 +218,42 @@ lattice_status lattice_set_conv_path(lattice *L, int path);
 lattice_status lattice_slice(lattice *L, const void *values, lattice_dtype values_dtype, int C, float *out);
 
 /*
+ * lattice_deform_slice -- slice with learned offsets on the barycentric
+ * weights (DeformSlice), optionally fused with a linear classifier.
+ *
+ * Sec. "Proposed Operations" (DeformSlicing), Eq. (deformSlice) and the
+ * network figure's DeformSlice block; Sec. "Implementation" fuses the final
+ * classifier so that the per-point features are never written.  For point p
+ * of the last splat, with simplex vertices v_k and weights b_k (k <= d):
+ *   q_k   = b_k x_{v_k}                     (Gather)
+ *   mx    = max_k q_k, per channel          (MaxPool over all d+1 vertices)
+ *   db_k  = tanh(b_delta + (q_k - mx) . w_delta)
+ *   f_p   = sum_k (b_k + db_k) x_{v_k}
+ *   out_p = f_p, or f_p W_cls^T + b_cls when w_cls is given.
+ * fp32 products and sums; tanh in fp32.
+ *   values        dev [V][C] vertex values (the last lattice conv's output).
+ *   values_dtype  storage of `values`: LATTICE_F32 or LATTICE_BF16.
+ *   C             channels, 1..1024; above 256 C must be a multiple of 4
+ *                 and values, w_delta and (w_cls or out) aligned to 16
+ *                 bytes (8 for bf16 values) -- true of every device
+ *                 allocation and of row offsets that are multiples of 4.
+ *   w_delta       dev [C] fp32 weights of the offsets' linear layer.
+ *   b_delta       its bias (a host value).
+ *   w_cls         dev [n_cls][C] fp32 classifier weights, or NULL for none.
+ *   b_cls         dev [n_cls] fp32 classifier bias, or NULL (zero).
+ *   n_cls         classes, 1..256 (ignored without w_cls).
+ *   out           dev fp32 [m][n_cls] logits with w_cls, else [m][C] f_p;
+ *                 must not overlap `values`.
+ *   delta         dev fp32 [m][d+1] receives db (the learned offsets), or
+ *                 NULL.
+ * Caller owns every buffer.  Returns LATTICE_E_STATE before the first splat,
+ * LATTICE_E_ARG for a size or pointer outside the above.
+ */
+lattice_status lattice_deform_slice(lattice *L, const void *values, lattice_dtype values_dtype, int C,
+                                    const float *w_delta, float b_delta, const float *w_cls, const float *b_cls,
+                                    int n_cls, float *out, float *delta);
+
+/*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to
  * even) on the lattice's stream: the weight format LATTICE_BF16 convs take.
  *   src  dev [n] fp32;  dst  dev [n] uint16 (bf16 bit patterns).
@@ -254,13 +290,19 @@ lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary);
 /*
  * Stage timing.  With lattice_set_timing(L, 1) the library records a pair of
  * hipEvents on its stream around every stage it launches (splat, neighbours,
- * conv, slice) and accumulates their elapsed times; lattice_get_timing
+ * conv, slice, deform slice) and accumulates their elapsed times; lattice_get_timing
  * synchronises and returns, per stage, the summed milliseconds and the number
  * of launches since the last reset (arrays of LATTICE_NUM_STAGES).
  * lattice_set_timing(L, 0) stops recording; (L, 2) resets the sums.
  */
-#define LATTICE_NUM_STAGES 4
-enum { LATTICE_STAGE_SPLAT = 0, LATTICE_STAGE_NEIGHBORS = 1, LATTICE_STAGE_CONV = 2, LATTICE_STAGE_SLICE = 3 };
+#define LATTICE_NUM_STAGES 5
+enum {
+    LATTICE_STAGE_SPLAT = 0,
+    LATTICE_STAGE_NEIGHBORS = 1,
+    LATTICE_STAGE_CONV = 2,
+    LATTICE_STAGE_SLICE = 3,
+    LATTICE_STAGE_DEFORM = 4
+};
 lattice_status lattice_set_timing(lattice *L, int mode);
 lattice_status lattice_get_timing(lattice *L, double *ms, int64_t *count);
 

@@ -311,7 +311,8 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
 
 
 def deform_slice(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta: np.ndarray, b_delta: float,
-                 w_cls: Optional[np.ndarray] = None, b_cls: Optional[np.ndarray] = None):
+                 w_cls: Optional[np.ndarray] = None, b_cls: Optional[np.ndarray] = None,
+                 with_delta_scale: bool = False):
     """DeformSlice (Sec. "Proposed Operations", DeformSlicing; Eq. deformSlice),
     optionally followed by the final linear classifier (Sec. "Implementation":
     the two are one fused operation).  float64 throughout.
@@ -332,7 +333,10 @@ def deform_slice(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta:
     and scale the magnitude against which a float32 evaluation's rounding is
     measured: for f, sum_k (|b| + |db|)|x| plus sum_k |x| times the tanh
     argument's sum of |terms| (tanh has slope at most 1); for the logits,
-    that scale and |f| carried through |W_cls| plus |b_cls|."""
+    that scale and |f| carried through |W_cls| plus |b_cls|.  With
+    with_delta_scale a fourth item follows: the tanh argument's sum of
+    |terms| [m, d+1], the scale of the offsets' rounding (plus tanh's own
+    few ulps)."""
     idx = np.asarray(idx, dtype=np.int64)
     b = np.asarray(bary, dtype=np.float64)
     X = np.asarray(values, dtype=np.float64)
@@ -352,8 +356,9 @@ def deform_slice(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta:
     absrows = np.abs(rows)
     f_scale = ((np.abs(b) + np.abs(delta))[:, :, None] * absrows).sum(axis=1) \
         + (arg_scale[:, :, None] * absrows).sum(axis=1)
+    extra = (arg_scale,) if with_delta_scale else ()
     if w_cls is None:
-        return f, delta, f_scale
+        return (f, delta, f_scale) + extra
     Wc = np.asarray(w_cls, dtype=np.float64)                  # [n_cls, C]
     logits = f @ Wc.T
     scale = (f_scale + np.abs(f)) @ np.abs(Wc).T
@@ -361,4 +366,4 @@ def deform_slice(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta:
         bc = np.asarray(b_cls, dtype=np.float64)
         logits = logits + bc
         scale = scale + np.abs(bc)
-    return logits, delta, scale
+    return (logits, delta, scale) + extra

@@ -100,6 +100,13 @@ hipError_t launch_conv(lattice *L, const void *in, lattice_dtype in_dt, int C_in
 // slice.hip
 hipError_t launch_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, float *out);
 
+// deform.hip
+int deform_max_channels(const void *values, lattice_dtype values_dt, int C, const float *w_delta, const float *w_cls,
+                        const float *out);
+hipError_t launch_deform_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, const float *w_delta,
+                               float b_delta, const float *w_cls, const float *b_cls, int n_cls, float *out,
+                               float *delta);
+
 // Workgroups are handed to the eight XCDs round robin (workgroup b runs on
 // XCD b % 8, checked on the device), and each XCD has its own L2.  Kernels
 // that give each workgroup one contiguous chunk of the work take chunk

@@ -361,6 +361,35 @@ lattice_status lattice_slice(lattice *L, const void *values, lattice_dtype value
     return timer_end(L, LATTICE_STAGE_SLICE, t0);
 }
 
+lattice_status lattice_deform_slice(lattice *L, const void *values, lattice_dtype values_dtype, int C,
+                                    const float *w_delta, float b_delta, const float *w_cls, const float *b_cls,
+                                    int n_cls, float *out, float *delta) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "deform_slice: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    if (C < 1 || (values_dtype != LATTICE_F32 && values_dtype != LATTICE_BF16) || (w_cls && (n_cls < 1 || n_cls > 256)) ||
+        (!w_cls && b_cls) || (L->m > 0 && (!values || !w_delta || !out))) {
+        set_err(L, "deform_slice: bad argument (C = %d, n_cls = %d)", C, n_cls);
+        return LATTICE_E_ARG;
+    }
+    const int cmax = deform_max_channels(values, values_dtype, C, w_delta, w_cls, out);
+    if (C > cmax) {
+        set_err(L, "deform_slice: C = %d above %d (C above 256 needs a multiple of 4 and aligned rows)", C, cmax);
+        return LATTICE_E_ARG;
+    }
+    hipEvent_t t0;
+    lattice_status s = timer_begin(L, LATTICE_STAGE_DEFORM, &t0);
+    if (s) return s;
+    if ((s = check_launch(L,
+                          launch_deform_slice(L, values, values_dtype, C, w_delta, b_delta, w_cls, b_cls, n_cls, out,
+                                              delta),
+                          "deform_slice")))
+        return s;
+    return timer_end(L, LATTICE_STAGE_DEFORM, t0);
+}
+
 lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst) {
     if (!L || n < 0 || (n > 0 && (!src || !dst))) return LATTICE_E_ARG;
     return check_launch(L, launch_to_bf16(L, src, n, dst), "to_bf16");

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "_lib", "liblattice.so")
 
 OK, E_ARG, E_STATE, E_RANGE, E_CAPACITY, E_NOMEM, E_HIP = range(7)
 F32, BF16 = 0, 1
-STAGES = ("splat", "neighbors", "conv", "slice")
+STAGES = ("splat", "neighbors", "conv", "slice", "deform")
 
 EXPORTS = (
     "lattice_create", "lattice_destroy", "lattice_max_vertices", "lattice_splat", "lattice_build_neighbors",
@@ -27,7 +27,7 @@ EXPORTS = (
     "lattice_slice", "lattice_weights_to_bf16", "lattice_num_vertices", "lattice_get_status",
     "lattice_get_keys", "lattice_get_neighbors", "lattice_get_point_simplex", "lattice_set_timing",
     "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
-    "lattice_last_error", "lattice_set_conv_path",
+    "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice",
 )
 
 _lib = None
@@ -57,6 +57,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_build_neighbors": (St, [P]),
         "lattice_conv": (St, [P, P, I, I, P, I, I, P, P, I]),
         "lattice_slice": (St, [P, P, I, I, P]),
+        "lattice_deform_slice": (St, [P, P, I, I, P, ctypes.c_float, P, P, I, P, P]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
         "lattice_num_vertices": (St, [P, ctypes.POINTER(I64)]),
         "lattice_get_status": (St, [P]),
@@ -255,6 +256,50 @@ class Lattice:
         self._check(self._lib.lattice_slice(self._h, _ptr(values), _STORAGE[values.dtype], C, _ptr(out)), "slice")
         return out
 
+    def deform_slice(self, values: torch.Tensor, w_delta: torch.Tensor, b_delta: float,
+                     w_cls: Optional[torch.Tensor] = None, b_cls: Optional[torch.Tensor] = None,
+                     out: Optional[torch.Tensor] = None, delta: Optional[torch.Tensor] = None,
+                     want_delta: bool = False):
+        """DeformSlice (Eq. deformSlice) onto the points of the last splat,
+        fused with the classifier ``f W_cls^T + b_cls`` when ``w_cls`` [n_cls, C]
+        is given.  Returns ``out`` ([m, n_cls] logits or [m, C] features, fp32)
+        and, with ``want_delta`` or a ``delta`` tensor, the offsets [m, d+1]."""
+        _dev(values, (torch.float32, torch.bfloat16), "values")
+        if values.dim() != 2 or values.shape[0] < self._rows_needed():
+            raise ValueError(f"values needs >= {self._rows_needed()} rows")
+        C = values.shape[1]
+        _dev(w_delta, torch.float32, "w_delta")
+        if w_delta.numel() != C:
+            raise ValueError("w_delta needs C entries")
+        n_cls = 0
+        if w_cls is not None:
+            _dev(w_cls, torch.float32, "w_cls")
+            if w_cls.dim() != 2 or w_cls.shape[1] != C:
+                raise ValueError("w_cls needs [n_cls, C]")
+            n_cls = w_cls.shape[0]
+            if b_cls is not None:
+                _dev(b_cls, torch.float32, "b_cls")
+                if b_cls.numel() != n_cls:
+                    raise ValueError("b_cls needs n_cls entries")
+        elif b_cls is not None:
+            raise ValueError("b_cls without w_cls")
+        width = n_cls if w_cls is not None else C
+        if out is None:
+            out = torch.empty((self.m, width), dtype=torch.float32, device=values.device)
+        _dev(out, torch.float32, "out")
+        if out.numel() < self.m * width:
+            raise ValueError(f"out needs [m, {width}]")
+        if delta is None and want_delta:
+            delta = torch.empty((self.m, self.d + 1), dtype=torch.float32, device=values.device)
+        if delta is not None:
+            _dev(delta, torch.float32, "delta")
+            if delta.numel() < self.m * (self.d + 1):
+                raise ValueError("delta needs [m, d+1]")
+        self._check(self._lib.lattice_deform_slice(self._h, _ptr(values), _STORAGE[values.dtype], C, _ptr(w_delta),
+                                                   float(b_delta), _ptr(w_cls), _ptr(b_cls), n_cls, _ptr(out),
+                                                   _ptr(delta)), "deform_slice")
+        return (out, delta) if delta is not None else out
+
     def weights_to_bf16(self, w: torch.Tensor) -> torch.Tensor:
         """Round fp32 weights to bf16 (nearest even) with the library's kernel."""
         _dev(w, torch.float32, "w")
@@ -293,8 +338,8 @@ class Lattice:
         self._check(self._lib.lattice_set_timing(self._h, int(mode)), "set_timing")
 
     def timing(self):
-        ms = (ctypes.c_double * 4)()
-        cnt = (ctypes.c_int64 * 4)()
+        ms = (ctypes.c_double * len(STAGES))()
+        cnt = (ctypes.c_int64 * len(STAGES))()
         self._check(self._lib.lattice_get_timing(self._h, ms, cnt), "get_timing")
         return {s: (float(ms[i]), int(cnt[i])) for i, s in enumerate(STAGES)}
 

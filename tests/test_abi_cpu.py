@@ -21,7 +21,8 @@ def _declared():
 
 def test_header_declares_the_hot_path():
     names = _declared()
-    for n in ("lattice_create", "lattice_splat", "lattice_conv", "lattice_slice", "lattice_destroy"):
+    for n in ("lattice_create", "lattice_splat", "lattice_conv", "lattice_slice", "lattice_deform_slice",
+              "lattice_destroy"):
         assert n in names
 
 
@@ -69,6 +70,7 @@ def test_null_lattice_is_rejected():
     assert lib.lattice_splat(None, None, None, 0, None, 0, 0, None, 0, None) == B.E_ARG
     assert lib.lattice_conv(None, None, 0, 1, None, 1, 0, None, None, 0) == B.E_ARG
     assert lib.lattice_slice(None, None, 0, 1, None) == B.E_ARG
+    assert lib.lattice_deform_slice(None, None, 0, 1, None, 0.0, None, None, 0, None, None) == B.E_ARG
     assert lib.lattice_get_status(None) == B.E_ARG
     V = ctypes.c_int64()
     assert lib.lattice_num_vertices(None, ctypes.byref(V)) == B.E_ARG

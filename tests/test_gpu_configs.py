@@ -5,13 +5,15 @@ Per workload: the lattice (keys, per-point vertices, weights, neighbours) is
 compared bit-exactly; splat values within 1e-5 of the sum of |terms|; each of
 the workload's convolutions is fed the oracle's splat values and compared on
 every vertex; slice is fed the oracle's conv output and compared on every
-point.
+point; DeformSlice with the fused classifier (the workload's class count) is
+fed seeded rows of the last conv's width and compared on a seeded sample of
+points.
 """
 import numpy as np
 import pytest
 import torch
 
-from datagen.clouds import make_workload
+from datagen.clouds import N_CLASSES, deform_weights, make_workload, random_rows
 from oracle import lattice_oracle as O
 from tests.gpu_util import REL_BF16, REL_F32, GpuLattice, assert_close_scaled, check_lattice, to_dev
 
@@ -64,6 +66,15 @@ def test_full_config_parity(config):
         sref, sscale = O.slice_(lat, y32)
         r = assert_close_scaled(sl, sref, sscale, REL_F32, "slice")
         print(f"  slice C={cv.c_out} max rel {r:.2e}", flush=True)
+    c_last = w.convs[-1].c_out
+    dw = deform_weights(c_last, N_CLASSES[config], seed=100 + config)
+    yv = random_rows(lat.V, c_last, seed=1500 + config)
+    got = L.deform_slice(g.to_gpu_order(yv), to_dev(dw.w_delta), dw.b_delta, to_dev(dw.w_cls),
+                         to_dev(dw.b_cls)).cpu().numpy()
+    sel = np.sort(np.random.default_rng(config).choice(w.m, size=min(w.m, 60000), replace=False))
+    ref, _, dscale = O.deform_slice(lat.idx[sel], lat.bary[sel], yv, dw.w_delta, dw.b_delta, dw.w_cls, dw.b_cls)
+    r = assert_close_scaled(got[sel], ref, dscale, REL_F32, "deform+classifier")
+    print(f"  deform C={c_last} classes={N_CLASSES[config]} on {len(sel)} points max rel {r:.2e}", flush=True)
     L.close()
 
 
