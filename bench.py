@@ -12,8 +12,11 @@ Prints one JSON line.  `value` is points per second of whole steps; the
 `roofline` object reports the step's slowest single-kernel stage (the
 neighbour search, a conv or the slice) against its own roofline, timed with
 HIP events recorded on the stream the kernels run on; `stages` gives every
-stage, the multi-kernel splat included; `cpu_baseline` is the CPU oracle
-timed on this host on a bounded sample.
+stage, the multi-kernel splat included (mean, and p10 / median / p90 over the
+steps); `stages_cold` repeats that with the caches evicted before every step;
+`hbm_frac_splat_slice` is the splat and slice bytes over their time against
+peak HBM; `cpu_baseline` is the CPU oracle timed on this host on a bounded
+sample with all its BLAS threads, `cpu_baseline_1core` with one.
 
 With --op deform the step ends in DeformSlice fused with the linear
 classifier (per-point logits, the network's output layer) instead of the
@@ -312,6 +315,7 @@ def main(argv=None):
     ap.add_argument("--op", choices=("slice", "deform"), default="slice",
                     help="end the step with the plain slice or with DeformSlice + classifier")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cache-flushed stage timings")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--graph", action="store_true", help="time graph replays of the step instead of eager steps")
@@ -360,15 +364,36 @@ def main(argv=None):
     for s_ in range(args.steps):
         pipe.run(evs[s_])
     torch.cuda.synchronize()
-    stage_ms = {n: 0.0 for n in names}
-    for s_ in range(args.steps):
-        for i, n in enumerate(names):
-            stage_ms[n] += evs[s_][i].elapsed_time(evs[s_][i + 1])
-    stage_ms = {n: v / args.steps for n, v in stage_ms.items()}
+    samples = {n: [evs[s_][i].elapsed_time(evs[s_][i + 1]) for s_ in range(args.steps)] for i, n in enumerate(names)}
+    stage_ms = {n: float(np.mean(v)) for n, v in samples.items()}
+
+    # Timed region 3 (cold): before every step a 512 MiB buffer is written
+    # (outside the events), which evicts the 256 MiB Infinity Cache and the
+    # L2s, so each stage starts from HBM as the first touch of a new cloud would.
+    cold = None
+    if not args.no_cold:
+        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda:0")
+        n_cold = min(args.steps, 50)
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(n_cold)]
+        torch.cuda.synchronize()
+        for s_ in range(n_cold):
+            with torch.cuda.stream(pipe.stream):
+                flush.fill_(float(s_))
+            pipe.run(cev[s_])
+        torch.cuda.synchronize()
+        cold = {n: [cev[s_][i].elapsed_time(cev[s_][i + 1]) for s_ in range(n_cold)] for i, n in enumerate(names)}
+        del flush
 
     n_cls = pipe.w_cls.shape[0] if args.op == "deform" else 0
     work = algorithmic_work(w, V, n_cls)
-    stages = {n: dict(ms=stage_ms[n], **roofline_entry(n, stage_ms[n], work[n])) for n in names}
+    def pct(v):
+        return {"p10": float(np.percentile(v, 10)), "median": float(np.median(v)), "p90": float(np.percentile(v, 90))}
+
+    stages = {n: dict(ms=stage_ms[n], ms_pct=pct(samples[n]), **roofline_entry(n, stage_ms[n], work[n]))
+              for n in names}
+    if cold is not None:
+        stages_cold = {n: dict(ms_pct=pct(cold[n]), **roofline_entry(n, float(np.median(cold[n])), work[n]))
+                       for n in names}
     # the roofline object covers one kernel: the slowest stage that is a
     # single launch (neighbours, each conv, slice); the splat stage (seven
     # kernels) is reported in `stages` with its own HBM roofline
@@ -404,12 +429,23 @@ def main(argv=None):
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
+        "hbm_frac_splat_slice": None if args.op != "slice" else
+        (work["splat"]["bytes"] + work["slice"]["bytes"]) / ((stage_ms["splat"] + stage_ms["slice"]) * 1e-3)
+        / (HBM_PEAK_GBS * 1e9),
         "timing": ("value: " + ("graph replays" if args.graph else "eager steps") + " of the whole step, no "
                    "events inside; stages and roofline: HIP events around each stage of eager steps on the "
-                   "same stream"),
+                   "same stream; stages_cold: the same after evicting the caches before every step "
+                   "(512 MiB write, outside the events), roofline of the median"),
     }
+    if cold is not None:
+        out["stages_cold"] = stages_cold
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, pipe.dw if args.op == "deform" else None)
+        dw = pipe.dw if args.op == "deform" else None
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, dw)
+        from threadpoolctl import threadpool_limits
+
+        with threadpool_limits(limits=1):
+            out["cpu_baseline_1core"] = cpu_baseline(w, args.cpu_budget / 2, dw)
     print(json.dumps(out))
     return 0
 
