@@ -367,3 +367,85 @@ def deform_slice(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta:
         logits = logits + bc
         scale = scale + np.abs(bc)
     return (logits, delta, scale) + extra
+
+
+# ---------------------------------------------------------------------------
+# Backward passes (Sec. "Implementation": the network is trained end to end,
+# so every lattice operation needs the gradient of a loss with respect to its
+# inputs).  Each one is the transpose of the forward linear map, written out
+# as its own definition: the derivative of a scalar loss L through
+# y = forward(x) is dL/dx = J^T dL/dy, with J the forward's Jacobian.
+# ---------------------------------------------------------------------------
+
+def slice_backward(lat: Lattice, grad_out: np.ndarray):
+    """Gradient of Eq. (slice) with respect to the vertex values, float64.
+
+    f_p = sum_k b_pk y_{idx[p,k]}  gives  dL/dy_v = sum over the (p, k) with
+    idx[p, k] = v of b_pk dL/df_p: each point scatters its gradient onto its
+    d+1 simplex vertices with the barycentric weights.  Returns (grad [V, C],
+    scale = the same sum of |terms|)."""
+    g = np.asarray(grad_out, dtype=np.float64)
+    m, dp1 = lat.idx.shape
+    out = np.zeros((lat.V, g.shape[1]))
+    scale = np.zeros_like(out)
+    for k in range(dp1):
+        v = lat.idx[:, k]
+        b = lat.bary[:, k][:, None]
+        np.add.at(out, v, b * g)
+        np.add.at(scale, v, np.abs(b * g))
+    return out, scale
+
+
+def splat_backward(lat: Lattice, grad_values: np.ndarray, normalize: bool = False,
+                   weight: Optional[np.ndarray] = None):
+    """Gradient of Eq. (splat) with respect to the point features, float64.
+
+    Raw splat x_v = sum_p b_pv f_p gives dL/df_p = sum_k b_pk dL/dx_{idx[p,k]}.
+    The normalised splat x_v / w_v (w_v = sum_p b_pv does not depend on f)
+    divides each vertex's gradient by w_v first (0 where w_v = 0, where the
+    forward value is the constant 0).  Returns (grad [m, C], scale)."""
+    g = np.asarray(grad_values, dtype=np.float64)
+    if normalize:
+        w = np.asarray(weight, dtype=np.float64)
+        inv = np.zeros_like(w)
+        inv[w != 0] = 1.0 / w[w != 0]
+        g = g * inv[:, None]
+    m, dp1 = lat.idx.shape
+    out = np.zeros((m, g.shape[1]))
+    scale = np.zeros_like(out)
+    for k in range(dp1):
+        b = lat.bary[:, k][:, None]
+        rows = g[lat.idx[:, k]]
+        out += b * rows
+        scale += np.abs(b * rows)
+    return out, scale
+
+
+def conv_backward(values: np.ndarray, nbr: np.ndarray, weight: np.ndarray, grad_out: np.ndarray):
+    """Gradients of the 1-ring convolution (Sec. "Common Operations":
+    Convolving), float64.
+
+    y_v[o] = sum_t sum_i x_{nbr(v,t)}[i] W[o,t,i] (+ bias[o]) gives
+      dL/dx_u[i]   = sum over (v, t) with nbr(v,t) = u of sum_o g_v[o] W[o,t,i]
+                     (each output row scatters back along the tap it read);
+      dL/dW[o,t,i] = sum_v g_v[o] x_{nbr(v,t)}[i]   (absent taps read zero);
+      dL/dbias[o]  = sum_v g_v[o].
+    Returns (grad_x, grad_w, grad_bias) and their sum-of-|terms| scales
+    (grad_x_scale, grad_w_scale, grad_bias_scale)."""
+    x = np.asarray(values, dtype=np.float64)
+    W = np.asarray(weight, dtype=np.float64)
+    g = np.asarray(grad_out, dtype=np.float64)
+    V = x.shape[0]
+    c_out, T, c_in = W.shape
+    gx = np.zeros((V, c_in))
+    gx_s = np.zeros((V, c_in))
+    gw = np.zeros((c_out, T, c_in))
+    gw_s = np.zeros((c_out, T, c_in))
+    for t in range(T):
+        present = nbr[:, t] >= 0
+        src = nbr[present, t]
+        np.add.at(gx, src, g[present] @ W[:, t, :])
+        np.add.at(gx_s, src, np.abs(g[present]) @ np.abs(W[:, t, :]))
+        gw[:, t, :] = g[present].T @ x[src]
+        gw_s[:, t, :] = np.abs(g[present]).T @ np.abs(x[src])
+    return gx, gw, g.sum(axis=0), gx_s, gw_s, np.abs(g).sum(axis=0)

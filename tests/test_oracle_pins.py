@@ -495,3 +495,111 @@ def test_deform_slice_identity_classifier():
     f, _, _ = O.deform_slice(lat.idx, lat.bary, X, wd, -0.2)
     lg, _, _ = O.deform_slice(lat.idx, lat.bary, X, wd, -0.2, np.eye(4), np.zeros(4))
     np.testing.assert_allclose(lg, f, rtol=0, atol=0)
+
+
+# --------------------------------------------------------------------------
+# backward passes: each gradient is the transpose of the forward's Jacobian.
+# Pinned against the Jacobian itself, built column by column from the forward
+# oracle (pinned above) on tiny lattices, and against torch autograd.
+# --------------------------------------------------------------------------
+
+def _tiny_lattice(d=3, m=40, seed=21, sigma=0.35):
+    w = random_cloud(m, d, seed, extent=1.0, C=2)
+    return w, O.build(w.pos, sigma)
+
+
+def _jacobian(f, shape_in):
+    """Dense Jacobian of a linear map by applying it to every unit input."""
+    n = int(np.prod(shape_in))
+    cols = []
+    for j in range(n):
+        e = np.zeros(n)
+        e[j] = 1.0
+        cols.append(np.asarray(f(e.reshape(shape_in)), dtype=np.float64).ravel())
+    return np.stack(cols, axis=1)
+
+
+@pytest.mark.parametrize("d", [2, 3, 4])
+def test_slice_backward_is_jacobian_transpose(d):
+    w, lat = _tiny_lattice(d=d, seed=20 + d)
+    C = 2
+    J = _jacobian(lambda y: O.slice_(lat, y)[0], (lat.V, C))
+    g = np.random.default_rng(d).standard_normal((lat.m, C))
+    got, scale = O.slice_backward(lat, g)
+    assert np.allclose(got.ravel(), J.T @ g.ravel(), rtol=1e-12, atol=1e-12)
+    assert np.all(scale >= np.abs(got) - 1e-12)
+
+
+@pytest.mark.parametrize("normalize", [False, True])
+def test_splat_backward_is_jacobian_transpose(normalize):
+    w, lat = _tiny_lattice(d=3, seed=31)
+    C = 2
+    J = _jacobian(lambda f: O.splat(lat, f, normalize=normalize)[0], (lat.m, C))
+    _, wt, _ = O.splat(lat, w.feat)
+    g = np.random.default_rng(5).standard_normal((lat.V, C))
+    got, _ = O.splat_backward(lat, g, normalize=normalize, weight=wt)
+    assert np.allclose(got.ravel(), J.T @ g.ravel(), rtol=1e-12, atol=1e-12)
+
+
+def test_splat_backward_zero_weight_vertex():
+    """A vertex whose every pair has weight 0 holds the constant 0 in the
+    normalised splat, so no gradient flows through it."""
+    pos = np.array([[0.0, 0.0, 0.0]], dtype=np.float32)   # on a remainder-0 vertex: 3 weights are 0
+    lat = O.build(pos, 1.0)
+    _, wt, _ = O.splat(lat, np.ones((1, 1), dtype=np.float32))
+    assert (wt == 0).sum() == 3
+    g = np.ones((lat.V, 1))
+    got, _ = O.splat_backward(lat, g, normalize=True, weight=wt)
+    assert np.allclose(got, 1.0)  # only the weight-1 vertex contributes, with 1/w = 1
+
+
+@pytest.mark.parametrize("d", [2, 3])
+def test_conv_backward_is_jacobian_transpose(d):
+    w, lat = _tiny_lattice(d=d, m=30, seed=40 + d)
+    nbr = O.neighbors(lat)
+    T = nbr.shape[1]
+    rng = np.random.default_rng(d)
+    c_in, c_out = 2, 3
+    x = rng.standard_normal((lat.V, c_in))
+    W = rng.standard_normal((c_out, T, c_in))
+    bias = rng.standard_normal(c_out)
+    g = rng.standard_normal((lat.V, c_out))
+    gx, gw, gb, gx_s, gw_s, gb_s = O.conv_backward(x, nbr, W, g)
+    Jx = _jacobian(lambda xx: O.conv(xx, nbr, W)[0], (lat.V, c_in))
+    Jw = _jacobian(lambda ww: O.conv(x, nbr, ww)[0], (c_out, T, c_in))
+    Jb = _jacobian(lambda bb: O.conv(x, nbr, W, bb)[0] - O.conv(x, nbr, W)[0], (c_out,))
+    assert np.allclose(gx.ravel(), Jx.T @ g.ravel(), rtol=1e-11, atol=1e-11)
+    assert np.allclose(gw.ravel(), Jw.T @ g.ravel(), rtol=1e-11, atol=1e-11)
+    assert np.allclose(gb, Jb.T @ g.ravel(), rtol=1e-11, atol=1e-11)
+    for got, s in ((gx, gx_s), (gw, gw_s), (gb, gb_s)):
+        assert np.all(s >= np.abs(got) - 1e-9)
+
+
+def test_backward_matches_torch_autograd():
+    """The whole chain splat -> conv -> slice, differentiated by torch autograd
+    (float64, CPU) from a forward written with sparse/dense torch products,
+    gives the oracle's chained backward."""
+    torch = pytest.importorskip("torch")
+    w, lat = _small_lattice(d=3, m=600, seed=12, C=3)
+    nbr = O.neighbors(lat)
+    T = nbr.shape[1]
+    rng = np.random.default_rng(3)
+    W = rng.standard_normal((4, T, 3))
+    gout = rng.standard_normal((lat.m, 4))
+    Bd = torch.from_numpy(lat.B.toarray())                          # [m, V]
+    f = torch.tensor(w.feat.astype(np.float64), requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    xv = Bd.T @ f                                                   # splat
+    Z = torch.zeros((lat.V, T, 3), dtype=torch.float64)
+    for t in range(T):
+        ok = torch.from_numpy(nbr[:, t] >= 0)
+        Z[ok, t] = xv[torch.from_numpy(nbr[nbr[:, t] >= 0, t])]
+    y = Z.reshape(lat.V, -1) @ Wt.reshape(4, -1).T                  # conv
+    out = Bd @ y                                                    # slice
+    (out * torch.from_numpy(gout)).sum().backward()
+    gy, _ = O.slice_backward(lat, gout)
+    vals, _, _ = O.splat(lat, w.feat)
+    gx, gw, _, _, _, _ = O.conv_backward(vals, nbr, W, gy)
+    gf, _ = O.splat_backward(lat, gx)
+    assert np.allclose(gw, Wt.grad.numpy(), rtol=1e-10, atol=1e-10)
+    assert np.allclose(gf, f.grad.numpy(), rtol=1e-10, atol=1e-10)
