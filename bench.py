@@ -22,7 +22,12 @@ With --op deform the step ends in DeformSlice fused with the linear
 classifier (per-point logits, the network's output layer) instead of the
 plain slice, and the `roofline` object covers that kernel.
 
-Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform] [--no-cpu-baseline]
+With --op train the step is the forward pass followed by its backward pass
+from a fixed point gradient dL/df: the slice's gradient (a splat of dL/df),
+each conv's input gradient and weight gradient in reverse order (two stages
+each), and the splat's gradient with respect to the point features.
+
+Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -101,6 +106,22 @@ class Pipeline:
             self.sliced = torch.empty((w.m, self.w_cls.shape[0]), dtype=torch.float32, device=dev)
         else:
             self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
+        if tail == "train":
+            from datagen.clouds import random_rows
+
+            # the loss gradient dL/df at the points: an input of the step
+            self.gout = torch.from_numpy(random_rows(w.m, c_last, seed=500 + w.config)).to(dev)
+            # a gradient row is stored as bf16 where the conv that reads it
+            # computes in bf16 (it would round it on load anyway)
+            def gstore(i):
+                return torch.bfloat16 if i >= 0 and self.convs[i].dtype == "bf16" else torch.float32
+            n = len(self.convs)
+            # dL/dy of the last conv (the slice's gradient), then dL/dx of each conv
+            self.gtop = torch.empty((mv, c_last), dtype=gstore(n - 1), device=dev)
+            self.gin = [torch.empty((mv, cv.c_in), dtype=gstore(i - 1), device=dev) for i, cv in enumerate(self.convs)]
+            self.gw = [torch.empty((cv.c_out, w.taps, cv.c_in), dtype=torch.float32, device=dev) for cv in self.convs]
+            self.gfeat = torch.empty((w.m, w.C), dtype=torch.float32, device=dev)
+            assert n > 0
         torch.cuda.synchronize()
 
     @property
@@ -160,12 +181,32 @@ class Pipeline:
             L.deform_slice(x, self.w_delta, self.dw.b_delta, self.w_cls, self.b_cls, out=self.sliced)
         else:
             L.slice(x, out=self.sliced)
+        if self.tail == "train":
+            n = len(self.convs)
+            mark()
+            L.slice_backward(self.gout, out=self.gtop)
+            for i in reversed(range(n)):
+                cv = self.convs[i]
+                xin = self.values if i == 0 else self.outs[i - 1]
+                gy = self.gtop if i == n - 1 else self.gin[i + 1]
+                mark()
+                L.conv_backward(gy, self.weights[i], dtype=cv.dtype, want_weight=False, grad_in=self.gin[i])
+                mark()
+                L.conv_backward(gy, self.weights[i], xin, dtype=cv.dtype, want_input=False, grad_w=self.gw[i])
+            mark()
+            L.splat_backward(self.gin[0], out=self.gfeat)
         mark()
         return self.sliced
 
     def stage_names(self):
-        return ["splat", "neighbors"] + [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}" for i, c in enumerate(self.convs)] \
-            + [self.tail]
+        fwd = ["splat", "neighbors"] + [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}" for i, c in enumerate(self.convs)]
+        if self.tail != "train":
+            return fwd + [self.tail]
+        bwd = ["slice_bwd"]
+        for i in reversed(range(len(self.convs))):
+            c = self.convs[i]
+            bwd += [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}_bwd_in", f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}_bwd_w"]
+        return fwd + ["slice"] + bwd + ["splat_bwd"]
 
 
 def algorithmic_work(w, V, n_cls=0):
@@ -199,6 +240,27 @@ def algorithmic_work(w, V, n_cls=0):
     c_last = w.convs[-1].c_out if w.convs else C
     work["slice"] = {"bytes": m * (8 * (d + 1) + 4 * c_last) + V * 4 * c_last}
     work["deform"] = {"bytes": m * (8 * (d + 1) + 4 * n_cls) + V * 4 * c_last + 4 * (c_last + n_cls * c_last + n_cls)}
+    # backward (--op train): a gradient row is bf16 where a bf16 conv reads it
+    def sg(i):
+        return 2 if i >= 0 and w.convs[i].dtype == "bf16" else 4
+    n = len(w.convs)
+    if n:
+        # slice backward: read dL/df (4 c_last) and the pair (8 B) per point-vertex pair, write the row
+        work["slice_bwd"] = {"bytes": m * (4 * c_last + 8 * (d + 1)) + V * sg(n - 1) * c_last}
+        for i, cv in enumerate(w.convs):
+            name = f"conv{i}_{cv.c_in}x{cv.c_out}_{cv.dtype}"
+            s_x = 2 if cv.dtype == "bf16" else 4
+            # input gradient: a forward conv C_out -> C_in with flipped weights
+            work[name + "_bwd_in"] = {
+                "bytes": V * (sg(i) * cv.c_out + 4 * T + sg(i - 1) * cv.c_in) + T * cv.c_in * cv.c_out * s_x,
+                "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": cv.dtype}
+            # weight gradient: read g, x and the neighbour row per vertex, write
+            # the fp32 weights; fp32 MFMA whatever the conv's dtype
+            work[name + "_bwd_w"] = {
+                "bytes": V * (sg(i) * cv.c_out + s_x * cv.c_in + 4 * T) + T * cv.c_in * cv.c_out * 4,
+                "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": "f32"}
+        # splat backward: the slice of the vertex gradient onto the points
+        work["splat_bwd"] = {"bytes": m * (8 * (d + 1) + 4 * C) + V * sg(-1) * C}
     return work
 
 
@@ -215,20 +277,29 @@ def roofline_entry(name, ms, wk):
     return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a / HBM_PEAK_GBS}
 
 
-def cpu_baseline(w, budget_s=20.0, dw=None):
+def cpu_baseline(w, budget_s=20.0, dw=None, train=False):
     """The CPU oracle, as it stands, over the same workload: whole steps
     (lattice build, splat, neighbours, every conv, slice -- or DeformSlice
-    with the classifier when `dw` holds its weights) repeated until about
-    `budget_s` seconds, reported as points/s."""
+    with the classifier when `dw` holds its weights; with `train` also the
+    backward pass of every stage) repeated until about `budget_s` seconds,
+    reported as points/s."""
     from threadpoolctl import threadpool_info
 
     from oracle import lattice_oracle as O
+
+    if train:
+        from datagen.clouds import random_rows
+
+        c_last = w.convs[-1].c_out if w.convs else w.C
+        gout = random_rows(w.m, c_last, seed=500 + w.config)
 
     def one():
         lat = O.build(w.pos, w.sigma, batch=w.batch)
         x, _, _ = O.splat(lat, w.feat)
         nbr = O.neighbors(lat)
+        ins = []
         for cv in w.convs:
+            ins.append(x)
             xi = x
             Wt = cv.weight
             if cv.dtype == "bf16":
@@ -239,6 +310,11 @@ def cpu_baseline(w, budget_s=20.0, dw=None):
             O.slice_(lat, x)
         else:
             O.deform_slice(lat.idx, lat.bary, x, dw.w_delta, dw.b_delta, dw.w_cls, dw.b_cls)
+        if train:
+            g, _ = O.slice_backward(lat, gout)
+            for cv, xi in zip(reversed(w.convs), reversed(ins)):
+                g, _, _, _, _, _ = O.conv_backward(xi, nbr, cv.weight, g)
+            O.splat_backward(lat, g)
 
     t0 = time.perf_counter()
     n = 0
@@ -312,8 +388,9 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG)
-    ap.add_argument("--op", choices=("slice", "deform"), default="slice",
-                    help="end the step with the plain slice or with DeformSlice + classifier")
+    ap.add_argument("--op", choices=("slice", "deform", "train"), default="slice",
+                    help="end the step with the plain slice, with DeformSlice + classifier, or run the "
+                         "forward and backward passes (train)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-flushed stage timings")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -398,7 +475,7 @@ def main(argv=None):
     # single launch (neighbours, each conv, slice); the splat stage (seven
     # kernels) is reported in `stages` with its own HBM roofline
     # (with --op deform: the DeformSlice + classifier kernel itself)
-    single = [n for n in names if n != "splat"]
+    single = [n for n in names if n not in ("splat", "slice_bwd")]
     dominant = "deform" if args.op == "deform" else max(single, key=lambda n: stage_ms[n])
     rf = dict(stages[dominant])
     rf.pop("ms")
@@ -409,8 +486,9 @@ def main(argv=None):
         rf["algorithmic_flops"] = work[dominant]["flops"]
 
     out = {
-        "metric": "points/s for splat+conv+slice" if args.op == "slice" else
-                  "points/s for splat+conv+deformslice+classifier",
+        "metric": {"slice": "points/s for splat+conv+slice",
+                   "deform": "points/s for splat+conv+deformslice+classifier",
+                   "train": "points/s for splat+conv+slice forward and backward"}[args.op],
         "value": w.m * args.steps / sec,
         "unit": "points/s",
         "n_gpus": 1,
@@ -425,11 +503,12 @@ def main(argv=None):
         "config": {"workload": WORKLOAD_NAMES.get(args.config, w.name), "points": w.m, "d": w.d,
                    "sigma": float(w.sigma[0]), "channels": w.C, "vertices": V,
                    "convs": [f"{c.c_in}->{c.c_out} {c.dtype}" for c in w.convs]}
-                  | ({"classes": n_cls, "tail": "deformslice+classifier"} if args.op == "deform" else {}),
+                  | ({"classes": n_cls, "tail": "deformslice+classifier"} if args.op == "deform" else {})
+                  | ({"tail": "slice, then the backward pass of every stage"} if args.op == "train" else {}),
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
-        "hbm_frac_splat_slice": None if args.op != "slice" else
+        "hbm_frac_splat_slice": None if args.op == "deform" else
         (work["splat"]["bytes"] + work["slice"]["bytes"]) / ((stage_ms["splat"] + stage_ms["slice"]) * 1e-3)
         / (HBM_PEAK_GBS * 1e9),
         "timing": ("value: " + ("graph replays" if args.graph else "eager steps") + " of the whole step, no "
@@ -439,7 +518,9 @@ def main(argv=None):
     }
     if cold is not None:
         out["stages_cold"] = stages_cold
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.op == "train":
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, None, train=True)
+    elif not args.no_cpu_baseline:
         dw = pipe.dw if args.op == "deform" else None
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, dw)
         from threadpoolctl import threadpool_limits

@@ -254,6 +254,79 @@ lattice_status lattice_deform_slice(lattice *L, const void *values, lattice_dtyp
                                     int n_cls, float *out, float *delta);
 
 /*
+ * Backward passes.  Sec. "Implementation": the network is trained end to
+ * end, so every lattice operation needs the gradient of a loss L with
+ * respect to its inputs.  Each forward is linear in what is differentiated,
+ * so each gradient is the transposed map of the forward with the same
+ * lattice (the last splat's simplex records and neighbour table).  All
+ * sums are fp32; the caller owns every buffer; rows 0..V-1 (or 0..m-1) are
+ * written.  Each returns LATTICE_E_STATE before the first splat and
+ * LATTICE_E_ARG for a bad size or a missing pointer.
+ */
+
+/*
+ * lattice_slice_backward -- gradient of Eq. (slice) with respect to the
+ * vertex values: dL/dy_v = sum over the points p with v in I_p of
+ * b_pv dL/df_p, i.e. Eq. (splat) applied to the point gradients.
+ *   grad_out      dev [m][C] fp32 dL/df (m of the last splat).
+ *   C             channels, 1..4096.
+ *   grad_values   dev [>= lattice_max_vertices][C] output dL/dy, rows 0..V-1
+ *                 written; must not overlap grad_out.
+ *   grad_dtype    storage of grad_values: LATTICE_F32, or LATTICE_BF16 (each
+ *                 fp32 sum rounded to nearest even).
+ * The first call with more channels than any splat before it grows the
+ * lattice's gather scratch (a device allocation).
+ */
+lattice_status lattice_slice_backward(lattice *L, const float *grad_out, int C, void *grad_values,
+                                      lattice_dtype grad_dtype);
+
+/*
+ * lattice_splat_backward -- gradient of Eq. (splat) with respect to the
+ * point features: dL/df_p = sum_k b_pk dL/dx_{v_k}, i.e. Eq. (slice)
+ * applied to the vertex gradients.  For the normalised splat (values
+ * x_v / w_v) each vertex gradient is divided by w_v first, and a vertex with
+ * w_v = 0 (whose value is the constant 0) passes no gradient.
+ *   grad_values   dev [V][C] dL/dx, stored as gv_dtype (LATTICE_F32 or LATTICE_BF16).
+ *   C             channels, 1..4096.
+ *   normalize     0: the raw splat;  1: the normalised splat.
+ *   weight        dev [V] fp32, the w_v the splat returned; required when
+ *                 normalize = 1, ignored otherwise.
+ *   grad_feat     dev [m][C] fp32 output dL/df.
+ */
+lattice_status lattice_splat_backward(lattice *L, const void *grad_values, lattice_dtype gv_dtype, int C,
+                                      int normalize, const float *weight, float *grad_feat);
+
+/*
+ * lattice_conv_backward -- gradients of lattice_conv (Sec. "Common
+ * Operations", Convolving):
+ *   dL/dx_u[i]    = sum over (v, t) with nbr(v,t) = u of sum_o g_v[o] W[o][t][i]
+ *   dL/dW[o][t][i] = sum_v g_v[o] x_{nbr(v,t)}[i]   (an absent tap reads zero)
+ *   dL/dbias[o]   = sum_v g_v[o]
+ * with g = dL/dy.  The input gradient is computed as a forward convolution
+ * of g with the flipped, transposed weights (the 1-ring is symmetric: tap
+ * 1+j of v is u exactly when tap d+2+j of u is v), on the same kernels as
+ * lattice_conv; the weight gradient is a product reduced over the vertices
+ * in fixed chunks added in a fixed order (run to run identical).
+ *   grad_out       dev [V][C_out] g, stored as g_dtype.
+ *   C_out, C_in    channels of the forward conv, 1..1024 each.
+ *   w              dev [C_out][T][C_in] forward weights (fp32 for dt =
+ *                  LATTICE_F32, bf16 for LATTICE_BF16); needed for grad_in.
+ *   dt             compute type as in lattice_conv: LATTICE_BF16 rounds g
+ *                  and x to bf16 before the products (exact products, fp32 sums).
+ *   in             dev [V][C_in] the forward input x, stored as in_dtype;
+ *                  needed for grad_w.
+ *   grad_in        dev [>= V][C_in] output dL/dx stored as grad_in_dtype, or NULL.
+ *   grad_w         dev [C_out][T][C_in] fp32 output dL/dW, or NULL.
+ *   grad_bias      dev [C_out] fp32 output dL/dbias, or NULL.
+ * The first call with a larger shape grows the lattice's backward scratch
+ * (flipped weights; one partial weight gradient per vertex chunk).
+ */
+lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
+                                     const void *w, int C_in, lattice_dtype dt, const void *in,
+                                     lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                     float *grad_w, float *grad_bias);
+
+/*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to
  * even) on the lattice's stream: the weight format LATTICE_BF16 convs take.
  *   src  dev [n] fp32;  dst  dev [n] uint16 (bf16 bit patterns).
@@ -295,13 +368,16 @@ lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary);
  * of launches since the last reset (arrays of LATTICE_NUM_STAGES).
  * lattice_set_timing(L, 0) stops recording; (L, 2) resets the sums.
  */
-#define LATTICE_NUM_STAGES 5
+#define LATTICE_NUM_STAGES 8
 enum {
     LATTICE_STAGE_SPLAT = 0,
     LATTICE_STAGE_NEIGHBORS = 1,
     LATTICE_STAGE_CONV = 2,
     LATTICE_STAGE_SLICE = 3,
-    LATTICE_STAGE_DEFORM = 4
+    LATTICE_STAGE_DEFORM = 4,
+    LATTICE_STAGE_SLICE_BACKWARD = 5,
+    LATTICE_STAGE_CONV_BACKWARD = 6,
+    LATTICE_STAGE_SPLAT_BACKWARD = 7
 };
 lattice_status lattice_set_timing(lattice *L, int mode);
 lattice_status lattice_get_timing(lattice *L, double *ms, int64_t *count);

@@ -1,5 +1,6 @@
 // Internal declarations shared by the host API (lattice.hip) and the kernel
-// translation units (splat.hip, neighbors.hip, conv.hip, slice.hip).
+// translation units (splat.hip, neighbors.hip, conv.hip, slice.hip, deform.hip,
+// backward.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -52,6 +53,11 @@ struct lattice {
     float *pweight = nullptr;   // [rows_max] partial weight sums
     float *partial = nullptr;   // [rows_max][partial_cols] partial feature sums, grown on demand
     int64_t partial_cols = 0;
+    // Backward scratch (backward.hip), grown on the first call that needs more.
+    void *wflip = nullptr;      // flipped, transposed conv weights [C_in][T][C_out]
+    int64_t wflip_bytes = 0;
+    float *wgpart = nullptr;    // weight-gradient partials [chunks][C_out][T][C_in], then bias partials
+    int64_t wgpart_floats = 0;
     int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
     int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
@@ -99,6 +105,15 @@ hipError_t launch_conv(lattice *L, const void *in, lattice_dtype in_dt, int C_in
 
 // slice.hip
 hipError_t launch_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, float *out);
+hipError_t launch_splat_backward(lattice *L, const void *grad_values, lattice_dtype gv_dt, int C,
+                                 const float *vweight, float *grad_feat);
+
+// backward.hip
+int wgrad_chunks(const lattice *L, int C_in, int C_out);
+hipError_t launch_conv_wgrad(lattice *L, const void *g, lattice_dtype g_dt, int C_out, const void *x,
+                             lattice_dtype x_dt, int C_in, lattice_dtype dt, int nch, float *partial,
+                             float *pbias, float *grad_w, float *grad_bias);
+hipError_t launch_flip_weights(lattice *L, const void *w, bool bf16, int C_out, int C_in, void *wt);
 
 // deform.hip
 int deform_max_channels(const void *values, lattice_dtype values_dt, int C, const float *w_delta, const float *w_cls,

@@ -47,6 +47,8 @@ void free_all(lattice *L) {
     (void)hipFree(L->rowmap);
     (void)hipFree(L->pweight);
     (void)hipFree(L->partial);
+    (void)hipFree(L->wflip);
+    (void)hipFree(L->wgpart);
     (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
     (void)hipFree(L->rank);
@@ -117,6 +119,35 @@ lattice_status copy_rows(lattice *L, const void *src, void *dst, int64_t row_wor
     hipLaunchKernelGGL(k_copy_rows, dim3(grid), dim3(256), 0, L->stream, reinterpret_cast<const uint32_t *>(src),
                        reinterpret_cast<uint32_t *>(dst), row_words, L->counters, fixed_rows);
     return check_launch(L, hipGetLastError(), "copy_rows");
+}
+
+// Grow a scratch buffer of the lattice to at least `need` bytes (a device
+// allocation, only when it is too small).
+lattice_status grow(lattice *L, void **buf, int64_t *have, int64_t need, const char *what) {
+    if (need <= *have) return LATTICE_OK;
+    if (*buf) HIP_TRY(L, hipFree(*buf));
+    *buf = nullptr;
+    *have = 0;
+    if (hipMalloc(buf, need) != hipSuccess) {
+        (void)hipGetLastError();
+        *buf = nullptr;
+        set_err(L, "%s: cannot allocate %lld bytes of scratch", what, (long long)need);
+        return LATTICE_E_NOMEM;
+    }
+    *have = need;
+    return LATTICE_OK;
+}
+
+// The gather scratch (partial rows of long pair lists) sized for C columns.
+lattice_status ensure_partial(lattice *L, int C, const char *what) {
+    const int64_t cols = (C + 3) & ~3;
+    if (cols <= L->partial_cols) return LATTICE_OK;
+    int64_t have = L->partial_cols * split_rows_max(L) * (int64_t)sizeof(float);
+    void *buf = L->partial;
+    lattice_status s = grow(L, &buf, &have, split_rows_max(L) * cols * (int64_t)sizeof(float), what);
+    L->partial = reinterpret_cast<float *>(buf);
+    L->partial_cols = s == LATTICE_OK ? cols : 0;
+    return s;
 }
 
 lattice_status ensure_neighbors(lattice *L) {
@@ -270,23 +301,10 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
     // Scratch for the partial rows of long pair lists, sized for C columns
     // (grown here, outside any timed or captured region of a caller that
     // splats once before it times or captures).
-    const int64_t cols = (C + 3) & ~3;
-    if (cols > L->partial_cols) {
-        if (L->partial) HIP_TRY(L, hipFree(L->partial));
-        L->partial = nullptr;
-        L->partial_cols = 0;
-        if (hipMalloc(&L->partial, split_rows_max(L) * cols * sizeof(float)) != hipSuccess) {
-            (void)hipGetLastError();
-            L->partial = nullptr;
-            set_err(L, "splat: cannot allocate %lld bytes of gather scratch",
-                    (long long)(split_rows_max(L) * cols * sizeof(float)));
-            return LATTICE_E_NOMEM;
-        }
-        L->partial_cols = cols;
-    }
-    hipEvent_t t0;
-    lattice_status s = timer_begin(L, LATTICE_STAGE_SPLAT, &t0);
+    lattice_status s = ensure_partial(L, C, "splat");
     if (s) return s;
+    hipEvent_t t0;
+    if ((s = timer_begin(L, LATTICE_STAGE_SPLAT, &t0))) return s;
     if ((s = check_launch(L, launch_clear_table(L), "clear_table"))) return s;
     if ((s = check_launch(L, launch_insert(L, pos, batch, m), "insert"))) return s;
     if ((s = check_launch(L, launch_number(L, m), "number"))) return s;
@@ -388,6 +406,107 @@ lattice_status lattice_deform_slice(lattice *L, const void *values, lattice_dtyp
                           "deform_slice")))
         return s;
     return timer_end(L, LATTICE_STAGE_DEFORM, t0);
+}
+
+lattice_status lattice_slice_backward(lattice *L, const float *grad_out, int C, void *grad_values,
+                                      lattice_dtype grad_dtype) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "slice_backward: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    if (C < 1 || C > 4096 || (L->m > 0 && (!grad_out || !grad_values)) ||
+        (grad_dtype != LATTICE_F32 && grad_dtype != LATTICE_BF16) ||
+        (grad_values && (const void *)grad_out == grad_values)) {
+        set_err(L, "slice_backward: bad argument (C = %d)", C);
+        return LATTICE_E_ARG;
+    }
+    lattice_status s = ensure_partial(L, C, "slice_backward");
+    if (s) return s;
+    hipEvent_t t0;
+    if ((s = timer_begin(L, LATTICE_STAGE_SLICE_BACKWARD, &t0))) return s;
+    // Eq. (splat) of the point gradients over the pair lists of the last splat
+    if ((s = check_launch(L, launch_gather(L, grad_out, C, 0, grad_values, grad_dtype, nullptr), "slice_backward")))
+        return s;
+    return timer_end(L, LATTICE_STAGE_SLICE_BACKWARD, t0);
+}
+
+lattice_status lattice_splat_backward(lattice *L, const void *grad_values, lattice_dtype gv_dtype, int C,
+                                      int normalize, const float *weight, float *grad_feat) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "splat_backward: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    if (C < 1 || C > 4096 || (normalize != 0 && normalize != 1) || (normalize && !weight) ||
+        (L->m > 0 && (!grad_values || !grad_feat)) || (gv_dtype != LATTICE_F32 && gv_dtype != LATTICE_BF16)) {
+        set_err(L, "splat_backward: bad argument (C = %d, normalize = %d)", C, normalize);
+        return LATTICE_E_ARG;
+    }
+    hipEvent_t t0;
+    lattice_status s = timer_begin(L, LATTICE_STAGE_SPLAT_BACKWARD, &t0);
+    if (s) return s;
+    // Eq. (slice) of the vertex gradients (divided by w_v for the normalised splat)
+    if ((s = check_launch(L, launch_splat_backward(L, grad_values, gv_dtype, C, normalize ? weight : nullptr,
+                                                   grad_feat),
+                          "splat_backward")))
+        return s;
+    return timer_end(L, LATTICE_STAGE_SPLAT_BACKWARD, t0);
+}
+
+lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
+                                     const void *w, int C_in, lattice_dtype dt, const void *in,
+                                     lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                     float *grad_w, float *grad_bias) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "conv_backward: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    auto bad_dt = [](lattice_dtype t) { return t != LATTICE_F32 && t != LATTICE_BF16; };
+    if (!grad_out || C_out < 1 || C_out > 1024 || C_in < 1 || C_in > 1024 || bad_dt(g_dtype) || bad_dt(dt) ||
+        (grad_in && (!w || bad_dt(grad_in_dtype) || grad_in == grad_out)) ||
+        ((grad_w || grad_bias) && !in) || (in && bad_dt(in_dtype)) || (!grad_in && !grad_w && !grad_bias)) {
+        set_err(L, "conv_backward: bad argument (C_out = %d, C_in = %d)", C_out, C_in);
+        return LATTICE_E_ARG;
+    }
+    lattice_status s = ensure_neighbors(L);
+    if (s) return s;
+    const int T = L->T;
+    const int nch = wgrad_chunks(L, C_in, C_out);
+    if (grad_in) {
+        const int64_t esz = dt == LATTICE_BF16 ? 2 : 4;
+        if ((s = grow(L, &L->wflip, &L->wflip_bytes, (int64_t)C_out * T * C_in * esz, "conv_backward"))) return s;
+    }
+    if (grad_w || grad_bias) {
+        void *buf = L->wgpart;
+        int64_t have = L->wgpart_floats * (int64_t)sizeof(float);
+        const int64_t need = (int64_t)nch * ((int64_t)C_out * T * C_in + C_out) * (int64_t)sizeof(float);
+        s = grow(L, &buf, &have, need, "conv_backward");
+        L->wgpart = reinterpret_cast<float *>(buf);
+        L->wgpart_floats = have / (int64_t)sizeof(float);
+        if (s) return s;
+    }
+    hipEvent_t t0;
+    if ((s = timer_begin(L, LATTICE_STAGE_CONV_BACKWARD, &t0))) return s;
+    if (grad_in) {
+        // dx = forward conv of g with W'[i][s][o] = W[o][flip(s)][i]
+        if ((s = check_launch(L, launch_flip_weights(L, w, dt == LATTICE_BF16, C_out, C_in, L->wflip),
+                              "conv_backward flip")))
+            return s;
+        if ((s = check_launch(L, launch_conv(L, grad_out, g_dtype, C_out, L->wflip, C_in, dt, nullptr, grad_in,
+                                             grad_in_dtype),
+                              "conv_backward input")))
+            return s;
+    }
+    if (grad_w || grad_bias) {
+        float *pbias = L->wgpart + (int64_t)nch * C_out * T * C_in;
+        if ((s = check_launch(L, launch_conv_wgrad(L, grad_out, g_dtype, C_out, in, in_dtype, C_in, dt, nch,
+                                                   L->wgpart, pbias, grad_w, grad_bias),
+                              "conv_backward weight")))
+            return s;
+    }
+    return timer_end(L, LATTICE_STAGE_CONV_BACKWARD, t0);
 }
 
 lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst) {

@@ -1,6 +1,11 @@
 // Slice (Eq. slice): f_p = sum_{v in I_p} b_pv x_v, with the vertex indices
 // and barycentric weights recorded by the last splat.
 //
+// The same gather is the gradient of the splat with respect to the point
+// features (Eq. splat is x = B^T f, so df = B dx).  For the normalised
+// splat x_v / w_v the vertex gradient is divided by w_v first (NORM: the
+// weight b_pv becomes b_pv / w_v, and 0 where w_v = 0).
+//
 // G lanes per point, each lane owning float4 column chunks j, j+G, ... of the
 // C channels: a row gather of the d+1 vertex rows is contiguous per group, so
 // a wavefront issues 64 x 16 B coalesced reads per vertex.
@@ -28,10 +33,10 @@ __device__ __forceinline__ float load1(const void *values, int64_t at) {
     return reinterpret_cast<const float *>(values)[at];
 }
 
-template <int D, bool VEC, bool IN_BF16>
+template <int D, bool VEC, bool IN_BF16, bool NORM>
 __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, const int32_t *__restrict__ idx,
                                                   const float *__restrict__ bary, const void *__restrict__ values,
-                                                  float *__restrict__ out) {
+                                                  const float *__restrict__ vweight, float *__restrict__ out) {
     constexpr int DP1 = D + 1;
     const int G = 1 << log2G;
     const int lane = threadIdx.x & 63;
@@ -49,6 +54,10 @@ __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, c
         for (int k = 0; k < DP1; ++k) {
             v[k] = idx[p * DP1 + k];
             b[k] = bary[p * DP1 + k];
+            if (NORM && v[k] >= 0) {
+                const float w = vweight[v[k]];
+                b[k] = w != 0.f ? b[k] / w : 0.f;
+            }
         }
         if (VEC) {
             const int C4 = C >> 2;
@@ -80,8 +89,8 @@ __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, c
 
 }  // namespace
 
-template <bool IN_BF16>
-static hipError_t slice_typed(lattice *L, const void *values, int C, float *out) {
+template <bool IN_BF16, bool NORM>
+static hipError_t slice_typed(lattice *L, const void *values, int C, const float *vweight, float *out) {
     const int64_t m = L->m;
     if (m == 0) return hipSuccess;
     const bool vec = (C % 4 == 0) && ((reinterpret_cast<uintptr_t>(values) & (IN_BF16 ? 7 : 15)) == 0) &&
@@ -95,11 +104,11 @@ static hipError_t slice_typed(lattice *L, const void *values, int C, float *out)
 #define SL_CASE(DD)                                                                                              \
     case DD:                                                                                                     \
         if (vec)                                                                                                 \
-            hipLaunchKernelGGL((k_slice<DD, true, IN_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, log2G, \
-                               L->idx, L->bary, values, out);                                                    \
+            hipLaunchKernelGGL((k_slice<DD, true, IN_BF16, NORM>), dim3(grid), dim3(kBlock), 0, L->stream, m, C,  \
+                               log2G, L->idx, L->bary, values, vweight, out);                                    \
         else                                                                                                     \
-            hipLaunchKernelGGL((k_slice<DD, false, IN_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, log2G, \
-                               L->idx, L->bary, values, out);                                                    \
+            hipLaunchKernelGGL((k_slice<DD, false, IN_BF16, NORM>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, \
+                               log2G, L->idx, L->bary, values, vweight, out);                                    \
         return hipGetLastError();
     switch (L->d) {
         SL_CASE(1)
@@ -113,5 +122,14 @@ static hipError_t slice_typed(lattice *L, const void *values, int C, float *out)
 }
 
 hipError_t launch_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, float *out) {
-    return values_dt == LATTICE_BF16 ? slice_typed<true>(L, values, C, out) : slice_typed<false>(L, values, C, out);
+    return values_dt == LATTICE_BF16 ? slice_typed<true, false>(L, values, C, nullptr, out)
+                                     : slice_typed<false, false>(L, values, C, nullptr, out);
+}
+
+hipError_t launch_splat_backward(lattice *L, const void *grad_values, lattice_dtype gv_dt, int C,
+                                 const float *vweight, float *grad_feat) {
+    if (vweight)
+        return gv_dt == LATTICE_BF16 ? slice_typed<true, true>(L, grad_values, C, vweight, grad_feat)
+                                     : slice_typed<false, true>(L, grad_values, C, vweight, grad_feat);
+    return launch_slice(L, grad_values, gv_dt, C, grad_feat);
 }

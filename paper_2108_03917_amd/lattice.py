@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "_lib", "liblattice.so")
 
 OK, E_ARG, E_STATE, E_RANGE, E_CAPACITY, E_NOMEM, E_HIP = range(7)
 F32, BF16 = 0, 1
-STAGES = ("splat", "neighbors", "conv", "slice", "deform")
+STAGES = ("splat", "neighbors", "conv", "slice", "deform", "slice_backward", "conv_backward", "splat_backward")
 
 EXPORTS = (
     "lattice_create", "lattice_destroy", "lattice_max_vertices", "lattice_splat", "lattice_build_neighbors",
@@ -27,7 +27,8 @@ EXPORTS = (
     "lattice_slice", "lattice_weights_to_bf16", "lattice_num_vertices", "lattice_get_status",
     "lattice_get_keys", "lattice_get_neighbors", "lattice_get_point_simplex", "lattice_set_timing",
     "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
-    "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice",
+    "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice", "lattice_slice_backward",
+    "lattice_splat_backward", "lattice_conv_backward",
 )
 
 _lib = None
@@ -58,6 +59,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_conv": (St, [P, P, I, I, P, I, I, P, P, I]),
         "lattice_slice": (St, [P, P, I, I, P]),
         "lattice_deform_slice": (St, [P, P, I, I, P, ctypes.c_float, P, P, I, P, P]),
+        "lattice_slice_backward": (St, [P, P, I, P, I]),
+        "lattice_splat_backward": (St, [P, P, I, I, I, P, P]),
+        "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
         "lattice_num_vertices": (St, [P, ctypes.POINTER(I64)]),
         "lattice_get_status": (St, [P]),
@@ -299,6 +303,107 @@ class Lattice:
                                                    float(b_delta), _ptr(w_cls), _ptr(b_cls), n_cls, _ptr(out),
                                                    _ptr(delta)), "deform_slice")
         return (out, delta) if delta is not None else out
+
+    # -- backward passes ------------------------------------------------
+    def slice_backward(self, grad_out: torch.Tensor, out: Optional[torch.Tensor] = None,
+                       out_dtype: str = "f32") -> torch.Tensor:
+        """Gradient of the slice with respect to the vertex values:
+        Eq. (splat) of ``grad_out`` [m, C] over the last splat's pairs.
+        Returns [max_vertices, C] (rows 0..V-1 hold the result)."""
+        _dev(grad_out, torch.float32, "grad_out")
+        if grad_out.dim() != 2 or grad_out.shape[0] != self.m:
+            raise ValueError(f"grad_out must be [m = {self.m}, C]")
+        C = grad_out.shape[1]
+        mv = self.max_vertices(self.m)
+        if out is None:
+            out = torch.empty((max(mv, 1), C), dtype=_TORCH[out_dtype], device=grad_out.device)
+        _dev(out, (torch.float32, torch.bfloat16), "out")
+        if out.dim() != 2 or out.shape[1] != C or out.shape[0] < self._rows_needed():
+            raise ValueError(f"out needs >= {self._rows_needed()} rows of {C}")
+        self._check(self._lib.lattice_slice_backward(self._h, _ptr(grad_out), C, _ptr(out), _STORAGE[out.dtype]),
+                    "slice_backward")
+        return out
+
+    def splat_backward(self, grad_values: torch.Tensor, normalize: bool = False,
+                       weight: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Gradient of the splat with respect to the point features: Eq.
+        (slice) of ``grad_values`` [>= V, C] (divided by the splat's weight
+        w_v first when ``normalize``).  Returns [m, C] fp32."""
+        _dev(grad_values, (torch.float32, torch.bfloat16), "grad_values")
+        if grad_values.dim() != 2 or grad_values.shape[0] < self._rows_needed():
+            raise ValueError(f"grad_values needs >= {self._rows_needed()} rows")
+        C = grad_values.shape[1]
+        if normalize:
+            if weight is None:
+                raise ValueError("the normalised splat's gradient needs its weight w_v")
+            _dev(weight, torch.float32, "weight")
+            if weight.numel() < self._rows_needed():
+                raise ValueError("weight needs >= V entries")
+        if out is None:
+            out = torch.empty((self.m, C), dtype=torch.float32, device=grad_values.device)
+        _dev(out, torch.float32, "out")
+        if out.numel() < self.m * C:
+            raise ValueError("out needs [m, C]")
+        self._check(self._lib.lattice_splat_backward(self._h, _ptr(grad_values), _STORAGE[grad_values.dtype], C,
+                                                     int(bool(normalize)), _ptr(weight if normalize else None),
+                                                     _ptr(out)), "splat_backward")
+        return out
+
+    def conv_backward(self, grad_out: torch.Tensor, w: torch.Tensor, x: Optional[torch.Tensor] = None,
+                      dtype: str = "f32", want_input: bool = True, want_weight: bool = True,
+                      want_bias: bool = False, grad_in_dtype: str = "f32",
+                      grad_in: Optional[torch.Tensor] = None, grad_w: Optional[torch.Tensor] = None,
+                      grad_bias: Optional[torch.Tensor] = None):
+        """Gradients of ``conv(x, w)`` given ``grad_out`` [>= V, C_out]:
+        returns (grad_in [rows, C_in] or None, grad_w [C_out, T, C_in] fp32
+        or None, grad_bias [C_out] fp32 or None).  Preallocated outputs may
+        be passed in (then the matching want_* flag is implied)."""
+        _dev(grad_out, (torch.float32, torch.bfloat16), "grad_out")
+        if dtype == "f32":
+            _dev(w, torch.float32, "w")
+            dt = F32
+        elif dtype == "bf16":
+            _dev(w, torch.bfloat16, "w")
+            dt = BF16
+        else:
+            raise ValueError("dtype must be 'f32' or 'bf16'")
+        C_out, T, C_in = w.shape
+        need = self._rows_needed()
+        if T != self.taps or grad_out.dim() != 2 or grad_out.shape[1] != C_out or grad_out.shape[0] < need:
+            raise ValueError(f"w must be [C_out, {self.taps}, C_in], grad_out [>= {need}, C_out]")
+        if x is not None:
+            _dev(x, (torch.float32, torch.bfloat16), "x")
+            if x.dim() != 2 or x.shape[1] != C_in or x.shape[0] < need:
+                raise ValueError(f"x must be [>= {need}, {C_in}]")
+        want_input = want_input or grad_in is not None
+        want_weight = want_weight or grad_w is not None
+        want_bias = want_bias or grad_bias is not None
+        if (want_weight or want_bias) and x is None:
+            raise ValueError("the weight and bias gradients need the forward input x")
+        gi = grad_in if grad_in is not None else (
+            torch.empty((grad_out.shape[0], C_in), dtype=_TORCH[grad_in_dtype], device=grad_out.device)
+            if want_input else None)
+        gw = grad_w if grad_w is not None else (
+            torch.empty((C_out, T, C_in), dtype=torch.float32, device=grad_out.device) if want_weight else None)
+        gb = grad_bias if grad_bias is not None else (
+            torch.empty((C_out,), dtype=torch.float32, device=grad_out.device) if want_bias else None)
+        if gi is not None:
+            _dev(gi, (torch.float32, torch.bfloat16), "grad_in")
+            if gi.dim() != 2 or gi.shape[1] != C_in or gi.shape[0] < need:
+                raise ValueError(f"grad_in needs [>= {need}, {C_in}]")
+        if gw is not None:
+            _dev(gw, torch.float32, "grad_w")
+            if gw.numel() != C_out * T * C_in:
+                raise ValueError("grad_w needs [C_out, T, C_in]")
+        if gb is not None:
+            _dev(gb, torch.float32, "grad_bias")
+            if gb.numel() != C_out:
+                raise ValueError("grad_bias needs C_out entries")
+        self._check(self._lib.lattice_conv_backward(
+            self._h, _ptr(grad_out), _STORAGE[grad_out.dtype], C_out, _ptr(w), C_in, dt, _ptr(x),
+            _STORAGE[x.dtype] if x is not None else F32, _ptr(gi), _STORAGE[gi.dtype] if gi is not None else F32,
+            _ptr(gw), _ptr(gb)), "conv_backward")
+        return gi, gw, gb
 
     def weights_to_bf16(self, w: torch.Tensor) -> torch.Tensor:
         """Round fp32 weights to bf16 (nearest even) with the library's kernel."""
