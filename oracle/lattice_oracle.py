@@ -277,7 +277,7 @@ def conv(values: np.ndarray, nbr: np.ndarray, weight: np.ndarray, bias: Optional
     with scale = sum_t |x_{nbr(v,t)}| |W_t|^T."""
     x = np.asarray(values, dtype=np.float64)
     W = np.asarray(weight, dtype=np.float64)
-    V = x.shape[0]
+    V = nbr.shape[0]            # one output row per table row (the input rows may be another lattice's)
     c_out, T, c_in = W.shape
     y = np.zeros((V, c_out))
     scale = np.zeros((V, c_out))
@@ -449,3 +449,87 @@ def conv_backward(values: np.ndarray, nbr: np.ndarray, weight: np.ndarray, grad_
         gw[:, t, :] = g[present].T @ x[src]
         gw_s[:, t, :] = np.abs(g[present]).T @ np.abs(x[src])
     return gx, gw, g.sum(axis=0), gx_s, gw_s, np.abs(g).sum(axis=0)
+
+
+# ---------------------------------------------------------------------------
+# Downsampling and upsampling (Sec. "Proposed Operations": Downsampling,
+# Upsampling, and the caption of the Coarsen figure).
+#
+# A coarse lattice is the lattice of the same cloud with the positions
+# divided by 2 (the same as doubling sigma: halving is exact in float32).
+# Downsampling: coarse vertex c' is embedded in the fine lattice as 2c' and
+# convolves over the fine vertices 2c' + offset_t (the 1-ring offsets), a
+# strided convolution.  Upsampling: fine vertex u is embedded in the coarse
+# lattice as u/2 and convolves over the coarse vertices (u + offset_t)/2; a
+# tap whose key has a fractional coordinate (it lies inside a coarse
+# simplex) contributes nothing, as does a tap whose vertex is not allocated.
+# This makes upsampling a transposed convolution.
+# ---------------------------------------------------------------------------
+
+def lookup(lat: Lattice, keys: np.ndarray, vbatch: Optional[np.ndarray] = None) -> np.ndarray:
+    """Vertex index of each key [n, d+1] (with batch ids [n] on a batched
+    lattice) in ``lat``, -1 where the key is not a vertex of it."""
+    d = lat.d
+    cols = ([("b", np.int64)] if lat.vbatch is not None else []) + [(f"c{i}", np.int64) for i in range(d)]
+    dt = np.dtype(cols)
+
+    def pack(coords, vb):
+        rec = np.empty(coords.shape[0], dtype=dt)
+        if lat.vbatch is not None:
+            rec["b"] = vb
+        for i in range(d):
+            rec[f"c{i}"] = coords[:, i]
+        return rec
+
+    table = pack(lat.keys, lat.vbatch)                  # canonical order is sorted
+    q = pack(np.asarray(keys, dtype=np.int64), vbatch)
+    pos = np.searchsorted(table, q)
+    out = np.full(q.shape[0], -1, dtype=np.int64)
+    hit = pos < lat.V
+    hit[hit] = table[pos[hit]] == q[hit]
+    out[hit] = pos[hit]
+    return out
+
+
+def coarsen(pos: np.ndarray, sigma, alpha: Optional[float] = None, batch: Optional[np.ndarray] = None) -> Lattice:
+    """The coarse lattice of a cloud: its lattice with the positions divided by 2."""
+    return build(np.asarray(pos, dtype=F32) / F32(2), sigma, alpha, batch)
+
+
+def down_neighbors(fine: Lattice, coarse: Lattice) -> np.ndarray:
+    """[V_coarse, T]: the fine vertex at 2c' + offset_t for each coarse vertex c', or -1."""
+    offs = neighbor_offsets(coarse.d)
+    out = np.empty((coarse.V, offs.shape[0]), dtype=np.int64)
+    for t, o in enumerate(offs):
+        out[:, t] = lookup(fine, 2 * coarse.keys + o, coarse.vbatch)
+    return out
+
+
+def up_neighbors(coarse: Lattice, fine: Lattice) -> np.ndarray:
+    """[V_fine, T]: the coarse vertex at (u + offset_t)/2 for each fine vertex u,
+    or -1 when that key is fractional or not a coarse vertex."""
+    offs = neighbor_offsets(fine.d)
+    out = np.full((fine.V, offs.shape[0]), -1, dtype=np.int64)
+    for t, o in enumerate(offs):
+        q = fine.keys + o
+        even = np.all(q % 2 == 0, axis=1)
+        if even.any():
+            vb = None if fine.vbatch is None else fine.vbatch[even]
+            out[even, t] = lookup(coarse, q[even] // 2, vb)
+    return out
+
+
+def downsample(fine: Lattice, coarse: Lattice, values: np.ndarray, weight: np.ndarray,
+               bias: Optional[np.ndarray] = None):
+    """Strided convolution from the fine lattice's values [V_fine, C_in] onto the
+    coarse vertices: y_c' = sum_t x_{fine(2c' + offset_t)} W_t^T (+ bias).
+    Returns (y [V_coarse, C_out], scale)."""
+    return conv(values, down_neighbors(fine, coarse), weight, bias)
+
+
+def upsample(coarse: Lattice, fine: Lattice, values: np.ndarray, weight: np.ndarray,
+             bias: Optional[np.ndarray] = None):
+    """Transposed convolution from the coarse lattice's values [V_coarse, C_in]
+    onto the fine vertices: z_u = sum_t x_{coarse((u + offset_t)/2)} W_t^T (+ bias),
+    fractional or absent taps contributing nothing.  Returns (z [V_fine, C_out], scale)."""
+    return conv(values, up_neighbors(coarse, fine), weight, bias)

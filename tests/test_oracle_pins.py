@@ -603,3 +603,110 @@ def test_backward_matches_torch_autograd():
     gf, _ = O.splat_backward(lat, gx)
     assert np.allclose(gw, Wt.grad.numpy(), rtol=1e-10, atol=1e-10)
     assert np.allclose(gf, f.grad.numpy(), rtol=1e-10, atol=1e-10)
+
+
+# --------------------------------------------------------------------------
+# downsampling / upsampling (Sec. "Proposed Operations": Downsampling,
+# Upsampling; the Coarsen figure: a strided and a transposed convolution)
+# --------------------------------------------------------------------------
+
+def _flip_transpose(W, d):
+    """W'[i][s][o] = W[o][flip(s)][i], flip exchanging taps +n_j and -n_j."""
+    T = W.shape[1]
+    flip = [0] + [1 + (d + 1) + j for j in range(d + 1)] + [1 + j for j in range(d + 1)]
+    return np.transpose(W[:, flip, :], (2, 1, 0))
+
+
+def test_d1_down_and_up_are_textbook_stride2_conv_and_transpose():
+    """In d = 1 the lattice is the integers a ~ key (a, -a); the ring offsets
+    are +-1 (twice), so downsampling is the stride-2 correlation of a 1-D
+    signal with a 3-tap kernel and upsampling is the stride-2 transposed
+    convolution, here built with scipy.ndimage on a dense signal."""
+    from scipy.ndimage import convolve1d, correlate1d
+
+    g = np.linspace(-3.0, 5.0, 4001, dtype=np.float32)[:, None]
+    sigma = 0.3
+    fine = O.build(g, sigma)
+    coarse = O.coarsen(g, sigma)
+    a = fine.keys[:, 0]
+    ac = coarse.keys[:, 0]
+    assert np.array_equal(a, np.arange(a.min(), a.max() + 1))      # every cell occupied
+    assert np.array_equal(ac, np.arange(ac.min(), ac.max() + 1))
+    rng = np.random.default_rng(0)
+    W = rng.standard_normal((1, 5, 1))
+    K = {-1: W[0, 2, 0] + W[0, 3, 0], 0: W[0, 0, 0], 1: W[0, 1, 0] + W[0, 4, 0]}
+    # dense fine signal on [lo, hi], zero-padded around the lattice's range
+    lo, hi = 2 * ac.min() - 2, 2 * ac.max() + 2
+    assert lo <= a.min() and hi >= a.max()
+    x = rng.standard_normal(fine.V)
+    X = np.zeros(hi - lo + 1)
+    X[a - lo] = x
+    full = correlate1d(X, [K[-1], K[0], K[1]], mode="constant", cval=0.0)
+    y, _ = O.downsample(fine, coarse, x[:, None], W)
+    assert np.allclose(y[:, 0], full[2 * ac - lo], rtol=1e-12, atol=1e-12)
+
+    U = rng.standard_normal((1, 5, 1))
+    k = {-1: U[0, 1, 0] + U[0, 4, 0], 0: U[0, 0, 0], 1: U[0, 2, 0] + U[0, 3, 0]}
+    yc = rng.standard_normal(coarse.V)
+    Zup = np.zeros(hi - lo + 1)
+    Zup[2 * ac - lo] = yc                                      # zero insertion
+    Z = convolve1d(Zup, [k[-1], k[0], k[1]], mode="constant", cval=0.0)
+    z, _ = O.upsample(coarse, fine, yc[:, None], U)
+    assert np.allclose(z[:, 0], Z[a - lo], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("d", [2, 3, 4])
+def test_downsample_is_fine_conv_sampled_at_embedded_vertices(d):
+    """Where 2c' is itself a fine vertex v, the coarse value equals the fine
+    lattice's convolution at v: its taps are v's 1-ring (a strided conv)."""
+    w = random_cloud(2500, d, 50 + d, extent=1.0, C=2)
+    sigma = {2: 0.08, 3: 0.15, 4: 0.3}[d]
+    fine = O.build(w.pos, sigma)
+    coarse = O.coarsen(w.pos, sigma)
+    nbr = O.neighbors(fine)
+    rng = np.random.default_rng(d)
+    x = rng.standard_normal((fine.V, 3))
+    W = rng.standard_normal((4, nbr.shape[1], 3))
+    y, _ = O.downsample(fine, coarse, x, W)
+    yf, _ = O.conv(x, nbr, W)
+    v = O.lookup(fine, 2 * coarse.keys)
+    assert (v >= 0).mean() > 0.3
+    assert np.allclose(y[v >= 0], yf[v[v >= 0]], rtol=1e-12, atol=1e-12)
+    # coarse keys embed into the fine lattice: 2c' sums to zero, coordinates congruent mod d+1
+    e = 2 * coarse.keys
+    assert np.all(e.sum(axis=1) == 0) and np.all((e - e[:, :1]) % (d + 1) == 0)
+
+
+@pytest.mark.parametrize("d,batched", [(2, False), (3, False), (3, True), (4, False)])
+def test_upsample_is_adjoint_of_downsample(d, batched):
+    """<down_W(x), y> = <x, up_W'(y)> with W' the flipped transposed weights:
+    upsampling is the transposed convolution of downsampling."""
+    w = random_cloud(2000, d, 60 + d, extent=1.0, C=2, n_batch=3 if batched else 0)
+    sigma = {2: 0.08, 3: 0.15, 4: 0.3}[d]
+    fine = O.build(w.pos, sigma, batch=w.batch)
+    coarse = O.coarsen(w.pos, sigma, batch=w.batch)
+    T = 2 * (d + 1) + 1
+    rng = np.random.default_rng(7)
+    W = rng.standard_normal((3, T, 2))
+    x = rng.standard_normal((fine.V, 2))
+    y = rng.standard_normal((coarse.V, 3))
+    dx, _ = O.downsample(fine, coarse, x, W)
+    uy, _ = O.upsample(coarse, fine, y, _flip_transpose(W, d))
+    assert np.isclose((dx * y).sum(), (x * uy).sum(), rtol=1e-10)
+    # and the taps that exist are not few
+    assert (O.up_neighbors(coarse, fine) >= 0).sum() > fine.V // 2
+
+
+def test_upsample_taps_follow_remainder_parity_in_3d():
+    """d = 3: a vertex's coordinates share its remainder mod 4, so an
+    even-remainder fine vertex u has u/2 integral and every (u +- n_j)/2
+    fractional (centre tap only), and an odd-remainder one the reverse."""
+    w = random_cloud(3000, 3, 70, extent=1.0, C=2)
+    fine = O.build(w.pos, 0.15)
+    coarse = O.coarsen(w.pos, 0.15)
+    up = O.up_neighbors(coarse, fine)
+    rem = fine.keys[:, 0] % 4
+    even = rem % 2 == 0
+    assert np.all(up[~even, 0] == -1)
+    assert np.all(up[even, 1:] == -1)
+    assert (up[even, 0] >= 0).mean() > 0.2 and (up[~even, 1:] >= 0).any(axis=1).mean() > 0.2
