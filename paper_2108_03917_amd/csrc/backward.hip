@@ -24,7 +24,7 @@
 // B = the gathered rows x_{nbr(v,t)}.  k_conv_wgrad gives each workgroup one
 // tap, one 64 x 64 tile of (output, input) channels and one chunk of the
 // vertices (chunk c of nch covers rows [c V / nch, (c+1) V / nch), V read on
-// the device).  Per step of 64 vertices it stages the 64 g rows and the 64
+// the device).  Per step of 32 vertices it stages the 32 g rows and the 32
 // gathered x rows in LDS as fp32 and four wavefronts each accumulate a
 // 32 x 32 block with v_mfma_f32_32x32x2f32 (K = the vertex index).  Each
 // chunk writes its tile to a partial buffer; k_wgrad_reduce adds the nch
@@ -39,7 +39,11 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kBlock = 256;
 constexpr int kTile = 64;   // output and input channels per tile
-constexpr int kStep = 64;   // vertices per K step
+constexpr int kStep = 32;   // vertices per K step
+constexpr int kRowsPer = kStep / (kBlock / 16);  // rows each loader thread stages per step
+constexpr int kWgPerCu = 4;  // weight-gradient workgroups per CU the chunk count aims at
+// (32-row steps at four workgroups per CU measured best over 64 and 128 rows
+// at two to eight workgroups per CU, on 64x64, 64x128 and 128x128 shapes)
 
 // fp32 -> bf16 -> fp32, round to nearest with ties to even (NaN stays NaN).
 __device__ __forceinline__ float round_bf16(float f) {
@@ -113,7 +117,7 @@ __global__ __launch_bounds__(kBlock) void k_conv_wgrad(const void *__restrict__ 
     const int ow = (wave >> 1) * 32;    // this wave's 32 x 32 block
     const int iw = (wave & 1) * 32;
     // Loader mapping: thread owns channel chunk c4 (4 channels) of rows
-    // r0, r0+16, r0+32, r0+48 of the step.
+    // r0, r0+16, r0+32, ... of the step.
     const int c4 = (tid & 15) * 4;
     const int r0 = tid >> 4;
 
@@ -122,25 +126,36 @@ __global__ __launch_bounds__(kBlock) void k_conv_wgrad(const void *__restrict__ 
     for (int r = 0; r < 16; ++r) acc[r] = 0.f;
     float bsum[4] = {0.f, 0.f, 0.f, 0.f};
 
-    float4 ga[4], xa[4];
+    // The neighbour indices of a step are loaded one step before its rows,
+    // so that a row gather never waits on its own index load.
+    float4 ga[kRowsPer], xa[kRowsPer];
+    int32_t ua[kRowsPer];
+    auto load_index = [&](int64_t k0) {
+#pragma unroll
+        for (int j = 0; j < kRowsPer; ++j) {
+            const int64_t v = k0 + r0 + 16 * j;
+            ua[j] = v < hi ? nbr[v * T + t] : -1;
+        }
+    };
     auto load_step = [&](int64_t k0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < kRowsPer; ++j) {
             const int64_t v = k0 + r0 + 16 * j;
             ga[j] = make_float4(0.f, 0.f, 0.f, 0.f);
             xa[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (v < hi) {
-                ga[j] = load4<G_BF16, VEC>(g, v, C_out, o0 + c4);
-                const int32_t u = nbr[v * T + t];
-                if (u >= 0) xa[j] = load4<X_BF16, VEC>(x, u, C_in, i0 + c4);
-            }
+            if (v < hi) ga[j] = load4<G_BF16, VEC>(g, v, C_out, o0 + c4);
+            if (ua[j] >= 0) xa[j] = load4<X_BF16, VEC>(x, ua[j], C_in, i0 + c4);
         }
     };
-    if (lo < hi) load_step(lo);
+    if (lo < hi) {
+        load_index(lo);
+        load_step(lo);
+        load_index(lo + kStep);
+    }
     for (int64_t k0 = lo; k0 < hi; k0 += kStep) {
         // registers -> LDS (rounded to bf16 for a bf16 computation)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < kRowsPer; ++j) {
             const int k = r0 + 16 * j;
             float4 a = ga[j], b = xa[j];
             if (do_bias) {
@@ -149,15 +164,17 @@ __global__ __launch_bounds__(kBlock) void k_conv_wgrad(const void *__restrict__ 
                 bsum[2] += a.z;
                 bsum[3] += a.w;
             }
-            if (ROUND) {
-                a = make_float4(round_bf16(a.x), round_bf16(a.y), round_bf16(a.z), round_bf16(a.w));
-                b = make_float4(round_bf16(b.x), round_bf16(b.y), round_bf16(b.z), round_bf16(b.w));
-            }
+            // (rows stored as bf16 are already rounded)
+            if (ROUND && !G_BF16) a = make_float4(round_bf16(a.x), round_bf16(a.y), round_bf16(a.z), round_bf16(a.w));
+            if (ROUND && !X_BF16) b = make_float4(round_bf16(b.x), round_bf16(b.y), round_bf16(b.z), round_bf16(b.w));
             *reinterpret_cast<float4 *>(&gs[swz(k, c4)]) = a;
             *reinterpret_cast<float4 *>(&xs[swz(k, c4)]) = b;
         }
         __syncthreads();
-        if (k0 + kStep < hi) load_step(k0 + kStep);  // next step's loads in flight during the MFMAs
+        if (k0 + kStep < hi) {  // next step's loads in flight during the MFMAs
+            load_step(k0 + kStep);
+            load_index(k0 + 2 * kStep);
+        }
 #pragma unroll 8
         for (int s = 0; s < kStep / 2; ++s) {
             const int k = 2 * s + h;
@@ -220,13 +237,13 @@ __global__ __launch_bounds__(kBlock) void k_flip_weights(const E *__restrict__ w
 
 }  // namespace
 
-// Number of vertex chunks of the weight gradient: about two workgroups per
-// CU over all taps and tiles, a multiple of 8 (the chunk's workgroups of
+// Number of vertex chunks of the weight gradient: about kWgPerCu workgroups
+// per CU over all taps and tiles, a multiple of 8 (the chunk's workgroups of
 // every tap then share one XCD's L2), and no more chunks than steps of 64
 // rows in the largest lattice.
 int wgrad_chunks(const lattice *L, int C_in, int C_out) {
     const int64_t tiles = (int64_t)((C_out + kTile - 1) / kTile) * ((C_in + kTile - 1) / kTile) * L->T;
-    int64_t nch = (2 * (int64_t)L->cu_count + tiles - 1) / tiles;
+    int64_t nch = (kWgPerCu * (int64_t)L->cu_count + tiles - 1) / tiles;
     nch = (nch + 7) / 8 * 8;
     const int64_t steps = (L->max_vertices + kStep - 1) / kStep;
     if (nch > steps) nch = steps;
