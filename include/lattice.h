@@ -327,6 +327,50 @@ lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_d
                                      float *grad_w, float *grad_bias);
 
 /*
+ * Downsampling and upsampling between two lattices of one cloud (Sec.
+ * "Proposed Operations": Downsampling, Upsampling, and the Coarsen figure).
+ * The coarse lattice is the cloud's lattice at twice the scale (the positions
+ * divided by 2): create it with sigma doubled and splat the same positions
+ * (C = 0 builds only the lattice).  Both lattices must have been splatted,
+ * have the same d, the same stream, the same alpha, both or neither be
+ * batched, and the coarse sigma must be exactly twice the fine one on every
+ * axis (LATTICE_E_ARG otherwise: this also catches the two lattices passed
+ * in the wrong order).
+ *
+ * lattice_downsample -- strided convolution onto the coarse vertices: coarse
+ * vertex c' is embedded in the fine lattice as 2c' and convolves over the
+ * fine vertices 2c' + offset_t, offset_t the 1-ring offsets in the tap order
+ * of lattice_conv (an unallocated vertex contributes zero):
+ *   y_c'[o] = bias[o] + sum_t sum_i x_{fine(2c' + offset_t)}[i] W[o][t][i].
+ *   fine, coarse  the two lattices; out has the coarse lattice's V rows.
+ *   in            dev [V_fine][C_in] fine vertex values, stored as in_dtype.
+ *   other arguments as in lattice_conv (weights [C_out][T][C_in], compute
+ *   type dt, optional bias, out dev [>= V_coarse][C_out] stored as out_dtype).
+ *
+ * lattice_upsample -- transposed convolution onto the fine vertices: fine
+ * vertex u is embedded in the coarse lattice as u/2 and convolves over the
+ * coarse vertices (u + offset_t)/2; a tap whose key has a fractional
+ * coordinate (it falls inside a coarse simplex) or is not allocated
+ * contributes zero:
+ *   z_u[o] = bias[o] + sum_t sum_i x_{coarse((u + offset_t)/2)}[i] W[o][t][i].
+ *   coarse, fine  the two lattices; out has the fine lattice's V rows.
+ *   in            dev [V_coarse][C_in] coarse vertex values.
+ * With W'[i][s][o] = W[o][flip(s)][i] (flip exchanging +n_j and -n_j),
+ * upsampling with W' is the adjoint of downsampling with W.
+ *
+ * Each builds (on its first call after either lattice's splat) a table of
+ * T lookups per output vertex, held by the output lattice, then runs the
+ * lattice_conv kernels over it.  Returns LATTICE_E_STATE if a lattice has not
+ * been splatted, LATTICE_E_ARG for mismatched lattices or bad arguments.
+ */
+lattice_status lattice_downsample(lattice *fine, lattice *coarse, const void *in, lattice_dtype in_dtype, int C_in,
+                                  const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
+                                  lattice_dtype out_dtype);
+lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, lattice_dtype in_dtype, int C_in,
+                                const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
+                                lattice_dtype out_dtype);
+
+/*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to
  * even) on the lattice's stream: the weight format LATTICE_BF16 convs take.
  *   src  dev [n] fp32;  dst  dev [n] uint16 (bf16 bit patterns).
@@ -368,7 +412,7 @@ lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary);
  * of launches since the last reset (arrays of LATTICE_NUM_STAGES).
  * lattice_set_timing(L, 0) stops recording; (L, 2) resets the sums.
  */
-#define LATTICE_NUM_STAGES 8
+#define LATTICE_NUM_STAGES 10
 enum {
     LATTICE_STAGE_SPLAT = 0,
     LATTICE_STAGE_NEIGHBORS = 1,
@@ -377,7 +421,9 @@ enum {
     LATTICE_STAGE_DEFORM = 4,
     LATTICE_STAGE_SLICE_BACKWARD = 5,
     LATTICE_STAGE_CONV_BACKWARD = 6,
-    LATTICE_STAGE_SPLAT_BACKWARD = 7
+    LATTICE_STAGE_SPLAT_BACKWARD = 7,
+    LATTICE_STAGE_DOWNSAMPLE = 8,  /* recorded on the output (coarse) lattice */
+    LATTICE_STAGE_UPSAMPLE = 9     /* recorded on the output (fine) lattice   */
 };
 lattice_status lattice_set_timing(lattice *L, int mode);
 lattice_status lattice_get_timing(lattice *L, double *ms, int64_t *count);

@@ -58,6 +58,15 @@ struct lattice {
     int64_t wflip_bytes = 0;
     float *wgpart = nullptr;    // weight-gradient partials [chunks][C_out][T][C_in], then bias partials
     int64_t wgpart_floats = 0;
+    // Cross-lattice neighbour tables [max_vertices][T], built on demand:
+    // xtab[0] when this lattice is the coarse output of a downsampling,
+    // xtab[1] when it is the fine output of an upsampling.  Each remembers
+    // the source lattice and both splat generations it was built for.
+    int32_t *xtab[2] = {nullptr, nullptr};
+    const lattice *xsrc[2] = {nullptr, nullptr};
+    uint64_t xsrc_gen[2] = {0, 0};
+    uint64_t xown_gen[2] = {0, 0};
+    uint64_t gen = 0;           // incremented by every splat
     int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
     int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
@@ -98,6 +107,7 @@ hipError_t launch_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst
 
 // neighbors.hip
 hipError_t launch_neighbors(lattice *L);
+hipError_t launch_cross(lattice *out, const lattice *src, bool up, int32_t *xnbr);
 
 // conv.hip
 hipError_t launch_conv(lattice *L, const void *in, lattice_dtype in_dt, int C_in, const void *w, int C_out,

@@ -49,6 +49,8 @@ void free_all(lattice *L) {
     (void)hipFree(L->partial);
     (void)hipFree(L->wflip);
     (void)hipFree(L->wgpart);
+    (void)hipFree(L->xtab[0]);
+    (void)hipFree(L->xtab[1]);
     (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
     (void)hipFree(L->rank);
@@ -314,6 +316,7 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
             return s;
     if ((s = timer_end(L, LATTICE_STAGE_SPLAT, t0))) return s;
     L->m = m;
+    L->gen += 1;
     L->splatted = true;
     L->nbr_valid = false;
     L->batched = batch != nullptr;
@@ -507,6 +510,79 @@ lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_d
             return s;
     }
     return timer_end(L, LATTICE_STAGE_CONV_BACKWARD, t0);
+}
+
+// Down (up = false) or upsampling from `src` onto the vertices of `dst`.
+static lattice_status resample(lattice *src, lattice *dst, bool up, const void *in, lattice_dtype in_dtype, int C_in,
+                               const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
+                               lattice_dtype out_dtype) {
+    const char *what = up ? "upsample" : "downsample";
+    if (!src || !dst) return LATTICE_E_ARG;
+    if (!src->splatted || !dst->splatted) {
+        set_err(dst, "%s: both lattices must be splatted first", what);
+        return LATTICE_E_STATE;
+    }
+    if (src == dst || src->d != dst->d || src->stream != dst->stream || src->batched != dst->batched ||
+        src->device != dst->device) {
+        set_err(dst, "%s: the lattices differ in d, stream, device or batching (or are the same)", what);
+        return LATTICE_E_ARG;
+    }
+    // The coarse lattice is the fine one at twice the scale (positions
+    // divided by 2), the same alpha.  This also rejects the two lattices
+    // passed in the wrong order, whose table would index past the input rows.
+    const lattice *fine = up ? dst : src, *coarse = up ? src : dst;
+    bool scales = fine->alpha == coarse->alpha;
+    for (int j = 0; j < fine->d; ++j) scales = scales && coarse->sigma[j] == 2.f * fine->sigma[j];
+    if (!scales) {
+        set_err(dst, "%s: the coarse lattice must have exactly twice the fine lattice's sigma and the same alpha "
+                "(source and destination in the order of the call)", what);
+        return LATTICE_E_ARG;
+    }
+    if (!in || !w || !out || C_in < 1 || C_in > 1024 || C_out < 1 || C_out > 1024 ||
+        (dt != LATTICE_F32 && dt != LATTICE_BF16) || (in_dtype != LATTICE_F32 && in_dtype != LATTICE_BF16) ||
+        (out_dtype != LATTICE_F32 && out_dtype != LATTICE_BF16) || in == out) {
+        set_err(dst, "%s: bad argument (C_in = %d, C_out = %d)", what, C_in, C_out);
+        return LATTICE_E_ARG;
+    }
+    const int k = up ? 1 : 0;
+    hipEvent_t t0;
+    const int stage = up ? LATTICE_STAGE_UPSAMPLE : LATTICE_STAGE_DOWNSAMPLE;
+    lattice_status s = timer_begin(dst, stage, &t0);
+    if (s) return s;
+    if (!dst->xtab[k]) {
+        if (hipMalloc(&dst->xtab[k], dst->max_vertices * (int64_t)dst->T * sizeof(int32_t)) != hipSuccess) {
+            (void)hipGetLastError();
+            dst->xtab[k] = nullptr;
+            set_err(dst, "%s: cannot allocate the cross-lattice table", what);
+            return LATTICE_E_NOMEM;
+        }
+        dst->xsrc[k] = nullptr;
+    }
+    if (dst->xsrc[k] != src || dst->xsrc_gen[k] != src->gen || dst->xown_gen[k] != dst->gen) {
+        if ((s = check_launch(dst, launch_cross(dst, src, up, dst->xtab[k]), what))) return s;
+        dst->xsrc[k] = src;
+        dst->xsrc_gen[k] = src->gen;
+        dst->xown_gen[k] = dst->gen;
+    }
+    // the conv kernels over the output lattice's vertices, reading rows of
+    // the source lattice through the cross table
+    lattice view = *dst;
+    view.nbr = dst->xtab[k];
+    if ((s = check_launch(dst, launch_conv(&view, in, in_dtype, C_in, w, C_out, dt, bias, out, out_dtype), what)))
+        return s;
+    return timer_end(dst, stage, t0);
+}
+
+lattice_status lattice_downsample(lattice *fine, lattice *coarse, const void *in, lattice_dtype in_dtype, int C_in,
+                                  const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
+                                  lattice_dtype out_dtype) {
+    return resample(fine, coarse, false, in, in_dtype, C_in, w, C_out, dt, bias, out, out_dtype);
+}
+
+lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, lattice_dtype in_dtype, int C_in,
+                                const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
+                                lattice_dtype out_dtype) {
+    return resample(coarse, fine, true, in, in_dtype, C_in, w, C_out, dt, bias, out, out_dtype);
 }
 
 lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst) {

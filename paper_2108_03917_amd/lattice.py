@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_PKG, "_lib", "liblattice.so")
 
 OK, E_ARG, E_STATE, E_RANGE, E_CAPACITY, E_NOMEM, E_HIP = range(7)
 F32, BF16 = 0, 1
-STAGES = ("splat", "neighbors", "conv", "slice", "deform", "slice_backward", "conv_backward", "splat_backward")
+STAGES = ("splat", "neighbors", "conv", "slice", "deform", "slice_backward", "conv_backward", "splat_backward",
+          "downsample", "upsample")
 
 EXPORTS = (
     "lattice_create", "lattice_destroy", "lattice_max_vertices", "lattice_splat", "lattice_build_neighbors",
@@ -28,7 +29,7 @@ EXPORTS = (
     "lattice_get_keys", "lattice_get_neighbors", "lattice_get_point_simplex", "lattice_set_timing",
     "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
     "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice", "lattice_slice_backward",
-    "lattice_splat_backward", "lattice_conv_backward",
+    "lattice_splat_backward", "lattice_conv_backward", "lattice_downsample", "lattice_upsample",
 )
 
 _lib = None
@@ -62,6 +63,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_slice_backward": (St, [P, P, I, P, I]),
         "lattice_splat_backward": (St, [P, P, I, I, I, P, P]),
         "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
+        "lattice_downsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
+        "lattice_upsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
         "lattice_num_vertices": (St, [P, ctypes.POINTER(I64)]),
         "lattice_get_status": (St, [P]),
@@ -303,6 +306,55 @@ class Lattice:
                                                    float(b_delta), _ptr(w_cls), _ptr(b_cls), n_cls, _ptr(out),
                                                    _ptr(delta)), "deform_slice")
         return (out, delta) if delta is not None else out
+
+    # -- downsampling / upsampling ----------------------------------------
+    def _resample(self, fn, src: "Lattice", dst: "Lattice", x, w, dtype, bias, out, out_dtype, what):
+        _dev(x, (torch.float32, torch.bfloat16), "x")
+        if dtype == "f32":
+            _dev(w, torch.float32, "w")
+            dt = F32
+        elif dtype == "bf16":
+            _dev(w, torch.bfloat16, "w")
+            dt = BF16
+        else:
+            raise ValueError("dtype must be 'f32' or 'bf16'")
+        C_out, T, C_in = w.shape
+        if T != self.taps or x.dim() != 2 or x.shape[1] != C_in or x.shape[0] < src._rows_needed():
+            raise ValueError(f"w must be [C_out, {self.taps}, C_in] and x [>= {src._rows_needed()}, C_in]")
+        if bias is not None:
+            _dev(bias, torch.float32, "bias")
+            if bias.numel() != C_out:
+                raise ValueError("bias must have C_out entries")
+        need = dst._rows_needed()
+        if out is None:
+            out = torch.empty((max(need, 1), C_out), dtype=_TORCH[out_dtype], device=x.device)
+        _dev(out, (torch.float32, torch.bfloat16), "out")
+        if out.dim() != 2 or out.shape[1] != C_out or out.shape[0] < need:
+            raise ValueError(f"out needs [>= {need}, {C_out}]")
+        # both entry points take (source lattice, destination lattice)
+        st = fn(src._h, dst._h, _ptr(x), _STORAGE[x.dtype], C_in, _ptr(w), C_out, dt, _ptr(bias), _ptr(out),
+                _STORAGE[out.dtype])
+        if st != OK:
+            msg = self._lib.lattice_last_error(dst._h)
+            raise LatticeError(st, f"{what}: {self._lib.lattice_status_string(st).decode()}: "
+                                   f"{msg.decode() if msg else ''}")
+        return out
+
+    def downsample(self, coarse: "Lattice", x: torch.Tensor, w: torch.Tensor, dtype: str = "f32",
+                   bias: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                   out_dtype: str = "f32") -> torch.Tensor:
+        """Strided convolution of this (fine) lattice's values ``x`` onto the
+        vertices of ``coarse`` (the same cloud at twice the scale)."""
+        return self._resample(self._lib.lattice_downsample, self, coarse, x, w, dtype, bias, out, out_dtype,
+                              "downsample")
+
+    def upsample(self, fine: "Lattice", x: torch.Tensor, w: torch.Tensor, dtype: str = "f32",
+                 bias: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                 out_dtype: str = "f32") -> torch.Tensor:
+        """Transposed convolution of this (coarse) lattice's values ``x`` onto
+        the vertices of ``fine``."""
+        return self._resample(self._lib.lattice_upsample, self, fine, x, w, dtype, bias, out, out_dtype,
+                              "upsample")
 
     # -- backward passes ------------------------------------------------
     def slice_backward(self, grad_out: torch.Tensor, out: Optional[torch.Tensor] = None,

@@ -87,3 +87,36 @@ def test_no_device_fails_loudly():
     st = lib.lattice_create(3, sig, 0.0, 10, 0, None, ctypes.byref(out))
     assert st in (B.E_HIP, B.E_NOMEM)
     assert not out.value
+
+
+def test_resample_binding_passes_source_then_destination(monkeypatch):
+    """lattice_downsample(fine, coarse, ...) and lattice_upsample(coarse, fine,
+    ...) both take the source lattice first: the binding must pass the
+    handles in that order (a swapped upsample indexes rows the input does not
+    have)."""
+    import torch
+
+    calls = []
+
+    class Stub:
+        def lattice_downsample(self, *a):
+            calls.append(("down", a[0], a[1]))
+            return 0
+
+        def lattice_upsample(self, *a):
+            calls.append(("up", a[0], a[1]))
+            return 0
+
+    monkeypatch.setattr(B, "_dev", lambda t, dtype, name: t)
+
+    def fake(handle, V):
+        L = object.__new__(B.Lattice)
+        L._lib, L._h, L.taps, L._V, L.m, L.d = Stub(), handle, 9, V, 10, 3
+        return L
+
+    fine, coarse = fake("FINE", 100), fake("COARSE", 40)
+    w = torch.zeros((4, 9, 4))
+    y = fine.downsample(coarse, torch.zeros((100, 4)), w)
+    z = coarse.upsample(fine, torch.zeros((40, 4)), w)
+    assert calls == [("down", "FINE", "COARSE"), ("up", "COARSE", "FINE")]
+    assert y.shape == (40, 4) and z.shape == (100, 4)
