@@ -27,7 +27,12 @@ from a fixed point gradient dL/df: the slice's gradient (a splat of dL/df),
 each conv's input gradient and weight gradient in reverse order (two stages
 each), and the splat's gradient with respect to the point features.
 
-Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train] [--no-cpu-baseline]
+With --op unet the step also builds the coarse lattice (the same points at
+twice the scale), downsamples the last conv's output onto it (a strided
+conv), upsamples it back onto the fine vertices (a transposed conv) and
+slices that: one level of the paper's U-Net.
+
+Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train|unet] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -106,6 +111,25 @@ class Pipeline:
             self.sliced = torch.empty((w.m, self.w_cls.shape[0]), dtype=torch.float32, device=dev)
         else:
             self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
+        if tail == "unet":
+            from datagen.clouds import conv_weight
+
+            sig = np.asarray(w.sigma, dtype=np.float32)
+            self.Lc = Lattice(w.d, 2 * sig, max_points=w.m, stream=self.stream)
+            mvc = self.Lc.max_vertices(w.m)
+            last = self.convs[-1]
+            st = torch.bfloat16 if last.dtype == "bf16" else torch.float32
+            self.rs_dtype = last.dtype
+            wd = torch.from_numpy(conv_weight(c_last, c_last, w.d, seed=600 + w.config)).to(dev)
+            wu = torch.from_numpy(conv_weight(c_last, c_last, w.d, seed=700 + w.config)).to(dev)
+            if last.dtype == "bf16":
+                wd, wu = self.L.weights_to_bf16(wd), self.L.weights_to_bf16(wu)
+            self.w_down, self.w_up = wd, wu
+            # the coarse rows feed a conv of the conv's dtype; the fine rows feed the slice
+            self.coarse_vals = torch.empty((mvc, c_last), dtype=st, device=dev)
+            self.up_vals = torch.empty((mv, c_last), dtype=torch.float32, device=dev)
+            # the last forward conv's output feeds the downsample: store it as its input dtype
+            self.outs[-1] = torch.empty((mv, c_last), dtype=st, device=dev)
         if tail == "train":
             from datagen.clouds import random_rows
 
@@ -169,6 +193,9 @@ class Pipeline:
 
         mark()
         L.splat(self.pos, self.feat, self.batch, values=self.values, want_weight=False)
+        if self.tail == "unet":
+            mark()
+            self.Lc.splat(self.pos, None, self.batch, want_weight=False)
         mark()
         L.build_neighbors()
         x = self.values
@@ -176,6 +203,12 @@ class Pipeline:
             mark()
             L.conv(x, wd, dtype=cv.dtype, out=out)
             x = out
+        if self.tail == "unet":
+            mark()
+            L.downsample(self.Lc, x, self.w_down, dtype=self.rs_dtype, out=self.coarse_vals)
+            mark()
+            self.Lc.upsample(L, self.coarse_vals, self.w_up, dtype=self.rs_dtype, out=self.up_vals)
+            x = self.up_vals
         mark()
         if self.tail == "deform":
             L.deform_slice(x, self.w_delta, self.dw.b_delta, self.w_cls, self.b_cls, out=self.sliced)
@@ -200,6 +233,8 @@ class Pipeline:
 
     def stage_names(self):
         fwd = ["splat", "neighbors"] + [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}" for i, c in enumerate(self.convs)]
+        if self.tail == "unet":
+            return ["splat", "coarse_lattice"] + fwd[1:] + ["downsample", "upsample", "slice"]
         if self.tail != "train":
             return fwd + [self.tail]
         bwd = ["slice_bwd"]
@@ -209,7 +244,7 @@ class Pipeline:
         return fwd + ["slice"] + bwd + ["splat_bwd"]
 
 
-def algorithmic_work(w, V, n_cls=0):
+def algorithmic_work(w, V, n_cls=0, Vc=0):
     """Compulsory HBM bytes (and MFMA flops) of each stage of one step.
 
     splat:     read positions (4d B), batch id (4 B), features (4C B) and write
@@ -261,6 +296,20 @@ def algorithmic_work(w, V, n_cls=0):
                 "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": "f32"}
         # splat backward: the slice of the vertex gradient onto the points
         work["splat_bwd"] = {"bytes": m * (8 * (d + 1) + 4 * C) + V * sg(-1) * C}
+    if n and Vc:
+        last = w.convs[-1]
+        s = 2 if last.dtype == "bf16" else 4
+        # coarse lattice: read the positions (and batch id), write the simplex
+        # record per point and the key per coarse vertex
+        work["coarse_lattice"] = {"bytes": m * (4 * d + 8 * (d + 1) + (4 if w.batch is not None else 0)) + Vc * 8}
+        # downsample: per coarse vertex its T indices and its output row, each
+        # fine row read once, the weights once; 2 T C C flops per coarse vertex
+        work["downsample"] = {"bytes": Vc * (4 * T + s * c_last) + V * s * c_last + T * c_last * c_last * s,
+                              "flops": 2 * Vc * T * c_last * c_last, "dtype": last.dtype}
+        # upsample: per fine vertex its T indices and its fp32 output row, each
+        # coarse row read once; every tap is multiplied (absent ones as zeros)
+        work["upsample"] = {"bytes": V * (4 * T + 4 * c_last) + Vc * s * c_last + T * c_last * c_last * s,
+                            "flops": 2 * V * T * c_last * c_last, "dtype": last.dtype}
     return work
 
 
@@ -277,12 +326,13 @@ def roofline_entry(name, ms, wk):
     return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a / HBM_PEAK_GBS}
 
 
-def cpu_baseline(w, budget_s=20.0, dw=None, train=False):
+def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False):
     """The CPU oracle, as it stands, over the same workload: whole steps
     (lattice build, splat, neighbours, every conv, slice -- or DeformSlice
     with the classifier when `dw` holds its weights; with `train` also the
-    backward pass of every stage) repeated until about `budget_s` seconds,
-    reported as points/s."""
+    backward pass of every stage; with `unet` the coarse lattice, the
+    downsample and the upsample before the slice) repeated until about
+    `budget_s` seconds, reported as points/s."""
     from threadpoolctl import threadpool_info
 
     from oracle import lattice_oracle as O
@@ -306,6 +356,13 @@ def cpu_baseline(w, budget_s=20.0, dw=None, train=False):
                 xi = O.round_bf16(x.astype(np.float32))
                 Wt = O.round_bf16(Wt)
             x, _ = O.conv(xi, nbr, Wt)
+        if unet:
+            from datagen.clouds import conv_weight
+
+            c = x.shape[1]
+            coarse = O.coarsen(w.pos, w.sigma, batch=w.batch)
+            xc, _ = O.downsample(lat, coarse, x, conv_weight(c, c, w.d, seed=600 + w.config))
+            x, _ = O.upsample(coarse, lat, xc, conv_weight(c, c, w.d, seed=700 + w.config))
         if dw is None:
             O.slice_(lat, x)
         else:
@@ -388,9 +445,9 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG)
-    ap.add_argument("--op", choices=("slice", "deform", "train"), default="slice",
-                    help="end the step with the plain slice, with DeformSlice + classifier, or run the "
-                         "forward and backward passes (train)")
+    ap.add_argument("--op", choices=("slice", "deform", "train", "unet"), default="slice",
+                    help="end the step with the plain slice, with DeformSlice + classifier, run the "
+                         "forward and backward passes (train), or add a coarse level (unet)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-flushed stage timings")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -462,7 +519,8 @@ def main(argv=None):
         del flush
 
     n_cls = pipe.w_cls.shape[0] if args.op == "deform" else 0
-    work = algorithmic_work(w, V, n_cls)
+    Vc = pipe.Lc.num_vertices() if args.op == "unet" else 0
+    work = algorithmic_work(w, V, n_cls, Vc)
     def pct(v):
         return {"p10": float(np.percentile(v, 10)), "median": float(np.median(v)), "p90": float(np.percentile(v, 90))}
 
@@ -475,7 +533,7 @@ def main(argv=None):
     # single launch (neighbours, each conv, slice); the splat stage (seven
     # kernels) is reported in `stages` with its own HBM roofline
     # (with --op deform: the DeformSlice + classifier kernel itself)
-    single = [n for n in names if n not in ("splat", "slice_bwd")]
+    single = [n for n in names if n not in ("splat", "slice_bwd", "coarse_lattice", "downsample", "upsample")]
     dominant = "deform" if args.op == "deform" else max(single, key=lambda n: stage_ms[n])
     rf = dict(stages[dominant])
     rf.pop("ms")
@@ -488,7 +546,8 @@ def main(argv=None):
     out = {
         "metric": {"slice": "points/s for splat+conv+slice",
                    "deform": "points/s for splat+conv+deformslice+classifier",
-                   "train": "points/s for splat+conv+slice forward and backward"}[args.op],
+                   "train": "points/s for splat+conv+slice forward and backward",
+                   "unet": "points/s for splat+conv+downsample+upsample+slice"}[args.op],
         "value": w.m * args.steps / sec,
         "unit": "points/s",
         "n_gpus": 1,
@@ -504,7 +563,8 @@ def main(argv=None):
                    "sigma": float(w.sigma[0]), "channels": w.C, "vertices": V,
                    "convs": [f"{c.c_in}->{c.c_out} {c.dtype}" for c in w.convs]}
                   | ({"classes": n_cls, "tail": "deformslice+classifier"} if args.op == "deform" else {})
-                  | ({"tail": "slice, then the backward pass of every stage"} if args.op == "train" else {}),
+                  | ({"tail": "slice, then the backward pass of every stage"} if args.op == "train" else {})
+                  | ({"coarse_vertices": Vc, "tail": "downsample+upsample+slice"} if args.op == "unet" else {}),
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
@@ -518,8 +578,9 @@ def main(argv=None):
     }
     if cold is not None:
         out["stages_cold"] = stages_cold
-    if not args.no_cpu_baseline and args.op == "train":
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, None, train=True)
+    if not args.no_cpu_baseline and args.op in ("train", "unet"):
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, None, train=args.op == "train",
+                                           unet=args.op == "unet")
     elif not args.no_cpu_baseline:
         dw = pipe.dw if args.op == "deform" else None
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, dw)
