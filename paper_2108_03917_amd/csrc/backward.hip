@@ -28,7 +28,7 @@
 // gathered x rows in LDS as fp32 and four wavefronts each accumulate a
 // 32 x 32 block with v_mfma_f32_32x32x2f32 (K = the vertex index).  Each
 // chunk writes its tile to a partial buffer; k_wgrad_reduce adds the nch
-// partials in chunk order, so the result does not depend on scheduling.
+// partials in a fixed order, so the result does not depend on scheduling.
 // The bias gradient (sum_v g_v) is summed from the same g rows by the
 // workgroups of tap 0 and the first input tile.
 #include "internal.h"
@@ -207,14 +207,34 @@ __global__ __launch_bounds__(kBlock) void k_conv_wgrad(const void *__restrict__ 
     }
 }
 
-// out[j] = sum over chunks c (in order) of part[c][j].
+// out[j] = sum over the nch chunk partials part[c][j], in a fixed order:
+// a workgroup owns 64 consecutive outputs; its four wavefronts sum the
+// chunks c = g, g+4, g+8, ... (g = wavefront) with four loads in flight, and
+// the four group sums are added in group order.
+constexpr int kRedCols = 64;
 __global__ __launch_bounds__(kBlock) void k_wgrad_reduce(const float *__restrict__ part, int nch, int64_t n,
                                                          float *__restrict__ out) {
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x; j < n; j += stride) {
-        float s = 0.f;
-        for (int c = 0; c < nch; ++c) s += part[(int64_t)c * n + j];
-        out[j] = s;
+    __shared__ float red[kBlock / kRedCols][kRedCols];
+    const int g = threadIdx.x / kRedCols;
+    const int64_t j = (int64_t)blockIdx.x * kRedCols + (threadIdx.x % kRedCols);
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    if (j < n) {
+        constexpr int G = kBlock / kRedCols;
+        int c = g;
+        for (; c + 3 * G < nch; c += 4 * G) {
+            s0 += part[(int64_t)c * n + j];
+            s1 += part[(int64_t)(c + G) * n + j];
+            s2 += part[(int64_t)(c + 2 * G) * n + j];
+            s3 += part[(int64_t)(c + 3 * G) * n + j];
+        }
+        for (; c < nch; c += G) s0 += part[(int64_t)c * n + j];
+    }
+    red[g][threadIdx.x % kRedCols] = (s0 + s1) + (s2 + s3);
+    __syncthreads();
+    if (g == 0 && j < n) {
+        float t = 0.f;
+        for (int q = 0; q < kBlock / kRedCols; ++q) t += red[q][threadIdx.x];
+        out[j] = t;
     }
 }
 
@@ -283,12 +303,12 @@ hipError_t launch_conv_wgrad(lattice *L, const void *g, lattice_dtype g_dt, int 
     if (e != hipSuccess) return e;
     if (grad_w) {
         const int64_t n = (int64_t)C_out * L->T * C_in;
-        hipLaunchKernelGGL(k_wgrad_reduce, dim3(grid_for(n, kBlock, L->cu_count, 2)), dim3(kBlock), 0, L->stream,
-                           partial, nch, n, grad_w);
+        hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((n + kRedCols - 1) / kRedCols)), dim3(kBlock), 0,
+                           L->stream, partial, nch, n, grad_w);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (grad_bias) {
-        hipLaunchKernelGGL(k_wgrad_reduce, dim3(grid_for(C_out, kBlock, L->cu_count, 1)), dim3(kBlock), 0,
+        hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((C_out + kRedCols - 1) / kRedCols)), dim3(kBlock), 0,
                            L->stream, pbias, nch, (int64_t)C_out, grad_bias);
         e = hipGetLastError();
     }
