@@ -387,3 +387,40 @@ def deform_weights(C: int, n_cls: int, seed: int, gain: float = 3.0) -> DeformWe
     w_cls = (rng.standard_normal((n_cls, C)) / np.sqrt(C)).astype(np.float32)
     b_cls = (rng.standard_normal(n_cls) * 0.1).astype(np.float32)
     return DeformWeights(w_delta, b_delta, w_cls, b_cls)
+
+
+# The PointNet of the network's first layer (1x1 widths 16, 32, 64 in the
+# paper's figure) and the raw per-point features it sees: the indoor room's
+# rgb + normal (6), the first three channels of the other object clouds and
+# one channel (a remission-like scalar) for the LiDAR clouds.
+POINTNET_WIDTHS = (16, 32, 64)
+
+
+def raw_point_features(w: Workload) -> np.ndarray:
+    """Raw per-point features [m, f_d] float32 of a workload (see above)."""
+    if "feat6" in w.extra:
+        return np.ascontiguousarray(w.extra["feat6"], dtype=np.float32)
+    k = 1 if w.config in (4, 5) else 3
+    return np.ascontiguousarray(w.feat[:, :k], dtype=np.float32)
+
+
+def pointnet_weights(k0: int, d: int, sigma: float, seed: int, widths=POINTNET_WIDTHS):
+    """Seeded PointNet parameters: a list of (a, s, W, b) per block, float32.
+
+    a ~ 1 + N(0, 0.1^2) and s ~ N(0, 0.1^2) per input channel (a group
+    normalisation's affine), except that the first block scales the d
+    position channels by 1/sigma (offsets from the local mean are of the
+    order of the lattice scale); W ~ N(0, 2/K) (He), b ~ N(0, 0.01^2)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    k = k0
+    for li, w_out in enumerate(widths):
+        a = (1.0 + 0.1 * rng.standard_normal(k)).astype(np.float32)
+        if li == 0:
+            a[:d] = a[:d] / np.float32(sigma)
+        s = (0.1 * rng.standard_normal(k)).astype(np.float32)
+        W = (rng.standard_normal((w_out, k)) * np.sqrt(2.0 / k)).astype(np.float32)
+        b = (0.01 * rng.standard_normal(w_out)).astype(np.float32)
+        out.append((a, s, W, b))
+        k = w_out
+    return out

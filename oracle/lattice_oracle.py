@@ -533,3 +533,66 @@ def upsample(coarse: Lattice, fine: Lattice, values: np.ndarray, weight: np.ndar
     onto the fine vertices: z_u = sum_t x_{coarse((u + offset_t)/2)} W_t^T (+ bias),
     fractional or absent taps contributing nothing.  Returns (z [V_fine, C_out], scale)."""
     return conv(values, up_neighbors(coarse, fine), weight, bias)
+
+
+# ---------------------------------------------------------------------------
+# Distribute and PointNet (Sec. "Proposed Operations": Distribute, Eq.
+# distribute; the network figure's PointNet block; Sec. "Performance"
+# suggests fusing the two into one operation).
+#
+# Every (point, simplex vertex) pair p in J_v hands the vertex the point's
+# position minus the mean position of all points of J_v, and the point's
+# features, concatenated: h_0 = [g_p - mu_v ; f_p].  A PointNet embeds each
+# such row: blocks of normalisation, ReLU and a 1x1 (fully connected) layer,
+# h_l = W_l relu(a_l * h_{l-1} + s_l) + b_l, where the normalisation enters as
+# the per-channel affine (a_l, s_l) that a group normalisation with known
+# statistics reduces to.  A max over the rows of each vertex (scatter-max)
+# gives its value x_v.
+# ---------------------------------------------------------------------------
+
+def local_mean(lat: Lattice, pos: np.ndarray) -> np.ndarray:
+    """mu_v = (1/|J_v|) sum_{p in J_v} g_p, float64 [V, d]: the mean position of
+    the points whose simplex contains v (every pair counts, whatever its weight)."""
+    g = np.asarray(pos, dtype=np.float64)
+    m, dp1 = lat.idx.shape
+    v = lat.idx.ravel()
+    p = np.repeat(np.arange(m), dp1)
+    s = np.zeros((lat.V, g.shape[1]))
+    np.add.at(s, v, g[p])
+    n = np.bincount(v, minlength=lat.V).astype(np.float64)
+    return s / n[:, None]
+
+
+def distribute_pointnet(lat: Lattice, pos: np.ndarray, feat: Optional[np.ndarray], layers):
+    """Distribute + PointNet + per-vertex max, float64.
+
+    ``layers`` is a list of (a, s, W, b) with W [w_l, K_l]; K_0 = d + f_d.
+    Returns (out [V, w_L], scale [V, w_L], mu [V, d]).  ``scale`` bounds the
+    rounding of a float32 evaluation: per row, the magnitudes |g_p| + |mu_v|
+    and |f_p| carried through |a|, |s|, |W|, |b| (ReLU is 1-Lipschitz), and
+    the max over the vertex's rows."""
+    g = np.asarray(pos, dtype=np.float64)
+    m, dp1 = lat.idx.shape
+    mu = local_mean(lat, pos)
+    v = lat.idx.ravel()
+    p = np.repeat(np.arange(m), dp1)
+    dg = g[p] - mu[v]                                        # D_G: positions minus the local mean
+    sg = np.abs(g[p]) + np.abs(mu[v])
+    if feat is not None and np.asarray(feat).shape[1] > 0:
+        f = np.asarray(feat, dtype=np.float64)[p]            # D_F: the features as they are
+        h = np.concatenate([dg, f], axis=1)
+        sc = np.concatenate([sg, np.abs(f)], axis=1)
+    else:
+        h, sc = dg, sg
+    for a, s, W, b in layers:
+        a = np.asarray(a, dtype=np.float64)
+        s = np.asarray(s, dtype=np.float64)
+        W = np.asarray(W, dtype=np.float64)
+        b = np.asarray(b, dtype=np.float64)
+        h = np.maximum(a * h + s, 0.0) @ W.T + b
+        sc = (np.abs(a) * sc + np.abs(s)) @ np.abs(W).T + np.abs(b)
+    out = np.full((lat.V, h.shape[1]), -np.inf)
+    np.maximum.at(out, v, h)
+    scale = np.zeros_like(out)
+    np.maximum.at(scale, v, sc)
+    return out, scale, mu

@@ -710,3 +710,89 @@ def test_upsample_taps_follow_remainder_parity_in_3d():
     assert np.all(up[~even, 0] == -1)
     assert np.all(up[even, 1:] == -1)
     assert (up[even, 0] >= 0).mean() > 0.2 and (up[~even, 1:] >= 0).any(axis=1).mean() > 0.2
+
+
+# --------------------------------------------------------------------------
+# Distribute + PointNet + per-vertex max (Sec. "Proposed Operations":
+# Distribute; the PointNet block of the network figure)
+# --------------------------------------------------------------------------
+
+def test_distribute_pointnet_worked_example_d1():
+    """Two points of one lattice cell in d = 1 (keys (0,0) and (1,-1)), worked
+    by hand.  Both vertices receive both points; the local mean is their
+    midpoint 0.5, so the distributed rows are (off, f) = (-0.2, 1) and
+    (0.2, -3).  Block 1: a = (1, 1), s = (1, 5) (ReLU is then the identity
+    here), W = [[1, 0], [-1, 0], [0, 1]], b = (-1, 1, -5) gives (off, -off, f);
+    block 2: a = 1, s = 0, W = [[1, 1, 0], [0, 0, 1]], b = 0 gives
+    (|off|, relu f).  Rows (0.2, 1) and (0.2, 0): the max is (0.2, 1) at both
+    vertices.  Without the mean it would be (0.7, 1); with a weighted mean
+    0.28; with a sum (0.4, 1); with [f ; off] concatenated (1, 0.2)."""
+    g = np.array([[0.3], [0.7]], dtype=np.float32)
+    f = np.array([[1.0], [-3.0]], dtype=np.float32)
+    lat = O.build(g, 1.0, alpha=1.0)
+    assert lat.V == 2 and sorted(map(tuple, lat.keys)) == [(0, 0), (1, -1)]
+    mu = O.local_mean(lat, g)
+    assert np.allclose(mu, 0.5, atol=1e-7)
+    L1 = (np.ones(2), np.array([1.0, 5.0]), np.array([[1.0, 0.0], [-1.0, 0.0], [0.0, 1.0]]),
+          np.array([-1.0, 1.0, -5.0]))
+    L2 = (np.ones(3), np.zeros(3), np.array([[1.0, 1.0, 0.0], [0.0, 0.0, 1.0]]), np.zeros(2))
+    out, scale, _ = O.distribute_pointnet(lat, g, f, [L1, L2])
+    assert np.allclose(out, [[0.2, 1.0], [0.2, 1.0]], atol=1e-6)
+    assert np.all(scale >= np.abs(out))
+
+
+def test_local_mean_offsets_sum_to_zero_and_counts():
+    w, lat = _small_lattice(d=3, m=2000, seed=80, C=3)
+    mu = O.local_mean(lat, w.pos)
+    g = w.pos.astype(np.float64)
+    resid = np.zeros_like(mu)
+    m, dp1 = lat.idx.shape
+    for k in range(dp1):
+        np.add.at(resid, lat.idx[:, k], g - mu[lat.idx[:, k]])
+    assert np.abs(resid).max() < 1e-9
+    # |J_v| from the keys themselves: the points whose simplex has v's key
+    keys = O.simplex_keys(*O.enclosing_simplex(lat.x))
+    cnt = {}
+    for kk in keys.reshape(-1, dp1):
+        cnt[tuple(kk)] = cnt.get(tuple(kk), 0) + 1
+    n = np.bincount(lat.idx.ravel(), minlength=lat.V)
+    assert all(cnt[tuple(lat.keys[v])] == n[v] for v in range(lat.V))
+
+
+def test_distribute_pointnet_matches_torch_index_reduce():
+    """The same network built from torch primitives (float64, CPU):
+    index_reduce 'mean' for the local mean, F.linear for the 1x1 layers and
+    index_reduce 'amax' for the per-vertex max."""
+    torch = pytest.importorskip("torch")
+    from datagen.clouds import pointnet_weights
+
+    w, lat = _small_lattice(d=3, m=3000, seed=81, C=4)
+    layers = pointnet_weights(3 + 4, 3, 0.15, seed=82)
+    out, _, mu = O.distribute_pointnet(lat, w.pos, w.feat, layers)
+    m, dp1 = lat.idx.shape
+    v = torch.from_numpy(lat.idx.ravel())
+    p = torch.arange(m).repeat_interleave(dp1)
+    g = torch.from_numpy(w.pos.astype(np.float64))
+    f = torch.from_numpy(w.feat.astype(np.float64))
+    tmu = torch.zeros((lat.V, 3), dtype=torch.float64).index_reduce_(0, v, g[p], "mean", include_self=False)
+    h = torch.cat([g[p] - tmu[v], f[p]], dim=1)
+    for a, s, W, b in layers:
+        h = torch.nn.functional.linear(torch.relu(torch.from_numpy(a.astype(np.float64)) * h
+                                                  + torch.from_numpy(s.astype(np.float64))),
+                                       torch.from_numpy(W.astype(np.float64)), torch.from_numpy(b.astype(np.float64)))
+    tout = torch.zeros((lat.V, h.shape[1]), dtype=torch.float64).index_reduce_(0, v, h, "amax", include_self=False)
+    assert np.allclose(mu, tmu.numpy(), rtol=1e-12, atol=1e-12)
+    assert np.allclose(out, tout.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_distribute_pointnet_is_point_permutation_invariant():
+    from datagen.clouds import pointnet_weights
+
+    w, lat = _small_lattice(d=4, m=1500, seed=83, C=2)
+    layers = pointnet_weights(4 + 2, 4, 0.15, seed=84)
+    out, _, _ = O.distribute_pointnet(lat, w.pos, w.feat, layers)
+    perm = np.random.default_rng(0).permutation(w.m)
+    lat2 = O.build(w.pos[perm], 0.15)
+    out2, _, _ = O.distribute_pointnet(lat2, w.pos[perm], w.feat[perm], layers)
+    assert np.array_equal(lat.keys, lat2.keys)
+    assert np.allclose(out, out2, rtol=1e-12, atol=1e-12)
