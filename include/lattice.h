@@ -371,6 +371,39 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
                                 lattice_dtype out_dtype);
 
 /*
+ * lattice_distribute_pointnet -- Distribute + PointNet + per-vertex max, fused
+ * into one operation so that the distributed rows are never stored.
+ *
+ * Sec. "Proposed Operations" (Distribute, Eq. distribute), the PointNet block
+ * of the network figure, and Sec. "Performance" (fusing the two).  Every pair
+ * (point p, vertex v of p's simplex) of the last splat is one row
+ *   h_0 = [g_p - mu_v ; f_p],  mu_v = mean of g_q over the points q of J_v
+ *   (every pair counts, whatever its barycentric weight);
+ * three blocks of normalisation, ReLU and a fully connected (1x1) layer
+ *   h_l = W_l relu(a_l * h_{l-1} + s_l) + b_l,  widths 16, 32, 64;
+ * and x_v = max over the rows of v of h_3, per channel.  (a_l, s_l) is the
+ * normalisation as a per-channel affine, which is what a group normalisation
+ * reduces to once its statistics are known; its statistics are not computed
+ * here.  fp32 products and sums; mu_v summed in fp64.
+ *   pos       dev [m][d] fp32, the positions the last splat was given.
+ *   feat      dev [m][f_d] fp32 point features, or NULL when f_d = 0.
+ *   f_d       feature channels, 0 <= f_d <= 16 - d.
+ *   params    dev fp32, per block l = 1, 2, 3 in order: a [K_l], s [K_l],
+ *             W [w_l][K_l] (row-major), b [w_l]; K_1 = d + f_d, K_2 = 16,
+ *             K_3 = 32, w = 16, 32, 64.
+ *   n_blocks  3;  widths  host [3], must be {16, 32, 64} (the widths the
+ *             fused kernel is built for).
+ *   out       dev [>= V][64] fp32 output x_v (rows 0..V-1 written).
+ *   mean      dev [>= V][d] fp32 output mu_v, or NULL.
+ * The first call allocates the lattice's scratch for it (an entry-to-vertex
+ * map and fp64 position sums).  Returns LATTICE_E_STATE before the first
+ * splat, LATTICE_E_ARG for anything outside the above.
+ */
+lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
+                                           const float *params, int n_blocks, const int *widths, float *out,
+                                           float *mean);
+
+/*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to
  * even) on the lattice's stream: the weight format LATTICE_BF16 convs take.
  *   src  dev [n] fp32;  dst  dev [n] uint16 (bf16 bit patterns).
@@ -412,7 +445,7 @@ lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary);
  * of launches since the last reset (arrays of LATTICE_NUM_STAGES).
  * lattice_set_timing(L, 0) stops recording; (L, 2) resets the sums.
  */
-#define LATTICE_NUM_STAGES 10
+#define LATTICE_NUM_STAGES 11
 enum {
     LATTICE_STAGE_SPLAT = 0,
     LATTICE_STAGE_NEIGHBORS = 1,
@@ -423,7 +456,8 @@ enum {
     LATTICE_STAGE_CONV_BACKWARD = 6,
     LATTICE_STAGE_SPLAT_BACKWARD = 7,
     LATTICE_STAGE_DOWNSAMPLE = 8,  /* recorded on the output (coarse) lattice */
-    LATTICE_STAGE_UPSAMPLE = 9     /* recorded on the output (fine) lattice   */
+    LATTICE_STAGE_UPSAMPLE = 9,    /* recorded on the output (fine) lattice   */
+    LATTICE_STAGE_DISTRIBUTE = 10
 };
 lattice_status lattice_set_timing(lattice *L, int mode);
 lattice_status lattice_get_timing(lattice *L, double *ms, int64_t *count);

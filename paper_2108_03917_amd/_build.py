@@ -19,7 +19,7 @@ LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "liblattice.so")
 ARCH = "gfx950"
 
-SOURCES = ["lattice.hip", "splat.hip", "neighbors.hip", "conv.hip", "slice.hip", "deform.hip", "backward.hip"]
+SOURCES = ["lattice.hip", "splat.hip", "neighbors.hip", "conv.hip", "slice.hip", "deform.hip", "backward.hip", "distribute.hip"]
 EXTRA = {"splat.hip": ["-ffp-contract=off"]}
 
 

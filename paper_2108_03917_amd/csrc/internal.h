@@ -15,6 +15,11 @@ enum : int { ST_CAPACITY = 1, ST_RANGE = 2 };
 // cuts into parts, and those parts.
 enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_SPLIT = 3, CNT_ROWS = 4, CNT_WORDS = 8 };
 
+// A vertex's pair list longer than kPart pairs is cut into parts of kPart
+// pairs (the splat's gather work units, also used by the distribute op); the
+// splat's numbering records the split vertices and their part rows.
+constexpr int kPart = 32;
+
 // Packed 64-bit vertex key: 16 bits per coordinate c_0..c_{d-1}, each stored
 // as c + KEY_BIAS (so a field is never 0 for |c| <= KEY_MAX), and for d <= 3
 // the batch id in bits 48..63.  c_d is implied by the zero sum.  0 marks an
@@ -67,6 +72,10 @@ struct lattice {
     uint64_t xsrc_gen[2] = {0, 0};
     uint64_t xown_gen[2] = {0, 0};
     uint64_t gen = 0;           // incremented by every splat
+    // Distribute + PointNet scratch (distribute.hip), allocated on first use.
+    int32_t *lvert = nullptr;   // [(d+1) max_points] vertex of each pair-list entry
+    double *macc = nullptr;     // [max_vertices][d] position sums of lists that cross a 64-entry chunk
+    float *mu = nullptr;        // [max_vertices][d] local means when the caller does not take them
     int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
     int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
@@ -124,6 +133,11 @@ hipError_t launch_conv_wgrad(lattice *L, const void *g, lattice_dtype g_dt, int 
                              lattice_dtype x_dt, int C_in, lattice_dtype dt, int nch, float *partial,
                              float *pbias, float *grad_w, float *grad_bias);
 hipError_t launch_flip_weights(lattice *L, const void *w, bool bf16, int C_out, int C_in, void *wt);
+
+// distribute.hip
+hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
+                                      float *out, float *mean);
+int pointnet_param_count(int k0);
 
 // deform.hip
 int deform_max_channels(const void *values, lattice_dtype values_dt, int C, const float *w_delta, const float *w_cls,

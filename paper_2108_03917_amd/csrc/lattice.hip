@@ -51,6 +51,9 @@ void free_all(lattice *L) {
     (void)hipFree(L->wgpart);
     (void)hipFree(L->xtab[0]);
     (void)hipFree(L->xtab[1]);
+    (void)hipFree(L->lvert);
+    (void)hipFree(L->macc);
+    (void)hipFree(L->mu);
     (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
     (void)hipFree(L->rank);
@@ -583,6 +586,46 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
                                 const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
                                 lattice_dtype out_dtype) {
     return resample(coarse, fine, true, in, in_dtype, C_in, w, C_out, dt, bias, out, out_dtype);
+}
+
+lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
+                                           const float *params, int n_blocks, const int *widths, float *out,
+                                           float *mean) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "distribute_pointnet: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    if (f_d < 0 || L->d + f_d > 16 || (f_d > 0 && L->m > 0 && !feat) || !params || !widths || n_blocks != 3 ||
+        widths[0] != 16 || widths[1] != 32 || widths[2] != 64 || (L->m > 0 && (!pos || !out))) {
+        set_err(L, "distribute_pointnet: bad argument (f_d = %d; the fused PointNet has 3 blocks of widths 16, "
+                "32, 64 and d + f_d <= 16)", f_d);
+        return LATTICE_E_ARG;
+    }
+    const int64_t E_max = (int64_t)(L->d + 1) * L->max_points;
+    lattice_status s = LATTICE_OK;
+    if (!L->lvert) {
+        bool ok = hipMalloc(&L->lvert, E_max * sizeof(int32_t)) == hipSuccess &&
+                  hipMalloc(&L->macc, L->max_vertices * L->d * sizeof(double)) == hipSuccess &&
+                  hipMalloc(&L->mu, L->max_vertices * L->d * sizeof(float)) == hipSuccess;
+        if (!ok) {
+            (void)hipGetLastError();
+            (void)hipFree(L->lvert);
+            (void)hipFree(L->macc);
+            (void)hipFree(L->mu);
+            L->lvert = nullptr;
+            L->macc = nullptr;
+            L->mu = nullptr;
+            set_err(L, "distribute_pointnet: cannot allocate its scratch");
+            return LATTICE_E_NOMEM;
+        }
+    }
+    hipEvent_t t0;
+    if ((s = timer_begin(L, LATTICE_STAGE_DISTRIBUTE, &t0))) return s;
+    if ((s = check_launch(L, launch_distribute_pointnet(L, pos, feat, f_d, params, out, mean),
+                          "distribute_pointnet")))
+        return s;
+    return timer_end(L, LATTICE_STAGE_DISTRIBUTE, t0);
 }
 
 lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst) {

@@ -428,7 +428,6 @@ __global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap
 constexpr int kPairsPerThread = 4;
 constexpr int64_t kChunk = (int64_t)kBlock * kPairsPerThread;
 constexpr int64_t kMaxScanBlocks = 4096;
-constexpr int kPart = 32;  // pairs per gather work unit
 
 __device__ __forceinline__ int wave_incl_scan(int x, int lane) {
 #pragma unroll

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_PKG, "_lib", "liblattice.so")
 OK, E_ARG, E_STATE, E_RANGE, E_CAPACITY, E_NOMEM, E_HIP = range(7)
 F32, BF16 = 0, 1
 STAGES = ("splat", "neighbors", "conv", "slice", "deform", "slice_backward", "conv_backward", "splat_backward",
-          "downsample", "upsample")
+          "downsample", "upsample", "distribute")
 
 EXPORTS = (
     "lattice_create", "lattice_destroy", "lattice_max_vertices", "lattice_splat", "lattice_build_neighbors",
@@ -30,6 +30,7 @@ EXPORTS = (
     "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
     "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice", "lattice_slice_backward",
     "lattice_splat_backward", "lattice_conv_backward", "lattice_downsample", "lattice_upsample",
+    "lattice_distribute_pointnet",
 )
 
 _lib = None
@@ -63,6 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_slice_backward": (St, [P, P, I, P, I]),
         "lattice_splat_backward": (St, [P, P, I, I, I, P, P]),
         "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
+        "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, P]),
         "lattice_downsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_upsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
@@ -306,6 +308,58 @@ class Lattice:
                                                    float(b_delta), _ptr(w_cls), _ptr(b_cls), n_cls, _ptr(out),
                                                    _ptr(delta)), "deform_slice")
         return (out, delta) if delta is not None else out
+
+    # -- distribute + PointNet ---------------------------------------------
+    POINTNET_WIDTHS = (16, 32, 64)
+
+    @staticmethod
+    def pack_pointnet(layers) -> torch.Tensor:
+        """Pack [(a, s, W, b)] per block (array-likes) into the flat fp32
+        layout lattice_distribute_pointnet takes (a, s, W row-major, b per
+        block), on the CPU."""
+        parts = []
+        for a, s, W, b in layers:
+            parts += [torch.as_tensor(x, dtype=torch.float32).reshape(-1) for x in (a, s, W, b)]
+        return torch.cat(parts)
+
+    def distribute_pointnet(self, pos: torch.Tensor, feat: Optional[torch.Tensor], params: torch.Tensor,
+                            out: Optional[torch.Tensor] = None, mean: Optional[torch.Tensor] = None,
+                            want_mean: bool = False):
+        """Distribute + PointNet + per-vertex max over the last splat's pairs:
+        ``pos`` [m, d] (the positions that were splatted), ``feat`` [m, f_d]
+        or None, ``params`` the packed parameters (see pack_pointnet) on the
+        device.  Returns out [rows, 64] (and the local means [rows, d] with
+        want_mean or a ``mean`` tensor)."""
+        _dev(pos, torch.float32, "pos")
+        if pos.dim() != 2 or pos.shape != (self.m, self.d):
+            raise ValueError(f"pos must be the splatted [m = {self.m}, {self.d}] positions")
+        f_d = 0
+        if feat is not None:
+            _dev(feat, torch.float32, "feat")
+            if feat.dim() != 2 or feat.shape[0] != self.m:
+                raise ValueError("feat must be [m, f_d]")
+            f_d = feat.shape[1]
+        _dev(params, torch.float32, "params")
+        k0 = self.d + f_d
+        n_par = 2 * k0 + 16 * k0 + 16 + 2 * 16 + 32 * 16 + 32 + 2 * 32 + 64 * 32 + 64
+        if params.numel() != n_par:
+            raise ValueError(f"params must hold {n_par} values for d + f_d = {k0}")
+        need = self._rows_needed()
+        if out is None:
+            out = torch.empty((max(need, 1), 64), dtype=torch.float32, device=pos.device)
+        _dev(out, torch.float32, "out")
+        if out.dim() != 2 or out.shape[1] != 64 or out.shape[0] < need:
+            raise ValueError(f"out needs [>= {need}, 64]")
+        if mean is None and want_mean:
+            mean = torch.empty((max(need, 1), self.d), dtype=torch.float32, device=pos.device)
+        if mean is not None:
+            _dev(mean, torch.float32, "mean")
+            if mean.numel() < need * self.d:
+                raise ValueError(f"mean needs [>= {need}, {self.d}]")
+        widths = (ctypes.c_int * 3)(*self.POINTNET_WIDTHS)
+        self._check(self._lib.lattice_distribute_pointnet(self._h, _ptr(pos), _ptr(feat), f_d, _ptr(params), 3,
+                                                          widths, _ptr(out), _ptr(mean)), "distribute_pointnet")
+        return (out, mean) if mean is not None else out
 
     # -- downsampling / upsampling ----------------------------------------
     def _resample(self, fn, src: "Lattice", dst: "Lattice", x, w, dtype, bias, out, out_dtype, what):

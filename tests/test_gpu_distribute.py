@@ -1,0 +1,107 @@
+"""GPU parity of Distribute + PointNet + per-vertex max (the fused operation)
+against the CPU oracle, through the C ABI.
+
+Every output row x_v (64 channels) is compared with the oracle's float64
+value within 1e-5 of its scale (the rows' magnitudes carried through |a|,
+|s|, |W|, |b|, the max over the vertex's rows); the local means within a few
+fp32 ulps of their magnitude.  Vertex order is canonicalised by sorted key.
+"""
+import numpy as np
+import pytest
+import torch
+
+from datagen.clouds import make_workload, pointnet_weights, random_cloud, raw_point_features
+from oracle import lattice_oracle as O
+from tests.gpu_util import REL_F32, GpuLattice, assert_close_scaled, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2108_03917_amd import load_library
+
+    load_library()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _run(pos, feat, sigma, batch=None, seed=0):
+    from paper_2108_03917_amd import Lattice
+
+    d = pos.shape[1]
+    f_d = 0 if feat is None else feat.shape[1]
+    L = Lattice(d, sigma, max_points=max(pos.shape[0], 1))
+    g = GpuLattice(L, pos, None, batch=batch)
+    lat = O.build(pos, sigma, batch=batch)
+    assert np.array_equal(g.keys, lat.keys)
+    sig0 = float(np.asarray(sigma, dtype=np.float64).reshape(-1)[0])
+    layers = pointnet_weights(d + f_d, d, sig0, seed=seed)
+    params = Lattice.pack_pointnet(layers).to("cuda:0")
+    out, mean = L.distribute_pointnet(to_dev(pos), None if feat is None else to_dev(feat), params, want_mean=True)
+    ref, scale, mu = O.distribute_pointnet(lat, pos, feat, layers)
+    got = g.from_gpu_order(out)
+    gmu = g.from_gpu_order(mean)
+    assert np.all(np.isfinite(got))
+    assert_close_scaled(gmu, mu, 2.0 ** -22 * np.abs(mu) + 1e-7 * np.abs(pos).max(), 1.0, "local mean")
+    assert_close_scaled(got, ref, scale, REL_F32, f"distribute+pointnet d={d} f_d={f_d}")
+    return lat
+
+
+@pytest.mark.parametrize("d,m,sigma,f_d", [(3, 6000, 0.15, 6), (3, 5000, 0.1, 0), (4, 5000, 0.3, 1),
+                                           (2, 4000, 0.08, 3)])
+def test_distribute_pointnet_parity(d, m, sigma, f_d):
+    w = random_cloud(m, d, seed=500 + d + f_d, extent=1.0, C=max(f_d, 1))
+    _run(w.pos, w.feat[:, :f_d] if f_d else None, sigma, seed=501 + d)
+
+
+def test_distribute_pointnet_batched():
+    w = random_cloud(6000, 3, seed=510, extent=1.0, C=3, n_batch=5)
+    _run(w.pos, w.feat, 0.15, batch=w.batch, seed=511)
+
+
+def test_distribute_pointnet_long_lists():
+    """Tight clusters: vertices with hundreds to thousands of rows, whose
+    lists span many 64-entry chunks (atomic max and fp64 atomic mean) and
+    are mapped in 32-entry parts."""
+    rng = np.random.default_rng(520)
+    centres = rng.uniform(-0.8, 0.8, size=(3, 3))
+    dense = centres[rng.integers(0, 3, 6000)] + rng.normal(0, 0.01, size=(6000, 3))
+    sparse = rng.uniform(-1, 1, size=(3000, 3))
+    pos = np.concatenate([dense, sparse]).astype(np.float32)[rng.permutation(9000)]
+    feat = rng.standard_normal((9000, 4)).astype(np.float32)
+    lat = _run(pos, feat, 0.1, seed=521)
+    n = np.bincount(lat.idx.ravel(), minlength=lat.V)
+    assert n.max() > 500 and (n > 64).sum() >= 3
+
+
+def test_distribute_pointnet_empty_and_rejects():
+    from paper_2108_03917_amd import Lattice, LatticeError
+
+    L = Lattice(3, 0.1, max_points=16)
+    L.splat(torch.zeros((0, 3), device="cuda:0"), None)
+    params = Lattice.pack_pointnet(pointnet_weights(3, 3, 0.1, seed=1)).to("cuda:0")
+    L.distribute_pointnet(torch.zeros((0, 3), device="cuda:0"), None, params)   # m = 0: nothing to do
+    torch.cuda.synchronize()
+    import ctypes
+
+    feat = torch.zeros((1, 16), device="cuda:0")
+    ok_widths = (ctypes.c_int * 3)(16, 32, 64)
+    with pytest.raises(LatticeError):        # d + f_d = 17 > 16
+        L._check(L._lib.lattice_distribute_pointnet(L._h, None, feat.data_ptr(), 14, params.data_ptr(), 3,
+                                                    ok_widths, None, None), "distribute_pointnet")
+    with pytest.raises(LatticeError):        # widths other than 16, 32, 64
+        L._check(L._lib.lattice_distribute_pointnet(L._h, None, None, 0, params.data_ptr(), 3,
+                                                    (ctypes.c_int * 3)(16, 32, 32), None, None),
+                 "distribute_pointnet")
+
+
+@pytest.mark.parametrize("config", [3, 4])
+def test_distribute_pointnet_full_size(config):
+    """The indoor room (200k points, rgb + normal) and the LiDAR scan (about
+    1.04e5 points in scan order, dense near the sensor), every vertex compared."""
+    w = make_workload(config)
+    _run(w.pos, raw_point_features(w), w.sigma, seed=530 + config)
