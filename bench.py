@@ -32,7 +32,13 @@ twice the scale), downsamples the last conv's output onto it (a strided
 conv), upsamples it back onto the fine vertices (a transposed conv) and
 slices that: one level of the paper's U-Net.
 
-Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train|unet] [--no-cpu-baseline]
+With --op pointnet the network's input layer replaces the splat of the
+features: the step builds the lattice, then Distribute + PointNet + per-vertex
+max (fused) turns the raw point features into the 64-channel vertex values
+the convs take (workloads whose first conv has 64 inputs).
+
+Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train|unet|pointnet]
+       [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -51,6 +57,10 @@ import numpy as np  # noqa: E402
 DEFAULT_CONFIG = 2          # part-segmentation-shaped batch: 16 objects x 2500 points
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+# fp32 vector units: 256 CUs x 4 SIMDs x 2.4 GHz x 64 lanes x 2 flops (FMA) at
+# the published rate; without packed fp32 instructions one wave64 FMA issues
+# every second cycle, so 78.6 TFLOP/s is the reachable ceiling here.
+ALU_PEAK_TFLOPS = 157.3
 
 WORKLOAD_NAMES = {
     1: "tiny-spheres-4096pts-d3",
@@ -111,6 +121,17 @@ class Pipeline:
             self.sliced = torch.empty((w.m, self.w_cls.shape[0]), dtype=torch.float32, device=dev)
         else:
             self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
+        if tail == "pointnet":
+            from datagen.clouds import pointnet_weights, raw_point_features
+
+            if not self.convs or self.convs[0].c_in != 64:
+                raise SystemExit("--op pointnet needs a workload whose first conv takes the PointNet's 64 channels "
+                                 "(workloads 2, 3, 5)")
+            raw = raw_point_features(w)
+            self.raw = torch.from_numpy(raw).to(dev)
+            self.pn_layers = pointnet_weights(w.d + raw.shape[1], w.d, float(w.sigma[0]), seed=800 + w.config)
+            self.pn_params = Lattice.pack_pointnet(self.pn_layers).to(dev)
+            self.values = torch.empty((mv, 64), dtype=torch.float32, device=dev)
         if tail == "unet":
             from datagen.clouds import conv_weight
 
@@ -192,7 +213,12 @@ class Pipeline:
                 k += 1
 
         mark()
-        L.splat(self.pos, self.feat, self.batch, values=self.values, want_weight=False)
+        if self.tail == "pointnet":
+            L.splat(self.pos, None, self.batch, want_weight=False)
+            mark()
+            L.distribute_pointnet(self.pos, self.raw, self.pn_params, out=self.values)
+        else:
+            L.splat(self.pos, self.feat, self.batch, values=self.values, want_weight=False)
         if self.tail == "unet":
             mark()
             self.Lc.splat(self.pos, None, self.batch, want_weight=False)
@@ -235,6 +261,8 @@ class Pipeline:
         fwd = ["splat", "neighbors"] + [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}" for i, c in enumerate(self.convs)]
         if self.tail == "unet":
             return ["splat", "coarse_lattice"] + fwd[1:] + ["downsample", "upsample", "slice"]
+        if self.tail == "pointnet":
+            return ["lattice", "distribute"] + fwd[1:] + ["slice"]
         if self.tail != "train":
             return fwd + [self.tail]
         bwd = ["slice_bwd"]
@@ -244,7 +272,7 @@ class Pipeline:
         return fwd + ["slice"] + bwd + ["splat_bwd"]
 
 
-def algorithmic_work(w, V, n_cls=0, Vc=0):
+def algorithmic_work(w, V, n_cls=0, Vc=0, f_raw=-1):
     """Compulsory HBM bytes (and MFMA flops) of each stage of one step.
 
     splat:     read positions (4d B), batch id (4 B), features (4C B) and write
@@ -296,6 +324,18 @@ def algorithmic_work(w, V, n_cls=0, Vc=0):
                 "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": "f32"}
         # splat backward: the slice of the vertex gradient onto the points
         work["splat_bwd"] = {"bytes": m * (8 * (d + 1) + 4 * C) + V * sg(-1) * C}
+    if f_raw >= 0:
+        E = m * (d + 1)
+        k0 = d + f_raw
+        # lattice only: read the positions (and batch id), write the record per
+        # point and the key per vertex
+        work["lattice"] = {"bytes": m * (4 * d + 8 * (d + 1) + (4 if w.batch is not None else 0)) + V * 8}
+        # distribute + PointNet: read each point's position and raw features,
+        # each pair-list entry (8 B) and each vertex's list header (8 B), write
+        # the 64-channel fp32 row; 2 (k0 16 + 16 32 + 32 64) flops per pair on
+        # fp32 MFMA
+        work["distribute"] = {"bytes": m * 4 * (d + f_raw) + E * 8 + V * (8 + 4 * 64),
+                              "flops": 2 * E * (k0 * 16 + 16 * 32 + 32 * 64), "dtype": "f32"}
     if n and Vc:
         last = w.convs[-1]
         s = 2 if last.dtype == "bf16" else 4
@@ -315,8 +355,15 @@ def algorithmic_work(w, V, n_cls=0, Vc=0):
 
 def roofline_entry(name, ms, wk):
     """achieved vs peak for one stage: MFMA-bound convs where their arithmetic
-    intensity exceeds the ridge, HBM otherwise."""
-    if "flops" in wk:
+    intensity exceeds the ridge, vector-ALU-bound work (dtype "alu") against the
+    fp32 vector peak, HBM otherwise."""
+    if wk.get("dtype") == "alu":
+        ridge = ALU_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+        if wk["flops"] / wk["bytes"] >= ridge:
+            a = wk["flops"] / (ms * 1e-3) / 1e12
+            return {"bound": "alu", "achieved": a, "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": a / ALU_PEAK_TFLOPS}
+    elif "flops" in wk:
         peak_t = MFMA_PEAK_TFLOPS[wk["dtype"]]
         ridge = peak_t * 1e12 / (HBM_PEAK_GBS * 1e9)
         if wk["flops"] / wk["bytes"] >= ridge:
@@ -326,13 +373,14 @@ def roofline_entry(name, ms, wk):
     return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a / HBM_PEAK_GBS}
 
 
-def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False):
+def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False, pointnet=None):
     """The CPU oracle, as it stands, over the same workload: whole steps
     (lattice build, splat, neighbours, every conv, slice -- or DeformSlice
     with the classifier when `dw` holds its weights; with `train` also the
     backward pass of every stage; with `unet` the coarse lattice, the
-    downsample and the upsample before the slice) repeated until about
-    `budget_s` seconds, reported as points/s."""
+    downsample and the upsample before the slice; with `pointnet` (its
+    layers) Distribute + PointNet instead of the features' splat) repeated
+    until about `budget_s` seconds, reported as points/s."""
     from threadpoolctl import threadpool_info
 
     from oracle import lattice_oracle as O
@@ -343,9 +391,17 @@ def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False):
         c_last = w.convs[-1].c_out if w.convs else w.C
         gout = random_rows(w.m, c_last, seed=500 + w.config)
 
+    if pointnet is not None:
+        from datagen.clouds import raw_point_features
+
+        raw = raw_point_features(w)
+
     def one():
         lat = O.build(w.pos, w.sigma, batch=w.batch)
-        x, _, _ = O.splat(lat, w.feat)
+        if pointnet is not None:
+            x, _, _ = O.distribute_pointnet(lat, w.pos, raw, pointnet)
+        else:
+            x, _, _ = O.splat(lat, w.feat)
         nbr = O.neighbors(lat)
         ins = []
         for cv in w.convs:
@@ -445,9 +501,10 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG)
-    ap.add_argument("--op", choices=("slice", "deform", "train", "unet"), default="slice",
+    ap.add_argument("--op", choices=("slice", "deform", "train", "unet", "pointnet"), default="slice",
                     help="end the step with the plain slice, with DeformSlice + classifier, run the "
-                         "forward and backward passes (train), or add a coarse level (unet)")
+                         "forward and backward passes (train), add a coarse level (unet), or start with "
+                         "Distribute + PointNet (pointnet)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-flushed stage timings")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -520,7 +577,8 @@ def main(argv=None):
 
     n_cls = pipe.w_cls.shape[0] if args.op == "deform" else 0
     Vc = pipe.Lc.num_vertices() if args.op == "unet" else 0
-    work = algorithmic_work(w, V, n_cls, Vc)
+    f_raw = pipe.raw.shape[1] if args.op == "pointnet" else -1
+    work = algorithmic_work(w, V, n_cls, Vc, f_raw)
     def pct(v):
         return {"p10": float(np.percentile(v, 10)), "median": float(np.median(v)), "p90": float(np.percentile(v, 90))}
 
@@ -533,7 +591,8 @@ def main(argv=None):
     # single launch (neighbours, each conv, slice); the splat stage (seven
     # kernels) is reported in `stages` with its own HBM roofline
     # (with --op deform: the DeformSlice + classifier kernel itself)
-    single = [n for n in names if n not in ("splat", "slice_bwd", "coarse_lattice", "downsample", "upsample")]
+    single = [n for n in names if n not in ("splat", "slice_bwd", "coarse_lattice", "downsample", "upsample",
+                                            "lattice", "distribute")]
     dominant = "deform" if args.op == "deform" else max(single, key=lambda n: stage_ms[n])
     rf = dict(stages[dominant])
     rf.pop("ms")
@@ -547,7 +606,8 @@ def main(argv=None):
         "metric": {"slice": "points/s for splat+conv+slice",
                    "deform": "points/s for splat+conv+deformslice+classifier",
                    "train": "points/s for splat+conv+slice forward and backward",
-                   "unet": "points/s for splat+conv+downsample+upsample+slice"}[args.op],
+                   "unet": "points/s for splat+conv+downsample+upsample+slice",
+                   "pointnet": "points/s for lattice+distribute/pointnet+conv+slice"}[args.op],
         "value": w.m * args.steps / sec,
         "unit": "points/s",
         "n_gpus": 1,
@@ -564,11 +624,13 @@ def main(argv=None):
                    "convs": [f"{c.c_in}->{c.c_out} {c.dtype}" for c in w.convs]}
                   | ({"classes": n_cls, "tail": "deformslice+classifier"} if args.op == "deform" else {})
                   | ({"tail": "slice, then the backward pass of every stage"} if args.op == "train" else {})
-                  | ({"coarse_vertices": Vc, "tail": "downsample+upsample+slice"} if args.op == "unet" else {}),
+                  | ({"coarse_vertices": Vc, "tail": "downsample+upsample+slice"} if args.op == "unet" else {})
+                  | ({"head": f"distribute+pointnet ({w.d}+{f_raw} -> 16 -> 32 -> 64)"} if args.op == "pointnet"
+                     else {}),
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
-        "hbm_frac_splat_slice": None if args.op == "deform" else
+        "hbm_frac_splat_slice": None if args.op in ("deform", "pointnet") else
         (work["splat"]["bytes"] + work["slice"]["bytes"]) / ((stage_ms["splat"] + stage_ms["slice"]) * 1e-3)
         / (HBM_PEAK_GBS * 1e9),
         "timing": ("value: " + ("graph replays" if args.graph else "eager steps") + " of the whole step, no "
@@ -578,9 +640,10 @@ def main(argv=None):
     }
     if cold is not None:
         out["stages_cold"] = stages_cold
-    if not args.no_cpu_baseline and args.op in ("train", "unet"):
+    if not args.no_cpu_baseline and args.op in ("train", "unet", "pointnet"):
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, None, train=args.op == "train",
-                                           unet=args.op == "unet")
+                                           unet=args.op == "unet",
+                                           pointnet=pipe.pn_layers if args.op == "pointnet" else None)
     elif not args.no_cpu_baseline:
         dw = pipe.dw if args.op == "deform" else None
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, dw)

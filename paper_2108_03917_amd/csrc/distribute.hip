@@ -18,19 +18,22 @@
 //                    also zeroes the vertex's fp64 position sum
 //   k_local_mean     one lane per entry; each wavefront owns 64 consecutive
 //                    entries and sums the positions of each run of equal
-//                    vertex in fp64 (LDS, one lane per coordinate); a run
+//                    vertex in fp64 (a segmented scan over shuffles); a run
 //                    that is the vertex's whole list writes mu_v, otherwise
 //                    the run is added to the vertex's fp64 sum atomically
 //   k_mean_finish    mu_v of the lists that cross a 64-entry chunk
-//   k_pointnet_init  -inf in the output rows of those vertices
-//   k_pointnet       one lane per entry runs the three blocks (parameters
-//                    in LDS, read by all lanes at once); block 3's outputs go
-//                    to LDS channel-major, 32 channels at a time; then lane c
-//                    walks the wavefront's entries keeping the running max of
-//                    channel c and stores it at the end of each run: a plain
-//                    store (32 lanes, half a row) when the run is the
-//                    vertex's whole list, else an atomic max.  The max is exact in any order, so the
-//                    result does not depend on scheduling.
+//   k_pointnet_rows  the key of -inf in the output rows of those vertices
+//                    (and, after k_pointnet, their keys decoded to floats)
+//   k_pointnet       the three blocks as fp32 MFMA products over the
+//                    wavefront's 64 entries (weight fragments held in
+//                    registers); block 3's outputs go to LDS channel-major;
+//                    then lane c walks the wavefront's entries keeping the
+//                    running max of channel c and stores it at the end of
+//                    each run: a plain store (64 lanes, one row) when the run
+//                    is the vertex's whole list, else an unsigned atomic max of an
+//                    order-preserving key (no returned value to wait for).
+//                    The max is exact in any order, so the result does not
+//                    depend on scheduling.
 #include "internal.h"
 
 namespace {
@@ -39,27 +42,28 @@ constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
 constexpr int kW1 = 16, kW2 = 32, kW3 = 64;  // block widths (the paper's figure)
 constexpr int kMaxK0 = 16;                   // d + f_d, zero-padded to 16
-constexpr int kHalf = kW3 / 2;               // block 3's outputs are staged 32 channels at a time
 constexpr int kYStride = 64 + 1;             // LDS row of one channel: 64 entries + 1 (bank offset)
-
-// LDS copy of the parameters, zero-padded to kMaxK0 inputs in block 1.
-struct PnLds {
-    float a0[kMaxK0], s0[kMaxK0], w0[kW1][kMaxK0], b0[kW1];
-    float a1[kW1], s1[kW1], w1[kW2][kW1], b1[kW2];
-    float a2[kW2], s2[kW2], w2[kW3][kW2], b2[kW3];
-};
 
 __device__ __forceinline__ float relu(float x) { return x > 0.f ? x : 0.f; }
 
-// Atomic max of a float in global memory (compare and swap on the bits).
-__device__ __forceinline__ void atomic_max_f32(float *addr, float val) {
-    unsigned int *a = reinterpret_cast<unsigned int *>(addr);
-    unsigned int old = __atomic_load_n(a, __ATOMIC_RELAXED);
-    while (val > __uint_as_float(old)) {
-        const unsigned int prev = atomicCAS(a, old, __float_as_uint(val));
-        if (prev == old) break;
-        old = prev;
-    }
+// Order-preserving map of a float to an unsigned integer (a > b exactly
+// when key(a) > key(b), for non-NaN values), so that an unsigned atomic max,
+// which needs no returned value, is a float max.  Rows that take atomic
+// maxima hold keys until k_pointnet_finish decodes them.
+__device__ __forceinline__ unsigned int max_key(float f) {
+    const unsigned int u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(unsigned int k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// Segment start of each lane: the highest lane at or below it whose entry
+// starts a run of equal vertex (head).
+__device__ __forceinline__ int run_start(bool head, int lane) {
+    const unsigned long long hb = __ballot(head);
+    const unsigned long long below = lane == 63 ? hb : (hb & ((2ull << lane) - 1ull));
+    return 63 - __clzll(below);
 }
 
 __global__ __launch_bounds__(kBlock) void k_entry_vertex(const int32_t *__restrict__ vinfo,
@@ -89,42 +93,48 @@ __global__ __launch_bounds__(kBlock) void k_entry_vertex(const int32_t *__restri
 // Whether entries [off, off + cnt) lie in one 64-entry chunk.
 __device__ __forceinline__ bool in_one_chunk(int off, int cnt) { return (off >> 6) == ((off + cnt - 1) >> 6); }
 
+// One lane per entry; the positions of each run of equal vertex within the
+// wavefront's 64 entries are summed by a segmented scan in fp64 (shuffles),
+// and the run's last lane writes mu_v or adds the run to the vertex's sum.
+template <int D>
 __global__ __launch_bounds__(kBlock) void k_local_mean(const int32_t *__restrict__ list,
                                                        const int32_t *__restrict__ lvert,
                                                        const int32_t *__restrict__ vinfo,
-                                                       const float *__restrict__ pos, int d,
+                                                       const float *__restrict__ pos,
                                                        const int32_t *__restrict__ counters,
                                                        double *__restrict__ macc, float *__restrict__ mu) {
-    __shared__ double gsh[kWaves][64][LATTICE_MAX_D];
-    __shared__ int32_t vsh[kWaves][64];
     const int64_t E = counters[CNT_E];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < E; base += (int64_t)gridDim.x * kBlock) {
-        const int64_t e = base + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int64_t nwaves = (int64_t)gridDim.x * kWaves;
+    for (int64_t c = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6; c * 64 < E; c += nwaves) {
+        const int64_t chunk0 = c * 64;
+        const int64_t e = chunk0 + lane;
         const bool valid = e < E;
         const int v = valid ? lvert[e] : -1;
         const int p = valid ? list[2 * e] : 0;
-        vsh[w][lane] = v;
-        for (int i = 0; i < d; ++i) gsh[w][lane][i] = valid ? (double)pos[(int64_t)p * d + i] : 0.0;
-        __syncthreads();
-        if (lane < d) {
-            const int i = lane;
-            const int64_t chunk0 = base + w * 64;
-            double acc = 0.0;
-            for (int j = 0; j < 64; ++j) {
-                const int vj = vsh[w][j];
-                if (vj < 0) break;
-                acc = (j == 0 || vsh[w][j - 1] != vj) ? gsh[w][j][i] : acc + gsh[w][j][i];
-                if (j == 63 || vsh[w][j + 1] != vj) {
-                    const int off = vinfo[2 * vj], cnt = vinfo[2 * vj + 1];
-                    if (off >= chunk0 && off + cnt <= chunk0 + 64)
-                        mu[(int64_t)vj * d + i] = (float)(acc / cnt);
-                    else
-                        atomicAdd(&macc[(int64_t)vj * d + i], acc);
-                }
+        double acc[D];
+#pragma unroll
+        for (int i = 0; i < D; ++i) acc[i] = valid ? (double)pos[(int64_t)p * D + i] : 0.0;
+        const int vprev = __shfl_up(v, 1), vnext = __shfl_down(v, 1);
+        const int start = run_start(lane == 0 || vprev != v, lane);
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+#pragma unroll
+            for (int i = 0; i < D; ++i) {
+                const double t = __shfl_up(acc[i], off);
+                if (lane - off >= start) acc[i] += t;
             }
         }
-        __syncthreads();
+        if (valid && (lane == 63 || vnext != v)) {
+            const int off = vinfo[2 * v], cnt = vinfo[2 * v + 1];
+            if (off >= chunk0 && off + cnt <= chunk0 + 64) {
+#pragma unroll
+                for (int i = 0; i < D; ++i) mu[(int64_t)v * D + i] = (float)(acc[i] / cnt);
+            } else {
+#pragma unroll
+                for (int i = 0; i < D; ++i) atomicAdd(&macc[(int64_t)v * D + i], acc[i]);
+            }
+        }
     }
 }
 
@@ -140,11 +150,13 @@ __global__ __launch_bounds__(kBlock) void k_mean_finish(const int32_t *__restric
     }
 }
 
-// -inf in the rows of the vertices whose list crosses a chunk boundary: the
-// vertex of entry 64k (k >= 1) when its list starts before it.
-__global__ __launch_bounds__(kBlock) void k_pointnet_init(const int32_t *__restrict__ lvert,
+// The key of -inf in the rows of the vertices whose list crosses a chunk
+// boundary (mode 0), or those rows' keys decoded back to floats (mode 1):
+// the vertex of entry 64k (k >= 1) when its list starts before it.  A long
+// list crosses several boundaries; only its first crossing does the work.
+__global__ __launch_bounds__(kBlock) void k_pointnet_rows(const int32_t *__restrict__ lvert,
                                                           const int32_t *__restrict__ vinfo,
-                                                          const int32_t *__restrict__ counters,
+                                                          const int32_t *__restrict__ counters, int mode,
                                                           float *__restrict__ out) {
     const int64_t E = counters[CNT_E];
     const int64_t nb = E > 0 ? (E - 1) / 64 : 0;  // boundaries 64, 128, ... below E
@@ -153,49 +165,117 @@ __global__ __launch_bounds__(kBlock) void k_pointnet_init(const int32_t *__restr
         const int64_t e0 = (q / kW3 + 1) * 64;
         const int c = (int)(q % kW3);
         const int v = lvert[e0];
-        if (vinfo[2 * v] < e0) out[(int64_t)v * kW3 + c] = -__builtin_huge_valf();
+        const int64_t off = vinfo[2 * v];
+        if (off >= e0 || off < e0 - 64) continue;  // not crossing here, or crossed an earlier boundary
+        unsigned int *row = reinterpret_cast<unsigned int *>(out) + (int64_t)v * kW3;
+        if (mode == 0)
+            row[c] = max_key(-__builtin_huge_valf());
+        else
+            out[(int64_t)v * kW3 + c] = key_value(row[c]);
     }
 }
 
+// The parameters in a fixed layout: block 1 zero-padded to kMaxK0 inputs
+// (a = s = W = 0 on the padding, so padded inputs contribute nothing), then
+// blocks 2 and 3 as packed.  Every offset is a compile-time constant.
+constexpr int kA0 = 0, kS0 = kA0 + kMaxK0, kWt0 = kS0 + kMaxK0, kB0 = kWt0 + kW1 * kMaxK0;
+constexpr int kA1 = kB0 + kW1, kS1 = kA1 + kW1, kWt1 = kS1 + kW1, kB1 = kWt1 + kW2 * kW1;
+constexpr int kA2 = kB1 + kW2, kS2 = kA2 + kW2, kWt2 = kS2 + kW2, kB2 = kWt2 + kW3 * kW2;
+constexpr int kPadded = kB2 + kW3;
+
+__global__ __launch_bounds__(kBlock) void k_pack_pointnet(const float *__restrict__ params, int k0,
+                                                          float *__restrict__ padded) {
+    for (int i = threadIdx.x; i < kPadded; i += kBlock) {
+        float x = 0.f;
+        if (i < kS0) {
+            if (i - kA0 < k0) x = params[i - kA0];
+        } else if (i < kWt0) {
+            if (i - kS0 < k0) x = params[k0 + (i - kS0)];
+        } else if (i < kB0) {
+            const int c = (i - kWt0) / kMaxK0, k = (i - kWt0) % kMaxK0;
+            if (k < k0) x = params[2 * k0 + c * k0 + k];
+        } else {
+            x = params[2 * k0 + kW1 * k0 + (i - kB0)];  // b0 and blocks 2, 3 as packed
+        }
+        padded[i] = x;
+    }
+}
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// v_mfma_f32_16x16x4f32: D[16 x 16] += A[16 x 4] B[4 x 16]; lane l supplies
+// A[l % 16][l / 16] and B[l / 16][l % 16]; register r of lane l holds
+// D[4 (l / 16) + r][l % 16].
+__device__ __forceinline__ f32x4_t mfma16(float a, float b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The three blocks on fp32 MFMA, with the entries as the columns:
+// D_l [w_l x 16 entries] = W_l [w_l x K] R_{l-1}^T [K x 16 entries], one
+// 16-entry column tile at a time (four per wavefront of 64 entries).
+// Register r of lane l then holds output channel 4 (l / 16) + r (+16 per row
+// tile) of entry l % 16, which is exactly the B operand the next block
+// needs if its K index at step t, lane quarter q, is that channel: each
+// lane's weight fragments are loaded once with that permutation, so no
+// activation moves between blocks.  Block 1's input comes from LDS (each
+// lane stages its own row).  The outputs go to LDS channel-major for the
+// per-run max.  Each wavefront loops over its own chunks (wavefront-level
+// synchronisation only).
 __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__ list,
                                                      const int32_t *__restrict__ lvert,
                                                      const int32_t *__restrict__ vinfo,
                                                      const float *__restrict__ pos, const float *__restrict__ feat,
-                                                     int d, int f_d, const float *__restrict__ params,
+                                                     int d, int f_d, const float *__restrict__ P,
                                                      const float *__restrict__ mu,
                                                      const int32_t *__restrict__ counters, float *__restrict__ out) {
-    __shared__ PnLds P;
-    __shared__ float ysh[kWaves][kHalf * kYStride];
+    __shared__ float ysh[kWaves][kW3 * kYStride];  // outputs [64 channels][64 entries]; first the staged inputs
     __shared__ int32_t vsh[kWaves][64];
     __shared__ int32_t fsh[kWaves][64];
 
-    // parameters -> LDS, block 1 zero-padded to kMaxK0 inputs
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int q = lane >> 4, j16 = lane & 15;
+    float *Y = ysh[w];
     const int k0 = d + f_d;
-    {
-        float *flat = reinterpret_cast<float *>(&P);
-        for (int i = threadIdx.x; i < (int)(sizeof(PnLds) / sizeof(float)); i += kBlock) flat[i] = 0.f;
-        __syncthreads();
-        int at = 0;
-        for (int i = threadIdx.x; i < k0; i += kBlock) {
-            P.a0[i] = params[at + i];
-            P.s0[i] = params[at + k0 + i];
+
+    // weight fragments (A operands) and per-channel affines of this lane
+    float wa1[4], na1[4], ns1[4];
+    float wa2[2][4], na2[2][4], ns2[2][4];
+    float wa3[4][8], bb3[4][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        wa1[t] = P[kWt0 + j16 * kMaxK0 + 4 * t + q];  // block 1: K = 4 t + q (the staged input order)
+        const int c = 4 * q + t;                       // block 1 output channel in register t
+        na1[t] = P[kA1 + c];
+        ns1[t] = fmaf(P[kA1 + c], P[kB0 + c], P[kS1 + c]);  // a (h + b) + s = a h + (a b + s)
+    }
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            wa2[mt][t] = P[kWt1 + (16 * mt + j16) * kW1 + 4 * q + t];  // block 2: K = 4 q + t
+            const int c = 16 * mt + 4 * q + t;
+            na2[mt][t] = P[kA2 + c];
+            ns2[mt][t] = fmaf(P[kA2 + c], P[kB1 + c], P[kS2 + c]);
         }
-        at += 2 * k0;
-        for (int i = threadIdx.x; i < kW1 * k0; i += kBlock) P.w0[i / k0][i % k0] = params[at + i];
-        at += kW1 * k0;
-        for (int i = threadIdx.x; i < kW1; i += kBlock) P.b0[i] = params[at + i];
-        at += kW1;
-        float *rest = &P.a1[0];  // blocks 2 and 3 are stored unpadded, in the packed order
-        const int nrest = 2 * kW1 + kW2 * kW1 + kW2 + 2 * kW2 + kW3 * kW2 + kW3;
-        for (int i = threadIdx.x; i < nrest; i += kBlock) rest[i] = params[at + i];
-        __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t)  // block 3: K = 16 (t / 4) + 4 q + t % 4
+            wa3[mt][t] = P[kWt2 + (16 * mt + j16) * kW2 + 16 * (t / 4) + 4 * q + (t % 4)];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bb3[mt][r] = P[kB2 + 16 * mt + 4 * q + r];
     }
 
     const int64_t E = counters[CNT_E];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    float *Y = ysh[w];
-    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < E; base += (int64_t)gridDim.x * kBlock) {
-        const int64_t chunk0 = base + w * 64;
+    const int64_t nwaves = (int64_t)gridDim.x * kWaves;
+    for (int64_t ch = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6; ch * 64 < E; ch += nwaves) {
+        const int64_t chunk0 = ch * 64;
         const int64_t e = chunk0 + lane;
         const bool valid = e < E;
         const int v = valid ? lvert[e] : -1;
@@ -213,72 +293,71 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         vsh[w][lane] = v;
         fsh[w][lane] = flags;
 
-        // h_0 = [g_p - mu_v ; f_p], zero-padded
-        float h0[kMaxK0];
+        // r_0 = relu(a_0 h_0 + s_0), h_0 = [g_p - mu_v ; f_p] zero-padded, staged in LDS
 #pragma unroll
-        for (int i = 0; i < kMaxK0; ++i) h0[i] = 0.f;
-        if (valid) {
-            for (int i = 0; i < d; ++i) h0[i] = pos[(int64_t)p * d + i] - mu[(int64_t)v * d + i];
-            for (int i = 0; i < f_d; ++i) h0[d + i] = feat[(int64_t)p * f_d + i];
+        for (int i = 0; i < kMaxK0; ++i) {
+            float x = 0.f;
+            if (valid && i < d) x = pos[(int64_t)p * d + i] - mu[(int64_t)v * d + i];
+            else if (valid && i < k0) x = feat[(int64_t)p * f_d + (i - d)];
+            Y[lane * (kMaxK0 + 1) + i] = relu(fmaf(P[kA0 + i], x, P[kS0 + i]));
         }
-        // block 1
-        float r[kW2];
+        wave_sync();
+        float b1[4][4];  // B operands of block 1: entry 16 nt + j16, K = 4 t + q
 #pragma unroll
-        for (int k = 0; k < kMaxK0; ++k) r[k] = relu(fmaf(P.a0[k], h0[k], P.s0[k]));
-        float h1[kW1];
+        for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-        for (int c = 0; c < kW1; ++c) {
-            float acc = P.b0[c];
+            for (int t = 0; t < 4; ++t) b1[nt][t] = Y[(16 * nt + j16) * (kMaxK0 + 1) + 4 * t + q];
+        wave_sync();
+
 #pragma unroll
-            for (int k = 0; k < kMaxK0; ++k) acc = fmaf(P.w0[c][k], r[k], acc);
-            h1[c] = acc;
-        }
-        // block 2
+        for (int nt = 0; nt < 4; ++nt) {
+            f32x4_t d1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int k = 0; k < kW1; ++k) r[k] = relu(fmaf(P.a1[k], h1[k], P.s1[k]));
-        float h2[kW2];
+            for (int t = 0; t < 4; ++t) d1 = mfma16(wa1[t], b1[nt][t], d1);
+            float r1[4];
 #pragma unroll
-        for (int c = 0; c < kW2; ++c) {
-            float acc = P.b1[c];
+            for (int t = 0; t < 4; ++t) r1[t] = relu(fmaf(na1[t], d1[t], ns1[t]));
+            f32x4_t d2[2];
 #pragma unroll
-            for (int k = 0; k < kW1; ++k) acc = fmaf(P.w1[c][k], r[k], acc);
-            h2[c] = acc;
-        }
-        // block 3, 32 output channels at a time into LDS (channel-major),
-        // then lane c < 32 keeps the running max of channel h*32 + c over
-        // each run of the wavefront's entries
+            for (int mt = 0; mt < 2; ++mt) {
+                d2[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int k = 0; k < kW2; ++k) r[k] = relu(fmaf(P.a2[k], h2[k], P.s2[k]));
-        for (int h = 0; h < kW3 / kHalf; ++h) {
-#pragma unroll 4
-            for (int c = 0; c < kHalf; ++c) {
-                const int co = h * kHalf + c;
-                float acc = P.b2[co];
-#pragma unroll
-                for (int k = 0; k < kW2; ++k) acc = fmaf(P.w2[co][k], r[k], acc);
-                Y[c * kYStride + lane] = acc;
+                for (int t = 0; t < 4; ++t) d2[mt] = mfma16(wa2[mt][t], r1[t], d2[mt]);
             }
-            __syncthreads();
-            if (lane < kHalf) {
-                const int c = lane;
-                float mx = 0.f;
+            float r2[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) r2[t] = relu(fmaf(na2[t / 4][t % 4], d2[t / 4][t % 4], ns2[t / 4][t % 4]));
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                f32x4_t d3 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int t = 0; t < 8; ++t) d3 = mfma16(wa3[mt][t], r2[t], d3);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) Y[(16 * mt + 4 * q + r) * kYStride + 16 * nt + j16] = d3[r] + bb3[mt][r];
+            }
+        }
+        wave_sync();
+
+        // lane c: running max of channel c over each run of the wavefront's entries
+        {
+            const int c = lane;
+            float mx = 0.f;
 #pragma unroll 8
-                for (int j = 0; j < 64; ++j) {
-                    const int vj = vsh[w][j];
-                    const int fj = fsh[w][j];
-                    const float y = Y[c * kYStride + j];
-                    mx = (fj & 1) ? y : fmaxf(mx, y);
-                    if (vj >= 0 && (fj & 2)) {
-                        float *dst = out + (int64_t)vj * kW3 + h * kHalf + c;
-                        if (fj & 4)
-                            *dst = mx;
-                        else
-                            atomic_max_f32(dst, mx);
-                    }
+            for (int jj = 0; jj < 64; ++jj) {
+                const int vj = vsh[w][jj];
+                const int fj = fsh[w][jj];
+                const float y = Y[c * kYStride + jj];
+                mx = (fj & 1) ? y : fmaxf(mx, y);
+                if (vj >= 0 && (fj & 2)) {
+                    float *dst = out + (int64_t)vj * kW3 + c;
+                    if (fj & 4)
+                        *dst = mx;
+                    else
+                        atomicMax(reinterpret_cast<unsigned int *>(dst), max_key(mx));
                 }
             }
-            __syncthreads();
         }
+        wave_sync();
     }
 }
 
@@ -286,6 +365,8 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 
 // Packed parameter count for d + f_d = k0 inputs: per block a [K], s [K],
 // W [w][K], b [w] with K the block's input width.
+int pointnet_padded_count() { return kPadded; }
+
 int pointnet_param_count(int k0) {
     return 2 * k0 + kW1 * k0 + kW1 + 2 * kW1 + kW2 * kW1 + kW2 + 2 * kW2 + kW3 * kW2 + kW3;
 }
@@ -302,16 +383,34 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned g_e = grid_for(E, kBlock, L->cu_count, 8);
-    hipLaunchKernelGGL(k_local_mean, dim3(g_e), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo, pos, d,
-                       L->counters, L->macc, mu);
+    switch (d) {
+#define LM_CASE(DD)                                                                                              \
+    case DD:                                                                                                     \
+        hipLaunchKernelGGL(k_local_mean<DD>, dim3(g_e), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo, \
+                           pos, L->counters, L->macc, mu);                                                       \
+        break;
+        LM_CASE(1)
+        LM_CASE(2)
+        LM_CASE(3)
+        LM_CASE(4)
+#undef LM_CASE
+        default:
+            return hipErrorInvalidValue;
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_mean_finish, dim3(g_v), dim3(kBlock), 0, L->stream, L->vinfo, L->macc, d, L->counters, mu);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned g_i = grid_for((E / 64 + 1) * kW3, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(k_pointnet_init, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, out);
+    hipLaunchKernelGGL(k_pointnet_rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 0,
+                       out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const unsigned g_p = grid_for(E, kBlock, L->cu_count, 3);  // 45 KB of LDS: three workgroups per CU
+    hipLaunchKernelGGL(k_pack_pointnet, dim3(1), dim3(kBlock), 0, L->stream, params, d + f_d, L->pn_params);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const unsigned g_p = grid_for(E, kBlock, L->cu_count, 2);  // 69 KB of LDS: two workgroups per CU
     hipLaunchKernelGGL(k_pointnet, dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo, pos, feat, d,
-                       f_d, params, mu, L->counters, out);
+                       f_d, L->pn_params, mu, L->counters, out);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_pointnet_rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 1,
+                       out);
     return hipGetLastError();
 }

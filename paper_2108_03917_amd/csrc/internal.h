@@ -76,6 +76,7 @@ struct lattice {
     int32_t *lvert = nullptr;   // [(d+1) max_points] vertex of each pair-list entry
     double *macc = nullptr;     // [max_vertices][d] position sums of lists that cross a 64-entry chunk
     float *mu = nullptr;        // [max_vertices][d] local means when the caller does not take them
+    float *pn_params = nullptr; // the PointNet parameters in the kernel's padded layout
     int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
     int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
@@ -138,6 +139,7 @@ hipError_t launch_flip_weights(lattice *L, const void *w, bool bf16, int C_out, 
 hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
                                       float *out, float *mean);
 int pointnet_param_count(int k0);
+int pointnet_padded_count();
 
 // deform.hip
 int deform_max_channels(const void *values, lattice_dtype values_dt, int C, const float *w_delta, const float *w_cls,

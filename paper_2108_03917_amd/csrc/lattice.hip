@@ -54,6 +54,7 @@ void free_all(lattice *L) {
     (void)hipFree(L->lvert);
     (void)hipFree(L->macc);
     (void)hipFree(L->mu);
+    (void)hipFree(L->pn_params);
     (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
     (void)hipFree(L->rank);
@@ -607,15 +608,18 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
     if (!L->lvert) {
         bool ok = hipMalloc(&L->lvert, E_max * sizeof(int32_t)) == hipSuccess &&
                   hipMalloc(&L->macc, L->max_vertices * L->d * sizeof(double)) == hipSuccess &&
-                  hipMalloc(&L->mu, L->max_vertices * L->d * sizeof(float)) == hipSuccess;
+                  hipMalloc(&L->mu, L->max_vertices * L->d * sizeof(float)) == hipSuccess &&
+                  hipMalloc(&L->pn_params, pointnet_padded_count() * sizeof(float)) == hipSuccess;
         if (!ok) {
             (void)hipGetLastError();
             (void)hipFree(L->lvert);
             (void)hipFree(L->macc);
             (void)hipFree(L->mu);
+            (void)hipFree(L->pn_params);
             L->lvert = nullptr;
             L->macc = nullptr;
             L->mu = nullptr;
+            L->pn_params = nullptr;
             set_err(L, "distribute_pointnet: cannot allocate its scratch");
             return LATTICE_E_NOMEM;
         }
