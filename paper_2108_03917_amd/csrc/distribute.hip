@@ -185,7 +185,7 @@ constexpr int kPadded = kB2 + kW3;
 
 __global__ __launch_bounds__(kBlock) void k_pack_pointnet(const float *__restrict__ params, int k0,
                                                           float *__restrict__ padded) {
-    for (int i = threadIdx.x; i < kPadded; i += kBlock) {
+    for (int i = blockIdx.x * kBlock + threadIdx.x; i < kPadded; i += gridDim.x * kBlock) {
         float x = 0.f;
         if (i < kS0) {
             if (i - kA0 < k0) x = params[i - kA0];
@@ -404,7 +404,8 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
     hipLaunchKernelGGL(k_pointnet_rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 0,
                        out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_pack_pointnet, dim3(1), dim3(kBlock), 0, L->stream, params, d + f_d, L->pn_params);
+    hipLaunchKernelGGL(k_pack_pointnet, dim3((kPadded + kBlock - 1) / kBlock), dim3(kBlock), 0, L->stream, params,
+                       d + f_d, L->pn_params);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned g_p = grid_for(E, kBlock, L->cu_count, 2);  // 69 KB of LDS: two workgroups per CU
     hipLaunchKernelGGL(k_pointnet, dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo, pos, feat, d,
