@@ -138,8 +138,9 @@ int64_t lattice_max_vertices(const lattice *L, int64_t m);
  *                the same rounding the conv would apply to fp32 rows).
  *   weight       dev [>= lattice_max_vertices(L, m)] fp32 output w_v, or NULL.
  * Resets the lattice: the previous vertex set, records and neighbour table
- * are discarded.  Vertex order is hash-slot order.  Device-side failures are
- * reported by lattice_num_vertices.
+ * are discarded.  Vertex order follows, in point order, the pair whose
+ * insertion created each vertex (the winner of a concurrent claim): it is not
+ * deterministic.  Device-side failures are reported by lattice_num_vertices.
  */
 lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch, int64_t m,
                              const float *feat, int C, int normalize, void *values,
