@@ -318,10 +318,10 @@ def algorithmic_work(w, V, n_cls=0, Vc=0, f_raw=-1):
                 "bytes": V * (sg(i) * cv.c_out + 4 * T + sg(i - 1) * cv.c_in) + T * cv.c_in * cv.c_out * s_x,
                 "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": cv.dtype}
             # weight gradient: read g, x and the neighbour row per vertex, write
-            # the fp32 weights; fp32 MFMA whatever the conv's dtype
+            # the fp32 weights; on the MFMA of the conv's dtype
             work[name + "_bwd_w"] = {
                 "bytes": V * (sg(i) * cv.c_out + s_x * cv.c_in + 4 * T) + T * cv.c_in * cv.c_out * 4,
-                "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": "f32"}
+                "flops": 2 * V * T * cv.c_in * cv.c_out, "dtype": cv.dtype}
         # splat backward: the slice of the vertex gradient onto the points
         work["splat_bwd"] = {"bytes": m * (8 * (d + 1) + 4 * C) + V * sg(-1) * C}
     if f_raw >= 0:

@@ -207,6 +207,163 @@ __global__ __launch_bounds__(kBlock) void k_conv_wgrad(const void *__restrict__ 
     }
 }
 
+// The bf16 computation on bf16 MFMA (v_mfma_f32_32x32x16_bf16): lane l
+// supplies A[l % 32][8 (l / 32) + 0..7] and B[8 (l / 32) + 0..7][l % 32],
+// eight consecutive K = vertex values per lane.  So the step's rows are
+// staged transposed in LDS, channel-major with the 32 vertices of the step
+// contiguous (row stride kTRow bytes): each thread loads two consecutive
+// rows of four channels, packs the two bf16 values of each channel into one
+// word and stores it at [channel][vertex pair].  Products of bf16 values are
+// exact in fp32 and the sums are fp32, as in the fp32-MFMA kernel.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kTStep = 32;   // vertices per step (two MFMA K-steps of 16)
+constexpr int kTRow = 80;    // LDS bytes per channel row: 32 bf16 + 16 bytes of padding
+
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Four consecutive channels [c, c+4) of row `row` as bf16 bits (rounded to
+// nearest even from fp32 storage), zero past C; C % 4 == 0 and aligned rows.
+template <bool BF16>
+__device__ __forceinline__ uint2 load4_bf16(const void *base, int64_t row, int C, int c) {
+    if (c >= C) return make_uint2(0u, 0u);
+    if (BF16) return *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(base) + row * C + c);
+    const float4 f = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(base) + row * C + c);
+    return make_uint2(bf16_rne(f.x) | (bf16_rne(f.y) << 16), bf16_rne(f.z) | (bf16_rne(f.w) << 16));
+}
+
+template <bool G_BF16, bool X_BF16>
+__global__ __launch_bounds__(kBlock) void k_conv_wgrad_bf16(const void *__restrict__ g, int C_out,
+                                                            const void *__restrict__ x, int C_in, int T,
+                                                            const int32_t *__restrict__ nbr,
+                                                            const int32_t *__restrict__ counters, int nch,
+                                                            float *__restrict__ partial, float *__restrict__ pbias) {
+    __shared__ __attribute__((aligned(16))) char gs[kTile * kTRow];
+    __shared__ __attribute__((aligned(16))) char xs[kTile * kTRow];
+    __shared__ float bred[kBlock / 16][kTile];
+
+    const int64_t V = counters[CNT_V];
+    const int chunk = blockIdx.x;
+    const int t = blockIdx.y;
+    const int tiles_i = (C_in + kTile - 1) / kTile;
+    const int o0 = (blockIdx.z / tiles_i) * kTile;
+    const int i0 = (blockIdx.z % tiles_i) * kTile;
+    const int64_t lo = V * chunk / nch;
+    const int64_t hi = V * (chunk + 1) / nch;
+    const bool do_bias = pbias != nullptr && t == 0 && i0 == 0;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int h = lane >> 5;
+    const int ow = (wave >> 1) * 32;
+    const int iw = (wave & 1) * 32;
+    // Loader mapping: channel chunk c4 (4 channels), rows 2 rp and 2 rp + 1 of the step.
+    const int c4 = (tid & 15) * 4;
+    const int rp = tid >> 4;
+
+    f32x16_t acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    float bsum[4] = {0.f, 0.f, 0.f, 0.f};
+
+    uint2 ga[2], xa[2];
+    int32_t ua[2];
+    auto load_index = [&](int64_t k0) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t v = k0 + 2 * rp + j;
+            ua[j] = v < hi ? nbr[v * T + t] : -1;
+        }
+    };
+    auto load_step = [&](int64_t k0) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t v = k0 + 2 * rp + j;
+            ga[j] = v < hi ? load4_bf16<G_BF16>(g, v, C_out, o0 + c4) : make_uint2(0u, 0u);
+            xa[j] = ua[j] >= 0 ? load4_bf16<X_BF16>(x, ua[j], C_in, i0 + c4) : make_uint2(0u, 0u);
+        }
+    };
+    // the bias sums the output gradient as stored (fp32 rows unrounded)
+    auto add_bias = [&](int64_t k0) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t v = k0 + 2 * rp + j;
+            if (v >= hi || o0 + c4 >= C_out) continue;
+            if (G_BF16) {
+                const uint2 u = ga[j];
+                bsum[0] += __uint_as_float(u.x << 16);
+                bsum[1] += __uint_as_float(u.x & 0xffff0000u);
+                bsum[2] += __uint_as_float(u.y << 16);
+                bsum[3] += __uint_as_float(u.y & 0xffff0000u);
+            } else {
+                const float4 f =
+                    *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(g) + v * C_out + o0 + c4);
+                bsum[0] += f.x;
+                bsum[1] += f.y;
+                bsum[2] += f.z;
+                bsum[3] += f.w;
+            }
+        }
+    };
+    if (lo < hi) {
+        load_index(lo);
+        load_step(lo);
+        load_index(lo + kTStep);
+    }
+    for (int64_t k0 = lo; k0 < hi; k0 += kTStep) {
+        if (do_bias) add_bias(k0);
+        // registers -> LDS: word e of a thread = channel c4 + e of rows 2 rp, 2 rp + 1
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int sh = (e & 1) * 16;
+            const uint32_t gw = ((((e < 2) ? ga[0].x : ga[0].y) >> sh) & 0xffffu) |
+                                ((((e < 2) ? ga[1].x : ga[1].y) >> sh) << 16);
+            const uint32_t xw = ((((e < 2) ? xa[0].x : xa[0].y) >> sh) & 0xffffu) |
+                                ((((e < 2) ? xa[1].x : xa[1].y) >> sh) << 16);
+            *reinterpret_cast<uint32_t *>(gs + (c4 + e) * kTRow + 4 * rp) = gw;
+            *reinterpret_cast<uint32_t *>(xs + (c4 + e) * kTRow + 4 * rp) = xw;
+        }
+        __syncthreads();
+        if (k0 + kTStep < hi) {
+            load_step(k0 + kTStep);
+            load_index(k0 + 2 * kTStep);
+        }
+#pragma unroll
+        for (int s = 0; s < kTStep / 16; ++s) {
+            const u32x4_t a = *reinterpret_cast<const u32x4_t *>(gs + (ow + (lane & 31)) * kTRow + 32 * s + 16 * h);
+            const u32x4_t b = *reinterpret_cast<const u32x4_t *>(xs + (iw + (lane & 31)) * kTRow + 32 * s + 16 * h);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                          __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+        }
+        __syncthreads();
+    }
+
+    float *dst = partial + (int64_t)chunk * C_out * T * C_in;
+    const int ic = i0 + iw + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int oc = o0 + ow + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (oc < C_out && ic < C_in) dst[((int64_t)oc * T + t) * C_in + ic] = acc[r];
+    }
+    if (do_bias) {
+        // threads tid and tid + 16 k (k = 0..15) share channel chunk c4
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bred[rp][c4 + e] = bsum[e];
+        __syncthreads();
+        if (tid < kTile) {
+            float sacc = 0.f;
+            for (int q = 0; q < kBlock / 16; ++q) sacc += bred[q][tid];
+            if (o0 + tid < C_out) pbias[(int64_t)chunk * C_out + o0 + tid] = sacc;
+        }
+    }
+}
+
 // out[j] = sum over the nch chunk partials part[c][j], in a fixed order:
 // a workgroup owns 64 consecutive outputs; its four wavefronts sum the
 // chunks c = g, g+4, g+8, ... (g = wavefront) with four loads in flight, and
@@ -280,6 +437,21 @@ hipError_t launch_conv_wgrad(lattice *L, const void *g, lattice_dtype g_dt, int 
                      (reinterpret_cast<uintptr_t>(x) & (xb ? 7 : 15)) == 0;
     const dim3 grid((unsigned)nch, (unsigned)L->T,
                     (unsigned)(((C_out + kTile - 1) / kTile) * ((C_in + kTile - 1) / kTile)));
+    if (rnd && vec) {
+        // bf16 computation on bf16 MFMA
+        if (gb && xb)
+            hipLaunchKernelGGL((k_conv_wgrad_bf16<true, true>), grid, dim3(kBlock), 0, L->stream, g, C_out, x, C_in,
+                               L->T, L->nbr, L->counters, nch, partial, grad_bias ? pbias : nullptr);
+        else if (gb)
+            hipLaunchKernelGGL((k_conv_wgrad_bf16<true, false>), grid, dim3(kBlock), 0, L->stream, g, C_out, x, C_in,
+                               L->T, L->nbr, L->counters, nch, partial, grad_bias ? pbias : nullptr);
+        else if (xb)
+            hipLaunchKernelGGL((k_conv_wgrad_bf16<false, true>), grid, dim3(kBlock), 0, L->stream, g, C_out, x, C_in,
+                               L->T, L->nbr, L->counters, nch, partial, grad_bias ? pbias : nullptr);
+        else
+            hipLaunchKernelGGL((k_conv_wgrad_bf16<false, false>), grid, dim3(kBlock), 0, L->stream, g, C_out, x,
+                               C_in, L->T, L->nbr, L->counters, nch, partial, grad_bias ? pbias : nullptr);
+    } else {
 #define WG(GB, XB, RN, VC)                                                                                      \
     hipLaunchKernelGGL((k_conv_wgrad<GB, XB, RN, VC>), grid, dim3(kBlock), 0, L->stream, g, C_out, x, C_in, L->T, \
                        L->nbr, L->counters, nch, partial, grad_bias ? pbias : nullptr)
@@ -299,6 +471,7 @@ hipError_t launch_conv_wgrad(lattice *L, const void *g, lattice_dtype g_dt, int 
     }
 #undef WG_V
 #undef WG
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (grad_w) {
