@@ -274,12 +274,57 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 
     const int64_t E = counters[CNT_E];
     const int64_t nwaves = (int64_t)gridDim.x * kWaves;
-    for (int64_t ch = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6; ch * 64 < E; ch += nwaves) {
-        const int64_t chunk0 = ch * 64;
-        const int64_t e = chunk0 + lane;
+    // Software pipeline over this wavefront's chunks: the entry's vertex and
+    // point (level 1) are loaded two chunks ahead, the vertex's list header,
+    // the point's position and features and the vertex's mean (level 2, which
+    // need level 1) one chunk ahead, so that a chunk's MFMAs never wait on
+    // its own gathers.
+    struct Rows {
+        int v, p;             // level 1
+        int off, cnt;         // level 2
+        float x[kMaxK0];      // h_0 (level 2)
+    };
+    auto level1 = [&](int64_t chk, Rows &R) {
+        const int64_t e = chk * 64 + lane;
         const bool valid = e < E;
-        const int v = valid ? lvert[e] : -1;
-        const int p = valid ? list[2 * e] : 0;
+        R.v = valid ? lvert[e] : -1;
+        R.p = valid ? list[2 * e] : 0;
+    };
+    auto level2 = [&](Rows &R) {
+        const bool valid = R.v >= 0;
+        R.off = valid ? vinfo[2 * R.v] : 0;
+        R.cnt = valid ? vinfo[2 * R.v + 1] : 0;
+#pragma unroll
+        for (int i = 0; i < kMaxK0; ++i) {
+            float x = 0.f;
+            if (valid && i < d) x = pos[(int64_t)R.p * d + i] - mu[(int64_t)R.v * d + i];
+            else if (valid && i < k0) x = feat[(int64_t)R.p * f_d + (i - d)];
+            R.x[i] = x;
+        }
+    };
+    int64_t ch = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    Rows cur, nxt;
+    int v2 = -1, p2 = 0;
+    if (ch * 64 < E) {
+        level1(ch, cur);
+        level2(cur);
+        level1(ch + nwaves, nxt);
+    }
+    for (; ch * 64 < E; ch += nwaves) {
+        // issue the next chunk's level 2 and the one after's level 1
+        {
+            Rows tmp;
+            tmp.v = nxt.v;
+            tmp.p = nxt.p;
+            const int64_t e2 = (ch + 2 * nwaves) * 64 + lane;
+            v2 = e2 < E ? lvert[e2] : -1;
+            p2 = e2 < E ? list[2 * e2] : 0;
+            level2(tmp);
+            nxt = tmp;
+        }
+        const int64_t chunk0 = ch * 64;
+        const int v = cur.v;
+        const bool valid = v >= 0;
         // run flags: 1 first entry of a run, 2 last, 4 the run is the vertex's whole list
         const int vprev = __shfl_up(v, 1);
         const int vnext = __shfl_down(v, 1);
@@ -287,20 +332,14 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         if (valid) {
             if (lane == 0 || vprev != v) flags |= 1;
             if (lane == 63 || vnext != v) flags |= 2;
-            const int off = vinfo[2 * v], cnt = vinfo[2 * v + 1];
-            if (off >= chunk0 && off + cnt <= chunk0 + 64) flags |= 4;
+            if (cur.off >= chunk0 && cur.off + cur.cnt <= chunk0 + 64) flags |= 4;
         }
         vsh[w][lane] = v;
         fsh[w][lane] = flags;
 
         // r_0 = relu(a_0 h_0 + s_0), h_0 = [g_p - mu_v ; f_p] zero-padded, staged in LDS
 #pragma unroll
-        for (int i = 0; i < kMaxK0; ++i) {
-            float x = 0.f;
-            if (valid && i < d) x = pos[(int64_t)p * d + i] - mu[(int64_t)v * d + i];
-            else if (valid && i < k0) x = feat[(int64_t)p * f_d + (i - d)];
-            Y[lane * (kMaxK0 + 1) + i] = relu(fmaf(P[kA0 + i], x, P[kS0 + i]));
-        }
+        for (int i = 0; i < kMaxK0; ++i) Y[lane * (kMaxK0 + 1) + i] = relu(fmaf(P[kA0 + i], cur.x[i], P[kS0 + i]));
         wave_sync();
         float b1[4][4];  // B operands of block 1: entry 16 nt + j16, K = 4 t + q
 #pragma unroll
@@ -358,6 +397,9 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
             }
         }
         wave_sync();
+        cur = nxt;
+        nxt.v = v2;
+        nxt.p = p2;
     }
 }
 
