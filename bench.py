@@ -131,7 +131,7 @@ class Pipeline:
             self.raw = torch.from_numpy(raw).to(dev)
             self.pn_layers = pointnet_weights(w.d + raw.shape[1], w.d, float(w.sigma[0]), seed=800 + w.config)
             self.pn_params = Lattice.pack_pointnet(self.pn_layers).to(dev)
-            self.values = torch.empty((mv, 64), dtype=torch.float32, device=dev)
+            self.values = torch.empty((mv, 64), dtype=storage(0), device=dev)
         if tail == "unet":
             from datagen.clouds import conv_weight
 
@@ -332,9 +332,9 @@ def algorithmic_work(w, V, n_cls=0, Vc=0, f_raw=-1):
         work["lattice"] = {"bytes": m * (4 * d + 8 * (d + 1) + (4 if w.batch is not None else 0)) + V * 8}
         # distribute + PointNet: read each point's position and raw features,
         # each pair-list entry (8 B) and each vertex's list header (8 B), write
-        # the 64-channel fp32 row; 2 (k0 16 + 16 32 + 32 64) flops per pair on
-        # fp32 MFMA
-        work["distribute"] = {"bytes": m * 4 * (d + f_raw) + E * 8 + V * (8 + 4 * 64),
+        # the 64-channel row (bf16 when the first conv is bf16); 2 (k0 16 +
+        # 16 32 + 32 64) flops per pair on fp32 MFMA
+        work["distribute"] = {"bytes": m * 4 * (d + f_raw) + E * 8 + V * (8 + s0 * 64),
                               "flops": 2 * E * (k0 * 16 + 16 * 32 + 32 * 64), "dtype": "f32"}
     if n and Vc:
         last = w.convs[-1]

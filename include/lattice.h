@@ -394,15 +394,17 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
  *             K_3 = 32, w = 16, 32, 64.
  *   n_blocks  3;  widths  host [3], must be {16, 32, 64} (the widths the
  *             fused kernel is built for).
- *   out       dev [>= V][64] fp32 output x_v (rows 0..V-1 written).
+ *   out       dev [>= V][64] output x_v (rows 0..V-1 written), in out_dtype:
+ *             LATTICE_F32, or LATTICE_BF16 (the fp32 max rounded to nearest
+ *             even once: the storage a bf16 conv that reads the rows takes).
  *   mean      dev [>= V][d] fp32 output mu_v, or NULL.
  * The first call allocates the lattice's scratch for it (an entry-to-vertex
- * map and fp64 position sums).  Returns LATTICE_E_STATE before the first
- * splat, LATTICE_E_ARG for anything outside the above.
+ * map, fp64 position sums and running-max keys).  Returns LATTICE_E_STATE
+ * before the first splat, LATTICE_E_ARG for anything outside the above.
  */
 lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
-                                           const float *params, int n_blocks, const int *widths, float *out,
-                                           float *mean);
+                                           const float *params, int n_blocks, const int *widths, void *out,
+                                           lattice_dtype out_dtype, float *mean);
 
 /*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to

@@ -221,12 +221,6 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kTStep = 32;   // vertices per step (two MFMA K-steps of 16)
 constexpr int kTRow = 80;    // LDS bytes per channel row: 32 bf16 + 16 bytes of padding
 
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
 // Four consecutive channels [c, c+4) of row `row` as bf16 bits (rounded to
 // nearest even from fp32 storage), zero past C; C % 4 == 0 and aligned rows.
 template <bool BF16>
@@ -234,7 +228,7 @@ __device__ __forceinline__ uint2 load4_bf16(const void *base, int64_t row, int C
     if (c >= C) return make_uint2(0u, 0u);
     if (BF16) return *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(base) + row * C + c);
     const float4 f = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(base) + row * C + c);
-    return make_uint2(bf16_rne(f.x) | (bf16_rne(f.y) << 16), bf16_rne(f.z) | (bf16_rne(f.w) << 16));
+    return make_uint2(bf16_bits(f.x) | (bf16_bits(f.y) << 16), bf16_bits(f.z) | (bf16_bits(f.w) << 16));
 }
 
 template <bool G_BF16, bool X_BF16>

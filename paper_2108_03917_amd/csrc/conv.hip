@@ -33,15 +33,6 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
-// fp32 -> bf16 bits, round to nearest with ties to even (NaN stays a quiet NaN).
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
-__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
 constexpr int kRowBytes = 144;  // one LDS row: 128 bytes of K plus 16 bytes of padding
 
 // Largest tap count (d = 4): the tile's neighbour rows are staged in LDS.
@@ -578,8 +569,12 @@ struct RsShape {
     static constexpr int W_ROWS_ROUND = (2 * TILE_BYTES) / (WCPR * 16) < C_OUT ? (2 * TILE_BYTES) / (WCPR * 16) : C_OUT;
     static constexpr int W_ROUNDS = C_OUT / W_ROWS_ROUND;
     static constexpr int W_DMA = W_ROWS_ROUND * WCPR / (64 * NW);  // weight loads per wavefront per round
-    static constexpr int PD = GPS >= 8 ? 1 : 2;            // operand read-ahead, in steps
     static constexpr int LDS = 2 * TILE_BYTES + 2 * NB_BYTES + RED_BYTES;
+    // Two workgroups per CU (two wavefronts per SIMD, at most 256 registers
+    // each) when both fit in LDS and the weight slice leaves room: the
+    // second workgroup's loads are in flight while the first multiplies.
+    static constexpr int WPE = (2 * LDS <= 160 * 1024 && KGW * 4 <= 160) ? 2 : 1;
+    static constexpr int PD = (GPS >= 8 || WPE == 2) ? 1 : 2;  // operand read-ahead, in steps
     static_assert(NCG * NRG * KS == NW && NRG >= 1, "wavefront roles");
     static_assert(KG % KS == 0 && KGW % T == 0, "groups per step");
     static_assert(TILE % (64 * NW) == 0, "tile loads");
@@ -591,7 +586,7 @@ struct RsShape {
 };
 
 template <bool BF16, bool OUT_BF16, int T, int C_IN, int C_OUT, int KS>
-__global__ __launch_bounds__(256) void k_conv_rs(const void *__restrict__ in_, const void *__restrict__ w_,
+__global__ __launch_bounds__(256, (RsShape<BF16, C_IN, C_OUT, T, KS>::WPE)) void k_conv_rs(const void *__restrict__ in_, const void *__restrict__ w_,
                                                  const float *__restrict__ bias, void *__restrict__ out,
                                                  const int32_t *__restrict__ nbr, int64_t nbr_ints,
                                                  const int32_t *__restrict__ counters,
@@ -720,10 +715,11 @@ __global__ __launch_bounds__(256) void k_conv_rs(const void *__restrict__ in_, c
             const int g = kg - t * S::GPT;
             return *reinterpret_cast<const u32x4_t *>(arow + t * S::SLICE * 16 + (((2 * g + h) ^ rs::swz<S::CPR>(r)) * 16));
         };
-        // Operand groups are read PD steps ahead of their MFMAs (one
-        // wavefront per SIMD: nothing else hides the LDS latency).  With
-        // PD = 1 a single set of registers: group g of step st+1 is read as
-        // soon as the MFMAs of group g of step st are issued.
+        // Operand groups are read PD steps ahead of their MFMAs (with one
+        // wavefront per SIMD nothing else hides the LDS latency; with two,
+        // the other one does).  With PD = 1 a single set of registers: group
+        // g of step st+1 is read as soon as the MFMAs of group g of step st
+        // are issued.
         constexpr int PD = S::PD;
         constexpr int NSETS = PD == 1 ? 1 : PD + 1;
         u32x4_t af[NSETS][S::GPS];
@@ -1152,7 +1148,7 @@ hipError_t launch_rs(lattice *L, const void *in, const void *w, const float *bia
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const int per_cu = (160 * 1024) / S::LDS < 2 ? 1 : 2;
+    const int per_cu = S::WPE;
     const int64_t tiles = (L->max_vertices + S::MT - 1) / S::MT;
     int64_t grid = (int64_t)L->cu_count * per_cu;
     if (grid > tiles) grid = tiles;

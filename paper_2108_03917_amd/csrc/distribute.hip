@@ -22,18 +22,24 @@
 //                    that is the vertex's whole list writes mu_v, otherwise
 //                    the run is added to the vertex's fp64 sum atomically
 //   k_mean_finish    mu_v of the lists that cross a 64-entry chunk
-//   k_pointnet_rows  the key of -inf in the output rows of those vertices
-//                    (and, after k_pointnet, their keys decoded to floats)
+//   k_pointnet_rows  the key of -inf in the key row of each vertex whose
+//                    list crosses a 64-entry chunk boundary (and, after
+//                    k_pointnet, those keys decoded into the output rows)
 //   k_pointnet       the three blocks as fp32 MFMA products over the
 //                    wavefront's 64 entries (weight fragments held in
 //                    registers); block 3's outputs go to LDS channel-major;
 //                    then lane c walks the wavefront's entries keeping the
 //                    running max of channel c and stores it at the end of
-//                    each run: a plain store (64 lanes, one row) when the run
-//                    is the vertex's whole list, else an unsigned atomic max of an
-//                    order-preserving key (no returned value to wait for).
+//                    each run: a plain store (64 lanes, one row, fp32 or bf16)
+//                    when the run is the vertex's whole list, else an
+//                    unsigned atomic max of an order-preserving key (no
+//                    returned value to wait for) into the vertex's key row.
+//                    A list that crosses a boundary starts in the chunk just
+//                    before it, and only one list crosses each boundary, so
+//                    key row j belongs to the list that starts in chunk j.
 //                    The max is exact in any order, so the result does not
-//                    depend on scheduling.
+//                    depend on scheduling; a bf16 row is rounded once, from
+//                    the fp32 max.
 #include "internal.h"
 
 namespace {
@@ -48,8 +54,7 @@ __device__ __forceinline__ float relu(float x) { return x > 0.f ? x : 0.f; }
 
 // Order-preserving map of a float to an unsigned integer (a > b exactly
 // when key(a) > key(b), for non-NaN values), so that an unsigned atomic max,
-// which needs no returned value, is a float max.  Rows that take atomic
-// maxima hold keys until k_pointnet_finish decodes them.
+// which needs no returned value, is a float max.
 __device__ __forceinline__ unsigned int max_key(float f) {
     const unsigned int u = __float_as_uint(f);
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
@@ -150,28 +155,38 @@ __global__ __launch_bounds__(kBlock) void k_mean_finish(const int32_t *__restric
     }
 }
 
-// The key of -inf in the rows of the vertices whose list crosses a chunk
-// boundary (mode 0), or those rows' keys decoded back to floats (mode 1):
-// the vertex of entry 64k (k >= 1) when its list starts before it.  A long
-// list crosses several boundaries; only its first crossing does the work.
+// Store channel c of output row v as fp32 or, rounded to nearest even, bf16.
+template <bool OUT_BF16>
+__device__ __forceinline__ void store_out(void *out, int64_t v, int c, float x) {
+    if (OUT_BF16)
+        reinterpret_cast<uint16_t *>(out)[v * kW3 + c] = (uint16_t)bf16_bits(x);
+    else
+        reinterpret_cast<float *>(out)[v * kW3 + c] = x;
+}
+
+// Lists that cross a chunk boundary: the vertex of entry 64 (j + 1), j >= 0,
+// when its list starts in chunk j.  Mode 0 sets key row j to the key of -inf;
+// mode 1 decodes it into the vertex's output row.  A long list crosses
+// several boundaries; only its first crossing does the work.
+template <bool OUT_BF16>
 __global__ __launch_bounds__(kBlock) void k_pointnet_rows(const int32_t *__restrict__ lvert,
                                                           const int32_t *__restrict__ vinfo,
                                                           const int32_t *__restrict__ counters, int mode,
-                                                          float *__restrict__ out) {
+                                                          unsigned int *__restrict__ keys, void *__restrict__ out) {
     const int64_t E = counters[CNT_E];
     const int64_t nb = E > 0 ? (E - 1) / 64 : 0;  // boundaries 64, 128, ... below E
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < nb * kW3; q += stride) {
-        const int64_t e0 = (q / kW3 + 1) * 64;
+        const int64_t j = q / kW3;
+        const int64_t e0 = (j + 1) * 64;
         const int c = (int)(q % kW3);
         const int v = lvert[e0];
         const int64_t off = vinfo[2 * v];
         if (off >= e0 || off < e0 - 64) continue;  // not crossing here, or crossed an earlier boundary
-        unsigned int *row = reinterpret_cast<unsigned int *>(out) + (int64_t)v * kW3;
         if (mode == 0)
-            row[c] = max_key(-__builtin_huge_valf());
+            keys[j * kW3 + c] = max_key(-__builtin_huge_valf());
         else
-            out[(int64_t)v * kW3 + c] = key_value(row[c]);
+            store_out<OUT_BF16>(out, v, c, key_value(keys[j * kW3 + c]));
     }
 }
 
@@ -227,13 +242,15 @@ __device__ __forceinline__ void wave_sync() {
 // lane stages its own row).  The outputs go to LDS channel-major for the
 // per-run max.  Each wavefront loops over its own chunks (wavefront-level
 // synchronisation only).
+template <bool OUT_BF16>
 __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__ list,
                                                      const int32_t *__restrict__ lvert,
                                                      const int32_t *__restrict__ vinfo,
                                                      const float *__restrict__ pos, const float *__restrict__ feat,
                                                      int d, int f_d, const float *__restrict__ P,
                                                      const float *__restrict__ mu,
-                                                     const int32_t *__restrict__ counters, float *__restrict__ out) {
+                                                     const int32_t *__restrict__ counters,
+                                                     unsigned int *__restrict__ keys, void *__restrict__ out) {
     __shared__ float ysh[kWaves][kW3 * kYStride];  // outputs [64 channels][64 entries]; first the staged inputs
     __shared__ int32_t vsh[kWaves][64];
     __shared__ int32_t fsh[kWaves][64];
@@ -334,7 +351,9 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
             if (lane == 63 || vnext != v) flags |= 2;
             if (cur.off >= chunk0 && cur.off + cur.cnt <= chunk0 + 64) flags |= 4;
         }
-        vsh[w][lane] = v;
+        // destination of the run: the output row, or the key row of the
+        // chunk where the vertex's list starts
+        vsh[w][lane] = (flags & 4) ? v : (valid ? (int)(cur.off >> 6) : -1);
         fsh[w][lane] = flags;
 
         // r_0 = relu(a_0 h_0 + s_0), h_0 = [g_p - mu_v ; f_p] zero-padded, staged in LDS
@@ -388,11 +407,10 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
                 const float y = Y[c * kYStride + jj];
                 mx = (fj & 1) ? y : fmaxf(mx, y);
                 if (vj >= 0 && (fj & 2)) {
-                    float *dst = out + (int64_t)vj * kW3 + c;
                     if (fj & 4)
-                        *dst = mx;
+                        store_out<OUT_BF16>(out, vj, c, mx);
                     else
-                        atomicMax(reinterpret_cast<unsigned int *>(dst), max_key(mx));
+                        atomicMax(keys + (int64_t)vj * kW3 + c, max_key(mx));
                 }
             }
         }
@@ -414,7 +432,7 @@ int pointnet_param_count(int k0) {
 }
 
 hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
-                                      float *out, float *mean) {
+                                      void *out, bool out_bf16, float *mean) {
     if (L->m == 0) return hipSuccess;
     const int d = L->d;
     float *mu = mean ? mean : L->mu;
@@ -442,18 +460,20 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_mean_finish, dim3(g_v), dim3(kBlock), 0, L->stream, L->vinfo, L->macc, d, L->counters, mu);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    auto rows = out_bf16 ? k_pointnet_rows<true> : k_pointnet_rows<false>;
     const unsigned g_i = grid_for((E / 64 + 1) * kW3, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(k_pointnet_rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 0,
+    hipLaunchKernelGGL(rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 0, L->pn_keys,
                        out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_pack_pointnet, dim3((kPadded + kBlock - 1) / kBlock), dim3(kBlock), 0, L->stream, params,
                        d + f_d, L->pn_params);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned g_p = grid_for(E, kBlock, L->cu_count, 2);  // 69 KB of LDS: two workgroups per CU
-    hipLaunchKernelGGL(k_pointnet, dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo, pos, feat, d,
-                       f_d, L->pn_params, mu, L->counters, out);
+    hipLaunchKernelGGL((out_bf16 ? k_pointnet<true> : k_pointnet<false>), dim3(g_p), dim3(kBlock), 0, L->stream,
+                       L->list, L->lvert, L->vinfo, pos, feat, d, f_d, L->pn_params, mu, L->counters, L->pn_keys,
+                       out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_pointnet_rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 1,
+    hipLaunchKernelGGL(rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 1, L->pn_keys,
                        out);
     return hipGetLastError();
 }

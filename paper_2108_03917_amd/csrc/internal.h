@@ -1,6 +1,6 @@
 // Internal declarations shared by the host API (lattice.hip) and the kernel
 // translation units (splat.hip, neighbors.hip, conv.hip, slice.hip, deform.hip,
-// backward.hip).
+// backward.hip, distribute.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -28,6 +28,15 @@ constexpr int KEY_BIAS = 32768;
 constexpr int KEY_MAX = 32767;
 
 struct HEntry;  // hash table entry (keys.h)
+
+// fp32 -> bf16 bits, round to nearest with ties to even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 struct lattice_timer {
     double ms = 0.0;    // summed elapsed time of read event pairs
@@ -77,6 +86,8 @@ struct lattice {
     double *macc = nullptr;     // [max_vertices][d] position sums of lists that cross a 64-entry chunk
     float *mu = nullptr;        // [max_vertices][d] local means when the caller does not take them
     float *pn_params = nullptr; // the PointNet parameters in the kernel's padded layout
+    unsigned int *pn_keys = nullptr;  // [(d+1) max_points / 64 + 1][64] running-max keys of lists
+                                      // that cross a 64-entry chunk (row j: the list starting in chunk j)
     int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
     int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
@@ -137,7 +148,7 @@ hipError_t launch_flip_weights(lattice *L, const void *w, bool bf16, int C_out, 
 
 // distribute.hip
 hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
-                                      float *out, float *mean);
+                                      void *out, bool out_bf16, float *mean);
 int pointnet_param_count(int k0);
 int pointnet_padded_count();
 

@@ -55,6 +55,7 @@ void free_all(lattice *L) {
     (void)hipFree(L->macc);
     (void)hipFree(L->mu);
     (void)hipFree(L->pn_params);
+    (void)hipFree(L->pn_keys);
     (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
     (void)hipFree(L->rank);
@@ -590,15 +591,16 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
 }
 
 lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
-                                           const float *params, int n_blocks, const int *widths, float *out,
-                                           float *mean) {
+                                           const float *params, int n_blocks, const int *widths, void *out,
+                                           lattice_dtype out_dtype, float *mean) {
     if (!L) return LATTICE_E_ARG;
     if (!L->splatted) {
         set_err(L, "distribute_pointnet: no lattice yet (call lattice_splat first)");
         return LATTICE_E_STATE;
     }
     if (f_d < 0 || L->d + f_d > 16 || (f_d > 0 && L->m > 0 && !feat) || !params || !widths || n_blocks != 3 ||
-        widths[0] != 16 || widths[1] != 32 || widths[2] != 64 || (L->m > 0 && (!pos || !out))) {
+        widths[0] != 16 || widths[1] != 32 || widths[2] != 64 || (L->m > 0 && (!pos || !out)) ||
+        (out_dtype != LATTICE_F32 && out_dtype != LATTICE_BF16)) {
         set_err(L, "distribute_pointnet: bad argument (f_d = %d; the fused PointNet has 3 blocks of widths 16, "
                 "32, 64 and d + f_d <= 16)", f_d);
         return LATTICE_E_ARG;
@@ -609,24 +611,28 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
         bool ok = hipMalloc(&L->lvert, E_max * sizeof(int32_t)) == hipSuccess &&
                   hipMalloc(&L->macc, L->max_vertices * L->d * sizeof(double)) == hipSuccess &&
                   hipMalloc(&L->mu, L->max_vertices * L->d * sizeof(float)) == hipSuccess &&
-                  hipMalloc(&L->pn_params, pointnet_padded_count() * sizeof(float)) == hipSuccess;
+                  hipMalloc(&L->pn_params, pointnet_padded_count() * sizeof(float)) == hipSuccess &&
+                  hipMalloc(&L->pn_keys, (E_max / 64 + 1) * 64 * sizeof(unsigned int)) == hipSuccess;
         if (!ok) {
             (void)hipGetLastError();
             (void)hipFree(L->lvert);
             (void)hipFree(L->macc);
             (void)hipFree(L->mu);
             (void)hipFree(L->pn_params);
+            (void)hipFree(L->pn_keys);
             L->lvert = nullptr;
             L->macc = nullptr;
             L->mu = nullptr;
             L->pn_params = nullptr;
+            L->pn_keys = nullptr;
             set_err(L, "distribute_pointnet: cannot allocate its scratch");
             return LATTICE_E_NOMEM;
         }
     }
     hipEvent_t t0;
     if ((s = timer_begin(L, LATTICE_STAGE_DISTRIBUTE, &t0))) return s;
-    if ((s = check_launch(L, launch_distribute_pointnet(L, pos, feat, f_d, params, out, mean),
+    if ((s = check_launch(L, launch_distribute_pointnet(L, pos, feat, f_d, params, out, out_dtype == LATTICE_BF16,
+                                                        mean),
                           "distribute_pointnet")))
         return s;
     return timer_end(L, LATTICE_STAGE_DISTRIBUTE, t0);

@@ -21,13 +21,6 @@ namespace {
 
 constexpr int kBlock = 256;
 
-// fp32 -> bf16 bits, round to nearest with ties to even (NaN stays a quiet NaN).
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
 
 struct ElevParams {
     float f[LATTICE_MAX_D];

@@ -64,7 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_slice_backward": (St, [P, P, I, P, I]),
         "lattice_splat_backward": (St, [P, P, I, I, I, P, P]),
         "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
-        "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, P]),
+        "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, I, P]),
         "lattice_downsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_upsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
@@ -324,12 +324,13 @@ class Lattice:
 
     def distribute_pointnet(self, pos: torch.Tensor, feat: Optional[torch.Tensor], params: torch.Tensor,
                             out: Optional[torch.Tensor] = None, mean: Optional[torch.Tensor] = None,
-                            want_mean: bool = False):
+                            want_mean: bool = False, out_dtype: str = "f32"):
         """Distribute + PointNet + per-vertex max over the last splat's pairs:
         ``pos`` [m, d] (the positions that were splatted), ``feat`` [m, f_d]
         or None, ``params`` the packed parameters (see pack_pointnet) on the
-        device.  Returns out [rows, 64] (and the local means [rows, d] with
-        want_mean or a ``mean`` tensor)."""
+        device.  Returns out [rows, 64], stored as fp32 or bf16 (the dtype of
+        ``out``, else ``out_dtype``), and the local means [rows, d] with
+        want_mean or a ``mean`` tensor."""
         _dev(pos, torch.float32, "pos")
         if pos.dim() != 2 or pos.shape != (self.m, self.d):
             raise ValueError(f"pos must be the splatted [m = {self.m}, {self.d}] positions")
@@ -346,8 +347,8 @@ class Lattice:
             raise ValueError(f"params must hold {n_par} values for d + f_d = {k0}")
         need = self._rows_needed()
         if out is None:
-            out = torch.empty((max(need, 1), 64), dtype=torch.float32, device=pos.device)
-        _dev(out, torch.float32, "out")
+            out = torch.empty((max(need, 1), 64), dtype=_TORCH[out_dtype], device=pos.device)
+        _dev(out, (torch.float32, torch.bfloat16), "out")
         if out.dim() != 2 or out.shape[1] != 64 or out.shape[0] < need:
             raise ValueError(f"out needs [>= {need}, 64]")
         if mean is None and want_mean:
@@ -358,7 +359,8 @@ class Lattice:
                 raise ValueError(f"mean needs [>= {need}, {self.d}]")
         widths = (ctypes.c_int * 3)(*self.POINTNET_WIDTHS)
         self._check(self._lib.lattice_distribute_pointnet(self._h, _ptr(pos), _ptr(feat), f_d, _ptr(params), 3,
-                                                          widths, _ptr(out), _ptr(mean)), "distribute_pointnet")
+                                                          widths, _ptr(out), _STORAGE[out.dtype], _ptr(mean)),
+                    "distribute_pointnet")
         return (out, mean) if mean is not None else out
 
     # -- downsampling / upsampling ----------------------------------------

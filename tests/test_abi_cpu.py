@@ -120,3 +120,31 @@ def test_resample_binding_passes_source_then_destination(monkeypatch):
     z = coarse.upsample(fine, torch.zeros((40, 4)), w)
     assert calls == [("down", "FINE", "COARSE"), ("up", "COARSE", "FINE")]
     assert y.shape == (40, 4) and z.shape == (100, 4)
+
+
+def test_distribute_binding_passes_the_output_storage(monkeypatch):
+    """lattice_distribute_pointnet takes the output's storage type right after
+    the output pointer: the binding derives it from the out tensor."""
+    import torch
+
+    calls = []
+
+    class Stub:
+        def lattice_distribute_pointnet(self, *a):
+            calls.append(a)
+            return 0
+
+    monkeypatch.setattr(B, "_dev", lambda t, dtype, name: t)
+    monkeypatch.setattr(B, "_ptr", lambda t: None if t is None else id(t))
+    L = object.__new__(B.Lattice)
+    L._lib, L._h, L.taps, L._V, L.m, L.d = Stub(), "H", 9, 50, 10, 3
+    k0 = 3   # d + f_d: per block a, s, W, b
+    params = torch.zeros(2 * k0 + 16 * k0 + 16 + 2 * 16 + 32 * 16 + 32 + 2 * 32 + 64 * 32 + 64)
+    for dt, code in ((torch.float32, B.F32), (torch.bfloat16, B.BF16)):
+        out = torch.zeros((50, 64), dtype=dt)
+        L.distribute_pointnet(torch.zeros((10, 3)), None, params, out=out)
+        a = calls[-1]
+        assert a[0] == "H" and a[3] == 0 and a[5] == 3
+        assert a[7] == id(out) and a[8] == code and a[9] is None
+    out = L.distribute_pointnet(torch.zeros((10, 3)), None, params, out_dtype="bf16")
+    assert out.dtype == torch.bfloat16 and calls[-1][8] == B.BF16

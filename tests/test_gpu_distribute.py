@@ -29,7 +29,7 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def _run(pos, feat, sigma, batch=None, seed=0):
+def _run(pos, feat, sigma, batch=None, seed=0, out_dtype="f32"):
     from paper_2108_03917_amd import Lattice
 
     d = pos.shape[1]
@@ -41,13 +41,19 @@ def _run(pos, feat, sigma, batch=None, seed=0):
     sig0 = float(np.asarray(sigma, dtype=np.float64).reshape(-1)[0])
     layers = pointnet_weights(d + f_d, d, sig0, seed=seed)
     params = Lattice.pack_pointnet(layers).to("cuda:0")
-    out, mean = L.distribute_pointnet(to_dev(pos), None if feat is None else to_dev(feat), params, want_mean=True)
+    out, mean = L.distribute_pointnet(to_dev(pos), None if feat is None else to_dev(feat), params, want_mean=True,
+                                      out_dtype=out_dtype)
     ref, scale, mu = O.distribute_pointnet(lat, pos, feat, layers)
-    got = g.from_gpu_order(out)
+    got = g.from_gpu_order(out.float())
     gmu = g.from_gpu_order(mean)
     assert np.all(np.isfinite(got))
     assert_close_scaled(gmu, mu, 2.0 ** -22 * np.abs(mu) + 1e-7 * np.abs(pos).max(), 1.0, "local mean")
-    assert_close_scaled(got, ref, scale, REL_F32, f"distribute+pointnet d={d} f_d={f_d}")
+    tag = f"distribute+pointnet d={d} f_d={f_d} {out_dtype}"
+    if out_dtype == "bf16":
+        # the fp32 max rounded once to nearest even: half a bf16 ulp of the value
+        assert_close_scaled(got, ref, REL_F32 * scale + 2.0 ** -8 * np.abs(ref), 1.0, tag)
+    else:
+        assert_close_scaled(got, ref, scale, REL_F32, tag)
     return lat
 
 
@@ -63,6 +69,14 @@ def test_distribute_pointnet_batched():
     _run(w.pos, w.feat, 0.15, batch=w.batch, seed=511)
 
 
+@pytest.mark.parametrize("d,f_d", [(3, 6), (4, 1)])
+def test_distribute_pointnet_bf16_rows(d, f_d):
+    """Output rows stored as bf16 (for a bf16 conv that reads them), the
+    whole-list stores and the decoded crossing lists both."""
+    w = random_cloud(6000, d, seed=515 + d, extent=1.0, C=f_d)
+    _run(w.pos, w.feat[:, :f_d], 0.15 if d == 3 else 0.3, seed=516 + d, out_dtype="bf16")
+
+
 def test_distribute_pointnet_long_lists():
     """Tight clusters: vertices with hundreds to thousands of rows, whose
     lists span many 64-entry chunks (atomic max and fp64 atomic mean) and
@@ -73,7 +87,8 @@ def test_distribute_pointnet_long_lists():
     sparse = rng.uniform(-1, 1, size=(3000, 3))
     pos = np.concatenate([dense, sparse]).astype(np.float32)[rng.permutation(9000)]
     feat = rng.standard_normal((9000, 4)).astype(np.float32)
-    lat = _run(pos, feat, 0.1, seed=521)
+    for out_dtype in ("f32", "bf16"):
+        lat = _run(pos, feat, 0.1, seed=521, out_dtype=out_dtype)
     n = np.bincount(lat.idx.ravel(), minlength=lat.V)
     assert n.max() > 500 and (n > 64).sum() >= 3
 
@@ -92,16 +107,20 @@ def test_distribute_pointnet_empty_and_rejects():
     ok_widths = (ctypes.c_int * 3)(16, 32, 64)
     with pytest.raises(LatticeError):        # d + f_d = 17 > 16
         L._check(L._lib.lattice_distribute_pointnet(L._h, None, feat.data_ptr(), 14, params.data_ptr(), 3,
-                                                    ok_widths, None, None), "distribute_pointnet")
+                                                    ok_widths, None, 0, None), "distribute_pointnet")
     with pytest.raises(LatticeError):        # widths other than 16, 32, 64
         L._check(L._lib.lattice_distribute_pointnet(L._h, None, None, 0, params.data_ptr(), 3,
-                                                    (ctypes.c_int * 3)(16, 32, 32), None, None),
+                                                    (ctypes.c_int * 3)(16, 32, 32), None, 0, None),
                  "distribute_pointnet")
+    with pytest.raises(LatticeError):        # an output type other than fp32 and bf16
+        L._check(L._lib.lattice_distribute_pointnet(L._h, None, None, 0, params.data_ptr(), 3, ok_widths, None, 7,
+                                                    None), "distribute_pointnet")
 
 
-@pytest.mark.parametrize("config", [3, 4])
-def test_distribute_pointnet_full_size(config):
-    """The indoor room (200k points, rgb + normal) and the LiDAR scan (about
-    1.04e5 points in scan order, dense near the sensor), every vertex compared."""
+@pytest.mark.parametrize("config,out_dtype", [(3, "bf16"), (4, "f32")])
+def test_distribute_pointnet_full_size(config, out_dtype):
+    """The indoor room (200k points, rgb + normal; bf16 rows, as the bench's
+    first conv reads them) and the LiDAR scan (about 1.04e5 points in scan
+    order, dense near the sensor), every vertex compared."""
     w = make_workload(config)
-    _run(w.pos, raw_point_features(w), w.sigma, seed=530 + config)
+    _run(w.pos, raw_point_features(w), w.sigma, seed=530 + config, out_dtype=out_dtype)
