@@ -617,34 +617,63 @@ __device__ __forceinline__ float4 fma4(float b, float4 y, float4 acc) {
     return acc;
 }
 
-// Sum b f over list entries [e0, e1) for float4 column c (VEC) or column c.
-template <bool VEC>
-__device__ __forceinline__ float4 sum_pairs(const int2 *__restrict__ L2, int e0, int e1, const float *__restrict__ feat,
-                                            int CV, int c) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+// One block of BLK list entries q (the first n of them real) for float4
+// column c (VEC) or column c: their rows are loaded together, then b f and b
+// are added for the real ones.  Selects, not branches: a branch would let
+// the compiler sink the loads into it and serialise them.
+template <bool VEC, int BLK>
+__device__ __forceinline__ void add_block(const int2 (&q)[BLK], int n, const float *__restrict__ feat, int CV, int c,
+                                          float4 &acc, float &w) {
     if (VEC) {
         const float4 *f4 = reinterpret_cast<const float4 *>(feat);
-        int e = e0;
-        for (; e + 4 <= e1; e += 4) {
-            const int2 q0 = L2[e], q1 = L2[e + 1], q2 = L2[e + 2], q3 = L2[e + 3];
-            const float4 y0 = f4[(int64_t)q0.x * CV + c], y1 = f4[(int64_t)q1.x * CV + c];
-            const float4 y2 = f4[(int64_t)q2.x * CV + c], y3 = f4[(int64_t)q3.x * CV + c];
-            acc = fma4(__int_as_float(q0.y), y0, acc);
-            acc = fma4(__int_as_float(q1.y), y1, acc);
-            acc = fma4(__int_as_float(q2.y), y2, acc);
-            acc = fma4(__int_as_float(q3.y), y3, acc);
-        }
-        for (; e < e1; ++e) {
-            const int2 q = L2[e];
-            acc = fma4(__int_as_float(q.y), f4[(int64_t)q.x * CV + c], acc);
+        float4 y[BLK];
+#pragma unroll
+        for (int i = 0; i < BLK; ++i) y[i] = f4[(int64_t)q[i].x * CV + c];
+#pragma unroll
+        for (int i = 0; i < BLK; ++i) {
+            const bool ok = i < n;
+            const float b = ok ? __int_as_float(q[i].y) : 0.f;
+            const float4 t = fma4(b, y[i], acc);
+            acc.x = ok ? t.x : acc.x;
+            acc.y = ok ? t.y : acc.y;
+            acc.z = ok ? t.z : acc.z;
+            acc.w = ok ? t.w : acc.w;
+            w += b;
         }
     } else {
-        for (int e = e0; e < e1; ++e) {
-            const int2 q = L2[e];
-            acc.x = fmaf(__int_as_float(q.y), feat[(int64_t)q.x * CV + c], acc.x);
+        float y[BLK];
+#pragma unroll
+        for (int i = 0; i < BLK; ++i) y[i] = CV > 0 ? feat[(int64_t)q[i].x * CV + c] : 0.f;
+#pragma unroll
+        for (int i = 0; i < BLK; ++i) {
+            const bool ok = i < n;
+            const float b = ok ? __int_as_float(q[i].y) : 0.f;
+            const float t = fmaf(b, y[i], acc.x);
+            acc.x = ok ? t : acc.x;
+            w += b;
         }
     }
-    return acc;
+}
+
+// The list entries [e, e + BLK) clamped to [.., e1): indices past e1 re-read
+// entry e1 - 1 (and are not added).
+template <int BLK>
+__device__ __forceinline__ void load_block(const int2 *__restrict__ L2, int e, int e1, int2 (&q)[BLK]) {
+#pragma unroll
+    for (int i = 0; i < BLK; ++i) q[i] = L2[e + i < e1 ? e + i : e1 - 1];
+}
+
+// Sum b f over list entries [e0, e1) for float4 column c (VEC) or column c,
+// added to acc, and the weights b added to w, in blocks of BLK entries: a
+// block's list loads are all issued, then its row loads, before any is used.
+template <bool VEC, int BLK>
+__device__ __forceinline__ void sum_pairs(const int2 *__restrict__ L2, int e0, int e1, const float *__restrict__ feat,
+                                          int CV, int c, float4 &acc, float &w) {
+    for (int e = e0; e < e1; e += BLK) {
+        int2 q[BLK];
+        load_block<BLK>(L2, e, e1, q);
+        add_block<VEC, BLK>(q, e1 - e, feat, CV, c, acc, w);
+    }
 }
 
 template <bool VEC>
@@ -672,7 +701,7 @@ __device__ __forceinline__ float4 scale4(float4 a, float w, int normalize) {
 //            would need a device-scope release per part, which costs more
 //            than the extra launch: every XCD has its own L2.)
 template <bool VEC, bool OUT_BF16>
-__global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ vinfo, const int32_t *__restrict__ list,
+__global__ __launch_bounds__(kBlock, 8) void k_gather(const int32_t *__restrict__ vinfo, const int32_t *__restrict__ list,
                                                    const int32_t *__restrict__ split,
                                                    const int32_t *__restrict__ rowmap, float *__restrict__ partial,
                                                    float *__restrict__ pweight, const float *__restrict__ feat,
@@ -690,50 +719,75 @@ __global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ v
     const int CV = VEC ? (C >> 2) : C;
     const int2 *L2 = reinterpret_cast<const int2 *>(list);
 
-    // Phase 1: short lists.
-    for (int64_t v0 = wave * gpw; v0 < V; v0 += nwaves * gpw) {
-        const int64_t v = v0 + grp;
-        if (v >= V) continue;
-        const int off = vinfo[2 * v];
-        const int cnt = vinfo[2 * v + 1];
-        if (cnt > kPart) continue;  // phase 2
+    // Phase 1: short lists.  The list header of the group's next vertex is
+    // loaded while this one is summed (two header registers, so that the
+    // wait for one header is not a wait for the other).  With C = 0
+    // (weights only) lane 0 of the group sums the weights alone.
+    const int2 *VI = reinterpret_cast<const int2 *>(vinfo);
+    const int64_t vstep = nwaves * gpw;
+    auto header = [&](int64_t v) { return v < V ? VI[v] : make_int2(0, kPart + 1); };
+    auto short_list = [&](int64_t v, int2 vi) {
+        if (v >= V || vi.y > kPart) return;
+        const int off = vi.x, e1 = vi.x + vi.y;
         float w = 0.f;
-        for (int e = off; e < off + cnt; ++e) w += __int_as_float(L2[e].y);
         for (int c = j; c < CV; c += G) {
-            const float4 acc = scale4<VEC>(sum_pairs<VEC>(L2, off, off + cnt, feat, CV, c), w, normalize);
+            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+            w = 0.f;
+            sum_pairs<VEC, 4>(L2, off, e1, feat, CV, c, acc, w);
+            acc = scale4<VEC>(acc, w, normalize);
             if (VEC)
                 store4<OUT_BF16>(values, v * CV + c, acc);
             else
                 store1<OUT_BF16>(values, v * C + c, acc.x);
         }
-        if (weight && j == 0) weight[v] = w;
+        if (weight && j == 0) {
+            if (CV == 0) {
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                sum_pairs<false, 4>(L2, off, e1, feat, 0, 0, acc, w);
+            }
+            weight[v] = w;
+        }
+    };
+    int64_t v = wave * gpw + grp;
+    int2 ha = header(v);
+    for (; v - grp < V; v += 2 * vstep) {
+        const int2 hb = header(v + vstep);
+        short_list(v, ha);
+        if (v - grp + vstep >= V) break;
+        ha = header(v + 2 * vstep);
+        short_list(v + vstep, hb);
     }
 
     // Phase 2: parts of long lists.
     for (int64_t u0 = wave * gpw; u0 < nrows; u0 += nwaves * gpw) {
         const int64_t u = u0 + grp;
         const bool live = u < nrows;
-        int sp = 0, v = 0, row0 = 0, parts = 1, off = 0, cnt = 0, e0 = 0, e1 = 0;
         if (live) {
-            sp = rowmap[u];
-            v = split[3 * sp];
-            row0 = split[3 * sp + 1];
-            parts = split[3 * sp + 2];
-            off = vinfo[2 * v];
-            cnt = vinfo[2 * v + 1];
+            const int sp = rowmap[u];
+            const int vv = split[3 * sp];
+            const int row0 = split[3 * sp + 1];
+            const int off = vinfo[2 * vv];
+            const int cnt = vinfo[2 * vv + 1];
             const int part = (int)(u - row0);
-            e0 = off + part * kPart;
-            e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
+            const int e0 = off + part * kPart;
+            const int e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
             float w = 0.f;
-            for (int e = e0; e < e1; ++e) w += __int_as_float(L2[e].y);
             for (int c = j; c < CV; c += G) {
-                const float4 acc = sum_pairs<VEC>(L2, e0, e1, feat, CV, c);
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                w = 0.f;
+                sum_pairs<VEC, 4>(L2, e0, e1, feat, CV, c, acc, w);
                 if (VEC)
                     reinterpret_cast<float4 *>(partial)[u * CV + c] = acc;
                 else
                     partial[u * C + c] = acc.x;
             }
-            if (j == 0) pweight[u] = w;
+            if (j == 0) {
+                if (CV == 0) {
+                    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                    sum_pairs<false, 4>(L2, e0, e1, feat, 0, 0, acc, w);
+                }
+                pweight[u] = w;
+            }
         }
     }
 }
