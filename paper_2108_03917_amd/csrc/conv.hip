@@ -564,12 +564,12 @@ struct RsShape {
     static constexpr int NB_INTS = MT * T;                 // neighbour block of a tile
     static constexpr int NB_DMA = (NB_INTS * 4 + 1023) / 1024;
     static constexpr int NB_BYTES = NB_DMA * 1024;
-    static constexpr int RED_BYTES = KS > 1 ? NCG * NRG * 16 * 64 * 4 : 0;  // partial sums
+    static constexpr int RED_BYTES = KS > 1 ? NCG * NRG * 16 * 64 * 4 : 0;  // partial sums (in the tile's buffer)
     static constexpr int WCPR = K * ESZ / 16;              // chunks per weight row
     static constexpr int W_ROWS_ROUND = (2 * TILE_BYTES) / (WCPR * 16) < C_OUT ? (2 * TILE_BYTES) / (WCPR * 16) : C_OUT;
     static constexpr int W_ROUNDS = C_OUT / W_ROWS_ROUND;
     static constexpr int W_DMA = W_ROWS_ROUND * WCPR / (64 * NW);  // weight loads per wavefront per round
-    static constexpr int LDS = 2 * TILE_BYTES + 2 * NB_BYTES + RED_BYTES;
+    static constexpr int LDS = 2 * TILE_BYTES + 2 * NB_BYTES;
     // Two workgroups per CU (two wavefronts per SIMD, at most 256 registers
     // each) when both fit in LDS and the weight slice leaves room: the
     // second workgroup's loads are in flight while the first multiplies.
@@ -583,6 +583,7 @@ struct RsShape {
     static_assert(W_ROWS_ROUND % 32 == 0 && C_OUT % W_ROWS_ROUND == 0, "weight rounds");
     static_assert((W_ROWS_ROUND * WCPR) % (64 * NW) == 0, "weight loads");
     static_assert(LDS <= 160 * 1024, "LDS");
+    static_assert(RED_BYTES <= TILE_BYTES, "partial sums fit in a tile buffer");
 };
 
 template <bool BF16, bool OUT_BF16, int T, int C_IN, int C_OUT, int KS>
@@ -597,7 +598,6 @@ __global__ __launch_bounds__(256, (RsShape<BF16, C_IN, C_OUT, T, KS>::WPE)) void
     extern __shared__ __attribute__((aligned(16))) char lds[];
     auto abuf = [&](int b) { return lds + b * S::TILE_BYTES; };                      // row tiles
     auto nbuf = [&](int b) { return lds + 2 * S::TILE_BYTES + b * S::NB_BYTES; };    // neighbour blocks
-    float *red = reinterpret_cast<float *>(lds + 2 * S::TILE_BYTES + 2 * S::NB_BYTES);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -763,8 +763,11 @@ __global__ __launch_bounds__(256, (RsShape<BF16, C_IN, C_OUT, T, KS>::WPE)) void
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc0[i] += acc1[i];
         if (KS > 1) {
-            // the second K half adds its partial sums through LDS
-            float *slot = red + ((cg * S::NRG + rg) * 16) * 64;
+            // the second K half adds its partial sums through LDS, in this
+            // tile's row buffer once every wavefront has read its operands
+            // (the next loads into it are issued after the next top barrier)
+            rs::lds_barrier();
+            float *slot = reinterpret_cast<float *>(abuf(b)) + ((cg * S::NRG + rg) * 16) * 64;
             if (ks == 1) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) slot[i * 64 + lane] = acc0[i];
@@ -1185,7 +1188,7 @@ bool try_rs(lattice *L, const void *in, int C_in, const void *w, int C_out, cons
             hipError_t *err) {
     const int T = L->T;
     if (T == 11 && C_in == 64 && C_out == 64) *err = launch_ring<true, OUT_BF16, 11, 64, 64>(L, in, w, bias, out);
-    else if (T == 9 && C_in == 64 && C_out == 64) *err = launch_rs<true, OUT_BF16, 9, 64, 64, 1>(L, in, w, bias, out);
+    else if (T == 9 && C_in == 64 && C_out == 64) *err = launch_rs<true, OUT_BF16, 9, 64, 64, 2>(L, in, w, bias, out);
     else if (T == 9 && C_in == 64 && C_out == 128) *err = launch_rs<true, OUT_BF16, 9, 64, 128, 1>(L, in, w, bias, out);
     else if (T == 9 && C_in == 128 && C_out == 128) *err = launch_rs<true, OUT_BF16, 9, 128, 128, 1>(L, in, w, bias, out);
     else if (T == 11 && C_in == 64 && C_out == 128) *err = launch_rs<true, OUT_BF16, 11, 64, 128, 1>(L, in, w, bias, out);
