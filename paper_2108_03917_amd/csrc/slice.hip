@@ -48,39 +48,62 @@ __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, c
     for (int64_t p0 = wave * ppw; p0 < m; p0 += nwaves * ppw) {
         const int64_t p = p0 + grp;
         if (p >= m) continue;
+        // A point whose insertion failed (the splat reports it) has vertex -1
+        // in some slots: those read another of its rows with weight 0, and a
+        // point with none reads nothing.  The d+1 row loads are unconditional
+        // so that they are all in flight together (with a branch per vertex
+        // the compiler issued them one round trip at a time).
         int v[DP1];
         float b[DP1];
+        int fb = -1;
 #pragma unroll
         for (int k = 0; k < DP1; ++k) {
             v[k] = idx[p * DP1 + k];
             b[k] = bary[p * DP1 + k];
-            if (NORM && v[k] >= 0) {
-                const float w = vweight[v[k]];
-                b[k] = w != 0.f ? b[k] / w : 0.f;
-            }
+            fb = v[k] >= 0 ? v[k] : fb;
+        }
+        const bool any = fb >= 0;
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            b[k] = v[k] >= 0 ? b[k] : 0.f;
+            v[k] = v[k] >= 0 ? v[k] : (any ? fb : 0);
+        }
+        if (NORM && any) {
+            float wv[DP1];
+#pragma unroll
+            for (int k = 0; k < DP1; ++k) wv[k] = vweight[v[k]];
+#pragma unroll
+            for (int k = 0; k < DP1; ++k) b[k] = wv[k] != 0.f ? b[k] / wv[k] : 0.f;
         }
         if (VEC) {
             const int C4 = C >> 2;
             float4 *out4 = reinterpret_cast<float4 *>(out) + p * C4;
             for (int c = j; c < C4; c += G) {
                 float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (any) {
+                    float4 y[DP1];
 #pragma unroll
-                for (int k = 0; k < DP1; ++k) {
-                    if (v[k] < 0) continue;
-                    const float4 y = load4<IN_BF16>(values, (int64_t)v[k] * C4 + c);
-                    acc.x = fmaf(b[k], y.x, acc.x);
-                    acc.y = fmaf(b[k], y.y, acc.y);
-                    acc.z = fmaf(b[k], y.z, acc.z);
-                    acc.w = fmaf(b[k], y.w, acc.w);
+                    for (int k = 0; k < DP1; ++k) y[k] = load4<IN_BF16>(values, (int64_t)v[k] * C4 + c);
+#pragma unroll
+                    for (int k = 0; k < DP1; ++k) {
+                        acc.x = fmaf(b[k], y[k].x, acc.x);
+                        acc.y = fmaf(b[k], y[k].y, acc.y);
+                        acc.z = fmaf(b[k], y[k].z, acc.z);
+                        acc.w = fmaf(b[k], y[k].w, acc.w);
+                    }
                 }
                 out4[c] = acc;
             }
         } else {
             for (int c = j; c < C; c += G) {
                 float acc = 0.f;
+                if (any) {
+                    float y[DP1];
 #pragma unroll
-                for (int k = 0; k < DP1; ++k)
-                    if (v[k] >= 0) acc = fmaf(b[k], load1<IN_BF16>(values, (int64_t)v[k] * C + c), acc);
+                    for (int k = 0; k < DP1; ++k) y[k] = load1<IN_BF16>(values, (int64_t)v[k] * C + c);
+#pragma unroll
+                    for (int k = 0; k < DP1; ++k) acc = fmaf(b[k], y[k], acc);
+                }
                 out[p * C + c] = acc;
             }
         }
