@@ -48,7 +48,10 @@ constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
 constexpr int kW1 = 16, kW2 = 32, kW3 = 64;  // block widths (the paper's figure)
 constexpr int kMaxK0 = 16;                   // d + f_d, zero-padded to 16
-constexpr int kYStride = 64 + 1;             // LDS row of one channel: 64 entries + 1 (bank offset)
+// LDS row of one output channel: 64 entries + 4 (16-byte aligned rows; the
+// 16 lanes of a quarter-wave reading 16 bytes each then cover all 64 banks,
+// and the MFMA output writes of the four lane quarters fall 16 banks apart)
+constexpr int kYStride = 64 + 4;
 
 __device__ __forceinline__ float relu(float x) { return x > 0.f ? x : 0.f; }
 
@@ -251,9 +254,7 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
                                                      const float *__restrict__ mu,
                                                      const int32_t *__restrict__ counters,
                                                      unsigned int *__restrict__ keys, void *__restrict__ out) {
-    __shared__ float ysh[kWaves][kW3 * kYStride];  // outputs [64 channels][64 entries]; first the staged inputs
-    __shared__ int32_t vsh[kWaves][64];
-    __shared__ int32_t fsh[kWaves][64];
+    __shared__ __attribute__((aligned(16))) float ysh[kWaves][kW3 * kYStride];  // outputs [64 channels][64 entries]; first the staged inputs
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, j16 = lane & 15;
@@ -353,8 +354,7 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         }
         // destination of the run: the output row, or the key row of the
         // chunk where the vertex's list starts
-        vsh[w][lane] = (flags & 4) ? v : (valid ? (int)(cur.off >> 6) : -1);
-        fsh[w][lane] = flags;
+        const int dest = (flags & 4) ? v : (valid ? (int)(cur.off >> 6) : -1);
 
         // r_0 = relu(a_0 h_0 + s_0), h_0 = [g_p - mu_v ; f_p] zero-padded, staged in LDS
 #pragma unroll
@@ -396,21 +396,28 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         }
         wave_sync();
 
-        // lane c: running max of channel c over each run of the wavefront's entries
+        // lane c: running max of channel c over each run of the wavefront's
+        // entries, four entries per LDS read; an entry's run flags and
+        // destination come from its lane (readlane: scalar values, so the
+        // store at a run's end is a uniform branch)
         {
             const int c = lane;
             float mx = 0.f;
-#pragma unroll 8
-            for (int jj = 0; jj < 64; ++jj) {
-                const int vj = vsh[w][jj];
-                const int fj = fsh[w][jj];
-                const float y = Y[c * kYStride + jj];
-                mx = (fj & 1) ? y : fmaxf(mx, y);
-                if (vj >= 0 && (fj & 2)) {
-                    if (fj & 4)
-                        store_out<OUT_BF16>(out, vj, c, mx);
-                    else
-                        atomicMax(keys + (int64_t)vj * kW3 + c, max_key(mx));
+#pragma unroll
+            for (int j4 = 0; j4 < 16; ++j4) {
+                const f32x4_t y4 = *reinterpret_cast<const f32x4_t *>(Y + c * kYStride + 4 * j4);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int jj = 4 * j4 + i;
+                    const int fj = __builtin_amdgcn_readlane(flags, jj);
+                    mx = (fj & 1) ? y4[i] : fmaxf(mx, y4[i]);
+                    if (fj & 2) {
+                        const int vj = __builtin_amdgcn_readlane(dest, jj);
+                        if (fj & 4)
+                            store_out<OUT_BF16>(out, vj, c, mx);
+                        else
+                            atomicMax(keys + (int64_t)vj * kW3 + c, max_key(mx));
+                    }
                 }
             }
         }
