@@ -1099,9 +1099,12 @@ hipError_t launch_mfma_n(lattice *L, const void *in, int C_in, const void *w, in
     constexpr int P = CM == 1 ? 2 : 3;
     // fp32: 64 x 64 tiles, four workgroups per CU (the fp32 MFMA is slow enough
     // that four waves per SIMD keep it busy; small tiles shorten the tail)
-    if (CM == 0) return launch_mfma<CM, OUT_BF16, 64, 64, 32, 32, 2>(L, in, C_in, w, C_out, bias, out);
-    if (C_out % 128 == 0) return launch_mfma<CM, OUT_BF16, 128, 128, 64, 64, P>(L, in, C_in, w, C_out, bias, out);
-    return launch_mfma<CM, OUT_BF16, 128, 64, 32, 64, P>(L, in, C_in, w, C_out, bias, out);
+    if constexpr (CM == 0) {
+        return launch_mfma<CM, OUT_BF16, 64, 64, 32, 32, 2>(L, in, C_in, w, C_out, bias, out);
+    } else {
+        if (C_out % 128 == 0) return launch_mfma<CM, OUT_BF16, 128, 128, 64, 64, P>(L, in, C_in, w, C_out, bias, out);
+        return launch_mfma<CM, OUT_BF16, 128, 64, 32, 64, P>(L, in, C_in, w, C_out, bias, out);
+    }
 }
 
 template <bool IN_BF16, bool BF16, bool OUT_BF16>
