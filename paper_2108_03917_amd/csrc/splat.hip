@@ -10,10 +10,10 @@
 //                   (point, vertex) pair from the slot's counter
 //   k_scan_count/assign  vertex indices (in order of creation) and pair-list ranges
 //   k_fill          per pair: slot -> vertex index, (p, b_pk) into the list
+//   k_gather_parts  the parts (kPart pairs) of long pair lists, as partial rows
 //   k_gather        per vertex: x_v = sum b_pv f_p and w_v = sum b_pv
-//                   (optionally x_v / w_v), each row written once; long pair
-//                   lists are summed in parts of kPart pairs
-//   k_gather_combine  per long list: the sum of its part rows
+//                   (optionally x_v / w_v), each row written once; a long
+//                   list's row is the sum of its part rows
 #include "internal.h"
 #include "keys.h"
 
@@ -676,6 +676,25 @@ __device__ __forceinline__ void sum_pairs(const int2 *__restrict__ L2, int e0, i
     }
 }
 
+// The same, with the next block's list loads issued together with this
+// block's row loads (one round trip per block instead of two; for the
+// 32-entry parts of long lists).
+template <bool VEC, int BLK>
+__device__ __forceinline__ void sum_pairs_ahead(const int2 *__restrict__ L2, int e0, int e1,
+                                                const float *__restrict__ feat, int CV, int c, float4 &acc,
+                                                float &w) {
+    if (e0 >= e1) return;
+    int2 q[BLK];
+    load_block<BLK>(L2, e0, e1, q);
+    for (int e = e0; e < e1; e += BLK) {
+        int2 qn[BLK];
+        load_block<BLK>(L2, e + BLK, e1, qn);  // past e1: re-reads entry e1 - 1, unused
+        add_block<VEC, BLK>(q, e1 - e, feat, CV, c, acc, w);
+#pragma unroll
+        for (int i = 0; i < BLK; ++i) q[i] = qn[i];
+    }
+}
+
 template <bool VEC>
 __device__ __forceinline__ float4 scale4(float4 a, float w, int normalize) {
     if (!normalize) return a;
@@ -690,24 +709,25 @@ __device__ __forceinline__ float4 scale4(float4 a, float w, int normalize) {
 
 // Eq. (splat), pulled per vertex: x_v = sum over the vertex's pair list of
 // b_pv f_p, and w_v = sum b_pv.  Work units are groups of G lanes, each lane
-// owning float4 (VEC) or single column chunks.
-//   Phase 1: a vertex with at most kPart pairs is one unit: its row is summed
-//            and written once (no zero fill, no float atomics).
-//   Phase 2: a longer list is cut into parts of kPart pairs, one unit each,
-//            so that dense regions (thousands of points on one vertex near a
-//            LiDAR sensor) do not serialise on one group.  A part writes its
-//            partial row (and partial weight) to scratch; k_gather_combine
-//            adds them in part order.  (Combining in the last part to finish
-//            would need a device-scope release per part, which costs more
-//            than the extra launch: every XCD has its own L2.)
-template <bool VEC, bool OUT_BF16>
-__global__ __launch_bounds__(kBlock, 8) void k_gather(const int32_t *__restrict__ vinfo, const int32_t *__restrict__ list,
-                                                   const int32_t *__restrict__ split,
-                                                   const int32_t *__restrict__ rowmap, float *__restrict__ partial,
-                                                   float *__restrict__ pweight, const float *__restrict__ feat,
-                                                   int C, int log2G, int normalize, void *__restrict__ values,
-                                                   float *__restrict__ weight, const int32_t *counters) {
-    const int64_t V = counters[CNT_V];
+// owning float4 (VEC) or single column chunks.  Two kernels:
+//   k_gather_parts  a list longer than kPart pairs is cut into parts of kPart
+//                   pairs, one unit each, so that dense regions (thousands of
+//                   points on one vertex near a LiDAR sensor) do not
+//                   serialise on one group; a part writes its partial row
+//                   (and partial weight) to scratch.
+//   k_gather        a vertex with at most kPart pairs is one unit: its row is
+//                   summed and written once (no zero fill, no float atomics);
+//                   then the split vertices: their parts added in part order.
+// (Combining in the last part to finish would need a device-scope release
+// per part, which costs more than a launch: every XCD has its own L2.)
+template <bool VEC>
+__global__ __launch_bounds__(kBlock) void k_gather_parts(const int32_t *__restrict__ vinfo,
+                                                         const int32_t *__restrict__ list,
+                                                         const int32_t *__restrict__ split,
+                                                         const int32_t *__restrict__ rowmap,
+                                                         float *__restrict__ partial, float *__restrict__ pweight,
+                                                         const float *__restrict__ feat, int C, int log2G,
+                                                         const int32_t *counters) {
     const int64_t nrows = counters[CNT_ROWS];
     const int G = 1 << log2G;
     const int lane = threadIdx.x & 63;
@@ -718,11 +738,59 @@ __global__ __launch_bounds__(kBlock, 8) void k_gather(const int32_t *__restrict_
     const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
     const int CV = VEC ? (C >> 2) : C;
     const int2 *L2 = reinterpret_cast<const int2 *>(list);
+    for (int64_t u0 = wave * gpw; u0 < nrows; u0 += nwaves * gpw) {
+        const int64_t u = u0 + grp;
+        if (u >= nrows) continue;
+        const int sp = rowmap[u];
+        const int vv = split[3 * sp];
+        const int row0 = split[3 * sp + 1];
+        const int off = vinfo[2 * vv];
+        const int cnt = vinfo[2 * vv + 1];
+        const int part = (int)(u - row0);
+        const int e0 = off + part * kPart;
+        const int e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
+        float w = 0.f;
+        for (int c = j; c < CV; c += G) {
+            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+            w = 0.f;
+            sum_pairs_ahead<VEC, 4>(L2, e0, e1, feat, CV, c, acc, w);
+            if (VEC)
+                reinterpret_cast<float4 *>(partial)[u * CV + c] = acc;
+            else
+                partial[u * C + c] = acc.x;
+        }
+        if (j == 0) {
+            if (CV == 0) {
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                sum_pairs<false, 4>(L2, e0, e1, feat, 0, 0, acc, w);
+            }
+            pweight[u] = w;
+        }
+    }
+}
 
-    // Phase 1: short lists.  The list header of the group's next vertex is
-    // loaded while this one is summed (two header registers, so that the
-    // wait for one header is not a wait for the other).  With C = 0
-    // (weights only) lane 0 of the group sums the weights alone.
+template <bool VEC, bool OUT_BF16>
+__global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ vinfo, const int32_t *__restrict__ list,
+                                                   const int32_t *__restrict__ split, const float *__restrict__ partial,
+                                                   const float *__restrict__ pweight, const float *__restrict__ feat,
+                                                   int C, int log2G, int normalize, void *__restrict__ values,
+                                                   float *__restrict__ weight, const int32_t *counters) {
+    const int64_t V = counters[CNT_V];
+    const int64_t ns = counters[CNT_SPLIT];
+    const int G = 1 << log2G;
+    const int lane = threadIdx.x & 63;
+    const int grp = lane >> log2G;
+    const int j = lane & (G - 1);
+    const int gpw = 64 >> log2G;  // groups per wave
+    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
+    const int CV = VEC ? (C >> 2) : C;
+    const int2 *L2 = reinterpret_cast<const int2 *>(list);
+
+    // Short lists.  The list header of the group's next vertex is loaded
+    // while this one is summed (two header registers, so that the wait for
+    // one header is not a wait for the other).  With C = 0 (weights only)
+    // lane 0 of the group sums the weights alone.
     const int2 *VI = reinterpret_cast<const int2 *>(vinfo);
     const int64_t vstep = nwaves * gpw;
     auto header = [&](int64_t v) { return v < V ? VI[v] : make_int2(0, kPart + 1); };
@@ -748,83 +816,55 @@ __global__ __launch_bounds__(kBlock, 8) void k_gather(const int32_t *__restrict_
             weight[v] = w;
         }
     };
-    int64_t v = wave * gpw + grp;
-    int2 ha = header(v);
-    for (; v - grp < V; v += 2 * vstep) {
-        const int2 hb = header(v + vstep);
-        short_list(v, ha);
-        if (v - grp + vstep >= V) break;
-        ha = header(v + 2 * vstep);
-        short_list(v + vstep, hb);
-    }
-
-    // Phase 2: parts of long lists.
-    for (int64_t u0 = wave * gpw; u0 < nrows; u0 += nwaves * gpw) {
-        const int64_t u = u0 + grp;
-        const bool live = u < nrows;
-        if (live) {
-            const int sp = rowmap[u];
-            const int vv = split[3 * sp];
-            const int row0 = split[3 * sp + 1];
-            const int off = vinfo[2 * vv];
-            const int cnt = vinfo[2 * vv + 1];
-            const int part = (int)(u - row0);
-            const int e0 = off + part * kPart;
-            const int e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
-            float w = 0.f;
-            for (int c = j; c < CV; c += G) {
-                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                w = 0.f;
-                sum_pairs<VEC, 4>(L2, e0, e1, feat, CV, c, acc, w);
-                if (VEC)
-                    reinterpret_cast<float4 *>(partial)[u * CV + c] = acc;
-                else
-                    partial[u * C + c] = acc.x;
-            }
-            if (j == 0) {
-                if (CV == 0) {
-                    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                    sum_pairs<false, 4>(L2, e0, e1, feat, 0, 0, acc, w);
-                }
-                pweight[u] = w;
-            }
+    {
+        int64_t v = wave * gpw + grp;
+        int2 ha = header(v);
+        for (; v - grp < V; v += 2 * vstep) {
+            const int2 hb = header(v + vstep);
+            short_list(v, ha);
+            if (v - grp + vstep >= V) break;
+            ha = header(v + 2 * vstep);
+            short_list(v + vstep, hb);
         }
     }
-}
 
-// Rows of the vertices whose lists k_gather summed in parts: the parts are
-// added in part order, then scaled and stored like a phase-1 row.
-template <bool VEC, bool OUT_BF16>
-__global__ __launch_bounds__(kBlock) void k_gather_combine(const int32_t *__restrict__ split, const float *partial,
-                                                           const float *pweight, int C, int log2G, int normalize,
-                                                           void *__restrict__ values, float *__restrict__ weight,
-                                                           const int32_t *counters) {
-    const int64_t ns = counters[CNT_SPLIT];
-    const int G = 1 << log2G;
-    const int lane = threadIdx.x & 63;
-    const int grp = lane >> log2G;
-    const int j = lane & (G - 1);
-    const int gpw = 64 >> log2G;
-    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
-    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
-    const int CV = VEC ? (C >> 2) : C;
+    // Split vertices: the part rows added in part order, four per block
+    // with all loads of a block in flight (a list of thousands of pairs has
+    // dozens of parts); rows past the last part re-read it and are not
+    // added.  Then scaled and stored like a short list's row.
+    constexpr int kB = 4;
     for (int64_t s0 = wave * gpw; s0 < ns; s0 += nwaves * gpw) {
         const int64_t sp = s0 + grp;
         if (sp >= ns) continue;
         const int v = split[3 * sp], row0 = split[3 * sp + 1], parts = split[3 * sp + 2];
+        const int rlast = row0 + parts - 1;
         float w = 0.f;
-        for (int r = 0; r < parts; ++r) w += pweight[row0 + r];
+        for (int r0 = 0; r0 < parts; r0 += kB) {
+            float pw[kB];
+#pragma unroll
+            for (int i = 0; i < kB; ++i) pw[i] = pweight[row0 + r0 + i < rlast ? row0 + r0 + i : rlast];
+#pragma unroll
+            for (int i = 0; i < kB; ++i) w += r0 + i < parts ? pw[i] : 0.f;
+        }
         for (int c = j; c < CV; c += G) {
             float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
-            for (int r = 0; r < parts; ++r) {
-                if (VEC) {
-                    const float4 a = reinterpret_cast<const float4 *>(partial)[(int64_t)(row0 + r) * CV + c];
-                    t.x += a.x;
-                    t.y += a.y;
-                    t.z += a.z;
-                    t.w += a.w;
-                } else {
-                    t.x += partial[(int64_t)(row0 + r) * C + c];
+            for (int r0 = 0; r0 < parts; r0 += kB) {
+                float4 a[kB];
+#pragma unroll
+                for (int i = 0; i < kB; ++i) {
+                    const int64_t row = row0 + r0 + i < rlast ? row0 + r0 + i : rlast;
+                    if (VEC)
+                        a[i] = reinterpret_cast<const float4 *>(partial)[row * CV + c];
+                    else
+                        a[i] = make_float4(partial[row * C + c], 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+                for (int i = 0; i < kB; ++i) {
+                    const bool ok = r0 + i < parts;
+                    t.x += ok ? a[i].x : 0.f;
+                    t.y += ok ? a[i].y : 0.f;
+                    t.z += ok ? a[i].z : 0.f;
+                    t.w += ok ? a[i].w : 0.f;
                 }
             }
             t = scale4<VEC>(t, w, normalize);
@@ -955,25 +995,24 @@ static hipError_t gather_typed(lattice *L, const float *feat, int C, int normali
     int log2G = 0;
     while ((1 << log2G) < lanes && log2G < 6) ++log2G;
     const int64_t gpw = 64 >> log2G;
+    // the parts of long lists first: the second kernel adds them
+    const unsigned g1 = grid_for((split_rows_max(L) + gpw - 1) / gpw * 64, kBlock, L->cu_count, 16);
+    if (vec)
+        hipLaunchKernelGGL((k_gather_parts<true>), dim3(g1), dim3(kBlock), 0, L->stream, L->vinfo, L->list, L->split,
+                           L->rowmap, L->partial, L->pweight, feat, C, log2G, L->counters);
+    else
+        hipLaunchKernelGGL((k_gather_parts<false>), dim3(g1), dim3(kBlock), 0, L->stream, L->vinfo, L->list, L->split,
+                           L->rowmap, L->partial, L->pweight, feat, C, log2G, L->counters);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     const int64_t waves = (L->max_vertices + gpw - 1) / gpw;
     const unsigned grid = grid_for(waves * 64, kBlock, L->cu_count, 16);
     if (vec)
         hipLaunchKernelGGL((k_gather<true, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
-                           L->split, L->rowmap, L->partial, L->pweight, feat, C, log2G, normalize, values,
-                           weight, L->counters);
+                           L->split, L->partial, L->pweight, feat, C, log2G, normalize, values, weight, L->counters);
     else
         hipLaunchKernelGGL((k_gather<false, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
-                           L->split, L->rowmap, L->partial, L->pweight, feat, C, log2G, normalize, values,
-                           weight, L->counters);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const unsigned g2 = grid_for(split_rows_max(L) * 64, kBlock, L->cu_count, 2);
-    if (vec)
-        hipLaunchKernelGGL((k_gather_combine<true, OUT_BF16>), dim3(g2), dim3(kBlock), 0, L->stream, L->split,
-                           L->partial, L->pweight, C, log2G, normalize, values, weight, L->counters);
-    else
-        hipLaunchKernelGGL((k_gather_combine<false, OUT_BF16>), dim3(g2), dim3(kBlock), 0, L->stream, L->split,
-                           L->partial, L->pweight, C, log2G, normalize, values, weight, L->counters);
+                           L->split, L->partial, L->pweight, feat, C, log2G, normalize, values, weight, L->counters);
     return hipGetLastError();
 }
 
