@@ -21,10 +21,10 @@
 //                    vertex in fp64 (a segmented scan over shuffles); a run
 //                    that is the vertex's whole list writes mu_v, otherwise
 //                    the run is added to the vertex's fp64 sum atomically
-//   k_mean_finish    mu_v of the lists that cross a 64-entry chunk
-//   k_pointnet_rows  the key of -inf in the key row of each vertex whose
-//                    list crosses a 64-entry chunk boundary (and, after
-//                    k_pointnet, those keys decoded into the output rows)
+//   k_pointnet_prep  mu_v of the lists that cross a 64-entry chunk; the key
+//                    of -inf in the key row of each vertex whose list crosses
+//                    a chunk boundary; the parameters in the padded layout
+//                    (three independent jobs in one launch)
 //   k_pointnet       the three blocks as fp32 MFMA products over the
 //                    wavefront's 64 entries (weight fragments held in
 //                    registers); block 3's outputs go to LDS channel-major;
@@ -146,12 +146,14 @@ __global__ __launch_bounds__(kBlock) void k_local_mean(const int32_t *__restrict
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_mean_finish(const int32_t *__restrict__ vinfo,
-                                                        const double *__restrict__ macc, int d,
-                                                        const int32_t *__restrict__ counters, float *__restrict__ mu) {
+// The bodies below take their block index and block count, so that one
+// launch (k_pointnet_prep) can run several of them side by side.
+__device__ __forceinline__ void mean_finish(int64_t bid, int64_t nblk, const int32_t *__restrict__ vinfo,
+                                            const double *__restrict__ macc, int d,
+                                            const int32_t *__restrict__ counters, float *__restrict__ mu) {
     const int64_t V = counters[CNT_V];
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < V; v += stride) {
+    const int64_t stride = nblk * kBlock;
+    for (int64_t v = bid * kBlock + threadIdx.x; v < V; v += stride) {
         const int off = vinfo[2 * v], cnt = vinfo[2 * v + 1];
         if (in_one_chunk(off, cnt)) continue;
         for (int i = 0; i < d; ++i) mu[v * d + i] = (float)(macc[v * d + i] / cnt);
@@ -172,14 +174,14 @@ __device__ __forceinline__ void store_out(void *out, int64_t v, int c, float x) 
 // mode 1 decodes it into the vertex's output row.  A long list crosses
 // several boundaries; only its first crossing does the work.
 template <bool OUT_BF16>
-__global__ __launch_bounds__(kBlock) void k_pointnet_rows(const int32_t *__restrict__ lvert,
-                                                          const int32_t *__restrict__ vinfo,
-                                                          const int32_t *__restrict__ counters, int mode,
-                                                          unsigned int *__restrict__ keys, void *__restrict__ out) {
+__device__ __forceinline__ void pointnet_rows(int64_t bid, int64_t nblk, const int32_t *__restrict__ lvert,
+                                              const int32_t *__restrict__ vinfo,
+                                              const int32_t *__restrict__ counters, int mode,
+                                              unsigned int *__restrict__ keys, void *__restrict__ out) {
     const int64_t E = counters[CNT_E];
     const int64_t nb = E > 0 ? (E - 1) / 64 : 0;  // boundaries 64, 128, ... below E
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < nb * kW3; q += stride) {
+    const int64_t stride = nblk * kBlock;
+    for (int64_t q = bid * kBlock + threadIdx.x; q < nb * kW3; q += stride) {
         const int64_t j = q / kW3;
         const int64_t e0 = (j + 1) * 64;
         const int c = (int)(q % kW3);
@@ -201,9 +203,9 @@ constexpr int kA1 = kB0 + kW1, kS1 = kA1 + kW1, kWt1 = kS1 + kW1, kB1 = kWt1 + k
 constexpr int kA2 = kB1 + kW2, kS2 = kA2 + kW2, kWt2 = kS2 + kW2, kB2 = kWt2 + kW3 * kW2;
 constexpr int kPadded = kB2 + kW3;
 
-__global__ __launch_bounds__(kBlock) void k_pack_pointnet(const float *__restrict__ params, int k0,
-                                                          float *__restrict__ padded) {
-    for (int i = blockIdx.x * kBlock + threadIdx.x; i < kPadded; i += gridDim.x * kBlock) {
+__device__ __forceinline__ void pack_pointnet(int64_t bid, int64_t nblk, const float *__restrict__ params, int k0,
+                                              float *__restrict__ padded) {
+    for (int64_t i = bid * kBlock + threadIdx.x; i < kPadded; i += nblk * kBlock) {
         float x = 0.f;
         if (i < kS0) {
             if (i - kA0 < k0) x = params[i - kA0];
@@ -217,6 +219,36 @@ __global__ __launch_bounds__(kBlock) void k_pack_pointnet(const float *__restric
         }
         padded[i] = x;
     }
+}
+
+// After the local means: mu_v of the crossing lists, the key rows set to
+// -inf, and the parameters packed, in one launch (block ranges nb_mean,
+// nb_rows, nb_pack).
+__global__ __launch_bounds__(kBlock) void k_pointnet_prep(const int32_t *__restrict__ vinfo,
+                                                          const double *__restrict__ macc, int d,
+                                                          const int32_t *__restrict__ counters,
+                                                          float *__restrict__ mu,
+                                                          const int32_t *__restrict__ lvert,
+                                                          unsigned int *__restrict__ keys,
+                                                          const float *__restrict__ params, int k0,
+                                                          float *__restrict__ padded, int nb_mean, int nb_rows,
+                                                          int nb_pack) {
+    const int b = blockIdx.x;
+    if (b < nb_mean)
+        mean_finish(b, nb_mean, vinfo, macc, d, counters, mu);
+    else if (b < nb_mean + nb_rows)
+        pointnet_rows<false>(b - nb_mean, nb_rows, lvert, vinfo, counters, 0, keys, nullptr);
+    else
+        pack_pointnet(b - nb_mean - nb_rows, nb_pack, params, k0, padded);
+}
+
+// After the PointNet: the crossing lists' keys decoded into their rows.
+template <bool OUT_BF16>
+__global__ __launch_bounds__(kBlock) void k_pointnet_rows(const int32_t *__restrict__ lvert,
+                                                          const int32_t *__restrict__ vinfo,
+                                                          const int32_t *__restrict__ counters,
+                                                          unsigned int *__restrict__ keys, void *__restrict__ out) {
+    pointnet_rows<OUT_BF16>(blockIdx.x, gridDim.x, lvert, vinfo, counters, 1, keys, out);
 }
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -465,22 +497,18 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
             return hipErrorInvalidValue;
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_mean_finish, dim3(g_v), dim3(kBlock), 0, L->stream, L->vinfo, L->macc, d, L->counters, mu);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    auto rows = out_bf16 ? k_pointnet_rows<true> : k_pointnet_rows<false>;
     const unsigned g_i = grid_for((E / 64 + 1) * kW3, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 0, L->pn_keys,
-                       out);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_pack_pointnet, dim3((kPadded + kBlock - 1) / kBlock), dim3(kBlock), 0, L->stream, params,
-                       d + f_d, L->pn_params);
+    const unsigned g_k = (kPadded + kBlock - 1) / kBlock;
+    hipLaunchKernelGGL(k_pointnet_prep, dim3(g_v + g_i + g_k), dim3(kBlock), 0, L->stream, L->vinfo, L->macc, d,
+                       L->counters, mu, L->lvert, L->pn_keys, params, d + f_d, L->pn_params, (int)g_v, (int)g_i,
+                       (int)g_k);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned g_p = grid_for(E, kBlock, L->cu_count, 2);  // 69 KB of LDS: two workgroups per CU
     hipLaunchKernelGGL((out_bf16 ? k_pointnet<true> : k_pointnet<false>), dim3(g_p), dim3(kBlock), 0, L->stream,
                        L->list, L->lvert, L->vinfo, pos, feat, d, f_d, L->pn_params, mu, L->counters, L->pn_keys,
                        out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(rows, dim3(g_i), dim3(kBlock), 0, L->stream, L->lvert, L->vinfo, L->counters, 1, L->pn_keys,
-                       out);
+    hipLaunchKernelGGL((out_bf16 ? k_pointnet_rows<true> : k_pointnet_rows<false>), dim3(g_i), dim3(kBlock), 0,
+                       L->stream, L->lvert, L->vinfo, L->counters, L->pn_keys, out);
     return hipGetLastError();
 }
