@@ -71,8 +71,8 @@ def _clustered_cloud(seed, C, m_dense=6000, m_sparse=3000):
                                                       (128, "f32", True), (520, "f32", False), (0, "f32", False)])
 def test_splat_long_pair_lists(C, values_dtype, normalize):
     """Vertices with up to thousands of (point, vertex) pairs: their lists are
-    summed in parts and combined by the last part; the result must not depend
-    on that split.  Two splats in a row on one lattice (the second smaller)
+    summed in parts of 32 pairs and the parts added in order; the result must
+    not depend on that split.  Two splats in a row on one lattice (the second smaller)
     check that no per-split state leaks from the first."""
     sigma = 0.1
     L = _lattice(3, sigma, 9000)
