@@ -13,7 +13,10 @@ enum : int { ST_CAPACITY = 1, ST_RANGE = 2 };
 // Slots of the device counter array.
 // CNT_SPLIT and CNT_ROWS count the vertices whose pair list the splat gather
 // cuts into parts, and those parts.
-enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_SPLIT = 3, CNT_ROWS = 4, CNT_WORDS = 8 };
+// CNT_SLOTS is the number of hash slots the last numbering recorded in
+// vslot (every occupied slot of the table, one per vertex), which the next
+// splat empties instead of the whole table.
+enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_SPLIT = 3, CNT_ROWS = 4, CNT_SLOTS = 5, CNT_WORDS = 8 };
 
 // A vertex's pair list longer than kPart pairs is cut into parts of kPart
 // pairs (the splat's gather work units, also used by the distribute op); the
@@ -58,6 +61,8 @@ struct lattice {
 
     HEntry *tab = nullptr;      // [cap] hash table {key, pair count, vertex index}
     uint64_t *vkeys = nullptr;  // [max_vertices] packed key of each vertex
+    int32_t *vslot = nullptr;   // [max_vertices] hash slot of each vertex (what the next splat empties)
+    bool full_clear = true;     // the table may hold keys vslot does not list: empty all of it
     int32_t *blk = nullptr;     // [scan_blocks_max()][4] per-block sums of the numbering scan
     int32_t *vinfo = nullptr;   // [max_vertices][2] (offset, count) of the vertex's pair list
     // Long pair lists are gathered in parts (splat.hip); at most

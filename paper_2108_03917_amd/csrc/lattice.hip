@@ -42,6 +42,7 @@ int64_t next_pow2(int64_t x) {
 void free_all(lattice *L) {
     (void)hipFree(L->tab);
     (void)hipFree(L->vkeys);
+    (void)hipFree(L->vslot);
     (void)hipFree(L->blk);
     (void)hipFree(L->split);
     (void)hipFree(L->rowmap);
@@ -232,6 +233,7 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
     const int dp1 = d + 1;
     bool ok = hipMalloc(&L->tab, L->cap * 16) == hipSuccess &&
               hipMalloc(&L->vkeys, L->max_vertices * sizeof(uint64_t)) == hipSuccess &&
+              hipMalloc(&L->vslot, L->max_vertices * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->blk, scan_blocks_max() * 4 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->split, split_rows_max(L) * 3 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->rowmap, split_rows_max(L) * sizeof(int32_t)) == hipSuccess &&
@@ -312,7 +314,10 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
     if (s) return s;
     hipEvent_t t0;
     if ((s = timer_begin(L, LATTICE_STAGE_SPLAT, &t0))) return s;
+    // The slots to empty are those the last splat listed; until this splat's
+    // launches have all gone out, the next one empties the whole table.
     if ((s = check_launch(L, launch_clear_table(L), "clear_table"))) return s;
+    L->full_clear = true;
     if ((s = check_launch(L, launch_insert(L, pos, batch, m), "insert"))) return s;
     if ((s = check_launch(L, launch_number(L, m), "number"))) return s;
     if ((s = check_launch(L, launch_fill(L, m), "fill"))) return s;
@@ -320,6 +325,7 @@ lattice_status lattice_splat(lattice *L, const float *pos, const int32_t *batch,
         if ((s = check_launch(L, launch_gather(L, feat, C, normalize, values, values_dtype, weight), "gather")))
             return s;
     if ((s = timer_end(L, LATTICE_STAGE_SPLAT, t0))) return s;
+    L->full_clear = false;
     L->m = m;
     L->gen += 1;
     L->splatted = true;

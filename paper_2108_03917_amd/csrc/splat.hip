@@ -3,7 +3,10 @@
 // barycentric accumulation of Eq. (splat).
 //
 // Kernel sequence of one lattice_splat (all on the lattice's stream):
-//   k_clear_table   empty the hash table, zero V, the pair count and the status
+//   k_clear_slots   empty the slots the last splat occupied (its vertices'
+//                   slots), zero V, the pair count and the status; the first
+//                   splat (and one after a failed launch) empties the whole
+//                   table instead (k_clear_table)
 //   k_insert        one thread per point: elevate, round, rank, wrap, weights,
 //                   keys; CAS-insert of the d+1 keys (runs of equal keys in
 //                   neighbouring lanes are inserted once), a rank for every
@@ -399,6 +402,21 @@ __global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap
     if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS) counters[threadIdx.x] = 0;
 }
 
+// The table after a completed splat: its occupied slots are exactly the
+// vertices' slots (a slot is taken only by the pair that creates a vertex),
+// listed in vslot[0 .. counters[CNT_SLOTS]).  Empty those, and zero every
+// counter but CNT_SLOTS (which every thread reads; the next numbering
+// rewrites it).
+__global__ __launch_bounds__(kBlock) void k_clear_slots(HEntry *tab, const int32_t *__restrict__ vslot,
+                                                        int32_t *counters) {
+    const int64_t n = counters[CNT_SLOTS];
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    uint4 *t4 = reinterpret_cast<uint4 *>(tab);
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
+        t4[vslot[i]] = make_uint4(0, 0, 0, 0);
+    if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS && threadIdx.x != CNT_SLOTS) counters[threadIdx.x] = 0;
+}
+
 // Vertex numbering and pair-list layout by a two-pass scan over the
 // (point, remainder) pairs in point order, of the pairs that created their
 // vertex: vertices are numbered in the order their first point appears, so
@@ -497,7 +515,8 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
                                                         int nb, HEntry *__restrict__ tab,
                                                         const int4 *__restrict__ blk, uint64_t *__restrict__ vkeys,
                                                         int32_t *__restrict__ vinfo, int32_t *__restrict__ split,
-                                                        int32_t *__restrict__ rowmap, int32_t *counters) {
+                                                        int32_t *__restrict__ rowmap, int32_t *__restrict__ vslot,
+                                                        int32_t *counters) {
     __shared__ int4 red[kBlock / 64];
     __shared__ int4 wsum[kBlock / 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -510,6 +529,7 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
     if ((int)blockIdx.x == nb - 1 && threadIdx.x == 0) {
         const int4 tot = add4(carry, blk[blockIdx.x]);
         counters[CNT_V] = tot.x;
+        counters[CNT_SLOTS] = tot.x;
         counters[CNT_E] = tot.y;
         counters[CNT_SPLIT] = tot.z;
         counters[CNT_ROWS] = tot.w;
@@ -550,6 +570,7 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
             if (q[i].x) {
                 const int v = at.x;
                 tab[sl[i]].vid = v;
+                vslot[v] = sl[i];
                 vkeys[v] = e[i].key;
                 vinfo[2 * v] = at.y;
                 vinfo[2 * v + 1] = q[i].y;
@@ -919,8 +940,13 @@ hipError_t dispatch_d(int d, F &&f) {
 }  // namespace
 
 hipError_t launch_clear_table(lattice *L) {
-    const unsigned grid = grid_for(L->cap, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->counters);
+    if (L->full_clear) {
+        const unsigned grid = grid_for(L->cap, kBlock, L->cu_count, 4);
+        hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->counters);
+    } else {
+        const unsigned grid = grid_for(L->max_vertices, kBlock, L->cu_count, 4);
+        hipLaunchKernelGGL(k_clear_slots, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->vslot, L->counters);
+    }
     return hipGetLastError();
 }
 
@@ -966,7 +992,7 @@ hipError_t launch_number(lattice *L, int64_t m) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan_assign, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->idx, n, span, (int)nb,
-                       L->tab, blk, L->vkeys, L->vinfo, L->split, L->rowmap, L->counters);
+                       L->tab, blk, L->vkeys, L->vinfo, L->split, L->rowmap, L->vslot, L->counters);
     return hipGetLastError();
 }
 
