@@ -3,10 +3,10 @@
 // barycentric accumulation of Eq. (splat).
 //
 // Kernel sequence of one lattice_splat (all on the lattice's stream):
-//   k_clear_slots   empty the slots the last splat occupied (its vertices'
-//                   slots), zero V, the pair count and the status; the first
-//                   splat (and one after a failed launch) empties the whole
-//                   table instead (k_clear_table)
+//   k_clear_table   empty the table: the slots the last splat occupied (its
+//                   vertices' slots) when they are few, else all of it (and
+//                   always all of it on the first splat or after a failed
+//                   launch); zero V, the pair count and the status
 //   k_insert        one thread per point: elevate, round, rank, wrap, weights,
 //                   keys; CAS-insert of the d+1 keys (runs of equal keys in
 //                   neighbouring lanes are inserted once), a rank for every
@@ -395,26 +395,29 @@ __global__ __launch_bounds__(NB) void k_insert_shared(const float *__restrict__ 
     if (status) atomicOr(counters + CNT_STATUS, status);
 }
 
-__global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap, int32_t *counters) {
+// Empty the hash table before a splat and zero the counters.  After a
+// completed splat the occupied slots are exactly the vertices' slots (a slot
+// is taken only by the pair that creates a vertex), listed in
+// vslot[0 .. n), n = counters[CNT_SLOTS].  A scattered 16-byte store costs
+// about a whole 128-byte line, so those n slots are emptied one by one when
+// 8n < cap, and the whole table is written otherwise.  `whole` (the first
+// splat, or one after a failed launch, when the table may hold keys vslot
+// does not list) always writes the whole table and zeroes every counter;
+// otherwise CNT_SLOTS, which every thread reads, is left for the next
+// numbering to rewrite.
+__global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap, const int32_t *__restrict__ vslot,
+                                                        int32_t *counters, int whole) {
+    const int64_t tid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     uint4 *t4 = reinterpret_cast<uint4 *>(tab);
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < cap; i += stride) t4[i] = make_uint4(0, 0, 0, 0);
-    if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS) counters[threadIdx.x] = 0;
-}
-
-// The table after a completed splat: its occupied slots are exactly the
-// vertices' slots (a slot is taken only by the pair that creates a vertex),
-// listed in vslot[0 .. counters[CNT_SLOTS]).  Empty those, and zero every
-// counter but CNT_SLOTS (which every thread reads; the next numbering
-// rewrites it).
-__global__ __launch_bounds__(kBlock) void k_clear_slots(HEntry *tab, const int32_t *__restrict__ vslot,
-                                                        int32_t *counters) {
-    const int64_t n = counters[CNT_SLOTS];
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    uint4 *t4 = reinterpret_cast<uint4 *>(tab);
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
-        t4[vslot[i]] = make_uint4(0, 0, 0, 0);
-    if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS && threadIdx.x != CNT_SLOTS) counters[threadIdx.x] = 0;
+    const uint4 zero = make_uint4(0, 0, 0, 0);
+    const int64_t n = whole ? cap : counters[CNT_SLOTS];
+    if (whole || 8 * n >= cap) {
+        for (int64_t i = tid; i < cap; i += stride) t4[i] = zero;
+    } else {
+        for (int64_t i = tid; i < n; i += stride) t4[vslot[i]] = zero;
+    }
+    if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS && (whole || threadIdx.x != CNT_SLOTS)) counters[threadIdx.x] = 0;
 }
 
 // Vertex numbering and pair-list layout by a two-pass scan over the
@@ -940,13 +943,9 @@ hipError_t dispatch_d(int d, F &&f) {
 }  // namespace
 
 hipError_t launch_clear_table(lattice *L) {
-    if (L->full_clear) {
-        const unsigned grid = grid_for(L->cap, kBlock, L->cu_count, 4);
-        hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->counters);
-    } else {
-        const unsigned grid = grid_for(L->max_vertices, kBlock, L->cu_count, 4);
-        hipLaunchKernelGGL(k_clear_slots, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->vslot, L->counters);
-    }
+    const unsigned grid = grid_for(L->cap, kBlock, L->cu_count, 4);
+    hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->vslot, L->counters,
+                       L->full_clear ? 1 : 0);
     return hipGetLastError();
 }
 
