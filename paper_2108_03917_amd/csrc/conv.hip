@@ -789,17 +789,19 @@ __global__ __launch_bounds__(256, (RsShape<BF16, C_IN, C_OUT, T, KS>::WPE)) void
 // LDS.  A slice is MT rows x C_in channels; each wavefront issues DPS
 // direct-to-LDS loads per slice.  At the top of slice j (tile i, tap t):
 //   wait until slices j .. j+PD are in LDS, barrier (slot of j-1 is free)
-//   t = 0: store tile i-1, clear the accumulators, and load the neighbour
-//   block of tile i+2
+//   t = 0: store tile i-1 and clear the accumulators
+//   t = 1: load the neighbour block of tile i+2 into tile i's buffer, whose
+//   last reads (the indices of tap T-1, at t = 0) the barrier has retired
+//   in every wavefront
 //   read the operands of slice j+PD; MFMAs of slice j, with the loads of
 //   slice j+T-1 (tap t-1 of tile i+1; for t = 0 the last tap of tile i)
 //   into the freed slot issued between them.
 // The wait is a vmcnt bound: loads complete in issue order, so "at most N
 // loads newer than slice j+PD outstanding" means j+PD has landed; N counts
 // the DMA groups issued after it (and the neighbour-block load where that
-// is newer: for 1 <= t < T-1-PD).  Stores are not counted: a store still in flight only makes the
-// wait longer.  Loads past the last tile read the zero row so that every
-// wavefront issues the same number of loads per slice.
+// is newer: for 2 <= t <= T-1-PD).  Stores are not counted: a store still
+// in flight only makes the wait longer.  Loads past the last tile read the
+// zero row so that every wavefront issues the same number of loads per slice.
 //
 // fp32: a lane's 16-byte chunk (2g + h) of a row holds channels 8g + 4h + i,
 // i = 0..3, the k = h operand of MFMA 32x32x2 number i of the group; the
@@ -972,7 +974,7 @@ __global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_,
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             // wait for slices j .. j+PD (see above), then the barrier
-            if (t >= 1 && t < T - 1 - S::PD)
+            if (t >= 2 && t <= T - 1 - S::PD)
                 rs::wait_vm_barrier<(T - 2 - S::PD) * S::DPS + 1>();
             else
                 rs::wait_vm_barrier<(T - 2 - S::PD) * S::DPS>();
@@ -984,8 +986,8 @@ __global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_,
             if (t == 0) {
                 if (!first) store_tile(k - tstride);
                 first = false;
-                load_nbr(k + 2 * tstride, b);
             }
+            if (t == 1) load_nbr(k + 2 * tstride, b);
             if (k == tile0 && t == 0) {
 #pragma unroll
                 for (int p = 0; p < S::PD; ++p) read_slice(p, p);
