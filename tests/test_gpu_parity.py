@@ -486,40 +486,45 @@ def test_resplat_sequence():
     the hash table, one after the other on one lattice: every splat that fits
     matches the oracle (keys, simplices, values, neighbours), whatever the
     splats before it left in the lattice's buffers.  The table is emptied
-    slot by slot after a splat of n vertices with 8n < capacity, and whole
-    otherwise (and after a failed splat); the sequence takes both ways."""
+    slot by slot after a splat of n vertices with 8n < capacity; otherwise,
+    and after a failed splat, it is emptied whole.  The sequence takes both
+    ways, on a small table and on a large one."""
     from paper_2108_03917_amd import LatticeError
     from paper_2108_03917_amd.lattice import E_CAPACITY
 
-    L = _lattice(3, 0.1, 5000, hash_capacity=16384)
-    cap = L.hash_capacity
     ways = set()
-    prev = None  # vertices of the splat before, None after a failed one
+
+    def run(L, clouds):
+        cap = L.hash_capacity
+        prev = None  # vertices of the splat before, None after a failed one
+        for i, w in enumerate(clouds):
+            if i > 0:
+                ways.add("slots" if prev is not None and 8 * prev < cap else "whole")
+            if w is None:
+                L.splat(torch.zeros((0, 3), device=dev()), torch.zeros((0, 4), device=dev()))
+                assert L.num_vertices() == 0, i
+                continue  # an empty splat leaves the list of occupied slots as it was
+            if w == "overflow":   # 5000 points spread thinly: more than 16384 vertices
+                big = random_cloud(5000, 3, seed=34, extent=40.0, C=4)
+                L.splat(to_dev(big.pos), to_dev(big.feat))
+                with pytest.raises(LatticeError) as ei:
+                    L.num_vertices()
+                assert ei.value.status == E_CAPACITY
+                prev = None
+                continue
+            g = GpuLattice(L, w.pos, w.feat)
+            lat = O.build(w.pos, 0.1)
+            check_lattice(g, lat)
+            ref, wref, scale = O.splat(lat, w.feat)
+            assert_close_scaled(g.values(), ref, scale, REL_F32, f"splat {i}")
+            assert np.array_equal(g.neighbors(), O.neighbors(lat)), i
+            prev = lat.V
+
     clouds = [random_cloud(5000, 3, seed=30, extent=1.0, C=4), random_cloud(1200, 3, seed=31, extent=0.5, C=4),
               None, random_cloud(3000, 3, seed=32, extent=2.0, C=4), "overflow",
               random_cloud(5000, 3, seed=30, extent=1.0, C=4), random_cloud(700, 3, seed=33, extent=1.0, C=4)]
-    for i, w in enumerate(clouds):
-        if i > 0:
-            ways.add("slots" if prev is not None and 8 * prev < cap else "whole")
-        if w is None:
-            L.splat(torch.zeros((0, 3), device=dev()), torch.zeros((0, 4), device=dev()))
-            assert L.num_vertices() == 0, i
-            continue  # an empty splat leaves the list of occupied slots as it was
-        if w == "overflow":   # 5000 points spread thinly: more than 16384 vertices
-            big = random_cloud(5000, 3, seed=34, extent=40.0, C=4)
-            L.splat(to_dev(big.pos), to_dev(big.feat))
-            with pytest.raises(LatticeError) as ei:
-                L.num_vertices()
-            assert ei.value.status == E_CAPACITY
-            prev = None
-            continue
-        g = GpuLattice(L, w.pos, w.feat)
-        lat = O.build(w.pos, 0.1)
-        check_lattice(g, lat)
-        ref, wref, scale = O.splat(lat, w.feat)
-        assert_close_scaled(g.values(), ref, scale, REL_F32, f"splat {i}")
-        assert np.array_equal(g.neighbors(), O.neighbors(lat)), i
-        prev = lat.V
+    run(_lattice(3, 0.1, 5000, hash_capacity=16384), clouds)
+    run(_lattice(3, 0.1, 5000, hash_capacity=1 << 19), [c for c in clouds if not isinstance(c, str)])
     assert ways == {"slots", "whole"}, ways
 
 
