@@ -424,3 +424,20 @@ def pointnet_weights(k0: int, d: int, sigma: float, seed: int, widths=POINTNET_W
         out.append((a, s, W, b))
         k = w_out
     return out
+
+
+def pointnet_gn_weights(k0: int, seed: int, widths=POINTNET_WIDTHS):
+    """Seeded PointNet parameters with group normalisation: a list of
+    (gamma, beta, W, b) per block, float32.  gamma ~ 1 + N(0, 0.1^2), beta ~
+    N(0, 0.1^2) per input channel, W ~ N(0, 2/K) (He), b ~ N(0, 0.01^2)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    k = k0
+    for w_out in widths:
+        gamma = (1.0 + 0.1 * rng.standard_normal(k)).astype(np.float32)
+        beta = (0.1 * rng.standard_normal(k)).astype(np.float32)
+        W = (rng.standard_normal((w_out, k)) * np.sqrt(2.0 / k)).astype(np.float32)
+        b = (0.01 * rng.standard_normal(w_out)).astype(np.float32)
+        out.append((gamma, beta, W, b))
+        k = w_out
+    return out

@@ -43,6 +43,11 @@ Readings of the paper taken here (the paper is silent on them):
 * Conv weight layout [C_out][T][C_in]: y_v[o] = sum_t sum_i x_{nbr(v,t)}[i] W[o,t,i].
 * Batched clouds are independent lattices; canonical vertex order is
   ascending (batch, c_0, .., c_{d-1}).
+* Distribute + PointNet: each block normalises its input rows with a group
+  normalisation (Sec. "Implementation": 32 groups by default) whose
+  statistics are taken over all the rows of one cloud (one batch id); with
+  fewer than 32 channels, or a count that 32 does not divide, the group count
+  is the largest divisor of the channel count not above 32.
 
 Parity unpinned: alpha, the rounding-tie rule and the rank-tie rule are
 conventions that the paper does not fix; both sides adopt the ones above.
@@ -563,14 +568,55 @@ def local_mean(lat: Lattice, pos: np.ndarray) -> np.ndarray:
     return s / n[:, None]
 
 
-def distribute_pointnet(lat: Lattice, pos: np.ndarray, feat: Optional[np.ndarray], layers):
-    """Distribute + PointNet + per-vertex max, float64.
+def default_groups(K: int, max_groups: int = 32) -> int:
+    """Group count of a group normalisation over K channels: the default of 32
+    groups (Sec. "Implementation"), reduced, where K is smaller than 32 or not
+    a multiple of it, to the largest divisor of K that is at most 32 (the
+    groups must split the channels evenly).  Below 32 channels every channel
+    is then its own group."""
+    return max(g for g in range(1, min(max_groups, K) + 1) if K % g == 0)
 
-    ``layers`` is a list of (a, s, W, b) with W [w_l, K_l]; K_0 = d + f_d.
-    Returns (out [V, w_L], scale [V, w_L], mu [V, d]).  ``scale`` bounds the
-    rounding of a float32 evaluation: per row, the magnitudes |g_p| + |mu_v|
-    and |f_p| carried through |a|, |s|, |W|, |b| (ReLU is 1-Lipschitz), and
-    the max over the vertex's rows."""
+
+def group_norm(h: np.ndarray, seg: np.ndarray, groups: int, gamma, beta, eps: float = 1e-5):
+    """Group normalisation (Wu and He, the method Sec. "Implementation" cites),
+    float64, of rows h [N, K] that belong to samples seg [N].
+
+    The K channels are cut into ``groups`` groups of K / groups consecutive
+    channels.  Within one sample (here one cloud, the rows of one batch id),
+    each group is centred by its mean and divided by sqrt(var + eps), the mean
+    and the variance (the biased one, dividing by the count) taken over every
+    row of the sample and every channel of the group; then channel c is
+    scaled by gamma_c and shifted by beta_c.
+
+    Returns (out [N, K], mean [S, groups], var [S, groups], samples [S]) with
+    the samples in ascending order."""
+    h = np.asarray(h, dtype=np.float64)
+    N, K = h.shape
+    assert K % groups == 0, (K, groups)
+    gamma = np.asarray(gamma, dtype=np.float64)
+    beta = np.asarray(beta, dtype=np.float64)
+    samples = np.unique(seg)
+    out = np.empty_like(h)
+    means = np.zeros((len(samples), groups))
+    varis = np.zeros((len(samples), groups))
+    for i, s in enumerate(samples):
+        rows = seg == s
+        x = h[rows].reshape(-1, groups, K // groups)
+        mu = x.mean(axis=(0, 2))
+        var = ((x - mu[None, :, None]) ** 2).mean(axis=(0, 2))
+        xn = (x - mu[None, :, None]) / np.sqrt(var + eps)[None, :, None]
+        out[rows] = xn.reshape(-1, K) * gamma + beta
+        means[i], varis[i] = mu, var
+    return out, means, varis, samples
+
+
+def distribute_rows(lat: Lattice, pos: np.ndarray, feat: Optional[np.ndarray]):
+    """The distributed rows of Eq. (distribute), float64: one row per pair
+    (point p, vertex v of p's simplex), h_0 = [g_p - mu_v ; f_p].
+
+    Returns (h0 [E, d + f_d], v [E], p [E], seg [E], mu [V, d]) where seg is
+    the cloud of each row (its vertex's batch id, 0 for an unbatched lattice),
+    plus the magnitudes |g_p| + |mu_v|, |f_p| of the row's terms [E, d + f_d]."""
     g = np.asarray(pos, dtype=np.float64)
     m, dp1 = lat.idx.shape
     mu = local_mean(lat, pos)
@@ -584,13 +630,50 @@ def distribute_pointnet(lat: Lattice, pos: np.ndarray, feat: Optional[np.ndarray
         sc = np.concatenate([sg, np.abs(f)], axis=1)
     else:
         h, sc = dg, sg
-    for a, s, W, b in layers:
+    seg = lat.vbatch[v] if lat.vbatch is not None else np.zeros(len(v), dtype=np.int64)
+    return h, v, p, seg, mu, sc
+
+
+def distribute_pointnet(lat: Lattice, pos: np.ndarray, feat: Optional[np.ndarray], layers, groups=None,
+                        eps: float = 1e-5):
+    """Distribute + PointNet + per-vertex max, float64.
+
+    Each block of the PointNet (the network figure) is a normalisation, a
+    ReLU and a fully connected 1x1 layer: h_l = W_l relu(N_l(h_{l-1})) + b_l;
+    then x_v is the channel-wise max over the rows of v.
+
+    * ``groups`` given (one group count per block): N_l is the group
+      normalisation of ``group_norm`` over all the rows of one cloud (per
+      batch id), and ``layers`` holds (gamma, beta, W, b) per block.
+    * ``groups`` None: N_l is the fixed per-channel affine a h + s (a
+      normalisation whose statistics are already folded in), and ``layers``
+      holds (a, s, W, b).
+
+    W is [w_l, K_l]; K_0 = d + f_d.  Returns (out [V, w_L], scale [V, w_L],
+    mu [V, d]).  ``scale`` bounds the rounding of a float32 evaluation: per
+    row, the magnitudes |g_p| + |mu_v| and |f_p| carried through each block
+    (the normalisation as |a| (|h| + |mean|) + |beta| with a = gamma /
+    sqrt(var + eps); ReLU is 1-Lipschitz; then |W|, |b|), and the max over
+    the vertex's rows."""
+    h, v, p, seg, mu, sc = distribute_rows(lat, pos, feat)
+    for li, (a, s, W, b) in enumerate(layers):
         a = np.asarray(a, dtype=np.float64)
         s = np.asarray(s, dtype=np.float64)
         W = np.asarray(W, dtype=np.float64)
         b = np.asarray(b, dtype=np.float64)
-        h = np.maximum(a * h + s, 0.0) @ W.T + b
-        sc = (np.abs(a) * sc + np.abs(s)) @ np.abs(W).T + np.abs(b)
+        if groups is None:
+            hn = a * h + s
+            scn = np.abs(a) * sc + np.abs(s)
+        else:
+            G = groups[li]
+            hn, means, varis, samples = group_norm(h, seg, G, a, s, eps)
+            K = h.shape[1]
+            row = np.searchsorted(samples, seg)
+            gmean = np.repeat(means, K // G, axis=1)[row]               # [E, K] the group's mean
+            ga = a / np.sqrt(np.repeat(varis, K // G, axis=1)[row] + eps)
+            scn = np.abs(ga) * (sc + np.abs(gmean)) + np.abs(s)
+        h = np.maximum(hn, 0.0) @ W.T + b
+        sc = scn @ np.abs(W).T + np.abs(b)
     out = np.full((lat.V, h.shape[1]), -np.inf)
     np.maximum.at(out, v, h)
     scale = np.zeros_like(out)

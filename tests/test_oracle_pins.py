@@ -796,3 +796,158 @@ def test_distribute_pointnet_is_point_permutation_invariant():
     out2, _, _ = O.distribute_pointnet(lat2, w.pos[perm], w.feat[perm], layers)
     assert np.array_equal(lat.keys, lat2.keys)
     assert np.allclose(out, out2, rtol=1e-12, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# Group normalisation in the PointNet of Distribute (Sec. "Implementation":
+# every convolution is pre-activated by a group normalisation of 32 groups
+# and a ReLU; the network figure's PointNet block is GN, ReLU, 1x1, three
+# times, then the max-pool)
+# --------------------------------------------------------------------------
+
+def test_default_groups_are_the_largest_divisor_up_to_32():
+    assert [O.default_groups(k) for k in (1, 4, 9, 16, 32, 48, 64, 96, 128)] == [1, 4, 9, 16, 32, 24, 32, 32, 32]
+
+
+@pytest.mark.parametrize("K,groups", [(8, 1), (8, 2), (8, 8), (9, 3), (9, 9), (32, 32), (64, 32)])
+def test_group_norm_matches_torch(K, groups):
+    """torch.nn.functional.group_norm (float64, CPU) on each sample's rows,
+    laid out as one [1, K, N] sample."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(K * 100 + groups)
+    N = 500
+    h = rng.normal(size=(N, K)) * rng.uniform(0.1, 5.0, size=K) + rng.normal(size=K) * 3
+    seg = rng.integers(0, 3, size=N) * 7          # three samples with ids 0, 7, 14
+    gamma, beta = rng.normal(size=K), rng.normal(size=K)
+    out, means, varis, samples = O.group_norm(h, seg, groups, gamma, beta, eps=1e-5)
+    assert list(samples) == [0, 7, 14]
+    for i, s in enumerate(samples):
+        x = torch.from_numpy(h[seg == s].T.copy())[None]
+        ref = torch.nn.functional.group_norm(x, groups, torch.from_numpy(gamma), torch.from_numpy(beta), eps=1e-5)
+        assert np.allclose(out[seg == s], ref[0].numpy().T, rtol=1e-12, atol=1e-12)
+        xg = x[0].reshape(groups, -1)
+        assert np.allclose(means[i], xg.mean(dim=1).numpy(), rtol=1e-12, atol=1e-12)
+        assert np.allclose(varis[i], xg.var(dim=1, unbiased=False).numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_group_norm_standardises_each_group_and_ignores_its_affine():
+    """With gamma = 1, beta = 0 and eps = 0 every (sample, group) comes out
+    with mean 0 and variance 1, and scaling a (sample, group) by a positive
+    factor and shifting it by a constant changes nothing."""
+    rng = np.random.default_rng(5)
+    N, K, G = 400, 12, 4
+    h = rng.normal(size=(N, K)) * 2 + 1
+    seg = (np.arange(N) >= 150).astype(np.int64)
+    out, _, _, _ = O.group_norm(h, seg, G, np.ones(K), np.zeros(K), eps=0.0)
+    for s in (0, 1):
+        for g in range(G):
+            x = out[seg == s][:, g * 3:(g + 1) * 3]
+            assert abs(x.mean()) < 1e-12 and abs(x.var() - 1.0) < 1e-12
+    h2 = h.copy()
+    for s in (0, 1):
+        for g in range(G):
+            a, c = rng.uniform(0.5, 4.0), rng.normal() * 10
+            rows = seg == s
+            h2[np.ix_(rows, range(g * 3, (g + 1) * 3))] = a * h[np.ix_(rows, range(g * 3, (g + 1) * 3))] + c
+    out2, _, _, _ = O.group_norm(h2, seg, G, np.ones(K), np.zeros(K), eps=0.0)
+    assert np.allclose(out, out2, rtol=1e-10, atol=1e-10)
+
+
+def test_distribute_pointnet_gn_worked_example_d1():
+    """Three points in d = 1 (alpha = sigma = 1, vertices at g = k sqrt 2),
+    worked by hand.  g = 0.3 and 0.7 fall in the cell of keys (0,0), (1,-1);
+    g = 2.0 in the cell of (1,-1), (2,-2).  Local means: 0.5, 1.0, 2.0.
+    Rows (offset, f) with f = (1, -1, 0): v0 (-0.2, 1), (0.2, -1); v1
+    (-0.7, 1), (-0.3, -1), (1.0, 0); v2 (0.0, 0).  One block: GN with two
+    groups (one channel each), gamma = 1, beta = 0, eps = 0; ReLU; W = I,
+    b = 0.  Over all six rows the offsets have mean 0 (they sum to zero per
+    vertex) and variance 1.66 / 6, so they divide by sqrt(0.27667) =
+    0.525991; the features have mean 0 and variance 4 / 6, so they divide by
+    0.816497.  The max per vertex: v0 (0.2 / 0.525991, 1 / 0.816497) =
+    (0.380235, 1.224745); v1 (1.0 / 0.525991, 1.224745) = (1.901173,
+    1.224745); v2 (0, 0).  Statistics per vertex instead of per cloud would
+    give v0 (1, 1) and no answer at v2 (zero variance)."""
+    g = np.array([[0.3], [0.7], [2.0]], dtype=np.float32)
+    f = np.array([[1.0], [-1.0], [0.0]], dtype=np.float32)
+    lat = O.build(g, 1.0, alpha=1.0)
+    assert [tuple(k) for k in lat.keys] == [(0, 0), (1, -1), (2, -2)]
+    layer = (np.ones(2), np.zeros(2), np.eye(2), np.zeros(2))
+    out, scale, mu = O.distribute_pointnet(lat, g, f, [layer], groups=[2], eps=0.0)
+    assert np.allclose(mu.ravel(), [0.5, 1.0, 2.0], atol=1e-7)
+    assert np.allclose(out, [[0.380235, 1.224745], [1.901173, 1.224745], [0.0, 0.0]], atol=2e-6)
+    assert np.all(scale >= np.abs(out))
+
+
+def _torch_pointnet_gn(torch, lat, pos, feat, layers, groups, eps):
+    """The same network from torch primitives (float64, CPU): index_reduce
+    'mean' for the local mean, group_norm per cloud, F.linear, index_reduce
+    'amax' for the per-vertex max."""
+    m, dp1 = lat.idx.shape
+    v = torch.from_numpy(lat.idx.ravel())
+    p = torch.arange(m).repeat_interleave(dp1)
+    g = torch.from_numpy(pos.astype(np.float64))
+    tmu = torch.zeros((lat.V, pos.shape[1]), dtype=torch.float64).index_reduce_(0, v, g[p], "mean",
+                                                                               include_self=False)
+    h = torch.cat([g[p] - tmu[v], torch.from_numpy(feat.astype(np.float64))[p]], dim=1)
+    seg = torch.from_numpy(lat.vbatch)[v] if lat.vbatch is not None else torch.zeros(len(v), dtype=torch.int64)
+    for (ga, be, W, b), G in zip(layers, groups):
+        hn = torch.empty_like(h)
+        for s in torch.unique(seg):
+            rows = seg == s
+            hn[rows] = torch.nn.functional.group_norm(h[rows].T[None], G, torch.from_numpy(ga.astype(np.float64)),
+                                                      torch.from_numpy(be.astype(np.float64)), eps=eps)[0].T
+        h = torch.nn.functional.linear(torch.relu(hn), torch.from_numpy(W.astype(np.float64)),
+                                       torch.from_numpy(b.astype(np.float64)))
+    return torch.zeros((lat.V, h.shape[1]), dtype=torch.float64).index_reduce_(0, v, h, "amax", include_self=False)
+
+
+@pytest.mark.parametrize("n_batch", [0, 3])
+def test_distribute_pointnet_gn_matches_torch(n_batch):
+    torch = pytest.importorskip("torch")
+    from datagen.clouds import pointnet_gn_weights
+
+    w, lat = _small_lattice(d=3, m=3000, seed=85, C=5, n_batch=n_batch)
+    layers = pointnet_gn_weights(3 + 5, seed=86)
+    groups = [O.default_groups(k) for k in (8, 16, 32)]
+    out, _, _ = O.distribute_pointnet(lat, w.pos, w.feat, layers, groups=groups, eps=1e-5)
+    ref = _torch_pointnet_gn(torch, lat, w.pos, w.feat, layers, groups, 1e-5)
+    assert np.allclose(out, ref.numpy(), rtol=1e-10, atol=1e-10)
+    # coarser groups than the default (block 1: one group of all 8 channels)
+    out2, _, _ = O.distribute_pointnet(lat, w.pos, w.feat, layers, groups=[1, 4, 8], eps=1e-5)
+    ref2 = _torch_pointnet_gn(torch, lat, w.pos, w.feat, layers, [1, 4, 8], 1e-5)
+    assert np.allclose(out2, ref2.numpy(), rtol=1e-10, atol=1e-10)
+    assert not np.allclose(out, out2, rtol=1e-3, atol=1e-3)
+
+
+def test_distribute_pointnet_gn_statistics_are_per_cloud():
+    """A batched lattice normalises each batch id over its own rows: the
+    output equals the clouds run one by one, and a cloud whose positions are
+    shifted and whose features are scaled and shifted (each feature channel
+    is its own group in block 1) gives the same output as the original."""
+    from datagen.clouds import pointnet_gn_weights
+
+    w = random_cloud(1200, 3, 87, extent=1.0, C=3)
+    pos2 = (w.pos + np.float32(3.0)).astype(np.float32)
+    feat2 = (w.feat * np.float32(8.0) - np.float32(5.0)).astype(np.float32)
+    layers = pointnet_gn_weights(3 + 3, seed=88)
+    groups = [O.default_groups(k) for k in (6, 16, 32)]
+    lat1 = O.build(w.pos, 0.15)
+    out1, _, _ = O.distribute_pointnet(lat1, w.pos, w.feat, layers, groups=groups, eps=0.0)
+    pos = np.concatenate([w.pos, pos2])
+    feat = np.concatenate([w.feat, feat2])
+    batch = np.repeat(np.array([0, 1], dtype=np.int32), w.m)
+    latb = O.build(pos, 0.15, batch=batch)
+    outb, _, _ = O.distribute_pointnet(latb, pos, feat, layers, groups=groups, eps=0.0)
+    lat2 = O.build(pos2, 0.15)
+    out2, _, _ = O.distribute_pointnet(lat2, pos2, feat2, layers, groups=groups, eps=0.0)
+    assert np.allclose(outb[latb.vbatch == 0], out1, rtol=1e-9, atol=1e-9)
+    assert np.allclose(outb[latb.vbatch == 1], out2, rtol=1e-9, atol=1e-9)
+    # The shifted cloud has its own lattice (the shift is not a lattice
+    # translation), so compare the block-1 normalisation of its feature
+    # channels, which does not depend on the vertex set: the same values, to
+    # the float32 rounding of 8 f - 5.
+    h1, _, _, seg1, _, _ = O.distribute_rows(lat1, w.pos, w.feat)
+    h2, _, _, seg2, _, _ = O.distribute_rows(lat2, pos2, feat2)
+    n1, _, _, _ = O.group_norm(h1[:, 3:], seg1, 3, np.ones(3), np.zeros(3), eps=0.0)
+    n2, _, _, _ = O.group_norm(h2[:, 3:], seg2, 3, np.ones(3), np.zeros(3), eps=0.0)
+    assert np.allclose(np.sort(n1, axis=0), np.sort(n2, axis=0), rtol=1e-6, atol=1e-6)
