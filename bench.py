@@ -8,6 +8,10 @@ feeds the next), and slice the last output back onto the points.  The inputs
 conv is bf16) are resident in HBM before the timed region; every step
 rebuilds the lattice from scratch.
 
+The default workload is the largest one: four LiDAR sweeps of a scene with
+moving boxes, 421 398 points in a d = 4 space-time lattice, one 64 -> 64 bf16
+conv with 11 taps.
+
 Prints one JSON line.  `value` is points per second of whole steps; the
 `roofline` object reports the step's slowest single-kernel stage (the
 neighbour search, a conv or the slice) against its own roofline, timed with
@@ -17,6 +21,11 @@ steps); `stages_cold` repeats that with the caches evicted before every step;
 `hbm_frac_splat_slice` is the splat and slice bytes over their time against
 peak HBM; `cpu_baseline` is the CPU oracle timed on this host on a bounded
 sample with all its BLAS threads, `cpu_baseline_1core` with one.
+`other_configs` repeats the plain step on the indoor room and the LiDAR scan
+(stages and rooflines), and `targets` sets the two performance goals against
+what was measured: splat + slice at 50% of peak HBM (on every workload timed),
+and the bf16 conv at C = 128 (the LiDAR scan's 128 -> 128) at 40% of peak bf16
+MFMA.  `roofline.traffic_source` says where the HBM traffic figure comes from.
 
 With --op deform the step ends in DeformSlice fused with the linear
 classifier (per-point logits, the network's output layer) instead of the
@@ -38,7 +47,7 @@ max (fused) turns the raw point features into the 64-channel vertex values
 the convs take (workloads whose first conv has 64 inputs).
 
 Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train|unet|pointnet]
-       [--no-cpu-baseline]
+       [--no-cpu-baseline] [--no-other-configs] [--no-cold]
 """
 from __future__ import annotations
 
@@ -54,7 +63,13 @@ if ROOT not in sys.path:
 
 import numpy as np  # noqa: E402
 
-DEFAULT_CONFIG = 2          # part-segmentation-shaped batch: 16 objects x 2500 points
+DEFAULT_CONFIG = 5          # the largest workload: four LiDAR sweeps in a d = 4 space-time lattice
+# Workloads whose stages are also timed in the default run (`other_configs`):
+# the indoor room (the largest d = 3 cloud) and the LiDAR scan (128 -> 128
+# bf16 conv, where the MFMA target is set).
+EXTRA_CONFIGS = (3, 4)
+TARGET_HBM_FRAC = 0.5       # splat + slice, algorithmic bytes over their time, of peak HBM
+TARGET_MFMA_FRAC = 0.4      # the bf16 lattice conv at C = 128 (LiDAR scan, 128 -> 128), of peak bf16 MFMA
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 # fp32 vector units: 256 CUs x 4 SIMDs x 2.4 GHz x 64 lanes x 2 flops (FMA) at
@@ -469,17 +484,26 @@ def source_hash(stage: str) -> str:
 
 def measured_traffic(workload: str, stage: str):
     """HBM bytes per launch of a stage from committed rocprofv3 counter runs
-    (FETCH_SIZE and WRITE_SIZE, each scaled by its copy-kernel calibration), or
-    None when there is no measurement or the kernel source has changed."""
+    (FETCH_SIZE and WRITE_SIZE, each scaled by its copy-kernel calibration),
+    with a note of where they come from; (None, reason) when there is no
+    measurement or the kernel source has changed since it was taken."""
+    rel = os.path.relpath(TRAFFIC_FILE, ROOT)
     if not os.path.exists(TRAFFIC_FILE):
-        return None
+        return None, f"no counter table ({rel})"
     with open(TRAFFIC_FILE) as fh:
         table = json.load(fh)
-    e = table.get("entries", {}).get(f"{workload}/{stage}")
-    if not e or e.get("source_sha1") != source_hash(stage):
-        return None
+    key = f"{workload}/{stage}"
+    e = table.get("entries", {}).get(key)
+    if not e:
+        return None, f"no counter run of this kernel in {rel}"
+    if e.get("source_sha1") != source_hash(stage):
+        return None, (f"{rel} entry {key} was measured on kernel source {e.get('source_sha1', '?')[:12]}, "
+                      f"the current source is {source_hash(stage)[:12]}")
     cal = table["calibration"]
-    return (e["fetch_kib"] * cal["fetch_scale"] + e["write_kib"] * cal["write_scale"]) * 1024.0
+    bytes_ = (e["fetch_kib"] * cal["fetch_scale"] + e["write_kib"] * cal["write_scale"]) * 1024.0
+    return bytes_, (f"{rel} entry {key}: a stored rocprofv3 --pmc run (FETCH_SIZE x {cal['fetch_scale']}, "
+                    f"WRITE_SIZE x {cal['write_scale']}, per dispatch) of the same command on kernel source "
+                    f"{e['source_sha1'][:12]}, not measured in this run")
 
 
 def calibrate_copy(mib: int):
@@ -495,6 +519,96 @@ def calibrate_copy(mib: int):
     print(json.dumps({"calibrate_copy_mib": mib}))
 
 
+def time_pipeline(pipe, steps, warmup, cold=True, graph=False):
+    """Warm up, then time `steps` whole steps (region 1), the same number
+    again with HIP events around every stage (region 2) and, with `cold`, up
+    to 50 steps with the caches evicted before each (region 3).  Returns the
+    seconds of region 1, V, and the per-stage millisecond samples of regions 2
+    and 3 (None without `cold`)."""
+    import torch
+
+    for _ in range(warmup):
+        pipe.run()
+    pipe.stream.synchronize()
+    V = pipe.L.num_vertices()
+
+    # Timed region 1: whole steps (eager, or graph replays with --graph).
+    step = pipe.run
+    if graph:
+        pipe.capture()
+        for _ in range(3):
+            pipe.replay()
+        step = pipe.replay
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+
+    # Timed region 2: the same steps run eagerly with HIP events recorded on
+    # the pipeline's stream around every stage (each conv and the slice are
+    # one kernel launch), for the per-stage times and the roofline.
+    names = pipe.stage_names()
+    nev = len(names) + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for s_ in range(steps):
+        pipe.run(evs[s_])
+    torch.cuda.synchronize()
+    samples = {n: [evs[s_][i].elapsed_time(evs[s_][i + 1]) for s_ in range(steps)] for i, n in enumerate(names)}
+
+    # Timed region 3 (cold): before every step a 512 MiB buffer is written
+    # (outside the events), which evicts the 256 MiB Infinity Cache and the
+    # L2s, so each stage starts from HBM as the first touch of a new cloud would.
+    cold_samples = None
+    if cold:
+        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda:0")
+        n_cold = min(steps, 50)
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(n_cold)]
+        torch.cuda.synchronize()
+        for s_ in range(n_cold):
+            with torch.cuda.stream(pipe.stream):
+                flush.fill_(float(s_))
+            pipe.run(cev[s_])
+        torch.cuda.synchronize()
+        cold_samples = {n: [cev[s_][i].elapsed_time(cev[s_][i + 1]) for s_ in range(n_cold)]
+                        for i, n in enumerate(names)}
+        del flush
+    return sec, V, samples, cold_samples
+
+
+def pct(v):
+    return {"p10": float(np.percentile(v, 10)), "median": float(np.median(v)), "p90": float(np.percentile(v, 90))}
+
+
+def splat_slice_frac(work, stage_ms):
+    """Splat + slice algorithmic bytes over their summed time, of peak HBM."""
+    return ((work["splat"]["bytes"] + work["slice"]["bytes"]) / ((stage_ms["splat"] + stage_ms["slice"]) * 1e-3)
+            / (HBM_PEAK_GBS * 1e9))
+
+
+def other_config(config, steps, warmup):
+    """The plain step (splat, neighbours, convs, slice) of another workload:
+    whole-step rate and every stage against its roofline (HIP events, mean and
+    percentiles over the steps; no cache eviction)."""
+    from datagen.clouds import make_workload
+
+    w = make_workload(config)
+    pipe = Pipeline(w, tail="slice")
+    sec, V, samples, _ = time_pipeline(pipe, steps, warmup, cold=False)
+    work = algorithmic_work(w, V)
+    stage_ms = {n: float(np.mean(v)) for n, v in samples.items()}
+    res = {"workload": WORKLOAD_NAMES[config], "points": w.m, "d": w.d, "vertices": V,
+           "value": w.m * steps / sec, "unit": "points/s", "ms_per_step": sec * 1e3 / steps,
+           "stages": {n: dict(ms=stage_ms[n], ms_pct=pct(samples[n]), **roofline_entry(n, stage_ms[n], work[n]))
+                      for n in samples},
+           "hbm_frac_splat_slice": splat_slice_frac(work, stage_ms)}
+    pipe.L.close()
+    del pipe
+    return res
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -507,6 +621,8 @@ def main(argv=None):
                          "Distribute + PointNet (pointnet)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-flushed stage timings")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the indoor and LiDAR steps timed after the main workload (and the targets)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--graph", action="store_true", help="time graph replays of the step instead of eager steps")
@@ -525,63 +641,14 @@ def main(argv=None):
 
     w = make_workload(args.config)
     pipe = Pipeline(w, tail=args.op)
-    for _ in range(args.warmup):
-        pipe.run()
-    pipe.stream.synchronize()
-    V = pipe.L.num_vertices()
-
-    # Timed region 1: whole steps (eager, or graph replays with --graph).
-    step = pipe.run
-    if args.graph:
-        pipe.capture()
-        for _ in range(3):
-            pipe.replay()
-        step = pipe.replay
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    sec = t1 - t0
-
-    # Timed region 2: the same steps run eagerly with HIP events recorded on
-    # the pipeline's stream around every stage (each conv and the slice are
-    # one kernel launch), for the per-stage times and the roofline.
+    sec, V, samples, cold = time_pipeline(pipe, args.steps, args.warmup, not args.no_cold, args.graph)
     names = pipe.stage_names()
-    nev = len(names) + 1
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for s_ in range(args.steps):
-        pipe.run(evs[s_])
-    torch.cuda.synchronize()
-    samples = {n: [evs[s_][i].elapsed_time(evs[s_][i + 1]) for s_ in range(args.steps)] for i, n in enumerate(names)}
     stage_ms = {n: float(np.mean(v)) for n, v in samples.items()}
-
-    # Timed region 3 (cold): before every step a 512 MiB buffer is written
-    # (outside the events), which evicts the 256 MiB Infinity Cache and the
-    # L2s, so each stage starts from HBM as the first touch of a new cloud would.
-    cold = None
-    if not args.no_cold:
-        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device="cuda:0")
-        n_cold = min(args.steps, 50)
-        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(n_cold)]
-        torch.cuda.synchronize()
-        for s_ in range(n_cold):
-            with torch.cuda.stream(pipe.stream):
-                flush.fill_(float(s_))
-            pipe.run(cev[s_])
-        torch.cuda.synchronize()
-        cold = {n: [cev[s_][i].elapsed_time(cev[s_][i + 1]) for s_ in range(n_cold)] for i, n in enumerate(names)}
-        del flush
 
     n_cls = pipe.w_cls.shape[0] if args.op == "deform" else 0
     Vc = pipe.Lc.num_vertices() if args.op == "unet" else 0
     f_raw = pipe.raw.shape[1] if args.op == "pointnet" else -1
     work = algorithmic_work(w, V, n_cls, Vc, f_raw)
-    def pct(v):
-        return {"p10": float(np.percentile(v, 10)), "median": float(np.median(v)), "p90": float(np.percentile(v, 90))}
-
     stages = {n: dict(ms=stage_ms[n], ms_pct=pct(samples[n]), **roofline_entry(n, stage_ms[n], work[n]))
               for n in names}
     if cold is not None:
@@ -597,7 +664,7 @@ def main(argv=None):
     rf = dict(stages[dominant])
     rf.pop("ms")
     rf["kernel"] = dominant
-    rf["traffic"] = measured_traffic(WORKLOAD_NAMES.get(args.config, w.name), dominant)
+    rf["traffic"], rf["traffic_source"] = measured_traffic(WORKLOAD_NAMES.get(args.config, w.name), dominant)
     rf["algorithmic_bytes"] = work[dominant]["bytes"]
     if "flops" in work[dominant]:
         rf["algorithmic_flops"] = work[dominant]["flops"]
@@ -630,9 +697,7 @@ def main(argv=None):
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
-        "hbm_frac_splat_slice": None if args.op in ("deform", "pointnet") else
-        (work["splat"]["bytes"] + work["slice"]["bytes"]) / ((stage_ms["splat"] + stage_ms["slice"]) * 1e-3)
-        / (HBM_PEAK_GBS * 1e9),
+        "hbm_frac_splat_slice": None if args.op in ("deform", "pointnet") else splat_slice_frac(work, stage_ms),
         "timing": ("value: " + ("graph replays" if args.graph else "eager steps") + " of the whole step, no "
                    "events inside; stages and roofline: HIP events around each stage of eager steps on the "
                    "same stream; stages_cold: the same after evicting the caches before every step "
@@ -640,6 +705,28 @@ def main(argv=None):
     }
     if cold is not None:
         out["stages_cold"] = stages_cold
+    if args.op == "slice" and not args.no_other_configs:
+        # the two performance targets, each on the workload it is set on
+        others = {str(c): other_config(c, min(args.steps, 20), min(args.warmup, 5))
+                  for c in EXTRA_CONFIGS if c != args.config}
+        out["other_configs"] = others
+        mine = {"workload": out["config"]["workload"], "stages": stages,
+                "hbm_frac_splat_slice": out["hbm_frac_splat_slice"]}
+        by_cfg = {str(args.config): mine, **others}
+        hb = {k: v["hbm_frac_splat_slice"] for k, v in by_cfg.items()}
+        tg = {"splat_slice_hbm_frac": {"target": TARGET_HBM_FRAC, "value": out["hbm_frac_splat_slice"],
+                                       "workload": out["config"]["workload"],
+                                       "met": out["hbm_frac_splat_slice"] >= TARGET_HBM_FRAC,
+                                       "by_workload": {by_cfg[k]["workload"]: v for k, v in hb.items()}}}
+        lidar = by_cfg.get("4")
+        if lidar is not None:
+            st = lidar["stages"]["conv0_128x128_bf16"]
+            tg["bf16_conv_c128_mfma_frac"] = {
+                "target": TARGET_MFMA_FRAC, "value": st["frac"], "bound": st["bound"],
+                "achieved_tflops": st["achieved"], "peak_tflops": st["peak"], "ms": st["ms"],
+                "kernel": "conv0_128x128_bf16", "workload": lidar["workload"],
+                "met": st["bound"] == "mfma" and st["frac"] >= TARGET_MFMA_FRAC}
+        out["targets"] = tg
     if not args.no_cpu_baseline and args.op in ("train", "unet", "pointnet"):
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, None, train=args.op == "train",
                                            unet=args.op == "unet",
