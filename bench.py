@@ -44,7 +44,8 @@ slices that: one level of the paper's U-Net.
 With --op pointnet the network's input layer replaces the splat of the
 features: the step builds the lattice, then Distribute + PointNet + per-vertex
 max (fused) turns the raw point features into the 64-channel vertex values
-the convs take (workloads whose first conv has 64 inputs).
+the convs take (workloads whose first conv has 64 inputs); each PointNet block
+starts with a group normalisation whose statistics are computed per cloud.
 
 Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train|unet|pointnet]
        [--no-cpu-baseline] [--no-other-configs] [--no-cold]
@@ -137,14 +138,17 @@ class Pipeline:
         else:
             self.sliced = torch.empty((w.m, c_last), dtype=torch.float32, device=dev)
         if tail == "pointnet":
-            from datagen.clouds import pointnet_weights, raw_point_features
+            from datagen.clouds import pointnet_gn_weights, raw_point_features
 
             if not self.convs or self.convs[0].c_in != 64:
                 raise SystemExit("--op pointnet needs a workload whose first conv takes the PointNet's 64 channels "
                                  "(workloads 2, 3, 5)")
             raw = raw_point_features(w)
             self.raw = torch.from_numpy(raw).to(dev)
-            self.pn_layers = pointnet_weights(w.d + raw.shape[1], w.d, float(w.sigma[0]), seed=800 + w.config)
+            k0 = w.d + raw.shape[1]
+            # group normalisation before each block, min(32, K) groups, per cloud
+            self.pn_layers = pointnet_gn_weights(k0, seed=800 + w.config)
+            self.pn_groups = [min(32, k) for k in (k0, 16, 32)]
             self.pn_params = Lattice.pack_pointnet(self.pn_layers).to(dev)
             self.values = torch.empty((mv, 64), dtype=storage(0), device=dev)
         if tail == "unet":
@@ -231,7 +235,7 @@ class Pipeline:
         if self.tail == "pointnet":
             L.splat(self.pos, None, self.batch, want_weight=False)
             mark()
-            L.distribute_pointnet(self.pos, self.raw, self.pn_params, out=self.values)
+            L.distribute_pointnet(self.pos, self.raw, self.pn_params, out=self.values, groups=self.pn_groups)
         else:
             L.splat(self.pos, self.feat, self.batch, values=self.values, want_weight=False)
         if self.tail == "unet":
@@ -348,7 +352,9 @@ def algorithmic_work(w, V, n_cls=0, Vc=0, f_raw=-1):
         # distribute + PointNet: read each point's position and raw features,
         # each pair-list entry (8 B) and each vertex's list header (8 B), write
         # the 64-channel row (bf16 when the first conv is bf16); 2 (k0 16 +
-        # 16 32 + 32 64) flops per pair on fp32 MFMA
+        # 16 32 + 32 64) flops per pair on fp32 MFMA (the group
+        # normalisation's statistics passes recompute blocks 1 and 2: not
+        # counted)
         work["distribute"] = {"bytes": m * 4 * (d + f_raw) + E * 8 + V * (8 + s0 * 64),
                               "flops": 2 * E * (k0 * 16 + 16 * 32 + 32 * 64), "dtype": "f32"}
     if n and Vc:
@@ -394,7 +400,8 @@ def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False, pointnet=No
     with the classifier when `dw` holds its weights; with `train` also the
     backward pass of every stage; with `unet` the coarse lattice, the
     downsample and the upsample before the slice; with `pointnet` (its
-    layers) Distribute + PointNet instead of the features' splat) repeated
+    layers and group counts) Distribute + PointNet instead of the features'
+    splat) repeated
     until about `budget_s` seconds, reported as points/s."""
     from threadpoolctl import threadpool_info
 
@@ -414,7 +421,8 @@ def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False, pointnet=No
     def one():
         lat = O.build(w.pos, w.sigma, batch=w.batch)
         if pointnet is not None:
-            x, _, _ = O.distribute_pointnet(lat, w.pos, raw, pointnet)
+            layers, groups = pointnet
+            x, _, _ = O.distribute_pointnet(lat, w.pos, raw, layers, groups=groups)
         else:
             x, _, _ = O.splat(lat, w.feat)
         nbr = O.neighbors(lat)
@@ -692,8 +700,8 @@ def main(argv=None):
                   | ({"classes": n_cls, "tail": "deformslice+classifier"} if args.op == "deform" else {})
                   | ({"tail": "slice, then the backward pass of every stage"} if args.op == "train" else {})
                   | ({"coarse_vertices": Vc, "tail": "downsample+upsample+slice"} if args.op == "unet" else {})
-                  | ({"head": f"distribute+pointnet ({w.d}+{f_raw} -> 16 -> 32 -> 64)"} if args.op == "pointnet"
-                     else {}),
+                  | ({"head": f"distribute+pointnet ({w.d}+{f_raw} -> 16 -> 32 -> 64, group norm "
+                              f"{pipe.pn_groups} per cloud)"} if args.op == "pointnet" else {}),
         "roofline": rf,
         "stages": stages,
         "vertices_per_s": V / (sum(v for n, v in stage_ms.items() if n.startswith("conv")) * 1e-3),
@@ -730,7 +738,7 @@ def main(argv=None):
     if not args.no_cpu_baseline and args.op in ("train", "unet", "pointnet"):
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, None, train=args.op == "train",
                                            unet=args.op == "unet",
-                                           pointnet=pipe.pn_layers if args.op == "pointnet" else None)
+                                           pointnet=(pipe.pn_layers, pipe.pn_groups) if args.op == "pointnet" else None)
     elif not args.no_cpu_baseline:
         dw = pipe.dw if args.op == "deform" else None
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, dw)

@@ -376,35 +376,56 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
  * into one operation so that the distributed rows are never stored.
  *
  * Sec. "Proposed Operations" (Distribute, Eq. distribute), the PointNet block
- * of the network figure, and Sec. "Performance" (fusing the two).  Every pair
- * (point p, vertex v of p's simplex) of the last splat is one row
+ * of the network figure, Sec. "Implementation" (every convolution is
+ * pre-activated by a group normalisation and a ReLU; 32 groups by default),
+ * and Sec. "Performance" (fusing the two).  Every pair (point p, vertex v of
+ * p's simplex) of the last splat is one row
  *   h_0 = [g_p - mu_v ; f_p],  mu_v = mean of g_q over the points q of J_v
  *   (every pair counts, whatever its barycentric weight);
  * three blocks of normalisation, ReLU and a fully connected (1x1) layer
- *   h_l = W_l relu(a_l * h_{l-1} + s_l) + b_l,  widths 16, 32, 64;
- * and x_v = max over the rows of v of h_3, per channel.  (a_l, s_l) is the
- * normalisation as a per-channel affine, which is what a group normalisation
- * reduces to once its statistics are known; its statistics are not computed
- * here.  fp32 products and sums; mu_v summed in fp64.
+ *   h_l = W_l relu(N_l(h_{l-1})) + b_l,  widths 16, 32, 64;
+ * and x_v = max over the rows of v of h_3, per channel.
+ *   groups given: N_l is a group normalisation with groups[l-1] groups of
+ *                 consecutive channels.  Per cloud (each batch id of a
+ *                 batched lattice is its own cloud) and group, the mean and
+ *                 the (biased) variance are taken over all the cloud's rows
+ *                 and the group's channels; then per channel
+ *                 gamma_c (h - mean) / sqrt(var + eps) + beta_c.  Computed on
+ *                 the device in three statistics passes (fp64 sums) before
+ *                 the final pass.
+ *   groups NULL:  N_l is the per-channel affine a_l h + s_l given by the
+ *                 caller (a normalisation whose statistics are known).
+ * fp32 products and sums; mu_v summed in fp64.
  *   pos       dev [m][d] fp32, the positions the last splat was given.
  *   feat      dev [m][f_d] fp32 point features, or NULL when f_d = 0.
  *   f_d       feature channels, 0 <= f_d <= 16 - d.
- *   params    dev fp32, per block l = 1, 2, 3 in order: a [K_l], s [K_l],
- *             W [w_l][K_l] (row-major), b [w_l]; K_1 = d + f_d, K_2 = 16,
- *             K_3 = 32, w = 16, 32, 64.
+ *   params    dev fp32, per block l = 1, 2, 3 in order: the normalisation's
+ *             per-channel vectors (gamma [K_l] then beta [K_l] with groups;
+ *             a [K_l] then s [K_l] without), W [w_l][K_l] (row-major), b
+ *             [w_l]; K_1 = d + f_d, K_2 = 16, K_3 = 32, w = 16, 32, 64.
  *   n_blocks  3;  widths  host [3], must be {16, 32, 64} (the widths the
  *             fused kernel is built for).
+ *   groups    host [3] group counts, each >= 1 and dividing its block's K_l,
+ *             or NULL (see above).  The paper's default of 32 groups is
+ *             min(32, K) groups for these widths: {d + f_d, 16, 32}.
+ *   eps       added to each variance (finite, >= 0; 1e-5 is the usual
+ *             value); unused without groups.
  *   out       dev [>= V][64] output x_v (rows 0..V-1 written), in out_dtype:
  *             LATTICE_F32, or LATTICE_BF16 (the fp32 max rounded to nearest
  *             even once: the storage a bf16 conv that reads the rows takes).
  *   mean      dev [>= V][d] fp32 output mu_v, or NULL.
+ * Per-cloud statistics cover batch ids 0..63: on a batched lattice with a
+ * larger batch id the call sets a device status that lattice_num_vertices
+ * and lattice_get_status report as LATTICE_E_RANGE (the rows of those
+ * clouds are then not normalised correctly).
  * The first call allocates the lattice's scratch for it (an entry-to-vertex
- * map, fp64 position sums and running-max keys).  Returns LATTICE_E_STATE
- * before the first splat, LATTICE_E_ARG for anything outside the above.
+ * map, fp64 position sums, running-max keys, and 1 MiB of statistics).
+ * Returns LATTICE_E_STATE before the first splat, LATTICE_E_ARG for anything
+ * outside the above.
  */
 lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
-                                           const float *params, int n_blocks, const int *widths, void *out,
-                                           lattice_dtype out_dtype, float *mean);
+                                           const float *params, int n_blocks, const int *widths, const int *groups,
+                                           float eps, void *out, lattice_dtype out_dtype, float *mean);
 
 /*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to
@@ -416,8 +437,9 @@ lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, 
 /*
  * lattice_num_vertices -- synchronise the stream and return V of the last
  * splat in *V.  Returns the device status (LATTICE_E_CAPACITY,
- * LATTICE_E_RANGE) if the splat failed on the device, LATTICE_E_STATE before
- * the first splat.
+ * LATTICE_E_RANGE) if the splat (or a distribute with group normalisation
+ * on more clouds than it keeps statistics for) failed on the device,
+ * LATTICE_E_STATE before the first splat.
  */
 lattice_status lattice_num_vertices(lattice *L, int64_t *V);
 

@@ -1245,14 +1245,17 @@ hipError_t dispatch_out(lattice *L, const void *in, lattice_dtype in_dt, int C_i
     const bool in_bf16 = in_dt == LATTICE_BF16;
     const bool bf16 = dt == LATTICE_BF16;
     const bool aligned = ((reinterpret_cast<uintptr_t>(in) & 15) == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    // the register-resident kernels store four columns at once (16 bytes of
+    // fp32, 8 of bf16); the others store single elements
+    const bool out_vec = (reinterpret_cast<uintptr_t>(out) & (OUT_BF16 ? 7 : 15)) == 0;
     const int path = L->conv_path;
-    if (aligned && (path == LATTICE_CONV_AUTO || path == LATTICE_CONV_RS) && bf16 && in_bf16) {
+    if (aligned && out_vec && (path == LATTICE_CONV_AUTO || path == LATTICE_CONV_RS) && bf16 && in_bf16) {
         hipError_t err = hipSuccess;
         if (try_rs<OUT_BF16>(L, in, C_in, w, C_out, bias, out, &err)) return err;
     }
     // fp32 64 -> 64: the register-resident kernel (K split over two
     // wavefronts) only on request; the LDS-tiled kernel is faster there
-    if (aligned && path == LATTICE_CONV_RS && !bf16 && !in_bf16 && L->T == 9 && C_in == 64 && C_out == 64)
+    if (aligned && out_vec && path == LATTICE_CONV_RS && !bf16 && !in_bf16 && L->T == 9 && C_in == 64 && C_out == 64)
         return launch_rs<false, OUT_BF16, 9, 64, 64, 2>(L, in, w, bias, out);
     if (aligned && path != LATTICE_CONV_TILED) {
         hipError_t err = hipSuccess;

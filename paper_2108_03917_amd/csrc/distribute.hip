@@ -6,16 +6,21 @@
 // Every pair (point p, simplex vertex v) of the last splat is one row:
 //   h_0 = [g_p - mu_v ; f_p]          (D_G: position minus the local mean
 //                                      mu_v of J_v; D_F: the features)
-//   h_l = W_l relu(a_l * h_{l-1} + s_l) + b_l,   l = 1, 2, 3, widths 16, 32, 64
+//   h_l = W_l relu(N_l(h_{l-1})) + b_l,   l = 1, 2, 3, widths 16, 32, 64
 //   x_v = max over the rows of v of h_3, per channel.
-// (a_l, s_l) is the normalisation as a per-channel affine: what a group
-// normalisation reduces to once its statistics are known.
+// N_l is a group normalisation (Sec. "Implementation": every convolution is
+// pre-activated by group normalisation and ReLU): per cloud (batch id) and
+// group of channels, the mean and variance over all the cloud's rows, then
+// per channel gamma (h - mean) / sqrt(var + eps) + beta.  Once the statistics
+// are known N_l is a per-channel affine a h + s, which is how the kernels
+// apply it; a caller may also give (a, s) directly (no statistics).
 //
 // The rows are the entries of the splat's pair lists, which are grouped by
 // vertex, so the rows of one vertex are consecutive:
 //   k_entry_vertex   entry -> vertex map (one thread per short list, one per
 //                    32-entry part of a long list, as the splat's gather);
-//                    also zeroes the vertex's fp64 position sum
+//                    also zeroes the vertex's fp64 position sum, and finds
+//                    the number of batch ids (clouds) of a batched lattice
 //   k_local_mean     one lane per entry; each wavefront owns 64 consecutive
 //                    entries and sums the positions of each run of equal
 //                    vertex in fp64 (a segmented scan over shuffles); a run
@@ -23,9 +28,17 @@
 //                    the run is added to the vertex's fp64 sum atomically
 //   k_pointnet_prep  mu_v of the lists that cross a 64-entry chunk; the key
 //                    of -inf in the key row of each vertex whose list crosses
-//                    a chunk boundary; the parameters in the padded layout
-//                    (three independent jobs in one launch)
-//   k_pointnet       the three blocks as fp32 MFMA products over the
+//                    a chunk boundary; the parameters in the padded layout;
+//                    the statistics rows zeroed (independent jobs in one
+//                    launch)
+//   with group normalisation, three statistics passes, each followed by
+//   k_gn_finalize, which turns the sums of the block's input into the
+//   affine (a, s) per cloud and channel:
+//     k_gn_stats0    h_0 per entry: per cloud, the row count and the fp64
+//                    sums of h_0 and h_0^2 per channel
+//     k_pointnet<1>  block 1 per entry: the sums of h_1 and h_1^2
+//     k_pointnet<2>  blocks 1 and 2: the sums of h_2 and h_2^2
+//   k_pointnet<3>    the three blocks as fp32 MFMA products over the
 //                    wavefront's 64 entries (weight fragments held in
 //                    registers); block 3's outputs go to LDS channel-major;
 //                    then lane c walks the wavefront's entries keeping the
@@ -40,6 +53,9 @@
 //                    The max is exact in any order, so the result does not
 //                    depend on scheduling; a bf16 row is rounded once, from
 //                    the fp32 max.
+//   k_pointnet_rows  the crossing lists' keys decoded into their rows.
+// The statistics are fp64 sums added with atomics (their order varies from
+// run to run by a few fp64 ulps, far below the fp32 results' rounding).
 #include "internal.h"
 
 namespace {
@@ -52,6 +68,29 @@ constexpr int kMaxK0 = 16;                   // d + f_d, zero-padded to 16
 // 16 lanes of a quarter-wave reading 16 bytes each then cover all 64 banks,
 // and the MFMA output writes of the four lane quarters fall 16 banks apart)
 constexpr int kYStride = 64 + 4;
+
+// Per cloud (batch id), the group normalisation's sums (fp64) of the three
+// blocks' inputs: block l's channel sums at kSum_l, sums of squares at kSq_l,
+// then the row count; and the affines (fp32) the kernels apply: a at kAff_l,
+// s at kAff_l + kAffW_l.  Block 1's input is padded to kMaxK0 channels.
+constexpr int kSum0 = 0, kSq0 = 16, kSum1 = 32, kSq1 = 48, kSum2 = 64, kSq2 = 96, kCount = 128;
+constexpr int kStatRow = 129;
+constexpr int kAff0 = 0, kAff1 = 32, kAff2 = 64, kAffRow = 128;
+// A cloud's batch id comes from its vertex's packed key (bits 48..63).  The
+// per-cloud statistics cover batch ids below kGnClouds.
+constexpr int kGnClouds = 64;
+// Same-address fp64 atomics from many wavefronts serialise (about 0.1 us
+// each, measured), so the statistics rows come in copies, each workgroup
+// (batched) or wavefront (unbatched) adding to one copy, and the finalize
+// adds the copies: kSpread copies of the one row of an unbatched lattice,
+// kSpreadB copies of each of the kGnClouds rows of a batched one.
+constexpr int kSpread = 64, kSpreadB = 16;
+constexpr int kStatRows = kSpreadB * kGnClouds > kSpread ? kSpreadB * kGnClouds : kSpread;
+__device__ __forceinline__ int64_t stat_row(int copy, int cloud, int batched) {
+    return batched ? (int64_t)copy * kGnClouds + cloud : copy;
+}
+// A batched lattice's workgroups first add their rows in LDS (one row per
+// cloud), then hand each row over once.
 
 __device__ __forceinline__ float relu(float x) { return x > 0.f ? x : 0.f; }
 
@@ -77,16 +116,27 @@ __device__ __forceinline__ int run_start(bool head, int lane) {
 __global__ __launch_bounds__(kBlock) void k_entry_vertex(const int32_t *__restrict__ vinfo,
                                                          const int32_t *__restrict__ split,
                                                          const int32_t *__restrict__ rowmap,
-                                                         const int32_t *__restrict__ counters, int d,
+                                                         const uint64_t *__restrict__ vkeys, int batched,
+                                                         int32_t *__restrict__ counters, int d,
                                                          int32_t *__restrict__ lvert, double *__restrict__ macc) {
     const int64_t V = counters[CNT_V];
     const int64_t nrows = counters[CNT_ROWS];
     const int64_t stride = (int64_t)gridDim.x * kBlock;
+    int nclouds = 0;  // batched: 1 + the largest batch id among this thread's vertices
     for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < V; v += stride) {
         for (int i = 0; i < d; ++i) macc[v * d + i] = 0.0;
+        if (batched) nclouds = max(nclouds, (int)(vkeys[v] >> 48) + 1);
         const int off = vinfo[2 * v], cnt = vinfo[2 * v + 1];
         if (cnt > kPart) continue;  // written by its parts below
         for (int e = off; e < off + cnt; ++e) lvert[e] = (int32_t)v;
+    }
+    if (batched) {
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) nclouds = max(nclouds, __shfl_xor(nclouds, o));
+        if ((threadIdx.x & 63) == 0 && nclouds > 0) {
+            atomicMax(counters + CNT_NB, nclouds);
+            if (nclouds > kGnClouds) atomicOr(counters + CNT_STATUS, ST_CLOUDS);
+        }
     }
     for (int64_t u = (int64_t)blockIdx.x * kBlock + threadIdx.x; u < nrows; u += stride) {
         const int sp = rowmap[u];
@@ -96,6 +146,11 @@ __global__ __launch_bounds__(kBlock) void k_entry_vertex(const int32_t *__restri
         const int e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
         for (int e = e0; e < e1; ++e) lvert[e] = v;
     }
+}
+
+// Number of clouds whose statistics are kept: 1 for an unbatched lattice.
+__device__ __forceinline__ int num_clouds(const int32_t *counters, int batched) {
+    return batched ? min(counters[CNT_NB], kGnClouds) : 1;
 }
 
 // Whether entries [off, off + cnt) lie in one 64-entry chunk.
@@ -221,9 +276,38 @@ __device__ __forceinline__ void pack_pointnet(int64_t bid, int64_t nblk, const f
     }
 }
 
+// Without statistics the caller's (a, s) are the affines of the one row
+// (cloud 0) the kernels read: block 1's zero-padded, then blocks 2 and 3.
+__device__ __forceinline__ void affine_row(int64_t bid, int64_t nblk, const float *__restrict__ params, int k0,
+                                           float *__restrict__ aff) {
+    const int o1 = 2 * k0 + kW1 * k0 + kW1;  // block 2's a
+    const int o2 = o1 + 2 * kW1 + kW2 * kW1 + kW2;  // block 3's a
+    for (int64_t i = bid * kBlock + threadIdx.x; i < kAffRow; i += nblk * kBlock) {
+        float x = 0.f;
+        if (i < kAff1) {
+            const int c = (int)i % kMaxK0;
+            if (c < k0) x = params[(i < kMaxK0 ? 0 : k0) + c];
+        } else if (i < kAff2) {
+            x = params[o1 + (int)(i - kAff1)];  // a [16] then s [16]
+        } else {
+            x = params[o2 + (int)(i - kAff2)];  // a [32] then s [32]
+        }
+        aff[i] = x;
+    }
+}
+
+// The statistics rows of the clouds present (or the copies of the one row),
+// zeroed.
+__device__ __forceinline__ void zero_stats(int64_t bid, int64_t nblk, const int32_t *__restrict__ counters,
+                                           int batched, double *__restrict__ stats) {
+    const int64_t n = (int64_t)kStatRows * kStatRow;
+    for (int64_t i = bid * kBlock + threadIdx.x; i < n; i += nblk * kBlock) stats[i] = 0.0;
+}
+
 // After the local means: mu_v of the crossing lists, the key rows set to
-// -inf, and the parameters packed, in one launch (block ranges nb_mean,
-// nb_rows, nb_pack).
+// -inf, the parameters packed, and either the caller's affines copied (no
+// statistics) or the statistics rows zeroed, in one launch (block ranges
+// nb_mean, nb_rows, nb_pack, nb_gn).
 __global__ __launch_bounds__(kBlock) void k_pointnet_prep(const int32_t *__restrict__ vinfo,
                                                           const double *__restrict__ macc, int d,
                                                           const int32_t *__restrict__ counters,
@@ -231,15 +315,213 @@ __global__ __launch_bounds__(kBlock) void k_pointnet_prep(const int32_t *__restr
                                                           const int32_t *__restrict__ lvert,
                                                           unsigned int *__restrict__ keys,
                                                           const float *__restrict__ params, int k0,
-                                                          float *__restrict__ padded, int nb_mean, int nb_rows,
-                                                          int nb_pack) {
+                                                          float *__restrict__ padded, int gn, int batched,
+                                                          double *__restrict__ stats, float *__restrict__ aff,
+                                                          int nb_mean, int nb_rows, int nb_pack, int nb_gn) {
     const int b = blockIdx.x;
     if (b < nb_mean)
         mean_finish(b, nb_mean, vinfo, macc, d, counters, mu);
     else if (b < nb_mean + nb_rows)
         pointnet_rows<false>(b - nb_mean, nb_rows, lvert, vinfo, counters, 0, keys, nullptr);
-    else
+    else if (b < nb_mean + nb_rows + nb_pack)
         pack_pointnet(b - nb_mean - nb_rows, nb_pack, params, k0, padded);
+    else if (gn)
+        zero_stats(b - nb_mean - nb_rows - nb_pack, nb_gn, counters, batched, stats);
+    else
+        affine_row(b - nb_mean - nb_rows - nb_pack, nb_gn, params, k0, aff);
+}
+
+// Sum x (and x^2) over the 16 lanes of a lane quarter (lanes with equal
+// l / 16); every lane of the quarter gets the sums.
+__device__ __forceinline__ double quarter_sum(double x) {
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) x += __shfl_xor(x, o);
+    return x;
+}
+
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) x += __shfl_xor(x, o);
+    return x;
+}
+
+// Group normalisation of block l's input (K channels in G groups of K / G):
+// per cloud b and channel c, from the fp64 sums, mean and (biased) variance
+// of c's group over the cloud's rows, then a = gamma_c / sqrt(var + eps) and
+// s = beta_c - a mean, rounded once to fp32.  gamma and beta are the packed
+// parameters' normalisation vectors.  Padded channels (c >= K) and absent
+// clouds (no rows) get a = s = 0.  One wavefront per (cloud, channel), its
+// lanes adding up the copies of the cloud's row.
+__global__ __launch_bounds__(kBlock) void k_gn_finalize(const double *__restrict__ stats,
+                                                        const float *__restrict__ P,
+                                                        const int32_t *__restrict__ counters, int batched, int l,
+                                                        int K, int G, float eps, float *__restrict__ aff) {
+    const int KP = l == 2 ? kW2 : kMaxK0;
+    const int sum_off = l == 0 ? kSum0 : (l == 1 ? kSum1 : kSum2);
+    const int sq_off = l == 0 ? kSq0 : (l == 1 ? kSq1 : kSq2);
+    const int aff_off = l == 0 ? kAff0 : (l == 1 ? kAff1 : kAff2);
+    const int ga_off = l == 0 ? kA0 : (l == 1 ? kA1 : kA2);
+    const int be_off = l == 0 ? kS0 : (l == 1 ? kS1 : kS2);
+    const int lane = threadIdx.x & 63;
+    const int64_t n = (int64_t)num_clouds(counters, batched) * KP;
+    const int ncopy = batched ? kSpreadB : kSpread;
+    const int gs = K / G;
+    for (int64_t i = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6; i < n; i += (int64_t)gridDim.x * kWaves) {
+        const int b = (int)(i / KP);
+        const int c = (int)(i % KP);
+        double rows = 0.0, sum = 0.0, sq = 0.0;
+        if (lane < ncopy) {
+            const double *st = stats + stat_row(lane, b, batched) * kStatRow;
+            rows = st[kCount];
+            if (c < K) {
+                const int c0 = c / gs * gs;
+                for (int j = c0; j < c0 + gs; ++j) {
+                    sum += st[sum_off + j];
+                    sq += st[sq_off + j];
+                }
+            }
+        }
+        rows = wave_sum(rows);
+        sum = wave_sum(sum);
+        sq = wave_sum(sq);
+        float a = 0.f, s = 0.f;
+        if (c < K && rows > 0.0) {
+            const double cnt = rows * gs;
+            const double mean = sum / cnt;
+            double var = sq / cnt - mean * mean;
+            var = var > 0.0 ? var : 0.0;
+            const double ad = (double)P[ga_off + c] / sqrt(var + (double)eps);
+            a = (float)ad;
+            s = (float)((double)P[be_off + c] - ad * mean);
+        }
+        if (lane == 0) {
+            aff[(int64_t)b * kAffRow + aff_off + c] = a;
+            aff[(int64_t)b * kAffRow + aff_off + KP + c] = s;
+        }
+    }
+}
+
+// The cloud of entry e's vertex v: its batch id, 0 for an unbatched lattice.
+// A batch id beyond the statistics' range (the call reports ST_CLOUDS) is
+// clamped, so that every access stays in bounds.
+__device__ __forceinline__ int cloud_of(const uint64_t *__restrict__ vkeys, int batched, int v) {
+    return batched ? min((int)(vkeys[v] >> 48), kGnClouds - 1) : 0;
+}
+
+// Per cloud, the row count and the sums of h_0 = [g_p - mu_v ; f_p] and of
+// its squares per channel.  One lane per entry; each wavefront takes one
+// contiguous range of chunks, so that its cloud changes only at the clouds'
+// boundaries, and adds up its rows in registers while they stay in one
+// cloud.  Unbatched, the sums go to the wavefront's copy of the one row at
+// the end.  Batched, they go (and the rows of a chunk that spans several
+// clouds go one by one) to the workgroup's LDS row of the cloud, and the
+// workgroup hands its rows over at the end.
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_gn_stats0(const int32_t *__restrict__ list,
+                                                      const int32_t *__restrict__ lvert,
+                                                      const uint64_t *__restrict__ vkeys, int batched,
+                                                      const float *__restrict__ pos, const float *__restrict__ feat,
+                                                      int f_d, const float *__restrict__ mu,
+                                                      const int32_t *__restrict__ counters,
+                                                      double *__restrict__ stats) {
+    constexpr int ROW = 2 * kMaxK0 + 1;  // sums, sums of squares, count
+    __shared__ double tbl[kGnClouds * ROW];
+    const int64_t E = counters[CNT_E];
+    const int lane = threadIdx.x & 63;
+    const int k0 = D + f_d;
+    const int nb = num_clouds(counters, batched);
+    if (batched) {
+        for (int i = threadIdx.x; i < nb * ROW; i += kBlock) tbl[i] = 0.0;
+        __syncthreads();
+    }
+    const int64_t nwaves = (int64_t)gridDim.x * kWaves;
+    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const int64_t nch = (E + 63) / 64, per = (nch + nwaves - 1) / nwaves;
+    const int64_t c_lo = wave * per, c_hi = c_lo + per < nch ? c_lo + per : nch;
+    double s[kMaxK0], q[kMaxK0], cnt = 0.0;
+#pragma unroll
+    for (int i = 0; i < kMaxK0; ++i) s[i] = q[i] = 0.0;
+    int held = -1;  // the cloud whose rows s, q, cnt hold (wave-uniform)
+    auto flush = [&]() {
+        if (held < 0) return;
+        const double c = wave_sum(cnt);
+#pragma unroll
+        for (int i = 0; i < kMaxK0; ++i) {
+            s[i] = wave_sum(s[i]);
+            q[i] = wave_sum(q[i]);
+        }
+        if (lane == 0) {
+            if (batched) {
+                double *row = tbl + held * ROW;  // LDS
+                atomicAdd(row + 2 * kMaxK0, c);
+                for (int i = 0; i < k0; ++i) {
+                    atomicAdd(row + i, s[i]);
+                    atomicAdd(row + kMaxK0 + i, q[i]);
+                }
+            } else {
+                double *st = stats + stat_row((int)(wave % kSpread), 0, 0) * kStatRow;
+                atomicAdd(st + kCount, c);
+                for (int i = 0; i < k0; ++i) {
+                    atomicAdd(st + kSum0 + i, s[i]);
+                    atomicAdd(st + kSq0 + i, q[i]);
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kMaxK0; ++i) s[i] = q[i] = 0.0;
+        cnt = 0.0;
+        held = -1;
+    };
+    for (int64_t c = c_lo; c < c_hi; ++c) {
+        const int64_t e = c * 64 + lane;
+        const bool valid = e < E;
+        const int v = valid ? lvert[e] : 0;
+        const int p = valid ? list[2 * e] : 0;
+        const int b = valid ? cloud_of(vkeys, batched, v) : -1;
+        float x[kMaxK0];
+#pragma unroll
+        for (int i = 0; i < kMaxK0; ++i) {
+            float t = 0.f;
+            if (valid && i < D) t = pos[(int64_t)p * D + i] - mu[(int64_t)v * D + i];
+            else if (valid && i < k0) t = feat[(int64_t)p * f_d + (i - D)];
+            x[i] = t;
+        }
+        const int bref = __builtin_amdgcn_readfirstlane(b);  // lane 0 is valid in every chunk
+        const bool uniform = __ballot(valid && b != bref) == 0ull;
+        if (uniform) {
+            if (bref != held) {
+                flush();
+                held = bref;
+            }
+            cnt += valid ? 1.0 : 0.0;
+#pragma unroll
+            for (int i = 0; i < kMaxK0; ++i) {
+                const double t = (double)x[i];
+                s[i] += t;
+                q[i] += t * t;
+            }
+        } else if (valid) {  // only batched lattices have chunks that span clouds
+            double *row = tbl + b * ROW;
+            atomicAdd(row + 2 * kMaxK0, 1.0);
+            for (int i = 0; i < k0; ++i) {
+                const double t = (double)x[i];
+                atomicAdd(row + i, t);
+                atomicAdd(row + kMaxK0 + i, t * t);
+            }
+        }
+    }
+    flush();
+    if (batched) {
+        __syncthreads();
+        const int copy = (int)(blockIdx.x % kSpreadB);
+        for (int i = threadIdx.x; i < nb * ROW; i += kBlock) {
+            const int b = i / ROW, j = i % ROW;
+            const double x = tbl[i];
+            if (x == 0.0) continue;
+            const int at = j == 2 * kMaxK0 ? kCount : (j < kMaxK0 ? kSum0 + j : kSq0 + (j - kMaxK0));
+            atomicAdd(stats + stat_row(copy, b, 1) * kStatRow + at, x);
+        }
+    }
 }
 
 // After the PointNet: the crossing lists' keys decoded into their rows.
@@ -274,44 +556,58 @@ __device__ __forceinline__ void wave_sync() {
 // needs if its K index at step t, lane quarter q, is that channel: each
 // lane's weight fragments are loaded once with that permutation, so no
 // activation moves between blocks.  Block 1's input comes from LDS (each
-// lane stages its own row).  The outputs go to LDS channel-major for the
-// per-run max.  Each wavefront loops over its own chunks (wavefront-level
-// synchronisation only).
-template <bool OUT_BF16>
+// lane stages its own row).  Each wavefront loops over its own chunks
+// (wavefront-level synchronisation only).
+//   MODE 1: block 1 only; the sums of h_1 and h_1^2 per cloud and channel.
+//   MODE 2: blocks 1 and 2; the sums of h_2 and h_2^2.
+//   MODE 3: all three blocks; the outputs go to LDS channel-major for the
+//           per-run max (see the file comment).
+// The normalisations are the per-cloud affines aff[cloud][..] (one row
+// when the lattice is unbatched or the caller gave the affines).  A chunk
+// whose entries all belong to one cloud (every chunk of an unbatched
+// lattice) uses that cloud's affines, kept in registers while the cloud
+// stays the same; a chunk that spans clouds loads each entry's own.
+template <int MODE, bool OUT_BF16>
 __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__ list,
                                                      const int32_t *__restrict__ lvert,
                                                      const int32_t *__restrict__ vinfo,
+                                                     const uint64_t *__restrict__ vkeys, int batched,
                                                      const float *__restrict__ pos, const float *__restrict__ feat,
                                                      int d, int f_d, const float *__restrict__ P,
+                                                     const float *__restrict__ aff,
                                                      const float *__restrict__ mu,
                                                      const int32_t *__restrict__ counters,
+                                                     double *__restrict__ stats,
                                                      unsigned int *__restrict__ keys, void *__restrict__ out) {
-    __shared__ __attribute__((aligned(16))) float ysh[kWaves][kW3 * kYStride];  // outputs [64 channels][64 entries]; first the staged inputs
+    // MODE 3: outputs [64 channels][64 entries], first the staged inputs;
+    // MODE 1, 2: the staged inputs only
+    constexpr int kYWave = MODE >= 3 ? kW3 * kYStride : 64 * (kMaxK0 + 1);
+    __shared__ __attribute__((aligned(16))) float ysh[kWaves][kYWave];
+    // MODE 1, 2 on a batched lattice: the workgroup's sums (then sums of
+    // squares) of the block's output per cloud
+    constexpr int KS = MODE == 1 ? kW1 : kW2;
+    __shared__ double gtbl[MODE < 3 ? kGnClouds * 2 * KS : 1];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int q = lane >> 4, j16 = lane & 15;
     float *Y = ysh[w];
     const int k0 = d + f_d;
 
-    // weight fragments (A operands) and per-channel affines of this lane
-    float wa1[4], na1[4], ns1[4];
-    float wa2[2][4], na2[2][4], ns2[2][4];
+    // weight fragments (A operands) and biases of this lane
+    float wa1[4], bias1[4];
+    float wa2[2][4], bias2[2][4];
     float wa3[4][8], bb3[4][4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
         wa1[t] = P[kWt0 + j16 * kMaxK0 + 4 * t + q];  // block 1: K = 4 t + q (the staged input order)
-        const int c = 4 * q + t;                       // block 1 output channel in register t
-        na1[t] = P[kA1 + c];
-        ns1[t] = fmaf(P[kA1 + c], P[kB0 + c], P[kS1 + c]);  // a (h + b) + s = a h + (a b + s)
+        bias1[t] = P[kB0 + 4 * q + t];                 // block 1 output channel in register t
     }
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             wa2[mt][t] = P[kWt1 + (16 * mt + j16) * kW1 + 4 * q + t];  // block 2: K = 4 q + t
-            const int c = 16 * mt + 4 * q + t;
-            na2[mt][t] = P[kA2 + c];
-            ns2[mt][t] = fmaf(P[kA2 + c], P[kB1 + c], P[kS2 + c]);
+            bias2[mt][t] = P[kB1 + 16 * mt + 4 * q + t];
         }
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
@@ -322,16 +618,106 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         for (int r = 0; r < 4; ++r) bb3[mt][r] = P[kB2 + 16 * mt + 4 * q + r];
     }
 
+    // The normalisations of one cloud, in this lane's layout: the staged
+    // input's (channel i of the lane's own entry) and, for the MFMA outputs
+    // in register t of row tile mt, channel 4 q + t (+16 mt).  The next
+    // block's bias is folded in: a (h + b) + s = a h + (a b + s).
+    struct Aff {
+        float a0[kMaxK0], s0[kMaxK0];
+        float a1[4], s1[4];
+        float a2[2][4], s2[2][4];
+    };
+    auto load_stage = [&](int b, float *a0, float *s0) {
+        const float *A = aff + (int64_t)b * kAffRow;
+#pragma unroll
+        for (int i = 0; i < kMaxK0; ++i) {
+            a0[i] = A[kAff0 + i];
+            s0[i] = A[kAff0 + kMaxK0 + i];
+        }
+    };
+    auto load_inner = [&](int b, float *a1, float *s1, float (*a2)[4], float (*s2)[4]) {
+        const float *A = aff + (int64_t)b * kAffRow;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int c = 4 * q + t;
+            a1[t] = A[kAff1 + c];
+            s1[t] = fmaf(a1[t], bias1[t], A[kAff1 + kW1 + c]);
+        }
+        if (MODE >= 3) {
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int c = 16 * mt + 4 * q + t;
+                    a2[mt][t] = A[kAff2 + c];
+                    s2[mt][t] = fmaf(a2[mt][t], bias2[mt][t], A[kAff2 + kW2 + c]);
+                }
+        }
+    };
+    Aff U;  // the affines of cloud `held` (wave-uniform)
+    int held = -1;
+
     const int64_t E = counters[CNT_E];
     const int64_t nwaves = (int64_t)gridDim.x * kWaves;
+    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    // This wavefront's chunks: strided over the grid for the final pass; one
+    // contiguous range for the statistics passes, so that a wavefront's
+    // cloud changes only at the clouds' boundaries.
+    const int64_t nch = (E + 63) / 64, per = (nch + nwaves - 1) / nwaves;
+    const int64_t c_first = MODE >= 3 ? wave : wave * per;
+    const int64_t c_end = MODE >= 3 ? nch : (c_first + per < nch ? c_first + per : nch);
+    const int64_t step = MODE >= 3 ? nwaves : 1;
+    // statistics of this lane's channels of the block's output (MODE 1:
+    // channel 4 q + t; MODE 2: 16 mt + 4 q + t) over the rows of cloud
+    // `sheld`, handed over when the cloud changes and at the end
+    constexpr int NS = MODE == 1 ? 4 : (MODE == 2 ? 8 : 1);
+    double ss[NS], sq[NS];
+#pragma unroll
+    for (int i = 0; i < NS; ++i) ss[i] = sq[i] = 0.0;
+    int sheld = -1;
+    auto chan = [&](int i) { return MODE == 1 ? 4 * q + i : 16 * (i / 4) + 4 * q + (i % 4); };
+    const int so = MODE == 1 ? kSum1 : kSum2, qo = MODE == 1 ? kSq1 : kSq2;
+    if (MODE < 3 && batched) {
+        for (int i = threadIdx.x; i < num_clouds(counters, batched) * 2 * KS; i += kBlock) gtbl[i] = 0.0;
+        __syncthreads();
+    }
+    auto flush = [&]() {
+        if (MODE >= 3 || sheld < 0) return;
+#pragma unroll
+        for (int i = 0; i < NS; ++i) {
+            ss[i] = quarter_sum(ss[i]);
+            sq[i] = quarter_sum(sq[i]);
+        }
+        if (j16 == 0) {
+            if (batched) {
+                double *row = gtbl + sheld * 2 * KS;  // LDS
+#pragma unroll
+                for (int i = 0; i < NS; ++i) {
+                    atomicAdd(row + chan(i), ss[i]);
+                    atomicAdd(row + KS + chan(i), sq[i]);
+                }
+            } else {
+                double *st = stats + stat_row((int)(wave % kSpread), 0, 0) * kStatRow;
+#pragma unroll
+                for (int i = 0; i < NS; ++i) {
+                    atomicAdd(st + so + chan(i), ss[i]);
+                    atomicAdd(st + qo + chan(i), sq[i]);
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NS; ++i) ss[i] = sq[i] = 0.0;
+        sheld = -1;
+    };
+
     // Software pipeline over this wavefront's chunks: the entry's vertex and
     // point (level 1) are loaded two chunks ahead, the vertex's list header,
-    // the point's position and features and the vertex's mean (level 2, which
-    // need level 1) one chunk ahead, so that a chunk's MFMAs never wait on
-    // its own gathers.
+    // cloud, the point's position and features and the vertex's mean (level
+    // 2, which need level 1) one chunk ahead, so that a chunk's MFMAs never
+    // wait on its own gathers.
     struct Rows {
         int v, p;             // level 1
-        int off, cnt;         // level 2
+        int off, cnt, b;      // level 2
         float x[kMaxK0];      // h_0 (level 2)
     };
     auto level1 = [&](int64_t chk, Rows &R) {
@@ -344,6 +730,7 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         const bool valid = R.v >= 0;
         R.off = valid ? vinfo[2 * R.v] : 0;
         R.cnt = valid ? vinfo[2 * R.v + 1] : 0;
+        R.b = valid ? cloud_of(vkeys, batched, R.v) : -1;
 #pragma unroll
         for (int i = 0; i < kMaxK0; ++i) {
             float x = 0.f;
@@ -352,21 +739,22 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
             R.x[i] = x;
         }
     };
-    int64_t ch = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    int64_t ch = c_first;
     Rows cur, nxt;
     int v2 = -1, p2 = 0;
-    if (ch * 64 < E) {
+    if (ch < c_end) {
         level1(ch, cur);
         level2(cur);
-        level1(ch + nwaves, nxt);
+        level1(ch + step, nxt);
     }
-    for (; ch * 64 < E; ch += nwaves) {
-        // issue the next chunk's level 2 and the one after's level 1
+    for (; ch < c_end; ch += step) {
+        // issue the next chunk's level 2 and the one after's level 1 (past
+        // this wavefront's range they are loaded and not used)
         {
             Rows tmp;
             tmp.v = nxt.v;
             tmp.p = nxt.p;
-            const int64_t e2 = (ch + 2 * nwaves) * 64 + lane;
+            const int64_t e2 = (ch + 2 * step) * 64 + lane;
             v2 = e2 < E ? lvert[e2] : -1;
             p2 = e2 < E ? list[2 * e2] : 0;
             level2(tmp);
@@ -375,22 +763,49 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         const int64_t chunk0 = ch * 64;
         const int v = cur.v;
         const bool valid = v >= 0;
-        // run flags: 1 first entry of a run, 2 last, 4 the run is the vertex's whole list
-        const int vprev = __shfl_up(v, 1);
-        const int vnext = __shfl_down(v, 1);
-        int flags = 0;
-        if (valid) {
-            if (lane == 0 || vprev != v) flags |= 1;
-            if (lane == 63 || vnext != v) flags |= 2;
-            if (cur.off >= chunk0 && cur.off + cur.cnt <= chunk0 + 64) flags |= 4;
+        // the chunk's cloud: lane 0's (every chunk's first entry is valid),
+        // and whether every entry shares it
+        const int bref = __builtin_amdgcn_readfirstlane(cur.b);
+        const bool uniform = __ballot(valid && cur.b != bref) == 0ull;
+        if (uniform && bref != held) {
+            load_stage(bref, U.a0, U.s0);
+            load_inner(bref, U.a1, U.s1, U.a2, U.s2);
+            held = bref;
         }
-        // destination of the run: the output row, or the key row of the
-        // chunk where the vertex's list starts
-        const int dest = (flags & 4) ? v : (valid ? (int)(cur.off >> 6) : -1);
+        if (MODE < 3 && (!uniform || bref != sheld)) {
+            flush();
+            if (uniform) sheld = bref;
+        }
+        // run flags: 1 first entry of a run, 2 last, 4 the run is the vertex's whole list
+        int flags = 0, dest = -1;
+        if (MODE >= 3) {
+            const int vprev = __shfl_up(v, 1);
+            const int vnext = __shfl_down(v, 1);
+            if (valid) {
+                if (lane == 0 || vprev != v) flags |= 1;
+                if (lane == 63 || vnext != v) flags |= 2;
+                if (cur.off >= chunk0 && cur.off + cur.cnt <= chunk0 + 64) flags |= 4;
+            }
+            // destination of the run: the output row, or the key row of the
+            // chunk where the vertex's list starts
+            dest = (flags & 4) ? v : (valid ? (int)(cur.off >> 6) : -1);
+        }
 
         // r_0 = relu(a_0 h_0 + s_0), h_0 = [g_p - mu_v ; f_p] zero-padded, staged in LDS
+        {
+            float a0[kMaxK0], s0[kMaxK0];
+            if (uniform) {
 #pragma unroll
-        for (int i = 0; i < kMaxK0; ++i) Y[lane * (kMaxK0 + 1) + i] = relu(fmaf(P[kA0 + i], cur.x[i], P[kS0 + i]));
+                for (int i = 0; i < kMaxK0; ++i) {
+                    a0[i] = U.a0[i];
+                    s0[i] = U.s0[i];
+                }
+            } else {
+                load_stage(valid ? cur.b : 0, a0, s0);
+            }
+#pragma unroll
+            for (int i = 0; i < kMaxK0; ++i) Y[lane * (kMaxK0 + 1) + i] = relu(fmaf(a0[i], cur.x[i], s0[i]));
+        }
         wave_sync();
         float b1[4][4];  // B operands of block 1: entry 16 nt + j16, K = 4 t + q
 #pragma unroll
@@ -401,12 +816,43 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
+            // this lane's entry in the tile: its cloud and validity
+            const int ebv = __shfl(valid ? cur.b : -1, 16 * nt + j16);
+            float a1[4], s1[4], a2[2][4], s2[2][4];
+            if (uniform) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    a1[t] = U.a1[t];
+                    s1[t] = U.s1[t];
+                    a2[0][t] = U.a2[0][t];
+                    s2[0][t] = U.s2[0][t];
+                    a2[1][t] = U.a2[1][t];
+                    s2[1][t] = U.s2[1][t];
+                }
+            } else if (MODE >= 2) {
+                load_inner(ebv >= 0 ? ebv : 0, a1, s1, a2, s2);
+            }
             f32x4_t d1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int t = 0; t < 4; ++t) d1 = mfma16(wa1[t], b1[nt][t], d1);
+            if (MODE == 1) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const double h = ebv >= 0 ? (double)(d1[t] + bias1[t]) : 0.0;
+                    if (uniform) {
+                        ss[t] += h;
+                        sq[t] += h * h;
+                    } else if (ebv >= 0) {  // only batched lattices have chunks that span clouds
+                        double *row = gtbl + ebv * 2 * KS;
+                        atomicAdd(row + chan(t), h);
+                        atomicAdd(row + KS + chan(t), h * h);
+                    }
+                }
+                continue;
+            }
             float r1[4];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) r1[t] = relu(fmaf(na1[t], d1[t], ns1[t]));
+            for (int t = 0; t < 4; ++t) r1[t] = relu(fmaf(a1[t], d1[t], s1[t]));
             f32x4_t d2[2];
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt) {
@@ -414,9 +860,25 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 #pragma unroll
                 for (int t = 0; t < 4; ++t) d2[mt] = mfma16(wa2[mt][t], r1[t], d2[mt]);
             }
+            if (MODE == 2) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const double h = ebv >= 0 ? (double)(d2[i / 4][i % 4] + bias2[i / 4][i % 4]) : 0.0;
+                    if (uniform) {
+                        ss[i] += h;
+                        sq[i] += h * h;
+                    } else if (ebv >= 0) {
+                        double *row = gtbl + ebv * 2 * KS;
+                        atomicAdd(row + chan(i), h);
+                        atomicAdd(row + KS + chan(i), h * h);
+                    }
+                }
+                continue;
+            }
             float r2[8];
 #pragma unroll
-            for (int t = 0; t < 8; ++t) r2[t] = relu(fmaf(na2[t / 4][t % 4], d2[t / 4][t % 4], ns2[t / 4][t % 4]));
+            for (int t = 0; t < 8; ++t)
+                r2[t] = relu(fmaf(a2[t / 4][t % 4], d2[t / 4][t % 4], s2[t / 4][t % 4]));
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 f32x4_t d3 = {0.f, 0.f, 0.f, 0.f};
@@ -426,13 +888,13 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
                 for (int r = 0; r < 4; ++r) Y[(16 * mt + 4 * q + r) * kYStride + 16 * nt + j16] = d3[r] + bb3[mt][r];
             }
         }
-        wave_sync();
 
-        // lane c: running max of channel c over each run of the wavefront's
-        // entries, four entries per LDS read; an entry's run flags and
-        // destination come from its lane (readlane: scalar values, so the
-        // store at a run's end is a uniform branch)
-        {
+        if (MODE >= 3) {
+            wave_sync();
+            // lane c: running max of channel c over each run of the wavefront's
+            // entries, four entries per LDS read; an entry's run flags and
+            // destination come from its lane (readlane: scalar values, so the
+            // store at a run's end is a uniform branch)
             const int c = lane;
             float mx = 0.f;
 #pragma unroll
@@ -458,6 +920,16 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         nxt.v = v2;
         nxt.p = p2;
     }
+    flush();
+    if (MODE < 3 && batched) {
+        __syncthreads();
+        const int copy = (int)(blockIdx.x % kSpreadB);
+        for (int i = threadIdx.x; i < num_clouds(counters, batched) * 2 * KS; i += kBlock) {
+            const int b = i / (2 * KS), j = i % (2 * KS);
+            const double x = gtbl[i];
+            if (x != 0.0) atomicAdd(stats + stat_row(copy, b, 1) * kStatRow + (j < KS ? so + j : qo + (j - KS)), x);
+        }
+    }
 }
 
 }  // namespace
@@ -470,15 +942,22 @@ int pointnet_param_count(int k0) {
     return 2 * k0 + kW1 * k0 + kW1 + 2 * kW1 + kW2 * kW1 + kW2 + 2 * kW2 + kW3 * kW2 + kW3;
 }
 
+// Bytes of the statistics (every copy of every cloud's row) and of the
+// affines (one row per cloud).
+int64_t pointnet_stats_bytes() { return (int64_t)kStatRows * kStatRow * (int64_t)sizeof(double); }
+int64_t pointnet_aff_bytes() { return (int64_t)kGnClouds * kAffRow * (int64_t)sizeof(float); }
+
 hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
-                                      void *out, bool out_bf16, float *mean) {
+                                      const int *groups, float eps, void *out, bool out_bf16, float *mean) {
     if (L->m == 0) return hipSuccess;
     const int d = L->d;
+    const int k0 = d + f_d;
+    const int batched = (groups && L->batched) ? 1 : 0;  // per-cloud statistics
     float *mu = mean ? mean : L->mu;
     const int64_t E = L->m * (int64_t)(d + 1);
     const unsigned g_v = grid_for(L->max_vertices, kBlock, L->cu_count, 8);
     hipLaunchKernelGGL(k_entry_vertex, dim3(g_v), dim3(kBlock), 0, L->stream, L->vinfo, L->split, L->rowmap,
-                       L->counters, d, L->lvert, L->macc);
+                       L->vkeys, batched, L->counters, d, L->lvert, L->macc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned g_e = grid_for(E, kBlock, L->cu_count, 8);
@@ -499,14 +978,54 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned g_i = grid_for((E / 64 + 1) * kW3, kBlock, L->cu_count, 4);
     const unsigned g_k = (kPadded + kBlock - 1) / kBlock;
-    hipLaunchKernelGGL(k_pointnet_prep, dim3(g_v + g_i + g_k), dim3(kBlock), 0, L->stream, L->vinfo, L->macc, d,
-                       L->counters, mu, L->lvert, L->pn_keys, params, d + f_d, L->pn_params, (int)g_v, (int)g_i,
-                       (int)g_k);
+    const unsigned g_z = groups ? grid_for((int64_t)kStatRows * kStatRow, kBlock, L->cu_count, 1) : 1;
+    hipLaunchKernelGGL(k_pointnet_prep, dim3(g_v + g_i + g_k + g_z), dim3(kBlock), 0, L->stream, L->vinfo, L->macc,
+                       d, L->counters, mu, L->lvert, L->pn_keys, params, k0, L->pn_params, groups ? 1 : 0, batched,
+                       L->pn_stats, L->pn_aff, (int)g_v, (int)g_i, (int)g_k, (int)g_z);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned g_p = grid_for(E, kBlock, L->cu_count, 2);  // 69 KB of LDS: two workgroups per CU
-    hipLaunchKernelGGL((out_bf16 ? k_pointnet<true> : k_pointnet<false>), dim3(g_p), dim3(kBlock), 0, L->stream,
-                       L->list, L->lvert, L->vinfo, pos, feat, d, f_d, L->pn_params, mu, L->counters, L->pn_keys,
-                       out);
+    if (groups) {
+        const int widths[3] = {k0, kW1, kW2};
+        auto finalize = [&](int l) {
+            const int kp = l == 2 ? kW2 : kMaxK0;
+            const unsigned g_f = grid_for((int64_t)(batched ? kGnClouds : 1) * kp * 64, kBlock, L->cu_count, 1);
+            hipLaunchKernelGGL(k_gn_finalize, dim3(g_f), dim3(kBlock), 0, L->stream, L->pn_stats, L->pn_params,
+                               L->counters, batched, l, widths[l], groups[l], eps, L->pn_aff);
+            return hipGetLastError();
+        };
+        // two workgroups per CU: each wavefront's range of chunks is long
+        // enough that its one hand-over of the sums is a small part of it
+        const unsigned g_s = grid_for(E, kBlock, L->cu_count, 2);
+        switch (d) {
+#define GS_CASE(DD)                                                                                                \
+    case DD:                                                                                                       \
+        hipLaunchKernelGGL(k_gn_stats0<DD>, dim3(g_s), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vkeys,    \
+                           batched, pos, feat, f_d, mu, L->counters, L->pn_stats);                                 \
+        break;
+            GS_CASE(1)
+            GS_CASE(2)
+            GS_CASE(3)
+            GS_CASE(4)
+#undef GS_CASE
+            default:
+                return hipErrorInvalidValue;
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = finalize(0)) != hipSuccess) return e;
+        hipLaunchKernelGGL((k_pointnet<1, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
+                           L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu, L->counters,
+                           L->pn_stats, L->pn_keys, out);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = finalize(1)) != hipSuccess) return e;
+        hipLaunchKernelGGL((k_pointnet<2, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
+                           L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu, L->counters,
+                           L->pn_stats, L->pn_keys, out);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = finalize(2)) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((out_bf16 ? k_pointnet<3, true> : k_pointnet<3, false>), dim3(g_p), dim3(kBlock), 0, L->stream,
+                       L->list, L->lvert, L->vinfo, L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu,
+                       L->counters, L->pn_stats, L->pn_keys, out);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((out_bf16 ? k_pointnet_rows<true> : k_pointnet_rows<false>), dim3(g_i), dim3(kBlock), 0,
                        L->stream, L->lvert, L->vinfo, L->counters, L->pn_keys, out);

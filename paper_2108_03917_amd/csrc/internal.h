@@ -9,14 +9,20 @@
 #include "lattice.h"
 
 // Device status bits, OR-ed into counters[CNT_STATUS] by kernels.
-enum : int { ST_CAPACITY = 1, ST_RANGE = 2 };
+// ST_CLOUDS: a batched lattice's batch ids exceed the range the group
+// normalisation keeps per-cloud statistics for.
+enum : int { ST_CAPACITY = 1, ST_RANGE = 2, ST_CLOUDS = 4 };
 // Slots of the device counter array.
 // CNT_SPLIT and CNT_ROWS count the vertices whose pair list the splat gather
 // cuts into parts, and those parts.
 // CNT_SLOTS is the number of hash slots the last numbering recorded in
 // vslot (every occupied slot of the table, one per vertex), which the next
 // splat empties instead of the whole table.
-enum : int { CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_SPLIT = 3, CNT_ROWS = 4, CNT_SLOTS = 5, CNT_WORDS = 8 };
+// CNT_NB is 1 + the largest batch id of a batched lattice's vertices (set by
+// the distribute operation, for its per-cloud statistics).
+enum : int {
+    CNT_V = 0, CNT_STATUS = 1, CNT_E = 2, CNT_SPLIT = 3, CNT_ROWS = 4, CNT_SLOTS = 5, CNT_NB = 6, CNT_WORDS = 8
+};
 
 // A vertex's pair list longer than kPart pairs is cut into parts of kPart
 // pairs (the splat's gather work units, also used by the distribute op); the
@@ -93,6 +99,10 @@ struct lattice {
     float *pn_params = nullptr; // the PointNet parameters in the kernel's padded layout
     unsigned int *pn_keys = nullptr;  // [(d+1) max_points / 64 + 1][64] running-max keys of lists
                                       // that cross a 64-entry chunk (row j: the list starting in chunk j)
+    // Group normalisation: per cloud, the fp64 sums of each block's input
+    // (in copies) and the affines applied.
+    double *pn_stats = nullptr;
+    float *pn_aff = nullptr;
     int32_t *idx = nullptr;     // [max_points][d+1] hash slot, then vertex index
     int32_t *rank = nullptr;    // [max_points][d+1] position of the pair in its vertex's list
     float *bary = nullptr;      // [max_points][d+1]
@@ -153,7 +163,9 @@ hipError_t launch_flip_weights(lattice *L, const void *w, bool bf16, int C_out, 
 
 // distribute.hip
 hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
-                                      void *out, bool out_bf16, float *mean);
+                                      const int *groups, float eps, void *out, bool out_bf16, float *mean);
+int64_t pointnet_stats_bytes();
+int64_t pointnet_aff_bytes();
 int pointnet_param_count(int k0);
 int pointnet_padded_count();
 

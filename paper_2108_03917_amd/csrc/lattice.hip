@@ -57,6 +57,8 @@ void free_all(lattice *L) {
     (void)hipFree(L->mu);
     (void)hipFree(L->pn_params);
     (void)hipFree(L->pn_keys);
+    (void)hipFree(L->pn_stats);
+    (void)hipFree(L->pn_aff);
     (void)hipFree(L->vinfo);
     (void)hipFree(L->idx);
     (void)hipFree(L->rank);
@@ -597,8 +599,8 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
 }
 
 lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
-                                           const float *params, int n_blocks, const int *widths, void *out,
-                                           lattice_dtype out_dtype, float *mean) {
+                                           const float *params, int n_blocks, const int *widths, const int *groups,
+                                           float eps, void *out, lattice_dtype out_dtype, float *mean) {
     if (!L) return LATTICE_E_ARG;
     if (!L->splatted) {
         set_err(L, "distribute_pointnet: no lattice yet (call lattice_splat first)");
@@ -610,6 +612,19 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
         set_err(L, "distribute_pointnet: bad argument (f_d = %d; the fused PointNet has 3 blocks of widths 16, "
                 "32, 64 and d + f_d <= 16)", f_d);
         return LATTICE_E_ARG;
+    }
+    if (groups) {
+        const int K[3] = {L->d + f_d, 16, 32};
+        for (int l = 0; l < 3; ++l)
+            if (groups[l] < 1 || K[l] % groups[l] != 0) {
+                set_err(L, "distribute_pointnet: block %d's %d input channels do not split into %d groups", l + 1,
+                        K[l], groups[l]);
+                return LATTICE_E_ARG;
+            }
+        if (!(eps >= 0.f) || !isfinite(eps)) {
+            set_err(L, "distribute_pointnet: eps must be finite and >= 0");
+            return LATTICE_E_ARG;
+        }
     }
     const int64_t E_max = (int64_t)(L->d + 1) * L->max_points;
     lattice_status s = LATTICE_OK;
@@ -635,10 +650,27 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
             return LATTICE_E_NOMEM;
         }
     }
+    // the normalisation's statistics and affines (1 MiB and 32 KiB)
+    if (!L->pn_stats || !L->pn_aff) {
+        (void)hipFree(L->pn_stats);
+        (void)hipFree(L->pn_aff);
+        L->pn_stats = nullptr;
+        L->pn_aff = nullptr;
+        if (hipMalloc(&L->pn_stats, pointnet_stats_bytes()) != hipSuccess ||
+            hipMalloc(&L->pn_aff, pointnet_aff_bytes()) != hipSuccess) {
+            (void)hipGetLastError();
+            (void)hipFree(L->pn_stats);
+            (void)hipFree(L->pn_aff);
+            L->pn_stats = nullptr;
+            L->pn_aff = nullptr;
+            set_err(L, "distribute_pointnet: cannot allocate the normalisation's statistics");
+            return LATTICE_E_NOMEM;
+        }
+    }
     hipEvent_t t0;
     if ((s = timer_begin(L, LATTICE_STAGE_DISTRIBUTE, &t0))) return s;
-    if ((s = check_launch(L, launch_distribute_pointnet(L, pos, feat, f_d, params, out, out_dtype == LATTICE_BF16,
-                                                        mean),
+    if ((s = check_launch(L, launch_distribute_pointnet(L, pos, feat, f_d, params, groups, eps, out,
+                                                        out_dtype == LATTICE_BF16, mean),
                           "distribute_pointnet")))
         return s;
     return timer_end(L, LATTICE_STAGE_DISTRIBUTE, t0);
@@ -664,6 +696,10 @@ static lattice_status device_status(lattice *L) {
     }
     if (st & ST_RANGE) {
         set_err(L, "splat: a key coordinate exceeds +-%d or a batch id is outside [0, 65535]", KEY_MAX);
+        return LATTICE_E_RANGE;
+    }
+    if (st & ST_CLOUDS) {
+        set_err(L, "distribute_pointnet: group normalisation keeps per-cloud statistics for batch ids 0..63 only");
         return LATTICE_E_RANGE;
     }
     return LATTICE_OK;

@@ -64,7 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_slice_backward": (St, [P, P, I, P, I]),
         "lattice_splat_backward": (St, [P, P, I, I, I, P, P]),
         "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
-        "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, I, P]),
+        "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, ctypes.c_float, P, I, P]),
         "lattice_downsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_upsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
@@ -324,12 +324,16 @@ class Lattice:
 
     def distribute_pointnet(self, pos: torch.Tensor, feat: Optional[torch.Tensor], params: torch.Tensor,
                             out: Optional[torch.Tensor] = None, mean: Optional[torch.Tensor] = None,
-                            want_mean: bool = False, out_dtype: str = "f32"):
+                            want_mean: bool = False, out_dtype: str = "f32", groups=None, eps: float = 1e-5):
         """Distribute + PointNet + per-vertex max over the last splat's pairs:
         ``pos`` [m, d] (the positions that were splatted), ``feat`` [m, f_d]
         or None, ``params`` the packed parameters (see pack_pointnet) on the
-        device.  Returns out [rows, 64], stored as fp32 or bf16 (the dtype of
-        ``out``, else ``out_dtype``), and the local means [rows, d] with
+        device.  With ``groups`` (three group counts, or "default" for
+        min(32, K) per block) each block's normalisation is a group
+        normalisation computed per cloud and ``params`` holds (gamma, beta, W,
+        b) per block; without, the normalisation is the fixed affine (a, s) of
+        ``params``.  Returns out [rows, 64], stored as fp32 or bf16 (the dtype
+        of ``out``, else ``out_dtype``), and the local means [rows, d] with
         want_mean or a ``mean`` tensor."""
         _dev(pos, torch.float32, "pos")
         if pos.dim() != 2 or pos.shape != (self.m, self.d):
@@ -358,8 +362,16 @@ class Lattice:
             if mean.numel() < need * self.d:
                 raise ValueError(f"mean needs [>= {need}, {self.d}]")
         widths = (ctypes.c_int * 3)(*self.POINTNET_WIDTHS)
+        gr = None
+        if groups is not None:
+            if isinstance(groups, str) and groups == "default":
+                groups = [min(32, k) for k in (k0, 16, 32)]
+            if len(groups) != 3:
+                raise ValueError("groups must hold one group count per block (3)")
+            gr = (ctypes.c_int * 3)(*[int(g) for g in groups])
         self._check(self._lib.lattice_distribute_pointnet(self._h, _ptr(pos), _ptr(feat), f_d, _ptr(params), 3,
-                                                          widths, _ptr(out), _STORAGE[out.dtype], _ptr(mean)),
+                                                          widths, gr, ctypes.c_float(eps), _ptr(out),
+                                                          _STORAGE[out.dtype], _ptr(mean)),
                     "distribute_pointnet")
         return (out, mean) if mean is not None else out
 

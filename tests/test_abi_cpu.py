@@ -145,6 +145,13 @@ def test_distribute_binding_passes_the_output_storage(monkeypatch):
         L.distribute_pointnet(torch.zeros((10, 3)), None, params, out=out)
         a = calls[-1]
         assert a[0] == "H" and a[3] == 0 and a[5] == 3
-        assert a[7] == id(out) and a[8] == code and a[9] is None
+        assert a[7] is None                               # no groups: the caller's affines
+        assert a[9] == id(out) and a[10] == code and a[11] is None
     out = L.distribute_pointnet(torch.zeros((10, 3)), None, params, out_dtype="bf16")
-    assert out.dtype == torch.bfloat16 and calls[-1][8] == B.BF16
+    assert out.dtype == torch.bfloat16 and calls[-1][10] == B.BF16
+    # group normalisation: three group counts ("default": min(32, K) per block) and eps
+    L.distribute_pointnet(torch.zeros((10, 3)), None, params, groups="default", eps=1e-3)
+    a = calls[-1]
+    assert list(a[7]) == [3, 16, 32] and abs(a[8].value - 1e-3) < 1e-9
+    L.distribute_pointnet(torch.zeros((10, 3)), None, params, groups=[1, 4, 8])
+    assert list(calls[-1][7]) == [1, 4, 8]
