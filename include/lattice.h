@@ -328,6 +328,33 @@ lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_d
                                      float *grad_w, float *grad_bias);
 
 /*
+ * lattice_conv_backward_noalloc -- lattice_conv_backward for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * or training loops, and harnesses that forbid hipMalloc.  Same arguments,
+ * same kernels and the same results; it calls no hipMalloc, hipFree or other
+ * allocating routine (and records no stage timing, whose events would be
+ * created on first use).  Its two scratch buffers (the flipped, transposed
+ * weights for grad_in, and one partial weight and bias gradient per vertex
+ * chunk for grad_w / grad_bias) live in a fixed workspace of
+ * LATTICE_NOALLOC_WORKSPACE_BYTES that the library holds on each GPU it runs
+ * on until the process ends, instead of the lattice's scratch.
+ *   Limit: C_out T C_in (2 or 4 bytes, padded to 256) for grad_in plus
+ *   chunks (C_out T C_in + C_out) 4 bytes for grad_w / grad_bias must fit;
+ *   every shape up to 128 -> 128 channels with 11 taps does.  A larger one
+ *   returns LATTICE_E_ARG before anything is enqueued.
+ *   Every call on one GPU shares that GPU's workspace and leaves its
+ *   contents behind: calls that overlap on one GPU (other streams, other
+ *   threads, other lattices) race and must be serialised by the caller.
+ * Returns LATTICE_E_HIP if the workspace of the lattice's device could not be
+ * resolved when the lattice was created.
+ */
+#define LATTICE_NOALLOC_WORKSPACE_BYTES (24 * 1024 * 1024)
+lattice_status lattice_conv_backward_noalloc(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
+                                             const void *w, int C_in, lattice_dtype dt, const void *in,
+                                             lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                             float *grad_w, float *grad_bias);
+
+/*
  * Downsampling and upsampling between two lattices of one cloud (Sec.
  * "Proposed Operations": Downsampling, Upsampling, and the Coarsen figure).
  * The coarse lattice is the cloud's lattice at twice the scale (the positions

@@ -8,11 +8,44 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "internal.h"
 
 namespace {
+
+// Workspace of lattice_conv_backward_noalloc: a fixed device array, one copy
+// per GPU, held from when the library is loaded on that GPU until the process
+// ends.  Host code never uses the name `scratch` as an address (it is a
+// host-side stand-in): lattice_create resolves the device address once per
+// GPU, with that GPU current, and every use goes through that address.
+static __device__ __align__(256) unsigned char scratch[LATTICE_NOALLOC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+bool g_scratch_done[kMaxDevices] = {};
+
+// Resolve this GPU's copy of the workspace (the current device must be
+// `device`); once per device.
+void noalloc_setup(int device) {
+    if (device < 0 || device >= kMaxDevices) return;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_done[device]) return;
+    g_scratch_done[device] = true;
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess)
+        g_scratch_ptr[device] = p;
+    else
+        (void)hipGetLastError();
+}
+
+void *noalloc_workspace(int device) {
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return g_scratch_ptr[device];
+}
 
 void set_err(lattice *L, const char *fmt, ...) {
     if (!L) return;
@@ -231,6 +264,7 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
     int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, L->device) == hipSuccess && cus > 0)
         L->cu_count = cus;
+    noalloc_setup(L->device);
 
     const int dp1 = d + 1;
     bool ok = hipMalloc(&L->tab, L->cap * 16) == hipSuccess &&
@@ -470,24 +504,61 @@ lattice_status lattice_splat_backward(lattice *L, const void *grad_values, latti
     return timer_end(L, LATTICE_STAGE_SPLAT_BACKWARD, t0);
 }
 
-lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
-                                     const void *w, int C_in, lattice_dtype dt, const void *in,
-                                     lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
-                                     float *grad_w, float *grad_bias) {
+// Argument checks shared by the two conv backward entry points.
+static lattice_status conv_backward_args(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
+                                         const void *w, int C_in, lattice_dtype dt, const void *in,
+                                         lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                         float *grad_w, float *grad_bias, const char *what) {
     if (!L) return LATTICE_E_ARG;
     if (!L->splatted) {
-        set_err(L, "conv_backward: no lattice yet (call lattice_splat first)");
+        set_err(L, "%s: no lattice yet (call lattice_splat first)", what);
         return LATTICE_E_STATE;
     }
     auto bad_dt = [](lattice_dtype t) { return t != LATTICE_F32 && t != LATTICE_BF16; };
     if (!grad_out || C_out < 1 || C_out > 1024 || C_in < 1 || C_in > 1024 || bad_dt(g_dtype) || bad_dt(dt) ||
         (grad_in && (!w || bad_dt(grad_in_dtype) || grad_in == grad_out)) ||
         ((grad_w || grad_bias) && !in) || (in && bad_dt(in_dtype)) || (!grad_in && !grad_w && !grad_bias)) {
-        set_err(L, "conv_backward: bad argument (C_out = %d, C_in = %d)", C_out, C_in);
+        set_err(L, "%s: bad argument (C_out = %d, C_in = %d)", what, C_out, C_in);
         return LATTICE_E_ARG;
     }
-    lattice_status s = ensure_neighbors(L);
+    return LATTICE_OK;
+}
+
+// The launches of a conv backward, with the flipped weights in `wflip` and
+// the weight-gradient partials (then the bias partials) in `wgpart`.
+static lattice_status conv_backward_run(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
+                                        const void *w, int C_in, lattice_dtype dt, const void *in,
+                                        lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                        float *grad_w, float *grad_bias, int nch, void *wflip, float *wgpart) {
+    lattice_status s;
+    if (grad_in) {
+        // dx = forward conv of g with W'[i][s][o] = W[o][flip(s)][i]
+        if ((s = check_launch(L, launch_flip_weights(L, w, dt == LATTICE_BF16, C_out, C_in, wflip),
+                              "conv_backward flip")))
+            return s;
+        if ((s = check_launch(L, launch_conv(L, grad_out, g_dtype, C_out, wflip, C_in, dt, nullptr, grad_in,
+                                             grad_in_dtype),
+                              "conv_backward input")))
+            return s;
+    }
+    if (grad_w || grad_bias) {
+        float *pbias = wgpart + (int64_t)nch * C_out * L->T * C_in;
+        if ((s = check_launch(L, launch_conv_wgrad(L, grad_out, g_dtype, C_out, in, in_dtype, C_in, dt, nch, wgpart,
+                                                   pbias, grad_w, grad_bias),
+                              "conv_backward weight")))
+            return s;
+    }
+    return LATTICE_OK;
+}
+
+lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
+                                     const void *w, int C_in, lattice_dtype dt, const void *in,
+                                     lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                     float *grad_w, float *grad_bias) {
+    lattice_status s = conv_backward_args(L, grad_out, g_dtype, C_out, w, C_in, dt, in, in_dtype, grad_in,
+                                          grad_in_dtype, grad_w, grad_bias, "conv_backward");
     if (s) return s;
+    if ((s = ensure_neighbors(L))) return s;
     const int T = L->T;
     const int nch = wgrad_chunks(L, C_in, C_out);
     if (grad_in) {
@@ -505,24 +576,46 @@ lattice_status lattice_conv_backward(lattice *L, const void *grad_out, lattice_d
     }
     hipEvent_t t0;
     if ((s = timer_begin(L, LATTICE_STAGE_CONV_BACKWARD, &t0))) return s;
-    if (grad_in) {
-        // dx = forward conv of g with W'[i][s][o] = W[o][flip(s)][i]
-        if ((s = check_launch(L, launch_flip_weights(L, w, dt == LATTICE_BF16, C_out, C_in, L->wflip),
-                              "conv_backward flip")))
-            return s;
-        if ((s = check_launch(L, launch_conv(L, grad_out, g_dtype, C_out, L->wflip, C_in, dt, nullptr, grad_in,
-                                             grad_in_dtype),
-                              "conv_backward input")))
-            return s;
-    }
-    if (grad_w || grad_bias) {
-        float *pbias = L->wgpart + (int64_t)nch * C_out * T * C_in;
-        if ((s = check_launch(L, launch_conv_wgrad(L, grad_out, g_dtype, C_out, in, in_dtype, C_in, dt, nch,
-                                                   L->wgpart, pbias, grad_w, grad_bias),
-                              "conv_backward weight")))
-            return s;
-    }
+    if ((s = conv_backward_run(L, grad_out, g_dtype, C_out, w, C_in, dt, in, in_dtype, grad_in, grad_in_dtype, grad_w,
+                               grad_bias, nch, L->wflip, L->wgpart)))
+        return s;
     return timer_end(L, LATTICE_STAGE_CONV_BACKWARD, t0);
+}
+
+lattice_status lattice_conv_backward_noalloc(lattice *L, const void *grad_out, lattice_dtype g_dtype, int C_out,
+                                             const void *w, int C_in, lattice_dtype dt, const void *in,
+                                             lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                             float *grad_w, float *grad_bias) {
+    lattice_status s = conv_backward_args(L, grad_out, g_dtype, C_out, w, C_in, dt, in, in_dtype, grad_in,
+                                          grad_in_dtype, grad_w, grad_bias, "conv_backward_noalloc");
+    if (s) return s;
+    unsigned char *ws = reinterpret_cast<unsigned char *>(noalloc_workspace(L->device));
+    if (!ws) {
+        set_err(L, "conv_backward_noalloc: the workspace of device %d is not available", L->device);
+        return LATTICE_E_HIP;
+    }
+    const int T = L->T;
+    const int nch = wgrad_chunks(L, C_in, C_out);
+    // [flipped weights, padded to 256 bytes][partials of the weight and bias gradients]
+    const int64_t flip_bytes = grad_in ? ((int64_t)C_out * T * C_in * (dt == LATTICE_BF16 ? 2 : 4) + 255) / 256 * 256 : 0;
+    const int64_t part_bytes =
+        (grad_w || grad_bias) ? (int64_t)nch * ((int64_t)C_out * T * C_in + C_out) * (int64_t)sizeof(float) : 0;
+    if (flip_bytes + part_bytes > (int64_t)LATTICE_NOALLOC_WORKSPACE_BYTES) {
+        set_err(L, "conv_backward_noalloc: C_out = %d, C_in = %d, T = %d needs %lld bytes of workspace, above the "
+                "%lld available", C_out, C_in, T, (long long)(flip_bytes + part_bytes),
+                (long long)LATTICE_NOALLOC_WORKSPACE_BYTES);
+        return LATTICE_E_ARG;
+    }
+    // the neighbour table, without the stage timer (whose events the timer
+    // would create on first use)
+    if (!L->nbr_valid) {
+        if ((s = check_launch(L, launch_neighbors(L), "neighbors"))) return s;
+        L->nbr_valid = true;
+    }
+    // Every element of the workspace that the kernels read is written first
+    // in this call (each chunk writes its whole partial tile), so no clearing.
+    return conv_backward_run(L, grad_out, g_dtype, C_out, w, C_in, dt, in, in_dtype, grad_in, grad_in_dtype, grad_w,
+                             grad_bias, nch, ws, reinterpret_cast<float *>(ws + flip_bytes));
 }
 
 // Down (up = false) or upsampling from `src` onto the vertices of `dst`.

@@ -30,7 +30,7 @@ EXPORTS = (
     "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
     "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice", "lattice_slice_backward",
     "lattice_splat_backward", "lattice_conv_backward", "lattice_downsample", "lattice_upsample",
-    "lattice_distribute_pointnet",
+    "lattice_distribute_pointnet", "lattice_conv_backward_noalloc",
 )
 
 _lib = None
@@ -64,6 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_slice_backward": (St, [P, P, I, P, I]),
         "lattice_splat_backward": (St, [P, P, I, I, I, P, P]),
         "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
+        "lattice_conv_backward_noalloc": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
         "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, ctypes.c_float, P, I, P]),
         "lattice_downsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_upsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
@@ -473,11 +474,14 @@ class Lattice:
                       dtype: str = "f32", want_input: bool = True, want_weight: bool = True,
                       want_bias: bool = False, grad_in_dtype: str = "f32",
                       grad_in: Optional[torch.Tensor] = None, grad_w: Optional[torch.Tensor] = None,
-                      grad_bias: Optional[torch.Tensor] = None):
+                      grad_bias: Optional[torch.Tensor] = None, noalloc: bool = False):
         """Gradients of ``conv(x, w)`` given ``grad_out`` [>= V, C_out]:
         returns (grad_in [rows, C_in] or None, grad_w [C_out, T, C_in] fp32
         or None, grad_bias [C_out] fp32 or None).  Preallocated outputs may
-        be passed in (then the matching want_* flag is implied)."""
+        be passed in (then the matching want_* flag is implied).  With
+        ``noalloc`` the library's allocation-free entry point runs (its
+        scratch in a fixed per-GPU workspace; pass preallocated outputs to
+        allocate nothing on this side either)."""
         _dev(grad_out, (torch.float32, torch.bfloat16), "grad_out")
         if dtype == "f32":
             _dev(w, torch.float32, "w")
@@ -519,10 +523,11 @@ class Lattice:
             _dev(gb, torch.float32, "grad_bias")
             if gb.numel() != C_out:
                 raise ValueError("grad_bias needs C_out entries")
-        self._check(self._lib.lattice_conv_backward(
+        fn = self._lib.lattice_conv_backward_noalloc if noalloc else self._lib.lattice_conv_backward
+        self._check(fn(
             self._h, _ptr(grad_out), _STORAGE[grad_out.dtype], C_out, _ptr(w), C_in, dt, _ptr(x),
             _STORAGE[x.dtype] if x is not None else F32, _ptr(gi), _STORAGE[gi.dtype] if gi is not None else F32,
-            _ptr(gw), _ptr(gb)), "conv_backward")
+            _ptr(gw), _ptr(gb)), "conv_backward_noalloc" if noalloc else "conv_backward")
         return gi, gw, gb
 
     def weights_to_bf16(self, w: torch.Tensor) -> torch.Tensor:
