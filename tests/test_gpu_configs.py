@@ -6,8 +6,9 @@ compared bit-exactly; splat values within 1e-5 of the sum of |terms|; each of
 the workload's convolutions is fed the oracle's splat values and compared on
 every vertex; slice is fed the oracle's conv output and compared on every
 point; DeformSlice with the fused classifier (the workload's class count) is
-fed seeded rows of the last conv's width and compared on a seeded sample of
-points.
+fed seeded rows of the last conv's width and compared on every point.  Each
+bf16 conv also runs on bf16-stored rows (the benchmark's kernels).  The
+benchmark's whole chain runs on every workload.
 """
 import numpy as np
 import pytest
@@ -60,31 +61,59 @@ def test_full_config_parity(config):
             r = assert_close_scaled(got, ref, cscale, REL_BF16, f"conv {cv.c_in}->{cv.c_out} bf16")
             refb, cscaleb = O.conv(O.round_bf16(x32), nbr, O.round_bf16(cv.weight))
             assert_close_scaled(got, refb, cscaleb, REL_F32, f"conv {cv.c_in}->{cv.c_out} bf16-input")
+            # the rows stored as bf16, as the benchmark stores them: the
+            # register-resident (or ring) kernels it runs there
+            xb = xin.to(torch.bfloat16)
+            for out_dtype in ("f32", "bf16"):
+                outb = L.conv(xb, wd, dtype="bf16", out_dtype=out_dtype)
+                gotb = g.from_gpu_order(outb.float())
+                extra = 2.0 ** -8 * np.abs(refb) if out_dtype == "bf16" else 0.0
+                assert_close_scaled(gotb, refb, REL_F32 * cscaleb + extra, 1.0,
+                                    f"conv {cv.c_in}->{cv.c_out} bf16 rows, {out_dtype} out")
         print(f"  conv {cv.c_in}->{cv.c_out} {cv.dtype} max rel {r:.2e}", flush=True)
         y32 = ref.astype(np.float32)
         sl = L.slice(g.to_gpu_order(y32)).cpu().numpy()
         sref, sscale = O.slice_(lat, y32)
         r = assert_close_scaled(sl, sref, sscale, REL_F32, "slice")
         print(f"  slice C={cv.c_out} max rel {r:.2e}", flush=True)
+    L.close()
+
+
+@pytest.mark.parametrize("config", [1, 2, 3, 4, 5])
+def test_full_config_deform_every_point(config):
+    """DeformSlice with the fused classifier on every point of the workload."""
+    from paper_2108_03917_amd import Lattice
+
+    w = make_workload(config)
+    L = Lattice(w.d, w.sigma, max_points=w.m)
+    g = GpuLattice(L, w.pos, None, batch=w.batch)
+    lat = O.build(w.pos, w.sigma, batch=w.batch)
+    assert np.array_equal(g.keys, lat.keys)
     c_last = w.convs[-1].c_out
     dw = deform_weights(c_last, N_CLASSES[config], seed=100 + config)
     yv = random_rows(lat.V, c_last, seed=1500 + config)
     got = L.deform_slice(g.to_gpu_order(yv), to_dev(dw.w_delta), dw.b_delta, to_dev(dw.w_cls),
                          to_dev(dw.b_cls)).cpu().numpy()
-    sel = np.sort(np.random.default_rng(config).choice(w.m, size=min(w.m, 60000), replace=False))
-    ref, _, dscale = O.deform_slice(lat.idx[sel], lat.bary[sel], yv, dw.w_delta, dw.b_delta, dw.w_cls, dw.b_cls)
-    r = assert_close_scaled(got[sel], ref, dscale, REL_F32, "deform+classifier")
-    print(f"  deform C={c_last} classes={N_CLASSES[config]} on {len(sel)} points max rel {r:.2e}", flush=True)
+    # the oracle in slices of points (each point is independent)
+    for p0 in range(0, w.m, 100000):
+        sl = slice(p0, min(w.m, p0 + 100000))
+        ref, _, dscale = O.deform_slice(lat.idx[sl], lat.bary[sl], yv, dw.w_delta, dw.b_delta, dw.w_cls,
+                                        dw.b_cls)
+        r = assert_close_scaled(got[sl], ref, dscale, REL_F32, f"deform+classifier points {p0}..")
+    print(f"\nconfig {config}: deform C={c_last} classes={N_CLASSES[config]} on all {w.m} points, "
+          f"last slice max rel {r:.2e}", flush=True)
     L.close()
 
 
-def test_bench_workload_end_to_end():
+@pytest.mark.parametrize("config", [1, 2, 3, 4, 5])
+def test_bench_workload_end_to_end(config):
     """splat -> every conv of the workload -> slice exactly as bench.py
-    launches it, against the oracle chain; the tolerance is 2e-2 (bf16) or
-    3e-5 (fp32 only) of the magnitude chain |B| |W|..|W| |B^T| |f|."""
+    launches it (rows stored as bf16 where a bf16 conv reads them), against
+    the oracle chain; the tolerance is 2e-2 (bf16) or 3e-5 (fp32 only) of the
+    magnitude chain |B| |W|..|W| |B^T| |f|."""
     import bench
 
-    w = make_workload(bench.DEFAULT_CONFIG)
+    w = make_workload(config)
     step = bench.Pipeline(w)
     res = step.run()
     step.stream.synchronize()   # the pipeline runs on its own stream
