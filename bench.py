@@ -634,6 +634,8 @@ def main(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--graph", action="store_true", help="time graph replays of the step instead of eager steps")
+    ap.add_argument("--conv-path", choices=("auto", "tiled", "ws", "rs"), default="auto",
+                    help="force one conv kernel family (the library picks per shape by default)")
     args = ap.parse_args(argv)
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
@@ -649,6 +651,7 @@ def main(argv=None):
 
     w = make_workload(args.config)
     pipe = Pipeline(w, tail=args.op)
+    pipe.L.set_conv_path(args.conv_path)
     sec, V, samples, cold = time_pipeline(pipe, args.steps, args.warmup, not args.no_cold, args.graph)
     names = pipe.stage_names()
     stage_ms = {n: float(np.mean(v)) for n, v in samples.items()}
