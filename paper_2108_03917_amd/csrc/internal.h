@@ -181,11 +181,28 @@ hipError_t launch_deform_slice(lattice *L, const void *values, lattice_dtype val
 // that give each workgroup one contiguous chunk of the work take chunk
 // xcd_order(b): the workgroups of one XCD then cover consecutive chunks, so
 // that neighbouring items (and the rows they share) meet in the same L2.
-// (Measured: this helps the pair-list fill; the vertex-row gathers of the
-// splat and the slice run faster with the plain interleaved order.)
+// (Measured: this helps the pair-list fill.)
 __device__ __forceinline__ int64_t xcd_order(int64_t b, int64_t nb) {
     if (nb % 8 != 0) return b;
     return (b % 8) * (nb / 8) + b / 8;
+}
+
+// A grid-stride loop over n items split among the XCDs: XCD x (the one
+// workgroup b runs on, b % 8) takes the contiguous range [x n / 8,
+// (x + 1) n / 8), and its wavefronts interleave within that range, so that
+// items next to each other (and the rows they share) meet in one XCD's L2.
+// Without a multiple of 8 workgroups, one range and every wavefront.
+struct XcdShare {
+    int64_t lo, hi;      // this XCD's items
+    int64_t wave, nwaves;  // this wavefront's index among the XCD's, and their number
+};
+__device__ __forceinline__ XcdShare xcd_share(int64_t n) {
+    const int64_t nb = gridDim.x;
+    const int64_t wpb = blockDim.x >> 6;
+    const int64_t w = threadIdx.x >> 6;
+    if (nb % 8 != 0) return {0, n, (int64_t)blockIdx.x * wpb + w, nb * wpb};
+    const int64_t x = blockIdx.x % 8;
+    return {n * x / 8, n * (x + 1) / 8, (int64_t)(blockIdx.x / 8) * wpb + w, (nb / 8) * wpb};
 }
 
 // This workgroup's chunk [lo, hi) of n items, chunks a multiple of `align`.

@@ -43,11 +43,12 @@ __global__ __launch_bounds__(kBlock) void k_slice(int64_t m, int C, int log2G, c
     const int grp = lane >> log2G;
     const int j = lane & (G - 1);
     const int ppw = 64 >> log2G;
-    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
-    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
-    for (int64_t p0 = wave * ppw; p0 < m; p0 += nwaves * ppw) {
+    // each XCD slices one contiguous range of points: neighbouring points
+    // share their vertex rows, which then meet in that XCD's L2
+    const XcdShare sh = xcd_share(m);
+    for (int64_t p0 = sh.lo + sh.wave * ppw; p0 < sh.hi; p0 += sh.nwaves * ppw) {
         const int64_t p = p0 + grp;
-        if (p >= m) continue;
+        if (p >= sh.hi) continue;
         // A point whose insertion failed (the splat reports it) has vertex -1
         // in some slots: those read another of its rows with weight 0, and a
         // point with none reads nothing.  The d+1 row loads are unconditional

@@ -758,13 +758,14 @@ __global__ __launch_bounds__(kBlock) void k_gather_parts(const int32_t *__restri
     const int grp = lane >> log2G;
     const int j = lane & (G - 1);
     const int gpw = 64 >> log2G;  // groups per wave
-    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
-    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
     const int CV = VEC ? (C >> 2) : C;
     const int2 *L2 = reinterpret_cast<const int2 *>(list);
-    for (int64_t u0 = wave * gpw; u0 < nrows; u0 += nwaves * gpw) {
+    // each XCD takes one contiguous range of parts (vertices in creation
+    // order): the point rows they share meet in its L2
+    const XcdShare sh = xcd_share(nrows);
+    for (int64_t u0 = sh.lo + sh.wave * gpw; u0 < sh.hi; u0 += sh.nwaves * gpw) {
         const int64_t u = u0 + grp;
-        if (u >= nrows) continue;
+        if (u >= sh.hi) continue;
         const int sp = rowmap[u];
         const int vv = split[3 * sp];
         const int row0 = split[3 * sp + 1];
@@ -806,20 +807,21 @@ __global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ v
     const int grp = lane >> log2G;
     const int j = lane & (G - 1);
     const int gpw = 64 >> log2G;  // groups per wave
-    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
-    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
     const int CV = VEC ? (C >> 2) : C;
     const int2 *L2 = reinterpret_cast<const int2 *>(list);
 
-    // Short lists.  The list header of the group's next vertex is loaded
-    // while this one is summed (two header registers, so that the wait for
-    // one header is not a wait for the other).  With C = 0 (weights only)
-    // lane 0 of the group sums the weights alone.
+    // Short lists, each XCD one contiguous range of vertices (in creation
+    // order, so the point rows they share meet in its L2).  The list header
+    // of the group's next vertex is loaded while this one is summed (two
+    // header registers, so that the wait for one header is not a wait for
+    // the other).  With C = 0 (weights only) lane 0 of the group sums the
+    // weights alone.
     const int2 *VI = reinterpret_cast<const int2 *>(vinfo);
-    const int64_t vstep = nwaves * gpw;
-    auto header = [&](int64_t v) { return v < V ? VI[v] : make_int2(0, kPart + 1); };
+    const XcdShare sh = xcd_share(V);
+    const int64_t vstep = sh.nwaves * gpw;
+    auto header = [&](int64_t v) { return v < sh.hi ? VI[v] : make_int2(0, kPart + 1); };
     auto short_list = [&](int64_t v, int2 vi) {
-        if (v >= V || vi.y > kPart) return;
+        if (v >= sh.hi || vi.y > kPart) return;
         const int off = vi.x, e1 = vi.x + vi.y;
         float w = 0.f;
         for (int c = j; c < CV; c += G) {
@@ -841,12 +843,12 @@ __global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ v
         }
     };
     {
-        int64_t v = wave * gpw + grp;
+        int64_t v = sh.lo + sh.wave * gpw + grp;
         int2 ha = header(v);
-        for (; v - grp < V; v += 2 * vstep) {
+        for (; v - grp < sh.hi; v += 2 * vstep) {
             const int2 hb = header(v + vstep);
             short_list(v, ha);
-            if (v - grp + vstep >= V) break;
+            if (v - grp + vstep >= sh.hi) break;
             ha = header(v + 2 * vstep);
             short_list(v + vstep, hb);
         }
@@ -857,9 +859,10 @@ __global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ v
     // dozens of parts); rows past the last part re-read it and are not
     // added.  Then scaled and stored like a short list's row.
     constexpr int kB = 4;
-    for (int64_t s0 = wave * gpw; s0 < ns; s0 += nwaves * gpw) {
+    const XcdShare ss = xcd_share(ns);
+    for (int64_t s0 = ss.lo + ss.wave * gpw; s0 < ss.hi; s0 += ss.nwaves * gpw) {
         const int64_t sp = s0 + grp;
-        if (sp >= ns) continue;
+        if (sp >= ss.hi) continue;
         const int v = split[3 * sp], row0 = split[3 * sp + 1], parts = split[3 * sp + 2];
         const int rlast = row0 + parts - 1;
         float w = 0.f;
