@@ -66,6 +66,7 @@ struct lattice {
     hipStream_t stream = nullptr;
 
     HEntry *tab = nullptr;      // [cap] hash table {key, pair count, vertex index}
+    uint32_t *occ = nullptr;    // [(cap + 31) / 32] occupancy bit of each slot (set by the numbering, for lookups)
     uint64_t *vkeys = nullptr;  // [max_vertices] packed key of each vertex
     int32_t *vslot = nullptr;   // [max_vertices] hash slot of each vertex (what the next splat empties)
     bool full_clear = true;     // the table may hold keys vslot does not list: empty all of it

@@ -58,12 +58,24 @@ __device__ __forceinline__ void unpack_key(uint64_t key, int *c, uint32_t &batch
 // Home slot of a key: the low bits of its mixed value.
 __device__ __forceinline__ uint32_t home_slot(uint64_t key, uint32_t mask) { return (uint32_t)key_mix(key) & mask; }
 
+// Whether hash slot h holds a vertex: bit h of the occupancy bitmap.
+__device__ __forceinline__ bool slot_taken(const uint32_t *__restrict__ occ, uint32_t h) {
+    return (occ[h >> 5] >> (h & 31)) & 1u;
+}
+
+// Mark slot h occupied (once per vertex, by the numbering; no returned value
+// to wait for).
+__device__ __forceinline__ void mark_taken(uint32_t *occ, uint32_t h) { atomicOr(occ + (h >> 5), 1u << (h & 31)); }
+
 // Look up N keys of a table that no thread is writing, all probes of one
 // round in flight together.  `want[k]` false skips key k.  Returns the vertex
-// index per key, -1 when absent.
+// index per key, -1 when absent.  Each probe first reads the slot's
+// occupancy bit (a bitmap of cap / 8 bytes, which stays in L2): an empty
+// slot ends the search without fetching the table's line, which is what most
+// lookups of absent neighbours come down to.
 template <int N>
-__device__ __forceinline__ void hash_find_all(const HEntry *__restrict__ tab, uint32_t mask, const uint64_t *key,
-                                              const bool *want, int *out) {
+__device__ __forceinline__ void hash_find_all(const HEntry *__restrict__ tab, const uint32_t *__restrict__ occ,
+                                              uint32_t mask, const uint64_t *key, const bool *want, int *out) {
     uint32_t h[N];
     bool pending[N];
 #pragma unroll
@@ -73,18 +85,21 @@ __device__ __forceinline__ void hash_find_all(const HEntry *__restrict__ tab, ui
         out[k] = -1;
     }
     for (uint32_t probe = 0; probe <= mask; ++probe) {
+        bool taken[N];
+#pragma unroll
+        for (int k = 0; k < N; ++k) taken[k] = pending[k] && slot_taken(occ, h[k]);
         HEntry e[N];
 #pragma unroll
         for (int k = 0; k < N; ++k)
-            if (pending[k]) e[k] = tab[h[k]];
+            if (taken[k]) e[k] = tab[h[k]];
         bool any = false;
 #pragma unroll
         for (int k = 0; k < N; ++k) {
             if (!pending[k]) continue;
-            if (e[k].key == key[k]) {
-                out[k] = e[k].vid;
+            if (!taken[k]) {
                 pending[k] = false;
-            } else if (e[k].key == 0ull) {
+            } else if (e[k].key == key[k]) {
+                out[k] = e[k].vid;
                 pending[k] = false;
             } else {
                 h[k] = (h[k] + 1) & mask;

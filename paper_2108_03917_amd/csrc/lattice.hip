@@ -74,6 +74,7 @@ int64_t next_pow2(int64_t x) {
 
 void free_all(lattice *L) {
     (void)hipFree(L->tab);
+    (void)hipFree(L->occ);
     (void)hipFree(L->vkeys);
     (void)hipFree(L->vslot);
     (void)hipFree(L->blk);
@@ -268,6 +269,7 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
 
     const int dp1 = d + 1;
     bool ok = hipMalloc(&L->tab, L->cap * 16) == hipSuccess &&
+              hipMalloc(&L->occ, (size_t)(L->cap + 31) / 32 * 4) == hipSuccess &&
               hipMalloc(&L->vkeys, L->max_vertices * sizeof(uint64_t)) == hipSuccess &&
               hipMalloc(&L->vslot, L->max_vertices * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->blk, scan_blocks_max() * 4 * sizeof(int32_t)) == hipSuccess &&

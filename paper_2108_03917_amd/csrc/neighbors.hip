@@ -16,7 +16,8 @@ constexpr int kBlock = 256;
 // looks up c - n_j; the thread of tap 1 also writes tap 0 (the vertex).
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_neighbors(const uint64_t *__restrict__ vkeys,
-                                                      const HEntry *__restrict__ tab, uint32_t mask,
+                                                      const HEntry *__restrict__ tab,
+                                                      const uint32_t *__restrict__ occ, uint32_t mask,
                                                       const int32_t *counters, int32_t *__restrict__ nbr) {
     constexpr int DP1 = D + 1;
     constexpr int R = 2 * DP1;  // ring taps
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(kBlock) void k_neighbors(const uint64_t *__restrict
         uint64_t key;
         const bool want = pack_key<D>(c, b, key);
         int found = -1;
-        hash_find_all<1>(tab, mask, &key, &want, &found);
+        hash_find_all<1>(tab, occ, mask, &key, &want, &found);
         int32_t *row = nbr + v * T;
         row[1 + tap] = found;
         if (tap == 0) row[0] = (int32_t)v;
@@ -55,7 +56,7 @@ hipError_t launch_neighbors(lattice *L) {
     switch (L->d) {
 #define NB_CASE(DD)                                                                                              \
     case DD:                                                                                                     \
-        hipLaunchKernelGGL(k_neighbors<DD>, dim3(grid), dim3(kBlock), 0, L->stream, L->vkeys, L->tab, mask,       \
+        hipLaunchKernelGGL(k_neighbors<DD>, dim3(grid), dim3(kBlock), 0, L->stream, L->vkeys, L->tab, L->occ, mask, \
                            L->counters, L->nbr);                                                                 \
         return hipGetLastError();
         NB_CASE(1)
@@ -84,7 +85,8 @@ namespace {
 
 template <int D, bool UP>
 __global__ __launch_bounds__(kBlock) void k_cross(const uint64_t *__restrict__ vkeys, const int32_t *counters,
-                                                  const HEntry *__restrict__ tab, uint32_t mask,
+                                                  const HEntry *__restrict__ tab, const uint32_t *__restrict__ occ,
+                                                  uint32_t mask,
                                                   int32_t *__restrict__ xnbr) {
     constexpr int DP1 = D + 1;
     constexpr int T = 2 * DP1 + 1;
@@ -113,7 +115,7 @@ __global__ __launch_bounds__(kBlock) void k_cross(const uint64_t *__restrict__ v
         uint64_t key = 0;
         const bool want = pack_key<D>(c, b, key) && integral;
         int found = -1;
-        hash_find_all<1>(tab, mask, &key, &want, &found);
+        hash_find_all<1>(tab, occ, mask, &key, &want, &found);
         xnbr[e] = found;
     }
 }
@@ -128,10 +130,10 @@ hipError_t launch_cross(lattice *out, const lattice *src, bool up, int32_t *xnbr
     case DD:                                                                                                     \
         if (up)                                                                                                  \
             hipLaunchKernelGGL((k_cross<DD, true>), dim3(grid), dim3(kBlock), 0, out->stream, out->vkeys,        \
-                               out->counters, src->tab, mask, xnbr);                                             \
+                               out->counters, src->tab, src->occ, mask, xnbr);                                   \
         else                                                                                                     \
             hipLaunchKernelGGL((k_cross<DD, false>), dim3(grid), dim3(kBlock), 0, out->stream, out->vkeys,       \
-                               out->counters, src->tab, mask, xnbr);                                             \
+                               out->counters, src->tab, src->occ, mask, xnbr);                                   \
         return hipGetLastError();
         CR_CASE(1)
         CR_CASE(2)

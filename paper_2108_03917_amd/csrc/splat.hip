@@ -405,8 +405,9 @@ __global__ __launch_bounds__(NB) void k_insert_shared(const float *__restrict__ 
 // does not list) always writes the whole table and zeroes every counter;
 // otherwise CNT_SLOTS, which every thread reads, is left for the next
 // numbering to rewrite.
-__global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap, const int32_t *__restrict__ vslot,
-                                                        int32_t *counters, int whole) {
+__global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, uint32_t *occ, int64_t cap,
+                                                        const int32_t *__restrict__ vslot, int32_t *counters,
+                                                        int whole) {
     const int64_t tid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     uint4 *t4 = reinterpret_cast<uint4 *>(tab);
@@ -414,8 +415,15 @@ __global__ __launch_bounds__(kBlock) void k_clear_table(HEntry *tab, int64_t cap
     const int64_t n = whole ? cap : counters[CNT_SLOTS];
     if (whole || 8 * n >= cap) {
         for (int64_t i = tid; i < cap; i += stride) t4[i] = zero;
+        for (int64_t i = tid; i < (cap + 31) / 32; i += stride) occ[i] = 0u;
     } else {
-        for (int64_t i = tid; i < n; i += stride) t4[vslot[i]] = zero;
+        // the listed slots and the occupancy words that hold their bits (only
+        // listed slots have a bit set)
+        for (int64_t i = tid; i < n; i += stride) {
+            const int32_t sl = vslot[i];
+            t4[sl] = zero;
+            occ[sl >> 5] = 0u;
+        }
     }
     if (blockIdx.x == 0 && threadIdx.x < CNT_WORDS && (whole || threadIdx.x != CNT_SLOTS)) counters[threadIdx.x] = 0;
 }
@@ -519,7 +527,7 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
                                                         const int4 *__restrict__ blk, uint64_t *__restrict__ vkeys,
                                                         int32_t *__restrict__ vinfo, int32_t *__restrict__ split,
                                                         int32_t *__restrict__ rowmap, int32_t *__restrict__ vslot,
-                                                        int32_t *counters) {
+                                                        uint32_t *occ, int32_t *counters) {
     __shared__ int4 red[kBlock / 64];
     __shared__ int4 wsum[kBlock / 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -574,6 +582,7 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
                 const int v = at.x;
                 tab[sl[i]].vid = v;
                 vslot[v] = sl[i];
+                mark_taken(occ, sl[i]);
                 vkeys[v] = e[i].key;
                 vinfo[2 * v] = at.y;
                 vinfo[2 * v + 1] = q[i].y;
@@ -947,8 +956,8 @@ hipError_t dispatch_d(int d, F &&f) {
 
 hipError_t launch_clear_table(lattice *L) {
     const unsigned grid = grid_for(L->cap, kBlock, L->cu_count, 4);
-    hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->cap, L->vslot, L->counters,
-                       L->full_clear ? 1 : 0);
+    hipLaunchKernelGGL(k_clear_table, dim3(grid), dim3(kBlock), 0, L->stream, L->tab, L->occ, L->cap, L->vslot,
+                       L->counters, L->full_clear ? 1 : 0);
     return hipGetLastError();
 }
 
@@ -994,7 +1003,7 @@ hipError_t launch_number(lattice *L, int64_t m) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan_assign, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->idx, n, span, (int)nb,
-                       L->tab, blk, L->vkeys, L->vinfo, L->split, L->rowmap, L->vslot, L->counters);
+                       L->tab, blk, L->vkeys, L->vinfo, L->split, L->rowmap, L->vslot, L->occ, L->counters);
     return hipGetLastError();
 }
 
