@@ -1,7 +1,9 @@
 """Build liblattice.so (gfx950) in-tree with hipcc.
 
-Every translation unit under ``csrc/`` is compiled in parallel to an object
-under ``_build/`` and linked into ``_lib/liblattice.so``.  The splat unit is
+Every library translation unit under ``csrc/`` is compiled in parallel to an
+object under ``_build/`` and linked into ``_lib/liblattice.so``.  ``peaks.hip``
+(sustained MFMA and HBM rates, a measurement aid) becomes its own executable,
+``_lib/peaks``.  The splat unit is
 compiled without floating-point contraction: the enclosing-simplex decision
 must follow one fixed sequence of individually rounded fp32 operations.
 """
@@ -21,6 +23,8 @@ ARCH = "gfx950"
 
 SOURCES = ["lattice.hip", "splat.hip", "neighbors.hip", "conv.hip", "slice.hip", "deform.hip", "backward.hip", "distribute.hip"]
 EXTRA = {"splat.hip": ["-ffp-contract=off"]}
+PEAKS_SRC = "peaks.hip"
+PEAKS = os.path.join(LIBDIR, "peaks")
 
 
 def hipcc() -> str:
@@ -56,6 +60,8 @@ def build(verbose: bool = False) -> str:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
         objs.append(obj)
         cmds.append([hipcc(), *common_flags(), *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
+    peaks_tmp = PEAKS + ".tmp"
+    cmds.append([hipcc(), *[f for f in common_flags() if f != "-fPIC"], os.path.join(CSRC, PEAKS_SRC), "-o", peaks_tmp])
     with ThreadPoolExecutor(max_workers=min(len(cmds), 8)) as ex:
         for lines in ex.map(_run, cmds):
             if verbose and lines:
@@ -63,6 +69,7 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
+    os.replace(peaks_tmp, PEAKS)
     if verbose:
         print("built", LIB)
     return LIB
