@@ -192,7 +192,7 @@ lattice_status lattice_conv(lattice *L, const void *in, lattice_dtype in_dtype, 
  * testing and benchmarking each kernel).
  *   LATTICE_CONV_AUTO    the fastest kernel built for the shape (default)
  *   LATTICE_CONV_TILED   the LDS-tiled kernel (weights and gathered rows
- *                        staged per K chunk), else the generic one
+ *                        staged per K chunk), else the any-shape one
  *   LATTICE_CONV_WS      weight slice resident in LDS, rows gathered straight
  *                        into registers, where built for the shape; else TILED
  *   LATTICE_CONV_RS      weights resident in registers, rows gathered into

@@ -22,8 +22,10 @@
 // persistent: V lives on the device, so the grid is sized for the largest
 // lattice and every workgroup reads V and strides over the tiles.
 //
-// k_conv_generic: one thread per output element, for channel counts the MFMA
-// tiling does not cover (e.g. 8 -> 16).
+// k_conv_any: MFMA over any channel counts and alignments (e.g. 8 -> 16),
+// with the operands gathered element by element.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace {
@@ -1042,42 +1044,163 @@ __global__ __launch_bounds__(256) void k_conv_ring(const void *__restrict__ in_,
     store_tile(n_tiles - 1 - (n_tiles - 1 - tile0) % tstride);
 }
 
-// Any storage/compute combination, one thread per output element.
-template <bool IN_BF16, bool BF16, bool OUT_BF16>
-__global__ __launch_bounds__(256) void k_conv_generic(const void *__restrict__ in, int C_in,
-                                                      const void *__restrict__ wv, int C_out, int T,
-                                                      const float *__restrict__ bias, void *__restrict__ out,
-                                                      const int32_t *__restrict__ nbr,
-                                                      const int32_t *__restrict__ counters) {
+// Any shape and any storage/compute combination on MFMA: the fallback for
+// channel counts the tilings above do not cover (C_in or C_out not a
+// multiple of 32 / 64, e.g. 8 -> 16), and for operands that are not 16-byte
+// aligned.  The product is the same Y = Z W^T over the flattened
+// K = T C_in: a workgroup of WM x WN wavefronts owns a (32 WM) x (32 WN)
+// output tile, each wavefront one 32 x 32 MFMA block.  K is walked in
+// chunks of KC = 64: every thread gathers its share of the chunk's
+// elements one by one (k -> tap k / C_in, channel k % C_in, through the
+// tile's neighbour indices staged in LDS), zero past K, past C_out and for
+// absent neighbours, converts them to the MFMA operand type and writes them
+// to LDS; the next chunk's elements are loaded into registers while the
+// current one is multiplied.  Operands in LDS are K-contiguous rows padded
+// by 16 bytes (an odd number of 16-byte units per row).  MMA_BF16: rows
+// rounded to bf16 (nearest even; bf16-stored rows are taken as they are)
+// and bf16 weights, MFMA 32x32x16; otherwise fp32 rows and weights, MFMA
+// 32x32x2 (lane half h holds k = 8 g + 4 h + c in component c of a group
+// g, as in k_conv_mfma).
+constexpr int kAnyKC = 64;
+
+template <bool IN_BF16, bool MMA_BF16, bool OUT_BF16, int WM, int WN>
+__global__ __launch_bounds__(WM * WN * 64) void k_conv_any(const void *__restrict__ in, int C_in,
+                                                           const void *__restrict__ wv, int C_out, int T,
+                                                           const float *__restrict__ bias, void *__restrict__ out,
+                                                           const int32_t *__restrict__ nbr,
+                                                           const int32_t *__restrict__ counters) {
+    constexpr int NT = WM * WN * 64;
+    constexpr int BM = 32 * WM;
+    constexpr int BN = 32 * WN;
+    constexpr int ESZ = MMA_BF16 ? 2 : 4;          // operand element in LDS
+    constexpr int PITCH = kAnyKC * ESZ + 16;       // bytes per LDS row
+    constexpr int A_PER = BM * kAnyKC / NT;        // A elements per thread per chunk
+    constexpr int B_PER = BN * kAnyKC / NT;
+    static_assert(A_PER * NT == BM * kAnyKC && B_PER * NT == BN * kAnyKC, "chunk split");
+    typedef typename std::conditional<MMA_BF16, uint16_t, float>::type op_t;
+
+    __shared__ __attribute__((aligned(16))) char As[BM * PITCH];
+    __shared__ __attribute__((aligned(16))) char Bs[BN * PITCH];
+    __shared__ int32_t nbr_s[BM * kMaxTaps];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WN;
+    const int wn = wave % WN;
+    const int lrow = lane & 31;
+    const int h = lane >> 5;
     const int64_t V = counters[CNT_V];
-    const int64_t n = V * C_out;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
-        const int64_t v = e / C_out;
-        const int o = (int)(e - v * C_out);
-        float acc = bias ? bias[o] : 0.f;
-        for (int t = 0; t < T; ++t) {
-            const int u = nbr[v * T + t];
-            if (u < 0) continue;
-            const int64_t xb = (int64_t)u * C_in;
-            const int64_t wb = ((int64_t)o * T + t) * C_in;
-            for (int i = 0; i < C_in; ++i) {
-                float xv = IN_BF16 ? bf16_to_f32(reinterpret_cast<const uint16_t *>(in)[xb + i])
-                                   : reinterpret_cast<const float *>(in)[xb + i];
-                float wvv;
-                if (BF16) {
-                    xv = __uint_as_float(bf16_bits(xv) << 16);
-                    wvv = bf16_to_f32(reinterpret_cast<const uint16_t *>(wv)[wb + i]);
-                } else {
-                    wvv = reinterpret_cast<const float *>(wv)[wb + i];
-                }
-                acc = fmaf(xv, wvv, acc);
+    const int64_t n_mt = (V + BM - 1) / BM;
+    const int n_nt = (C_out + BN - 1) / BN;
+    const int64_t ntiles = n_mt * n_nt;
+    const int64_t K = (int64_t)T * C_in;
+    const int64_t NQ = (K + kAnyKC - 1) / kAnyKC;
+
+    // Lane kk of every wavefront owns K column kk of each chunk (rows
+    // wave, wave + NW, ...), so the tap and channel of its elements are
+    // worked out once per chunk, and a wavefront reads 64 consecutive
+    // elements of one row.
+    constexpr int NW = WM * WN;
+    const int kk = lane;
+    auto a_elem = [&](int r, int t, int i, bool in_k) -> op_t {
+        float x = 0.f;
+        uint16_t xb = 0;
+        const int u = in_k ? nbr_s[r * T + t] : -1;
+        if (u >= 0) {
+            if (IN_BF16) {
+                xb = reinterpret_cast<const uint16_t *>(in)[(int64_t)u * C_in + i];
+                x = bf16_to_f32(xb);
+            } else {
+                x = reinterpret_cast<const float *>(in)[(int64_t)u * C_in + i];
+                xb = (uint16_t)bf16_bits(x);
             }
         }
-        if (OUT_BF16)
-            reinterpret_cast<uint16_t *>(out)[e] = (uint16_t)bf16_bits(acc);
-        else
-            reinterpret_cast<float *>(out)[e] = acc;
+        if constexpr (MMA_BF16) return xb;
+        else return x;
+    };
+
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t row_base = (tile / n_nt) * BM;
+        const int col_base = (int)(tile % n_nt) * BN;
+        for (int i = tid; i < BM * T; i += NT) {
+            const int64_t e = row_base * T + i;
+            nbr_s[i] = (e < V * T) ? nbr[e] : -1;
+        }
+        __syncthreads();
+
+        op_t ar[A_PER], br[B_PER];
+        auto load_chunk = [&](int64_t q) {
+            const int64_t k = q * kAnyKC + kk;
+            const bool in_k = k < K;
+            const int t = in_k ? (int)(k / C_in) : 0;
+            const int i = in_k ? (int)(k - (int64_t)t * C_in) : 0;
+#pragma unroll
+            for (int j = 0; j < A_PER; ++j) ar[j] = a_elem(wave + j * NW, t, i, in_k);
+#pragma unroll
+            for (int j = 0; j < B_PER; ++j) {
+                const int col = col_base + wave + j * NW;
+                br[j] = (in_k && col < C_out) ? reinterpret_cast<const op_t *>(wv)[(int64_t)col * K + k] : op_t(0);
+            }
+        };
+        auto store_chunk = [&]() {
+#pragma unroll
+            for (int j = 0; j < A_PER; ++j)
+                *reinterpret_cast<op_t *>(As + (wave + j * NW) * PITCH + kk * ESZ) = ar[j];
+#pragma unroll
+            for (int j = 0; j < B_PER; ++j)
+                *reinterpret_cast<op_t *>(Bs + (wave + j * NW) * PITCH + kk * ESZ) = br[j];
+        };
+
+        f32x16_t acc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+        const char *arow = As + (wm * 32 + lrow) * PITCH;
+        const char *brow = Bs + (wn * 32 + lrow) * PITCH;
+
+        load_chunk(0);
+        for (int64_t q = 0; q < NQ; ++q) {
+            store_chunk();
+            __syncthreads();
+            if (q + 1 < NQ) load_chunk(q + 1);
+            if constexpr (MMA_BF16) {
+#pragma unroll
+                for (int g = 0; g < kAnyKC / 16; ++g) {
+                    const u32x4_t a = *reinterpret_cast<const u32x4_t *>(arow + (16 * g + 8 * h) * 2);
+                    const u32x4_t b = *reinterpret_cast<const u32x4_t *>(brow + (16 * g + 8 * h) * 2);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                                  __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+                }
+            } else {
+#pragma unroll
+                for (int g = 0; g < kAnyKC / 8; ++g) {
+                    const u32x4_t a = *reinterpret_cast<const u32x4_t *>(arow + (8 * g + 4 * h) * 4);
+                    const u32x4_t b = *reinterpret_cast<const u32x4_t *>(brow + (8 * g + 4 * h) * 4);
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[c]), __uint_as_float(b[c]), acc,
+                                                                   0, 0, 0);
+                }
+            }
+            __syncthreads();  // LDS is rewritten by the next chunk
+        }
+
+        // register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
+        const int col = col_base + wn * 32 + lrow;
+        if (col < C_out) {
+            const float bc = bias ? bias[col] : 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = row_base + wm * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+                if (row < V) {
+                    const float y = acc[r] + bc;
+                    if (OUT_BF16)
+                        reinterpret_cast<uint16_t *>(out)[row * C_out + col] = (uint16_t)bf16_bits(y);
+                    else
+                        reinterpret_cast<float *>(out)[row * C_out + col] = y;
+                }
+            }
+        }
     }
 }
 
@@ -1109,13 +1232,21 @@ hipError_t launch_mfma_n(lattice *L, const void *in, int C_in, const void *w, in
     }
 }
 
-template <bool IN_BF16, bool BF16, bool OUT_BF16>
-hipError_t launch_generic(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias,
-                          void *out) {
-    const unsigned grid = grid_for(L->max_vertices * (int64_t)C_out, 256, L->cu_count, 8);
-    hipLaunchKernelGGL((k_conv_generic<IN_BF16, BF16, OUT_BF16>), dim3(grid), dim3(256), 0, L->stream, in, C_in, w,
-                       C_out, L->T, bias, out, L->nbr, L->counters);
-    return hipGetLastError();
+template <bool IN_BF16, bool MMA_BF16, bool OUT_BF16>
+hipError_t launch_any(lattice *L, const void *in, int C_in, const void *w, int C_out, const float *bias, void *out) {
+    if (L->T > kMaxTaps) return hipErrorInvalidValue;
+    // C_out <= 32: 128 x 32 tiles (four wavefronts along M); else 64 x 64
+    auto go = [&](auto kern, int bm, int bn) {
+        const int64_t tiles = ((L->max_vertices + bm - 1) / bm) * ((C_out + bn - 1) / bn);
+        int64_t grid = (int64_t)L->cu_count * 4;
+        if (grid > tiles) grid = tiles;
+        if (grid < 1) grid = 1;
+        hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), 0, L->stream, in, C_in, w, C_out, L->T, bias, out,
+                           L->nbr, L->counters);
+        return hipGetLastError();
+    };
+    if (C_out <= 32) return go(k_conv_any<IN_BF16, MMA_BF16, OUT_BF16, 4, 1>, 128, 32);
+    return go(k_conv_any<IN_BF16, MMA_BF16, OUT_BF16, 2, 2>, 64, 64);
 }
 
 constexpr int kWsMaxLds = 152 * 1024;  // weight slice budget of one workgroup
@@ -1270,10 +1401,10 @@ hipError_t dispatch_out(lattice *L, const void *in, lattice_dtype in_dt, int C_i
             return launch_mfma_n<2, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
     }
     if (in_bf16)
-        return bf16 ? launch_generic<true, true, OUT_BF16>(L, in, C_in, w, C_out, bias, out)
-                    : launch_generic<true, false, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
-    return bf16 ? launch_generic<false, true, OUT_BF16>(L, in, C_in, w, C_out, bias, out)
-                : launch_generic<false, false, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
+        return bf16 ? launch_any<true, true, OUT_BF16>(L, in, C_in, w, C_out, bias, out)
+                    : launch_any<true, false, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
+    return bf16 ? launch_any<false, true, OUT_BF16>(L, in, C_in, w, C_out, bias, out)
+                : launch_any<false, false, OUT_BF16>(L, in, C_in, w, C_out, bias, out);
 }
 
 }  // namespace

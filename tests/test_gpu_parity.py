@@ -175,7 +175,7 @@ def test_neighbors_parity(d):
 
 CONV_CASES = [
     # d, sigma, m, C_in, C_out, dtype, bias
-    (3, 0.05, 4096, 8, 16, "f32", False),     # generic kernel (tiny config shape)
+    (3, 0.05, 4096, 8, 16, "f32", False),     # any-shape MFMA kernel (tiny config shape)
     (3, 0.1, 6000, 64, 64, "f32", False),     # fp32 MFMA, BN = 64
     (3, 0.1, 6000, 32, 128, "f32", True),     # fp32 MFMA, one chunk per tap, BN = 128
     (3, 0.1, 6000, 64, 64, "bf16", False),    # bf16 MFMA, BN = 64
@@ -183,8 +183,12 @@ CONV_CASES = [
     (3, 0.1, 5000, 128, 128, "bf16", False),  # two chunks per tap
     (3, 0.1, 5000, 64, 192, "bf16", False),   # three N tiles of 64
     (4, 0.3, 5000, 64, 64, "bf16", False),    # T = 11
-    (3, 0.1, 3000, 96, 64, "bf16", False),    # C_in not a multiple of 64: generic
+    (3, 0.1, 3000, 96, 64, "bf16", False),    # C_in not a multiple of 64: any-shape MFMA kernel
     (2, 0.05, 3000, 5, 7, "f32", True),       # odd channels, d = 2
+    (3, 0.1, 3000, 96, 48, "f32", True),      # any-shape, 64 x 64 tiles, C_out tail of 16
+    (4, 0.3, 3000, 16, 40, "bf16", True),     # any-shape, T = 11, K = 176 (three chunks, tail)
+    (1, 0.05, 2000, 3, 1, "f32", False),      # any-shape, d = 1 (T = 5), one output channel
+    (3, 0.1, 3000, 200, 24, "bf16", False),   # any-shape, K = 1800 over 29 chunks, 128 x 32 tiles
     (3, 0.5, 300, 64, 64, "bf16", False),     # V below one tile
 ]
 
@@ -220,6 +224,48 @@ def test_conv_parity(case):
         Wr = O.round_bf16(W).astype(np.float64)
         ref_b, scale_b = O.conv(xr, nbr, Wr, b)
         assert_close_scaled(got, ref_b, scale_b, REL_F32, "bf16 conv vs bf16-input oracle")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_conv_unaligned_operands(dtype):
+    """Rows, weights and output one element past a 16-byte boundary: a
+    shape the tiled kernels serve when aligned runs on the any-shape MFMA
+    kernel, with the same result."""
+    d, sigma, m, C_in, C_out = 3, 0.1, 5000, 64, 64
+    w = random_cloud(m, d, seed=950, extent=1.0, C=1)
+    L = _lattice(d, sigma, m)
+    g = GpuLattice(L, w.pos, w.feat)
+    lat = O.build(w.pos, sigma)
+    nbr = O.neighbors(lat)
+    x = random_rows(lat.V, C_in, seed=951)
+    W = conv_weight(C_in, C_out, d, seed=952)
+    b = random_rows(1, C_out, seed=953)[0]
+
+    def shifted(t):
+        buf = torch.empty(t.numel() + 1, dtype=t.dtype, device=t.device)
+        v = buf[1:].view(t.shape)
+        v.copy_(t)
+        assert v.data_ptr() % 16 != 0
+        return v
+
+    wd = to_dev(W)
+    if dtype == "bf16":
+        wd = L.weights_to_bf16(wd)
+    xd = g.to_gpu_order(x)
+    ref_aligned = L.conv(xd, wd, dtype=dtype, bias=to_dev(b))
+    out = shifted(torch.zeros_like(ref_aligned))
+    got = L.conv(shifted(xd), shifted(wd), dtype=dtype, bias=to_dev(b), out=out)
+    ref, scale = O.conv(x, nbr, W, b)
+    if dtype == "f32":
+        assert_close_scaled(g.from_gpu_order(got), ref, scale, REL_F32, "unaligned f32 conv")
+    else:
+        xr = O.round_bf16(x).astype(np.float64)
+        Wr = O.round_bf16(W).astype(np.float64)
+        ref_b, scale_b = O.conv(xr, nbr, Wr, b)
+        assert_close_scaled(g.from_gpu_order(got), ref_b, scale_b, REL_F32, "unaligned bf16 conv")
+    # and the aligned launch (another kernel) agrees within the same bound
+    assert_close_scaled(g.from_gpu_order(got), g.from_gpu_order(ref_aligned).astype(np.float64), scale, REL_F32,
+                        "unaligned vs aligned")
 
 
 BF16_ULP = 2.0 ** -8   # bound on the relative error of one round-to-nearest to bf16
