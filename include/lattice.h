@@ -94,7 +94,9 @@ typedef enum {
  *   alpha          elevation scale; <= 0 selects (d+1) * sqrt(2/3).
  *   max_points     upper bound on m for every later splat, >= 1.
  *   hash_capacity  number of hash slots; 0 selects the next power of two
- *                  >= (d+1) * max_points, which can never fill up.  A non-zero
+ *                  >= 1.5 (d+1) max_points: it can never fill up, and at
+ *                  most two thirds of its slots are ever taken, which keeps
+ *                  the probe chains of failed lookups short.  A non-zero
  *                  value is rounded up to a power of two; a table that fills
  *                  makes splat report LATTICE_E_CAPACITY.
  *   stream         hipStream_t every call of this lattice is enqueued on

@@ -249,7 +249,10 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
     L->inv_dp1 = (float)(1.0 / (d + 1));
     L->max_points = max_points;
     const int64_t keys_max = (int64_t)(d + 1) * max_points;
-    L->cap = next_pow2(hash_capacity > 0 ? hash_capacity : keys_max);
+    // default: room for every pair's vertex with a third of the slots to
+    // spare, so that the linear probe chains of lookups that fail (most ring
+    // neighbours of a sparse scan are absent) stay short at the worst load
+    L->cap = next_pow2(hash_capacity > 0 ? hash_capacity : (3 * keys_max + 1) / 2);
     if (L->cap > (int64_t)1 << 30) {
         delete L;
         return LATTICE_E_ARG;

@@ -511,6 +511,31 @@ def test_single_point_and_duplicates():
     assert_close_scaled(g.weight(), wref, wref, REL_F32, "duplicate weight")
 
 
+@pytest.mark.parametrize("explicit_capacity", [False, True])
+def test_sparse_cloud_near_worst_load(explicit_capacity):
+    """A cloud so sparse that nearly every (point, vertex) pair creates its
+    own vertex: V is close to (d+1) m, the most a table must hold.  The
+    default capacity keeps the load at or below 2/3; a table of exactly
+    (d+1) m slots runs at a load near 1, where most lookups (the absent ring
+    neighbours) probe long chains.  Both give the oracle's keys, simplices
+    and neighbour table."""
+    d, m, sigma = 3, 4096, 0.0005
+    rng = np.random.default_rng(77)
+    pos = rng.uniform(0.0, 1.0, (m, d)).astype(np.float32)
+    feat = rng.standard_normal((m, 2)).astype(np.float32)
+    keys_max = (d + 1) * m
+    L = _lattice(d, sigma, m, hash_capacity=keys_max if explicit_capacity else 0)
+    if explicit_capacity:
+        assert L.hash_capacity == keys_max
+    else:
+        assert L.hash_capacity >= 1.5 * keys_max
+    g = GpuLattice(L, pos, feat)
+    lat = O.build(pos, sigma)
+    assert lat.V >= 0.99 * keys_max, lat.V
+    check_lattice(g, lat)
+    assert np.array_equal(g.neighbors(), O.neighbors(lat))
+
+
 def test_capacity_error_is_reported():
     from paper_2108_03917_amd import LatticeError
     from paper_2108_03917_amd.lattice import E_CAPACITY
