@@ -401,6 +401,45 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
                                 lattice_dtype out_dtype);
 
 /*
+ * lattice_downsample_backward, lattice_upsample_backward -- gradients of the
+ * two resamplings above with respect to their input, weights and bias, given
+ * grad_out on the output lattice's vertices (the paper trains every lattice
+ * operator end to end, Sec. "Implementation"; these are the adjoints of the
+ * operations defined in Sec. "Proposed Operations").
+ *   grad_in[u][i] = sum over (v, t) with table(v, t) = u of
+ *                   sum_o grad_out[v][o] W[o][t][i]
+ *   grad_w[o][t][i] = sum_v grad_out[v][o] in[table(v, t)][i]
+ *   grad_bias[o]    = sum_v grad_out[v][o]
+ * where table is the forward's cross table (v runs over the output lattice's
+ * vertices, u over the input lattice's).  The input gradient is computed as
+ * the resampling in the other direction with W'[i][s][o] = W[o][flip(s)][i]
+ * (the adjoint stated above), the weight gradient by the conv weight-gradient
+ * kernels over the forward table, summed in a fixed order.
+ *   fine, coarse / coarse, fine   as in the forward call.
+ *   grad_out   dev [V_out][C_out], stored as g_dtype.
+ *   w          dev forward weights [C_out][T][C_in] (fp32 or bf16 by dt); needed
+ *              for grad_in.
+ *   in         dev forward input [V_in][C_in] stored as in_dtype; needed for
+ *              grad_w and grad_bias.
+ *   grad_in    dev [V_in][C_in] stored as grad_in_dtype, or NULL.
+ *   grad_w     dev [C_out][T][C_in] fp32, or NULL.
+ *   grad_bias  dev [C_out] fp32, or NULL.
+ *   dt         as in lattice_conv (LATTICE_BF16 rounds the operands to bf16).
+ * At least one of grad_in, grad_w, grad_bias.  The flipped weights are kept
+ * by the input lattice and the weight-gradient partials by the output
+ * lattice (grown on demand).  Returns as the forward calls, and
+ * LATTICE_E_ARG when grad_in overlaps grad_out or in.
+ */
+lattice_status lattice_downsample_backward(lattice *fine, lattice *coarse, const void *grad_out,
+                                           lattice_dtype g_dtype, int C_out, const void *w, int C_in,
+                                           lattice_dtype dt, const void *in, lattice_dtype in_dtype, void *grad_in,
+                                           lattice_dtype grad_in_dtype, float *grad_w, float *grad_bias);
+lattice_status lattice_upsample_backward(lattice *coarse, lattice *fine, const void *grad_out, lattice_dtype g_dtype,
+                                         int C_out, const void *w, int C_in, lattice_dtype dt, const void *in,
+                                         lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                         float *grad_w, float *grad_bias);
+
+/*
  * lattice_distribute_pointnet -- Distribute + PointNet + per-vertex max, fused
  * into one operation so that the distributed rows are never stored.
  *
@@ -499,7 +538,7 @@ lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary);
  * of launches since the last reset (arrays of LATTICE_NUM_STAGES).
  * lattice_set_timing(L, 0) stops recording; (L, 2) resets the sums.
  */
-#define LATTICE_NUM_STAGES 11
+#define LATTICE_NUM_STAGES 15
 enum {
     LATTICE_STAGE_SPLAT = 0,
     LATTICE_STAGE_NEIGHBORS = 1,
@@ -511,7 +550,11 @@ enum {
     LATTICE_STAGE_SPLAT_BACKWARD = 7,
     LATTICE_STAGE_DOWNSAMPLE = 8,  /* recorded on the output (coarse) lattice */
     LATTICE_STAGE_UPSAMPLE = 9,    /* recorded on the output (fine) lattice   */
-    LATTICE_STAGE_DISTRIBUTE = 10
+    LATTICE_STAGE_DISTRIBUTE = 10,
+    LATTICE_STAGE_DOWNSAMPLE_BACKWARD = 11,  /* recorded on the coarse lattice */
+    LATTICE_STAGE_UPSAMPLE_BACKWARD = 12,    /* recorded on the fine lattice   */
+    LATTICE_STAGE_DEFORM_BACKWARD = 13,
+    LATTICE_STAGE_DISTRIBUTE_BACKWARD = 14
 };
 lattice_status lattice_set_timing(lattice *L, int mode);
 lattice_status lattice_get_timing(lattice *L, double *ms, int64_t *count);

@@ -540,6 +540,23 @@ def upsample(coarse: Lattice, fine: Lattice, values: np.ndarray, weight: np.ndar
     return conv(values, up_neighbors(coarse, fine), weight, bias)
 
 
+def downsample_backward(fine: Lattice, coarse: Lattice, values: np.ndarray, weight: np.ndarray,
+                        grad_out: np.ndarray):
+    """Gradients of downsample (a linear map of the fine values and of the
+    weights): conv_backward over the coarse vertices' table into the fine
+    lattice.  values [V_fine, C_in] is the forward input, grad_out
+    [V_coarse, C_out].  Returns conv_backward's six arrays (grad_x has the
+    fine lattice's V rows)."""
+    return conv_backward(values, down_neighbors(fine, coarse), weight, grad_out)
+
+
+def upsample_backward(coarse: Lattice, fine: Lattice, values: np.ndarray, weight: np.ndarray,
+                      grad_out: np.ndarray):
+    """Gradients of upsample: conv_backward over the fine vertices' table into
+    the coarse lattice (values [V_coarse, C_in], grad_out [V_fine, C_out])."""
+    return conv_backward(values, up_neighbors(coarse, fine), weight, grad_out)
+
+
 # ---------------------------------------------------------------------------
 # Distribute and PointNet (Sec. "Proposed Operations": Distribute, Eq.
 # distribute; the network figure's PointNet block; Sec. "Performance"

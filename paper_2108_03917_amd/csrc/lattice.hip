@@ -623,11 +623,9 @@ lattice_status lattice_conv_backward_noalloc(lattice *L, const void *grad_out, l
                              grad_bias, nch, ws, reinterpret_cast<float *>(ws + flip_bytes));
 }
 
-// Down (up = false) or upsampling from `src` onto the vertices of `dst`.
-static lattice_status resample(lattice *src, lattice *dst, bool up, const void *in, lattice_dtype in_dtype, int C_in,
-                               const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
-                               lattice_dtype out_dtype) {
-    const char *what = up ? "upsample" : "downsample";
+// Checks of a lattice pair for down (up = false) or upsampling from `src`
+// onto the vertices of `dst`.
+static lattice_status resample_pair(lattice *src, lattice *dst, bool up, const char *what) {
     if (!src || !dst) return LATTICE_E_ARG;
     if (!src->splatted || !dst->splatted) {
         set_err(dst, "%s: both lattices must be splatted first", what);
@@ -649,17 +647,14 @@ static lattice_status resample(lattice *src, lattice *dst, bool up, const void *
                 "(source and destination in the order of the call)", what);
         return LATTICE_E_ARG;
     }
-    if (!in || !w || !out || C_in < 1 || C_in > 1024 || C_out < 1 || C_out > 1024 ||
-        (dt != LATTICE_F32 && dt != LATTICE_BF16) || (in_dtype != LATTICE_F32 && in_dtype != LATTICE_BF16) ||
-        (out_dtype != LATTICE_F32 && out_dtype != LATTICE_BF16) || in == out) {
-        set_err(dst, "%s: bad argument (C_in = %d, C_out = %d)", what, C_in, C_out);
-        return LATTICE_E_ARG;
-    }
+    return LATTICE_OK;
+}
+
+// The table of `dst` (one row of T indices per vertex of dst) into the rows
+// of `src`: downsampling 2c' + offset_t, upsampling (u + offset_t) / 2.
+// Built on first use and again after either lattice is splatted.
+static lattice_status cross_table(lattice *dst, lattice *src, bool up, const char *what, int32_t **table) {
     const int k = up ? 1 : 0;
-    hipEvent_t t0;
-    const int stage = up ? LATTICE_STAGE_UPSAMPLE : LATTICE_STAGE_DOWNSAMPLE;
-    lattice_status s = timer_begin(dst, stage, &t0);
-    if (s) return s;
     if (!dst->xtab[k]) {
         if (hipMalloc(&dst->xtab[k], dst->max_vertices * (int64_t)dst->T * sizeof(int32_t)) != hipSuccess) {
             (void)hipGetLastError();
@@ -670,17 +665,108 @@ static lattice_status resample(lattice *src, lattice *dst, bool up, const void *
         dst->xsrc[k] = nullptr;
     }
     if (dst->xsrc[k] != src || dst->xsrc_gen[k] != src->gen || dst->xown_gen[k] != dst->gen) {
-        if ((s = check_launch(dst, launch_cross(dst, src, up, dst->xtab[k]), what))) return s;
+        lattice_status s = check_launch(dst, launch_cross(dst, src, up, dst->xtab[k]), what);
+        if (s) return s;
         dst->xsrc[k] = src;
         dst->xsrc_gen[k] = src->gen;
         dst->xown_gen[k] = dst->gen;
     }
+    *table = dst->xtab[k];
+    return LATTICE_OK;
+}
+
+// Down (up = false) or upsampling from `src` onto the vertices of `dst`.
+static lattice_status resample(lattice *src, lattice *dst, bool up, const void *in, lattice_dtype in_dtype, int C_in,
+                               const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
+                               lattice_dtype out_dtype) {
+    const char *what = up ? "upsample" : "downsample";
+    lattice_status s = resample_pair(src, dst, up, what);
+    if (s) return s;
+    if (!in || !w || !out || C_in < 1 || C_in > 1024 || C_out < 1 || C_out > 1024 ||
+        (dt != LATTICE_F32 && dt != LATTICE_BF16) || (in_dtype != LATTICE_F32 && in_dtype != LATTICE_BF16) ||
+        (out_dtype != LATTICE_F32 && out_dtype != LATTICE_BF16) || in == out) {
+        set_err(dst, "%s: bad argument (C_in = %d, C_out = %d)", what, C_in, C_out);
+        return LATTICE_E_ARG;
+    }
+    hipEvent_t t0;
+    const int stage = up ? LATTICE_STAGE_UPSAMPLE : LATTICE_STAGE_DOWNSAMPLE;
+    if ((s = timer_begin(dst, stage, &t0))) return s;
+    int32_t *table = nullptr;
+    if ((s = cross_table(dst, src, up, what, &table))) return s;
     // the conv kernels over the output lattice's vertices, reading rows of
     // the source lattice through the cross table
     lattice view = *dst;
-    view.nbr = dst->xtab[k];
+    view.nbr = table;
     if ((s = check_launch(dst, launch_conv(&view, in, in_dtype, C_in, w, C_out, dt, bias, out, out_dtype), what)))
         return s;
+    return timer_end(dst, stage, t0);
+}
+
+// Gradients of resample(src -> dst, up) given grad_out on dst's vertices.
+// Both are adjoints that reuse the forward kernels:
+//   grad_in (rows of src): the resampling in the other direction (dst -> src)
+//     of grad_out with W'[i][s][o] = W[o][flip(s)][i]: downsampling reads
+//     fine 2c' + offset_t, so fine u receives from the coarse c' with
+//     c' = (u - offset_t) / 2 = (u + offset_flip(t)) / 2, which is tap
+//     flip(t) of the upsampling table, and the other way round;
+//   grad_w, grad_bias: the conv weight gradient over dst's vertices with the
+//     forward's cross table (dW_t = sum over v of g_v^T x_{table(v,t)}).
+static lattice_status resample_backward(lattice *src, lattice *dst, bool up, const void *grad_out,
+                                        lattice_dtype g_dtype, int C_out, const void *w, int C_in, lattice_dtype dt,
+                                        const void *in, lattice_dtype in_dtype, void *grad_in,
+                                        lattice_dtype grad_in_dtype, float *grad_w, float *grad_bias) {
+    const char *what = up ? "upsample_backward" : "downsample_backward";
+    lattice_status s = resample_pair(src, dst, up, what);
+    if (s) return s;
+    if ((s = conv_backward_args(dst, grad_out, g_dtype, C_out, w, C_in, dt, in, in_dtype, grad_in, grad_in_dtype,
+                                grad_w, grad_bias, what)))
+        return s;
+    if (in && in == grad_in) {
+        set_err(dst, "%s: grad_in must not overlap the forward input", what);
+        return LATTICE_E_ARG;
+    }
+    const int T = dst->T;
+    const int nch = (grad_w || grad_bias) ? wgrad_chunks(dst, C_in, C_out) : 0;
+    if (grad_in) {
+        const int64_t esz = dt == LATTICE_BF16 ? 2 : 4;
+        if ((s = grow(src, &src->wflip, &src->wflip_bytes, (int64_t)C_out * T * C_in * esz, what))) return s;
+    }
+    if (grad_w || grad_bias) {
+        void *buf = dst->wgpart;
+        int64_t have = dst->wgpart_floats * (int64_t)sizeof(float);
+        const int64_t need = (int64_t)nch * ((int64_t)C_out * T * C_in + C_out) * (int64_t)sizeof(float);
+        s = grow(dst, &buf, &have, need, what);
+        dst->wgpart = reinterpret_cast<float *>(buf);
+        dst->wgpart_floats = have / (int64_t)sizeof(float);
+        if (s) return s;
+    }
+    hipEvent_t t0;
+    const int stage = up ? LATTICE_STAGE_UPSAMPLE_BACKWARD : LATTICE_STAGE_DOWNSAMPLE_BACKWARD;
+    if ((s = timer_begin(dst, stage, &t0))) return s;
+    if (grad_in) {
+        int32_t *back = nullptr;
+        if ((s = cross_table(src, dst, !up, what, &back))) return s;
+        if ((s = check_launch(src, launch_flip_weights(src, w, dt == LATTICE_BF16, C_out, C_in, src->wflip),
+                              what)))
+            return s;
+        lattice view = *src;
+        view.nbr = back;
+        if ((s = check_launch(src, launch_conv(&view, grad_out, g_dtype, C_out, src->wflip, C_in, dt, nullptr, grad_in,
+                                               grad_in_dtype),
+                              what)))
+            return s;
+    }
+    if (grad_w || grad_bias) {
+        int32_t *fwd = nullptr;
+        if ((s = cross_table(dst, src, up, what, &fwd))) return s;
+        lattice view = *dst;
+        view.nbr = fwd;
+        float *pbias = dst->wgpart + (int64_t)nch * C_out * T * C_in;
+        if ((s = check_launch(dst, launch_conv_wgrad(&view, grad_out, g_dtype, C_out, in, in_dtype, C_in, dt, nch,
+                                                     dst->wgpart, pbias, grad_w, grad_bias),
+                              what)))
+            return s;
+    }
     return timer_end(dst, stage, t0);
 }
 
@@ -694,6 +780,22 @@ lattice_status lattice_upsample(lattice *coarse, lattice *fine, const void *in, 
                                 const void *w, int C_out, lattice_dtype dt, const float *bias, void *out,
                                 lattice_dtype out_dtype) {
     return resample(coarse, fine, true, in, in_dtype, C_in, w, C_out, dt, bias, out, out_dtype);
+}
+
+lattice_status lattice_downsample_backward(lattice *fine, lattice *coarse, const void *grad_out,
+                                           lattice_dtype g_dtype, int C_out, const void *w, int C_in,
+                                           lattice_dtype dt, const void *in, lattice_dtype in_dtype, void *grad_in,
+                                           lattice_dtype grad_in_dtype, float *grad_w, float *grad_bias) {
+    return resample_backward(fine, coarse, false, grad_out, g_dtype, C_out, w, C_in, dt, in, in_dtype, grad_in,
+                             grad_in_dtype, grad_w, grad_bias);
+}
+
+lattice_status lattice_upsample_backward(lattice *coarse, lattice *fine, const void *grad_out, lattice_dtype g_dtype,
+                                         int C_out, const void *w, int C_in, lattice_dtype dt, const void *in,
+                                         lattice_dtype in_dtype, void *grad_in, lattice_dtype grad_in_dtype,
+                                         float *grad_w, float *grad_bias) {
+    return resample_backward(coarse, fine, true, grad_out, g_dtype, C_out, w, C_in, dt, in, in_dtype, grad_in,
+                             grad_in_dtype, grad_w, grad_bias);
 }
 
 lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,

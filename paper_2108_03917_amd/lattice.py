@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(_PKG, "_lib", "liblattice.so")
 OK, E_ARG, E_STATE, E_RANGE, E_CAPACITY, E_NOMEM, E_HIP = range(7)
 F32, BF16 = 0, 1
 STAGES = ("splat", "neighbors", "conv", "slice", "deform", "slice_backward", "conv_backward", "splat_backward",
-          "downsample", "upsample", "distribute")
+          "downsample", "upsample", "distribute", "downsample_backward", "upsample_backward", "deform_backward",
+          "distribute_backward")
 
 EXPORTS = (
     "lattice_create", "lattice_destroy", "lattice_max_vertices", "lattice_splat", "lattice_build_neighbors",
@@ -30,7 +31,8 @@ EXPORTS = (
     "lattice_get_timing", "lattice_hash_capacity", "lattice_dim", "lattice_status_string",
     "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice", "lattice_slice_backward",
     "lattice_splat_backward", "lattice_conv_backward", "lattice_downsample", "lattice_upsample",
-    "lattice_distribute_pointnet", "lattice_conv_backward_noalloc",
+    "lattice_distribute_pointnet", "lattice_conv_backward_noalloc", "lattice_downsample_backward",
+    "lattice_upsample_backward",
 )
 
 _lib = None
@@ -68,6 +70,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, ctypes.c_float, P, I, P]),
         "lattice_downsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_upsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
+        "lattice_downsample_backward": (St, [P, P, P, I, I, P, I, I, P, I, P, I, P, P]),
+        "lattice_upsample_backward": (St, [P, P, P, I, I, P, I, I, P, I, P, I, P, P]),
         "lattice_weights_to_bf16": (St, [P, P, I64, P]),
         "lattice_num_vertices": (St, [P, ctypes.POINTER(I64)]),
         "lattice_get_status": (St, [P]),
@@ -424,6 +428,58 @@ class Lattice:
         the vertices of ``fine``."""
         return self._resample(self._lib.lattice_upsample, self, fine, x, w, dtype, bias, out, out_dtype,
                               "upsample")
+
+    def _resample_backward(self, fn, src: "Lattice", dst: "Lattice", grad_out, w, x, dtype, want_input,
+                           want_weight, want_bias, grad_in_dtype, what):
+        _dev(grad_out, (torch.float32, torch.bfloat16), "grad_out")
+        if dtype == "f32":
+            _dev(w, torch.float32, "w")
+            dt = F32
+        elif dtype == "bf16":
+            _dev(w, torch.bfloat16, "w")
+            dt = BF16
+        else:
+            raise ValueError("dtype must be 'f32' or 'bf16'")
+        C_out, T, C_in = w.shape
+        n_in, n_out = src._rows_needed(), dst._rows_needed()
+        if T != self.taps or grad_out.dim() != 2 or grad_out.shape[1] != C_out or grad_out.shape[0] < n_out:
+            raise ValueError(f"w must be [C_out, {self.taps}, C_in], grad_out [>= {n_out}, C_out]")
+        if x is not None:
+            _dev(x, (torch.float32, torch.bfloat16), "x")
+            if x.dim() != 2 or x.shape[1] != C_in or x.shape[0] < n_in:
+                raise ValueError(f"x must be [>= {n_in}, {C_in}]")
+        if (want_weight or want_bias) and x is None:
+            raise ValueError("the weight and bias gradients need the forward input x")
+        dev_ = grad_out.device
+        gi = torch.empty((max(n_in, 1), C_in), dtype=_TORCH[grad_in_dtype], device=dev_) if want_input else None
+        gw = torch.empty((C_out, T, C_in), dtype=torch.float32, device=dev_) if want_weight else None
+        gb = torch.empty((C_out,), dtype=torch.float32, device=dev_) if want_bias else None
+        # both entry points take (source lattice, destination lattice) of the forward call
+        st = fn(src._h, dst._h, _ptr(grad_out), _STORAGE[grad_out.dtype], C_out, _ptr(w), C_in, dt, _ptr(x),
+                _STORAGE[x.dtype] if x is not None else F32, _ptr(gi), _STORAGE[gi.dtype] if gi is not None else F32,
+                _ptr(gw), _ptr(gb))
+        if st != OK:
+            msg = self._lib.lattice_last_error(dst._h)
+            raise LatticeError(st, f"{what}: {self._lib.lattice_status_string(st).decode()}: "
+                                   f"{msg.decode() if msg else ''}")
+        return gi, gw, gb
+
+    def downsample_backward(self, coarse: "Lattice", grad_out: torch.Tensor, w: torch.Tensor,
+                            x: Optional[torch.Tensor] = None, dtype: str = "f32", want_input: bool = True,
+                            want_weight: bool = True, want_bias: bool = False, grad_in_dtype: str = "f32"):
+        """Gradients of ``self.downsample(coarse, x, w)`` given ``grad_out`` on
+        the coarse vertices: (grad_in [rows of this lattice, C_in] or None,
+        grad_w [C_out, T, C_in] or None, grad_bias [C_out] or None)."""
+        return self._resample_backward(self._lib.lattice_downsample_backward, self, coarse, grad_out, w, x, dtype,
+                                       want_input, want_weight, want_bias, grad_in_dtype, "downsample_backward")
+
+    def upsample_backward(self, fine: "Lattice", grad_out: torch.Tensor, w: torch.Tensor,
+                          x: Optional[torch.Tensor] = None, dtype: str = "f32", want_input: bool = True,
+                          want_weight: bool = True, want_bias: bool = False, grad_in_dtype: str = "f32"):
+        """Gradients of ``self.upsample(fine, x, w)`` given ``grad_out`` on the
+        fine vertices."""
+        return self._resample_backward(self._lib.lattice_upsample_backward, self, fine, grad_out, w, x, dtype,
+                                       want_input, want_weight, want_bias, grad_in_dtype, "upsample_backward")
 
     # -- backward passes ------------------------------------------------
     def slice_backward(self, grad_out: torch.Tensor, out: Optional[torch.Tensor] = None,

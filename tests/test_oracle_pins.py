@@ -697,6 +697,40 @@ def test_upsample_is_adjoint_of_downsample(d, batched):
     assert (O.up_neighbors(coarse, fine) >= 0).sum() > fine.V // 2
 
 
+@pytest.mark.parametrize("d,batched", [(2, False), (3, True), (4, False)])
+def test_resample_backward_is_the_adjoint_and_the_weight_derivative(d, batched):
+    """Both resamplings are bilinear in (input, weights): for random x, W, g
+    <op(x, W), g> = <x, grad_x(g)> = <W, grad_w(g)>, and grad_bias = sum_v g_v
+    (the derivative of <op(x, W) + bias, g> in bias).  The input gradient of
+    each is also the other resampling with the flipped transposed weights,
+    the identity the GPU path computes it by."""
+    w = random_cloud(1500, d, 80 + d, extent=1.0, C=2, n_batch=2 if batched else 0)
+    sigma = {2: 0.08, 3: 0.15, 4: 0.3}[d]
+    fine = O.build(w.pos, sigma, batch=w.batch)
+    coarse = O.coarsen(w.pos, sigma, batch=w.batch)
+    T = 2 * (d + 1) + 1
+    rng = np.random.default_rng(90 + d)
+    for up in (False, True):
+        src, dst = (coarse, fine) if up else (fine, coarse)
+        C_in, C_out = 3, 2
+        W = rng.standard_normal((C_out, T, C_in))
+        x = rng.standard_normal((src.V, C_in))
+        g = rng.standard_normal((dst.V, C_out))
+        fwd = O.upsample if up else O.downsample
+        bwd = O.upsample_backward if up else O.downsample_backward
+        y, _ = fwd(src, dst, x, W)
+        gx, gw, gb, _, _, _ = bwd(src, dst, x, W, g)
+        ip = (y * g).sum()
+        assert gx.shape == x.shape and gw.shape == W.shape
+        assert np.isclose(ip, (x * gx).sum(), rtol=1e-10)
+        assert np.isclose(ip, (W * gw).sum(), rtol=1e-10)
+        yb, _ = fwd(src, dst, x, W, bias=np.ones(C_out))
+        assert np.allclose(gb, g.sum(axis=0)) and np.isclose(((yb - y) * g).sum(), gb.sum(), rtol=1e-10)
+        other = O.downsample if up else O.upsample
+        gx2, _ = other(dst, src, g, _flip_transpose(W, d))
+        assert np.allclose(gx, gx2, rtol=1e-12, atol=1e-12)
+
+
 def test_upsample_taps_follow_remainder_parity_in_3d():
     """d = 3: a vertex's coordinates share its remainder mod 4, so an
     even-remainder fine vertex u has u/2 integral and every (u +- n_j)/2
