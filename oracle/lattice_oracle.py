@@ -374,6 +374,88 @@ def deform_slice(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta:
     return (logits, delta, scale) + extra
 
 
+def deform_slice_backward(idx: np.ndarray, bary: np.ndarray, values: np.ndarray, w_delta: np.ndarray,
+                          b_delta: float, grad_out: np.ndarray, V: int, w_cls: Optional[np.ndarray] = None,
+                          b_cls: Optional[np.ndarray] = None):
+    """Gradients of deform_slice (with or without the classifier) given
+    grad_out = dL/dout [m, n_cls or C], float64, written from the forward's
+    steps in reverse:
+      classifier   gf_p = grad_out_p W_cls, dW_cls = grad_out^T f, db_cls = sum_p grad_out_p
+      slice        dx_pk += (b_pk + db_pk) gf_p,  ddb_pk = gf_p . x_pk
+      Tanh         darg_pk = ddb_pk (1 - db_pk^2)
+      Linear       dw_delta = sum_pk darg_pk (q_pk - mx_p),  db_delta = sum_pk darg_pk,
+                   d(q_pk - mx_p) = darg_pk w_delta
+      SubtractMax  dq_pk += darg_pk w_delta,  dmx_p = -(sum_k darg_pk) w_delta
+      MaxPool      dq_{p,k*,c} += dmx_{p,c} for k* the maximising vertex of channel c
+      Gather       dx_pk += b_pk dq_pk, and dX_v = sum of dx_pk over the pairs with v_pk = v
+    The max routes its gradient to one vertex per channel, a decision that
+    rounding can flip near a tie, so it is taken in float32 as a float32
+    evaluation makes it: on the products float32(b_pk) * float32(x_pk), the
+    first (lowest k) of equal maxima winning.  Invalid vertices (index -1)
+    read a zero row and receive nothing.
+    Returns (dX [V, C], dw_delta [C], db_delta, dW_cls or None, db_cls or
+    None) and their scales (dX_scale, dw_scale, db_scale, dW_cls_scale,
+    db_cls_scale): sums of |terms|, with the offsets' rounding (the forward's
+    tanh-argument scale) carried through b + db and 1 - db^2."""
+    idx = np.asarray(idx, dtype=np.int64)
+    b = np.asarray(bary, dtype=np.float64)
+    X = np.asarray(values, dtype=np.float64)
+    w = np.asarray(w_delta, dtype=np.float64)
+    G = np.asarray(grad_out, dtype=np.float64)
+    m, dp1 = idx.shape
+    C = X.shape[1]
+    valid = idx >= 0
+    rows = np.zeros((m, dp1, C))
+    rows[valid] = X[idx[valid]]
+    # forward quantities
+    q = b[:, :, None] * rows
+    mx = q.max(axis=1)
+    diff = q - mx[:, None, :]
+    delta = np.tanh(b_delta + diff @ w)
+    f = ((b + delta)[:, :, None] * rows).sum(axis=1)
+    _, _, f_scale, arg_scale = deform_slice(idx, bary, values, w_delta, b_delta, with_delta_scale=True)
+    # the maximising vertex of each channel, decided in float32
+    q32 = np.asarray(bary, dtype=np.float32)[:, :, None] * rows.astype(np.float32)
+    am = q32.argmax(axis=1)                                   # first of equal maxima
+    onehot = am[:, None, :] == np.arange(dp1)[None, :, None]  # [m, dp1, C]
+    # classifier
+    if w_cls is not None:
+        Wc = np.asarray(w_cls, dtype=np.float64)
+        gf = G @ Wc
+        gs = np.abs(G) @ np.abs(Wc)
+        dWc = G.T @ f
+        dWc_s = np.abs(G).T @ (f_scale + np.abs(f))
+        dbc = G.sum(axis=0)
+        dbc_s = np.abs(G).sum(axis=0)
+    else:
+        gf, gs = G, np.abs(G)
+        dWc = dWc_s = dbc = dbc_s = None
+    # slice, Tanh
+    ddelta = np.einsum("pkc,pc->pk", rows, gf)
+    darg = ddelta * (1.0 - delta ** 2)
+    S = darg.sum(axis=1)
+    # Linear
+    dw = np.einsum("pk,pkc->c", darg, diff)
+    dbd = darg.sum()
+    # SubtractMax, MaxPool, Gather: the gradient of each pair's row
+    dx = ((b + delta)[:, :, None] * gf[:, None, :]
+          + (b * darg)[:, :, None] * w[None, None, :]
+          - (b * S[:, None])[:, :, None] * onehot * w[None, None, :])
+    dX = np.zeros((V, C))
+    np.add.at(dX, idx[valid], dx[valid])
+    # scales
+    absrows = np.abs(rows)
+    dds = np.einsum("pkc,pc->pk", absrows, gs)
+    darg_s = dds + np.abs(ddelta) * 2.0 * np.abs(delta) * arg_scale
+    S_s = darg_s.sum(axis=1)
+    dx_s = ((np.abs(b) + np.abs(delta) + arg_scale)[:, :, None] * gs[:, None, :]
+            + (np.abs(b) * (darg_s + S_s[:, None]))[:, :, None] * np.abs(w)[None, None, :])
+    dX_s = np.zeros((V, C))
+    np.add.at(dX_s, idx[valid], dx_s[valid])
+    dw_s = np.einsum("pk,pkc->c", darg_s, np.abs(q) + np.abs(mx)[:, None, :])
+    return (dX, dw, dbd, dWc, dbc), (dX_s, dw_s, darg_s.sum(), dWc_s, dbc_s)
+
+
 # ---------------------------------------------------------------------------
 # Backward passes (Sec. "Implementation": the network is trained end to end,
 # so every lattice operation needs the gradient of a loss with respect to its

@@ -485,6 +485,77 @@ def test_deform_slice_is_permutation_equivariant():
     np.testing.assert_allclose(dl2, np.take_along_axis(dl, perm, axis=1), rtol=0, atol=0)
 
 
+@pytest.mark.parametrize("with_cls,invalid", [(True, False), (False, False), (True, True)])
+def test_deform_slice_backward_matches_autograd(with_cls, invalid):
+    """The hand-written backward of DeformSlice (and its classifier) against
+    torch autograd of the forward's formula in float64 (torch's max sends
+    its gradient to the index it returns, the first maximum, as the oracle
+    does).  Some simplex slots set to -1 (a failed insertion) read zero rows
+    and receive nothing."""
+    import torch
+
+    w = random_cloud(300, 3, seed=67, extent=1.0, C=1)
+    lat = O.build(w.pos, 0.15)
+    rng = np.random.default_rng(68)
+    C, n_cls = 6, 4
+    X = rng.standard_normal((lat.V, C))
+    wd = rng.standard_normal(C)
+    bd = 0.2
+    Wc = rng.standard_normal((n_cls, C)) if with_cls else None
+    bc = rng.standard_normal(n_cls) if with_cls else None
+    idx = lat.idx.copy()
+    if invalid:
+        idx[rng.random(idx.shape) < 0.05] = -1
+    G = rng.standard_normal((idx.shape[0], n_cls if with_cls else C))
+    (dX, dwd, dbd, dWc, dbc), _ = O.deform_slice_backward(idx, lat.bary, X, wd, bd, G, lat.V, Wc, bc)
+
+    Xt = torch.tensor(X, requires_grad=True)
+    wt = torch.tensor(wd, requires_grad=True)
+    bdt = torch.tensor(bd, dtype=torch.float64, requires_grad=True)
+    it = torch.tensor(idx)
+    b = torch.tensor(lat.bary)
+    rows = Xt[it.clamp(min=0)] * (it >= 0)[..., None]
+    q = b[..., None] * rows
+    mx, _ = q.max(dim=1)
+    delta = torch.tanh(bdt + (q - mx[:, None, :]) @ wt)
+    f = ((b + delta)[..., None] * rows).sum(1)
+    if with_cls:
+        Wct = torch.tensor(Wc, requires_grad=True)
+        bct = torch.tensor(bc, requires_grad=True)
+        out = f @ Wct.T + bct
+    else:
+        out = f
+    (out * torch.tensor(G)).sum().backward()
+    np.testing.assert_allclose(dX, Xt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dwd, wt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    assert np.isclose(dbd, bdt.grad.item(), rtol=1e-10)
+    if with_cls:
+        np.testing.assert_allclose(dWc, Wct.grad.numpy(), rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(dbc, bct.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def test_deform_slice_backward_max_routes_to_first_fp32_maximum():
+    """Two vertices whose products b x tie in float32 (but not in float64):
+    the max's gradient goes to the lower slot, by the float32 decision."""
+    idx = np.array([[0, 1]])
+    b = np.array([[0.5, 0.5]])
+    x0 = 1.0
+    x1 = 1.0 + 2.0 ** -30                  # equal to x0 in float32, larger in float64
+    X = np.array([[x0], [x1]])
+    G = np.array([[1.0]])
+    (dX, _, _, _, _), _ = O.deform_slice_backward(idx, b, X, np.array([1.0]), 0.0, G, 2)
+    # forward (float64): mx = q_1, db_0 = tanh(0.5 (x0 - x1)), db_1 = 0, gf = 1;
+    # dx_pk = (b + db_k) gf + b darg_k w - b S w [k == k*], darg_k = x_k (1 - db_k^2),
+    # S = darg_0 + darg_1, and k* = 0 (the float32 tie goes to the first slot)
+    db0 = np.tanh(0.5 * (x0 - x1))
+    darg = np.array([x0 * (1.0 - db0 ** 2), x1])
+    S = darg.sum()
+    want = [(0.5 + db0) + 0.5 * darg[0] - 0.5 * S, 0.5 + 0.5 * darg[1]]
+    np.testing.assert_allclose(dX[:, 0], want, rtol=0, atol=1e-15)
+    # with the decision taken in float64 the gradient would have gone to slot 1
+    assert abs(want[0] - (0.5 + db0 + 0.5 * darg[0])) > 0.5
+
+
 def test_deform_slice_identity_classifier():
     """An identity classifier with zero bias returns f itself."""
     w = random_cloud(100, 3, seed=65, extent=1.0, C=1)
