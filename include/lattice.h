@@ -300,6 +300,38 @@ lattice_status lattice_splat_backward(lattice *L, const void *grad_values, latti
                                       int normalize, const float *weight, float *grad_feat);
 
 /*
+ * lattice_deform_slice_backward -- gradients of lattice_deform_slice (Eq.
+ * deformSlice and the fused classifier) given g = dL/dout, through the
+ * forward's steps in reverse:
+ *   gf_p     = g_p W_cls (with the classifier) or g_p
+ *   dW_cls   = sum_p g_p^T f_p,      db_cls = sum_p g_p
+ *   darg_pk  = (gf_p . x_k)(1 - db_pk^2),  S_p = sum_k darg_pk
+ *   dw_delta = sum_pk darg_pk (q_pk - mx_p),  db_delta = sum_pk darg_pk
+ *   dx_pk    = (b_pk + db_pk) gf_p + b_pk w_delta (darg_pk - [k = k*] S_p),
+ *   dX_v     = sum of dx_pk over the pairs with v_pk = v,
+ * k* per channel the vertex whose product b x wins the max (the first of
+ * equal maxima of the fp32 products, as the forward computes them).  fp32
+ * throughout; the vertex gradient is pulled over the splat's pair lists (no
+ * atomics) and the weight gradients are summed in a fixed order.
+ *   values, values_dtype, C, w_delta, b_delta, w_cls, n_cls   as in the
+ *                 forward (C 1..1024; b_cls does not enter the gradients).
+ *   grad_out      dev fp32 [m][n_cls] with w_cls, else [m][C].
+ *   grad_values   dev [>= V][C] dX stored as grad_dtype, or NULL; must not
+ *                 overlap values or grad_out.
+ *   grad_w_delta  dev fp32 [C], or NULL.     grad_b_delta  dev fp32 [1], or NULL.
+ *   grad_w_cls    dev fp32 [n_cls][C], or NULL (needs w_cls).
+ *   grad_b_cls    dev fp32 [n_cls], or NULL (needs w_cls).
+ * At least one output.  Per-point records (5C + 12(d+1) bytes per point,
+ * 4C more with the classifier) are kept in the lattice's scratch, grown on
+ * demand.
+ */
+lattice_status lattice_deform_slice_backward(lattice *L, const void *values, lattice_dtype values_dtype, int C,
+                                             const float *w_delta, float b_delta, const float *w_cls, int n_cls,
+                                             const float *grad_out, void *grad_values, lattice_dtype grad_dtype,
+                                             float *grad_w_delta, float *grad_b_delta, float *grad_w_cls,
+                                             float *grad_b_cls);
+
+/*
  * lattice_conv_backward -- gradients of lattice_conv (Sec. "Common
  * Operations", Convolving):
  *   dL/dx_u[i]    = sum over (v, t) with nbr(v,t) = u of sum_o g_v[o] W[o][t][i]

@@ -21,7 +21,8 @@ LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "liblattice.so")
 ARCH = "gfx950"
 
-SOURCES = ["lattice.hip", "splat.hip", "neighbors.hip", "conv.hip", "slice.hip", "deform.hip", "backward.hip", "distribute.hip"]
+SOURCES = ["lattice.hip", "splat.hip", "neighbors.hip", "conv.hip", "slice.hip", "deform.hip", "deform_bwd.hip",
+           "backward.hip", "distribute.hip"]
 EXTRA = {"splat.hip": ["-ffp-contract=off"]}
 PEAKS_SRC = "peaks.hip"
 PEAKS = os.path.join(LIBDIR, "peaks")

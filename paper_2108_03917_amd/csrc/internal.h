@@ -84,6 +84,8 @@ struct lattice {
     int64_t wflip_bytes = 0;
     float *wgpart = nullptr;    // weight-gradient partials [chunks][C_out][T][C_in], then bias partials
     int64_t wgpart_floats = 0;
+    void *dfb = nullptr;        // DeformSlice backward: per-point records and partials (deform_bwd.hip)
+    int64_t dfb_bytes = 0;
     // Cross-lattice neighbour tables [max_vertices][T], built on demand:
     // xtab[0] when this lattice is the coarse output of a downsampling,
     // xtab[1] when it is the fine output of an upsampling.  Each remembers
@@ -176,6 +178,14 @@ int deform_max_channels(const void *values, lattice_dtype values_dt, int C, cons
 hipError_t launch_deform_slice(lattice *L, const void *values, lattice_dtype values_dt, int C, const float *w_delta,
                                float b_delta, const float *w_cls, const float *b_cls, int n_cls, float *out,
                                float *delta);
+
+// deform_bwd.hip
+int64_t deform_backward_scratch_bytes(const lattice *L, int C, int n_cls);
+hipError_t launch_deform_backward(lattice *L, const void *values, lattice_dtype values_dt, int C,
+                                  const float *w_delta, float b_delta, const float *w_cls, int n_cls,
+                                  const float *grad_out, void *grad_values, lattice_dtype grad_dt,
+                                  float *grad_w_delta, float *grad_b_delta, float *grad_w_cls, float *grad_b_cls,
+                                  void *scratch);
 
 // Workgroups are handed to the eight XCDs round robin (workgroup b runs on
 // XCD b % 8, checked on the device), and each XCD has its own L2.  Kernels

@@ -77,6 +77,7 @@ void free_all(lattice *L) {
     (void)hipFree(L->occ);
     (void)hipFree(L->vkeys);
     (void)hipFree(L->vslot);
+    (void)hipFree(L->dfb);
     (void)hipFree(L->blk);
     (void)hipFree(L->split);
     (void)hipFree(L->rowmap);
@@ -461,6 +462,39 @@ lattice_status lattice_deform_slice(lattice *L, const void *values, lattice_dtyp
                           "deform_slice")))
         return s;
     return timer_end(L, LATTICE_STAGE_DEFORM, t0);
+}
+
+lattice_status lattice_deform_slice_backward(lattice *L, const void *values, lattice_dtype values_dtype, int C,
+                                             const float *w_delta, float b_delta, const float *w_cls, int n_cls,
+                                             const float *grad_out, void *grad_values, lattice_dtype grad_dtype,
+                                             float *grad_w_delta, float *grad_b_delta, float *grad_w_cls,
+                                             float *grad_b_cls) {
+    if (!L) return LATTICE_E_ARG;
+    if (!L->splatted) {
+        set_err(L, "deform_slice_backward: no lattice yet (call lattice_splat first)");
+        return LATTICE_E_STATE;
+    }
+    auto bad_dt = [](lattice_dtype t) { return t != LATTICE_F32 && t != LATTICE_BF16; };
+    const bool any_out = grad_values || grad_w_delta || grad_b_delta || grad_w_cls || grad_b_cls;
+    if (C < 1 || C > 1024 || bad_dt(values_dtype) || bad_dt(grad_dtype) || (w_cls && (n_cls < 1 || n_cls > 256)) ||
+        (!w_cls && (grad_w_cls || grad_b_cls)) || !any_out || !values || !w_delta || (L->m > 0 && !grad_out) ||
+        (grad_values && (grad_values == values || grad_values == (const void *)grad_out))) {
+        set_err(L, "deform_slice_backward: bad argument (C = %d, n_cls = %d)", C, n_cls);
+        return LATTICE_E_ARG;
+    }
+    const int ncls = w_cls ? n_cls : 0;
+    lattice_status s = grow(L, &L->dfb, &L->dfb_bytes, deform_backward_scratch_bytes(L, C, ncls),
+                            "deform_slice_backward");
+    if (s) return s;
+    hipEvent_t t0;
+    if ((s = timer_begin(L, LATTICE_STAGE_DEFORM_BACKWARD, &t0))) return s;
+    if ((s = check_launch(L,
+                          launch_deform_backward(L, values, values_dtype, C, w_delta, b_delta, w_cls, ncls, grad_out,
+                                                 grad_values, grad_dtype, grad_w_delta, grad_b_delta, grad_w_cls,
+                                                 grad_b_cls, L->dfb),
+                          "deform_slice_backward")))
+        return s;
+    return timer_end(L, LATTICE_STAGE_DEFORM_BACKWARD, t0);
 }
 
 lattice_status lattice_slice_backward(lattice *L, const float *grad_out, int C, void *grad_values,

@@ -32,7 +32,7 @@ EXPORTS = (
     "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice", "lattice_slice_backward",
     "lattice_splat_backward", "lattice_conv_backward", "lattice_downsample", "lattice_upsample",
     "lattice_distribute_pointnet", "lattice_conv_backward_noalloc", "lattice_downsample_backward",
-    "lattice_upsample_backward",
+    "lattice_upsample_backward", "lattice_deform_slice_backward",
 )
 
 _lib = None
@@ -63,6 +63,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_conv": (St, [P, P, I, I, P, I, I, P, P, I]),
         "lattice_slice": (St, [P, P, I, I, P]),
         "lattice_deform_slice": (St, [P, P, I, I, P, ctypes.c_float, P, P, I, P, P]),
+        "lattice_deform_slice_backward": (St, [P, P, I, I, P, ctypes.c_float, P, I, P, P, I, P, P, P, P]),
         "lattice_slice_backward": (St, [P, P, I, P, I]),
         "lattice_splat_backward": (St, [P, P, I, I, I, P, P]),
         "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
@@ -585,6 +586,46 @@ class Lattice:
             _STORAGE[x.dtype] if x is not None else F32, _ptr(gi), _STORAGE[gi.dtype] if gi is not None else F32,
             _ptr(gw), _ptr(gb)), "conv_backward_noalloc" if noalloc else "conv_backward")
         return gi, gw, gb
+
+    def deform_slice_backward(self, values: torch.Tensor, w_delta: torch.Tensor, b_delta: float,
+                              grad_out: torch.Tensor, w_cls: Optional[torch.Tensor] = None,
+                              want_values: bool = True, want_w_delta: bool = True, want_b_delta: bool = True,
+                              want_cls: bool = True, grad_dtype: str = "f32"):
+        """Gradients of ``deform_slice(values, w_delta, b_delta, w_cls, b_cls)``
+        given ``grad_out`` (fp32 [m, n_cls] with ``w_cls``, else [m, C]).
+        Returns (grad_values [rows, C], grad_w_delta [C], grad_b_delta [1],
+        grad_w_cls [n_cls, C], grad_b_cls [n_cls]); unrequested ones (and the
+        classifier's without ``w_cls``) are None."""
+        _dev(values, (torch.float32, torch.bfloat16), "values")
+        need = self._rows_needed()
+        if values.dim() != 2 or values.shape[0] < need:
+            raise ValueError(f"values needs >= {need} rows")
+        C = values.shape[1]
+        _dev(w_delta, torch.float32, "w_delta")
+        if w_delta.numel() != C:
+            raise ValueError("w_delta needs C entries")
+        n_cls = 0
+        if w_cls is not None:
+            _dev(w_cls, torch.float32, "w_cls")
+            if w_cls.dim() != 2 or w_cls.shape[1] != C:
+                raise ValueError("w_cls needs [n_cls, C]")
+            n_cls = w_cls.shape[0]
+        width = n_cls if w_cls is not None else C
+        _dev(grad_out, torch.float32, "grad_out")
+        if grad_out.numel() < self.m * width:
+            raise ValueError(f"grad_out needs [m, {width}]")
+        dev_ = values.device
+        gv = torch.empty((max(need, 1), C), dtype=_TORCH[grad_dtype], device=dev_) if want_values else None
+        gw = torch.empty((C,), dtype=torch.float32, device=dev_) if want_w_delta else None
+        gb = torch.empty((1,), dtype=torch.float32, device=dev_) if want_b_delta else None
+        with_cls = want_cls and w_cls is not None
+        gwc = torch.empty((n_cls, C), dtype=torch.float32, device=dev_) if with_cls else None
+        gbc = torch.empty((n_cls,), dtype=torch.float32, device=dev_) if with_cls else None
+        self._check(self._lib.lattice_deform_slice_backward(
+            self._h, _ptr(values), _STORAGE[values.dtype], C, _ptr(w_delta), float(b_delta), _ptr(w_cls), n_cls,
+            _ptr(grad_out), _ptr(gv), _STORAGE[gv.dtype] if gv is not None else F32, _ptr(gw), _ptr(gb), _ptr(gwc),
+            _ptr(gbc)), "deform_slice_backward")
+        return gv, gw, gb, gwc, gbc
 
     def weights_to_bf16(self, w: torch.Tensor) -> torch.Tensor:
         """Round fp32 weights to bf16 (nearest even) with the library's kernel."""

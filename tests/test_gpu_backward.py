@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 import torch
 
-from datagen.clouds import conv_weight, make_workload, random_cloud, random_rows
+from datagen.clouds import conv_weight, deform_weights, make_workload, random_cloud, random_rows
 from oracle import lattice_oracle as O
 from tests.gpu_util import REL_BF16, REL_F32, GpuLattice, assert_close_scaled, to_dev
 
@@ -181,6 +181,66 @@ def test_conv_backward_empty_lattice():
                                  want_bias=True)
     torch.cuda.synchronize()
     assert torch.count_nonzero(gw) == 0 and torch.count_nonzero(gb) == 0
+
+
+@pytest.mark.parametrize("d,C,n_cls,bf16", [
+    (3, 64, 20, False), (3, 64, 0, False), (4, 64, 26, True), (2, 16, 3, False), (3, 200, 0, False),
+    (3, 1024, 5, False), (1, 5, 0, False), (3, 128, 64, True)])
+def test_deform_slice_backward_parity(d, C, n_cls, bf16):
+    """Every gradient of DeformSlice (and its classifier): the vertex values
+    (pulled over the pair lists), the offsets' weights and bias, the
+    classifier's weights and bias, against the oracle's float64 backward
+    (the max routed to the first float32 maximum, the decision the kernel
+    takes).  Shapes: one to sixteen channel chunks per lane, bf16 rows, d = 1..4."""
+    sigma = {1: 0.05, 2: 0.1, 3: 0.15, 4: 0.3}[d]
+    L, g, lat = _setup(d, 5000, sigma, seed=380 + d + C)
+    y = random_rows(lat.V, C, seed=381 + C)
+    if bf16:
+        y = O.round_bf16(y.astype(np.float32)).astype(np.float32)
+    yd = g.to_gpu_order(y)
+    if bf16:
+        yd = yd.to(torch.bfloat16)
+    dw = deform_weights(C, max(n_cls, 1), seed=382 + C)
+    with_cls = n_cls > 0
+    G = random_rows(L.m, n_cls if with_cls else C, seed=383 + C)
+    wc = to_dev(dw.w_cls) if with_cls else None
+    gv, gwd, gbd, gwc, gbc = L.deform_slice_backward(yd, to_dev(dw.w_delta), dw.b_delta, to_dev(G), wc)
+    (rX, rw, rb, rWc, rbc), (sX, sw, sb, sWc, sbc) = O.deform_slice_backward(
+        lat.idx, lat.bary, y, dw.w_delta, dw.b_delta, G, lat.V, dw.w_cls if with_cls else None)
+    tag = f"deform backward d={d} C={C} n_cls={n_cls} bf16={bf16}"
+    assert_close_scaled(g.from_gpu_order(gv), rX, sX, REL_F32, tag + " values")
+    assert_close_scaled(gwd.cpu().numpy(), rw, sw, REL_F32, tag + " w_delta")
+    assert_close_scaled(gbd.cpu().numpy(), np.array([rb]), np.array([sb]), REL_F32, tag + " b_delta")
+    if with_cls:
+        assert_close_scaled(gwc.cpu().numpy(), rWc, sWc, REL_F32, tag + " w_cls")
+        assert_close_scaled(gbc.cpu().numpy(), rbc, sbc, REL_F32, tag + " b_cls")
+    else:
+        assert gwc is None and gbc is None
+
+
+def test_deform_slice_backward_without_offsets_is_slice_backward():
+    """Zero offset weights and bias: db = 0, so the vertex gradient of the
+    point features is the slice's backward (the splat of grad_out), and the
+    offsets' weight gradient is sum_pk (gf . x_k)(q_pk - mx_p)."""
+    L, g, lat = _setup(3, 5000, 0.15, seed=390)
+    y = random_rows(lat.V, 32, seed=391)
+    G = random_rows(L.m, 32, seed=392)
+    z = torch.zeros(32, device="cuda:0")
+    gv, _, _, _, _ = L.deform_slice_backward(g.to_gpu_order(y), z, 0.0, to_dev(G))
+    ref = L.slice_backward(to_dev(G))
+    V = g.V
+    assert torch.allclose(gv[:V], ref[:V], rtol=1e-5, atol=1e-6)
+
+
+def test_deform_slice_backward_argument_checks():
+    from paper_2108_03917_amd import LatticeError
+
+    L, g, lat = _setup(3, 2000, 0.15, seed=393)
+    y = torch.zeros((L.max_vertices(), 8), device="cuda:0")
+    G = torch.zeros((L.m, 8), device="cuda:0")
+    with pytest.raises(LatticeError):     # no output requested
+        L.deform_slice_backward(y, torch.zeros(8, device="cuda:0"), 0.0, G, want_values=False, want_w_delta=False,
+                                want_b_delta=False)
 
 
 def test_backward_repeatable_bits():
