@@ -15,8 +15,9 @@
 
 struct __attribute__((aligned(16))) HEntry {
     unsigned long long key;  // 0 = empty
-    int32_t count;           // pairs (p, k) whose vertex k has this key
-    int32_t vid;             // vertex index (written by the thread that claimed the slot)
+    int32_t count;           // pairs (p, k) whose vertex k has this key; after the numbering,
+                             // the offset of the vertex's pair list (the count is then in vinfo)
+    int32_t vid;             // vertex index (written by the numbering)
 };
 static_assert(sizeof(HEntry) == 16, "hash entry is 16 bytes");
 

@@ -580,7 +580,9 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
         for (int i = 0; i < kPairsPerThread; ++i) {
             if (q[i].x) {
                 const int v = at.x;
-                tab[sl[i]].vid = v;
+                // the list offset replaces the count (read above; vinfo keeps
+                // it), so the fill finds both in one load of the entry
+                *reinterpret_cast<int2 *>(&tab[sl[i]].count) = make_int2(at.y, v);
                 vslot[v] = sl[i];
                 mark_taken(occ, sl[i]);
                 vkeys[v] = e[i].key;
@@ -607,18 +609,39 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_fill(int64_t n, int32_t *__restrict__ idx, const int32_t *__restrict__ rank,
                                                  const float *__restrict__ bary, const HEntry *__restrict__ tab,
-                                                 const int32_t *__restrict__ vinfo, int32_t *__restrict__ list) {
+                                                 int32_t *__restrict__ list) {
     constexpr int DP1 = D + 1;
+    constexpr int U = 2;  // pairs per thread whose loads are in flight together
     int64_t lo, hi;
     block_chunk(n, kBlock, lo, hi);
-    for (int64_t e = lo + threadIdx.x; e < hi; e += kBlock) {
-        const int s = idx[e];
-        if (s < 0) continue;
-        const int v = tab[s & (kCreator - 1)].vid;
-        idx[e] = v;
-        const int64_t at = (int64_t)vinfo[2 * v] + rank[e];
-        list[2 * at] = (int32_t)(e / DP1);
-        list[2 * at + 1] = __float_as_int(bary[e]);
+    for (int64_t e0 = lo + threadIdx.x; e0 < hi; e0 += U * kBlock) {
+        int s[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t e = e0 + u * kBlock;
+            s[u] = e < hi ? idx[e] : -1;
+        }
+        int2 ov[U];
+        int r[U];
+        float b[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t e = e0 + u * kBlock;
+            if (s[u] >= 0) {
+                ov[u] = *reinterpret_cast<const int2 *>(&tab[s[u] & (kCreator - 1)].count);  // (list offset, vertex)
+                r[u] = rank[e];
+                b[u] = bary[e];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t e = e0 + u * kBlock;
+            if (s[u] >= 0) {
+                idx[e] = ov[u].y;
+                const int64_t at = (int64_t)ov[u].x + r[u];
+                *reinterpret_cast<int2 *>(list + 2 * at) = make_int2((int32_t)(e / DP1), __float_as_int(b[u]));
+            }
+        }
     }
 }
 
@@ -1019,7 +1042,7 @@ hipError_t launch_fill(lattice *L, int64_t m) {
     return dispatch_d(L->d, [&](auto dc) {
         constexpr int D = decltype(dc)::value;
         hipLaunchKernelGGL(k_fill<D>, dim3(grid), dim3(kBlock), 0, L->stream, n, L->idx, L->rank, L->bary, L->tab,
-                           L->vinfo, L->list);
+                           L->list);
         return hipGetLastError();
     });
 }
