@@ -778,3 +778,100 @@ def distribute_pointnet(lat: Lattice, pos: np.ndarray, feat: Optional[np.ndarray
     scale = np.zeros_like(out)
     np.maximum.at(scale, v, sc)
     return out, scale, mu
+
+
+def _pointnet_forward_cache(lat: Lattice, pos, feat, layers, groups, eps):
+    """The forward of distribute_pointnet keeping what its backward needs,
+    float64: per block l the input h, the normalised xhat (h itself for the
+    fixed affine), the per-row normalisation factor 1/sqrt(var + eps) (1 for
+    the fixed affine), hn, the ReLU output r; the rows' vertices, clouds, and
+    the last block's output."""
+    h, v, p, seg, mu, _ = distribute_rows(lat, pos, feat)
+    blocks = []
+    for li, (a, s, W, b) in enumerate(layers):
+        a = np.asarray(a, dtype=np.float64)
+        s = np.asarray(s, dtype=np.float64)
+        W = np.asarray(W, dtype=np.float64)
+        b = np.asarray(b, dtype=np.float64)
+        K = h.shape[1]
+        if groups is None:
+            xhat, rstd, G = h, np.ones_like(h), None
+        else:
+            G = groups[li]
+            _, means, varis, samples = group_norm(h, seg, G, a, s, eps)
+            row = np.searchsorted(samples, seg)
+            mean = np.repeat(means, K // G, axis=1)[row]
+            rstd = 1.0 / np.sqrt(np.repeat(varis, K // G, axis=1)[row] + eps)
+            xhat = (h - mean) * rstd
+        hn = a * xhat + s
+        r = np.maximum(hn, 0.0)
+        blocks.append(dict(h=h, xhat=xhat, rstd=rstd, hn=hn, r=r, a=a, W=W, G=G))
+        h = r @ W.T + b
+    return blocks, h, v, seg
+
+
+def _group_mean(x: np.ndarray, seg: np.ndarray, G: int) -> np.ndarray:
+    """Per row, the mean of x over its cloud's rows and its group's channels."""
+    N, K = x.shape
+    out = np.empty_like(x)
+    for s_ in np.unique(seg):
+        rows = seg == s_
+        m = x[rows].reshape(-1, G, K // G).mean(axis=(0, 2))
+        out[rows] = np.repeat(m, K // G)[None, :]
+    return out
+
+
+def pointnet_backward_rows(blocks, seg, dh: np.ndarray):
+    """Backward of the PointNet blocks given dL/dh of the last block's rows
+    [E, w_L], float64.  Per block, from the last:
+      db = sum_rows dh,  dW = dh^T r,  dr = dh W,  dhn = dr [hn > 0];
+      normalisation hn = a xhat + s (a = gamma, s = beta with groups):
+        da = sum_rows dhn xhat,  ds = sum_rows dhn,
+        dh_prev = a dhn (fixed affine), or with group normalisation
+        (xhat = (h - mean) rstd over a cloud's rows and a group's channels)
+        dh_prev = rstd (g - mean(g) - xhat mean(g xhat)),  g = a dhn,
+        the means over the same rows and channels.
+    Returns [(da, ds, dW, db)] per block, in block order."""
+    out = []
+    for blk in reversed(blocks):
+        db = dh.sum(axis=0)
+        dW = dh.T @ blk["r"]
+        dr = dh @ blk["W"]
+        dhn = dr * (blk["hn"] > 0)
+        da = (dhn * blk["xhat"]).sum(axis=0)
+        ds = dhn.sum(axis=0)
+        g = blk["a"] * dhn
+        if blk["G"] is None:
+            dh = g
+        else:
+            G = blk["G"]
+            dh = blk["rstd"] * (g - _group_mean(g, seg, G) - blk["xhat"] * _group_mean(g * blk["xhat"], seg, G))
+        out.append((da, ds, dW, db))
+    return out[::-1]
+
+
+def distribute_pointnet_backward(lat: Lattice, pos: np.ndarray, feat: Optional[np.ndarray], layers,
+                                 grad_out: np.ndarray, groups=None, eps: float = 1e-5):
+    """Gradients of distribute_pointnet with respect to every block's
+    parameters (gamma and beta, or a and s; W; b) given grad_out = dL/dx
+    [V, w_L], float64.  The max sends grad_out[v, c] to the row of v whose
+    channel c is largest (the first such row in row order).  The positions
+    and features are the network's raw inputs and get no gradient.
+    Returns ([(da, ds, dW, db)] per block, argmax [V, w_L] row indices,
+    last-block rows [E, w_L], the rows' vertices [E], the forward cache,
+    the rows' clouds)."""
+    blocks, h3, v, seg = _pointnet_forward_cache(lat, pos, feat, layers, groups, eps)
+    E, w = h3.shape
+    g = np.asarray(grad_out, dtype=np.float64)
+    order = np.argsort(v, kind="stable")                   # rows grouped by vertex, row order kept
+    am = np.full((lat.V, w), -1, dtype=np.int64)
+    starts = np.searchsorted(v[order], np.arange(lat.V))
+    ends = np.searchsorted(v[order], np.arange(lat.V), side="right")
+    for vv in range(lat.V):
+        rows = order[starts[vv]:ends[vv]]
+        if len(rows):
+            am[vv] = rows[np.argmax(h3[rows], axis=0)]     # first maximum in row order
+    dh = np.zeros((E, w))
+    vv, cc = np.nonzero(am >= 0)
+    np.add.at(dh, (am[vv, cc], cc), g[vv, cc])
+    return pointnet_backward_rows(blocks, seg, dh), am, h3, v, blocks, seg

@@ -1024,6 +1024,57 @@ def test_distribute_pointnet_gn_matches_torch(n_batch):
     assert not np.allclose(out, out2, rtol=1e-3, atol=1e-3)
 
 
+@pytest.mark.parametrize("n_batch,use_groups", [(0, True), (3, True), (0, False)])
+def test_distribute_pointnet_backward_matches_autograd(n_batch, use_groups):
+    """The hand-written backward of the PointNet blocks (group normalisation
+    or the fixed affine, ReLU, the 1x1 layers, the per-vertex max) against
+    torch autograd of the forward built from torch primitives, float64:
+    every block's gamma / a, beta / s, W and b.  torch's amax sends the
+    gradient to the maximum (evenly among exact ties; random data has none)."""
+    torch = pytest.importorskip("torch")
+    from datagen.clouds import pointnet_gn_weights
+
+    w, lat = _small_lattice(d=3, m=800, seed=87, C=2, n_batch=n_batch)
+    layers = pointnet_gn_weights(3 + 2, seed=88)
+    groups = [O.default_groups(k) for k in (5, 16, 32)] if use_groups else None
+    rng = np.random.default_rng(89)
+    G = rng.standard_normal((lat.V, 64))
+    grads, am, h3, v, _, _ = O.distribute_pointnet_backward(lat, w.pos, w.feat, layers, G, groups=groups, eps=1e-5)
+
+    m, dp1 = lat.idx.shape
+    vt = torch.from_numpy(lat.idx.ravel())
+    p = torch.arange(m).repeat_interleave(dp1)
+    g = torch.from_numpy(w.pos.astype(np.float64))
+    tmu = torch.zeros((lat.V, 3), dtype=torch.float64).index_reduce_(0, vt, g[p], "mean", include_self=False)
+    h = torch.cat([g[p] - tmu[vt], torch.from_numpy(w.feat.astype(np.float64))[p]], dim=1)
+    seg = torch.from_numpy(lat.vbatch)[vt] if lat.vbatch is not None else torch.zeros(len(vt), dtype=torch.int64)
+    params = []
+    for li, (ga, be, W, b) in enumerate(layers):
+        ga, be, W, b = (torch.tensor(np.asarray(x, np.float64), requires_grad=True) for x in (ga, be, W, b))
+        params.append((ga, be, W, b))
+        if use_groups:
+            parts = []
+            hn = torch.zeros_like(h)
+            for s_ in torch.unique(seg):
+                rows = torch.nonzero(seg == s_)[:, 0]
+                gn = torch.nn.functional.group_norm(h[rows].T[None], groups[li], ga, be, eps=1e-5)[0].T
+                hn = hn.index_put((rows,), gn)
+        else:
+            hn = ga * h + be
+        h = torch.nn.functional.linear(torch.relu(hn), W, b)
+    out = torch.zeros((lat.V, 64), dtype=torch.float64).index_reduce(0, vt, h, "amax", include_self=False)
+    (out * torch.from_numpy(G)).sum().backward()
+    for (da, ds, dW, db), (ga, be, W, b) in zip(grads, params):
+        np.testing.assert_allclose(da, ga.grad.numpy(), rtol=1e-9, atol=1e-9)
+        np.testing.assert_allclose(ds, be.grad.numpy(), rtol=1e-9, atol=1e-9)
+        np.testing.assert_allclose(dW, W.grad.numpy(), rtol=1e-9, atol=1e-9)
+        np.testing.assert_allclose(db, b.grad.numpy(), rtol=1e-9, atol=1e-9)
+    # the max's rows: each vertex's winning row is one of its own, and holds the forward's value
+    out_ref, _, _ = O.distribute_pointnet(lat, w.pos, w.feat, layers, groups=groups, eps=1e-5)
+    assert np.all(v[am] == np.arange(lat.V)[:, None])
+    np.testing.assert_allclose(np.take_along_axis(h3, am, axis=0), out_ref, rtol=0, atol=1e-12)
+
+
 def test_distribute_pointnet_gn_statistics_are_per_cloud():
     """A batched lattice normalises each batch id over its own rows: the
     output equals the clouds run one by one, and a cloud whose positions are
