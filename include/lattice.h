@@ -528,6 +528,37 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
                                            float eps, void *out, lattice_dtype out_dtype, float *mean);
 
 /*
+ * lattice_distribute_pointnet_backward -- gradients of
+ * lattice_distribute_pointnet with respect to every block's parameters, given
+ * grad_out = dL/dx (the network trains end to end, Sec. "Implementation").
+ * The max sends grad_out[v][c] to the row of v whose last-block output c is
+ * largest (the first such row of v's pair list); then, from the last block:
+ *   db = sum_rows dh,  dW = dh^T r,  dr = dh W,  dhn = dr [hn > 0],
+ *   d(gamma or a) = sum_rows dhn xhat,  d(beta or s) = sum_rows dhn,
+ *   with group normalisation (xhat = (h - mean) rstd per cloud and group)
+ *   dh_prev = rstd (gn - mean(gn) - xhat mean(gn xhat)),  gn = gamma dhn,
+ *   the means over the cloud's rows and the group's channels; with the
+ *   fixed affine dh_prev = a dhn.
+ * The positions and features are the network's raw inputs and get no
+ * gradient.  The call first runs the forward (its statistics and affines),
+ * then recomputes each row's activations in fp32.  Sums are fp32 per
+ * wavefront, the partial sums added in a fixed order in fp64: two calls on
+ * the same inputs give identical bits.
+ *   pos, feat, f_d, params, n_blocks, widths, groups, eps   as in the forward.
+ *   grad_out     dev fp32 [>= V][64] dL/dx.
+ *   grad_params  dev fp32 output in the layout of params (per block:
+ *                d(gamma or a) [K], d(beta or s) [K], dW [w][K], db [w]);
+ *                must not overlap params.
+ * The first call grows the lattice's scratch for it (a record of 512 bytes
+ * per pair and the partial sums).  Returns as the forward, and
+ * LATTICE_E_ARG for a missing grad_out or grad_params.
+ */
+lattice_status lattice_distribute_pointnet_backward(lattice *L, const float *pos, const float *feat, int f_d,
+                                                    const float *params, int n_blocks, const int *widths,
+                                                    const int *groups, float eps, const float *grad_out,
+                                                    float *grad_params);
+
+/*
  * lattice_weights_to_bf16 -- round n fp32 values to bf16 (nearest, ties to
  * even) on the lattice's stream: the weight format LATTICE_BF16 convs take.
  *   src  dev [n] fp32;  dst  dev [n] uint16 (bf16 bit patterns).

@@ -932,6 +932,458 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
     }
 }
 
+// ---------------------------------------------------------------------------
+// Backward of the PointNet blocks: the gradients of every block's parameters
+// (gamma and beta, or a and s; W; b) given g = dL/dx [V][64].  The positions
+// and features are the network's raw inputs and get none.  With the forward
+// run first (its statistics, affines, local means and entry-to-vertex map),
+// per entry e of vertex v (one row):
+//   k_dpn_norm     per cloud and block, each input channel's group mean and
+//                  1 / sqrt(var + eps) from the fp64 sums (mean 0, 1 for the
+//                  fixed affine)
+//   k_dpn_rows     the record of e: block inputs h0 (padded), h1, h2 and the
+//                  last block's output h3, fp32
+//   k_dpn_argmax   one wavefront per vertex, lane = channel c: the row whose
+//                  h3[c] is largest (the first in list order), which receives
+//                  g[v][c]; dW3[c][.] += g r3 and db3[c] += g of that row
+//   k_dpn_back<S>  one lane per entry: dh3 (its routed channels), then back
+//                  through block 3 (S = 3: dgamma3, dbeta3 and the group
+//                  sums of gamma dhn and gamma dhn xhat), through block 2
+//                  (S = 2: needs block 3's group means; dW2, db2, dgamma2,
+//                  dbeta2, block 2's group sums) or through block 1 (S = 1:
+//                  dW1, db1, dgamma1, dbeta1).  A group normalisation's input
+//                  gradient is rstd (gn - mean(gn) - xhat mean(gn xhat)),
+//                  gn = gamma dhn, the means over the cloud's rows and the
+//                  group's channels.
+// Sums over entries: per wavefront (shuffles; a wavefront whose rows span
+// clouds adds each cloud's lanes apart) into the wavefront's own LDS row, in
+// the order of its chunks; the workgroup's rows added in wavefront order
+// into one partial row per workgroup (or wavefront), and those added in a
+// fixed order (k_dpn_reduce): the gradients do not depend on scheduling.
+// Lanes past the last entry add zeros: with group normalisation an input
+// gradient has mean terms even where no output gradient reaches the row, so
+// such lanes zero theirs explicitly.
+constexpr int kNrmRow = 3 * 2 * 32;              // per cloud: (mean, rstd) per block and input channel
+constexpr int kRecH1 = kMaxK0, kRecH2 = kRecH1 + kW1, kRecH3 = kRecH2 + kW2, kRec = kRecH3 + kW3;
+constexpr int kPArg = kW3 * kW2 + kW3;                           // per wavefront: dW3, db3
+constexpr int kPB3 = 2 * kW2 + kGnClouds * kW2 * 2;              // dgamma3, dbeta3, group sums
+constexpr int kPB2 = kW2 * kW1 + kW2 + 2 * kW1 + kGnClouds * kW1 * 2;  // dW2, db2, dgamma2, dbeta2, group sums
+constexpr int kPB1 = kW1 * kMaxK0 + kW1 + 2 * kMaxK0;            // dW1, db1, dgamma1, dbeta1
+
+__device__ __forceinline__ float wave_sum_f(float x) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) x += __shfl_xor(x, o);
+    return x;
+}
+
+// Block l's input width (l = 0, 1, 2) and its padded width.
+__host__ __device__ __forceinline__ int in_width(int l, int k0) { return l == 0 ? k0 : (l == 1 ? kW1 : kW2); }
+__host__ __device__ __forceinline__ int in_padded(int l) { return l == 2 ? kW2 : kMaxK0; }
+
+__global__ __launch_bounds__(kBlock) void k_dpn_norm(const double *__restrict__ stats,
+                                                     const int32_t *__restrict__ counters, int batched, int use_gn,
+                                                     int k0, int G0, int G1, int G2, float eps,
+                                                     float *__restrict__ nrm, double *__restrict__ rows_out) {
+    const int lane = threadIdx.x & 63;
+    const int64_t n = (int64_t)num_clouds(counters, batched) * 3 * 32;
+    const int ncopy = batched ? kSpreadB : kSpread;
+    for (int64_t i = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6; i < n; i += (int64_t)gridDim.x * kWaves) {
+        const int b = (int)(i / 96);
+        const int l = (int)(i % 96) / 32;
+        const int c = (int)(i % 32);
+        const int K = in_width(l, k0);
+        const int G = l == 0 ? G0 : (l == 1 ? G1 : G2);
+        float mean = 0.f, rstd = 1.f;
+        double rows = 0.0;
+        if (use_gn) {
+            const int sum_off = l == 0 ? kSum0 : (l == 1 ? kSum1 : kSum2);
+            const int sq_off = l == 0 ? kSq0 : (l == 1 ? kSq1 : kSq2);
+            const int gs = K / G;
+            double sum = 0.0, sq = 0.0;
+            if (lane < ncopy) {
+                const double *st = stats + stat_row(lane, b, batched) * kStatRow;
+                rows = st[kCount];
+                if (c < K) {
+                    const int c0 = c / gs * gs;
+                    for (int j = c0; j < c0 + gs; ++j) {
+                        sum += st[sum_off + j];
+                        sq += st[sq_off + j];
+                    }
+                }
+            }
+            rows = wave_sum(rows);
+            sum = wave_sum(sum);
+            sq = wave_sum(sq);
+            if (c < K && rows > 0.0) {
+                const double cnt = rows * gs;
+                const double m = sum / cnt;
+                double var = sq / cnt - m * m;
+                var = var > 0.0 ? var : 0.0;
+                mean = (float)m;
+                rstd = (float)(1.0 / sqrt(var + (double)eps));
+            }
+        }
+        if (lane == 0) {
+            nrm[(int64_t)b * kNrmRow + l * 64 + 2 * c] = mean;
+            nrm[(int64_t)b * kNrmRow + l * 64 + 2 * c + 1] = rstd;
+            if (l == 0 && c == 0) rows_out[b] = rows;
+        }
+    }
+}
+
+// Stage the padded parameters in LDS.
+__device__ __forceinline__ void load_params(const float *__restrict__ P, float *Ps) {
+    for (int i = threadIdx.x; i < kPadded; i += kBlock) Ps[i] = P[i];
+    __syncthreads();
+}
+
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_dpn_rows(const int32_t *__restrict__ list, const int32_t *__restrict__ lvert,
+                                                     const uint64_t *__restrict__ vkeys, int batched,
+                                                     const float *__restrict__ pos, const float *__restrict__ feat,
+                                                     int f_d, const float *__restrict__ mu,
+                                                     const float *__restrict__ P, const float *__restrict__ aff,
+                                                     const int32_t *__restrict__ counters, float *__restrict__ rec) {
+    __shared__ float Ps[kPadded];
+    load_params(P, Ps);
+    const int64_t E = counters[CNT_E];
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < E; e += (int64_t)gridDim.x * kBlock) {
+        const int64_t p = list[2 * e];
+        const int v = lvert[e];
+        const float *A = aff + (int64_t)cloud_of(vkeys, batched, v) * kAffRow;
+        float h0[kMaxK0], h1[kW1], h2[kW2];
+#pragma unroll
+        for (int j = 0; j < kMaxK0; ++j) {
+            float x = 0.f;
+            if (j < D) x = pos[p * D + j] - mu[(int64_t)v * D + j];
+            else if (j < D + f_d) x = feat[p * f_d + (j - D)];
+            h0[j] = x;
+        }
+        float r[kW2];
+#pragma unroll
+        for (int c = 0; c < kMaxK0; ++c) r[c] = relu(fmaf(A[kAff0 + c], h0[c], A[kAff0 + kMaxK0 + c]));
+#pragma unroll
+        for (int o = 0; o < kW1; ++o) {
+            float s = Ps[kB0 + o];
+#pragma unroll
+            for (int c = 0; c < kMaxK0; ++c) s = fmaf(Ps[kWt0 + o * kMaxK0 + c], r[c], s);
+            h1[o] = s;
+        }
+#pragma unroll
+        for (int c = 0; c < kW1; ++c) r[c] = relu(fmaf(A[kAff1 + c], h1[c], A[kAff1 + kW1 + c]));
+#pragma unroll
+        for (int o = 0; o < kW2; ++o) {
+            float s = Ps[kB1 + o];
+#pragma unroll
+            for (int c = 0; c < kW1; ++c) s = fmaf(Ps[kWt1 + o * kW1 + c], r[c], s);
+            h2[o] = s;
+        }
+#pragma unroll
+        for (int c = 0; c < kW2; ++c) r[c] = relu(fmaf(A[kAff2 + c], h2[c], A[kAff2 + kW2 + c]));
+        float *R = rec + e * kRec;
+#pragma unroll
+        for (int j = 0; j < kMaxK0; ++j) R[j] = h0[j];
+#pragma unroll
+        for (int j = 0; j < kW1; ++j) R[kRecH1 + j] = h1[j];
+#pragma unroll
+        for (int j = 0; j < kW2; ++j) R[kRecH2 + j] = h2[j];
+        for (int o = 0; o < kW3; ++o) {
+            float s = Ps[kB2 + o];
+#pragma unroll
+            for (int c = 0; c < kW2; ++c) s = fmaf(Ps[kWt2 + o * kW2 + c], r[c], s);
+            R[kRecH3 + o] = s;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict__ vinfo,
+                                                       const uint64_t *__restrict__ vkeys, int batched,
+                                                       const float *__restrict__ aff, const float *__restrict__ rec,
+                                                       const float *__restrict__ grad_out,
+                                                       const int32_t *__restrict__ counters, int32_t *__restrict__ am,
+                                                       float *__restrict__ part) {
+    const int lane = threadIdx.x & 63;  // output channel c
+    const int64_t V = counters[CNT_V];
+    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
+    float dw[kW2], db = 0.f;
+#pragma unroll
+    for (int j = 0; j < kW2; ++j) dw[j] = 0.f;
+    for (int64_t v = wave; v < V; v += nwaves) {
+        const int64_t off = vinfo[2 * v];
+        const int cnt = vinfo[2 * v + 1];
+        float best = 0.f;
+        int64_t be = off;
+        for (int i = 0; i < cnt; ++i) {
+            const float x = rec[(off + i) * kRec + kRecH3 + lane];
+            if (i == 0 || x > best) {
+                best = x;
+                be = off + i;
+            }
+        }
+        am[v * kW3 + lane] = (int32_t)be;
+        const float g = grad_out[v * kW3 + lane];
+        db += g;
+        const float *A = aff + (int64_t)cloud_of(vkeys, batched, (int)v) * kAffRow;
+        const float *R = rec + be * kRec + kRecH2;
+#pragma unroll
+        for (int j = 0; j < kW2; ++j) dw[j] = fmaf(g, relu(fmaf(A[kAff2 + j], R[j], A[kAff2 + kW2 + j])), dw[j]);
+    }
+    float *out = part + wave * kPArg;
+#pragma unroll
+    for (int j = 0; j < kW2; ++j) out[lane * kW2 + j] = dw[j];
+    out[kW3 * kW2 + lane] = db;
+}
+
+// Add a wavefront's per-lane values of one slot into the wavefront's own LDS
+// row (lane 0 adds, in program order).
+__device__ __forceinline__ void wave_add(float *acc, int q, float x) {
+    x = wave_sum_f(x);
+    if ((threadIdx.x & 63) == 0) acc[q] += x;
+}
+
+// The group sums of one block: per channel j < K, x[j] and x[j] y[j] added
+// to the slots q0 + (cloud * K + j / gs) * 2 and that + 1 of the lanes'
+// clouds.  A wavefront within one cloud adds once; one that spans clouds
+// adds each cloud's lanes apart (masked sums, the clouds in lane order).
+template <int K>
+__device__ __forceinline__ void wave_add_groups(float *acc, int q0, int gs, int cloud, bool live, bool one_cloud,
+                                                const float *x, const float *y) {
+    if (one_cloud) {
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const int q = q0 + (cloud * K + j / gs) * 2;
+            wave_add(acc, q, x[j]);
+            wave_add(acc, q + 1, x[j] * y[j]);
+        }
+        return;
+    }
+    unsigned long long todo = __ballot(live);
+    while (todo) {
+        const int cb = __shfl(cloud, __builtin_ctzll(todo));
+        const bool mine = live && cloud == cb;
+        todo &= ~__ballot(mine);
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const int q = q0 + (cb * K + j / gs) * 2;
+            wave_add(acc, q, mine ? x[j] : 0.f);
+            wave_add(acc, q + 1, mine ? x[j] * y[j] : 0.f);
+        }
+    }
+}
+
+template <int S>
+__global__ __launch_bounds__(kBlock) void k_dpn_back(const int32_t *__restrict__ lvert,
+                                                     const uint64_t *__restrict__ vkeys, int batched, int use_gn,
+                                                     int G1, int G2, const float *__restrict__ P,
+                                                     const float *__restrict__ aff, const float *__restrict__ nrm,
+                                                     const float *__restrict__ gm, const float *__restrict__ rec,
+                                                     const int32_t *__restrict__ am,
+                                                     const float *__restrict__ grad_out,
+                                                     const int32_t *__restrict__ counters, float *__restrict__ part) {
+    constexpr int NP = S == 3 ? kPB3 : (S == 2 ? kPB2 : kPB1);
+    __shared__ float Ps[kPadded];
+    __shared__ float accs[kWaves * NP];  // one row per wavefront
+    for (int i = threadIdx.x; i < kWaves * NP; i += kBlock) accs[i] = 0.f;
+    load_params(P, Ps);
+    const int lane = threadIdx.x & 63;
+    float *acc = accs + (threadIdx.x >> 6) * NP;
+    const int64_t E = counters[CNT_E];
+    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
+    const int gs3 = kW2 / G2, gs2 = kW1 / G1;  // channels per group of blocks 3 and 2
+    for (int64_t e0 = wave * 64; e0 < E; e0 += nwaves * 64) {
+        const int64_t e = e0 + lane;
+        const bool live = e < E;
+        const int v = live ? lvert[e] : 0;
+        const int cloud = cloud_of(vkeys, batched, v);
+        const float *A = aff + (int64_t)cloud * kAffRow;
+        const float *N = nrm + (int64_t)cloud * kNrmRow;
+        const float *R = rec + (live ? e : 0) * kRec;
+        // block 3: dr3 = W3^T dh3 over the output channels routed to this
+        // row (dh3[o] = g[v][o] where the row wins channel o, else 0), then
+        // dhn3 = dr3 [hn3 > 0]
+        float dhn3[kW2], xh3[kW2];
+#pragma unroll
+        for (int j = 0; j < kW2; ++j) dhn3[j] = 0.f;
+        if (live) {
+            for (int o = 0; o < kW3; ++o) {
+                if (am[(int64_t)v * kW3 + o] != (int32_t)e) continue;
+                const float g = grad_out[(int64_t)v * kW3 + o];
+#pragma unroll
+                for (int j = 0; j < kW2; ++j) dhn3[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dhn3[j]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kW2; ++j) {
+            const float h = R[kRecH2 + j];
+            dhn3[j] = fmaf(A[kAff2 + j], h, A[kAff2 + kW2 + j]) > 0.f ? dhn3[j] : 0.f;
+            xh3[j] = (h - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
+        }
+        const bool one_cloud = __ballot(live && cloud != __shfl(cloud, 0)) == 0ull;
+        if (S == 3) {
+#pragma unroll
+            for (int j = 0; j < kW2; ++j) {
+                wave_add(acc, j, dhn3[j] * xh3[j]);   // dgamma3
+                wave_add(acc, kW2 + j, dhn3[j]);      // dbeta3
+            }
+            if (use_gn) {
+                // each channel's terms go to its group's slot
+                float g3[kW2];
+#pragma unroll
+                for (int j = 0; j < kW2; ++j) g3[j] = Ps[kA2 + j] * dhn3[j];
+                wave_add_groups<kW2>(acc, 2 * kW2, gs3, cloud, live, one_cloud, g3, xh3);
+            }
+        } else {
+            // block 3's input gradient
+            float dh2[kW2];
+#pragma unroll
+            for (int j = 0; j < kW2; ++j) {
+                const float gj = Ps[kA2 + j] * dhn3[j];
+                if (use_gn) {
+                    const float *M = gm + ((int64_t)cloud * 2 + 1) * kW2 * 2 + (j / gs3) * 2;
+                    dh2[j] = live ? N[2 * 64 + 2 * j + 1] * (gj - M[0] - xh3[j] * M[1]) : 0.f;
+                } else {
+                    dh2[j] = gj;
+                }
+            }
+            // block 2: r2, dr2 = W2^T dh2, dhn2, xhat2
+            float r2[kW1], dhn2[kW1], xh2[kW1];
+#pragma unroll
+            for (int c = 0; c < kW1; ++c) {
+                const float h = R[kRecH1 + c];
+                const float hn = fmaf(A[kAff1 + c], h, A[kAff1 + kW1 + c]);
+                r2[c] = relu(hn);
+                float s = 0.f;
+#pragma unroll
+                for (int j = 0; j < kW2; ++j) s = fmaf(dh2[j], Ps[kWt1 + j * kW1 + c], s);
+                dhn2[c] = hn > 0.f ? s : 0.f;
+                xh2[c] = (h - N[1 * 64 + 2 * c]) * N[1 * 64 + 2 * c + 1];
+            }
+            if (S == 2) {
+#pragma unroll
+                for (int j = 0; j < kW2; ++j) {
+#pragma unroll
+                    for (int c = 0; c < kW1; ++c) wave_add(acc, j * kW1 + c, dh2[j] * r2[c]);  // dW2
+                    wave_add(acc, kW2 * kW1 + j, dh2[j]);                                   // db2
+                }
+#pragma unroll
+                for (int c = 0; c < kW1; ++c) {
+                    wave_add(acc, kW2 * kW1 + kW2 + c, dhn2[c] * xh2[c]);        // dgamma2
+                    wave_add(acc, kW2 * kW1 + kW2 + kW1 + c, dhn2[c]);           // dbeta2
+                }
+                if (use_gn) {
+                    float g2[kW1];
+#pragma unroll
+                    for (int c = 0; c < kW1; ++c) g2[c] = Ps[kA1 + c] * dhn2[c];
+                    wave_add_groups<kW1>(acc, kW2 * kW1 + kW2 + 2 * kW1, gs2, cloud, live, one_cloud, g2, xh2);
+                }
+            } else {
+                // block 2's input gradient, then block 1
+                float dh1[kW1];
+#pragma unroll
+                for (int c = 0; c < kW1; ++c) {
+                    const float gc = Ps[kA1 + c] * dhn2[c];
+                    if (use_gn) {
+                        const float *M = gm + ((int64_t)cloud * 2 + 0) * kW2 * 2 + (c / gs2) * 2;
+                        dh1[c] = live ? N[1 * 64 + 2 * c + 1] * (gc - M[0] - xh2[c] * M[1]) : 0.f;
+                    } else {
+                        dh1[c] = gc;
+                    }
+                }
+                float r1[kMaxK0];
+#pragma unroll
+                for (int c = 0; c < kMaxK0; ++c) r1[c] = relu(fmaf(A[kAff0 + c], R[c], A[kAff0 + kMaxK0 + c]));
+#pragma unroll
+                for (int o = 0; o < kW1; ++o) {
+#pragma unroll
+                    for (int c = 0; c < kMaxK0; ++c) wave_add(acc, o * kMaxK0 + c, dh1[o] * r1[c]);  // dW1
+                    wave_add(acc, kW1 * kMaxK0 + o, dh1[o]);                                       // db1
+                }
+#pragma unroll
+                for (int c = 0; c < kMaxK0; ++c) {
+                    float s = 0.f;
+#pragma unroll
+                    for (int o = 0; o < kW1; ++o) s = fmaf(dh1[o], Ps[kWt0 + o * kMaxK0 + c], s);
+                    const float h = R[c];
+                    const float dhn1 = fmaf(A[kAff0 + c], h, A[kAff0 + kMaxK0 + c]) > 0.f ? s : 0.f;
+                    const float xh1 = (h - N[2 * c]) * N[2 * c + 1];
+                    wave_add(acc, kW1 * kMaxK0 + kW1 + c, dhn1 * xh1);            // dgamma1
+                    wave_add(acc, kW1 * kMaxK0 + kW1 + kMaxK0 + c, dhn1);         // dbeta1
+                }
+            }
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < NP; i += kBlock) {
+        float x = accs[i];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) x += accs[w * NP + i];
+        part[(int64_t)blockIdx.x * NP + i] = x;
+    }
+}
+
+// out[j] = sum over r < rows of part[r * n + j], in order of r (fp64).
+__global__ __launch_bounds__(kBlock) void k_dpn_reduce(const float *__restrict__ part, int64_t rows, int64_t n,
+                                                       float *__restrict__ out) {
+    const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (j >= n) return;
+    double s = 0.0;
+    for (int64_t r = 0; r < rows; ++r) s += (double)part[r * n + j];
+    out[j] = (float)s;
+}
+
+// The group means of block l's (l = 1: block 2, l = 2: block 3) gradient
+// sums: gm[cloud][l - 1][group] = (sum gn, sum gn xhat) / (rows * group size).
+__global__ __launch_bounds__(kBlock) void k_dpn_gnmean(const float *__restrict__ sums, int l, int G,
+                                                       const double *__restrict__ rows,
+                                                       const int32_t *__restrict__ counters, int batched,
+                                                       float *__restrict__ gm) {
+    const int K = l == 2 ? kW2 : kW1;
+    const int gsz = K / G;
+    const int nc = num_clouds(counters, batched);  // the clouds k_dpn_norm counted
+    for (int i = threadIdx.x + blockIdx.x * kBlock; i < nc * G; i += gridDim.x * kBlock) {
+        const int b = i / G, gi = i % G;
+        const double n = rows[b] * gsz;
+        const float *s = sums + (b * K + gi) * 2;
+        float *o = gm + ((int64_t)b * 2 + (l - 1)) * kW2 * 2 + gi * 2;
+        o[0] = n > 0.0 ? (float)(s[0] / n) : 0.f;
+        o[1] = n > 0.0 ? (float)(s[1] / n) : 0.f;
+    }
+}
+
+// The reduced sums in the caller's layout: per block, d(gamma or a) [K],
+// d(beta or s) [K], dW [w][K], db [w].
+__global__ __launch_bounds__(kBlock) void k_dpn_out(const float *__restrict__ r1, const float *__restrict__ r2,
+                                                    const float *__restrict__ r3, const float *__restrict__ rarg,
+                                                    int k0, float *__restrict__ grad) {
+    const int n1 = 2 * k0 + kW1 * k0 + kW1, n2 = 2 * kW1 + kW2 * kW1 + kW2, n3 = 2 * kW2 + kW3 * kW2 + kW3;
+    for (int i = threadIdx.x + blockIdx.x * kBlock; i < n1 + n2 + n3; i += gridDim.x * kBlock) {
+        float x;
+        if (i < n1) {
+            if (i < k0) x = r1[kW1 * kMaxK0 + kW1 + i];
+            else if (i < 2 * k0) x = r1[kW1 * kMaxK0 + kW1 + kMaxK0 + (i - k0)];
+            else if (i < 2 * k0 + kW1 * k0) {
+                const int o = (i - 2 * k0) / k0, c = (i - 2 * k0) % k0;
+                x = r1[o * kMaxK0 + c];
+            } else {
+                x = r1[kW1 * kMaxK0 + (i - 2 * k0 - kW1 * k0)];
+            }
+        } else if (i < n1 + n2) {
+            const int j = i - n1;
+            if (j < 2 * kW1) x = r2[kW2 * kW1 + kW2 + j];          // dgamma2, dbeta2
+            else if (j < 2 * kW1 + kW2 * kW1) x = r2[j - 2 * kW1];  // dW2
+            else x = r2[kW2 * kW1 + (j - 2 * kW1 - kW2 * kW1)];     // db2
+        } else {
+            const int j = i - n1 - n2;
+            if (j < 2 * kW2) x = r3[j];                              // dgamma3, dbeta3
+            else if (j < 2 * kW2 + kW3 * kW2) x = rarg[j - 2 * kW2]; // dW3
+            else x = rarg[kW3 * kW2 + (j - 2 * kW2 - kW3 * kW2)];    // db3
+        }
+        grad[i] = x;
+    }
+}
+
 }  // namespace
 
 // Packed parameter count for d + f_d = k0 inputs: per block a [K], s [K],
@@ -1029,5 +1481,112 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((out_bf16 ? k_pointnet_rows<true> : k_pointnet_rows<false>), dim3(g_i), dim3(kBlock), 0,
                        L->stream, L->lvert, L->vinfo, L->counters, L->pn_keys, out);
+    return hipGetLastError();
+}
+
+// Scratch of the backward (offsets in bytes, 256-aligned).
+struct DpnLayout {
+    int64_t out, rec, am, nrm, rows, gm, parg, pb3, pb2, pb1, r3, r2, r1, rarg, total;
+    int nwaves_arg, nwg;
+};
+
+static DpnLayout dpn_layout(const lattice *L) {
+    auto al = [](int64_t x) { return (x + 255) / 256 * 256; };
+    DpnLayout l;
+    l.nwaves_arg = L->cu_count * 4 * kWaves;  // four workgroups per CU
+    l.nwg = L->cu_count * 4;
+    const int64_t V = L->max_vertices, E = (int64_t)(L->d + 1) * L->max_points;
+    int64_t at = 0;
+    l.out = at;  at += al(V * kW3 * 4);
+    l.rec = at;  at += al(E * kRec * 4);
+    l.am = at;   at += al(V * kW3 * 4);
+    l.nrm = at;  at += al((int64_t)kGnClouds * kNrmRow * 4);
+    l.rows = at; at += al((int64_t)kGnClouds * 8);
+    l.gm = at;   at += al((int64_t)kGnClouds * 2 * kW2 * 2 * 4);
+    l.parg = at; at += al((int64_t)l.nwaves_arg * kPArg * 4);
+    l.pb3 = at;  at += al((int64_t)l.nwg * kPB3 * 4);
+    l.pb2 = at;  at += al((int64_t)l.nwg * kPB2 * 4);
+    l.pb1 = at;  at += al((int64_t)l.nwg * kPB1 * 4);
+    l.r3 = at;   at += al(kPB3 * 4);
+    l.r2 = at;   at += al(kPB2 * 4);
+    l.r1 = at;   at += al(kPB1 * 4);
+    l.rarg = at; at += al(kPArg * 4);
+    l.total = at;
+    return l;
+}
+
+int64_t pointnet_backward_scratch_bytes(const lattice *L) { return dpn_layout(L).total; }
+
+hipError_t launch_distribute_backward(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
+                                      const int *groups, float eps, const float *grad_out, float *grad_params,
+                                      void *scratch) {
+    if (L->m == 0) {
+        // no rows: every gradient is zero
+        const int n = pointnet_param_count(L->d + f_d);
+        hipLaunchKernelGGL(k_dpn_reduce, dim3((n + kBlock - 1) / kBlock), dim3(kBlock), 0, L->stream,
+                           grad_params, (int64_t)0, (int64_t)n, grad_params);
+        return hipGetLastError();
+    }
+    const DpnLayout l = dpn_layout(L);
+    char *s = reinterpret_cast<char *>(scratch);
+    auto F = [&](int64_t off) { return reinterpret_cast<float *>(s + off); };
+    const int k0 = L->d + f_d;
+    const int use_gn = groups ? 1 : 0;
+    const int batched = (groups && L->batched) ? 1 : 0;
+    const int G0 = groups ? groups[0] : 1, G1 = groups ? groups[1] : 1, G2 = groups ? groups[2] : 1;
+    // the forward: entry-to-vertex map, local means, statistics and affines
+    hipError_t e = launch_distribute_pointnet(L, pos, feat, f_d, params, groups, eps, F(l.out), false, nullptr);
+    if (e != hipSuccess) return e;
+    double *rows = reinterpret_cast<double *>(s + l.rows);
+    hipLaunchKernelGGL(k_dpn_norm, dim3((unsigned)((kGnClouds * 96 + kWaves - 1) / kWaves)), dim3(kBlock), 0,
+                       L->stream, L->pn_stats, L->counters, batched, use_gn, k0, G0, G1, G2, eps, F(l.nrm), rows);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const unsigned g_e = grid_for((int64_t)(L->d + 1) * L->m, kBlock, L->cu_count, 4);
+    switch (L->d) {
+#define DR_CASE(DD)                                                                                              \
+    case DD:                                                                                                     \
+        hipLaunchKernelGGL(k_dpn_rows<DD>, dim3(g_e), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vkeys,   \
+                           batched, pos, feat, f_d, L->mu, L->pn_params, L->pn_aff, L->counters, F(l.rec));      \
+        break;
+        DR_CASE(1)
+        DR_CASE(2)
+        DR_CASE(3)
+        DR_CASE(4)
+#undef DR_CASE
+        default:
+            return hipErrorInvalidValue;
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    int32_t *am = reinterpret_cast<int32_t *>(s + l.am);
+    hipLaunchKernelGGL(k_dpn_argmax, dim3((unsigned)(l.nwaves_arg / kWaves)), dim3(kBlock), 0, L->stream, L->vinfo,
+                       L->vkeys, batched, L->pn_aff, F(l.rec), grad_out, L->counters, am, F(l.parg));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    auto reduce = [&](const float *part, int64_t nrows, int64_t n, float *out) {
+        hipLaunchKernelGGL(k_dpn_reduce, dim3((unsigned)((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, L->stream,
+                           part, nrows, n, out);
+        return hipGetLastError();
+    };
+    auto back = [&](auto kern, int64_t part_off) {
+        hipLaunchKernelGGL(kern, dim3((unsigned)l.nwg), dim3(kBlock), 0, L->stream, L->lvert, L->vkeys, batched,
+                           use_gn, G1, G2, L->pn_params, L->pn_aff, F(l.nrm), F(l.gm), F(l.rec), am, grad_out,
+                           L->counters, F(part_off));
+        return hipGetLastError();
+    };
+    auto gnmean = [&](const float *sums, int lb, int G) {
+        hipLaunchKernelGGL(k_dpn_gnmean, dim3(1), dim3(kBlock), 0, L->stream, sums, lb, G, rows, L->counters, batched,
+                           F(l.gm));
+        return hipGetLastError();
+    };
+    if ((e = back(k_dpn_back<3>, l.pb3)) != hipSuccess) return e;
+    if ((e = reduce(F(l.pb3), l.nwg, kPB3, F(l.r3))) != hipSuccess) return e;
+    if (use_gn && (e = gnmean(F(l.r3) + 2 * kW2, 2, G2)) != hipSuccess) return e;
+    if ((e = back(k_dpn_back<2>, l.pb2)) != hipSuccess) return e;
+    if ((e = reduce(F(l.pb2), l.nwg, kPB2, F(l.r2))) != hipSuccess) return e;
+    if (use_gn && (e = gnmean(F(l.r2) + kW2 * kW1 + kW2 + 2 * kW1, 1, G1)) != hipSuccess) return e;
+    if ((e = back(k_dpn_back<1>, l.pb1)) != hipSuccess) return e;
+    if ((e = reduce(F(l.pb1), l.nwg, kPB1, F(l.r1))) != hipSuccess) return e;
+    if ((e = reduce(F(l.parg), l.nwaves_arg, kPArg, F(l.rarg))) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_dpn_out, dim3(16), dim3(kBlock), 0, L->stream, F(l.r1), F(l.r2), F(l.r3), F(l.rarg), k0,
+                       grad_params);
     return hipGetLastError();
 }

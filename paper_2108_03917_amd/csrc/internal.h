@@ -86,6 +86,8 @@ struct lattice {
     int64_t wgpart_floats = 0;
     void *dfb = nullptr;        // DeformSlice backward: per-point records and partials (deform_bwd.hip)
     int64_t dfb_bytes = 0;
+    void *pnb = nullptr;        // Distribute + PointNet backward: row records and partials (distribute.hip)
+    int64_t pnb_bytes = 0;
     // Cross-lattice neighbour tables [max_vertices][T], built on demand:
     // xtab[0] when this lattice is the coarse output of a downsampling,
     // xtab[1] when it is the fine output of an upsampling.  Each remembers
@@ -171,6 +173,10 @@ int64_t pointnet_stats_bytes();
 int64_t pointnet_aff_bytes();
 int pointnet_param_count(int k0);
 int pointnet_padded_count();
+int64_t pointnet_backward_scratch_bytes(const lattice *L);
+hipError_t launch_distribute_backward(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
+                                      const int *groups, float eps, const float *grad_out, float *grad_params,
+                                      void *scratch);
 
 // deform.hip
 int deform_max_channels(const void *values, lattice_dtype values_dt, int C, const float *w_delta, const float *w_cls,

@@ -78,6 +78,7 @@ void free_all(lattice *L) {
     (void)hipFree(L->vkeys);
     (void)hipFree(L->vslot);
     (void)hipFree(L->dfb);
+    (void)hipFree(L->pnb);
     (void)hipFree(L->blk);
     (void)hipFree(L->split);
     (void)hipFree(L->rowmap);
@@ -832,36 +833,36 @@ lattice_status lattice_upsample_backward(lattice *coarse, lattice *fine, const v
                              grad_in_dtype, grad_w, grad_bias);
 }
 
-lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
-                                           const float *params, int n_blocks, const int *widths, const int *groups,
-                                           float eps, void *out, lattice_dtype out_dtype, float *mean) {
+// Checks and scratch shared by the Distribute + PointNet forward and backward
+// (`out_ok`: the call's own output arguments are valid).
+static lattice_status distribute_prepare(lattice *L, const float *pos, const float *feat, int f_d,
+                                         const float *params, int n_blocks, const int *widths, const int *groups,
+                                         float eps, bool out_ok, const char *what) {
     if (!L) return LATTICE_E_ARG;
     if (!L->splatted) {
-        set_err(L, "distribute_pointnet: no lattice yet (call lattice_splat first)");
+        set_err(L, "%s: no lattice yet (call lattice_splat first)", what);
         return LATTICE_E_STATE;
     }
     if (f_d < 0 || L->d + f_d > 16 || (f_d > 0 && L->m > 0 && !feat) || !params || !widths || n_blocks != 3 ||
-        widths[0] != 16 || widths[1] != 32 || widths[2] != 64 || (L->m > 0 && (!pos || !out)) ||
-        (out_dtype != LATTICE_F32 && out_dtype != LATTICE_BF16)) {
-        set_err(L, "distribute_pointnet: bad argument (f_d = %d; the fused PointNet has 3 blocks of widths 16, "
-                "32, 64 and d + f_d <= 16)", f_d);
+        widths[0] != 16 || widths[1] != 32 || widths[2] != 64 || (L->m > 0 && !pos) || !out_ok) {
+        set_err(L, "%s: bad argument (f_d = %d; the fused PointNet has 3 blocks of widths 16, "
+                "32, 64 and d + f_d <= 16)", what, f_d);
         return LATTICE_E_ARG;
     }
     if (groups) {
         const int K[3] = {L->d + f_d, 16, 32};
         for (int l = 0; l < 3; ++l)
             if (groups[l] < 1 || K[l] % groups[l] != 0) {
-                set_err(L, "distribute_pointnet: block %d's %d input channels do not split into %d groups", l + 1,
-                        K[l], groups[l]);
+                set_err(L, "%s: block %d's %d input channels do not split into %d groups", what, l + 1, K[l],
+                        groups[l]);
                 return LATTICE_E_ARG;
             }
         if (!(eps >= 0.f) || !isfinite(eps)) {
-            set_err(L, "distribute_pointnet: eps must be finite and >= 0");
+            set_err(L, "%s: eps must be finite and >= 0", what);
             return LATTICE_E_ARG;
         }
     }
     const int64_t E_max = (int64_t)(L->d + 1) * L->max_points;
-    lattice_status s = LATTICE_OK;
     if (!L->lvert) {
         bool ok = hipMalloc(&L->lvert, E_max * sizeof(int32_t)) == hipSuccess &&
                   hipMalloc(&L->macc, L->max_vertices * L->d * sizeof(double)) == hipSuccess &&
@@ -880,7 +881,7 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
             L->mu = nullptr;
             L->pn_params = nullptr;
             L->pn_keys = nullptr;
-            set_err(L, "distribute_pointnet: cannot allocate its scratch");
+            set_err(L, "%s: cannot allocate its scratch", what);
             return LATTICE_E_NOMEM;
         }
     }
@@ -897,10 +898,21 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
             (void)hipFree(L->pn_aff);
             L->pn_stats = nullptr;
             L->pn_aff = nullptr;
-            set_err(L, "distribute_pointnet: cannot allocate the normalisation's statistics");
+            set_err(L, "%s: cannot allocate the normalisation's statistics", what);
             return LATTICE_E_NOMEM;
         }
     }
+    return LATTICE_OK;
+}
+
+lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const float *feat, int f_d,
+                                           const float *params, int n_blocks, const int *widths, const int *groups,
+                                           float eps, void *out, lattice_dtype out_dtype, float *mean) {
+    lattice_status s = distribute_prepare(L, pos, feat, f_d, params, n_blocks, widths, groups, eps,
+                                          (L && (L->m == 0 || out)) &&
+                                              (out_dtype == LATTICE_F32 || out_dtype == LATTICE_BF16),
+                                          "distribute_pointnet");
+    if (s) return s;
     hipEvent_t t0;
     if ((s = timer_begin(L, LATTICE_STAGE_DISTRIBUTE, &t0))) return s;
     if ((s = check_launch(L, launch_distribute_pointnet(L, pos, feat, f_d, params, groups, eps, out,
@@ -908,6 +920,25 @@ lattice_status lattice_distribute_pointnet(lattice *L, const float *pos, const f
                           "distribute_pointnet")))
         return s;
     return timer_end(L, LATTICE_STAGE_DISTRIBUTE, t0);
+}
+
+lattice_status lattice_distribute_pointnet_backward(lattice *L, const float *pos, const float *feat, int f_d,
+                                                    const float *params, int n_blocks, const int *widths,
+                                                    const int *groups, float eps, const float *grad_out,
+                                                    float *grad_params) {
+    lattice_status s = distribute_prepare(L, pos, feat, f_d, params, n_blocks, widths, groups, eps,
+                                          L && grad_params && grad_params != params && (L->m == 0 || grad_out),
+                                          "distribute_pointnet_backward");
+    if (s) return s;
+    if ((s = grow(L, &L->pnb, &L->pnb_bytes, pointnet_backward_scratch_bytes(L), "distribute_pointnet_backward")))
+        return s;
+    hipEvent_t t0;
+    if ((s = timer_begin(L, LATTICE_STAGE_DISTRIBUTE_BACKWARD, &t0))) return s;
+    if ((s = check_launch(L, launch_distribute_backward(L, pos, feat, f_d, params, groups, eps, grad_out, grad_params,
+                                                        L->pnb),
+                          "distribute_pointnet_backward")))
+        return s;
+    return timer_end(L, LATTICE_STAGE_DISTRIBUTE_BACKWARD, t0);
 }
 
 lattice_status lattice_weights_to_bf16(lattice *L, const float *src, int64_t n, uint16_t *dst) {

@@ -32,7 +32,7 @@ EXPORTS = (
     "lattice_last_error", "lattice_set_conv_path", "lattice_deform_slice", "lattice_slice_backward",
     "lattice_splat_backward", "lattice_conv_backward", "lattice_downsample", "lattice_upsample",
     "lattice_distribute_pointnet", "lattice_conv_backward_noalloc", "lattice_downsample_backward",
-    "lattice_upsample_backward", "lattice_deform_slice_backward",
+    "lattice_upsample_backward", "lattice_deform_slice_backward", "lattice_distribute_pointnet_backward",
 )
 
 _lib = None
@@ -69,6 +69,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lattice_conv_backward": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
         "lattice_conv_backward_noalloc": (St, [P, P, I, I, P, I, I, P, I, P, I, P, P]),
         "lattice_distribute_pointnet": (St, [P, P, P, I, P, I, P, P, ctypes.c_float, P, I, P]),
+        "lattice_distribute_pointnet_backward": (St, [P, P, P, I, P, I, P, P, ctypes.c_float, P, P]),
         "lattice_downsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_upsample": (St, [P, P, P, I, I, P, I, I, P, P, I]),
         "lattice_downsample_backward": (St, [P, P, P, I, I, P, I, I, P, I, P, I, P, P]),
@@ -380,6 +381,48 @@ class Lattice:
                                                           _STORAGE[out.dtype], _ptr(mean)),
                     "distribute_pointnet")
         return (out, mean) if mean is not None else out
+
+    def distribute_pointnet_backward(self, pos: torch.Tensor, feat: Optional[torch.Tensor], params: torch.Tensor,
+                                     grad_out: torch.Tensor, groups=None, eps: float = 1e-5,
+                                     grad_params: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Gradients of ``distribute_pointnet(pos, feat, params, groups=groups,
+        eps=eps)`` with respect to ``params`` given ``grad_out`` = dL/dx
+        [>= V, 64] fp32: a tensor in the layout of ``params``."""
+        _dev(pos, torch.float32, "pos")
+        if pos.dim() != 2 or pos.shape != (self.m, self.d):
+            raise ValueError(f"pos must be the splatted [m = {self.m}, {self.d}] positions")
+        f_d = 0
+        if feat is not None:
+            _dev(feat, torch.float32, "feat")
+            if feat.dim() != 2 or feat.shape[0] != self.m:
+                raise ValueError("feat must be [m, f_d]")
+            f_d = feat.shape[1]
+        _dev(params, torch.float32, "params")
+        k0 = self.d + f_d
+        n_par = 2 * k0 + 16 * k0 + 16 + 2 * 16 + 32 * 16 + 32 + 2 * 32 + 64 * 32 + 64
+        if params.numel() != n_par:
+            raise ValueError(f"params must hold {n_par} values for d + f_d = {k0}")
+        _dev(grad_out, torch.float32, "grad_out")
+        need = self._rows_needed()
+        if grad_out.dim() != 2 or grad_out.shape[1] != 64 or grad_out.shape[0] < need:
+            raise ValueError(f"grad_out needs [>= {need}, 64]")
+        if grad_params is None:
+            grad_params = torch.empty_like(params)
+        _dev(grad_params, torch.float32, "grad_params")
+        if grad_params.numel() != n_par:
+            raise ValueError("grad_params needs the layout of params")
+        widths = (ctypes.c_int * 3)(*self.POINTNET_WIDTHS)
+        gr = None
+        if groups is not None:
+            if isinstance(groups, str) and groups == "default":
+                groups = [min(32, k) for k in (k0, 16, 32)]
+            if len(groups) != 3:
+                raise ValueError("groups must hold one group count per block (3)")
+            gr = (ctypes.c_int * 3)(*[int(g) for g in groups])
+        self._check(self._lib.lattice_distribute_pointnet_backward(
+            self._h, _ptr(pos), _ptr(feat), f_d, _ptr(params), 3, widths, gr, ctypes.c_float(eps), _ptr(grad_out),
+            _ptr(grad_params)), "distribute_pointnet_backward")
+        return grad_params
 
     # -- downsampling / upsampling ----------------------------------------
     def _resample(self, fn, src: "Lattice", dst: "Lattice", x, w, dtype, bias, out, out_dtype, what):

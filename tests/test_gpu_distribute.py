@@ -218,3 +218,272 @@ def test_distribute_pointnet_gn_too_many_clouds_is_reported():
     L.splat(pos, None, to_dev(np.minimum(batch, 63)), want_weight=False)
     L.distribute_pointnet(pos, feat, params, groups="default")
     assert L.status() == OK
+
+
+# --------------------------------------------------------------------------
+# backward: the gradients of every block's parameters
+# --------------------------------------------------------------------------
+
+def _unpack(flat, k0):
+    """Split a packed parameter vector into (a, s, W, b) per block."""
+    out, at, K = [], 0, k0
+    for w in (16, 32, 64):
+        a = flat[at:at + K]; at += K
+        s = flat[at:at + K]; at += K
+        W = flat[at:at + w * K].reshape(w, K); at += w * K
+        b = flat[at:at + w]; at += w
+        out.append((a, s, W, b))
+        K = w
+    return out
+
+
+def _abs_backward(blocks, seg, seed, inject, use_gn, actual=False):
+    """The backward's sum of |terms| per parameter: the oracle's backward
+    with every quantity replaced by its magnitude (products of magnitudes,
+    the group normalisation's mean terms added), seeded with ``seed``
+    [E, 64] at the last block's output and ``inject[l]`` [E, K_l] added at
+    each block's normalised input gradient.  The forward's activations enter
+    by their forward scale (sum of |terms|), or with ``actual`` by their own
+    magnitude: where the forward rounds to well within 1e-5 of its values
+    (no large cancellation), the latter bounds the backward's rounding
+    without multiplying the forward's cancellations into every term."""
+    out = []
+    dh = seed
+    for li in range(len(blocks) - 1, -1, -1):
+        blk = blocks[li]
+        r_m = np.abs(blk["r"]) if actual else blk["r_s"]
+        x_m = np.abs(blk["xhat"]) if actual else blk["xhat_s"]
+        db = dh.sum(axis=0)
+        dW = dh.T @ r_m
+        dr = dh @ np.abs(blk["W"])
+        dhn = dr * (blk["hn"] > 0) + inject[li]
+        da = (dhn * x_m).sum(axis=0)
+        ds = dhn.sum(axis=0)
+        g = np.abs(blk["a"]) * dhn
+        if use_gn:
+            G = blk["G"]
+            dh = blk["rstd"] * (g + O._group_mean(g, seg, G) + x_m * O._group_mean(g * x_m, seg, G))
+        else:
+            dh = g
+        out.append((da, ds, dW, db))
+    return out[::-1]
+
+
+def _gn_layers_plain(k0, d, seed):
+    """Group-normalisation parameters with gamma = 1 and beta = 0 (about half
+    of the normalised inputs negative: both ReLU branches taken), block 1's
+    weights of the position channels zero (a vertex with one row has its
+    local mean at its point, so those channels are zero)."""
+    out = []
+    for li, (ga, be, W, b) in enumerate(pointnet_gn_weights(k0, seed=seed)):
+        if li == 0:
+            W = W.copy()
+            W[:, :d] = 0.0
+        out.append((np.ones_like(ga), np.zeros_like(be), W, b))
+    return out
+
+
+def _forward_scales(blocks, layers, h_s):
+    """Per block the forward's sum-of-|terms| scale of xhat and of the ReLU
+    input; returns the last block's output scale."""
+    for li, blk in enumerate(blocks):
+        a = np.abs(blk["a"])
+        mean_abs = np.abs(blk["h"] - blk["xhat"] / blk["rstd"])
+        xs = (h_s + mean_abs) * blk["rstd"]
+        hn_s = a * xs + np.abs(blk["hn"] - blk["a"] * blk["xhat"])
+        blk["xhat_s"], blk["r_s"] = xs, hn_s
+        h_s = hn_s @ np.abs(blk["W"]).T + np.abs(np.asarray(layers[li][3], np.float64))
+    return h_s
+
+
+# A float32 evaluation of this graph rounds at most about 96 times along any
+# path (h0; per block the affine's two operations and a dot product of up to
+# 32 terms; the statistics' finalisation), so its error is at most gamma_96 =
+# 96 u / (1 - 96 u), u = 2^-24, times the sum of |terms|: the band within
+# which a float32 evaluation may decide a max or a ReLU the other way.
+_U = 2.0 ** -24
+_BAND = 96 * _U / (1 - 96 * _U)
+
+
+def _setup_backward(pos, feat, sigma, layers, groups, batch=None, seed=0):
+    from paper_2108_03917_amd import Lattice
+
+    d = pos.shape[1]
+    L = Lattice(d, sigma, max_points=max(pos.shape[0], 1))
+    g = GpuLattice(L, pos, None, batch=batch)
+    lat = O.build(pos, sigma, batch=batch)
+    assert np.array_equal(g.keys, lat.keys)
+    params = Lattice.pack_pointnet(layers).to("cuda:0")
+    G = np.random.default_rng(seed + 1).standard_normal((lat.V, 64)).astype(np.float32)
+    gp = L.distribute_pointnet_backward(to_dev(pos), None if feat is None else to_dev(feat), params,
+                                        g.to_gpu_order(G), groups=groups, eps=1e-5)
+    got = _unpack(gp.cpu().numpy().astype(np.float64), d + (0 if feat is None else feat.shape[1]))
+    ref, am, h3, v, blocks, seg = O.distribute_pointnet_backward(lat, pos, feat, layers, G, groups=groups, eps=1e-5)
+    h3_s = _forward_scales(blocks, layers, O.distribute_rows(lat, pos, feat)[5])
+    return lat, G, got, ref, am, h3, h3_s, v, blocks, seg
+
+
+@pytest.mark.parametrize("d,f_d,groups,batched", [(3, 3, "default", False), (4, 1, "default", False),
+                                                  (2, 2, (2, 4, 8), False), (3, 2, "default", True)])
+def test_distribute_pointnet_backward_parity(d, f_d, groups, batched):
+    """Every block's parameter gradients (gamma, beta, W, b) with group
+    normalisation against the oracle's float64 backward on a sparse cloud
+    (every pair its own vertex: each vertex has one row, so the max decides
+    nothing; the entry counts 12000, 15000 and 9000 leave the last chunk of
+    64 lanes partly empty, whose lanes must add nothing although the group
+    means give every row an input gradient).  Bar: 1e-5 of the backward's sum of |terms| at the forward's
+    values, plus, for each ReLU input within float32 rounding of zero (a
+    handful; the test counts them), the whole effect of the other branch.
+    Batched: four clouds (batch ids 0, 3, 7, 11) drawn per point, so that
+    most wavefronts' rows span clouds and their group sums go per cloud."""
+    m = 3000
+    rng = np.random.default_rng(580 + d + (10 if batched else 0))
+    pos = rng.uniform(0.0, 1.0, (m, d)).astype(np.float32)
+    feat = rng.standard_normal((m, f_d)).astype(np.float32)
+    batch = rng.choice(np.array([0, 3, 7, 11], dtype=np.int32), size=m) if batched else None
+    k0 = d + f_d
+    og = [min(32, k) for k in (k0, 16, 32)] if groups == "default" else list(groups)
+    layers = _gn_layers_plain(k0, d, seed=581 + d)
+    sigma = 0.0001 if d == 2 else 0.0005      # small enough that no two points share a vertex
+    lat, G, got, ref, am, h3, h3_s, v, blocks, seg = _setup_backward(pos, feat, sigma, layers, og, batch=batch,
+                                                                     seed=582)
+    assert np.bincount(v).max() == 1                                      # one row per vertex
+    if batched:
+        assert len(np.unique(seg)) == 4
+    E = h3.shape[0]
+    seed_abs = np.zeros((E, 64))
+    vv, cc = np.nonzero(am >= 0)
+    np.add.at(seed_abs, (am[vv, cc], cc), np.abs(G[vv, cc]))
+    scale = _abs_backward(blocks, seg, seed_abs, [np.zeros_like(b["hn"]) for b in blocks], True, actual=True)
+    # the real input gradient of each block's ReLU, for the branches in doubt
+    dh = np.zeros((E, 64))
+    np.add.at(dh, (am[vv, cc], cc), G[vv, cc])
+    inj, n_doubt = [None] * 3, 0
+    for li in range(2, -1, -1):
+        blk = blocks[li]
+        dr = dh @ blk["W"]
+        doubt = (np.abs(blk["hn"]) <= _BAND * blk["r_s"]) & (blk["hn"] != 0.0)   # exact zeros decide alike
+        inj[li] = np.where(doubt, np.abs(dr), 0.0)
+        n_doubt += int(doubt.sum())
+        gn_ = blk["a"] * (dr * (blk["hn"] > 0))
+        Gc = blk["G"]
+        dh = blk["rstd"] * (gn_ - O._group_mean(gn_, seg, Gc) - blk["xhat"] * O._group_mean(gn_ * blk["xhat"], seg, Gc))
+    assert n_doubt <= 100, n_doubt
+    allow = _abs_backward(blocks, seg, np.zeros((E, 64)), inj, True, actual=True)
+    names = ("gamma", "beta", "W", "b")
+    for li in range(3):
+        for q in range(4):
+            assert_close_scaled(got[li][q], ref[li][q], REL_F32 * scale[li][q] + allow[li][q], 1.0,
+                                f"pointnet backward d={d} block {li + 1} d{names[q]}")
+
+
+def _sites_cloud(d, n_sites, per, seed, sigma):
+    """Sites far apart (no two share a lattice vertex), each ``per`` points
+    within one simplex, point i of a site with features 1 + i + U(0, 0.5):
+    every vertex's rows are its site's points, one per point, and with
+    positive weights the last point wins every channel by a wide margin."""
+    rng = np.random.default_rng(seed)
+    side = int(np.ceil(n_sites ** (1.0 / d)))
+    grid = np.stack(np.meshgrid(*[np.arange(side)] * d, indexing="ij"), -1).reshape(-1, d)[:n_sites]
+    centres = grid * 40.0 * sigma + rng.uniform(0, 10 * sigma, size=(n_sites, d))
+    pos = np.repeat(centres, per, axis=0) + rng.normal(0, 0.002 * sigma, size=(n_sites * per, d))
+    base = np.tile(np.arange(per, dtype=np.float64), n_sites)[:, None]
+    feat = 1.0 + base + rng.uniform(0, 0.5, size=(n_sites * per, 4))
+    return pos.astype(np.float32), feat.astype(np.float32)
+
+
+def _positive_affine_layers(k0, d, seed):
+    """Fixed-affine parameters with a = 1, s = 0 (s = 3 on the position
+    channels, whose weights are zero), W ~ U(0.05, 0.3), b ~ U(0, 0.1): with
+    positive features every activation is positive, far from the ReLU's
+    kink, and free of cancellation."""
+    rng = np.random.default_rng(seed)
+    out, K = [], k0
+    for w in (16, 32, 64):
+        a = np.ones(K, np.float32)
+        s_ = np.zeros(K, np.float32)
+        W = rng.uniform(0.05, 0.3, size=(w, K)).astype(np.float32)
+        if K == k0:
+            s_[:d] = 3.0
+            W[:, :d] = 0.0
+        b = rng.uniform(0.0, 0.1, size=w).astype(np.float32)
+        out.append((a, s_, W, b))
+        K = w
+    return out
+
+
+@pytest.mark.parametrize("d", [2, 3, 4])
+def test_distribute_pointnet_backward_routing(d):
+    """Several rows per vertex (three points of a site per vertex) with the
+    fixed affine: the max routes each g[v][c] to the winning row, then every
+    block's parameter gradients (a, s, W, b) match the oracle within 1e-5 of
+    their sum of |terms|.  Positive weights and features keep every decision
+    far outside float32 rounding, which the test checks first."""
+    sigma = 0.05
+    pos, feat = _sites_cloud(d, 400, 3, 600 + d, sigma)
+    k0 = d + 4
+    layers = _positive_affine_layers(k0, d, 601)
+    lat, G, got, ref, am, h3, h3_s, v, blocks, seg = _setup_backward(pos, feat, sigma, layers, None, seed=602)
+    cnt = np.bincount(v)
+    assert (cnt == 3).mean() > 0.9
+    order = np.argsort(v, kind="stable")
+    starts = np.searchsorted(v[order], np.arange(lat.V))
+    ends = np.searchsorted(v[order], np.arange(lat.V), side="right")
+    for u in range(lat.V):
+        rows = order[starts[u]:ends[u]]
+        top = h3[am[u], np.arange(64)]
+        other = rows[:, None] != am[u][None, :]
+        gap = top[None, :] - h3[rows]
+        bound = _BAND * (h3_s[rows] + h3_s[am[u], np.arange(64)][None, :])
+        assert not np.any(other & (gap <= bound)), "a maximum within rounding of another row"
+    for blk in blocks:
+        assert np.all(np.abs(blk["hn"]) > _BAND * blk["r_s"]), "a ReLU input within rounding of zero"
+    E = h3.shape[0]
+    seed_abs = np.zeros((E, 64))
+    vv, cc = np.nonzero(am >= 0)
+    np.add.at(seed_abs, (am[vv, cc], cc), np.abs(G[vv, cc]))
+    scale = _abs_backward(blocks, seg, seed_abs, [np.zeros_like(b["hn"]) for b in blocks], False)
+    for li in range(3):
+        for q, name in enumerate(("a", "s", "W", "b")):
+            assert_close_scaled(got[li][q], ref[li][q], scale[li][q], REL_F32,
+                                f"pointnet backward routing d={d} block {li + 1} d{name}")
+
+
+def test_distribute_pointnet_backward_repeatable_and_checks():
+    """Five clouds drawn per point (several rows per vertex, waves spanning
+    clouds) with group normalisation: two calls give identical bits (every
+    sum in a fixed order), the gradients are finite and not all zero.  A
+    missing output or too few rows of grad_out are refused before any
+    launch."""
+    from paper_2108_03917_amd import Lattice, LatticeError
+
+    w = random_cloud(6000, 3, seed=620, extent=1.0, C=3, n_batch=5)
+    L = Lattice(3, 0.15, max_points=w.m)
+    g = GpuLattice(L, w.pos, None, batch=w.batch)
+    layers = pointnet_gn_weights(6, seed=621)
+    params = Lattice.pack_pointnet(layers).to("cuda:0")
+    G = to_dev(np.random.default_rng(622).standard_normal((L.max_vertices(), 64)).astype(np.float32))
+    pos, feat = to_dev(w.pos), to_dev(w.feat)
+    a = L.distribute_pointnet_backward(pos, feat, params, G, groups="default")
+    b = L.distribute_pointnet_backward(pos, feat, params, G, groups="default")
+    assert torch.equal(a, b)
+    assert torch.isfinite(a).all() and a.abs().max() > 0
+    with pytest.raises(ValueError):
+        L.distribute_pointnet_backward(pos, feat, params, G[:10], groups="default")
+    import ctypes
+    from paper_2108_03917_amd.lattice import load_library
+    lib = load_library()
+    widths = (ctypes.c_int * 3)(16, 32, 64)
+    st = lib.lattice_distribute_pointnet_backward(L._h, ctypes.c_void_p(pos.data_ptr()),
+                                                  ctypes.c_void_p(feat.data_ptr()), 3,
+                                                  ctypes.c_void_p(params.data_ptr()), 3, widths, None,
+                                                  ctypes.c_float(1e-5), ctypes.c_void_p(G.data_ptr()), None)
+    assert st != 0
+    bad = (ctypes.c_int * 3)(16, 32, 32)
+    out = torch.empty_like(params)
+    st = lib.lattice_distribute_pointnet_backward(L._h, ctypes.c_void_p(pos.data_ptr()),
+                                                  ctypes.c_void_p(feat.data_ptr()), 3,
+                                                  ctypes.c_void_p(params.data_ptr()), 3, bad, None,
+                                                  ctypes.c_float(1e-5), ctypes.c_void_p(G.data_ptr()),
+                                                  ctypes.c_void_p(out.data_ptr()))
+    assert st != 0
