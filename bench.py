@@ -47,8 +47,14 @@ max (fused) turns the raw point features into the 64-channel vertex values
 the convs take (workloads whose first conv has 64 inputs); each PointNet block
 starts with a group normalisation whose statistics are computed per cloud.
 
+With --backward (after --op deform, unet or pointnet) the step adds the
+backward pass of every stage from a fixed gradient at its output: DeformSlice
+with the classifier (dL/d logits), or the slice, then the upsample's and the
+downsample's, every conv's input and weight gradients, and last the splat's
+(dL/d features) or Distribute + PointNet's (every block's parameters).
+
 Usage: python bench.py [--steps K] [--warmup W] [--config N] [--op slice|deform|train|unet|pointnet]
-       [--no-cpu-baseline] [--no-other-configs] [--no-cold]
+       [--backward] [--no-cpu-baseline] [--no-other-configs] [--no-cold]
 """
 from __future__ import annotations
 
@@ -96,13 +102,16 @@ class Pipeline:
     (V stays on the device), so the step can be captured once as a HIP graph
     and replayed."""
 
-    def __init__(self, w, stream=None, tail="slice"):
+    def __init__(self, w, stream=None, tail="slice", backward=False):
         import torch
 
         from paper_2108_03917_amd import Lattice
 
         self.w = w
         self.tail = tail
+        # --op train is the slice step with its backward pass; --backward adds
+        # the backward pass to the deform, unet and pointnet steps
+        self.backward = backward or tail == "train"
         dev = torch.device("cuda:0")
         torch.cuda.set_device(dev)
         self.stream = stream if stream is not None else torch.cuda.Stream(device=dev)
@@ -170,11 +179,13 @@ class Pipeline:
             self.up_vals = torch.empty((mv, c_last), dtype=torch.float32, device=dev)
             # the last forward conv's output feeds the downsample: store it as its input dtype
             self.outs[-1] = torch.empty((mv, c_last), dtype=st, device=dev)
-        if tail == "train":
+        if self.backward:
             from datagen.clouds import random_rows
 
-            # the loss gradient dL/df at the points: an input of the step
-            self.gout = torch.from_numpy(random_rows(w.m, c_last, seed=500 + w.config)).to(dev)
+            # the loss gradient at the points (dL/d logits after DeformSlice
+            # with the classifier, else dL/df): an input of the step
+            n_out = self.w_cls.shape[0] if tail == "deform" else c_last
+            self.gout = torch.from_numpy(random_rows(w.m, n_out, seed=500 + w.config)).to(dev)
             # a gradient row is stored as bf16 where the conv that reads it
             # computes in bf16 (it would round it on load anyway)
             def gstore(i):
@@ -185,6 +196,10 @@ class Pipeline:
             self.gin = [torch.empty((mv, cv.c_in), dtype=gstore(i - 1), device=dev) for i, cv in enumerate(self.convs)]
             self.gw = [torch.empty((cv.c_out, w.taps, cv.c_in), dtype=torch.float32, device=dev) for cv in self.convs]
             self.gfeat = torch.empty((w.m, w.C), dtype=torch.float32, device=dev)
+            if tail == "unet":
+                self.g_up = torch.empty((mv, c_last), dtype=torch.float32, device=dev)
+            if tail == "pointnet":
+                self.gparams = torch.empty_like(self.pn_params)
             assert n > 0
         torch.cuda.synchronize()
 
@@ -259,36 +274,59 @@ class Pipeline:
             L.deform_slice(x, self.w_delta, self.dw.b_delta, self.w_cls, self.b_cls, out=self.sliced)
         else:
             L.slice(x, out=self.sliced)
-        if self.tail == "train":
+        if self.backward:
             n = len(self.convs)
+            gdt = "bf16" if self.convs[-1].dtype == "bf16" else "f32"
             mark()
-            L.slice_backward(self.gout, out=self.gtop)
+            if self.tail == "deform":
+                gy = L.deform_slice_backward(x, self.w_delta, self.dw.b_delta, self.gout, w_cls=self.w_cls,
+                                             grad_dtype=gdt)[0]
+            elif self.tail == "unet":
+                L.slice_backward(self.gout, out=self.g_up)
+                mark()
+                g_coarse = self.Lc.upsample_backward(L, self.g_up, self.w_up, x=self.coarse_vals,
+                                                     dtype=self.rs_dtype, grad_in_dtype=self.rs_dtype)[0]
+                mark()
+                gy = L.downsample_backward(self.Lc, g_coarse, self.w_down, x=self.outs[-1], dtype=self.rs_dtype,
+                                           grad_in_dtype=gdt)[0]
+            else:
+                L.slice_backward(self.gout, out=self.gtop)
+                gy = self.gtop
             for i in reversed(range(n)):
                 cv = self.convs[i]
                 xin = self.values if i == 0 else self.outs[i - 1]
-                gy = self.gtop if i == n - 1 else self.gin[i + 1]
+                g = gy if i == n - 1 else self.gin[i + 1]
                 mark()
-                L.conv_backward(gy, self.weights[i], dtype=cv.dtype, want_weight=False, grad_in=self.gin[i])
+                L.conv_backward(g, self.weights[i], dtype=cv.dtype, want_weight=False, grad_in=self.gin[i])
                 mark()
-                L.conv_backward(gy, self.weights[i], xin, dtype=cv.dtype, want_input=False, grad_w=self.gw[i])
+                L.conv_backward(g, self.weights[i], xin, dtype=cv.dtype, want_input=False, grad_w=self.gw[i])
             mark()
-            L.splat_backward(self.gin[0], out=self.gfeat)
+            if self.tail == "pointnet":
+                L.distribute_pointnet_backward(self.pos, self.raw, self.pn_params, self.gin[0], groups=self.pn_groups,
+                                               grad_params=self.gparams)
+            else:
+                L.splat_backward(self.gin[0], out=self.gfeat)
         mark()
         return self.sliced
 
     def stage_names(self):
         fwd = ["splat", "neighbors"] + [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}" for i, c in enumerate(self.convs)]
         if self.tail == "unet":
-            return ["splat", "coarse_lattice"] + fwd[1:] + ["downsample", "upsample", "slice"]
-        if self.tail == "pointnet":
-            return ["lattice", "distribute"] + fwd[1:] + ["slice"]
-        if self.tail != "train":
-            return fwd + [self.tail]
-        bwd = ["slice_bwd"]
+            names = ["splat", "coarse_lattice"] + fwd[1:] + ["downsample", "upsample", "slice"]
+        elif self.tail == "pointnet":
+            names = ["lattice", "distribute"] + fwd[1:] + ["slice"]
+        elif self.tail == "deform":
+            names = fwd + ["deform"]
+        else:
+            names = fwd + ["slice"]
+        if not self.backward:
+            return names
+        bwd = {"deform": ["deform_bwd"], "unet": ["slice_bwd", "upsample_bwd", "downsample_bwd"]}.get(self.tail,
+                                                                                                     ["slice_bwd"])
         for i in reversed(range(len(self.convs))):
             c = self.convs[i]
             bwd += [f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}_bwd_in", f"conv{i}_{c.c_in}x{c.c_out}_{c.dtype}_bwd_w"]
-        return fwd + ["slice"] + bwd + ["splat_bwd"]
+        return names + bwd + ["distribute_bwd" if self.tail == "pointnet" else "splat_bwd"]
 
 
 def algorithmic_work(w, V, n_cls=0, Vc=0, f_raw=-1):
@@ -357,6 +395,13 @@ def algorithmic_work(w, V, n_cls=0, Vc=0, f_raw=-1):
         # counted)
         work["distribute"] = {"bytes": m * 4 * (d + f_raw) + E * 8 + V * (8 + s0 * 64),
                               "flops": 2 * E * (k0 * 16 + 16 * 32 + 32 * 64), "dtype": "f32"}
+        # its backward (every block's parameter gradients): the same reads plus
+        # dL/dx (4 x 64 B per vertex); the forward's products once more and
+        # the backward's two per layer (input and weight gradients), on the
+        # fp32 vector units (the fp32 per-pair records it stores and rereads
+        # are not counted)
+        work["distribute_bwd"] = {"bytes": m * 4 * (d + f_raw) + E * 8 + V * (8 + 4 * 64),
+                                  "flops": 3 * 2 * E * (k0 * 16 + 16 * 32 + 32 * 64), "dtype": "alu"}
     if n and Vc:
         last = w.convs[-1]
         s = 2 if last.dtype == "bf16" else 4
@@ -371,6 +416,22 @@ def algorithmic_work(w, V, n_cls=0, Vc=0, f_raw=-1):
         # coarse row read once; every tap is multiplied (absent ones as zeros)
         work["upsample"] = {"bytes": V * (4 * T + 4 * c_last) + Vc * s * c_last + T * c_last * c_last * s,
                             "flops": 2 * V * T * c_last * c_last, "dtype": last.dtype}
+        # their backward passes (input and weight gradients in one call): the
+        # output gradient, the forward input and the input gradient once per
+        # row, the taps, the weights read and their gradient written (fp32);
+        # the flops of the forward twice
+        work["upsample_bwd"] = {"bytes": V * (4 * c_last + 4 * T) + Vc * 2 * s * c_last
+                                + T * c_last * c_last * (s + 4),
+                                "flops": 4 * V * T * c_last * c_last, "dtype": last.dtype}
+        work["downsample_bwd"] = {"bytes": Vc * (s * c_last + 4 * T) + V * 2 * s * c_last
+                                  + T * c_last * c_last * (s + 4),
+                                  "flops": 4 * Vc * T * c_last * c_last, "dtype": last.dtype}
+    if n and n_cls:
+        # DeformSlice + classifier backward: per point the record and dL/d
+        # logits, per vertex its row read and its gradient row written, the
+        # weights read and their gradients written
+        work["deform_bwd"] = {"bytes": m * (8 * (d + 1) + 4 * n_cls) + V * (sg(n - 1) + sg(n - 1)) * c_last
+                              + 8 * (c_last + n_cls * c_last + n_cls)}
     return work
 
 
@@ -397,12 +458,12 @@ def roofline_entry(name, ms, wk):
 def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False, pointnet=None):
     """The CPU oracle, as it stands, over the same workload: whole steps
     (lattice build, splat, neighbours, every conv, slice -- or DeformSlice
-    with the classifier when `dw` holds its weights; with `train` also the
-    backward pass of every stage; with `unet` the coarse lattice, the
-    downsample and the upsample before the slice; with `pointnet` (its
-    layers and group counts) Distribute + PointNet instead of the features'
-    splat) repeated
-    until about `budget_s` seconds, reported as points/s."""
+    with the classifier when `dw` holds its weights; with `unet` the coarse
+    lattice, the downsample and the upsample before the slice; with
+    `pointnet` (its layers and group counts) Distribute + PointNet instead of
+    the features' splat; with `train` also the backward pass of every stage,
+    down to the features or the PointNet's parameters) repeated until about
+    `budget_s` seconds, reported as points/s."""
     from threadpoolctl import threadpool_info
 
     from oracle import lattice_oracle as O
@@ -411,7 +472,7 @@ def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False, pointnet=No
         from datagen.clouds import random_rows
 
         c_last = w.convs[-1].c_out if w.convs else w.C
-        gout = random_rows(w.m, c_last, seed=500 + w.config)
+        gout = random_rows(w.m, dw.w_cls.shape[0] if dw is not None else c_last, seed=500 + w.config)
 
     if pointnet is not None:
         from datagen.clouds import raw_point_features
@@ -435,22 +496,35 @@ def cpu_baseline(w, budget_s=20.0, dw=None, train=False, unet=False, pointnet=No
                 xi = O.round_bf16(x.astype(np.float32))
                 Wt = O.round_bf16(Wt)
             x, _ = O.conv(xi, nbr, Wt)
+        x_last = x
         if unet:
             from datagen.clouds import conv_weight
 
             c = x.shape[1]
             coarse = O.coarsen(w.pos, w.sigma, batch=w.batch)
-            xc, _ = O.downsample(lat, coarse, x, conv_weight(c, c, w.d, seed=600 + w.config))
-            x, _ = O.upsample(coarse, lat, xc, conv_weight(c, c, w.d, seed=700 + w.config))
+            wd = conv_weight(c, c, w.d, seed=600 + w.config)
+            wu = conv_weight(c, c, w.d, seed=700 + w.config)
+            xc, _ = O.downsample(lat, coarse, x, wd)
+            x, _ = O.upsample(coarse, lat, xc, wu)
         if dw is None:
             O.slice_(lat, x)
         else:
             O.deform_slice(lat.idx, lat.bary, x, dw.w_delta, dw.b_delta, dw.w_cls, dw.b_cls)
         if train:
-            g, _ = O.slice_backward(lat, gout)
+            if dw is not None:
+                g = O.deform_slice_backward(lat.idx, lat.bary, x, dw.w_delta, dw.b_delta, gout, lat.V, dw.w_cls,
+                                            dw.b_cls)[0][0]
+            else:
+                g, _ = O.slice_backward(lat, gout)
+            if unet:
+                g = O.upsample_backward(coarse, lat, xc, wu, g)[0]
+                g = O.downsample_backward(lat, coarse, x_last, wd, g)[0]
             for cv, xi in zip(reversed(w.convs), reversed(ins)):
                 g, _, _, _, _, _ = O.conv_backward(xi, nbr, cv.weight, g)
-            O.splat_backward(lat, g)
+            if pointnet is not None:
+                O.distribute_pointnet_backward(lat, w.pos, raw, pointnet[0], g, groups=pointnet[1])
+            else:
+                O.splat_backward(lat, g)
 
     t0 = time.perf_counter()
     n = 0
@@ -627,6 +701,9 @@ def main(argv=None):
                     help="end the step with the plain slice, with DeformSlice + classifier, run the "
                          "forward and backward passes (train), add a coarse level (unet), or start with "
                          "Distribute + PointNet (pointnet)")
+    ap.add_argument("--backward", action="store_true",
+                    help="with --op deform, unet or pointnet: add the backward pass of every stage (--op train "
+                         "is the slice step with its backward pass)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-flushed stage timings")
     ap.add_argument("--no-other-configs", action="store_true",
@@ -650,7 +727,9 @@ def main(argv=None):
     from datagen.clouds import make_workload
 
     w = make_workload(args.config)
-    pipe = Pipeline(w, tail=args.op)
+    if args.backward and args.op not in ("deform", "unet", "pointnet"):
+        raise SystemExit("--backward goes with --op deform, unet or pointnet (--op train is the slice step's)")
+    pipe = Pipeline(w, tail=args.op, backward=args.backward)
     pipe.L.set_conv_path(args.conv_path)
     sec, V, samples, cold = time_pipeline(pipe, args.steps, args.warmup, not args.no_cold, args.graph)
     names = pipe.stage_names()
@@ -670,7 +749,8 @@ def main(argv=None):
     # kernels) is reported in `stages` with its own HBM roofline
     # (with --op deform: the DeformSlice + classifier kernel itself)
     single = [n for n in names if n not in ("splat", "slice_bwd", "coarse_lattice", "downsample", "upsample",
-                                            "lattice", "distribute")]
+                                            "lattice", "distribute", "deform_bwd", "upsample_bwd", "downsample_bwd",
+                                            "distribute_bwd")]
     dominant = "deform" if args.op == "deform" else max(single, key=lambda n: stage_ms[n])
     rf = dict(stages[dominant])
     rf.pop("ms")
@@ -685,7 +765,8 @@ def main(argv=None):
                    "deform": "points/s for splat+conv+deformslice+classifier",
                    "train": "points/s for splat+conv+slice forward and backward",
                    "unet": "points/s for splat+conv+downsample+upsample+slice",
-                   "pointnet": "points/s for lattice+distribute/pointnet+conv+slice"}[args.op],
+                   "pointnet": "points/s for lattice+distribute/pointnet+conv+slice"}[args.op]
+                  + (" forward and backward" if args.backward else ""),
         "value": w.m * args.steps / sec,
         "unit": "points/s",
         "n_gpus": 1,
@@ -702,6 +783,9 @@ def main(argv=None):
                    "convs": [f"{c.c_in}->{c.c_out} {c.dtype}" for c in w.convs]}
                   | ({"classes": n_cls, "tail": "deformslice+classifier"} if args.op == "deform" else {})
                   | ({"tail": "slice, then the backward pass of every stage"} if args.op == "train" else {})
+                  | ({"backward": "the backward pass of every stage, down to the "
+                                  + ("PointNet's parameters" if args.op == "pointnet" else "point features")}
+                     if args.backward else {})
                   | ({"coarse_vertices": Vc, "tail": "downsample+upsample+slice"} if args.op == "unet" else {})
                   | ({"head": f"distribute+pointnet ({w.d}+{f_raw} -> 16 -> 32 -> 64, group norm "
                               f"{pipe.pn_groups} per cloud)"} if args.op == "pointnet" else {}),
@@ -738,9 +822,9 @@ def main(argv=None):
                 "kernel": "conv0_128x128_bf16", "workload": lidar["workload"],
                 "met": st["bound"] == "mfma" and st["frac"] >= TARGET_MFMA_FRAC}
         out["targets"] = tg
-    if not args.no_cpu_baseline and args.op in ("train", "unet", "pointnet"):
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, None, train=args.op == "train",
-                                           unet=args.op == "unet",
+    if not args.no_cpu_baseline and (args.op in ("train", "unet", "pointnet") or args.backward):
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, pipe.dw if args.op == "deform" else None,
+                                           train=pipe.backward, unet=args.op == "unet",
                                            pointnet=(pipe.pn_layers, pipe.pn_groups) if args.op == "pointnet" else None)
     elif not args.no_cpu_baseline:
         dw = pipe.dw if args.op == "deform" else None

@@ -23,10 +23,13 @@
 //                  per wavefront (written as partials at the end).
 //   k_dfb_gather   one wavefront per vertex over its pair list (the splat's
 //                  lists: no atomics), lane = channel.
-//   k_dfb_cls      dW_cls and db_cls partials per chunk of points.
-//   k_dfb_reduce   every partial added in a fixed order: the results do not
+//   k_dfb_cls      dW_cls and db_cls partials per chunk of 1024 points, a
+//                  tile of 16 classes x 64 channels per workgroup, the
+//                  chunk's g and f staged through LDS 128 points at a time.
+//   rowsum         every partial added in a fixed order: the results do not
 //                  depend on scheduling.
 #include "internal.h"
+#include "rowsum.h"
 
 namespace {
 
@@ -46,7 +49,7 @@ __device__ __forceinline__ float value_at(const void *values, int64_t at) {
 
 // Scratch carved out of one buffer (offsets in bytes, each 256-aligned).
 struct DfbLayout {
-    int64_t gf, am, coef, f, pw, pb, pc, pbc, total;
+    int64_t gf, am, coef, f, pw, pb, pc, pbc, tmp, total;
 };
 
 __host__ __device__ inline int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
@@ -62,6 +65,10 @@ inline DfbLayout dfb_layout(int64_t m, int C, int dp1, int n_cls, int nwaves, in
     l.pb = at;   at += align256((int64_t)nwaves * 4);
     l.pc = at;   at += n_cls > 0 ? align256((int64_t)nch * n_cls * C * 4) : 0;
     l.pbc = at;  at += n_cls > 0 ? align256((int64_t)nch * n_cls * 4) : 0;
+    // the row sums' chunk sums, for the largest of the four reductions
+    int64_t t = rowsum::scratch_floats(nwaves, C);
+    if (n_cls > 0 && rowsum::scratch_floats(nch, (int64_t)n_cls * C) > t) t = rowsum::scratch_floats(nch, (int64_t)n_cls * C);
+    l.tmp = at;  at += align256(t * 4);
     l.total = at;
     return l;
 }
@@ -273,42 +280,57 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
     }
 }
 
-// Classifier gradients, chunk `blockIdx.y` of the points and classes
-// 4 blockIdx.x .. +3: each thread owns channels c = threadIdx.x + 256 i.
-__global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int C, int n_cls, int nch,
-                                                    const float *__restrict__ grad_out, const float *__restrict__ f,
-                                                    float *__restrict__ part_c, float *__restrict__ part_bc) {
-    const int cls0 = blockIdx.x * 4;
-    const int ch = blockIdx.y;
-    const int64_t p0 = m * ch / nch, p1 = m * (ch + 1) / nch;
-    for (int c = threadIdx.x; c < C; c += kBlock) {
-        float acc[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int64_t p = p0; p < p1; ++p) {
-            const float fv = f[p * C + c];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (cls0 + j < n_cls) acc[j] = fmaf(grad_out[p * n_cls + cls0 + j], fv, acc[j]);
+// Classifier gradients: dW_cls [n_cls][C] = sum_p g_p^T f_p and db_cls =
+// sum_p g_p over chunk blockIdx.z of kClsChunk points, for the 16 classes
+// from 16 blockIdx.y and the 64 channels from 64 blockIdx.x.  Thread t owns
+// class t / 16 and channels 4 (t mod 16) .. +3; the chunk's g and f pass
+// through LDS kClsTile points at a time (zero past m, n_cls and C).
+constexpr int kClsChunk = 1024, kClsTile = 128, kClsK = 16, kClsC = 64;
+__global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int C, int n_cls, const float *__restrict__ grad_out,
+                                                    const float *__restrict__ f, float *__restrict__ part_c,
+                                                    float *__restrict__ part_bc) {
+    __shared__ float gs[kClsTile][kClsK];
+    __shared__ float4 fs[kClsTile][kClsC / 4];
+    const int t = threadIdx.x;
+    const int k = t >> 4, cq = t & 15;
+    const int c0 = blockIdx.x * kClsC, k0 = blockIdx.y * kClsK;
+    const int64_t chunk = blockIdx.z;
+    const int64_t p0 = chunk * kClsChunk;
+    const int64_t p1 = p0 + kClsChunk < m ? p0 + kClsChunk : m;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float accb = 0.f;
+    for (int64_t q0 = p0; q0 < p1; q0 += kClsTile) {
+        for (int i = t; i < kClsTile * kClsK; i += kBlock) {
+            const int pp = i / kClsK, kk = i % kClsK;
+            const int64_t p = q0 + pp;
+            gs[pp][kk] = (p < p1 && k0 + kk < n_cls) ? grad_out[p * n_cls + k0 + kk] : 0.f;
         }
+        for (int i = t; i < kClsTile * kClsC; i += kBlock) {
+            const int pp = i / kClsC, cc = i % kClsC;
+            const int64_t p = q0 + pp;
+            reinterpret_cast<float *>(&fs[pp][0])[cc] = (p < p1 && c0 + cc < C) ? f[p * C + c0 + cc] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int pp = 0; pp < kClsTile; ++pp) {
+            const float g = gs[pp][k];
+            const float4 x = fs[pp][cq];
+            acc.x = fmaf(g, x.x, acc.x);
+            acc.y = fmaf(g, x.y, acc.y);
+            acc.z = fmaf(g, x.z, acc.z);
+            acc.w = fmaf(g, x.w, acc.w);
+            accb += g;
+        }
+        __syncthreads();
+    }
+    if (k0 + k < n_cls) {
+        float *o = part_c + (chunk * n_cls + k0 + k) * C;
+        const float a[4] = {acc.x, acc.y, acc.z, acc.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (cls0 + j < n_cls) part_c[((int64_t)ch * n_cls + cls0 + j) * C + c] = acc[j];
+        for (int i = 0; i < 4; ++i)
+            if (c0 + 4 * cq + i < C) o[c0 + 4 * cq + i] = a[i];
+        if (blockIdx.x == 0 && cq == 0) part_bc[chunk * n_cls + k0 + k] = accb;
     }
-    if (threadIdx.x < 4 && cls0 + (int)threadIdx.x < n_cls) {
-        const int cls = cls0 + threadIdx.x;
-        float s = 0.f;
-        for (int64_t p = p0; p < p1; ++p) s += grad_out[p * n_cls + cls];
-        part_bc[(int64_t)ch * n_cls + cls] = s;
-    }
-}
-
-// out[j] = sum over r < rows of part[r * n + j], in order of r.
-__global__ __launch_bounds__(kBlock) void k_dfb_reduce(const float *__restrict__ part, int64_t rows, int64_t n,
-                                                       float *__restrict__ out) {
-    const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (j >= n) return;
-    float s = 0.f;
-    for (int64_t r = 0; r < rows; ++r) s += part[r * n + j];
-    out[j] = s;
 }
 
 template <int D, bool IN_BF16, bool CLS>
@@ -384,33 +406,19 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
     if (e != hipSuccess) return e;
     if (grad_values && (e = launch_gather_ch<D>(L, ch, out_bf16, C, coef, gf, am, w_delta, grad_values)) != hipSuccess)
         return e;
-    if (grad_w_delta) {
-        hipLaunchKernelGGL(k_dfb_reduce, dim3((C + kBlock - 1) / kBlock), dim3(kBlock), 0, L->stream, pw,
-                           (int64_t)nwaves, (int64_t)C, grad_w_delta);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    if (grad_b_delta) {
-        hipLaunchKernelGGL(k_dfb_reduce, dim3(1), dim3(kBlock), 0, L->stream, pb, (int64_t)nwaves, (int64_t)1,
-                           grad_b_delta);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
+    float *tmp = reinterpret_cast<float *>(scratch + l.tmp);
+    if (grad_w_delta && (e = rowsum::sum(L->stream, pw, nwaves, C, tmp, grad_w_delta)) != hipSuccess) return e;
+    if (grad_b_delta && (e = rowsum::sum(L->stream, pb, nwaves, 1, tmp, grad_b_delta)) != hipSuccess) return e;
     if (w_cls && (grad_w_cls || grad_b_cls)) {
         float *pc = reinterpret_cast<float *>(scratch + l.pc);
         float *pbc = reinterpret_cast<float *>(scratch + l.pbc);
-        hipLaunchKernelGGL(k_dfb_cls, dim3((unsigned)((n_cls + 3) / 4), (unsigned)nch), dim3(kBlock), 0, L->stream,
-                           L->m, C, n_cls, nch, grad_out, f, pc, pbc);
+        hipLaunchKernelGGL(k_dfb_cls, dim3((unsigned)((C + kClsC - 1) / kClsC), (unsigned)((n_cls + kClsK - 1) / kClsK),
+                                           (unsigned)nch),
+                           dim3(kBlock), 0, L->stream, L->m, C, n_cls, grad_out, f, pc, pbc);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if (grad_w_cls) {
-            const int64_t n = (int64_t)n_cls * C;
-            hipLaunchKernelGGL(k_dfb_reduce, dim3((unsigned)((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, L->stream,
-                               pc, (int64_t)nch, n, grad_w_cls);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-        }
-        if (grad_b_cls) {
-            hipLaunchKernelGGL(k_dfb_reduce, dim3((unsigned)((n_cls + kBlock - 1) / kBlock)), dim3(kBlock), 0,
-                               L->stream, pbc, (int64_t)nch, (int64_t)n_cls, grad_b_cls);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-        }
+        if (grad_w_cls && (e = rowsum::sum(L->stream, pc, nch, (int64_t)n_cls * C, tmp, grad_w_cls)) != hipSuccess)
+            return e;
+        if (grad_b_cls && (e = rowsum::sum(L->stream, pbc, nch, n_cls, tmp, grad_b_cls)) != hipSuccess) return e;
     }
     return hipSuccess;
 }
@@ -420,10 +428,8 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
 // Wavefronts of the point kernel and point chunks of the classifier kernel.
 void deform_backward_shape(const lattice *L, int *nwaves, int *nch) {
     *nwaves = L->cu_count * 4 * 4;  // four workgroups of four wavefronts per CU
-    int64_t c = L->m / 1024;
-    if (c < 1) c = 1;
-    if (c > 256) c = 256;
-    *nch = (int)c;
+    const int64_t c = (L->m + kClsChunk - 1) / kClsChunk;  // classifier chunks
+    *nch = (int)(c < 1 ? 1 : c);
 }
 
 int64_t deform_backward_scratch_bytes(const lattice *L, int C, int n_cls) {

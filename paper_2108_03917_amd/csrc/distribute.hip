@@ -57,6 +57,7 @@
 // The statistics are fp64 sums added with atomics (their order varies from
 // run to run by a few fp64 ulps, far below the fp32 results' rounding).
 #include "internal.h"
+#include "rowsum.h"
 
 namespace {
 
@@ -945,36 +946,47 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 //                  last block's output h3, fp32
 //   k_dpn_argmax   one wavefront per vertex, lane = channel c: the row whose
 //                  h3[c] is largest (the first in list order), which receives
-//                  g[v][c]; dW3[c][.] += g r3 and db3[c] += g of that row
-//   k_dpn_back<S>  one lane per entry: dh3 (its routed channels), then back
-//                  through block 3 (S = 3: dgamma3, dbeta3 and the group
-//                  sums of gamma dhn and gamma dhn xhat), through block 2
-//                  (S = 2: needs block 3's group means; dW2, db2, dgamma2,
-//                  dbeta2, block 2's group sums) or through block 1 (S = 1:
-//                  dW1, db1, dgamma1, dbeta1).  A group normalisation's input
-//                  gradient is rstd (gn - mean(gn) - xhat mean(gn xhat)),
-//                  gn = gamma dhn, the means over the cloud's rows and the
-//                  group's channels.
-// Sums over entries: per wavefront (shuffles; a wavefront whose rows span
-// clouds adds each cloud's lanes apart) into the wavefront's own LDS row, in
-// the order of its chunks; the workgroup's rows added in wavefront order
-// into one partial row per workgroup (or wavefront), and those added in a
-// fixed order (k_dpn_reduce): the gradients do not depend on scheduling.
-// Lanes past the last entry add zeros: with group normalisation an input
-// gradient has mean terms even where no output gradient reaches the row, so
-// such lanes zero theirs explicitly.
+//                  g[v][c]; dW3[c][.] += g r3 and db3[c] += g of that row; per
+//                  entry the mask of the channels it receives
+//   k_dpn_back<S>  one wavefront per workgroup, a lane per entry: back through
+//                  block 3 (S = 3: dhn3 from the routed channels, stored per
+//                  entry; dgamma3, dbeta3 and the group sums of gamma dhn and
+//                  gamma dhn xhat), block 2 (S = 2: needs block 3's group
+//                  means; dhn2 stored per entry; dW2, db2, dgamma2, dbeta2,
+//                  block 2's group sums) or block 1 (S = 1: dW1, db1, dgamma1,
+//                  dbeta1).  A group normalisation's input gradient is rstd
+//                  (gn - mean(gn) - xhat mean(gn xhat)), gn = gamma dhn, the
+//                  means over the cloud's rows and the group's channels.
+// Sums over entries, per chunk of 64 entries: the entries' vectors are staged
+// in the wavefront's LDS; lane c adds column c over them, in entry order, into
+// a register kept over the wavefront's chunks (the per-channel sums); the
+// weight gradients dW = sum_e dh_e r_e^T run on fp32 MFMA 32x32x2 (two entries
+// a step) into accumulators kept the same way.  A group sum is a gamma-weighted
+// sum of per-channel sums: with one cloud it is formed from those at the end;
+// with several, lane (group, part) adds each entry to its cloud's slot of an
+// LDS table, in entry order.  Each wavefront writes one partial row; the rows
+// are added in a fixed order (rowsum): the gradients do not depend on
+// scheduling.  Lanes past the last entry add zeros: with group normalisation
+// an input gradient has mean terms even where no output gradient reaches the
+// row, so such lanes zero theirs explicitly.
 constexpr int kNrmRow = 3 * 2 * 32;              // per cloud: (mean, rstd) per block and input channel
 constexpr int kRecH1 = kMaxK0, kRecH2 = kRecH1 + kW1, kRecH3 = kRecH2 + kW2, kRec = kRecH3 + kW3;
 constexpr int kPArg = kW3 * kW2 + kW3;                           // per wavefront: dW3, db3
-constexpr int kPB3 = 2 * kW2 + kGnClouds * kW2 * 2;              // dgamma3, dbeta3, group sums
-constexpr int kPB2 = kW2 * kW1 + kW2 + 2 * kW1 + kGnClouds * kW1 * 2;  // dW2, db2, dgamma2, dbeta2, group sums
-constexpr int kPB1 = kW1 * kMaxK0 + kW1 + 2 * kMaxK0;            // dW1, db1, dgamma1, dbeta1
-
-__device__ __forceinline__ float wave_sum_f(float x) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) x += __shfl_xor(x, o);
-    return x;
+// Partial rows of the passes: S = 3 dgamma3 [32], dbeta3 [32]; S = 2 dW2
+// [32][16], db2 [32], dgamma2 [16], dbeta2 [16]; S = 1 dW1 [16][16], db1
+// [16], dgamma1 [16], dbeta1 [16]; then (S = 3, 2) the group sums, slot
+// (cloud K + group) 2 + part, of one cloud or (batched) of kGnClouds.
+constexpr int kPB3Base = 2 * kW2, kPB2Base = kW2 * kW1 + kW2 + 2 * kW1;
+constexpr int kPB3 = kPB3Base + kGnClouds * kW2 * 2;
+constexpr int kPB2 = kPB2Base + kGnClouds * kW1 * 2;
+constexpr int kPB1 = kW1 * kMaxK0 + kW1 + 2 * kMaxK0;
+__host__ __device__ inline int pb_len(int S, int batched) {
+    const int nc = batched ? kGnClouds : 1;
+    return S == 3 ? kPB3Base + nc * kW2 * 2 : (S == 2 ? kPB2Base + nc * kW1 * 2 : kPB1);
 }
+constexpr int kStg = 80;  // staged floats per entry (64-entry chunks)
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // Block l's input width (l = 0, 1, 2) and its padded width.
 __host__ __device__ __forceinline__ int in_width(int l, int k0) { return l == 0 ? k0 : (l == 1 ? kW1 : kW2); }
@@ -1100,8 +1112,8 @@ __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict
                                                        const uint64_t *__restrict__ vkeys, int batched,
                                                        const float *__restrict__ aff, const float *__restrict__ rec,
                                                        const float *__restrict__ grad_out,
-                                                       const int32_t *__restrict__ counters, int32_t *__restrict__ am,
-                                                       float *__restrict__ part) {
+                                                       const int32_t *__restrict__ counters,
+                                                       uint64_t *__restrict__ routed, float *__restrict__ part) {
     const int lane = threadIdx.x & 63;  // output channel c
     const int64_t V = counters[CNT_V];
     const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
@@ -1121,7 +1133,17 @@ __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict
                 be = off + i;
             }
         }
-        am[v * kW3 + lane] = (int32_t)be;
+        // per entry of v, the mask of the channels it wins (lane k of a block
+        // of 64 entries stores entry k's)
+        for (int i0 = 0; i0 < cnt; i0 += 64) {
+            const int nb = cnt - i0 < 64 ? cnt - i0 : 64;
+            uint64_t mine = 0;
+            for (int k = 0; k < nb; ++k) {
+                const uint64_t mk = __ballot(be == off + i0 + k);
+                mine = lane == k ? mk : mine;
+            }
+            if (lane < nb) routed[off + i0 + lane] = mine;
+        }
         const float g = grad_out[v * kW3 + lane];
         db += g;
         const float *A = aff + (int64_t)cloud_of(vkeys, batched, (int)v) * kAffRow;
@@ -1135,64 +1157,41 @@ __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict
     out[kW3 * kW2 + lane] = db;
 }
 
-// Add a wavefront's per-lane values of one slot into the wavefront's own LDS
-// row (lane 0 adds, in program order).
-__device__ __forceinline__ void wave_add(float *acc, int q, float x) {
-    x = wave_sum_f(x);
-    if ((threadIdx.x & 63) == 0) acc[q] += x;
-}
-
-// The group sums of one block: per channel j < K, x[j] and x[j] y[j] added
-// to the slots q0 + (cloud * K + j / gs) * 2 and that + 1 of the lanes'
-// clouds.  A wavefront within one cloud adds once; one that spans clouds
-// adds each cloud's lanes apart (masked sums, the clouds in lane order).
-template <int K>
-__device__ __forceinline__ void wave_add_groups(float *acc, int q0, int gs, int cloud, bool live, bool one_cloud,
-                                                const float *x, const float *y) {
-    if (one_cloud) {
-#pragma unroll
-        for (int j = 0; j < K; ++j) {
-            const int q = q0 + (cloud * K + j / gs) * 2;
-            wave_add(acc, q, x[j]);
-            wave_add(acc, q + 1, x[j] * y[j]);
-        }
-        return;
-    }
-    unsigned long long todo = __ballot(live);
-    while (todo) {
-        const int cb = __shfl(cloud, __builtin_ctzll(todo));
-        const bool mine = live && cloud == cb;
-        todo &= ~__ballot(mine);
-#pragma unroll
-        for (int j = 0; j < K; ++j) {
-            const int q = q0 + (cb * K + j / gs) * 2;
-            wave_add(acc, q, mine ? x[j] : 0.f);
-            wave_add(acc, q + 1, mine ? x[j] * y[j] : 0.f);
-        }
-    }
-}
-
+// One backward pass (see above).  din: the previous pass's stored per-entry
+// gradient (S = 2: dhn3 [E][32], S = 1: dhn2 [E][16]); dout: this pass's
+// (S = 3: dhn3, S = 2: dhn2).  One wavefront per workgroup.
 template <int S>
-__global__ __launch_bounds__(kBlock) void k_dpn_back(const int32_t *__restrict__ lvert,
-                                                     const uint64_t *__restrict__ vkeys, int batched, int use_gn,
-                                                     int G1, int G2, const float *__restrict__ P,
-                                                     const float *__restrict__ aff, const float *__restrict__ nrm,
-                                                     const float *__restrict__ gm, const float *__restrict__ rec,
-                                                     const int32_t *__restrict__ am,
-                                                     const float *__restrict__ grad_out,
-                                                     const int32_t *__restrict__ counters, float *__restrict__ part) {
-    constexpr int NP = S == 3 ? kPB3 : (S == 2 ? kPB2 : kPB1);
+__global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lvert,
+                                                 const uint64_t *__restrict__ vkeys, int batched, int use_gn, int G1,
+                                                 int G2, const float *__restrict__ P, const float *__restrict__ aff,
+                                                 const float *__restrict__ nrm, const float *__restrict__ gm,
+                                                 const float *__restrict__ rec, const uint64_t *__restrict__ routed,
+                                                 const float *__restrict__ grad_out, const float *__restrict__ din,
+                                                 float *__restrict__ dout, const int32_t *__restrict__ counters,
+                                                 float *__restrict__ part) {
+    constexpr int K = S == 3 ? kW2 : (S == 2 ? kW1 : kMaxK0);  // channels of block S's normalisation
+    constexpr int NV = S == 1 ? 3 * 16 : 64;                    // staged columns with a per-channel sum
+    constexpr int DH = 32, RR = S == 2 ? 64 : 48;               // staged dh and r (S = 2, 1)
     __shared__ float Ps[kPadded];
-    __shared__ float accs[kWaves * NP];  // one row per wavefront
-    for (int i = threadIdx.x; i < kWaves * NP; i += kBlock) accs[i] = 0.f;
-    load_params(P, Ps);
-    const int lane = threadIdx.x & 63;
-    float *acc = accs + (threadIdx.x >> 6) * NP;
+    __shared__ float stg[64 * kStg];
+    __shared__ int scl[64];
+    extern __shared__ float tab[];  // per-cloud group sums, batched only: [kGnClouds][2 K] (launch size)
+    const int lane = threadIdx.x;
+    for (int i = lane; i < kPadded; i += 64) Ps[i] = P[i];
+    const bool tabbed = S != 1 && use_gn && batched;
+    if (tabbed)
+        for (int i = lane; i < kGnClouds * 2 * K; i += 64) tab[i] = 0.f;
+    __syncthreads();
     const int64_t E = counters[CNT_E];
-    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
-    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
-    const int gs3 = kW2 / G2, gs2 = kW1 / G1;  // channels per group of blocks 3 and 2
-    for (int64_t e0 = wave * 64; e0 < E; e0 += nwaves * 64) {
+    const int G = S == 3 ? G2 : G1;
+    const int gs = K / G;                                       // channels per group (S = 3, 2)
+    const int gs3 = kW2 / G2, gs2 = kW1 / G1;
+    float vacc = 0.f;
+    f32x16_t macc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) macc[i] = 0.f;
+    float *st = stg + lane * kStg;
+    for (int64_t e0 = (int64_t)blockIdx.x * 64; e0 < E; e0 += (int64_t)gridDim.x * 64) {
         const int64_t e = e0 + lane;
         const bool live = e < E;
         const int v = live ? lvert[e] : 0;
@@ -1200,137 +1199,214 @@ __global__ __launch_bounds__(kBlock) void k_dpn_back(const int32_t *__restrict__
         const float *A = aff + (int64_t)cloud * kAffRow;
         const float *N = nrm + (int64_t)cloud * kNrmRow;
         const float *R = rec + (live ? e : 0) * kRec;
-        // block 3: dr3 = W3^T dh3 over the output channels routed to this
-        // row (dh3[o] = g[v][o] where the row wins channel o, else 0), then
-        // dhn3 = dr3 [hn3 > 0]
-        float dhn3[kW2], xh3[kW2];
-#pragma unroll
-        for (int j = 0; j < kW2; ++j) dhn3[j] = 0.f;
-        if (live) {
-            for (int o = 0; o < kW3; ++o) {
-                if (am[(int64_t)v * kW3 + o] != (int32_t)e) continue;
-                const float g = grad_out[(int64_t)v * kW3 + o];
-#pragma unroll
-                for (int j = 0; j < kW2; ++j) dhn3[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dhn3[j]);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < kW2; ++j) {
-            const float h = R[kRecH2 + j];
-            dhn3[j] = fmaf(A[kAff2 + j], h, A[kAff2 + kW2 + j]) > 0.f ? dhn3[j] : 0.f;
-            xh3[j] = (h - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
-        }
-        const bool one_cloud = __ballot(live && cloud != __shfl(cloud, 0)) == 0ull;
         if (S == 3) {
+            // dr3 = W3^T dh3, dh3 = g_v on the channels routed to this entry
+            // (its mask) and 0 elsewhere: the row of g is loaded whole, and
+            // the channels run in the same order in every lane, so that the
+            // weights are LDS broadcasts
+            const uint64_t mk = live ? routed[e] : 0ull;
+            float gv[kW3];
+            const float *grow = grad_out + (int64_t)v * kW3;
+            if ((reinterpret_cast<uintptr_t>(grad_out) & 15) == 0) {  // 16-byte rows (uniform branch)
+                const float4 *g4 = reinterpret_cast<const float4 *>(grow);
 #pragma unroll
-            for (int j = 0; j < kW2; ++j) {
-                wave_add(acc, j, dhn3[j] * xh3[j]);   // dgamma3
-                wave_add(acc, kW2 + j, dhn3[j]);      // dbeta3
-            }
-            if (use_gn) {
-                // each channel's terms go to its group's slot
-                float g3[kW2];
-#pragma unroll
-                for (int j = 0; j < kW2; ++j) g3[j] = Ps[kA2 + j] * dhn3[j];
-                wave_add_groups<kW2>(acc, 2 * kW2, gs3, cloud, live, one_cloud, g3, xh3);
-            }
-        } else {
-            // block 3's input gradient
-            float dh2[kW2];
-#pragma unroll
-            for (int j = 0; j < kW2; ++j) {
-                const float gj = Ps[kA2 + j] * dhn3[j];
-                if (use_gn) {
-                    const float *M = gm + ((int64_t)cloud * 2 + 1) * kW2 * 2 + (j / gs3) * 2;
-                    dh2[j] = live ? N[2 * 64 + 2 * j + 1] * (gj - M[0] - xh3[j] * M[1]) : 0.f;
-                } else {
-                    dh2[j] = gj;
+                for (int q = 0; q < kW3 / 4; ++q) {
+                    const float4 t4 = g4[q];
+                    gv[4 * q] = t4.x;
+                    gv[4 * q + 1] = t4.y;
+                    gv[4 * q + 2] = t4.z;
+                    gv[4 * q + 3] = t4.w;
                 }
+            } else {
+#pragma unroll
+                for (int o = 0; o < kW3; ++o) gv[o] = grow[o];
             }
-            // block 2: r2, dr2 = W2^T dh2, dhn2, xhat2
-            float r2[kW1], dhn2[kW1], xh2[kW1];
+            float dr[kW2];
+#pragma unroll
+            for (int j = 0; j < kW2; ++j) dr[j] = 0.f;
+#pragma unroll 4
+            for (int o = 0; o < kW3; ++o) {
+                const float g = ((mk >> o) & 1ull) ? gv[o] : 0.f;
+#pragma unroll
+                for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dr[j]);
+            }
+#pragma unroll
+            for (int j = 0; j < kW2; ++j) {
+                const float h = R[kRecH2 + j];
+                const float d = (live && fmaf(A[kAff2 + j], h, A[kAff2 + kW2 + j]) > 0.f) ? dr[j] : 0.f;
+                const float xh = (h - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
+                dr[j] = d;
+                st[j] = d;
+                st[kW2 + j] = d * xh;
+            }
+            if (live) {
+                float4 *o4 = reinterpret_cast<float4 *>(dout + e * kW2);
+#pragma unroll
+                for (int q = 0; q < kW2 / 4; ++q) o4[q] = make_float4(dr[4 * q], dr[4 * q + 1], dr[4 * q + 2], dr[4 * q + 3]);
+            }
+        } else if (S == 2) {
+            // block 3's input gradient dh2, then block 2: r2, dr2 = W2^T dh2, dhn2
+            float dh[kW2];
+            const float4 *i4 = reinterpret_cast<const float4 *>(din + (live ? e : 0) * kW2);
+#pragma unroll
+            for (int q = 0; q < kW2 / 4; ++q) {
+                const float4 d4 = live ? i4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+                dh[4 * q] = d4.x;
+                dh[4 * q + 1] = d4.y;
+                dh[4 * q + 2] = d4.z;
+                dh[4 * q + 3] = d4.w;
+            }
+#pragma unroll
+            for (int j = 0; j < kW2; ++j) {
+                const float gj = Ps[kA2 + j] * dh[j];
+                if (use_gn) {
+                    const float xh = (R[kRecH2 + j] - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
+                    const float *M = gm + ((int64_t)cloud * 2 + 1) * kW2 * 2 + (j / gs3) * 2;
+                    dh[j] = live ? N[2 * 64 + 2 * j + 1] * (gj - M[0] - xh * M[1]) : 0.f;
+                } else {
+                    dh[j] = gj;
+                }
+                st[DH + j] = dh[j];
+            }
+            float dn[kW1];
 #pragma unroll
             for (int c = 0; c < kW1; ++c) {
                 const float h = R[kRecH1 + c];
                 const float hn = fmaf(A[kAff1 + c], h, A[kAff1 + kW1 + c]);
-                r2[c] = relu(hn);
-                float s = 0.f;
+                float s_ = 0.f;
 #pragma unroll
-                for (int j = 0; j < kW2; ++j) s = fmaf(dh2[j], Ps[kWt1 + j * kW1 + c], s);
-                dhn2[c] = hn > 0.f ? s : 0.f;
-                xh2[c] = (h - N[1 * 64 + 2 * c]) * N[1 * 64 + 2 * c + 1];
+                for (int j = 0; j < kW2; ++j) s_ = fmaf(dh[j], Ps[kWt1 + j * kW1 + c], s_);
+                const float d = hn > 0.f ? s_ : 0.f;
+                const float xh = (h - N[1 * 64 + 2 * c]) * N[1 * 64 + 2 * c + 1];
+                dn[c] = d;
+                st[c] = d;
+                st[kW1 + c] = d * xh;
+                st[RR + c] = live ? relu(hn) : 0.f;
             }
-            if (S == 2) {
+            if (live) {
+                float4 *o4 = reinterpret_cast<float4 *>(dout + e * kW1);
 #pragma unroll
-                for (int j = 0; j < kW2; ++j) {
+                for (int q = 0; q < kW1 / 4; ++q) o4[q] = make_float4(dn[4 * q], dn[4 * q + 1], dn[4 * q + 2], dn[4 * q + 3]);
+            }
+        } else {
+            // block 2's input gradient dh1, then block 1: r1, dr1 = W1^T dh1, dhn1
+            float dh[kW1];
+            const float4 *i4 = reinterpret_cast<const float4 *>(din + (live ? e : 0) * kW1);
 #pragma unroll
-                    for (int c = 0; c < kW1; ++c) wave_add(acc, j * kW1 + c, dh2[j] * r2[c]);  // dW2
-                    wave_add(acc, kW2 * kW1 + j, dh2[j]);                                   // db2
-                }
+            for (int q = 0; q < kW1 / 4; ++q) {
+                const float4 d4 = live ? i4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+                dh[4 * q] = d4.x;
+                dh[4 * q + 1] = d4.y;
+                dh[4 * q + 2] = d4.z;
+                dh[4 * q + 3] = d4.w;
+            }
 #pragma unroll
-                for (int c = 0; c < kW1; ++c) {
-                    wave_add(acc, kW2 * kW1 + kW2 + c, dhn2[c] * xh2[c]);        // dgamma2
-                    wave_add(acc, kW2 * kW1 + kW2 + kW1 + c, dhn2[c]);           // dbeta2
-                }
+            for (int c = 0; c < kW1; ++c) {
+                const float gc = Ps[kA1 + c] * dh[c];
                 if (use_gn) {
-                    float g2[kW1];
-#pragma unroll
-                    for (int c = 0; c < kW1; ++c) g2[c] = Ps[kA1 + c] * dhn2[c];
-                    wave_add_groups<kW1>(acc, kW2 * kW1 + kW2 + 2 * kW1, gs2, cloud, live, one_cloud, g2, xh2);
+                    const float xh = (R[kRecH1 + c] - N[1 * 64 + 2 * c]) * N[1 * 64 + 2 * c + 1];
+                    const float *M = gm + ((int64_t)cloud * 2 + 0) * kW2 * 2 + (c / gs2) * 2;
+                    dh[c] = live ? N[1 * 64 + 2 * c + 1] * (gc - M[0] - xh * M[1]) : 0.f;
+                } else {
+                    dh[c] = gc;
                 }
-            } else {
-                // block 2's input gradient, then block 1
-                float dh1[kW1];
+                st[DH + c] = dh[c];
+            }
 #pragma unroll
-                for (int c = 0; c < kW1; ++c) {
-                    const float gc = Ps[kA1 + c] * dhn2[c];
-                    if (use_gn) {
-                        const float *M = gm + ((int64_t)cloud * 2 + 0) * kW2 * 2 + (c / gs2) * 2;
-                        dh1[c] = live ? N[1 * 64 + 2 * c + 1] * (gc - M[0] - xh2[c] * M[1]) : 0.f;
-                    } else {
-                        dh1[c] = gc;
-                    }
-                }
-                float r1[kMaxK0];
+            for (int c = 0; c < kMaxK0; ++c) {
+                const float h = R[c];
+                const float hn = fmaf(A[kAff0 + c], h, A[kAff0 + kMaxK0 + c]);
+                float s_ = 0.f;
 #pragma unroll
-                for (int c = 0; c < kMaxK0; ++c) r1[c] = relu(fmaf(A[kAff0 + c], R[c], A[kAff0 + kMaxK0 + c]));
-#pragma unroll
-                for (int o = 0; o < kW1; ++o) {
-#pragma unroll
-                    for (int c = 0; c < kMaxK0; ++c) wave_add(acc, o * kMaxK0 + c, dh1[o] * r1[c]);  // dW1
-                    wave_add(acc, kW1 * kMaxK0 + o, dh1[o]);                                       // db1
-                }
-#pragma unroll
-                for (int c = 0; c < kMaxK0; ++c) {
-                    float s = 0.f;
-#pragma unroll
-                    for (int o = 0; o < kW1; ++o) s = fmaf(dh1[o], Ps[kWt0 + o * kMaxK0 + c], s);
-                    const float h = R[c];
-                    const float dhn1 = fmaf(A[kAff0 + c], h, A[kAff0 + kMaxK0 + c]) > 0.f ? s : 0.f;
-                    const float xh1 = (h - N[2 * c]) * N[2 * c + 1];
-                    wave_add(acc, kW1 * kMaxK0 + kW1 + c, dhn1 * xh1);            // dgamma1
-                    wave_add(acc, kW1 * kMaxK0 + kW1 + kMaxK0 + c, dhn1);         // dbeta1
-                }
+                for (int o = 0; o < kW1; ++o) s_ = fmaf(dh[o], Ps[kWt0 + o * kMaxK0 + c], s_);
+                const float d = hn > 0.f ? s_ : 0.f;
+                st[c] = d;
+                st[kMaxK0 + c] = d * ((h - N[2 * c]) * N[2 * c + 1]);
+                st[RR + c] = live ? relu(hn) : 0.f;
             }
         }
+        scl[lane] = live ? cloud : -1;
+        __syncthreads();
+        // per-channel sums: lane c adds column c, entries in order
+        if (lane < NV) {
+#pragma unroll 8
+            for (int k = 0; k < 64; ++k) vacc += stg[k * kStg + lane];
+        }
+        // batched group sums: lane (group, part) adds each entry to its cloud
+        if (tabbed && lane < 2 * G) {
+            const int grp = lane >> 1, pt = lane & 1;
+            for (int k = 0; k < 64; ++k) {
+                const int cl = scl[k];
+                if (cl < 0) continue;
+                float x = 0.f;
+                for (int t = 0; t < gs; ++t) {
+                    const int ch = grp * gs + t;
+                    x = fmaf(Ps[(S == 3 ? kA2 : kA1) + ch], stg[k * kStg + pt * K + ch], x);
+                }
+                tab[cl * 2 * K + lane] += x;
+            }
+        }
+        // weight gradient: two entries a step, dh rows as A, r rows as B
+        if (S != 3) {
+            const int i = lane & 31, half = lane >> 5;
+#pragma unroll 4
+            for (int s2 = 0; s2 < 32; ++s2) {
+                const float *row = stg + (2 * s2 + half) * kStg;
+                const float a = (S == 2 || i < kW1) ? row[DH + (i & (S == 2 ? 31 : 15))] : 0.f;
+                const float b = i < 16 ? row[RR + (i & 15)] : 0.f;
+                macc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, macc, 0, 0, 0);
+            }
+        }
+        __syncthreads();  // the staging is rewritten by the next chunk
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < NP; i += kBlock) {
-        float x = accs[i];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) x += accs[w * NP + i];
-        part[(int64_t)blockIdx.x * NP + i] = x;
-    }
-}
 
-// out[j] = sum over r < rows of part[r * n + j], in order of r (fp64).
-__global__ __launch_bounds__(kBlock) void k_dpn_reduce(const float *__restrict__ part, int64_t rows, int64_t n,
-                                                       float *__restrict__ out) {
-    const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (j >= n) return;
-    double s = 0.0;
-    for (int64_t r = 0; r < rows; ++r) s += (double)part[r * n + j];
-    out[j] = (float)s;
+    // the wavefront's partial row
+    const int np = pb_len(S, batched);
+    float *out = part + (int64_t)blockIdx.x * np;
+    if (S == 3) {
+        out[lane < kW2 ? kW2 + lane : lane - kW2] = vacc;  // dbeta3 (columns 0..31), dgamma3 (32..63)
+    } else if (S == 2) {
+        if (lane < kW1) out[kW2 * kW1 + kW2 + kW1 + lane] = vacc;                  // dbeta2
+        else if (lane < 2 * kW1) out[kW2 * kW1 + kW2 + (lane - kW1)] = vacc;       // dgamma2
+        else out[kW2 * kW1 + (lane - 2 * kW1)] = vacc;                             // db2
+    } else {
+        if (lane < kMaxK0) out[kW1 * kMaxK0 + kW1 + kMaxK0 + lane] = vacc;         // dbeta1
+        else if (lane < 2 * kMaxK0) out[kW1 * kMaxK0 + kW1 + (lane - kMaxK0)] = vacc;  // dgamma1
+        else if (lane < 3 * kMaxK0) out[kW1 * kMaxK0 + (lane - 2 * kMaxK0)] = vacc;    // db1
+    }
+    if (S != 3) {
+        // the MFMA tile: lane l holds column l mod 32, register r row
+        // 8 (r / 4) + 4 (l / 32) + r mod 4
+        const int j = lane & 31;
+        constexpr int NI = S == 2 ? kW2 : kW1, NJ = S == 2 ? kW1 : kMaxK0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int i = 8 * (r / 4) + 4 * (lane >> 5) + (r & 3);
+            if (i < NI && j < NJ) out[i * NJ + j] = macc[r];
+        }
+    }
+    if (S != 1 && use_gn) {
+        const int base = S == 3 ? kPB3Base : kPB2Base;
+        if (tabbed) {
+            __syncthreads();
+            for (int i = lane; i < kGnClouds * 2 * K; i += 64) out[base + i] = tab[i];
+        } else {
+            // one cloud: group sum = sum over the group's channels of gamma
+            // times the per-channel sum (dbeta's column, or dgamma's: dbeta
+            // in lane ch, dgamma in lane K + ch)
+            const int grp = lane >> 1, pt = lane & 1;
+            float x = 0.f;
+            for (int t = 0; t < gs; ++t) {
+                const int ch = (grp < G ? grp : 0) * gs + t;
+                const float y = __shfl(vacc, pt * K + ch);
+                x = fmaf(Ps[(S == 3 ? kA2 : kA1) + ch], y, x);
+            }
+            if (lane < 2 * K) out[base + lane] = grp < G ? x : 0.f;
+        }
+    } else if (S != 1) {
+        const int base = S == 3 ? kPB3Base : kPB2Base;
+        for (int i = lane; i < np - base; i += 64) out[base + i] = 0.f;
+    }
 }
 
 // The group means of block l's (l = 1: block 2, l = 2: block 3) gradient
@@ -1486,31 +1562,37 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
 
 // Scratch of the backward (offsets in bytes, 256-aligned).
 struct DpnLayout {
-    int64_t out, rec, am, nrm, rows, gm, parg, pb3, pb2, pb1, r3, r2, r1, rarg, total;
-    int nwaves_arg, nwg;
+    int64_t out, rec, routed, d3, d2, nrm, rows, gm, parg, pb3, pb2, pb1, r3, r2, r1, rarg, tmp, total;
+    int nwaves_arg, nwaves;
 };
 
 static DpnLayout dpn_layout(const lattice *L) {
     auto al = [](int64_t x) { return (x + 255) / 256 * 256; };
     DpnLayout l;
-    l.nwaves_arg = L->cu_count * 4 * kWaves;  // four workgroups per CU
-    l.nwg = L->cu_count * 4;
+    l.nwaves_arg = L->cu_count * 4 * kWaves;  // four workgroups of four wavefronts per CU
+    l.nwaves = L->cu_count * 4;               // backward passes: four one-wavefront workgroups per CU
     const int64_t V = L->max_vertices, E = (int64_t)(L->d + 1) * L->max_points;
     int64_t at = 0;
-    l.out = at;  at += al(V * kW3 * 4);
-    l.rec = at;  at += al(E * kRec * 4);
-    l.am = at;   at += al(V * kW3 * 4);
-    l.nrm = at;  at += al((int64_t)kGnClouds * kNrmRow * 4);
-    l.rows = at; at += al((int64_t)kGnClouds * 8);
-    l.gm = at;   at += al((int64_t)kGnClouds * 2 * kW2 * 2 * 4);
-    l.parg = at; at += al((int64_t)l.nwaves_arg * kPArg * 4);
-    l.pb3 = at;  at += al((int64_t)l.nwg * kPB3 * 4);
-    l.pb2 = at;  at += al((int64_t)l.nwg * kPB2 * 4);
-    l.pb1 = at;  at += al((int64_t)l.nwg * kPB1 * 4);
-    l.r3 = at;   at += al(kPB3 * 4);
-    l.r2 = at;   at += al(kPB2 * 4);
-    l.r1 = at;   at += al(kPB1 * 4);
-    l.rarg = at; at += al(kPArg * 4);
+    l.out = at;    at += al(V * kW3 * 4);
+    l.rec = at;    at += al(E * kRec * 4);
+    l.routed = at; at += al(E * 8);
+    l.d3 = at;     at += al(E * kW2 * 4);
+    l.d2 = at;     at += al(E * kW1 * 4);
+    l.nrm = at;    at += al((int64_t)kGnClouds * kNrmRow * 4);
+    l.rows = at;   at += al((int64_t)kGnClouds * 8);
+    l.gm = at;     at += al((int64_t)kGnClouds * 2 * kW2 * 2 * 4);
+    l.parg = at;   at += al((int64_t)l.nwaves_arg * kPArg * 4);
+    l.pb3 = at;    at += al((int64_t)l.nwaves * kPB3 * 4);
+    l.pb2 = at;    at += al((int64_t)l.nwaves * kPB2 * 4);
+    l.pb1 = at;    at += al((int64_t)l.nwaves * kPB1 * 4);
+    l.r3 = at;     at += al(kPB3 * 4);
+    l.r2 = at;     at += al(kPB2 * 4);
+    l.r1 = at;     at += al(kPB1 * 4);
+    l.rarg = at;   at += al(kPArg * 4);
+    int64_t t = rowsum::scratch_floats(l.nwaves_arg, kPArg);
+    for (int64_t n : {kPB3, kPB2, kPB1})
+        if (rowsum::scratch_floats(l.nwaves, n) > t) t = rowsum::scratch_floats(l.nwaves, n);
+    l.tmp = at;    at += al(t * 4);
     l.total = at;
     return l;
 }
@@ -1520,13 +1602,8 @@ int64_t pointnet_backward_scratch_bytes(const lattice *L) { return dpn_layout(L)
 hipError_t launch_distribute_backward(lattice *L, const float *pos, const float *feat, int f_d, const float *params,
                                       const int *groups, float eps, const float *grad_out, float *grad_params,
                                       void *scratch) {
-    if (L->m == 0) {
-        // no rows: every gradient is zero
-        const int n = pointnet_param_count(L->d + f_d);
-        hipLaunchKernelGGL(k_dpn_reduce, dim3((n + kBlock - 1) / kBlock), dim3(kBlock), 0, L->stream,
-                           grad_params, (int64_t)0, (int64_t)n, grad_params);
-        return hipGetLastError();
-    }
+    if (L->m == 0)  // no rows: every gradient is zero (a sum of no rows)
+        return rowsum::sum(L->stream, grad_params, 0, pointnet_param_count(L->d + f_d), nullptr, grad_params);
     const DpnLayout l = dpn_layout(L);
     char *s = reinterpret_cast<char *>(scratch);
     auto F = [&](int64_t off) { return reinterpret_cast<float *>(s + off); };
@@ -1557,19 +1634,18 @@ hipError_t launch_distribute_backward(lattice *L, const float *pos, const float 
             return hipErrorInvalidValue;
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    int32_t *am = reinterpret_cast<int32_t *>(s + l.am);
+    uint64_t *routed = reinterpret_cast<uint64_t *>(s + l.routed);
     hipLaunchKernelGGL(k_dpn_argmax, dim3((unsigned)(l.nwaves_arg / kWaves)), dim3(kBlock), 0, L->stream, L->vinfo,
-                       L->vkeys, batched, L->pn_aff, F(l.rec), grad_out, L->counters, am, F(l.parg));
+                       L->vkeys, batched, L->pn_aff, F(l.rec), grad_out, L->counters, routed, F(l.parg));
     if ((e = hipGetLastError()) != hipSuccess) return e;
     auto reduce = [&](const float *part, int64_t nrows, int64_t n, float *out) {
-        hipLaunchKernelGGL(k_dpn_reduce, dim3((unsigned)((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, L->stream,
-                           part, nrows, n, out);
-        return hipGetLastError();
+        return rowsum::sum(L->stream, part, nrows, n, F(l.tmp), out);
     };
-    auto back = [&](auto kern, int64_t part_off) {
-        hipLaunchKernelGGL(kern, dim3((unsigned)l.nwg), dim3(kBlock), 0, L->stream, L->lvert, L->vkeys, batched,
-                           use_gn, G1, G2, L->pn_params, L->pn_aff, F(l.nrm), F(l.gm), F(l.rec), am, grad_out,
-                           L->counters, F(part_off));
+    auto back = [&](auto kern, int K, const float *din, float *dout, int64_t part_off) {
+        const size_t tab = (use_gn && batched && K > 0) ? (size_t)kGnClouds * 2 * K * sizeof(float) : 0;
+        hipLaunchKernelGGL(kern, dim3((unsigned)l.nwaves), dim3(64), tab, L->stream, L->lvert, L->vkeys, batched,
+                           use_gn, G1, G2, L->pn_params, L->pn_aff, F(l.nrm), F(l.gm), F(l.rec), routed, grad_out,
+                           din, dout, L->counters, F(part_off));
         return hipGetLastError();
     };
     auto gnmean = [&](const float *sums, int lb, int G) {
@@ -1577,14 +1653,14 @@ hipError_t launch_distribute_backward(lattice *L, const float *pos, const float 
                            F(l.gm));
         return hipGetLastError();
     };
-    if ((e = back(k_dpn_back<3>, l.pb3)) != hipSuccess) return e;
-    if ((e = reduce(F(l.pb3), l.nwg, kPB3, F(l.r3))) != hipSuccess) return e;
-    if (use_gn && (e = gnmean(F(l.r3) + 2 * kW2, 2, G2)) != hipSuccess) return e;
-    if ((e = back(k_dpn_back<2>, l.pb2)) != hipSuccess) return e;
-    if ((e = reduce(F(l.pb2), l.nwg, kPB2, F(l.r2))) != hipSuccess) return e;
-    if (use_gn && (e = gnmean(F(l.r2) + kW2 * kW1 + kW2 + 2 * kW1, 1, G1)) != hipSuccess) return e;
-    if ((e = back(k_dpn_back<1>, l.pb1)) != hipSuccess) return e;
-    if ((e = reduce(F(l.pb1), l.nwg, kPB1, F(l.r1))) != hipSuccess) return e;
+    if ((e = back(k_dpn_back<3>, kW2, nullptr, F(l.d3), l.pb3)) != hipSuccess) return e;
+    if ((e = reduce(F(l.pb3), l.nwaves, pb_len(3, batched), F(l.r3))) != hipSuccess) return e;
+    if (use_gn && (e = gnmean(F(l.r3) + kPB3Base, 2, G2)) != hipSuccess) return e;
+    if ((e = back(k_dpn_back<2>, kW1, F(l.d3), F(l.d2), l.pb2)) != hipSuccess) return e;
+    if ((e = reduce(F(l.pb2), l.nwaves, pb_len(2, batched), F(l.r2))) != hipSuccess) return e;
+    if (use_gn && (e = gnmean(F(l.r2) + kPB2Base, 1, G1)) != hipSuccess) return e;
+    if ((e = back(k_dpn_back<1>, 0, F(l.d2), nullptr, l.pb1)) != hipSuccess) return e;
+    if ((e = reduce(F(l.pb1), l.nwaves, kPB1, F(l.r1))) != hipSuccess) return e;
     if ((e = reduce(F(l.parg), l.nwaves_arg, kPArg, F(l.rarg))) != hipSuccess) return e;
     hipLaunchKernelGGL(k_dpn_out, dim3(16), dim3(kBlock), 0, L->stream, F(l.r1), F(l.r2), F(l.r3), F(l.rarg), k0,
                        grad_params);
