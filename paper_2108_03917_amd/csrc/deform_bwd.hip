@@ -23,7 +23,7 @@
 //                  per wavefront (written as partials at the end).
 //   k_dfb_gather   one wavefront per vertex over its pair list (the splat's
 //                  lists: no atomics), lane = channel.
-//   k_dfb_cls      dW_cls and db_cls partials per chunk of 1024 points, a
+//   k_dfb_cls      dW_cls and db_cls partials per chunk of 256 points, a
 //                  tile of 16 classes x 64 channels per workgroup, the
 //                  chunk's g and f staged through LDS 128 points at a time.
 //   rowsum         every partial added in a fixed order: the results do not
@@ -34,11 +34,19 @@
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kClsLdsFloats = 4096;  // classifier weights staged in LDS up to 16 KB (occupancy kept)
 
-__device__ __forceinline__ float wave_sum_f(float x) {
+// N wavefront sums at once (each step of the N butterflies issued together).
+template <int N>
+__device__ __forceinline__ void wave_sum_n(float *x) {
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
-    return x;
+    for (int off = 32; off > 0; off >>= 1) {
+        float y[N];
+#pragma unroll
+        for (int k = 0; k < N; ++k) y[k] = __shfl_xor(x[k], off, 64);
+#pragma unroll
+        for (int k = 0; k < N; ++k) x[k] += y[k];
+    }
 }
 
 template <bool IN_BF16>
@@ -49,12 +57,12 @@ __device__ __forceinline__ float value_at(const void *values, int64_t at) {
 
 // Scratch carved out of one buffer (offsets in bytes, each 256-aligned).
 struct DfbLayout {
-    int64_t gf, am, coef, f, pw, pb, pc, pbc, tmp, total;
+    int64_t gf, am, coef, f, pw, pb, pc, pbc, tmp, part, total;
 };
 
 __host__ __device__ inline int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
 
-inline DfbLayout dfb_layout(int64_t m, int C, int dp1, int n_cls, int nwaves, int nch) {
+inline DfbLayout dfb_layout(int64_t m, int C, int dp1, int n_cls, int nwaves, int nch, int64_t part_rows) {
     DfbLayout l;
     int64_t at = 0;
     l.gf = at;   at += align256(m * C * 4);
@@ -69,6 +77,7 @@ inline DfbLayout dfb_layout(int64_t m, int C, int dp1, int n_cls, int nwaves, in
     int64_t t = rowsum::scratch_floats(nwaves, C);
     if (n_cls > 0 && rowsum::scratch_floats(nch, (int64_t)n_cls * C) > t) t = rowsum::scratch_floats(nch, (int64_t)n_cls * C);
     l.tmp = at;  at += align256(t * 4);
+    l.part = at; at += align256(part_rows * 2 * C * 4);  // the long lists' part rows: acc, accw
     l.total = at;
     return l;
 }
@@ -95,15 +104,39 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
         acc_w[i] = 0.f;
     }
     float acc_b = 0.f;
+    // the classifier's weights in LDS when they fit (wcs = 1), else read
+    // from global memory
+    extern __shared__ float wcs_lds[];
+    const bool wcs = CLS && (int64_t)n_cls * C <= kClsLdsFloats;
+    if (wcs) {
+        for (int64_t i = threadIdx.x; i < (int64_t)n_cls * C; i += kBlock) wcs_lds[i] = w_cls[i];
+        __syncthreads();
+    }
+    const float *wc = wcs ? wcs_lds : w_cls;
 
+    // the next point's record is loaded while this point is processed
+    int vn[DP1];
+    float bn[DP1];
+    auto load_record = [&](int64_t p) {
+        const int64_t q = p < m ? p : 0;
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            vn[k] = idx[q * DP1 + k];
+            bn[k] = bary[q * DP1 + k];
+        }
+    };
+    if (wave < m) load_record(wave);
     for (int64_t p = wave; p < m; p += nwaves) {
         int v[DP1];
         float b[DP1];
 #pragma unroll
         for (int k = 0; k < DP1; ++k) {
-            v[k] = idx[p * DP1 + k];
-            b[k] = bary[p * DP1 + k];
+            v[k] = vn[k];
+            b[k] = bn[k];
         }
+        // the point's logit gradient, lane cls holding g[cls] (64 at a time)
+        float gl = 0.f;
+        if (CLS && lane < n_cls) gl = grad_out[p * n_cls + lane];
         float x[DP1][CH];
 #pragma unroll
         for (int k = 0; k < DP1; ++k)
@@ -112,6 +145,7 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
                 const int c = lane + 64 * i;
                 x[k][i] = (c < C && v[k] >= 0) ? value_at<IN_BF16>(values, (int64_t)v[k] * C + c) : 0.f;
             }
+        load_record(p + nwaves);
         // MaxPool with the winning vertex (first of equal maxima)
         float mx[CH];
         int am[CH];
@@ -135,8 +169,11 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
             float s = 0.f;
 #pragma unroll
             for (int i = 0; i < CH; ++i) s = fmaf(b[k] * x[k][i] - mx[i], wd[i], s);
-            db[k] = tanhf(b_delta + wave_sum_f(s));
+            db[k] = s;
         }
+        wave_sum_n<DP1>(db);  // the d+1 reductions interleaved
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) db[k] = tanhf(b_delta + db[k]);
         // gf = g W_cls (classifier) or g
         float gf[CH];
 #pragma unroll
@@ -146,12 +183,16 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
             if (!CLS && c < C) gf[i] = grad_out[p * C + c];
         }
         if (CLS) {
-            for (int cls = 0; cls < n_cls; ++cls) {
-                const float g = grad_out[p * n_cls + cls];
+            for (int c0 = 0; c0 < n_cls; c0 += 64) {
+                if (c0 > 0) gl = lane + c0 < n_cls ? grad_out[p * n_cls + c0 + lane] : 0.f;
+                const int nb = n_cls - c0 < 64 ? n_cls - c0 : 64;
+                for (int t = 0; t < nb; ++t) {
+                    const float g = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gl), t));
 #pragma unroll
-                for (int i = 0; i < CH; ++i) {
-                    const int c = lane + 64 * i;
-                    if (c < C) gf[i] = fmaf(g, w_cls[(int64_t)cls * C + c], gf[i]);
+                    for (int i = 0; i < CH; ++i) {
+                        const int c = lane + 64 * i;
+                        if (c < C) gf[i] = fmaf(g, wc[(int64_t)(c0 + t) * C + c], gf[i]);
+                    }
                 }
             }
         }
@@ -163,7 +204,12 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
             float s = 0.f;
 #pragma unroll
             for (int i = 0; i < CH; ++i) s = fmaf(gf[i], x[k][i], s);
-            darg[k] = wave_sum_f(s) * (1.f - db[k] * db[k]);
+            darg[k] = s;
+        }
+        wave_sum_n<DP1>(darg);
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            darg[k] *= 1.f - db[k] * db[k];
             S += darg[k];
         }
         // Linear backward, accumulated per lane channel
@@ -203,69 +249,118 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
     if (lane == 0) part_b[wave] = acc_b;
 }
 
-// dX_v over v's pair list: for pair (p, b) the slot k of v in p's simplex,
-// then dx_pk.  Four entries' loads are issued together.
+// Over the pair-list entries [e0, e1) of vertex v: for pair (p, b) the slot k
+// of v in p's simplex, then the two sums whose combination is dX_v:
+// acc = sum alpha_pk gf_p, accw = sum (beta_pk - [k = k*_pc] gamma_pk), with
+// dX_v = acc + w_delta accw.  Four entries' loads are issued together.
+template <int D, int CH>
+__device__ __forceinline__ void dx_sums(int64_t e0, int64_t e1, int v, int C, const int32_t *__restrict__ list,
+                                        const int32_t *__restrict__ idx, const float *__restrict__ coef,
+                                        const float *__restrict__ gf, const uint8_t *__restrict__ am, float *acc,
+                                        float *accw) {
+    constexpr int DP1 = D + 1;
+    constexpr int U = 4;
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) acc[i] = accw[i] = 0.f;
+    for (int64_t q0 = e0; q0 < e1; q0 += U) {
+        int64_t p[U];
+        int k[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            ok[u] = q0 + u < e1;
+            p[u] = ok[u] ? list[2 * (q0 + u)] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            k[u] = 0;
+#pragma unroll
+            for (int j = 0; j < DP1; ++j)
+                if (idx[p[u] * DP1 + j] == (int32_t)v) k[u] = j;
+        }
+        float al[U], be[U], ga[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float *cf = coef + (p[u] * DP1 + k[u]) * 3;
+            al[u] = ok[u] ? cf[0] : 0.f;
+            be[u] = ok[u] ? cf[1] : 0.f;
+            ga[u] = ok[u] ? cf[2] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int i = 0; i < CH; ++i) {
+                const int c = lane + 64 * i;
+                if (c < C) {
+                    const float g = gf[p[u] * C + c];
+                    const bool win = am[p[u] * C + c] == k[u];
+                    acc[i] = fmaf(al[u], g, acc[i]);
+                    accw[i] += win ? be[u] - ga[u] : be[u];
+                }
+            }
+    }
+}
+
+// The parts of long pair lists (the splat's split lists: more than kPart
+// entries, cut into parts of kPart): one wavefront per part row, writing its
+// acc and accw to part row u of `partial` [rows][2 C].
+template <int D, int CH>
+__global__ __launch_bounds__(kBlock) void k_dfb_parts(const int32_t *__restrict__ counters, int C,
+                                                      const int32_t *__restrict__ vinfo,
+                                                      const int32_t *__restrict__ list,
+                                                      const int32_t *__restrict__ split,
+                                                      const int32_t *__restrict__ rowmap,
+                                                      const int32_t *__restrict__ idx, const float *__restrict__ coef,
+                                                      const float *__restrict__ gf, const uint8_t *__restrict__ am,
+                                                      float *__restrict__ partial) {
+    const int lane = threadIdx.x & 63;
+    const int64_t nrows = counters[CNT_ROWS];
+    const XcdShare sh = xcd_share(nrows);
+    for (int64_t u = sh.lo + sh.wave; u < sh.hi; u += sh.nwaves) {
+        const int sp = rowmap[u];
+        const int v = split[3 * sp];
+        const int row0 = split[3 * sp + 1];
+        const int64_t off = vinfo[2 * v];
+        const int cnt = vinfo[2 * v + 1];
+        const int64_t e0 = off + (u - row0) * kPart;
+        const int64_t e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
+        float acc[CH], accw[CH];
+        dx_sums<D, CH>(e0, e1, v, C, list, idx, coef, gf, am, acc, accw);
+        float *o = partial + u * 2 * C;
+#pragma unroll
+        for (int i = 0; i < CH; ++i) {
+            const int c = lane + 64 * i;
+            if (c < C) {
+                o[c] = acc[i];
+                o[C + c] = accw[i];
+            }
+        }
+    }
+}
+
+// dX_v: a vertex with at most kPart entries over its list, a split vertex
+// by adding its part rows in part order; one wavefront per vertex, lane =
+// channel.
 template <int D, int CH, bool OUT_BF16>
 __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict__ counters, int C,
                                                        const int32_t *__restrict__ vinfo,
                                                        const int32_t *__restrict__ list,
+                                                       const int32_t *__restrict__ split,
                                                        const int32_t *__restrict__ idx, const float *__restrict__ coef,
                                                        const float *__restrict__ gf, const uint8_t *__restrict__ am,
+                                                       const float *__restrict__ partial,
                                                        const float *__restrict__ w_delta, void *__restrict__ out) {
-    constexpr int DP1 = D + 1;
-    constexpr int U = 4;
     const int lane = threadIdx.x & 63;
     const int64_t V = counters[CNT_V];
+    const int64_t ns = counters[CNT_SPLIT];
     float wd[CH];
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
         const int c = lane + 64 * i;
         wd[i] = c < C ? w_delta[c] : 0.f;
     }
-    const XcdShare sh = xcd_share(V);
-    for (int64_t v = sh.lo + sh.wave; v < sh.hi; v += sh.nwaves) {
-        const int64_t off = vinfo[2 * v];
-        const int cnt = vinfo[2 * v + 1];
-        float acc[CH], accw[CH];
-#pragma unroll
-        for (int i = 0; i < CH; ++i) acc[i] = accw[i] = 0.f;
-        for (int e0 = 0; e0 < cnt; e0 += U) {
-            int64_t p[U];
-            int k[U];
-            bool ok[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                ok[u] = e0 + u < cnt;
-                p[u] = ok[u] ? list[2 * (off + e0 + u)] : 0;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                k[u] = 0;
-#pragma unroll
-                for (int j = 0; j < DP1; ++j)
-                    if (idx[p[u] * DP1 + j] == (int32_t)v) k[u] = j;
-            }
-            float al[U], be[U], ga[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const float *cf = coef + (p[u] * DP1 + k[u]) * 3;
-                al[u] = ok[u] ? cf[0] : 0.f;
-                be[u] = ok[u] ? cf[1] : 0.f;
-                ga[u] = ok[u] ? cf[2] : 0.f;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int i = 0; i < CH; ++i) {
-                    const int c = lane + 64 * i;
-                    if (c < C) {
-                        const float g = gf[p[u] * C + c];
-                        const bool win = am[p[u] * C + c] == k[u];
-                        acc[i] = fmaf(al[u], g, acc[i]);
-                        accw[i] += win ? be[u] - ga[u] : be[u];
-                    }
-                }
-        }
+    auto store = [&](int64_t v, const float *acc, const float *accw) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
             const int c = lane + 64 * i;
@@ -277,6 +372,34 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
                     reinterpret_cast<float *>(out)[v * C + c] = r;
             }
         }
+    };
+    const XcdShare sh = xcd_share(V);
+    for (int64_t v = sh.lo + sh.wave; v < sh.hi; v += sh.nwaves) {
+        const int64_t off = vinfo[2 * v];
+        const int cnt = vinfo[2 * v + 1];
+        if (cnt > kPart) continue;  // a split vertex: below
+        float acc[CH], accw[CH];
+        dx_sums<D, CH>(off, off + cnt, (int)v, C, list, idx, coef, gf, am, acc, accw);
+        store(v, acc, accw);
+    }
+    const XcdShare ss = xcd_share(ns);
+    for (int64_t sp = ss.lo + ss.wave; sp < ss.hi; sp += ss.nwaves) {
+        const int v = split[3 * sp], row0 = split[3 * sp + 1], parts = split[3 * sp + 2];
+        float acc[CH], accw[CH];
+#pragma unroll
+        for (int i = 0; i < CH; ++i) acc[i] = accw[i] = 0.f;
+        for (int u = 0; u < parts; ++u) {
+            const float *o = partial + ((int64_t)row0 + u) * 2 * C;
+#pragma unroll
+            for (int i = 0; i < CH; ++i) {
+                const int c = lane + 64 * i;
+                if (c < C) {
+                    acc[i] += o[c];
+                    accw[i] += o[C + c];
+                }
+            }
+        }
+        store(v, acc, accw);
     }
 }
 
@@ -285,7 +408,7 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
 // from 16 blockIdx.y and the 64 channels from 64 blockIdx.x.  Thread t owns
 // class t / 16 and channels 4 (t mod 16) .. +3; the chunk's g and f pass
 // through LDS kClsTile points at a time (zero past m, n_cls and C).
-constexpr int kClsChunk = 1024, kClsTile = 128, kClsK = 16, kClsC = 64;
+constexpr int kClsChunk = 256, kClsTile = 128, kClsK = 16, kClsC = 64;
 __global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int C, int n_cls, const float *__restrict__ grad_out,
                                                     const float *__restrict__ f, float *__restrict__ part_c,
                                                     float *__restrict__ part_bc) {
@@ -337,8 +460,9 @@ template <int D, bool IN_BF16, bool CLS>
 hipError_t launch_points_ch(lattice *L, int ch, unsigned grid, const void *values, int C, const float *w_delta,
                             float b_delta, const float *w_cls, int n_cls, const float *grad_out, float *gf,
                             uint8_t *am, float *coef, float *f, float *pw, float *pb) {
+    const size_t lds = (CLS && (int64_t)n_cls * C <= kClsLdsFloats) ? (size_t)n_cls * C * sizeof(float) : 0;
     auto go = [&](auto kern) {
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(kBlock), 0, L->stream, L->m, C, L->idx, L->bary, values, w_delta,
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(kBlock), lds, L->stream, L->m, C, L->idx, L->bary, values, w_delta,
                            b_delta, w_cls, n_cls, grad_out, gf, am, coef, f, pw, pb);
         return hipGetLastError();
     };
@@ -353,27 +477,35 @@ hipError_t launch_points_ch(lattice *L, int ch, unsigned grid, const void *value
 
 template <int D>
 hipError_t launch_gather_ch(lattice *L, int ch, bool out_bf16, int C, const float *coef, const float *gf,
-                            const uint8_t *am, const float *w_delta, void *out) {
-    const int64_t waves = L->max_vertices;
-    int64_t grid = (waves + 3) / 4;
+                            const uint8_t *am, const float *w_delta, float *partial, void *out) {
     const int64_t cap = (int64_t)L->cu_count * 8;
-    if (grid > cap) grid = cap;
-    grid = (grid + 7) / 8 * 8;  // whole XCD groups: each XCD takes one range of vertices
-    auto go = [&](auto kern) {
-        hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kBlock), 0, L->stream, L->counters, C, L->vinfo, L->list,
-                           L->idx, coef, gf, am, w_delta, out);
+    auto grid_of = [&](int64_t waves) {
+        int64_t g = (waves + 3) / 4;
+        if (g > cap) g = cap;
+        return (g + 7) / 8 * 8;  // whole XCD groups: each XCD takes one range
+    };
+    const int64_t g_parts = grid_of(split_rows_max(L)), g_vert = grid_of(L->max_vertices);
+    auto go = [&](auto parts_kern, auto kern) {
+        hipLaunchKernelGGL(parts_kern, dim3((unsigned)g_parts), dim3(kBlock), 0, L->stream, L->counters, C, L->vinfo,
+                           L->list, L->split, L->rowmap, L->idx, coef, gf, am, partial);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, dim3((unsigned)g_vert), dim3(kBlock), 0, L->stream, L->counters, C, L->vinfo, L->list,
+                           L->split, L->idx, coef, gf, am, partial, w_delta, out);
         return hipGetLastError();
     };
-#define DFB_G(CHV)                                                                        \
-    case CHV:                                                                             \
-        return out_bf16 ? go(k_dfb_gather<D, CHV, true>) : go(k_dfb_gather<D, CHV, false>);
+#define DFB_G(CHV)                                                                                       \
+    case CHV:                                                                                            \
+        return out_bf16 ? go(k_dfb_parts<D, CHV>, k_dfb_gather<D, CHV, true>)                            \
+                        : go(k_dfb_parts<D, CHV>, k_dfb_gather<D, CHV, false>);
     switch (ch) {
         DFB_G(1)
         DFB_G(2)
         DFB_G(4)
         DFB_G(8)
         default:
-            return out_bf16 ? go(k_dfb_gather<D, 16, true>) : go(k_dfb_gather<D, 16, false>);
+            return out_bf16 ? go(k_dfb_parts<D, 16>, k_dfb_gather<D, 16, true>)
+                            : go(k_dfb_parts<D, 16>, k_dfb_gather<D, 16, false>);
     }
 #undef DFB_G
 }
@@ -384,7 +516,7 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
                  float *grad_w_delta, float *grad_b_delta, float *grad_w_cls, float *grad_b_cls, char *scratch,
                  int nwaves, int nch) {
     const int ch = C <= 64 ? 1 : C <= 128 ? 2 : C <= 256 ? 4 : C <= 512 ? 8 : 16;
-    const DfbLayout l = dfb_layout(L->m, C, D + 1, w_cls ? n_cls : 0, nwaves, nch);
+    const DfbLayout l = dfb_layout(L->m, C, D + 1, w_cls ? n_cls : 0, nwaves, nch, split_rows_max(L));
     float *gf = reinterpret_cast<float *>(scratch + l.gf);
     uint8_t *am = reinterpret_cast<uint8_t *>(scratch + l.am);
     float *coef = reinterpret_cast<float *>(scratch + l.coef);
@@ -404,7 +536,8 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
                     : launch_points_ch<D, false, false>(L, ch, grid, values, C, w_delta, b_delta, w_cls, 0, grad_out,
                                                         gf, am, coef, f, pw, pb);
     if (e != hipSuccess) return e;
-    if (grad_values && (e = launch_gather_ch<D>(L, ch, out_bf16, C, coef, gf, am, w_delta, grad_values)) != hipSuccess)
+    if (grad_values && (e = launch_gather_ch<D>(L, ch, out_bf16, C, coef, gf, am, w_delta,
+                                                reinterpret_cast<float *>(scratch + l.part), grad_values)) != hipSuccess)
         return e;
     float *tmp = reinterpret_cast<float *>(scratch + l.tmp);
     if (grad_w_delta && (e = rowsum::sum(L->stream, pw, nwaves, C, tmp, grad_w_delta)) != hipSuccess) return e;
@@ -427,7 +560,7 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
 
 // Wavefronts of the point kernel and point chunks of the classifier kernel.
 void deform_backward_shape(const lattice *L, int *nwaves, int *nch) {
-    *nwaves = L->cu_count * 4 * 4;  // four workgroups of four wavefronts per CU
+    *nwaves = L->cu_count * 8 * 4;  // eight workgroups of four wavefronts per CU (a point per wavefront at a time)
     const int64_t c = (L->m + kClsChunk - 1) / kClsChunk;  // classifier chunks
     *nch = (int)(c < 1 ? 1 : c);
 }
@@ -435,7 +568,7 @@ void deform_backward_shape(const lattice *L, int *nwaves, int *nch) {
 int64_t deform_backward_scratch_bytes(const lattice *L, int C, int n_cls) {
     int nwaves, nch;
     deform_backward_shape(L, &nwaves, &nch);
-    return dfb_layout(L->m, C, L->d + 1, n_cls, nwaves, nch).total;
+    return dfb_layout(L->m, C, L->d + 1, n_cls, nwaves, nch, split_rows_max(L)).total;
 }
 
 hipError_t launch_deform_backward(lattice *L, const void *values, lattice_dtype values_dt, int C,
