@@ -456,6 +456,194 @@ __global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int C, int n_cls,
     }
 }
 
+// The same per-point work for C a multiple of 4 up to 256 (the segmentation
+// networks' widths): a group of G = 2^LG lanes per point, lane j holding the
+// float4 chunk j of each row, 64 / G points per wavefront side by side; the
+// dot products over C are group sums (d+1 of them interleaved).  The
+// per-channel sums of dw_delta are added across the groups at the end.
+template <bool IN_BF16>
+__device__ __forceinline__ float4 row4(const void *values, int64_t at4) {
+    if (IN_BF16) {
+        const uint2 u = reinterpret_cast<const uint2 *>(values)[at4];
+        return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                           __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+    }
+    return reinterpret_cast<const float4 *>(values)[at4];
+}
+
+template <int LG, int N>
+__device__ __forceinline__ void group_sum_n(float *x) {
+#pragma unroll
+    for (int off = (1 << LG) >> 1; off > 0; off >>= 1) {
+        float y[N];
+#pragma unroll
+        for (int k = 0; k < N; ++k) y[k] = __shfl_xor(x[k], off, 64);
+#pragma unroll
+        for (int k = 0; k < N; ++k) x[k] += y[k];
+    }
+}
+
+template <int D, int LG, bool IN_BF16, bool CLS>
+__global__ __launch_bounds__(kBlock) void k_dfb_points_g(int64_t m, int C, const int32_t *__restrict__ idx,
+                                                         const float *__restrict__ bary,
+                                                         const void *__restrict__ values,
+                                                         const float *__restrict__ w_delta, float b_delta,
+                                                         const float *__restrict__ w_cls, int n_cls,
+                                                         const float *__restrict__ grad_out,
+                                                         float *__restrict__ gf_out, uint8_t *__restrict__ am_out,
+                                                         float *__restrict__ coef, float *__restrict__ f_out,
+                                                         float *__restrict__ part_w, float *__restrict__ part_b) {
+    constexpr int DP1 = D + 1;
+    constexpr int G = 1 << LG;
+    constexpr int PPW = 64 / G;
+    const int lane = threadIdx.x & 63;
+    const int grp = lane >> LG, j = lane & (G - 1);
+    const int NC = C >> 2;
+    const bool has = j < NC;
+    const int64_t wave = ((int64_t)blockIdx.x * kBlock + threadIdx.x) >> 6;
+    const int64_t nwaves = ((int64_t)gridDim.x * kBlock) >> 6;
+    extern __shared__ float wcs_lds[];
+    const bool wcs = CLS && (int64_t)n_cls * C <= kClsLdsFloats;
+    if (wcs) {
+        for (int64_t i = threadIdx.x; i < (int64_t)n_cls * C; i += kBlock) wcs_lds[i] = w_cls[i];
+        __syncthreads();
+    }
+    const float *wc = wcs ? wcs_lds : w_cls;
+    const float4 wd = has ? reinterpret_cast<const float4 *>(w_delta)[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 acc_w = make_float4(0.f, 0.f, 0.f, 0.f);
+    float acc_b = 0.f;
+    for (int64_t p0 = wave * PPW; p0 < m; p0 += nwaves * PPW) {
+        const int64_t p = p0 + grp;
+        const bool live = p < m;
+        const int64_t q = live ? p : 0;
+        int v[DP1];
+        float b[DP1];
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            v[k] = idx[q * DP1 + k];
+            b[k] = live ? bary[q * DP1 + k] : 0.f;
+        }
+        float4 x[DP1];
+#pragma unroll
+        for (int k = 0; k < DP1; ++k)
+            x[k] = (has && live && v[k] >= 0) ? row4<IN_BF16>(values, (int64_t)v[k] * NC + j)
+                                              : make_float4(0.f, 0.f, 0.f, 0.f);
+        // MaxPool with the winning vertex (first of equal maxima), per channel
+        float4 mx = make_float4(b[0] * x[0].x, b[0] * x[0].y, b[0] * x[0].z, b[0] * x[0].w);
+        int a0 = 0, a1 = 0, a2 = 0, a3 = 0;
+#pragma unroll
+        for (int k = 1; k < DP1; ++k) {
+            const float q0 = b[k] * x[k].x, q1 = b[k] * x[k].y, q2 = b[k] * x[k].z, q3 = b[k] * x[k].w;
+            if (q0 > mx.x) { mx.x = q0; a0 = k; }
+            if (q1 > mx.y) { mx.y = q1; a1 = k; }
+            if (q2 > mx.z) { mx.z = q2; a2 = k; }
+            if (q3 > mx.w) { mx.w = q3; a3 = k; }
+        }
+        // the offsets, as the forward computes them
+        float db[DP1];
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            float t = 0.f;
+            t = fmaf(b[k] * x[k].x - mx.x, wd.x, t);
+            t = fmaf(b[k] * x[k].y - mx.y, wd.y, t);
+            t = fmaf(b[k] * x[k].z - mx.z, wd.z, t);
+            t = fmaf(b[k] * x[k].w - mx.w, wd.w, t);
+            db[k] = t;
+        }
+        group_sum_n<LG, DP1>(db);
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) db[k] = tanhf(b_delta + db[k]);
+        // gf = g W_cls (classifier) or g, this lane's four channels
+        float4 gf = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (!CLS) {
+            if (has && live) gf = reinterpret_cast<const float4 *>(grad_out)[q * NC + j];
+        } else {
+            for (int c0 = 0; c0 < n_cls; c0 += G) {
+                // lane j of the group holds the point's g[c0 + j]; class c0 + t from lane t
+                const float gl = (live && c0 + j < n_cls) ? grad_out[q * n_cls + c0 + j] : 0.f;
+                const int nb = n_cls - c0 < G ? n_cls - c0 : G;
+                for (int t = 0; t < nb; ++t) {
+                    const float g = __shfl(gl, (grp << LG) + t, 64);
+                    if (has) {
+                        const float4 w = *reinterpret_cast<const float4 *>(wc + (int64_t)(c0 + t) * C + 4 * j);
+                        gf.x = fmaf(g, w.x, gf.x);
+                        gf.y = fmaf(g, w.y, gf.y);
+                        gf.z = fmaf(g, w.z, gf.z);
+                        gf.w = fmaf(g, w.w, gf.w);
+                    }
+                }
+            }
+        }
+        // Tanh backward, and S
+        float darg[DP1];
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            float t = 0.f;
+            t = fmaf(gf.x, x[k].x, t);
+            t = fmaf(gf.y, x[k].y, t);
+            t = fmaf(gf.z, x[k].z, t);
+            t = fmaf(gf.w, x[k].w, t);
+            darg[k] = t;
+        }
+        group_sum_n<LG, DP1>(darg);
+        float S = 0.f;
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            darg[k] *= 1.f - db[k] * db[k];
+            S += darg[k];
+        }
+        // Linear backward, accumulated per channel
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) {
+            acc_w.x = fmaf(darg[k], b[k] * x[k].x - mx.x, acc_w.x);
+            acc_w.y = fmaf(darg[k], b[k] * x[k].y - mx.y, acc_w.y);
+            acc_w.z = fmaf(darg[k], b[k] * x[k].z - mx.z, acc_w.z);
+            acc_w.w = fmaf(darg[k], b[k] * x[k].w - mx.w, acc_w.w);
+        }
+        if (j == 0 && live) acc_b += S;
+        // per-point records for the vertex gather and the classifier
+        if (has && live) {
+            reinterpret_cast<float4 *>(gf_out)[p * NC + j] = gf;
+            reinterpret_cast<uint32_t *>(am_out)[p * NC + j] =
+                (uint32_t)a0 | ((uint32_t)a1 << 8) | ((uint32_t)a2 << 16) | ((uint32_t)a3 << 24);
+            if (CLS) {
+                float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                for (int k = 0; k < DP1; ++k) {
+                    const float w = b[k] + db[k];
+                    f.x = fmaf(w, x[k].x, f.x);
+                    f.y = fmaf(w, x[k].y, f.y);
+                    f.z = fmaf(w, x[k].z, f.z);
+                    f.w = fmaf(w, x[k].w, f.w);
+                }
+                reinterpret_cast<float4 *>(f_out)[p * NC + j] = f;
+            }
+        }
+        // slot k's coefficients from lane k mod G of the group
+        if (live) {
+#pragma unroll
+            for (int k = 0; k < DP1; ++k)
+                if ((k & (G - 1)) == j) {
+                    coef[(p * DP1 + k) * 3 + 0] = b[k] + db[k];
+                    coef[(p * DP1 + k) * 3 + 1] = b[k] * darg[k];
+                    coef[(p * DP1 + k) * 3 + 2] = b[k] * S;
+                }
+        }
+    }
+    // the groups' per-channel sums added (lane j of every group holds chunk j)
+#pragma unroll
+    for (int off = G; off < 64; off <<= 1) {
+        acc_w.x += __shfl_xor(acc_w.x, off, 64);
+        acc_w.y += __shfl_xor(acc_w.y, off, 64);
+        acc_w.z += __shfl_xor(acc_w.z, off, 64);
+        acc_w.w += __shfl_xor(acc_w.w, off, 64);
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) acc_b += __shfl_xor(acc_b, off, 64);
+    if (grp == 0 && has) reinterpret_cast<float4 *>(part_w)[wave * NC + j] = acc_w;
+    if (lane == 0) part_b[wave] = acc_b;
+}
+
 template <int D, bool IN_BF16, bool CLS>
 hipError_t launch_points_ch(lattice *L, int ch, unsigned grid, const void *values, int C, const float *w_delta,
                             float b_delta, const float *w_cls, int n_cls, const float *grad_out, float *gf,
@@ -466,6 +654,26 @@ hipError_t launch_points_ch(lattice *L, int ch, unsigned grid, const void *value
                            b_delta, w_cls, n_cls, grad_out, gf, am, coef, f, pw, pb);
         return hipGetLastError();
     };
+    // the grouped kernel: C a multiple of 4 up to 256, rows (and, without the
+    // classifier, dL/df and w_delta) aligned for their vector loads
+    const bool grouped = C % 4 == 0 && C <= 256 &&
+                         (reinterpret_cast<uintptr_t>(values) & (IN_BF16 ? 7 : 15)) == 0 &&
+                         (reinterpret_cast<uintptr_t>(w_delta) & 15) == 0 &&
+                         (CLS ? (reinterpret_cast<uintptr_t>(w_cls) & 15) == 0
+                              : (reinterpret_cast<uintptr_t>(grad_out) & 15) == 0);
+    if (grouped) {
+        int lg = 0;
+        while ((1 << lg) < C / 4) ++lg;
+        switch (lg) {
+            case 0: return go(k_dfb_points_g<D, 0, IN_BF16, CLS>);
+            case 1: return go(k_dfb_points_g<D, 1, IN_BF16, CLS>);
+            case 2: return go(k_dfb_points_g<D, 2, IN_BF16, CLS>);
+            case 3: return go(k_dfb_points_g<D, 3, IN_BF16, CLS>);
+            case 4: return go(k_dfb_points_g<D, 4, IN_BF16, CLS>);
+            case 5: return go(k_dfb_points_g<D, 5, IN_BF16, CLS>);
+            default: return go(k_dfb_points_g<D, 6, IN_BF16, CLS>);
+        }
+    }
     switch (ch) {
         case 1: return go(k_dfb_points<D, IN_BF16, CLS, 1>);
         case 2: return go(k_dfb_points<D, IN_BF16, CLS, 2>);

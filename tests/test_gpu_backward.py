@@ -185,7 +185,7 @@ def test_conv_backward_empty_lattice():
 
 @pytest.mark.parametrize("d,C,n_cls,bf16", [
     (3, 64, 20, False), (3, 64, 0, False), (4, 64, 26, True), (2, 16, 3, False), (3, 200, 0, False),
-    (3, 1024, 5, False), (1, 5, 0, False), (3, 128, 64, True)])
+    (3, 1024, 5, False), (1, 5, 0, False), (3, 128, 64, True), (4, 16, 7, False), (3, 4, 0, False)])
 def test_deform_slice_backward_parity(d, C, n_cls, bf16):
     """Every gradient of DeformSlice (and its classifier): the vertex values
     (pulled over the pair lists), the offsets' weights and bias, the
