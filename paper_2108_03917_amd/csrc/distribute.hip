@@ -65,6 +65,9 @@ constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
 constexpr int kW1 = 16, kW2 = 32, kW3 = 64;  // block widths (the paper's figure)
 constexpr int kMaxK0 = 16;                   // d + f_d, zero-padded to 16
+// The backward's per-entry record: h_0 (padded), h_1, h_2 (the blocks'
+// inputs) and h_3 (the last block's output), fp32, 512 bytes
+constexpr int kRecH1 = kMaxK0, kRecH2 = kRecH1 + kW1, kRecH3 = kRecH2 + kW2, kRec = kRecH3 + kW3;
 // LDS row of one output channel: 64 entries + 4 (16-byte aligned rows; the
 // 16 lanes of a quarter-wave reading 16 bytes each then cover all 64 banks,
 // and the MFMA output writes of the four lane quarters fall 16 banks apart)
@@ -579,10 +582,11 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
                                                      const float *__restrict__ mu,
                                                      const int32_t *__restrict__ counters,
                                                      double *__restrict__ stats,
-                                                     unsigned int *__restrict__ keys, void *__restrict__ out) {
+                                                     unsigned int *__restrict__ keys, void *__restrict__ out,
+                                                     float *__restrict__ rec, uint64_t *__restrict__ routed) {
     // MODE 3: outputs [64 channels][64 entries], first the staged inputs;
-    // MODE 1, 2: the staged inputs only
-    constexpr int kYWave = MODE >= 3 ? kW3 * kYStride : 64 * (kMaxK0 + 1);
+    // MODE 1, 2, 4: the staged inputs only
+    constexpr int kYWave = MODE == 3 ? kW3 * kYStride : 64 * (kMaxK0 + 1);
     __shared__ __attribute__((aligned(16))) float ysh[kWaves][kYWave];
     // MODE 1, 2 on a batched lattice: the workgroup's sums (then sums of
     // squares) of the block's output per cloud
@@ -777,9 +781,18 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
             flush();
             if (uniform) sheld = bref;
         }
+        // MODE 4: the entry's record starts with h_0, and its routing mask
+        // is cleared (the backward's argmax sets the masks of the winners)
+        if (MODE == 4 && valid) {
+            float *R = rec + (chunk0 + lane) * kRec;
+#pragma unroll
+            for (int i = 0; i < kMaxK0; i += 4)
+                *reinterpret_cast<float4 *>(R + i) = make_float4(cur.x[i], cur.x[i + 1], cur.x[i + 2], cur.x[i + 3]);
+            routed[chunk0 + lane] = 0ull;
+        }
         // run flags: 1 first entry of a run, 2 last, 4 the run is the vertex's whole list
         int flags = 0, dest = -1;
-        if (MODE >= 3) {
+        if (MODE == 3) {
             const int vprev = __shfl_up(v, 1);
             const int vnext = __shfl_down(v, 1);
             if (valid) {
@@ -880,17 +893,37 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 #pragma unroll
             for (int t = 0; t < 8; ++t)
                 r2[t] = relu(fmaf(a2[t / 4][t % 4], d2[t / 4][t % 4], s2[t / 4][t % 4]));
+            // MODE 4: this lane's four channels of h_1, h_2 (and below h_3)
+            // of entry 16 nt + j16 go to its record
+            float *R = MODE == 4 ? rec + (chunk0 + 16 * nt + j16) * kRec : nullptr;
+            if (MODE == 4 && ebv >= 0) {
+                *reinterpret_cast<float4 *>(R + kRecH1 + 4 * q) =
+                    make_float4(d1[0] + bias1[0], d1[1] + bias1[1], d1[2] + bias1[2], d1[3] + bias1[3]);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt)
+                    *reinterpret_cast<float4 *>(R + kRecH2 + 16 * mt + 4 * q) =
+                        make_float4(d2[mt][0] + bias2[mt][0], d2[mt][1] + bias2[mt][1], d2[mt][2] + bias2[mt][2],
+                                    d2[mt][3] + bias2[mt][3]);
+            }
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 f32x4_t d3 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int t = 0; t < 8; ++t) d3 = mfma16(wa3[mt][t], r2[t], d3);
+                if (MODE == 4) {
+                    if (ebv >= 0)
+                        *reinterpret_cast<float4 *>(R + kRecH3 + 16 * mt + 4 * q) =
+                            make_float4(d3[0] + bb3[mt][0], d3[1] + bb3[mt][1], d3[2] + bb3[mt][2],
+                                        d3[3] + bb3[mt][3]);
+                } else {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) Y[(16 * mt + 4 * q + r) * kYStride + 16 * nt + j16] = d3[r] + bb3[mt][r];
+                    for (int r = 0; r < 4; ++r)
+                        Y[(16 * mt + 4 * q + r) * kYStride + 16 * nt + j16] = d3[r] + bb3[mt][r];
+                }
             }
         }
 
-        if (MODE >= 3) {
+        if (MODE == 3) {
             wave_sync();
             // lane c: running max of channel c over each run of the wavefront's
             // entries, four entries per LDS read; an entry's run flags and
@@ -942,8 +975,9 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 //   k_dpn_norm     per cloud and block, each input channel's group mean and
 //                  1 / sqrt(var + eps) from the fp64 sums (mean 0, 1 for the
 //                  fixed affine)
-//   k_dpn_rows     the record of e: block inputs h0 (padded), h1, h2 and the
-//                  last block's output h3, fp32
+//   k_pointnet<4>  the record of e: block inputs h0 (padded), h1, h2 and the
+//                  last block's output h3, fp32, from the forward's MFMA pass
+//                  (the values its max took)
 //   k_dpn_argmax   one wavefront per vertex, lane = channel c: the row whose
 //                  h3[c] is largest (the first in list order), which receives
 //                  g[v][c]; dW3[c][.] += g r3 and db3[c] += g of that row; per
@@ -970,7 +1004,6 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 // an input gradient has mean terms even where no output gradient reaches the
 // row, so such lanes zero theirs explicitly.
 constexpr int kNrmRow = 3 * 2 * 32;              // per cloud: (mean, rstd) per block and input channel
-constexpr int kRecH1 = kMaxK0, kRecH2 = kRecH1 + kW1, kRecH3 = kRecH2 + kW2, kRec = kRecH3 + kW3;
 constexpr int kPArg = kW3 * kW2 + kW3;                           // per wavefront: dW3, db3
 // Partial rows of the passes: S = 3 dgamma3 [32], dbeta3 [32]; S = 2 dW2
 // [32][16], db2 [32], dgamma2 [16], dbeta2 [16]; S = 1 dW1 [16][16], db1
@@ -985,6 +1018,7 @@ __host__ __device__ inline int pb_len(int S, int batched) {
     return S == 3 ? kPB3Base + nc * kW2 * 2 : (S == 2 ? kPB2Base + nc * kW1 * 2 : kPB1);
 }
 constexpr int kStg = 80;  // staged floats per entry (64-entry chunks)
+constexpr int kSparseBits = 24;  // pass 3 visits only the routed channels when no entry has more
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
@@ -1049,65 +1083,6 @@ __device__ __forceinline__ void load_params(const float *__restrict__ P, float *
     __syncthreads();
 }
 
-template <int D>
-__global__ __launch_bounds__(kBlock) void k_dpn_rows(const int32_t *__restrict__ list, const int32_t *__restrict__ lvert,
-                                                     const uint64_t *__restrict__ vkeys, int batched,
-                                                     const float *__restrict__ pos, const float *__restrict__ feat,
-                                                     int f_d, const float *__restrict__ mu,
-                                                     const float *__restrict__ P, const float *__restrict__ aff,
-                                                     const int32_t *__restrict__ counters, float *__restrict__ rec) {
-    __shared__ float Ps[kPadded];
-    load_params(P, Ps);
-    const int64_t E = counters[CNT_E];
-    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < E; e += (int64_t)gridDim.x * kBlock) {
-        const int64_t p = list[2 * e];
-        const int v = lvert[e];
-        const float *A = aff + (int64_t)cloud_of(vkeys, batched, v) * kAffRow;
-        float h0[kMaxK0], h1[kW1], h2[kW2];
-#pragma unroll
-        for (int j = 0; j < kMaxK0; ++j) {
-            float x = 0.f;
-            if (j < D) x = pos[p * D + j] - mu[(int64_t)v * D + j];
-            else if (j < D + f_d) x = feat[p * f_d + (j - D)];
-            h0[j] = x;
-        }
-        float r[kW2];
-#pragma unroll
-        for (int c = 0; c < kMaxK0; ++c) r[c] = relu(fmaf(A[kAff0 + c], h0[c], A[kAff0 + kMaxK0 + c]));
-#pragma unroll
-        for (int o = 0; o < kW1; ++o) {
-            float s = Ps[kB0 + o];
-#pragma unroll
-            for (int c = 0; c < kMaxK0; ++c) s = fmaf(Ps[kWt0 + o * kMaxK0 + c], r[c], s);
-            h1[o] = s;
-        }
-#pragma unroll
-        for (int c = 0; c < kW1; ++c) r[c] = relu(fmaf(A[kAff1 + c], h1[c], A[kAff1 + kW1 + c]));
-#pragma unroll
-        for (int o = 0; o < kW2; ++o) {
-            float s = Ps[kB1 + o];
-#pragma unroll
-            for (int c = 0; c < kW1; ++c) s = fmaf(Ps[kWt1 + o * kW1 + c], r[c], s);
-            h2[o] = s;
-        }
-#pragma unroll
-        for (int c = 0; c < kW2; ++c) r[c] = relu(fmaf(A[kAff2 + c], h2[c], A[kAff2 + kW2 + c]));
-        float *R = rec + e * kRec;
-#pragma unroll
-        for (int j = 0; j < kMaxK0; ++j) R[j] = h0[j];
-#pragma unroll
-        for (int j = 0; j < kW1; ++j) R[kRecH1 + j] = h1[j];
-#pragma unroll
-        for (int j = 0; j < kW2; ++j) R[kRecH2 + j] = h2[j];
-        for (int o = 0; o < kW3; ++o) {
-            float s = Ps[kB2 + o];
-#pragma unroll
-            for (int c = 0; c < kW2; ++c) s = fmaf(Ps[kWt2 + o * kW2 + c], r[c], s);
-            R[kRecH3 + o] = s;
-        }
-    }
-}
-
 __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict__ vinfo,
                                                        const uint64_t *__restrict__ vkeys, int batched,
                                                        const float *__restrict__ aff, const float *__restrict__ rec,
@@ -1124,30 +1099,35 @@ __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict
     for (int64_t v = wave; v < V; v += nwaves) {
         const int64_t off = vinfo[2 * v];
         const int cnt = vinfo[2 * v + 1];
+        // the first maximum in list order, eight entries' loads in flight
+        constexpr int U = 8;
         float best = 0.f;
-        int64_t be = off;
-        for (int i = 0; i < cnt; ++i) {
-            const float x = rec[(off + i) * kRec + kRecH3 + lane];
-            if (i == 0 || x > best) {
-                best = x;
-                be = off + i;
-            }
+        int be = (int)off;  // entry indices fit in 32 bits
+        for (int i0 = 0; i0 < cnt; i0 += U) {
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = i0 + u < cnt ? rec[(off + i0 + u) * kRec + kRecH3 + lane] : 0.f;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (i0 + u < cnt && (i0 + u == 0 || x[u] > best)) {
+                    best = x[u];
+                    be = (int)(off + i0 + u);
+                }
         }
-        // per entry of v, the mask of the channels it wins (lane k of a block
-        // of 64 entries stores entry k's)
-        for (int i0 = 0; i0 < cnt; i0 += 64) {
-            const int nb = cnt - i0 < 64 ? cnt - i0 : 64;
-            uint64_t mine = 0;
-            for (int k = 0; k < nb; ++k) {
-                const uint64_t mk = __ballot(be == off + i0 + k);
-                mine = lane == k ? mk : mine;
-            }
-            if (lane < nb) routed[off + i0 + lane] = mine;
+        // the mask of each winning entry (the others were zeroed with their
+        // records): one store per distinct winner, by its first lane
+        uint64_t todo = ~0ull;
+        while (todo) {
+            const int leader = __builtin_ctzll(todo);
+            const int w = __shfl(be, leader);
+            const uint64_t mk = __ballot(be == w);
+            if (lane == leader) routed[w] = mk;
+            todo &= ~mk;
         }
         const float g = grad_out[v * kW3 + lane];
         db += g;
         const float *A = aff + (int64_t)cloud_of(vkeys, batched, (int)v) * kAffRow;
-        const float *R = rec + be * kRec + kRecH2;
+        const float *R = rec + (int64_t)be * kRec + kRecH2;
 #pragma unroll
         for (int j = 0; j < kW2; ++j) dw[j] = fmaf(g, relu(fmaf(A[kAff2 + j], R[j], A[kAff2 + kW2 + j])), dw[j]);
     }
@@ -1160,7 +1140,7 @@ __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict
 // One backward pass (see above).  din: the previous pass's stored per-entry
 // gradient (S = 2: dhn3 [E][32], S = 1: dhn2 [E][16]); dout: this pass's
 // (S = 3: dhn3, S = 2: dhn2).  One wavefront per workgroup.
-template <int S>
+template <int S, bool BATCHED>
 __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lvert,
                                                  const uint64_t *__restrict__ vkeys, int batched, int use_gn, int G1,
                                                  int G2, const float *__restrict__ P, const float *__restrict__ aff,
@@ -1178,9 +1158,19 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
     extern __shared__ float tab[];  // per-cloud group sums, batched only: [kGnClouds][2 K] (launch size)
     const int lane = threadIdx.x;
     for (int i = lane; i < kPadded; i += 64) Ps[i] = P[i];
-    const bool tabbed = S != 1 && use_gn && batched;
+    const bool tabbed = S != 1 && use_gn && BATCHED;
     if (tabbed)
         for (int i = lane; i < kGnClouds * 2 * K; i += 64) tab[i] = 0.f;
+    // one cloud: its affines, normalisation and group means in LDS (the
+    // lanes read them as broadcasts instead of a global load per channel)
+    constexpr int kCst = kAffRow + kNrmRow + 2 * kW2 * 2;
+    __shared__ float cst[BATCHED ? 1 : kCst];
+    if (!BATCHED) {
+        for (int i = lane; i < kAffRow; i += 64) cst[i] = aff[i];
+        for (int i = lane; i < kNrmRow; i += 64) cst[kAffRow + i] = nrm[i];
+        if (S != 3)  // the group means exist from pass 2 on
+            for (int i = lane; i < 2 * kW2 * 2; i += 64) cst[kAffRow + kNrmRow + i] = gm[i];
+    }
     __syncthreads();
     const int64_t E = counters[CNT_E];
     const int G = S == 3 ? G2 : G1;
@@ -1195,9 +1185,10 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
         const int64_t e = e0 + lane;
         const bool live = e < E;
         const int v = live ? lvert[e] : 0;
-        const int cloud = cloud_of(vkeys, batched, v);
-        const float *A = aff + (int64_t)cloud * kAffRow;
-        const float *N = nrm + (int64_t)cloud * kNrmRow;
+        const int cloud = BATCHED ? cloud_of(vkeys, 1, v) : 0;
+        const float *A = BATCHED ? aff + (int64_t)cloud * kAffRow : cst;
+        const float *N = BATCHED ? nrm + (int64_t)cloud * kNrmRow : cst + kAffRow;
+        const float *GM = BATCHED ? gm + (int64_t)cloud * 2 * kW2 * 2 : cst + kAffRow + kNrmRow;
         const float *R = rec + (live ? e : 0) * kRec;
         if (S == 3) {
             // dr3 = W3^T dh3, dh3 = g_v on the channels routed to this entry
@@ -1224,11 +1215,32 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
             float dr[kW2];
 #pragma unroll
             for (int j = 0; j < kW2; ++j) dr[j] = 0.f;
-#pragma unroll 4
-            for (int o = 0; o < kW3; ++o) {
-                const float g = ((mk >> o) & 1ull) ? gv[o] : 0.f;
+            // Where every entry of the wavefront receives few channels (dense
+            // vertices share their 64 channels among many entries), only the
+            // set bits are visited, the row of g read back from this lane's
+            // staging row; else all 64 channels, the weights as broadcasts.
+            // The choice depends only on the data: repeated calls agree.
+            int pc = __popcll(mk);
 #pragma unroll
-                for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dr[j]);
+            for (int off = 32; off > 0; off >>= 1) pc = max(pc, __shfl_xor(pc, off));
+            if (pc <= kSparseBits) {
+#pragma unroll
+                for (int o = 0; o < kW3; ++o) st[o] = gv[o];
+                uint64_t bits = mk;
+                while (bits) {
+                    const int o = __builtin_ctzll(bits);
+                    bits &= bits - 1;
+                    const float g = st[o];
+#pragma unroll
+                    for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dr[j]);
+                }
+            } else {
+#pragma unroll 4
+                for (int o = 0; o < kW3; ++o) {
+                    const float g = ((mk >> o) & 1ull) ? gv[o] : 0.f;
+#pragma unroll
+                    for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dr[j]);
+                }
             }
 #pragma unroll
             for (int j = 0; j < kW2; ++j) {
@@ -1261,7 +1273,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
                 const float gj = Ps[kA2 + j] * dh[j];
                 if (use_gn) {
                     const float xh = (R[kRecH2 + j] - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
-                    const float *M = gm + ((int64_t)cloud * 2 + 1) * kW2 * 2 + (j / gs3) * 2;
+                    const float *M = GM + kW2 * 2 + (j / gs3) * 2;
                     dh[j] = live ? N[2 * 64 + 2 * j + 1] * (gj - M[0] - xh * M[1]) : 0.f;
                 } else {
                     dh[j] = gj;
@@ -1305,7 +1317,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
                 const float gc = Ps[kA1 + c] * dh[c];
                 if (use_gn) {
                     const float xh = (R[kRecH1 + c] - N[1 * 64 + 2 * c]) * N[1 * 64 + 2 * c + 1];
-                    const float *M = gm + ((int64_t)cloud * 2 + 0) * kW2 * 2 + (c / gs2) * 2;
+                    const float *M = GM + (c / gs2) * 2;
                     dh[c] = live ? N[1 * 64 + 2 * c + 1] * (gc - M[0] - xh * M[1]) : 0.f;
                 } else {
                     dh[c] = gc;
@@ -1542,18 +1554,18 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
         if ((e = finalize(0)) != hipSuccess) return e;
         hipLaunchKernelGGL((k_pointnet<1, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
                            L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu, L->counters,
-                           L->pn_stats, L->pn_keys, out);
+                           L->pn_stats, L->pn_keys, out, nullptr, nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = finalize(1)) != hipSuccess) return e;
         hipLaunchKernelGGL((k_pointnet<2, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
                            L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu, L->counters,
-                           L->pn_stats, L->pn_keys, out);
+                           L->pn_stats, L->pn_keys, out, nullptr, nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = finalize(2)) != hipSuccess) return e;
     }
     hipLaunchKernelGGL((out_bf16 ? k_pointnet<3, true> : k_pointnet<3, false>), dim3(g_p), dim3(kBlock), 0, L->stream,
                        L->list, L->lvert, L->vinfo, L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu,
-                       L->counters, L->pn_stats, L->pn_keys, out);
+                       L->counters, L->pn_stats, L->pn_keys, out, nullptr, nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((out_bf16 ? k_pointnet_rows<true> : k_pointnet_rows<false>), dim3(g_i), dim3(kBlock), 0,
                        L->stream, L->lvert, L->vinfo, L->counters, L->pn_keys, out);
@@ -1618,23 +1630,14 @@ hipError_t launch_distribute_backward(lattice *L, const float *pos, const float 
     hipLaunchKernelGGL(k_dpn_norm, dim3((unsigned)((kGnClouds * 96 + kWaves - 1) / kWaves)), dim3(kBlock), 0,
                        L->stream, L->pn_stats, L->counters, batched, use_gn, k0, G0, G1, G2, eps, F(l.nrm), rows);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const unsigned g_e = grid_for((int64_t)(L->d + 1) * L->m, kBlock, L->cu_count, 4);
-    switch (L->d) {
-#define DR_CASE(DD)                                                                                              \
-    case DD:                                                                                                     \
-        hipLaunchKernelGGL(k_dpn_rows<DD>, dim3(g_e), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vkeys,   \
-                           batched, pos, feat, f_d, L->mu, L->pn_params, L->pn_aff, L->counters, F(l.rec));      \
-        break;
-        DR_CASE(1)
-        DR_CASE(2)
-        DR_CASE(3)
-        DR_CASE(4)
-#undef DR_CASE
-        default:
-            return hipErrorInvalidValue;
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // the per-entry records (h_0 .. h_3) by the forward's own MFMA pass, so
+    // that the argmax sees exactly the values the forward's max took
     uint64_t *routed = reinterpret_cast<uint64_t *>(s + l.routed);
+    const unsigned g_p = grid_for((int64_t)(L->d + 1) * L->m, kBlock, L->cu_count, 2);
+    hipLaunchKernelGGL((k_pointnet<4, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
+                       L->vkeys, batched, pos, feat, L->d, f_d, L->pn_params, L->pn_aff, L->mu, L->counters,
+                       L->pn_stats, L->pn_keys, nullptr, F(l.rec), routed);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_dpn_argmax, dim3((unsigned)(l.nwaves_arg / kWaves)), dim3(kBlock), 0, L->stream, L->vinfo,
                        L->vkeys, batched, L->pn_aff, F(l.rec), grad_out, L->counters, routed, F(l.parg));
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1653,13 +1656,19 @@ hipError_t launch_distribute_backward(lattice *L, const float *pos, const float 
                            F(l.gm));
         return hipGetLastError();
     };
-    if ((e = back(k_dpn_back<3>, kW2, nullptr, F(l.d3), l.pb3)) != hipSuccess) return e;
+    if ((e = batched ? back(k_dpn_back<3, true>, kW2, nullptr, F(l.d3), l.pb3)
+                   : back(k_dpn_back<3, false>, kW2, nullptr, F(l.d3), l.pb3)) != hipSuccess)
+        return e;
     if ((e = reduce(F(l.pb3), l.nwaves, pb_len(3, batched), F(l.r3))) != hipSuccess) return e;
     if (use_gn && (e = gnmean(F(l.r3) + kPB3Base, 2, G2)) != hipSuccess) return e;
-    if ((e = back(k_dpn_back<2>, kW1, F(l.d3), F(l.d2), l.pb2)) != hipSuccess) return e;
+    if ((e = batched ? back(k_dpn_back<2, true>, kW1, F(l.d3), F(l.d2), l.pb2)
+                   : back(k_dpn_back<2, false>, kW1, F(l.d3), F(l.d2), l.pb2)) != hipSuccess)
+        return e;
     if ((e = reduce(F(l.pb2), l.nwaves, pb_len(2, batched), F(l.r2))) != hipSuccess) return e;
     if (use_gn && (e = gnmean(F(l.r2) + kPB2Base, 1, G1)) != hipSuccess) return e;
-    if ((e = back(k_dpn_back<1>, 0, F(l.d2), nullptr, l.pb1)) != hipSuccess) return e;
+    if ((e = batched ? back(k_dpn_back<1, true>, 0, F(l.d2), nullptr, l.pb1)
+                   : back(k_dpn_back<1, false>, 0, F(l.d2), nullptr, l.pb1)) != hipSuccess)
+        return e;
     if ((e = reduce(F(l.pb1), l.nwaves, kPB1, F(l.r1))) != hipSuccess) return e;
     if ((e = reduce(F(l.parg), l.nwaves_arg, kPArg, F(l.rarg))) != hipSuccess) return e;
     hipLaunchKernelGGL(k_dpn_out, dim3(16), dim3(kBlock), 0, L->stream, F(l.r1), F(l.r2), F(l.r3), F(l.rarg), k0,
