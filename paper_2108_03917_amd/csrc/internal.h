@@ -76,6 +76,7 @@ struct lattice {
     // split_rows_max() parts and split vertices per splat.
     int32_t *split = nullptr;   // [rows_max][3] (vertex, first part row, parts) per split vertex
     int32_t *rowmap = nullptr;  // [rows_max] split index of each part row
+    int32_t *partrec = nullptr; // [rows_max][2] (list offset of its first pair, pairs) of each part row
     float *pweight = nullptr;   // [rows_max] partial weight sums
     float *partial = nullptr;   // [rows_max][partial_cols] partial feature sums, grown on demand
     int64_t partial_cols = 0;

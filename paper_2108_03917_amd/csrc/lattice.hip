@@ -82,6 +82,7 @@ void free_all(lattice *L) {
     (void)hipFree(L->blk);
     (void)hipFree(L->split);
     (void)hipFree(L->rowmap);
+    (void)hipFree(L->partrec);
     (void)hipFree(L->pweight);
     (void)hipFree(L->partial);
     (void)hipFree(L->wflip);
@@ -280,6 +281,7 @@ lattice_status lattice_create(int d, const float *sigma, double alpha, int64_t m
               hipMalloc(&L->blk, scan_blocks_max() * 4 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->split, split_rows_max(L) * 3 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->rowmap, split_rows_max(L) * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&L->partrec, split_rows_max(L) * 2 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->pweight, split_rows_max(L) * sizeof(float)) == hipSuccess &&
               hipMalloc(&L->vinfo, L->max_vertices * 2 * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&L->idx, max_points * dp1 * sizeof(int32_t)) == hipSuccess &&

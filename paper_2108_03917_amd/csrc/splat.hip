@@ -526,7 +526,8 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
                                                         int nb, HEntry *__restrict__ tab,
                                                         const int4 *__restrict__ blk, uint64_t *__restrict__ vkeys,
                                                         int32_t *__restrict__ vinfo, int32_t *__restrict__ split,
-                                                        int32_t *__restrict__ rowmap, int32_t *__restrict__ vslot,
+                                                        int32_t *__restrict__ rowmap, int2 *__restrict__ partrec,
+                                                        int32_t *__restrict__ vslot,
                                                         uint32_t *occ, int32_t *counters) {
     __shared__ int4 red[kBlock / 64];
     __shared__ int4 wsum[kBlock / 64];
@@ -593,7 +594,11 @@ __global__ __launch_bounds__(kBlock) void k_scan_assign(const int32_t *__restric
                     split[3 * sp] = v;
                     split[3 * sp + 1] = row0;
                     split[3 * sp + 2] = q[i].w;
-                    for (int j = 0; j < q[i].w; ++j) rowmap[row0 + j] = sp;
+                    for (int j = 0; j < q[i].w; ++j) {
+                        rowmap[row0 + j] = sp;
+                        const int left = q[i].y - j * kPart;
+                        partrec[row0 + j] = make_int2(at.y + j * kPart, left < kPart ? left : kPart);
+                    }
                 }
             }
             at = add4(at, q[i]);
@@ -751,6 +756,66 @@ __device__ __forceinline__ void sum_pairs_ahead(const int2 *__restrict__ L2, int
     }
 }
 
+// Short lists (at most kPart pairs) for float4 columns, one column per lane
+// of a group of G = 2^LG lanes (G >= CV; a lane past the last column reads
+// column CV - 1 and stores nothing).  The group's lanes load a list's entries
+// together, entry t by lane t mod G into its register t / G: one round trip
+// for the whole list, issued a list ahead of its rows.  The rows are then
+// loaded kRowBlk at a time, each entry handed to the group by a lane shuffle,
+// and added in list order (the order sum_pairs adds them in).
+constexpr int kRowBlk = 8;
+
+template <int LG>
+struct ListRegs {
+    static constexpr int NE = (kPart + (1 << LG) - 1) >> LG;
+    int x[NE], y[NE];
+};
+
+// The entries [e0, e0 + n) of a list; n outside [1, kPart] (no list to add)
+// loads entry 0, which exists whenever a list is read.
+template <int LG>
+__device__ __forceinline__ void load_list(const int2 *__restrict__ L2, int e0, int n, int j, ListRegs<LG> &q) {
+    const bool ok = n >= 1 && n <= kPart;
+#pragma unroll
+    for (int r = 0; r < ListRegs<LG>::NE; ++r) {
+        const int t = (r << LG) + j;
+        const int2 e = L2[ok ? e0 + (t < n ? t : n - 1) : 0];  // past n: entry n - 1 again, not added
+        q.x[r] = e.x;
+        q.y[r] = e.y;
+    }
+}
+
+template <int LG>
+__device__ __forceinline__ void sum_rows(const ListRegs<LG> &q, int n, const float4 *__restrict__ f4, int CV, int cc,
+                                         int gbase, float4 &acc, float &w) {
+    constexpr int G = 1 << LG;
+#pragma unroll
+    for (int t0 = 0; t0 < kPart; t0 += kRowBlk) {
+        if (t0 >= n) break;
+        float4 y[kRowBlk];
+        float b[kRowBlk];
+#pragma unroll
+        for (int i = 0; i < kRowBlk; ++i) {
+            const int t = t0 + i;
+            const int src = gbase + (t & (G - 1));
+            const int pt = __shfl(q.x[t >> LG], src, 64);
+            b[i] = __int_as_float(__shfl(q.y[t >> LG], src, 64));
+            y[i] = f4[(int64_t)pt * CV + cc];
+        }
+#pragma unroll
+        for (int i = 0; i < kRowBlk; ++i) {
+            const bool ok = t0 + i < n;
+            const float bb = ok ? b[i] : 0.f;
+            const float4 t = fma4(bb, y[i], acc);
+            acc.x = ok ? t.x : acc.x;
+            acc.y = ok ? t.y : acc.y;
+            acc.z = ok ? t.z : acc.z;
+            acc.w = ok ? t.w : acc.w;
+            w += bb;
+        }
+    }
+}
+
 template <bool VEC>
 __device__ __forceinline__ float4 scale4(float4 a, float w, int normalize) {
     if (!normalize) return a;
@@ -776,11 +841,12 @@ __device__ __forceinline__ float4 scale4(float4 a, float w, int normalize) {
 //                   then the split vertices: their parts added in part order.
 // (Combining in the last part to finish would need a device-scope release
 // per part, which costs more than a launch: every XCD has its own L2.)
-template <bool VEC>
+template <bool VEC, int LG>
 __global__ __launch_bounds__(kBlock) void k_gather_parts(const int32_t *__restrict__ vinfo,
                                                          const int32_t *__restrict__ list,
                                                          const int32_t *__restrict__ split,
                                                          const int32_t *__restrict__ rowmap,
+                                                         const int2 *__restrict__ partrec,
                                                          float *__restrict__ partial, float *__restrict__ pweight,
                                                          const float *__restrict__ feat, int C, int log2G,
                                                          const int32_t *counters) {
@@ -795,6 +861,34 @@ __global__ __launch_bounds__(kBlock) void k_gather_parts(const int32_t *__restri
     // each XCD takes one contiguous range of parts (vertices in creation
     // order): the point rows they share meet in its L2
     const XcdShare sh = xcd_share(nrows);
+    if constexpr (LG > 0) {
+        // the part's record and list a step ahead of its rows
+        const int gbase = lane & ~(G - 1);
+        const int cc = j < CV ? j : CV - 1;
+        const int64_t ustep = sh.nwaves * gpw;
+        auto rec = [&](int64_t u) { return u < sh.hi ? partrec[u] : make_int2(0, 0); };
+        int64_t u = sh.lo + sh.wave * gpw + grp;
+        int2 r = rec(u);
+        ListRegs<LG> q;
+        load_list<LG>(L2, r.x, r.y, j, q);
+        int2 rn = rec(u + ustep);
+        for (; u - grp < sh.hi; u += ustep) {
+            ListRegs<LG> qn;
+            load_list<LG>(L2, rn.x, rn.y, j, qn);
+            const int2 rnn = rec(u + 2 * ustep);
+            if (u < sh.hi) {
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                float w = 0.f;
+                sum_rows<LG>(q, r.y, reinterpret_cast<const float4 *>(feat), CV, cc, gbase, acc, w);
+                if (j < CV) reinterpret_cast<float4 *>(partial)[u * CV + j] = acc;
+                if (j == 0) pweight[u] = w;
+            }
+            q = qn;
+            r = rn;
+            rn = rnn;
+        }
+        return;
+    }
     for (int64_t u0 = sh.lo + sh.wave * gpw; u0 < sh.hi; u0 += sh.nwaves * gpw) {
         const int64_t u = u0 + grp;
         if (u >= sh.hi) continue;
@@ -826,7 +920,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_parts(const int32_t *__restri
     }
 }
 
-template <bool VEC, bool OUT_BF16>
+template <bool VEC, bool OUT_BF16, int LG>
 __global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ vinfo, const int32_t *__restrict__ list,
                                                    const int32_t *__restrict__ split, const float *__restrict__ partial,
                                                    const float *__restrict__ pweight, const float *__restrict__ feat,
@@ -874,7 +968,32 @@ __global__ __launch_bounds__(kBlock) void k_gather(const int32_t *__restrict__ v
             weight[v] = w;
         }
     };
-    {
+    if constexpr (LG > 0) {
+        // the next vertex's list loaded while this one's rows are
+        const int gbase = lane & ~(G - 1);
+        const int cc = j < CV ? j : CV - 1;
+        int64_t v = sh.lo + sh.wave * gpw + grp;
+        int2 h = header(v);
+        ListRegs<LG> q;
+        load_list<LG>(L2, h.x, h.y, j, q);
+        int2 hn = header(v + vstep);
+        for (; v - grp < sh.hi; v += vstep) {
+            ListRegs<LG> qn;
+            load_list<LG>(L2, hn.x, hn.y, j, qn);
+            const int2 hnn = header(v + 2 * vstep);
+            if (v < sh.hi && h.y <= kPart) {
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                float w = 0.f;
+                sum_rows<LG>(q, h.y, reinterpret_cast<const float4 *>(feat), CV, cc, gbase, acc, w);
+                acc = scale4<true>(acc, w, normalize);
+                if (j < CV) store4<OUT_BF16>(values, v * CV + j, acc);
+                if (weight && j == 0) weight[v] = w;
+            }
+            q = qn;
+            h = hn;
+            hn = hnn;
+        }
+    } else {
         int64_t v = sh.lo + sh.wave * gpw + grp;
         int2 ha = header(v);
         for (; v - grp < sh.hi; v += 2 * vstep) {
@@ -1026,7 +1145,8 @@ hipError_t launch_number(lattice *L, int64_t m) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan_assign, dim3((unsigned)nb), dim3(kBlock), 0, L->stream, L->idx, n, span, (int)nb,
-                       L->tab, blk, L->vkeys, L->vinfo, L->split, L->rowmap, L->vslot, L->occ, L->counters);
+                       L->tab, blk, L->vkeys, L->vinfo, L->split, L->rowmap, reinterpret_cast<int2 *>(L->partrec),
+                       L->vslot, L->occ, L->counters);
     return hipGetLastError();
 }
 
@@ -1057,23 +1177,33 @@ static hipError_t gather_typed(lattice *L, const float *feat, int C, int normali
     const int64_t gpw = 64 >> log2G;
     // the parts of long lists first: the second kernel adds them
     const unsigned g1 = grid_for((split_rows_max(L) + gpw - 1) / gpw * 64, kBlock, L->cu_count, 16);
-    if (vec)
-        hipLaunchKernelGGL((k_gather_parts<true>), dim3(g1), dim3(kBlock), 0, L->stream, L->vinfo, L->list, L->split,
-                           L->rowmap, L->partial, L->pweight, feat, C, log2G, L->counters);
-    else
-        hipLaunchKernelGGL((k_gather_parts<false>), dim3(g1), dim3(kBlock), 0, L->stream, L->vinfo, L->list, L->split,
-                           L->rowmap, L->partial, L->pweight, feat, C, log2G, L->counters);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
     const int64_t waves = (L->max_vertices + gpw - 1) / gpw;
     const unsigned grid = grid_for(waves * 64, kBlock, L->cu_count, 16);
-    if (vec)
-        hipLaunchKernelGGL((k_gather<true, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
+    // float4 columns, one per lane of a group of 4 to 64 lanes: the lists
+    // are loaded by the group together
+    auto launch = [&](auto vc, auto lc) -> hipError_t {
+        constexpr bool VEC = decltype(vc)::value;
+        constexpr int LG = decltype(lc)::value;
+        hipLaunchKernelGGL((k_gather_parts<VEC, LG>), dim3(g1), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
+                           L->split, L->rowmap, reinterpret_cast<const int2 *>(L->partrec), L->partial, L->pweight,
+                           feat, C, log2G, L->counters);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_gather<VEC, OUT_BF16, LG>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
                            L->split, L->partial, L->pweight, feat, C, log2G, normalize, values, weight, L->counters);
-    else
-        hipLaunchKernelGGL((k_gather<false, OUT_BF16>), dim3(grid), dim3(kBlock), 0, L->stream, L->vinfo, L->list,
-                           L->split, L->partial, L->pweight, feat, C, log2G, normalize, values, weight, L->counters);
-    return hipGetLastError();
+        return hipGetLastError();
+    };
+    using T = std::true_type;
+    using F = std::false_type;
+    if (!vec) return launch(F{}, std::integral_constant<int, 0>{});
+    switch (lanes <= 64 ? log2G : 0) {
+        case 2: return launch(T{}, std::integral_constant<int, 2>{});
+        case 3: return launch(T{}, std::integral_constant<int, 3>{});
+        case 4: return launch(T{}, std::integral_constant<int, 4>{});
+        case 5: return launch(T{}, std::integral_constant<int, 5>{});
+        case 6: return launch(T{}, std::integral_constant<int, 6>{});
+        default: return launch(T{}, std::integral_constant<int, 0>{});
+    }
 }
 
 hipError_t launch_gather(lattice *L, const float *feat, int C, int normalize, void *values, lattice_dtype values_dt,
