@@ -249,84 +249,92 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
     if (lane == 0) part_b[wave] = acc_b;
 }
 
-// Over the pair-list entries [e0, e1) of vertex v: for pair (p, b) the slot k
-// of v in p's simplex, then the two sums whose combination is dX_v:
-// acc = sum alpha_pk gf_p, accw = sum (beta_pk - [k = k*_pc] gamma_pk), with
-// dX_v = acc + w_delta accw.  Four entries' loads are issued together.
+// Over the pair-list entries of a vertex (n of them, 1 <= n <= kPart), each
+// giving a point p and the vertex's slot k in p's simplex, the two sums whose
+// combination is dX_v: acc = sum alpha_pk gf_p and accw = sum (beta_pk -
+// [k = k*_pc] gamma_pk), with dX_v = acc + w_delta accw.  Lane t holds entry
+// t (`x`, loaded a list ahead by dx_entry) and loads its three coefficients;
+// then the rows of gf and am are loaded several entries at a time, each
+// entry's values read from its lane, and added in list order.
+__device__ __forceinline__ int dx_entry(const int32_t *__restrict__ list, int64_t e0, int n, int lane) {
+    const bool ok = n >= 1 && n <= kPart;  // otherwise entry 0, which exists whenever a list is read
+    return list[2 * (ok ? e0 + (lane < n ? lane : n - 1) : 0)];
+}
+
 template <int D, int CH>
-__device__ __forceinline__ void dx_sums(int64_t e0, int64_t e1, int v, int C, const int32_t *__restrict__ list,
-                                        const int32_t *__restrict__ idx, const float *__restrict__ coef,
+__device__ __forceinline__ void dx_sums(int x, int n, int C, const float *__restrict__ coef,
                                         const float *__restrict__ gf, const uint8_t *__restrict__ am, float *acc,
                                         float *accw) {
     constexpr int DP1 = D + 1;
-    constexpr int U = 4;
+    constexpr int NB = CH >= 8 ? 1 : 8 / CH;  // entries whose rows are in flight together
     const int lane = threadIdx.x & 63;
+    const int pl = list_point(x), kl = list_slot(x);
+    const float *cf = coef + ((int64_t)pl * DP1 + kl) * 3;
+    const float all = cf[0], bel = cf[1], gal = cf[2];
 #pragma unroll
     for (int i = 0; i < CH; ++i) acc[i] = accw[i] = 0.f;
-    for (int64_t q0 = e0; q0 < e1; q0 += U) {
-        int64_t p[U];
-        int k[U];
-        bool ok[U];
+    for (int t0 = 0; t0 < n; t0 += NB) {
+        int ps[NB], ks[NB];
+        float al[NB], be[NB], ga[NB];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            ok[u] = q0 + u < e1;
-            p[u] = ok[u] ? list[2 * (q0 + u)] : 0;
+        for (int u = 0; u < NB; ++u) {
+            const int t = t0 + u;  // below 2 kPart; lanes past n hold entry n - 1
+            ps[u] = __builtin_amdgcn_readlane(pl, t);
+            ks[u] = __builtin_amdgcn_readlane(kl, t);
+            al[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(all), t));
+            be[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bel), t));
+            ga[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gal), t));
         }
+        // rows past n are not loaded (a wave-uniform branch)
+        float g[NB][CH];
+        int a[NB][CH];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            k[u] = 0;
-#pragma unroll
-            for (int j = 0; j < DP1; ++j)
-                if (idx[p[u] * DP1 + j] == (int32_t)v) k[u] = j;
-        }
-        float al[U], be[U], ga[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const float *cf = coef + (p[u] * DP1 + k[u]) * 3;
-            al[u] = ok[u] ? cf[0] : 0.f;
-            be[u] = ok[u] ? cf[1] : 0.f;
-            ga[u] = ok[u] ? cf[2] : 0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
+        for (int u = 0; u < NB; ++u)
 #pragma unroll
             for (int i = 0; i < CH; ++i) {
                 const int c = lane + 64 * i;
-                if (c < C) {
-                    const float g = gf[p[u] * C + c];
-                    const bool win = am[p[u] * C + c] == k[u];
-                    acc[i] = fmaf(al[u], g, acc[i]);
-                    accw[i] += win ? be[u] - ga[u] : be[u];
+                g[u][i] = 0.f;
+                a[u][i] = 0;
+                if (t0 + u < n && c < C) {
+                    g[u][i] = gf[(int64_t)ps[u] * C + c];
+                    a[u][i] = am[(int64_t)ps[u] * C + c];
                 }
             }
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            if (t0 + u >= n) break;
+#pragma unroll
+            for (int i = 0; i < CH; ++i) {
+                acc[i] = fmaf(al[u], g[u][i], acc[i]);
+                accw[i] += a[u][i] == ks[u] ? be[u] - ga[u] : be[u];
+            }
+        }
     }
 }
 
 // The parts of long pair lists (the splat's split lists: more than kPart
 // entries, cut into parts of kPart): one wavefront per part row, writing its
-// acc and accw to part row u of `partial` [rows][2 C].
+// acc and accw to part row u of `partial` [rows][2 C]; the next part's
+// entries are loaded while this one is summed.
 template <int D, int CH>
 __global__ __launch_bounds__(kBlock) void k_dfb_parts(const int32_t *__restrict__ counters, int C,
-                                                      const int32_t *__restrict__ vinfo,
                                                       const int32_t *__restrict__ list,
-                                                      const int32_t *__restrict__ split,
-                                                      const int32_t *__restrict__ rowmap,
-                                                      const int32_t *__restrict__ idx, const float *__restrict__ coef,
+                                                      const int2 *__restrict__ partrec, const float *__restrict__ coef,
                                                       const float *__restrict__ gf, const uint8_t *__restrict__ am,
                                                       float *__restrict__ partial) {
     const int lane = threadIdx.x & 63;
     const int64_t nrows = counters[CNT_ROWS];
     const XcdShare sh = xcd_share(nrows);
-    for (int64_t u = sh.lo + sh.wave; u < sh.hi; u += sh.nwaves) {
-        const int sp = rowmap[u];
-        const int v = split[3 * sp];
-        const int row0 = split[3 * sp + 1];
-        const int64_t off = vinfo[2 * v];
-        const int cnt = vinfo[2 * v + 1];
-        const int64_t e0 = off + (u - row0) * kPart;
-        const int64_t e1 = e0 + kPart < off + cnt ? e0 + kPart : off + cnt;
+    auto rec = [&](int64_t u) { return u < sh.hi ? partrec[u] : make_int2(0, 0); };
+    int64_t u = sh.lo + sh.wave;
+    int2 r = rec(u);
+    int x = dx_entry(list, r.x, r.y, lane);
+    int2 rn = rec(u + sh.nwaves);
+    for (; u < sh.hi; u += sh.nwaves) {
+        const int xn = dx_entry(list, rn.x, rn.y, lane);
+        const int2 rnn = rec(u + 2 * sh.nwaves);
         float acc[CH], accw[CH];
-        dx_sums<D, CH>(e0, e1, v, C, list, idx, coef, gf, am, acc, accw);
+        dx_sums<D, CH>(x, r.y, C, coef, gf, am, acc, accw);
         float *o = partial + u * 2 * C;
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
@@ -336,6 +344,9 @@ __global__ __launch_bounds__(kBlock) void k_dfb_parts(const int32_t *__restrict_
                 o[C + c] = accw[i];
             }
         }
+        x = xn;
+        r = rn;
+        rn = rnn;
     }
 }
 
@@ -347,7 +358,7 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
                                                        const int32_t *__restrict__ vinfo,
                                                        const int32_t *__restrict__ list,
                                                        const int32_t *__restrict__ split,
-                                                       const int32_t *__restrict__ idx, const float *__restrict__ coef,
+                                                       const float *__restrict__ coef,
                                                        const float *__restrict__ gf, const uint8_t *__restrict__ am,
                                                        const float *__restrict__ partial,
                                                        const float *__restrict__ w_delta, void *__restrict__ out) {
@@ -373,14 +384,25 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
             }
         }
     };
+    // short lists, the next vertex's entries loaded while this one is summed
     const XcdShare sh = xcd_share(V);
-    for (int64_t v = sh.lo + sh.wave; v < sh.hi; v += sh.nwaves) {
-        const int64_t off = vinfo[2 * v];
-        const int cnt = vinfo[2 * v + 1];
-        if (cnt > kPart) continue;  // a split vertex: below
-        float acc[CH], accw[CH];
-        dx_sums<D, CH>(off, off + cnt, (int)v, C, list, idx, coef, gf, am, acc, accw);
-        store(v, acc, accw);
+    const int2 *VI = reinterpret_cast<const int2 *>(vinfo);
+    auto header = [&](int64_t v) { return v < sh.hi ? VI[v] : make_int2(0, 0); };
+    int64_t v = sh.lo + sh.wave;
+    int2 h = header(v);
+    int x = dx_entry(list, h.x, h.y, lane);
+    int2 hn = header(v + sh.nwaves);
+    for (; v < sh.hi; v += sh.nwaves) {
+        const int xn = dx_entry(list, hn.x, hn.y, lane);
+        const int2 hnn = header(v + 2 * sh.nwaves);
+        if (h.y <= kPart) {  // a split vertex: below
+            float acc[CH], accw[CH];
+            dx_sums<D, CH>(x, h.y, C, coef, gf, am, acc, accw);
+            store(v, acc, accw);
+        }
+        x = xn;
+        h = hn;
+        hn = hnn;
     }
     const XcdShare ss = xcd_share(ns);
     for (int64_t sp = ss.lo + ss.wave; sp < ss.hi; sp += ss.nwaves) {
@@ -694,12 +716,12 @@ hipError_t launch_gather_ch(lattice *L, int ch, bool out_bf16, int C, const floa
     };
     const int64_t g_parts = grid_of(split_rows_max(L)), g_vert = grid_of(L->max_vertices);
     auto go = [&](auto parts_kern, auto kern) {
-        hipLaunchKernelGGL(parts_kern, dim3((unsigned)g_parts), dim3(kBlock), 0, L->stream, L->counters, C, L->vinfo,
-                           L->list, L->split, L->rowmap, L->idx, coef, gf, am, partial);
+        hipLaunchKernelGGL(parts_kern, dim3((unsigned)g_parts), dim3(kBlock), 0, L->stream, L->counters, C, L->list,
+                           reinterpret_cast<const int2 *>(L->partrec), coef, gf, am, partial);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(kern, dim3((unsigned)g_vert), dim3(kBlock), 0, L->stream, L->counters, C, L->vinfo, L->list,
-                           L->split, L->idx, coef, gf, am, partial, w_delta, out);
+                           L->split, coef, gf, am, partial, w_delta, out);
         return hipGetLastError();
     };
 #define DFB_G(CHV)                                                                                       \

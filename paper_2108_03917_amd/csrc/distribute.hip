@@ -178,7 +178,7 @@ __global__ __launch_bounds__(kBlock) void k_local_mean(const int32_t *__restrict
         const int64_t e = chunk0 + lane;
         const bool valid = e < E;
         const int v = valid ? lvert[e] : -1;
-        const int p = valid ? list[2 * e] : 0;
+        const int p = valid ? list_point(list[2 * e]) : 0;
         double acc[D];
 #pragma unroll
         for (int i = 0; i < D; ++i) acc[i] = valid ? (double)pos[(int64_t)p * D + i] : 0.0;
@@ -480,7 +480,7 @@ __global__ __launch_bounds__(kBlock) void k_gn_stats0(const int32_t *__restrict_
         const int64_t e = c * 64 + lane;
         const bool valid = e < E;
         const int v = valid ? lvert[e] : 0;
-        const int p = valid ? list[2 * e] : 0;
+        const int p = valid ? list_point(list[2 * e]) : 0;
         const int b = valid ? cloud_of(vkeys, batched, v) : -1;
         float x[kMaxK0];
 #pragma unroll
@@ -729,7 +729,7 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         const int64_t e = chk * 64 + lane;
         const bool valid = e < E;
         R.v = valid ? lvert[e] : -1;
-        R.p = valid ? list[2 * e] : 0;
+        R.p = valid ? list_point(list[2 * e]) : 0;
     };
     auto level2 = [&](Rows &R) {
         const bool valid = R.v >= 0;
@@ -761,7 +761,7 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
             tmp.p = nxt.p;
             const int64_t e2 = (ch + 2 * step) * 64 + lane;
             v2 = e2 < E ? lvert[e2] : -1;
-            p2 = e2 < E ? list[2 * e2] : 0;
+            p2 = e2 < E ? list_point(list[2 * e2]) : 0;
             level2(tmp);
             nxt = tmp;
         }

@@ -29,6 +29,18 @@ enum : int {
 // splat's numbering records the split vertices and their part rows.
 constexpr int kPart = 32;
 
+// A pair-list entry is (point and slot, weight): the point index p in bits
+// 0..27 (lattice_create bounds max_points by 2^28) and in bits 28..30 the
+// slot k (the remainder) of the vertex in p's simplex, so that a consumer
+// finds the pair's per-point record (p (d+1) + k) without a search.
+constexpr int kListPointBits = 28;
+constexpr int32_t kListPointMask = (1 << kListPointBits) - 1;
+__host__ __device__ __forceinline__ int32_t list_entry(int64_t p, int k) {
+    return (int32_t)p | (k << kListPointBits);
+}
+__host__ __device__ __forceinline__ int32_t list_point(int32_t x) { return x & kListPointMask; }
+__host__ __device__ __forceinline__ int list_slot(int32_t x) { return x >> kListPointBits; }
+
 // Packed 64-bit vertex key: 16 bits per coordinate c_0..c_{d-1}, each stored
 // as c + KEY_BIAS (so a field is never 0 for |c| <= KEY_MAX), and for d <= 3
 // the batch id in bits 48..63.  c_d is implied by the zero sum.  0 marks an

@@ -644,7 +644,9 @@ __global__ __launch_bounds__(kBlock) void k_fill(int64_t n, int32_t *__restrict_
             if (s[u] >= 0) {
                 idx[e] = ov[u].y;
                 const int64_t at = (int64_t)ov[u].x + r[u];
-                *reinterpret_cast<int2 *>(list + 2 * at) = make_int2((int32_t)(e / DP1), __float_as_int(b[u]));
+                const int64_t pt = e / DP1;
+                *reinterpret_cast<int2 *>(list + 2 * at) =
+                    make_int2(list_entry(pt, (int)(e - pt * DP1)), __float_as_int(b[u]));
             }
         }
     }
@@ -689,7 +691,7 @@ __device__ __forceinline__ void add_block(const int2 (&q)[BLK], int n, const flo
         const float4 *f4 = reinterpret_cast<const float4 *>(feat);
         float4 y[BLK];
 #pragma unroll
-        for (int i = 0; i < BLK; ++i) y[i] = f4[(int64_t)q[i].x * CV + c];
+        for (int i = 0; i < BLK; ++i) y[i] = f4[(int64_t)list_point(q[i].x) * CV + c];
 #pragma unroll
         for (int i = 0; i < BLK; ++i) {
             const bool ok = i < n;
@@ -704,7 +706,7 @@ __device__ __forceinline__ void add_block(const int2 (&q)[BLK], int n, const flo
     } else {
         float y[BLK];
 #pragma unroll
-        for (int i = 0; i < BLK; ++i) y[i] = CV > 0 ? feat[(int64_t)q[i].x * CV + c] : 0.f;
+        for (int i = 0; i < BLK; ++i) y[i] = CV > 0 ? feat[(int64_t)list_point(q[i].x) * CV + c] : 0.f;
 #pragma unroll
         for (int i = 0; i < BLK; ++i) {
             const bool ok = i < n;
@@ -761,8 +763,9 @@ __device__ __forceinline__ void sum_pairs_ahead(const int2 *__restrict__ L2, int
 // column CV - 1 and stores nothing).  The group's lanes load a list's entries
 // together, entry t by lane t mod G into its register t / G: one round trip
 // for the whole list, issued a list ahead of its rows.  The rows are then
-// loaded kRowBlk at a time, each entry handed to the group by a lane shuffle,
-// and added in list order (the order sum_pairs adds them in).
+// loaded kRowBlk at a time (none past the list's end), each entry handed to
+// the group by a lane shuffle, and added in list order (the order sum_pairs
+// adds them in).
 constexpr int kRowBlk = 8;
 
 template <int LG>
@@ -798,9 +801,10 @@ __device__ __forceinline__ void sum_rows(const ListRegs<LG> &q, int n, const flo
         for (int i = 0; i < kRowBlk; ++i) {
             const int t = t0 + i;
             const int src = gbase + (t & (G - 1));
-            const int pt = __shfl(q.x[t >> LG], src, 64);
+            const int pt = list_point(__shfl(q.x[t >> LG], src, 64));
             b[i] = __int_as_float(__shfl(q.y[t >> LG], src, 64));
-            y[i] = f4[(int64_t)pt * CV + cc];
+            y[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (t < n) y[i] = f4[(int64_t)pt * CV + cc];  // rows past n are not loaded
         }
 #pragma unroll
         for (int i = 0; i < kRowBlk; ++i) {
