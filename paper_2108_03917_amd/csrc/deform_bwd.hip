@@ -23,9 +23,9 @@
 //                  per wavefront (written as partials at the end).
 //   k_dfb_gather   one wavefront per vertex over its pair list (the splat's
 //                  lists: no atomics), lane = channel.
-//   k_dfb_cls      dW_cls and db_cls partials per chunk of 256 points, a
-//                  tile of 16 classes x 64 channels per workgroup, the
-//                  chunk's g and f staged through LDS 128 points at a time.
+//   k_dfb_cls      dW_cls and db_cls partials per chunk of 256 points, on
+//                  fp32 MFMA: a wavefront per chunk and tile of 32 classes x
+//                  64 channels, the chunk's g and f rows as the operands.
 //   rowsum         every partial added in a fixed order: the results do not
 //                  depend on scheduling.
 #include "internal.h"
@@ -426,55 +426,64 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
 }
 
 // Classifier gradients: dW_cls [n_cls][C] = sum_p g_p^T f_p and db_cls =
-// sum_p g_p over chunk blockIdx.z of kClsChunk points, for the 16 classes
-// from 16 blockIdx.y and the 64 channels from 64 blockIdx.x.  Thread t owns
-// class t / 16 and channels 4 (t mod 16) .. +3; the chunk's g and f pass
-// through LDS kClsTile points at a time (zero past m, n_cls and C).
-constexpr int kClsChunk = 256, kClsTile = 128, kClsK = 16, kClsC = 64;
-__global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int C, int n_cls, const float *__restrict__ grad_out,
-                                                    const float *__restrict__ f, float *__restrict__ part_c,
-                                                    float *__restrict__ part_bc) {
-    __shared__ float gs[kClsTile][kClsK];
-    __shared__ float4 fs[kClsTile][kClsC / 4];
-    const int t = threadIdx.x;
-    const int k = t >> 4, cq = t & 15;
-    const int c0 = blockIdx.x * kClsC, k0 = blockIdx.y * kClsK;
-    const int64_t chunk = blockIdx.z;
+// sum_p g_p, as partial sums over chunks of kClsChunk points, on fp32 MFMA.
+// One wavefront per chunk and tile of 32 classes x 64 channels (blockIdx.y):
+// v_mfma_f32_32x32x2f32 with A = the chunk's g rows transposed (32 classes x
+// 2 points: lane l holds class l mod 32 of point l / 32 of the pair) and B
+// = their f rows (2 points x 32 channels), twice (channels c0 .. c0 + 31 and
+// c0 + 32 .. c0 + 63).  The tile with c0 = 0 also sums each class's g values
+// (db_cls).  Classes past n_cls, channels past C and points past m are zeros.
+constexpr int kClsChunk = 256;
+constexpr int kClsSteps = 8;  // point pairs whose loads are in flight together
+typedef float f32x16c_t __attribute__((ext_vector_type(16)));
+
+__global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int nch, int C, int n_cls,
+                                                    const float *__restrict__ grad_out, const float *__restrict__ f,
+                                                    float *__restrict__ part_c, float *__restrict__ part_bc) {
+    const int lane = threadIdx.x & 63;
+    const int64_t chunk = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+    if (chunk >= nch) return;  // a whole wavefront; the kernel has no barrier
+    const int ntc = (C + 63) / 64;
+    const int k0 = (int)(blockIdx.y / ntc) * 32, c0 = (int)(blockIdx.y % ntc) * 64;
+    const int row = lane & 31, half = lane >> 5;
+    const int kA = k0 + row, cB0 = c0 + row, cB1 = c0 + 32 + row;
+    const bool okA = kA < n_cls, okB0 = cB0 < C, okB1 = cB1 < C;
     const int64_t p0 = chunk * kClsChunk;
     const int64_t p1 = p0 + kClsChunk < m ? p0 + kClsChunk : m;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    float accb = 0.f;
-    for (int64_t q0 = p0; q0 < p1; q0 += kClsTile) {
-        for (int i = t; i < kClsTile * kClsK; i += kBlock) {
-            const int pp = i / kClsK, kk = i % kClsK;
-            const int64_t p = q0 + pp;
-            gs[pp][kk] = (p < p1 && k0 + kk < n_cls) ? grad_out[p * n_cls + k0 + kk] : 0.f;
-        }
-        for (int i = t; i < kClsTile * kClsC; i += kBlock) {
-            const int pp = i / kClsC, cc = i % kClsC;
-            const int64_t p = q0 + pp;
-            reinterpret_cast<float *>(&fs[pp][0])[cc] = (p < p1 && c0 + cc < C) ? f[p * C + c0 + cc] : 0.f;
-        }
-        __syncthreads();
-#pragma unroll 8
-        for (int pp = 0; pp < kClsTile; ++pp) {
-            const float g = gs[pp][k];
-            const float4 x = fs[pp][cq];
-            acc.x = fmaf(g, x.x, acc.x);
-            acc.y = fmaf(g, x.y, acc.y);
-            acc.z = fmaf(g, x.z, acc.z);
-            acc.w = fmaf(g, x.w, acc.w);
-            accb += g;
-        }
-        __syncthreads();
-    }
-    if (k0 + k < n_cls) {
-        float *o = part_c + (chunk * n_cls + k0 + k) * C;
-        const float a[4] = {acc.x, acc.y, acc.z, acc.w};
+    f32x16c_t acc0, acc1;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (c0 + 4 * cq + i < C) o[c0 + 4 * cq + i] = a[i];
-        if (blockIdx.x == 0 && cq == 0) part_bc[chunk * n_cls + k0 + k] = accb;
+    for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.f;
+    float sb = 0.f;
+    for (int64_t q = p0; q < p1; q += 2 * kClsSteps) {
+        float a[kClsSteps], b0[kClsSteps], b1[kClsSteps];
+#pragma unroll
+        for (int s = 0; s < kClsSteps; ++s) {
+            const int64_t p = q + 2 * s + half;
+            const bool okp = p < p1;
+            a[s] = okp && okA ? grad_out[p * n_cls + kA] : 0.f;
+            b0[s] = okp && okB0 ? f[p * C + cB0] : 0.f;
+            b1[s] = okp && okB1 ? f[p * C + cB1] : 0.f;
+        }
+#pragma unroll
+        for (int s = 0; s < kClsSteps; ++s) {
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b0[s], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b1[s], acc1, 0, 0, 0);
+            sb += a[s];
+        }
+    }
+    // D: lane l holds channel l mod 32, in register r the class 8 (r / 4) + 4 (l / 32) + r mod 4
+    float *o = part_c + chunk * n_cls * C;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int k = k0 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (k < n_cls) {
+            if (okB0) o[(int64_t)k * C + cB0] = acc0[r];
+            if (okB1) o[(int64_t)k * C + cB1] = acc1[r];
+        }
+    }
+    if (c0 == 0) {
+        sb += __shfl_xor(sb, 32, 64);
+        if (half == 0 && okA) part_bc[chunk * n_cls + kA] = sb;
     }
 }
 
@@ -504,6 +513,8 @@ __device__ __forceinline__ void group_sum_n(float *x) {
         for (int k = 0; k < N; ++k) x[k] += y[k];
     }
 }
+
+constexpr int kGl = 4;  // registers of g classes loaded ahead, per lane
 
 template <int D, int LG, bool IN_BF16, bool CLS>
 __global__ __launch_bounds__(kBlock) void k_dfb_points_g(int64_t m, int C, const int32_t *__restrict__ idx,
@@ -545,6 +556,14 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points_g(int64_t m, int C, const
             v[k] = idx[q * DP1 + k];
             b[k] = live ? bary[q * DP1 + k] : 0.f;
         }
+        // the point's first kGl G classes of g, loaded with its record (lane j
+        // of the group holds class i G + j in gpre[i])
+        float gpre[kGl];
+#pragma unroll
+        for (int i = 0; i < kGl; ++i) {
+            const int c = i * G + j;
+            gpre[i] = (CLS && live && c < n_cls) ? grad_out[q * n_cls + c] : 0.f;
+        }
         float4 x[DP1];
 #pragma unroll
         for (int k = 0; k < DP1; ++k)
@@ -582,7 +601,11 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points_g(int64_t m, int C, const
         } else {
             for (int c0 = 0; c0 < n_cls; c0 += G) {
                 // lane j of the group holds the point's g[c0 + j]; class c0 + t from lane t
-                const float gl = (live && c0 + j < n_cls) ? grad_out[q * n_cls + c0 + j] : 0.f;
+                const int ci = c0 >> LG;
+                float gl = gpre[0];
+#pragma unroll
+                for (int i = 1; i < kGl; ++i) gl = ci == i ? gpre[i] : gl;
+                if (ci >= kGl) gl = (live && c0 + j < n_cls) ? grad_out[q * n_cls + c0 + j] : 0.f;
                 const int nb = n_cls - c0 < G ? n_cls - c0 : G;
                 for (int t = 0; t < nb; ++t) {
                     const float g = __shfl(gl, (grp << LG) + t, 64);
@@ -775,9 +798,9 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
     if (w_cls && (grad_w_cls || grad_b_cls)) {
         float *pc = reinterpret_cast<float *>(scratch + l.pc);
         float *pbc = reinterpret_cast<float *>(scratch + l.pbc);
-        hipLaunchKernelGGL(k_dfb_cls, dim3((unsigned)((C + kClsC - 1) / kClsC), (unsigned)((n_cls + kClsK - 1) / kClsK),
-                                           (unsigned)nch),
-                           dim3(kBlock), 0, L->stream, L->m, C, n_cls, grad_out, f, pc, pbc);
+        const unsigned tiles = (unsigned)(((n_cls + 31) / 32) * ((C + 63) / 64));
+        hipLaunchKernelGGL(k_dfb_cls, dim3((unsigned)((nch + kBlock / 64 - 1) / (kBlock / 64)), tiles), dim3(kBlock), 0,
+                           L->stream, L->m, nch, C, n_cls, grad_out, f, pc, pbc);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (grad_w_cls && (e = rowsum::sum(L->stream, pc, nch, (int64_t)n_cls * C, tmp, grad_w_cls)) != hipSuccess)
             return e;
