@@ -25,7 +25,7 @@
 //                  lists: no atomics), lane = channel.
 //   k_dfb_cls      dW_cls and db_cls partials per chunk of 256 points, on
 //                  fp32 MFMA: a wavefront per chunk and tile of 32 classes x
-//                  64 channels, the chunk's g and f rows as the operands.
+//                  32 channels, the chunk's g and f rows as the operands.
 //   rowsum         every partial added in a fixed order: the results do not
 //                  depend on scheduling.
 #include "internal.h"
@@ -35,6 +35,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kClsLdsFloats = 4096;  // classifier weights staged in LDS up to 16 KB (occupancy kept)
+constexpr int kDxRows1 = 8;          // list entries whose gf and am rows are loaded together, C <= 64
 
 // N wavefront sums at once (each step of the N butterflies issued together).
 template <int N>
@@ -253,24 +254,34 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points(int64_t m, int C, const i
 // giving a point p and the vertex's slot k in p's simplex, the two sums whose
 // combination is dX_v: acc = sum alpha_pk gf_p and accw = sum (beta_pk -
 // [k = k*_pc] gamma_pk), with dX_v = acc + w_delta accw.  Lane t holds entry
-// t (`x`, loaded a list ahead by dx_entry) and loads its three coefficients;
-// then the rows of gf and am are loaded several entries at a time, each
-// entry's values read from its lane, and added in list order.
+// t (`x`, from dx_entry) and its three coefficients (dx_coef); the rows of
+// gf and am are loaded several entries at a time (dx_rows), each entry's
+// values read from its lane, and added in list order.  The kernels load a
+// list's entries two lists ahead and its coefficients one list ahead.
 __device__ __forceinline__ int dx_entry(const int32_t *__restrict__ list, int64_t e0, int n, int lane) {
     const bool ok = n >= 1 && n <= kPart;  // otherwise entry 0, which exists whenever a list is read
     return list[2 * (ok ? e0 + (lane < n ? lane : n - 1) : 0)];
 }
 
-template <int D, int CH>
-__device__ __forceinline__ void dx_sums(int x, int n, int C, const float *__restrict__ coef,
-                                        const float *__restrict__ gf, const uint8_t *__restrict__ am, float *acc,
-                                        float *accw) {
-    constexpr int DP1 = D + 1;
-    constexpr int NB = CH >= 8 ? 1 : 8 / CH;  // entries whose rows are in flight together
+struct DxCoef {
+    float al, be, ga;
+};
+
+template <int D>
+__device__ __forceinline__ DxCoef dx_coef(int x, const float *__restrict__ coef) {
+    const float *cf = coef + ((int64_t)list_point(x) * (D + 1) + list_slot(x)) * 3;
+    return DxCoef{cf[0], cf[1], cf[2]};
+}
+
+template <int CH>
+constexpr int dx_block() { return CH == 1 ? kDxRows1 : CH >= 8 ? 1 : 8 / CH; }
+
+template <int CH>
+__device__ __forceinline__ void dx_rows(int x, DxCoef q, int n, int C, const float *__restrict__ gf,
+                                        const uint8_t *__restrict__ am, float *acc, float *accw) {
+    constexpr int NB = dx_block<CH>();  // entries whose rows are in flight together
     const int lane = threadIdx.x & 63;
     const int pl = list_point(x), kl = list_slot(x);
-    const float *cf = coef + ((int64_t)pl * DP1 + kl) * 3;
-    const float all = cf[0], bel = cf[1], gal = cf[2];
 #pragma unroll
     for (int i = 0; i < CH; ++i) acc[i] = accw[i] = 0.f;
     for (int t0 = 0; t0 < n; t0 += NB) {
@@ -281,9 +292,9 @@ __device__ __forceinline__ void dx_sums(int x, int n, int C, const float *__rest
             const int t = t0 + u;  // below 2 kPart; lanes past n hold entry n - 1
             ps[u] = __builtin_amdgcn_readlane(pl, t);
             ks[u] = __builtin_amdgcn_readlane(kl, t);
-            al[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(all), t));
-            be[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bel), t));
-            ga[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gal), t));
+            al[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q.al), t));
+            be[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q.be), t));
+            ga[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q.ga), t));
         }
         // rows past n are not loaded (a wave-uniform branch)
         float g[NB][CH];
@@ -314,8 +325,7 @@ __device__ __forceinline__ void dx_sums(int x, int n, int C, const float *__rest
 
 // The parts of long pair lists (the splat's split lists: more than kPart
 // entries, cut into parts of kPart): one wavefront per part row, writing its
-// acc and accw to part row u of `partial` [rows][2 C]; the next part's
-// entries are loaded while this one is summed.
+// acc and accw to part row u of `partial` [rows][2 C].
 template <int D, int CH>
 __global__ __launch_bounds__(kBlock) void k_dfb_parts(const int32_t *__restrict__ counters, int C,
                                                       const int32_t *__restrict__ list,
@@ -325,16 +335,21 @@ __global__ __launch_bounds__(kBlock) void k_dfb_parts(const int32_t *__restrict_
     const int lane = threadIdx.x & 63;
     const int64_t nrows = counters[CNT_ROWS];
     const XcdShare sh = xcd_share(nrows);
+    const int64_t st = sh.nwaves;
     auto rec = [&](int64_t u) { return u < sh.hi ? partrec[u] : make_int2(0, 0); };
     int64_t u = sh.lo + sh.wave;
-    int2 r = rec(u);
-    int x = dx_entry(list, r.x, r.y, lane);
-    int2 rn = rec(u + sh.nwaves);
-    for (; u < sh.hi; u += sh.nwaves) {
-        const int xn = dx_entry(list, rn.x, rn.y, lane);
-        const int2 rnn = rec(u + 2 * sh.nwaves);
+    int2 r0 = rec(u);
+    int x0 = dx_entry(list, r0.x, r0.y, lane);
+    int2 r1 = rec(u + st);
+    DxCoef q0 = dx_coef<D>(x0, coef);
+    int x1 = dx_entry(list, r1.x, r1.y, lane);
+    int2 r2 = rec(u + 2 * st);
+    for (; u < sh.hi; u += st) {
+        const DxCoef q1 = dx_coef<D>(x1, coef);
+        const int x2 = dx_entry(list, r2.x, r2.y, lane);
+        const int2 r3 = rec(u + 3 * st);
         float acc[CH], accw[CH];
-        dx_sums<D, CH>(x, r.y, C, coef, gf, am, acc, accw);
+        dx_rows<CH>(x0, q0, r0.y, C, gf, am, acc, accw);
         float *o = partial + u * 2 * C;
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
@@ -344,9 +359,12 @@ __global__ __launch_bounds__(kBlock) void k_dfb_parts(const int32_t *__restrict_
                 o[C + c] = accw[i];
             }
         }
-        x = xn;
-        r = rn;
-        rn = rnn;
+        r0 = r1;
+        x0 = x1;
+        q0 = q1;
+        r1 = r2;
+        x1 = x2;
+        r2 = r3;
     }
 }
 
@@ -384,25 +402,33 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
             }
         }
     };
-    // short lists, the next vertex's entries loaded while this one is summed
+    // short lists: headers three vertices ahead, entries two, coefficients one
     const XcdShare sh = xcd_share(V);
+    const int64_t st = sh.nwaves;
     const int2 *VI = reinterpret_cast<const int2 *>(vinfo);
     auto header = [&](int64_t v) { return v < sh.hi ? VI[v] : make_int2(0, 0); };
     int64_t v = sh.lo + sh.wave;
-    int2 h = header(v);
-    int x = dx_entry(list, h.x, h.y, lane);
-    int2 hn = header(v + sh.nwaves);
-    for (; v < sh.hi; v += sh.nwaves) {
-        const int xn = dx_entry(list, hn.x, hn.y, lane);
-        const int2 hnn = header(v + 2 * sh.nwaves);
-        if (h.y <= kPart) {  // a split vertex: below
+    int2 h0 = header(v);
+    int x0 = dx_entry(list, h0.x, h0.y, lane);
+    int2 h1 = header(v + st);
+    DxCoef q0 = dx_coef<D>(x0, coef);
+    int x1 = dx_entry(list, h1.x, h1.y, lane);
+    int2 h2 = header(v + 2 * st);
+    for (; v < sh.hi; v += st) {
+        const DxCoef q1 = dx_coef<D>(x1, coef);
+        const int x2 = dx_entry(list, h2.x, h2.y, lane);
+        const int2 h3 = header(v + 3 * st);
+        if (h0.y <= kPart) {  // a split vertex: below
             float acc[CH], accw[CH];
-            dx_sums<D, CH>(x, h.y, C, coef, gf, am, acc, accw);
+            dx_rows<CH>(x0, q0, h0.y, C, gf, am, acc, accw);
             store(v, acc, accw);
         }
-        x = xn;
-        h = hn;
-        hn = hnn;
+        h0 = h1;
+        x0 = x1;
+        q0 = q1;
+        h1 = h2;
+        x1 = x2;
+        h2 = h3;
     }
     const XcdShare ss = xcd_share(ns);
     for (int64_t sp = ss.lo + ss.wave; sp < ss.hi; sp += ss.nwaves) {
@@ -427,12 +453,12 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
 
 // Classifier gradients: dW_cls [n_cls][C] = sum_p g_p^T f_p and db_cls =
 // sum_p g_p, as partial sums over chunks of kClsChunk points, on fp32 MFMA.
-// One wavefront per chunk and tile of 32 classes x 64 channels (blockIdx.y):
+// One wavefront per chunk and tile of 32 classes x 32 channels (blockIdx.y):
 // v_mfma_f32_32x32x2f32 with A = the chunk's g rows transposed (32 classes x
 // 2 points: lane l holds class l mod 32 of point l / 32 of the pair) and B
-// = their f rows (2 points x 32 channels), twice (channels c0 .. c0 + 31 and
-// c0 + 32 .. c0 + 63).  The tile with c0 = 0 also sums each class's g values
-// (db_cls).  Classes past n_cls, channels past C and points past m are zeros.
+// = their f rows (2 points x 32 channels).  The tiles with c0 = 0 also sum
+// each class's g values (db_cls).  Classes past n_cls, channels past C and
+// points past m are zeros.
 constexpr int kClsChunk = 256;
 constexpr int kClsSteps = 8;  // point pairs whose loads are in flight together
 typedef float f32x16c_t __attribute__((ext_vector_type(16)));
@@ -443,31 +469,29 @@ __global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int nch, int C, i
     const int lane = threadIdx.x & 63;
     const int64_t chunk = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
     if (chunk >= nch) return;  // a whole wavefront; the kernel has no barrier
-    const int ntc = (C + 63) / 64;
-    const int k0 = (int)(blockIdx.y / ntc) * 32, c0 = (int)(blockIdx.y % ntc) * 64;
+    const int ntc = (C + 31) / 32;
+    const int k0 = (int)(blockIdx.y / ntc) * 32, c0 = (int)(blockIdx.y % ntc) * 32;
     const int row = lane & 31, half = lane >> 5;
-    const int kA = k0 + row, cB0 = c0 + row, cB1 = c0 + 32 + row;
-    const bool okA = kA < n_cls, okB0 = cB0 < C, okB1 = cB1 < C;
+    const int kA = k0 + row, cB = c0 + row;
+    const bool okA = kA < n_cls, okB = cB < C;
     const int64_t p0 = chunk * kClsChunk;
     const int64_t p1 = p0 + kClsChunk < m ? p0 + kClsChunk : m;
-    f32x16c_t acc0, acc1;
+    f32x16c_t acc;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.f;
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
     float sb = 0.f;
     for (int64_t q = p0; q < p1; q += 2 * kClsSteps) {
-        float a[kClsSteps], b0[kClsSteps], b1[kClsSteps];
+        float a[kClsSteps], b[kClsSteps];
 #pragma unroll
         for (int s = 0; s < kClsSteps; ++s) {
             const int64_t p = q + 2 * s + half;
             const bool okp = p < p1;
             a[s] = okp && okA ? grad_out[p * n_cls + kA] : 0.f;
-            b0[s] = okp && okB0 ? f[p * C + cB0] : 0.f;
-            b1[s] = okp && okB1 ? f[p * C + cB1] : 0.f;
+            b[s] = okp && okB ? f[p * C + cB] : 0.f;
         }
 #pragma unroll
         for (int s = 0; s < kClsSteps; ++s) {
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b0[s], acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b1[s], acc1, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], acc, 0, 0, 0);
             sb += a[s];
         }
     }
@@ -476,10 +500,7 @@ __global__ __launch_bounds__(kBlock) void k_dfb_cls(int64_t m, int nch, int C, i
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         const int k = k0 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (k < n_cls) {
-            if (okB0) o[(int64_t)k * C + cB0] = acc0[r];
-            if (okB1) o[(int64_t)k * C + cB1] = acc1[r];
-        }
+        if (k < n_cls && okB) o[(int64_t)k * C + cB] = acc[r];
     }
     if (c0 == 0) {
         sb += __shfl_xor(sb, 32, 64);
@@ -545,6 +566,15 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points_g(int64_t m, int C, const
     const float4 wd = has ? reinterpret_cast<const float4 *>(w_delta)[j] : make_float4(0.f, 0.f, 0.f, 0.f);
     float4 acc_w = make_float4(0.f, 0.f, 0.f, 0.f);
     float acc_b = 0.f;
+    // a point's vertex ids are loaded an iteration ahead of its rows
+    int vn[DP1];
+    auto load_ids = [&](int64_t p0n) {
+        const int64_t pn = p0n + grp;
+        const int64_t qn = pn < m ? pn : 0;
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) vn[k] = idx[qn * DP1 + k];
+    };
+    load_ids(wave * PPW);
     for (int64_t p0 = wave * PPW; p0 < m; p0 += nwaves * PPW) {
         const int64_t p = p0 + grp;
         const bool live = p < m;
@@ -552,10 +582,10 @@ __global__ __launch_bounds__(kBlock) void k_dfb_points_g(int64_t m, int C, const
         int v[DP1];
         float b[DP1];
 #pragma unroll
-        for (int k = 0; k < DP1; ++k) {
-            v[k] = idx[q * DP1 + k];
-            b[k] = live ? bary[q * DP1 + k] : 0.f;
-        }
+        for (int k = 0; k < DP1; ++k) v[k] = vn[k];
+        load_ids(p0 + nwaves * PPW);
+#pragma unroll
+        for (int k = 0; k < DP1; ++k) b[k] = live ? bary[q * DP1 + k] : 0.f;
         // the point's first kGl G classes of g, loaded with its record (lane j
         // of the group holds class i G + j in gpre[i])
         float gpre[kGl];
@@ -798,7 +828,7 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
     if (w_cls && (grad_w_cls || grad_b_cls)) {
         float *pc = reinterpret_cast<float *>(scratch + l.pc);
         float *pbc = reinterpret_cast<float *>(scratch + l.pbc);
-        const unsigned tiles = (unsigned)(((n_cls + 31) / 32) * ((C + 63) / 64));
+        const unsigned tiles = (unsigned)(((n_cls + 31) / 32) * ((C + 31) / 32));
         hipLaunchKernelGGL(k_dfb_cls, dim3((unsigned)((nch + kBlock / 64 - 1) / (kBlock / 64)), tiles), dim3(kBlock), 0,
                            L->stream, L->m, nch, C, n_cls, grad_out, f, pc, pbc);
         if ((e = hipGetLastError()) != hipSuccess) return e;
