@@ -218,6 +218,42 @@ def test_deform_slice_backward_parity(d, C, n_cls, bf16):
         assert gwc is None and gbc is None
 
 
+@pytest.mark.parametrize("C,n_cls,bf16", [(64, 20, False), (128, 7, True), (16, 0, False)])
+def test_deform_slice_backward_long_pair_lists(C, n_cls, bf16):
+    """DeformSlice backward on clustered clouds: vertices with thousands of
+    pairs are summed in parts of 32 entries (part rows added in part order),
+    next to short lists; twice on one lattice, the second cloud smaller, so
+    that no part record or list entry of the first splat leaks into the
+    second."""
+    L = _lattice(3, 0.1, 9000)
+    for rep, (md, ms) in enumerate([(6000, 3000), (2500, 700)]):
+        pos = _clustered(70 + rep, md, ms)
+        g = GpuLattice(L, pos, None)
+        lat = O.build(pos, 0.1)
+        assert g.V == lat.V and np.array_equal(g.keys, lat.keys)
+        counts = np.bincount(lat.idx.reshape(-1), minlength=lat.V)
+        assert counts.max() > 500 and (counts > 32).sum() >= 3 and (counts <= 32).sum() > 100
+        y = random_rows(lat.V, C, seed=71 + C + rep)
+        if bf16:
+            y = O.round_bf16(y.astype(np.float32)).astype(np.float32)
+        yd = g.to_gpu_order(y)
+        if bf16:
+            yd = yd.to(torch.bfloat16)
+        dw = deform_weights(C, max(n_cls, 1), seed=72 + C)
+        with_cls = n_cls > 0
+        G = random_rows(pos.shape[0], n_cls if with_cls else C, seed=73 + C + rep)
+        gv, gwd, gbd, gwc, gbc = L.deform_slice_backward(yd, to_dev(dw.w_delta), dw.b_delta, to_dev(G),
+                                                          to_dev(dw.w_cls) if with_cls else None)
+        (rX, rw, rb, rWc, rbc), (sX, sw, sb, sWc, sbc) = O.deform_slice_backward(
+            lat.idx, lat.bary, y, dw.w_delta, dw.b_delta, G, lat.V, dw.w_cls if with_cls else None)
+        tag = f"deform backward, split lists C={C} n_cls={n_cls} rep={rep}"
+        assert_close_scaled(g.from_gpu_order(gv), rX, sX, REL_F32, tag + " values")
+        assert_close_scaled(gwd.cpu().numpy(), rw, sw, REL_F32, tag + " w_delta")
+        if with_cls:
+            assert_close_scaled(gwc.cpu().numpy(), rWc, sWc, REL_F32, tag + " w_cls")
+            assert_close_scaled(gbc.cpu().numpy(), rbc, sbc, REL_F32, tag + " b_cls")
+
+
 def test_deform_slice_backward_without_offsets_is_slice_backward():
     """Zero offset weights and bias: db = 0, so the vertex gradient of the
     point features is the slice's backward (the splat of grad_out), and the

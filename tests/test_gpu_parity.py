@@ -68,12 +68,16 @@ def _clustered_cloud(seed, C, m_dense=6000, m_sparse=3000):
 
 
 @pytest.mark.parametrize("C,values_dtype,normalize", [(3, "f32", False), (64, "f32", False), (64, "bf16", False),
-                                                      (128, "f32", True), (520, "f32", False), (0, "f32", False)])
+                                                      (128, "f32", True), (520, "f32", False), (0, "f32", False),
+                                                      (12, "f32", False), (32, "bf16", False), (96, "f32", True),
+                                                      (256, "f32", False)])
 def test_splat_long_pair_lists(C, values_dtype, normalize):
     """Vertices with up to thousands of (point, vertex) pairs: their lists are
     summed in parts of 32 pairs and the parts added in order; the result must
     not depend on that split.  Two splats in a row on one lattice (the second smaller)
-    check that no per-split state leaks from the first."""
+    check that no per-split state leaks from the first.  Channel counts cover
+    every group width of the float4 gather (4 to 64 lanes, with idle lanes
+    when C / 4 is not a power of two) and the scalar one."""
     sigma = 0.1
     L = _lattice(3, sigma, 9000)
     for rep, (md, ms) in enumerate([(6000, 3000), (2500, 700)]):
