@@ -65,9 +65,9 @@ constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
 constexpr int kW1 = 16, kW2 = 32, kW3 = 64;  // block widths (the paper's figure)
 constexpr int kMaxK0 = 16;                   // d + f_d, zero-padded to 16
-// The backward's per-entry record: h_0 (padded), h_1, h_2 (the blocks'
-// inputs) and h_3 (the last block's output), fp32, 512 bytes
-constexpr int kRecH1 = kMaxK0, kRecH2 = kRecH1 + kW1, kRecH3 = kRecH2 + kW2, kRec = kRecH3 + kW3;
+// The backward's per-entry record: h_0 (padded), h_1 and h_2 (the blocks'
+// inputs), fp32, 256 bytes
+constexpr int kRecH1 = kMaxK0, kRecH2 = kRecH1 + kW1, kRec = kRecH2 + kW2;
 // LDS row of one output channel: 64 entries + 4 (16-byte aligned rows; the
 // 16 lanes of a quarter-wave reading 16 bytes each then cover all 64 banks,
 // and the MFMA output writes of the four lane quarters fall 16 banks apart)
@@ -572,7 +572,7 @@ __device__ __forceinline__ void wave_sync() {
 // lattice) uses that cloud's affines, kept in registers while the cloud
 // stays the same; a chunk that spans clouds loads each entry's own.
 template <int MODE, bool OUT_BF16>
-__global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__ list,
+__global__ __launch_bounds__(kBlock, 2) void k_pointnet(const int32_t *__restrict__ list,
                                                      const int32_t *__restrict__ lvert,
                                                      const int32_t *__restrict__ vinfo,
                                                      const uint64_t *__restrict__ vkeys, int batched,
@@ -583,10 +583,11 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
                                                      const int32_t *__restrict__ counters,
                                                      double *__restrict__ stats,
                                                      unsigned int *__restrict__ keys, void *__restrict__ out,
-                                                     float *__restrict__ rec, uint64_t *__restrict__ routed) {
-    // MODE 3: outputs [64 channels][64 entries], first the staged inputs;
-    // MODE 1, 2, 4: the staged inputs only
-    constexpr int kYWave = MODE == 3 ? kW3 * kYStride : 64 * (kMaxK0 + 1);
+                                                     float *__restrict__ rec, uint64_t *__restrict__ routed,
+                                                     int32_t *__restrict__ win, uint2 *__restrict__ wslot) {
+    // MODE 3, 4: outputs [64 channels][64 entries], first the staged inputs;
+    // MODE 1, 2: the staged inputs only
+    constexpr int kYWave = MODE >= 3 ? kW3 * kYStride : 64 * (kMaxK0 + 1);
     __shared__ __attribute__((aligned(16))) float ysh[kWaves][kYWave];
     // MODE 1, 2 on a batched lattice: the workgroup's sums (then sums of
     // squares) of the block's output per cloud
@@ -792,7 +793,7 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
         }
         // run flags: 1 first entry of a run, 2 last, 4 the run is the vertex's whole list
         int flags = 0, dest = -1;
-        if (MODE == 3) {
+        if (MODE >= 3) {
             const int vprev = __shfl_up(v, 1);
             const int vnext = __shfl_down(v, 1);
             if (valid) {
@@ -893,8 +894,8 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 #pragma unroll
             for (int t = 0; t < 8; ++t)
                 r2[t] = relu(fmaf(a2[t / 4][t % 4], d2[t / 4][t % 4], s2[t / 4][t % 4]));
-            // MODE 4: this lane's four channels of h_1, h_2 (and below h_3)
-            // of entry 16 nt + j16 go to its record
+            // MODE 4: this lane's four channels of h_1 and h_2 of entry
+            // 16 nt + j16 go to its record
             float *R = MODE == 4 ? rec + (chunk0 + 16 * nt + j16) * kRec : nullptr;
             if (MODE == 4 && ebv >= 0) {
                 *reinterpret_cast<float4 *>(R + kRecH1 + 4 * q) =
@@ -910,16 +911,8 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
                 f32x4_t d3 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int t = 0; t < 8; ++t) d3 = mfma16(wa3[mt][t], r2[t], d3);
-                if (MODE == 4) {
-                    if (ebv >= 0)
-                        *reinterpret_cast<float4 *>(R + kRecH3 + 16 * mt + 4 * q) =
-                            make_float4(d3[0] + bb3[mt][0], d3[1] + bb3[mt][1], d3[2] + bb3[mt][2],
-                                        d3[3] + bb3[mt][3]);
-                } else {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        Y[(16 * mt + 4 * q + r) * kYStride + 16 * nt + j16] = d3[r] + bb3[mt][r];
-                }
+                for (int r = 0; r < 4; ++r) Y[(16 * mt + 4 * q + r) * kYStride + 16 * nt + j16] = d3[r] + bb3[mt][r];
             }
         }
 
@@ -945,6 +938,40 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
                             store_out<OUT_BF16>(out, vj, c, mx);
                         else
                             atomicMax(keys + (int64_t)vj * kW3 + c, max_key(mx));
+                    }
+                }
+            }
+        }
+        if (MODE == 4) {
+            wave_sync();
+            // lane c: the first maximum of channel c over each run of the
+            // wavefront's entries (the values the forward's max takes, in
+            // entry order), kept at the end of the run: the winning entry of
+            // a list that lies within this chunk; for a list that crosses a
+            // chunk boundary, the run's (value, entry) in slot 0 of the chunk
+            // (the run that holds the chunk's first entry) or slot 1 (the run
+            // that holds its last), which the argmax combines in chunk order
+            const int c = lane;
+            float mx = 0.f;
+            int be = 0, r0 = 0;
+#pragma unroll
+            for (int j4 = 0; j4 < 16; ++j4) {
+                const f32x4_t y4 = *reinterpret_cast<const f32x4_t *>(Y + c * kYStride + 4 * j4);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int jj = 4 * j4 + i;
+                    const int fj = __builtin_amdgcn_readlane(flags, jj);
+                    if (fj & 1) r0 = jj;
+                    if ((fj & 1) || y4[i] > mx) {
+                        mx = y4[i];
+                        be = jj;
+                    }
+                    if (fj & 2) {
+                        if (fj & 4)
+                            win[(int64_t)__builtin_amdgcn_readlane(dest, jj) * kW3 + c] = (int32_t)(chunk0 + be);
+                        else
+                            wslot[(ch * 2 + (r0 == 0 ? 0 : 1)) * kW3 + c] =
+                                make_uint2(__float_as_uint(mx), (uint32_t)(chunk0 + be));
                     }
                 }
             }
@@ -975,13 +1002,16 @@ __global__ __launch_bounds__(kBlock) void k_pointnet(const int32_t *__restrict__
 //   k_dpn_norm     per cloud and block, each input channel's group mean and
 //                  1 / sqrt(var + eps) from the fp64 sums (mean 0, 1 for the
 //                  fixed affine)
-//   k_pointnet<4>  the record of e: block inputs h0 (padded), h1, h2 and the
-//                  last block's output h3, fp32, from the forward's MFMA pass
-//                  (the values its max took)
-//   k_dpn_argmax   one wavefront per vertex, lane = channel c: the row whose
-//                  h3[c] is largest (the first in list order), which receives
-//                  g[v][c]; dW3[c][.] += g r3 and db3[c] += g of that row; per
-//                  entry the mask of the channels it receives
+//   k_pointnet<4>  the forward's MFMA pass once more: the record of e (block
+//                  inputs h0 (padded), h1, h2, fp32) and, per vertex and
+//                  channel c, the entry whose h3[c] is largest (the first in
+//                  list order), found over each run of a wavefront's entries
+//                  as the forward's max is (the values its max took)
+//   k_dpn_argmax   one wavefront per vertex, lane = channel c: the winning
+//                  row (a list that crosses chunks: its runs' winners combined
+//                  in chunk order) receives g[v][c]; dW3[c][.] += g r3 and
+//                  db3[c] += g of that row; per entry the mask of the channels
+//                  it receives
 //   k_dpn_back<S>  one wavefront per workgroup, a lane per entry: back through
 //                  block 3 (S = 3: dhn3 from the routed channels, stored per
 //                  entry; dgamma3, dbeta3 and the group sums of gamma dhn and
@@ -1086,6 +1116,8 @@ __device__ __forceinline__ void load_params(const float *__restrict__ P, float *
 __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict__ vinfo,
                                                        const uint64_t *__restrict__ vkeys, int batched,
                                                        const float *__restrict__ aff, const float *__restrict__ rec,
+                                                       const int32_t *__restrict__ win,
+                                                       const uint2 *__restrict__ wslot,
                                                        const float *__restrict__ grad_out,
                                                        const int32_t *__restrict__ counters,
                                                        uint64_t *__restrict__ routed, float *__restrict__ part) {
@@ -1099,20 +1131,25 @@ __global__ __launch_bounds__(kBlock) void k_dpn_argmax(const int32_t *__restrict
     for (int64_t v = wave; v < V; v += nwaves) {
         const int64_t off = vinfo[2 * v];
         const int cnt = vinfo[2 * v + 1];
-        // the first maximum in list order, eight entries' loads in flight
-        constexpr int U = 8;
-        float best = 0.f;
-        int be = (int)off;  // entry indices fit in 32 bits
-        for (int i0 = 0; i0 < cnt; i0 += U) {
-            float x[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) x[u] = i0 + u < cnt ? rec[(off + i0 + u) * kRec + kRecH3 + lane] : 0.f;
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (i0 + u < cnt && (i0 + u == 0 || x[u] > best)) {
-                    best = x[u];
-                    be = (int)(off + i0 + u);
+        // the winning entry of channel c (the first maximum in list order):
+        // recorded by the records pass for a list within one chunk, else
+        // the runs' slots combined in chunk order
+        const int64_t j0 = off >> 6, j1 = (off + cnt - 1) >> 6;
+        int be;
+        if (j0 == j1) {
+            be = win[v * kW3 + lane];
+        } else {
+            float best = 0.f;
+            be = (int)off;
+            for (int64_t j = j0; j <= j1; ++j) {
+                const int sl = (j == j0 && (off & 63) != 0) ? 1 : 0;
+                const uint2 r = wslot[(j * 2 + sl) * kW3 + lane];
+                const float x = __uint_as_float(r.x);
+                if (j == j0 || x > best) {
+                    best = x;
+                    be = (int)r.y;
                 }
+            }
         }
         // the mask of each winning entry (the others were zeroed with their
         // records): one store per distinct winner, by its first lane
@@ -1554,18 +1591,18 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
         if ((e = finalize(0)) != hipSuccess) return e;
         hipLaunchKernelGGL((k_pointnet<1, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
                            L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu, L->counters,
-                           L->pn_stats, L->pn_keys, out, nullptr, nullptr);
+                           L->pn_stats, L->pn_keys, out, nullptr, nullptr, nullptr, nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = finalize(1)) != hipSuccess) return e;
         hipLaunchKernelGGL((k_pointnet<2, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
                            L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu, L->counters,
-                           L->pn_stats, L->pn_keys, out, nullptr, nullptr);
+                           L->pn_stats, L->pn_keys, out, nullptr, nullptr, nullptr, nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = finalize(2)) != hipSuccess) return e;
     }
     hipLaunchKernelGGL((out_bf16 ? k_pointnet<3, true> : k_pointnet<3, false>), dim3(g_p), dim3(kBlock), 0, L->stream,
                        L->list, L->lvert, L->vinfo, L->vkeys, batched, pos, feat, d, f_d, L->pn_params, L->pn_aff, mu,
-                       L->counters, L->pn_stats, L->pn_keys, out, nullptr, nullptr);
+                       L->counters, L->pn_stats, L->pn_keys, out, nullptr, nullptr, nullptr, nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((out_bf16 ? k_pointnet_rows<true> : k_pointnet_rows<false>), dim3(g_i), dim3(kBlock), 0,
                        L->stream, L->lvert, L->vinfo, L->counters, L->pn_keys, out);
@@ -1574,7 +1611,7 @@ hipError_t launch_distribute_pointnet(lattice *L, const float *pos, const float 
 
 // Scratch of the backward (offsets in bytes, 256-aligned).
 struct DpnLayout {
-    int64_t out, rec, routed, d3, d2, nrm, rows, gm, parg, pb3, pb2, pb1, r3, r2, r1, rarg, tmp, total;
+    int64_t out, rec, routed, win, wslot, d3, d2, nrm, rows, gm, parg, pb3, pb2, pb1, r3, r2, r1, rarg, tmp, total;
     int nwaves_arg, nwaves;
 };
 
@@ -1588,6 +1625,8 @@ static DpnLayout dpn_layout(const lattice *L) {
     l.out = at;    at += al(V * kW3 * 4);
     l.rec = at;    at += al(E * kRec * 4);
     l.routed = at; at += al(E * 8);
+    l.win = at;    at += al(V * kW3 * 4);
+    l.wslot = at;  at += al((E + 63) / 64 * 2 * kW3 * 8);
     l.d3 = at;     at += al(E * kW2 * 4);
     l.d2 = at;     at += al(E * kW1 * 4);
     l.nrm = at;    at += al((int64_t)kGnClouds * kNrmRow * 4);
@@ -1636,10 +1675,12 @@ hipError_t launch_distribute_backward(lattice *L, const float *pos, const float 
     const unsigned g_p = grid_for((int64_t)(L->d + 1) * L->m, kBlock, L->cu_count, 2);
     hipLaunchKernelGGL((k_pointnet<4, false>), dim3(g_p), dim3(kBlock), 0, L->stream, L->list, L->lvert, L->vinfo,
                        L->vkeys, batched, pos, feat, L->d, f_d, L->pn_params, L->pn_aff, L->mu, L->counters,
-                       L->pn_stats, L->pn_keys, nullptr, F(l.rec), routed);
+                       L->pn_stats, L->pn_keys, nullptr, F(l.rec), routed, reinterpret_cast<int32_t *>(s + l.win),
+                       reinterpret_cast<uint2 *>(s + l.wslot));
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_dpn_argmax, dim3((unsigned)(l.nwaves_arg / kWaves)), dim3(kBlock), 0, L->stream, L->vinfo,
-                       L->vkeys, batched, L->pn_aff, F(l.rec), grad_out, L->counters, routed, F(l.parg));
+                       L->vkeys, batched, L->pn_aff, F(l.rec), reinterpret_cast<const int32_t *>(s + l.win),
+                       reinterpret_cast<const uint2 *>(s + l.wslot), grad_out, L->counters, routed, F(l.parg));
     if ((e = hipGetLastError()) != hipSuccess) return e;
     auto reduce = [&](const float *part, int64_t nrows, int64_t n, float *out) {
         return rowsum::sum(L->stream, part, nrows, n, F(l.tmp), out);
