@@ -1272,7 +1272,8 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
                     for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dr[j]);
                 }
             } else {
-#pragma unroll 4
+                // (fully unrolled: gv stays in registers)
+#pragma unroll
                 for (int o = 0; o < kW3; ++o) {
                     const float g = ((mk >> o) & 1ull) ? gv[o] : 0.f;
 #pragma unroll
