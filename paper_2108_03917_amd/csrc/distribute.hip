@@ -1047,7 +1047,9 @@ __host__ __device__ inline int pb_len(int S, int batched) {
     const int nc = batched ? kGnClouds : 1;
     return S == 3 ? kPB3Base + nc * kW2 * 2 : (S == 2 ? kPB2Base + nc * kW1 * 2 : kPB1);
 }
-constexpr int kStg = 80;  // staged floats per entry (64-entry chunks)
+// staged floats per entry (64-entry chunks); an odd pitch puts a lane's own
+// row writes and the column reads on 64 different banks
+constexpr int kStg = 81;
 constexpr int kSparseBits = 24;  // pass 3 visits only the routed channels when no entry has more
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
