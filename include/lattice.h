@@ -92,7 +92,8 @@ typedef enum {
  *                  space-time lattice uses d = 4).
  *   sigma          host [d] fp32, per-axis lattice scale, each > 0.
  *   alpha          elevation scale; <= 0 selects (d+1) * sqrt(2/3).
- *   max_points     upper bound on m for every later splat, >= 1.
+ *   max_points     upper bound on m for every later splat, 1 .. 2^28 (the
+ *                  pair lists hold a point index in 28 bits).
  *   hash_capacity  number of hash slots; 0 selects the next power of two
  *                  >= 1.5 (d+1) max_points: it can never fill up, and at
  *                  most two thirds of its slots are ever taken, which keeps

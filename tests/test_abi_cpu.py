@@ -52,6 +52,7 @@ def test_create_rejects_bad_arguments_without_device():
         (3, bad_sig, 0.0, 10, 0),    # sigma <= 0
         (3, nan_sig, 0.0, 10, 0),    # sigma NaN
         (3, sig, 0.0, 0, 0),         # no points
+        (3, sig, 0.0, (1 << 28) + 1, 0),  # above 2^28 points (a pair-list entry holds the point in 28 bits)
         (3, sig, 0.0, 10, -1),       # negative capacity
         (3, sig, float("inf"), 10, 0),
     ]
