@@ -316,7 +316,9 @@ lattice_status lattice_splat_backward(lattice *L, const void *grad_values, latti
  * atomics) and the weight gradients are summed in a fixed order.
  *   values, values_dtype, C, w_delta, b_delta, w_cls, n_cls   as in the
  *                 forward (C 1..1024; b_cls does not enter the gradients).
- *   grad_out      dev fp32 [m][n_cls] with w_cls, else [m][C].
+ *   grad_out      dev fp32 [m][n_cls] with w_cls, else [m][C].  With an
+ *                 empty cloud (m = 0) values and grad_out may be NULL, and
+ *                 the weight gradients are zero.
  *   grad_values   dev [>= V][C] dX stored as grad_dtype, or NULL; must not
  *                 overlap values or grad_out.
  *   grad_w_delta  dev fp32 [C], or NULL.     grad_b_delta  dev fp32 [1], or NULL.

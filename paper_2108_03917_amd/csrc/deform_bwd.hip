@@ -267,8 +267,11 @@ struct DxCoef {
     float al, be, ga;
 };
 
+// The coefficients of a list of n entries; n outside [1, kPart] (a header
+// past the range, whose entry 0 may predate this splat) loads nothing.
 template <int D>
-__device__ __forceinline__ DxCoef dx_coef(int x, const float *__restrict__ coef) {
+__device__ __forceinline__ DxCoef dx_coef(int x, int n, const float *__restrict__ coef) {
+    if (n < 1 || n > kPart) return DxCoef{0.f, 0.f, 0.f};
     const float *cf = coef + ((int64_t)list_point(x) * (D + 1) + list_slot(x)) * 3;
     return DxCoef{cf[0], cf[1], cf[2]};
 }
@@ -341,11 +344,11 @@ __global__ __launch_bounds__(kBlock) void k_dfb_parts(const int32_t *__restrict_
     int2 r0 = rec(u);
     int x0 = dx_entry(list, r0.x, r0.y, lane);
     int2 r1 = rec(u + st);
-    DxCoef q0 = dx_coef<D>(x0, coef);
+    DxCoef q0 = dx_coef<D>(x0, r0.y, coef);
     int x1 = dx_entry(list, r1.x, r1.y, lane);
     int2 r2 = rec(u + 2 * st);
     for (; u < sh.hi; u += st) {
-        const DxCoef q1 = dx_coef<D>(x1, coef);
+        const DxCoef q1 = dx_coef<D>(x1, r1.y, coef);
         const int x2 = dx_entry(list, r2.x, r2.y, lane);
         const int2 r3 = rec(u + 3 * st);
         float acc[CH], accw[CH];
@@ -411,11 +414,11 @@ __global__ __launch_bounds__(kBlock) void k_dfb_gather(const int32_t *__restrict
     int2 h0 = header(v);
     int x0 = dx_entry(list, h0.x, h0.y, lane);
     int2 h1 = header(v + st);
-    DxCoef q0 = dx_coef<D>(x0, coef);
+    DxCoef q0 = dx_coef<D>(x0, h0.y, coef);
     int x1 = dx_entry(list, h1.x, h1.y, lane);
     int2 h2 = header(v + 2 * st);
     for (; v < sh.hi; v += st) {
-        const DxCoef q1 = dx_coef<D>(x1, coef);
+        const DxCoef q1 = dx_coef<D>(x1, h1.y, coef);
         const int x2 = dx_entry(list, h2.x, h2.y, lane);
         const int2 h3 = header(v + 3 * st);
         if (h0.y <= kPart) {  // a split vertex: below

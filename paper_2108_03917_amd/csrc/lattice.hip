@@ -480,7 +480,7 @@ lattice_status lattice_deform_slice_backward(lattice *L, const void *values, lat
     auto bad_dt = [](lattice_dtype t) { return t != LATTICE_F32 && t != LATTICE_BF16; };
     const bool any_out = grad_values || grad_w_delta || grad_b_delta || grad_w_cls || grad_b_cls;
     if (C < 1 || C > 1024 || bad_dt(values_dtype) || bad_dt(grad_dtype) || (w_cls && (n_cls < 1 || n_cls > 256)) ||
-        (!w_cls && (grad_w_cls || grad_b_cls)) || !any_out || !values || !w_delta || (L->m > 0 && !grad_out) ||
+        (!w_cls && (grad_w_cls || grad_b_cls)) || !any_out || (L->m > 0 && (!values || !grad_out)) || !w_delta ||
         (grad_values && (grad_values == values || grad_values == (const void *)grad_out))) {
         set_err(L, "deform_slice_backward: bad argument (C = %d, n_cls = %d)", C, n_cls);
         return LATTICE_E_ARG;

@@ -254,6 +254,28 @@ def test_deform_slice_backward_long_pair_lists(C, n_cls, bf16):
             assert_close_scaled(gbc.cpu().numpy(), rbc, sbc, REL_F32, tag + " b_cls")
 
 
+@pytest.mark.parametrize("n_cls", [0, 20])
+def test_deform_slice_backward_empty_cloud(n_cls):
+    """An empty cloud after a non-empty one on the same lattice: no pairs, so
+    the offsets' and the classifier's gradients are zero (sums of no
+    points); the per-list work reads nothing of the earlier splat's lists."""
+    L = _lattice(3, 0.15, 4000)
+    pos = random_cloud(4000, 3, seed=395, extent=1.0, C=1).pos
+    L.splat(to_dev(pos), None)
+    L.splat(torch.zeros((0, 3), device="cuda:0"), None)
+    assert L.num_vertices() == 0 and L.m == 0
+    C = 64
+    dw = deform_weights(C, max(n_cls, 1), seed=396)
+    y = torch.randn((L.max_vertices(), C), device="cuda:0")
+    G = torch.zeros((1, n_cls if n_cls else C), device="cuda:0")
+    wc = to_dev(dw.w_cls) if n_cls else None
+    _, gwd, gbd, gwc, gbc = L.deform_slice_backward(y, to_dev(dw.w_delta), dw.b_delta, G, wc)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(gwd) == 0 and torch.count_nonzero(gbd) == 0
+    if n_cls:
+        assert torch.count_nonzero(gwc) == 0 and torch.count_nonzero(gbc) == 0
+
+
 def test_deform_slice_backward_without_offsets_is_slice_backward():
     """Zero offset weights and bias: db = 0, so the vertex gradient of the
     point features is the slice's backward (the splat of grad_out), and the

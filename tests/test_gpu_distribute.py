@@ -412,20 +412,22 @@ def _positive_affine_layers(k0, d, seed):
     return out
 
 
-@pytest.mark.parametrize("d", [2, 3, 4])
-def test_distribute_pointnet_backward_routing(d):
-    """Several rows per vertex (three points of a site per vertex) with the
-    fixed affine: the max routes each g[v][c] to the winning row, then every
-    block's parameter gradients (a, s, W, b) match the oracle within 1e-5 of
-    their sum of |terms|.  Positive weights and features keep every decision
-    far outside float32 rounding, which the test checks first."""
+@pytest.mark.parametrize("d,per", [(2, 3), (3, 3), (4, 3), (3, 150), (4, 150)])
+def test_distribute_pointnet_backward_routing(d, per):
+    """Several rows per vertex (the points of a site: three, or 150 so that
+    every list crosses 64-row chunks and its winner is found from the runs
+    of several chunks) with the fixed affine: the max routes each g[v][c] to
+    the winning row, then every block's parameter gradients (a, s, W, b)
+    match the oracle within 1e-5 of their sum of |terms|.  Positive weights
+    and features keep every decision far outside float32 rounding, which the
+    test checks first."""
     sigma = 0.05
-    pos, feat = _sites_cloud(d, 400, 3, 600 + d, sigma)
+    pos, feat = _sites_cloud(d, 400 if per == 3 else 60, per, 600 + d + per, sigma)
     k0 = d + 4
     layers = _positive_affine_layers(k0, d, 601)
     lat, G, got, ref, am, h3, h3_s, v, blocks, seg = _setup_backward(pos, feat, sigma, layers, None, seed=602)
     cnt = np.bincount(v)
-    assert (cnt == 3).mean() > 0.9
+    assert (cnt == per).mean() > 0.9
     order = np.argsort(v, kind="stable")
     starts = np.searchsorted(v[order], np.arange(lat.V))
     ends = np.searchsorted(v[order], np.arange(lat.V), side="right")
