@@ -599,7 +599,10 @@ lattice_status lattice_get_point_simplex(lattice *L, int32_t *idx, float *bary);
 /*
  * Stage timing.  With lattice_set_timing(L, 1) the library records a pair of
  * hipEvents on its stream around every stage it launches (splat, neighbours,
- * conv, slice, deform slice) and accumulates their elapsed times; lattice_get_timing
+ * conv, slice, deform slice); the slice and the deform slice, one kernel
+ * each, have their kernel's launch record the pair at the kernel's start and
+ * end (the kernel's own duration, without the gap before it).  It
+ * accumulates their elapsed times; lattice_get_timing
  * synchronises and returns, per stage, the summed milliseconds and the number
  * of launches since the last reset (arrays of LATTICE_NUM_STAGES).
  * lattice_set_timing(L, 0) stops recording; (L, 2) resets the sums.

@@ -30,6 +30,8 @@
 
 #include "internal.h"
 
+#include <hip/hip_ext.h>
+
 namespace {
 
 constexpr int kBlock = 256;
@@ -419,8 +421,9 @@ template <int D, bool IN_BF16, int CH>
 hipError_t launch_d(lattice *L, bool vec, int log2G, unsigned grid, const void *values, int C, const float *w_delta,
                     float b_delta, const float *w_cls, const float *b_cls, int n_cls, float *out, float *delta) {
 #define DS_LAUNCH(VV, CC)                                                                                         \
-    hipLaunchKernelGGL((k_deform_generic<D, VV, IN_BF16, CC, CH>), dim3(grid), dim3(kBlock), 0, L->stream, L->m, C, \
-                       log2G, L->idx, L->bary, values, w_delta, b_delta, w_cls, b_cls, n_cls, out, delta)
+    hipExtLaunchKernelGGL((k_deform_generic<D, VV, IN_BF16, CC, CH>), dim3(grid), dim3(kBlock), 0, L->stream,    \
+                          L->kt_start, L->kt_stop, 0, L->m, C, log2G, L->idx, L->bary, values, w_delta, b_delta, \
+                          w_cls, b_cls, n_cls, out, delta)
     if (vec) {
         if (w_cls)
             DS_LAUNCH(true, true);
@@ -473,9 +476,9 @@ unsigned fast_grid(const lattice *L, unsigned grid) {
 template <int D, int LG, bool IN_BF16, int NCB>
 hipError_t launch_fast1(lattice *L, unsigned grid, const void *values, int C, const float *w_delta, float b_delta,
                         const float *w_cls, const float *b_cls, int n_cls, float *out, float *delta) {
-    hipLaunchKernelGGL((k_deform_fast<D, LG, IN_BF16, NCB>), dim3(fast_grid<D, LG, IN_BF16, NCB>(L, grid)),
-                       dim3(kBlock), 0, L->stream, L->m, C, L->idx, L->bary, values, w_delta, b_delta, w_cls, b_cls,
-                       n_cls, out, delta);
+    hipExtLaunchKernelGGL((k_deform_fast<D, LG, IN_BF16, NCB>), dim3(fast_grid<D, LG, IN_BF16, NCB>(L, grid)),
+                          dim3(kBlock), 0, L->stream, L->kt_start, L->kt_stop, 0, L->m, C, L->idx, L->bary, values,
+                          w_delta, b_delta, w_cls, b_cls, n_cls, out, delta);
     return hipGetLastError();
 }
 

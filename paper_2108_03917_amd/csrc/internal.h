@@ -141,6 +141,10 @@ struct lattice {
     int timing = 0;
     lattice_timer timers[LATTICE_NUM_STAGES];
     void *events = nullptr;  // per-stage event pools and pending pairs (lattice.hip)
+    // With timing on, the events that a stage made of one kernel (slice,
+    // deform slice) has its launch record at the kernel's start and end
+    // (hipExtLaunchKernelGGL); null otherwise
+    hipEvent_t kt_start = nullptr, kt_stop = nullptr;
 
     char err[512] = {0};
 };

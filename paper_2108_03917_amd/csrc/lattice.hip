@@ -146,6 +146,49 @@ lattice_status timer_end(lattice *L, int stage, hipEvent_t start) {
     return LATTICE_OK;
 }
 
+// A stage made of one kernel: two events that its launch records at the
+// kernel's start and end (L->kt_start, L->kt_stop), so that the stage's time
+// is the kernel's own duration; timer_kernel_end files the pair and clears
+// the fields (also after a failed launch).
+static lattice_status pool_event(lattice *L, stage_events *se, hipEvent_t *e) {
+    if (!se->pool.empty()) {
+        *e = se->pool.back();
+        se->pool.pop_back();
+        return LATTICE_OK;
+    }
+    HIP_TRY(L, hipEventCreate(e));
+    return LATTICE_OK;
+}
+
+lattice_status timer_kernel_begin(lattice *L, int stage) {
+    L->kt_start = L->kt_stop = nullptr;
+    if (!L->timing) return LATTICE_OK;
+    stage_events *se = events_of(L) + stage;
+    hipEvent_t a, b;
+    lattice_status s = pool_event(L, se, &a);
+    if (s) return s;
+    if ((s = pool_event(L, se, &b))) {
+        se->pool.push_back(a);
+        return s;
+    }
+    L->kt_start = a;
+    L->kt_stop = b;
+    return LATTICE_OK;
+}
+
+void timer_kernel_end(lattice *L, int stage, bool launched) {
+    if (L->kt_start) {
+        stage_events *se = events_of(L) + stage;
+        if (launched) {
+            se->pending.emplace_back(L->kt_start, L->kt_stop);
+        } else {
+            se->pool.push_back(L->kt_start);
+            se->pool.push_back(L->kt_stop);
+        }
+    }
+    L->kt_start = L->kt_stop = nullptr;
+}
+
 lattice_status check_launch(lattice *L, hipError_t e, const char *what) {
     if (e != hipSuccess) return hip_fail(L, e, what);
     return LATTICE_OK;
@@ -431,11 +474,11 @@ lattice_status lattice_slice(lattice *L, const void *values, lattice_dtype value
         set_err(L, "slice: bad argument (C = %d)", C);
         return LATTICE_E_ARG;
     }
-    hipEvent_t t0;
-    lattice_status s = timer_begin(L, LATTICE_STAGE_SLICE, &t0);
+    lattice_status s = timer_kernel_begin(L, LATTICE_STAGE_SLICE);
     if (s) return s;
-    if ((s = check_launch(L, launch_slice(L, values, values_dtype, C, out), "slice"))) return s;
-    return timer_end(L, LATTICE_STAGE_SLICE, t0);
+    const hipError_t e = launch_slice(L, values, values_dtype, C, out);
+    timer_kernel_end(L, LATTICE_STAGE_SLICE, e == hipSuccess && L->m > 0);
+    return check_launch(L, e, "slice");
 }
 
 lattice_status lattice_deform_slice(lattice *L, const void *values, lattice_dtype values_dtype, int C,
@@ -456,15 +499,12 @@ lattice_status lattice_deform_slice(lattice *L, const void *values, lattice_dtyp
         set_err(L, "deform_slice: C = %d above %d (C above 256 needs a multiple of 4 and aligned rows)", C, cmax);
         return LATTICE_E_ARG;
     }
-    hipEvent_t t0;
-    lattice_status s = timer_begin(L, LATTICE_STAGE_DEFORM, &t0);
+    lattice_status s = timer_kernel_begin(L, LATTICE_STAGE_DEFORM);
     if (s) return s;
-    if ((s = check_launch(L,
-                          launch_deform_slice(L, values, values_dtype, C, w_delta, b_delta, w_cls, b_cls, n_cls, out,
-                                              delta),
-                          "deform_slice")))
-        return s;
-    return timer_end(L, LATTICE_STAGE_DEFORM, t0);
+    const hipError_t e =
+        launch_deform_slice(L, values, values_dtype, C, w_delta, b_delta, w_cls, b_cls, n_cls, out, delta);
+    timer_kernel_end(L, LATTICE_STAGE_DEFORM, e == hipSuccess && L->m > 0);
+    return check_launch(L, e, "deform_slice");
 }
 
 lattice_status lattice_deform_slice_backward(lattice *L, const void *values, lattice_dtype values_dtype, int C,

@@ -11,6 +11,8 @@
 // a wavefront issues 64 x 16 B coalesced reads per vertex.
 #include "internal.h"
 
+#include <hip/hip_ext.h>
+
 namespace {
 
 constexpr int kBlock = 256;
@@ -128,11 +130,11 @@ static hipError_t slice_typed(lattice *L, const void *values, int C, const float
 #define SL_CASE(DD)                                                                                              \
     case DD:                                                                                                     \
         if (vec)                                                                                                 \
-            hipLaunchKernelGGL((k_slice<DD, true, IN_BF16, NORM>), dim3(grid), dim3(kBlock), 0, L->stream, m, C,  \
-                               log2G, L->idx, L->bary, values, vweight, out);                                    \
+            hipExtLaunchKernelGGL((k_slice<DD, true, IN_BF16, NORM>), dim3(grid), dim3(kBlock), 0, L->stream,    \
+                                  L->kt_start, L->kt_stop, 0, m, C, log2G, L->idx, L->bary, values, vweight, out); \
         else                                                                                                     \
-            hipLaunchKernelGGL((k_slice<DD, false, IN_BF16, NORM>), dim3(grid), dim3(kBlock), 0, L->stream, m, C, \
-                               log2G, L->idx, L->bary, values, vweight, out);                                    \
+            hipExtLaunchKernelGGL((k_slice<DD, false, IN_BF16, NORM>), dim3(grid), dim3(kBlock), 0, L->stream,   \
+                                  L->kt_start, L->kt_stop, 0, m, C, log2G, L->idx, L->bary, values, vweight, out); \
         return hipGetLastError();
     switch (L->d) {
         SL_CASE(1)

@@ -664,6 +664,13 @@ def test_stage_timing_records_every_stage():
     assert all(t[s][1] == 1 and t[s][0] > 0 for s in ("splat", "neighbors", "conv", "slice", "deform")), t
     L.set_timing(2)
     assert all(v == (0.0, 0) for v in L.timing().values())
+    # the slice and the deform slice are timed at their kernel's start and
+    # end; an empty cloud launches no kernel and records nothing
+    L.splat(torch.zeros((0, 3), device=dev()), None)
+    L.slice(torch.zeros((1, 64), device=dev()))
+    L.deform_slice(torch.zeros((1, 64), device=dev()), torch.zeros(64, device=dev()), 0.0)
+    t = L.timing()
+    assert t["slice"] == (0.0, 0) and t["deform"] == (0.0, 0), t
 
 
 # ---------------------------------------------------------------------------
