@@ -846,7 +846,10 @@ hipError_t run_d(lattice *L, const void *values, bool in_bf16, int C, const floa
 
 // Wavefronts of the point kernel and point chunks of the classifier kernel.
 void deform_backward_shape(const lattice *L, int *nwaves, int *nch) {
-    *nwaves = L->cu_count * 8 * 4;  // eight workgroups of four wavefronts per CU (a point per wavefront at a time)
+    // four workgroups of four wavefronts per CU, as many as the point kernel's
+    // registers let a CU hold at once (twice that left a tail of waiting
+    // workgroups: four frames 181 against 178 us)
+    *nwaves = L->cu_count * 4 * 4;
     const int64_t c = (L->m + kClsChunk - 1) / kClsChunk;  // classifier chunks
     *nch = (int)(c < 1 ? 1 : c);
 }
