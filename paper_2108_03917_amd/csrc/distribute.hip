@@ -721,6 +721,7 @@ __global__ __launch_bounds__(kBlock, 2) void k_pointnet(const int32_t *__restric
     // cloud, the point's position and features and the vertex's mean (level
     // 2, which need level 1) one chunk ahead, so that a chunk's MFMAs never
     // wait on its own gathers.
+    const bool pos4 = d == 4 && ((reinterpret_cast<uintptr_t>(pos) | reinterpret_cast<uintptr_t>(mu)) & 15) == 0;
     struct Rows {
         int v, p;             // level 1
         int off, cnt, b;      // level 2
@@ -737,12 +738,25 @@ __global__ __launch_bounds__(kBlock, 2) void k_pointnet(const int32_t *__restric
         R.off = valid ? vinfo[2 * R.v] : 0;
         R.cnt = valid ? vinfo[2 * R.v + 1] : 0;
         R.b = valid ? cloud_of(vkeys, batched, R.v) : -1;
+        if (pos4) {
+            // d = 4 with 16-byte aligned rows: the position and the mean as
+            // one 16-byte load each
+            const float4 pp = valid ? reinterpret_cast<const float4 *>(pos)[R.p] : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 mm = valid ? reinterpret_cast<const float4 *>(mu)[R.v] : make_float4(0.f, 0.f, 0.f, 0.f);
+            R.x[0] = pp.x - mm.x;
+            R.x[1] = pp.y - mm.y;
+            R.x[2] = pp.z - mm.z;
+            R.x[3] = pp.w - mm.w;
 #pragma unroll
-        for (int i = 0; i < kMaxK0; ++i) {
-            float x = 0.f;
-            if (valid && i < d) x = pos[(int64_t)R.p * d + i] - mu[(int64_t)R.v * d + i];
-            else if (valid && i < k0) x = feat[(int64_t)R.p * f_d + (i - d)];
-            R.x[i] = x;
+            for (int i = 4; i < kMaxK0; ++i) R.x[i] = valid && i < k0 ? feat[(int64_t)R.p * f_d + (i - 4)] : 0.f;
+        } else {
+#pragma unroll
+            for (int i = 0; i < kMaxK0; ++i) {
+                float x = 0.f;
+                if (valid && i < d) x = pos[(int64_t)R.p * d + i] - mu[(int64_t)R.v * d + i];
+                else if (valid && i < k0) x = feat[(int64_t)R.p * f_d + (i - d)];
+                R.x[i] = x;
+            }
         }
     };
     int64_t ch = c_first;
@@ -1191,12 +1205,21 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
     constexpr int K = S == 3 ? kW2 : (S == 2 ? kW1 : kMaxK0);  // channels of block S's normalisation
     constexpr int NV = S == 1 ? 3 * 16 : 64;                    // staged columns with a per-channel sum
     constexpr int DH = 32, RR = S == 2 ? 64 : 48;               // staged dh and r (S = 2, 1)
+    // pass 3 stages block 3's weight rows at a pitch of 36 floats (and a_2
+    // after them): lanes that read different rows in the sparse loop then
+    // fall on different LDS banks (at 32 they shared one)
+    constexpr int kWP = 36, kA2P = S == 3 ? kW3 * kWP : kA2;
     __shared__ float Ps[kPadded];
     __shared__ float stg[64 * kStg];
     __shared__ int scl[64];
     extern __shared__ float tab[];  // per-cloud group sums, batched only: [kGnClouds][2 K] (launch size)
     const int lane = threadIdx.x;
-    for (int i = lane; i < kPadded; i += 64) Ps[i] = P[i];
+    if (S == 3) {
+        for (int i = lane; i < kW3 * kW2; i += 64) Ps[(i / kW2) * kWP + (i % kW2)] = P[kWt2 + i];
+        for (int i = lane; i < kW2; i += 64) Ps[kA2P + i] = P[kA2 + i];
+    } else {
+        for (int i = lane; i < kPadded; i += 64) Ps[i] = P[i];
+    }
     const bool tabbed = S != 1 && use_gn && BATCHED;
     if (tabbed)
         for (int i = lane; i < kGnClouds * 2 * K; i += 64) tab[i] = 0.f;
@@ -1229,6 +1252,18 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
         const float *N = BATCHED ? nrm + (int64_t)cloud * kNrmRow : cst + kAffRow;
         const float *GM = BATCHED ? gm + (int64_t)cloud * 2 * kW2 * 2 : cst + kAffRow + kNrmRow;
         const float *R = rec + (live ? e : 0) * kRec;
+        // the part of the record this pass reads, as 16-byte loads (a lane's
+        // record is 256 contiguous bytes)
+        constexpr int RLO = S == 3 ? kRecH2 : (S == 2 ? kRecH1 : 0), RHI = S == 1 ? kRecH2 : kRec;
+        float rv[kRec];
+#pragma unroll
+        for (int q = RLO / 4; q < RHI / 4; ++q) {
+            const float4 t = reinterpret_cast<const float4 *>(R)[q];
+            rv[4 * q] = t.x;
+            rv[4 * q + 1] = t.y;
+            rv[4 * q + 2] = t.z;
+            rv[4 * q + 3] = t.w;
+        }
         if (S == 3) {
             // dr3 = W3^T dh3, dh3 = g_v on the channels routed to this entry
             // (its mask) and 0 elsewhere: the row of g is loaded whole, and
@@ -1271,7 +1306,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
                     bits &= bits - 1;
                     const float g = st[o];
 #pragma unroll
-                    for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dr[j]);
+                    for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[o * kWP + j], dr[j]);
                 }
             } else {
                 // (fully unrolled: gv stays in registers)
@@ -1279,12 +1314,12 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
                 for (int o = 0; o < kW3; ++o) {
                     const float g = ((mk >> o) & 1ull) ? gv[o] : 0.f;
 #pragma unroll
-                    for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[kWt2 + o * kW2 + j], dr[j]);
+                    for (int j = 0; j < kW2; ++j) dr[j] = fmaf(g, Ps[o * kWP + j], dr[j]);
                 }
             }
 #pragma unroll
             for (int j = 0; j < kW2; ++j) {
-                const float h = R[kRecH2 + j];
+                const float h = rv[kRecH2 + j];
                 const float d = (live && fmaf(A[kAff2 + j], h, A[kAff2 + kW2 + j]) > 0.f) ? dr[j] : 0.f;
                 const float xh = (h - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
                 dr[j] = d;
@@ -1312,7 +1347,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
             for (int j = 0; j < kW2; ++j) {
                 const float gj = Ps[kA2 + j] * dh[j];
                 if (use_gn) {
-                    const float xh = (R[kRecH2 + j] - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
+                    const float xh = (rv[kRecH2 + j] - N[2 * 64 + 2 * j]) * N[2 * 64 + 2 * j + 1];
                     const float *M = GM + kW2 * 2 + (j / gs3) * 2;
                     dh[j] = live ? N[2 * 64 + 2 * j + 1] * (gj - M[0] - xh * M[1]) : 0.f;
                 } else {
@@ -1323,7 +1358,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
             float dn[kW1];
 #pragma unroll
             for (int c = 0; c < kW1; ++c) {
-                const float h = R[kRecH1 + c];
+                const float h = rv[kRecH1 + c];
                 const float hn = fmaf(A[kAff1 + c], h, A[kAff1 + kW1 + c]);
                 float s_ = 0.f;
 #pragma unroll
@@ -1356,7 +1391,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
             for (int c = 0; c < kW1; ++c) {
                 const float gc = Ps[kA1 + c] * dh[c];
                 if (use_gn) {
-                    const float xh = (R[kRecH1 + c] - N[1 * 64 + 2 * c]) * N[1 * 64 + 2 * c + 1];
+                    const float xh = (rv[kRecH1 + c] - N[1 * 64 + 2 * c]) * N[1 * 64 + 2 * c + 1];
                     const float *M = GM + (c / gs2) * 2;
                     dh[c] = live ? N[1 * 64 + 2 * c + 1] * (gc - M[0] - xh * M[1]) : 0.f;
                 } else {
@@ -1366,7 +1401,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
             }
 #pragma unroll
             for (int c = 0; c < kMaxK0; ++c) {
-                const float h = R[c];
+                const float h = rv[c];
                 const float hn = fmaf(A[kAff0 + c], h, A[kAff0 + kMaxK0 + c]);
                 float s_ = 0.f;
 #pragma unroll
@@ -1393,7 +1428,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
                 float x = 0.f;
                 for (int t = 0; t < gs; ++t) {
                     const int ch = grp * gs + t;
-                    x = fmaf(Ps[(S == 3 ? kA2 : kA1) + ch], stg[k * kStg + pt * K + ch], x);
+                    x = fmaf(Ps[(S == 3 ? kA2P : kA1) + ch], stg[k * kStg + pt * K + ch], x);
                 }
                 tab[cl * 2 * K + lane] += x;
             }
@@ -1451,7 +1486,7 @@ __global__ __launch_bounds__(64) void k_dpn_back(const int32_t *__restrict__ lve
             for (int t = 0; t < gs; ++t) {
                 const int ch = (grp < G ? grp : 0) * gs + t;
                 const float y = __shfl(vacc, pt * K + ch);
-                x = fmaf(Ps[(S == 3 ? kA2 : kA1) + ch], y, x);
+                x = fmaf(Ps[(S == 3 ? kA2P : kA1) + ch], y, x);
             }
             if (lane < 2 * K) out[base + lane] = grp < G ? x : 0.f;
         }
