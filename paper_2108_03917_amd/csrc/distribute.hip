@@ -749,6 +749,17 @@ __global__ __launch_bounds__(kBlock, 2) void k_pointnet(const int32_t *__restric
             R.x[3] = pp.w - mm.w;
 #pragma unroll
             for (int i = 4; i < kMaxK0; ++i) R.x[i] = valid && i < k0 ? feat[(int64_t)R.p * f_d + (i - 4)] : 0.f;
+        } else if (d == 3) {
+            // d = 3: three adjacent 4-byte loads each (unconditional, so that
+            // they merge into one 12-byte load)
+            const int64_t p3 = (int64_t)(valid ? R.p : 0) * 3, v3 = (int64_t)(valid ? R.v : 0) * 3;
+            const float p0 = pos[p3], p1 = pos[p3 + 1], p2 = pos[p3 + 2];
+            const float m0 = mu[v3], m1 = mu[v3 + 1], m2 = mu[v3 + 2];
+            R.x[0] = valid ? p0 - m0 : 0.f;
+            R.x[1] = valid ? p1 - m1 : 0.f;
+            R.x[2] = valid ? p2 - m2 : 0.f;
+#pragma unroll
+            for (int i = 3; i < kMaxK0; ++i) R.x[i] = valid && i < k0 ? feat[(int64_t)R.p * f_d + (i - 3)] : 0.f;
         } else {
 #pragma unroll
             for (int i = 0; i < kMaxK0; ++i) {
