@@ -181,7 +181,10 @@ __global__ __launch_bounds__(kBlock) void k_local_mean(const int32_t *__restrict
         const int p = valid ? list_point(list[2 * e]) : 0;
         double acc[D];
 #pragma unroll
-        for (int i = 0; i < D; ++i) acc[i] = valid ? (double)pos[(int64_t)p * D + i] : 0.0;
+        for (int i = 0; i < D; ++i) {
+            const float pv = pos[(int64_t)p * D + i];  // unconditional (p = 0 past the end): the loads merge
+            acc[i] = valid ? (double)pv : 0.0;
+        }
         const int vprev = __shfl_up(v, 1), vnext = __shfl_down(v, 1);
         const int start = run_start(lane == 0 || vprev != v, lane);
 #pragma unroll
@@ -486,8 +489,14 @@ __global__ __launch_bounds__(kBlock) void k_gn_stats0(const int32_t *__restrict_
 #pragma unroll
         for (int i = 0; i < kMaxK0; ++i) {
             float t = 0.f;
-            if (valid && i < D) t = pos[(int64_t)p * D + i] - mu[(int64_t)v * D + i];
-            else if (valid && i < k0) t = feat[(int64_t)p * f_d + (i - D)];
+            if (i < D) {
+                // unconditional (p = v = 0 past the end), so that the D
+                // adjacent loads merge into one
+                const float pv = pos[(int64_t)p * D + i], mv = mu[(int64_t)v * D + i];
+                t = valid ? pv - mv : 0.f;
+            } else if (valid && i < k0) {
+                t = feat[(int64_t)p * f_d + (i - D)];
+            }
             x[i] = t;
         }
         const int bref = __builtin_amdgcn_readfirstlane(b);  // lane 0 is valid in every chunk
